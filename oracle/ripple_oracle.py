@@ -1,0 +1,394 @@
+"""CPU oracle for exact incremental GNN embedding propagation (Ripple, arXiv 2505.12112).
+
+TEST INFRASTRUCTURE. Only the test-suite, the package smoke check and the
+benchmark's CPU-baseline timing may import this module. The HIP library never
+calls it, and it shares no code with the library: it does not know about
+cached aggregates, deltas, frontiers or bitmaps. It recomputes every layer of
+the GNN from scratch on the post-batch graph and derives the affected vertex
+sets from the graph structure alone.
+
+Passages followed:
+
+* GNN layer: Sec. II-A, Eq. (1)-(2): x^l_u = Aggregate^l({h^{l-1}_v : v in N(u)}),
+  h^l_u = sigma(Update^l(h^{l-1}_u, x^l_u)).
+* Linear aggregators sum, mean and weighted sum: Sec. II-C, table "Popular Linear
+  Aggregation functions in GNNs".
+* N(u) is the set of in-neighbours; updates flow from source to sink along
+  out-edges: Sec. IV-B (inserting C->A first changes h^1 of the sink A, whose
+  recompute pulls the h^0 of all of A's in-neighbours).
+* Update types (edge insert, edge delete, vertex-feature change; no vertex
+  insert/delete) and fixed-size batches: Sec. IV-A.
+* Affected vertices: an edge update touches the sink at every hop, and a vertex
+  touched at hop l touches its out-neighbours at hop l+1; a feature update of u
+  touches u's out-neighbours at hop 1: Sec. II-B and Sec. IV-B. No pruning:
+  every reached vertex counts as affected: Sec. IV-C.
+* Combined updates give the same result as applying them one by one: Sec.
+  IV-C.1 ("Combining multiple updates at a vertex").
+* Exact within floating-point precision: Sec. VI.
+
+Readings where the paper is silent (each is listed with its reason in the
+design notes of the repository):
+
+* simple directed graph: inserting a present arc, deleting an absent arc and
+  inserting or deleting a self-loop change nothing;
+* a batch has sequential semantics: the net effect is what applying its ops in
+  order would leave (last feature write wins);
+* on an undirected graph an edge op acts on both arcs;
+* GraphSAGE: h = sigma(W_self h_self + W_neigh agg + b) with agg the sum, or the
+  mean (0 when the in-degree is 0);
+* GCN with symmetric normalisation: implicit self-loop,
+  alpha_uv = 1/sqrt((d_out(u)+1)(d_in(v)+1));
+* ReLU after every layer but the last.
+
+Arithmetic is float64 by default; the aggregation uses a scipy sparse product
+and the transform a dense matrix product.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+import scipy.sparse as sp
+
+OP_INSERT = 1
+OP_DELETE = 2
+OP_FEATURE = 3
+
+
+# ----------------------------------------------------------------------------
+# model
+# ----------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class OracleModel:
+    """agg in {"sum", "mean", "gcn"}; weights are [d_l, d_{l-1}] (y = W x)."""
+    agg: str
+    w_self: List[Optional[np.ndarray]]
+    w_neigh: List[np.ndarray]
+    bias: List[np.ndarray]
+    relu: List[bool]
+
+    @property
+    def num_layers(self) -> int:
+        return len(self.w_neigh)
+
+    @staticmethod
+    def from_weights(mw, dtype=np.float64) -> "OracleModel":
+        """Accepts any object with agg / w_self / w_neigh / bias / relu attributes."""
+        return OracleModel(
+            mw.agg,
+            [None if w is None else np.asarray(w, dtype) for w in mw.w_self],
+            [np.asarray(w, dtype) for w in mw.w_neigh],
+            [np.asarray(b, dtype) for b in mw.bias],
+            list(mw.relu))
+
+
+# ----------------------------------------------------------------------------
+# graph: a set of arcs kept as sorted int64 keys u*n + v
+# ----------------------------------------------------------------------------
+
+class OracleGraph:
+    def __init__(self, n: int, src, dst, undirected: bool = False):
+        self.n = int(n)
+        self.undirected = bool(undirected)
+        src = np.asarray(src, np.int64)
+        dst = np.asarray(dst, np.int64)
+        if undirected:
+            src, dst = np.concatenate([src, dst]), np.concatenate([dst, src])
+        keys = src * self.n + dst
+        keys = keys[src != dst]
+        self.keys = np.unique(keys)
+
+    def copy(self) -> "OracleGraph":
+        g = OracleGraph.__new__(OracleGraph)
+        g.n, g.undirected, g.keys = self.n, self.undirected, self.keys.copy()
+        return g
+
+    @property
+    def num_arcs(self) -> int:
+        return int(self.keys.size)
+
+    def arcs(self) -> Tuple[np.ndarray, np.ndarray]:
+        return self.keys // self.n, self.keys % self.n
+
+    def has_arcs(self, keys: np.ndarray) -> np.ndarray:
+        keys = np.asarray(keys, np.int64)
+        j = np.searchsorted(self.keys, keys)
+        jj = np.minimum(j, max(self.keys.size - 1, 0))
+        return (j < self.keys.size) & (self.keys[jj] == keys) if self.keys.size else \
+            np.zeros(keys.shape, bool)
+
+    def out_degree(self) -> np.ndarray:
+        return np.bincount(self.keys // self.n, minlength=self.n)
+
+    def in_degree(self) -> np.ndarray:
+        return np.bincount(self.keys % self.n, minlength=self.n)
+
+    def out_neighbours(self, verts: np.ndarray) -> np.ndarray:
+        """All v with (u, v) an arc for some u in verts (with repeats)."""
+        verts = np.asarray(verts, np.int64)
+        if verts.size == 0:
+            return np.empty(0, np.int64)
+        lo = np.searchsorted(self.keys, verts * self.n)
+        hi = np.searchsorted(self.keys, (verts + 1) * self.n)
+        if int((hi - lo).sum()) == 0:
+            return np.empty(0, np.int64)
+        idx = np.concatenate([np.arange(a, b) for a, b in zip(lo, hi) if b > a])
+        return self.keys[idx] % self.n
+
+    def in_adjacency(self, weights: Optional[np.ndarray] = None, dtype=np.float64) -> sp.csr_matrix:
+        """Sparse A with A[v, u] = weight of arc u->v (1 by default): row v lists
+        v's in-neighbours, so A @ H sums in-neighbour rows (Eq. (1))."""
+        u, v = self.arcs()
+        w = np.ones(u.size, dtype) if weights is None else np.asarray(weights, dtype)
+        return sp.csr_matrix((w, (v, u)), shape=(self.n, self.n))
+
+
+# ----------------------------------------------------------------------------
+# applying a batch (sequential semantics) and its net effect
+# ----------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class NetEffect:
+    ins_src: np.ndarray
+    ins_dst: np.ndarray
+    del_src: np.ndarray
+    del_dst: np.ndarray
+    features: np.ndarray       # F: sorted distinct vertices with a feature write
+    heads: np.ndarray          # sorted distinct sinks of net-changed arcs
+    tails: np.ndarray          # sorted distinct sources of net-changed arcs
+    out_deg_changed: np.ndarray  # sorted vertices whose out-degree changed
+    edge_keys: int             # distinct non-loop edge keys the batch touched
+    noop_edge_ops: int         # self-loop edge ops + touched keys with no net change
+
+
+def apply_batch(graph: OracleGraph, x: np.ndarray, ops: np.ndarray,
+                feat_rows: np.ndarray) -> Tuple[OracleGraph, np.ndarray, NetEffect]:
+    """Applies `ops` in order to (graph, x) and returns (graph', x', net effect).
+
+    An insert sets an arc present and a delete sets it absent, so the final
+    state of an arc is fixed by the last op naming it; comparing with the
+    pre-batch state gives the net inserts and deletes. Undirected graphs apply
+    each edge op to both arcs and count the unordered edge once."""
+    n = graph.n
+    ops = np.asarray(ops)
+    x_new = np.array(x, copy=True)
+    final: Dict[Tuple[int, int], bool] = {}
+    feat_vertices = set()
+    selfloops = 0
+    for kind, u, v, f in ops.tolist():
+        if kind == OP_FEATURE:
+            x_new[u] = feat_rows[f]
+            feat_vertices.add(u)
+            continue
+        if kind not in (OP_INSERT, OP_DELETE):
+            raise ValueError(f"bad op kind {kind}")
+        if u == v:
+            selfloops += 1
+            continue
+        key = (min(u, v), max(u, v)) if graph.undirected else (u, v)
+        final[key] = (kind == OP_INSERT)
+    keys_touched = list(final.keys())
+    ins, dels = [], []
+    noop_keys = 0
+    if keys_touched:
+        arr = np.array(keys_touched, np.int64)
+        present = graph.has_arcs(arr[:, 0] * n + arr[:, 1])
+        for (a, b), was in zip(keys_touched, present.tolist()):
+            now = final[(a, b)]
+            if now == was:
+                noop_keys += 1
+                continue
+            pairs = [(a, b), (b, a)] if graph.undirected else [(a, b)]
+            (ins if now else dels).extend(pairs)
+    ins = np.array(ins, np.int64).reshape(-1, 2)
+    dels = np.array(dels, np.int64).reshape(-1, 2)
+    g2 = graph.copy()
+    keep = g2.keys
+    if dels.size:
+        keep = np.setdiff1d(keep, dels[:, 0] * n + dels[:, 1], assume_unique=True)
+    if ins.size:
+        keep = np.union1d(keep, ins[:, 0] * n + ins[:, 1])
+    g2.keys = keep
+    ch = np.concatenate([ins, dels]) if (ins.size or dels.size) else np.empty((0, 2), np.int64)
+    od_change = np.zeros(n, np.int64)
+    np.add.at(od_change, ins[:, 0], 1)
+    np.add.at(od_change, dels[:, 0], -1)
+    net = NetEffect(
+        ins[:, 0], ins[:, 1], dels[:, 0], dels[:, 1],
+        np.array(sorted(feat_vertices), np.int64),
+        np.unique(ch[:, 1]), np.unique(ch[:, 0]),
+        np.nonzero(od_change)[0].astype(np.int64),
+        len(keys_touched), noop_keys + selfloops)
+    return g2, x_new, net
+
+
+# ----------------------------------------------------------------------------
+# full layer-wise recompute (the definition, Eq. (1)-(2))
+# ----------------------------------------------------------------------------
+
+def aggregate(graph: OracleGraph, h: np.ndarray, agg: str) -> np.ndarray:
+    """x_v = Aggregate({h_u : u in N_in(v)}) for every v (table of linear
+    aggregators). GCN's weighted sum includes v itself (implicit self-loop)."""
+    h = np.asarray(h)
+    if agg == "sum":
+        return graph.in_adjacency(dtype=h.dtype) @ h
+    if agg == "mean":
+        s = graph.in_adjacency(dtype=h.dtype) @ h
+        deg = graph.in_degree()
+        out = np.zeros_like(s)
+        nz = deg > 0
+        out[nz] = s[nz] / deg[nz, None]
+        return out
+    if agg == "gcn":
+        dout = graph.out_degree().astype(h.dtype)
+        din = graph.in_degree().astype(h.dtype)
+        u, v = graph.arcs()
+        alpha = 1.0 / np.sqrt((dout[u] + 1.0) * (din[v] + 1.0))
+        a = graph.in_adjacency(alpha, dtype=h.dtype)
+        a_self = 1.0 / np.sqrt((dout + 1.0) * (din + 1.0))
+        return a @ h + a_self[:, None] * h
+    raise ValueError(agg)
+
+
+def layer(graph: OracleGraph, h_prev: np.ndarray, model: OracleModel, l: int) -> np.ndarray:
+    """One layer l (1-based): Update^l then sigma (Eq. (2))."""
+    agg = aggregate(graph, h_prev, model.agg)
+    wn, b = model.w_neigh[l - 1], model.bias[l - 1]
+    if model.agg == "gcn":
+        out = agg @ wn.T + b
+    else:
+        out = h_prev @ model.w_self[l - 1].T + agg @ wn.T + b
+    if model.relu[l - 1]:
+        out = np.maximum(out, 0.0)
+    return out
+
+
+def full_recompute(graph: OracleGraph, x: np.ndarray, model: OracleModel,
+                   dtype=np.float64) -> List[np.ndarray]:
+    """[H^0 = X, H^1, ..., H^L] for all vertices, layer by layer."""
+    hs = [np.asarray(x, dtype)]
+    m = model if dtype == np.float64 else OracleModel.from_weights(model, dtype)
+    for l in range(1, model.num_layers + 1):
+        hs.append(layer(graph, hs[-1], m, l))
+    return hs
+
+
+# ----------------------------------------------------------------------------
+# structural affected sets
+# ----------------------------------------------------------------------------
+
+def affected_sets(graph_post: OracleGraph, net: NetEffect, agg: str,
+                  num_layers: int) -> List[np.ndarray]:
+    """A^0 .. A^L as sorted int64 arrays.
+
+    A^0 = F (vertices whose features were written). At hop l the vertices whose
+    layer-(l-1) contribution changed are D^l = A^{l-1}, plus, under GCN, every
+    vertex whose out-degree changed (its normalisation scales all its outgoing
+    contributions and its own self-loop). A^l holds D^l's post-batch
+    out-neighbours, every sink of a net-changed arc (its neighbourhood changed),
+    and D^l itself (its own previous embedding enters its update)."""
+    sets = [np.unique(net.features)]
+    for _ in range(num_layers):
+        d = sets[-1]
+        if agg == "gcn":
+            d = np.union1d(d, net.out_deg_changed)
+        a = np.union1d(np.union1d(graph_post.out_neighbours(d), net.heads), d)
+        sets.append(a.astype(np.int64))
+    return sets
+
+
+# ----------------------------------------------------------------------------
+# sampled vertex-wise evaluation (for graphs too large to recompute often)
+# ----------------------------------------------------------------------------
+
+def sampled_embeddings(graph: OracleGraph, x: np.ndarray, model: OracleModel,
+                       vertices: Sequence[int], upto_layer: Optional[int] = None,
+                       dtype=np.float64) -> Tuple[np.ndarray, np.ndarray]:
+    """h^l_v at layer l = upto_layer (default L) for the given vertices, computed
+    only on the in-neighbourhood Eq. (1)-(2) reach (vertex-wise inference).
+    Returns (sorted distinct vertices, their rows)."""
+    L = model.num_layers if upto_layer is None else int(upto_layer)
+    verts = np.unique(np.asarray(vertices, np.int64))
+    src, dst = graph.arcs()
+    order = np.argsort(dst, kind="stable")
+    s_sorted, d_sorted = src[order], dst[order]
+    dout = graph.out_degree().astype(dtype)
+    din = graph.in_degree().astype(dtype)
+
+    def in_arcs(rows):
+        lo = np.searchsorted(d_sorted, rows)
+        hi = np.searchsorted(d_sorted, rows, side="right")
+        cnt = hi - lo
+        row_of = np.repeat(np.arange(rows.size), cnt)
+        start = np.repeat(lo - np.concatenate([[0], np.cumsum(cnt)[:-1]]), cnt)
+        idx = start + np.arange(int(cnt.sum()))
+        return row_of, s_sorted[idx]
+
+    need = [None] * (L + 1)
+    need[L] = verts
+    for l in range(L, 0, -1):
+        _, us = in_arcs(need[l])
+        need[l - 1] = np.union1d(need[l], us)
+    h = np.asarray(x, dtype)[need[0]]
+    for l in range(1, L + 1):
+        rows, prev = need[l], need[l - 1]
+        row_of, us = in_arcs(rows)
+        col = np.searchsorted(prev, us)
+        if model.agg == "gcn":
+            w = 1.0 / np.sqrt((dout[us] + 1.0) * (din[rows][row_of] + 1.0))
+        elif model.agg == "mean":
+            w = 1.0 / din[rows][row_of]
+        else:
+            w = np.ones(us.size, dtype)
+        agg = sp.csr_matrix((w, (row_of, col)), shape=(rows.size, prev.size)) @ h
+        self_rows = h[np.searchsorted(prev, rows)]
+        wn = np.asarray(model.w_neigh[l - 1], dtype)
+        b = np.asarray(model.bias[l - 1], dtype)
+        if model.agg == "gcn":
+            a_self = 1.0 / np.sqrt((dout[rows] + 1.0) * (din[rows] + 1.0))
+            out = (agg + a_self[:, None] * self_rows) @ wn.T + b
+        else:
+            out = self_rows @ np.asarray(model.w_self[l - 1], dtype).T + agg @ wn.T + b
+        if model.relu[l - 1]:
+            out = np.maximum(out, 0.0)
+        h = out
+    return verts, h
+
+
+# ----------------------------------------------------------------------------
+# a stateful driver and the error measure
+# ----------------------------------------------------------------------------
+
+class OracleState:
+    """Graph + features + model; applies batches and recomputes on demand."""
+
+    def __init__(self, n, src, dst, x, model: OracleModel, undirected=False):
+        self.graph = OracleGraph(n, src, dst, undirected)
+        self.x = np.asarray(x, np.float64).copy()
+        self.model = model
+
+    def apply(self, ops, feat_rows):
+        g2, x2, net = apply_batch(self.graph, self.x, ops, np.asarray(feat_rows, np.float64))
+        self.graph, self.x = g2, x2
+        sets = affected_sets(g2, net, self.model.agg, self.model.num_layers)
+        return net, sets
+
+    def embeddings(self, dtype=np.float64) -> List[np.ndarray]:
+        return full_recompute(self.graph, self.x, self.model, dtype)
+
+
+def row_relative_error(h: np.ndarray, h_ref: np.ndarray) -> float:
+    """max_v ||h_v - h*_v||_inf / max(||h*_v||_inf, eps), eps = 1e-3 * RMS(H*):
+    the per-vertex relative error, with a floor so that rows the ReLU zeroed do
+    not divide by zero."""
+    h = np.asarray(h, np.float64)
+    h_ref = np.asarray(h_ref, np.float64)
+    if h_ref.size == 0:
+        return 0.0
+    eps = 1e-3 * math.sqrt(float(np.mean(h_ref * h_ref))) + 1e-30
+    num = np.max(np.abs(h - h_ref), axis=1)
+    den = np.maximum(np.max(np.abs(h_ref), axis=1), eps)
+    return float(np.max(num / den))

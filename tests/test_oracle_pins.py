@@ -1,0 +1,343 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself:
+hand-derived closed forms, textbook special cases, the paper's worked examples,
+brute force on tiny inputs and invariants the paper states."""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import ripple_oracle as O
+from paper_2505_12112_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _model(agg, w_self, w_neigh, bias, relu):
+    return O.OracleModel(
+        agg,
+        [None if w is None else np.array(w, np.float64) for w in w_self],
+        [np.array(w, np.float64) for w in w_neigh],
+        [np.array(b, np.float64) for b in bias],
+        list(relu))
+
+
+def _random_model(rng, agg, dims, relu_all=False, relu_none=False):
+    ws, wn, bs, act = [], [], [], []
+    L = len(dims) - 1
+    for l in range(1, L + 1):
+        ws.append(None if agg == "gcn" else rng.standard_normal((dims[l], dims[l - 1])))
+        wn.append(rng.standard_normal((dims[l], dims[l - 1])))
+        bs.append(rng.standard_normal(dims[l]) * 0.1)
+        act.append(False if relu_none else (True if relu_all else l < L))
+    return O.OracleModel(agg, ws, wn, bs, act)
+
+
+def _eval_expr(s):
+    return float(eval(s, {"__builtins__": {}}, {"sqrt": math.sqrt}))
+
+
+# ---------------------------------------------------------------------------
+# hand-derived closed forms
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("case", ["sage_sum_2layer", "sage_mean_1layer", "gcn_directed_1layer"])
+def test_hand_derived_values(case):
+    fx = json.load(open(os.path.join(GOLDEN, "hand_small_graph.json")))
+    arcs = np.array(fx["arcs"])
+    c = fx["cases"][case]
+    g = O.OracleGraph(fx["n"], arcs[:, 0], arcs[:, 1])
+    m = _model(c["agg"], c["w_self"], c["w_neigh"], c["bias"], c["relu"])
+    hs = O.full_recompute(g, np.array(fx["x"], np.float64), m)
+    for layer, rows in c["expected"].items():
+        want = np.array([[_eval_expr(e) for e in r] for r in rows])
+        np.testing.assert_allclose(hs[int(layer)], want, rtol=0, atol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# textbook special cases
+# ---------------------------------------------------------------------------
+
+def test_sum_aggregation_is_brute_force_in_neighbour_sum():
+    """W_self=0, W_neigh=I, no bias, no activation: H^1 = plain in-neighbour sum,
+    computed here by a loop over the arc list (no sparse algebra)."""
+    rng = np.random.default_rng(1)
+    n, d = 40, 5
+    src, dst = synth.erdos_renyi(n, 150, rng)
+    x = rng.standard_normal((n, d))
+    m = O.OracleModel("sum", [np.zeros((d, d))], [np.eye(d)], [np.zeros(d)], [False])
+    h1 = O.full_recompute(O.OracleGraph(n, src, dst), x, m)[1]
+    want = np.zeros((n, d))
+    for u, v in zip(src.tolist(), dst.tolist()):
+        want[v] += x[u]
+    np.testing.assert_allclose(h1, want, rtol=0, atol=1e-12)
+
+
+def test_gcn_matches_kipf_closed_form_on_undirected_graphs():
+    """On an undirected graph GCN's layer is D^-1/2 (A+I) D^-1/2 H W^T + b (Kipf &
+    Welling), built here with dense matrices."""
+    rng = np.random.default_rng(2)
+    n, d0, d1 = 30, 4, 3
+    src, dst = synth.erdos_renyi(n, 60, rng, undirected=True)
+    a = np.zeros((n, n))
+    a[src, dst] = 1
+    a[dst, src] = 1
+    ahat = a + np.eye(n)
+    dinv = np.diag(1.0 / np.sqrt(ahat.sum(1)))
+    x = rng.standard_normal((n, d0))
+    w = rng.standard_normal((d1, d0))
+    b = rng.standard_normal(d1)
+    m = O.OracleModel("gcn", [None], [w], [b], [False])
+    h1 = O.full_recompute(O.OracleGraph(n, src, dst, undirected=True), x, m)[1]
+    want = dinv @ ahat @ dinv @ x @ w.T + b
+    np.testing.assert_allclose(h1, want, rtol=0, atol=1e-12)
+
+
+def test_mean_equals_scaled_sum_on_in_regular_graph():
+    """Every vertex has in-degree k (out-degrees vary): SAGE-mean with W_neigh
+    equals SAGE-sum with W_neigh / k. Dividing by the out-degree would fail."""
+    rng = np.random.default_rng(3)
+    n, k, d = 25, 3, 4
+    src, dst = [], []
+    for v in range(n):
+        for u in rng.choice([w for w in range(n) if w != v], k, replace=False):
+            src.append(u)
+            dst.append(v)
+    g = O.OracleGraph(n, src, dst)
+    assert len(set(g.out_degree().tolist())) > 1
+    x = rng.standard_normal((n, d))
+    ws, wn, b = rng.standard_normal((d, d)), rng.standard_normal((d, d)), rng.standard_normal(d)
+    hm = O.full_recompute(g, x, O.OracleModel("mean", [ws], [wn], [b], [True]))[1]
+    hs = O.full_recompute(g, x, O.OracleModel("sum", [ws], [wn / k], [b], [True]))[1]
+    np.testing.assert_allclose(hm, hs, rtol=1e-13, atol=1e-13)
+
+
+def test_mean_with_no_in_neighbours_is_zero_aggregate():
+    g = O.OracleGraph(3, [0], [1])
+    x = np.array([[1.0], [2.0], [3.0]])
+    m = O.OracleModel("mean", [np.zeros((1, 1))], [np.eye(1)], [np.zeros(1)], [False])
+    np.testing.assert_array_equal(O.full_recompute(g, x, m)[1], [[0.0], [1.0], [0.0]])
+
+
+# ---------------------------------------------------------------------------
+# the paper's worked examples (affected sets)
+# ---------------------------------------------------------------------------
+
+def _paper_examples():
+    return json.load(open(os.path.join(GOLDEN, "paper_examples.json")))["examples"]
+
+
+@pytest.mark.parametrize("ex", _paper_examples(), ids=lambda e: e["name"])
+def test_paper_worked_examples(ex):
+    names = ex["vertices"]
+    ix = {v: i for i, v in enumerate(names)}
+    arcs = np.array([[ix[a], ix[b]] for a, b in ex["arcs"]])
+    g = O.OracleGraph(len(names), arcs[:, 0], arcs[:, 1])
+    ops, rows = [], []
+    for op in ex["batch"]:
+        if op[0] == "feature":
+            ops.append([O.OP_FEATURE, ix[op[1]], -1, len(rows)])
+            rows.append([7.0])
+        else:
+            kind = O.OP_INSERT if op[0] == "insert" else O.OP_DELETE
+            ops.append([kind, ix[op[1]], ix[op[2]], -1])
+    x = np.zeros((len(names), 1))
+    g2, _, net = O.apply_batch(g, x, np.array(ops), np.array(rows).reshape(-1, 1))
+    sets = O.affected_sets(g2, net, ex["agg"], ex["num_layers"])
+    for layer, want in ex["affected"].items():
+        got = sorted(names[i] for i in sets[int(layer)])
+        assert got == sorted(want), (ex["name"], layer, got, want)
+
+
+# ---------------------------------------------------------------------------
+# brute force: structural affected sets vs numerically changed rows
+# ---------------------------------------------------------------------------
+
+def _changed_rows(h_pre, h_post):
+    return np.nonzero(np.any(h_pre != h_post, axis=1))[0]
+
+
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
+@pytest.mark.parametrize("undirected", [False, True])
+def test_affected_sets_equal_changed_rows_without_activation(agg, undirected):
+    """With no activation and generic values, a vertex's embedding changes iff it
+    is structurally affected (Sec. IV-C: no pruning, and nothing else changes)."""
+    rng = np.random.default_rng(10 + ("sum", "mean", "gcn").index(agg) + 7 * undirected)
+    n, L = 30, 3
+    dims = (3, 4, 3, 2)
+    for trial in range(12):
+        src, dst = synth.erdos_renyi(n, 45 if undirected else 70, rng, undirected=undirected)
+        st = O.OracleState(n, src, dst, rng.standard_normal((n, dims[0])),
+                           _random_model(rng, agg, dims, relu_none=True), undirected)
+        pre = st.embeddings()
+        a, b = st.graph.arcs()
+        batch = synth.adversarial_batch(rng, n, dims[0], bs=int(rng.integers(1, 10)),
+                                        hot=6, existing=(a, b))
+        net, sets = st.apply(batch.ops, batch.feat_rows)
+        post = st.embeddings()
+        for l in range(1, L + 1):
+            np.testing.assert_array_equal(_changed_rows(pre[l], post[l]), sets[l],
+                                          err_msg=f"trial {trial} layer {l}")
+
+
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
+def test_changed_rows_within_affected_sets_with_relu(agg):
+    rng = np.random.default_rng(30)
+    n, dims = 40, (4, 5, 3)
+    for _ in range(8):
+        src, dst = synth.erdos_renyi(n, 90, rng)
+        st = O.OracleState(n, src, dst, rng.standard_normal((n, dims[0])),
+                           _random_model(rng, agg, dims, relu_all=True))
+        pre = st.embeddings()
+        a, b = st.graph.arcs()
+        batch = synth.adversarial_batch(rng, n, dims[0], bs=8, hot=8, existing=(a, b))
+        _, sets = st.apply(batch.ops, batch.feat_rows)
+        post = st.embeddings()
+        for l in range(1, 3):
+            assert set(_changed_rows(pre[l], post[l]).tolist()) <= set(sets[l].tolist())
+
+
+def test_gcn_tail_with_unchanged_out_degree_does_not_dirty_its_out_arcs():
+    """u loses one out-arc and gains another in the same batch: d_out(u) is
+    unchanged, so only the two sinks are affected at hop 1 (plus nothing else)."""
+    g = O.OracleGraph(5, [0, 0, 1], [1, 2, 3])
+    ops = np.array([[O.OP_DELETE, 0, 1, -1], [O.OP_INSERT, 0, 4, -1]])
+    g2, _, net = O.apply_batch(g, np.zeros((5, 1)), ops, np.zeros((0, 1)))
+    assert net.out_deg_changed.size == 0
+    sets = O.affected_sets(g2, net, "gcn", 1)
+    np.testing.assert_array_equal(sets[1], [1, 4])
+
+
+# ---------------------------------------------------------------------------
+# sequential semantics and invariants
+# ---------------------------------------------------------------------------
+
+def _brute_apply(n, arcs_set, x, ops, rows, undirected):
+    """Op-by-op application on a Python set (the plain meaning of a batch)."""
+    arcs_set = set(arcs_set)
+    x = x.copy()
+    for kind, u, v, f in ops.tolist():
+        if kind == O.OP_FEATURE:
+            x[u] = rows[f]
+            continue
+        if u == v:
+            continue
+        pairs = [(u, v), (v, u)] if undirected else [(u, v)]
+        for p in pairs:
+            if kind == O.OP_INSERT:
+                arcs_set.add(p)
+            else:
+                arcs_set.discard(p)
+    return arcs_set, x
+
+
+@pytest.mark.parametrize("undirected", [False, True])
+def test_batch_equals_op_by_op_application(undirected):
+    """Sec. IV-C.1: combined updates equal the updates applied one at a time."""
+    rng = np.random.default_rng(40 + undirected)
+    n, d = 25, 3
+    for _ in range(20):
+        src, dst = synth.erdos_renyi(n, 40, rng, undirected=undirected)
+        g = O.OracleGraph(n, src, dst, undirected)
+        x = rng.standard_normal((n, d))
+        a, b = g.arcs()
+        batch = synth.adversarial_batch(rng, n, d, bs=15, hot=5, existing=(a, b))
+        g2, x2, net = O.apply_batch(g, x, batch.ops, batch.feat_rows)
+        want_set, want_x = _brute_apply(n, zip(a.tolist(), b.tolist()), x, batch.ops,
+                                        batch.feat_rows, undirected)
+        got = set(zip(*[t.tolist() for t in g2.arcs()]))
+        assert got == want_set
+        np.testing.assert_array_equal(x2, want_x)
+        # one op per batch reaches the same state
+        g3, x3 = g, x
+        for i in range(batch.size):
+            g3, x3, _ = O.apply_batch(g3, x3, batch.ops[i:i + 1], batch.feat_rows)
+        np.testing.assert_array_equal(g3.keys, g2.keys)
+        np.testing.assert_array_equal(x3, x2)
+        # net sets are consistent with the two snapshots
+        pre = set(zip(a.tolist(), b.tolist()))
+        assert set(zip(net.ins_src.tolist(), net.ins_dst.tolist())) == got - pre
+        assert set(zip(net.del_src.tolist(), net.del_dst.tolist())) == pre - got
+
+
+def test_insert_then_delete_restores_embeddings():
+    rng = np.random.default_rng(50)
+    n, dims = 30, (3, 4, 2)
+    src, dst = synth.erdos_renyi(n, 60, rng)
+    st = O.OracleState(n, src, dst, rng.standard_normal((n, 3)), _random_model(rng, "mean", dims))
+    before = st.embeddings()
+    new = [(u, v) for u, v in itertools.product(range(n), range(n))
+           if u != v and not st.graph.has_arcs(np.array([u * n + v]))[0]][:10]
+    ins = np.array([[O.OP_INSERT, u, v, -1] for u, v in new])
+    dels = np.array([[O.OP_DELETE, u, v, -1] for u, v in new])
+    st.apply(ins, np.zeros((0, 3)))
+    st.apply(dels, np.zeros((0, 3)))
+    after = st.embeddings()
+    for l in range(3):
+        np.testing.assert_array_equal(before[l], after[l])
+
+
+def test_noop_accounting():
+    g = O.OracleGraph(4, [0, 1], [1, 2])
+    ops = np.array([
+        [O.OP_INSERT, 0, 1, -1],   # present already: no net change
+        [O.OP_DELETE, 2, 3, -1],   # absent: no net change
+        [O.OP_INSERT, 3, 3, -1],   # self-loop
+        [O.OP_INSERT, 2, 3, -1],   # net insert (last op on key (2,3))
+        [O.OP_DELETE, 1, 2, -1],   # net delete
+        [O.OP_FEATURE, 1, -1, 0],
+        [O.OP_FEATURE, 1, -1, 1],  # last write wins
+    ])
+    rows = np.array([[1.0, 1.0], [2.0, 2.0]])
+    g2, x2, net = O.apply_batch(g, np.zeros((4, 2)), ops, rows)
+    assert net.edge_keys == 3 and net.noop_edge_ops == 2
+    np.testing.assert_array_equal(net.ins_src, [2])
+    np.testing.assert_array_equal(net.del_src, [1])
+    np.testing.assert_array_equal(x2[1], [2.0, 2.0])
+    np.testing.assert_array_equal(net.heads, [2, 3])
+    np.testing.assert_array_equal(net.tails, [1, 2])
+
+
+def test_permutation_equivariance():
+    """Relabelling vertices permutes the embeddings (catches index mix-ups)."""
+    rng = np.random.default_rng(60)
+    n, dims = 35, (3, 5, 2)
+    src, dst = synth.erdos_renyi(n, 80, rng)
+    x = rng.standard_normal((n, 3))
+    perm = rng.permutation(n)
+    for agg in ("sum", "mean", "gcn"):
+        m = _random_model(rng, agg, dims)
+        h = O.full_recompute(O.OracleGraph(n, src, dst), x, m)
+        xp = np.empty_like(x)
+        xp[perm] = x
+        hp = O.full_recompute(O.OracleGraph(n, perm[src], perm[dst]), xp, m)
+        for l in range(3):
+            np.testing.assert_allclose(hp[l][perm], h[l], rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
+def test_sampled_embeddings_match_full_recompute(agg):
+    rng = np.random.default_rng(70)
+    n, dims = 200, (4, 6, 5, 3)
+    src, dst = synth.erdos_renyi(n, 900, rng)
+    g = O.OracleGraph(n, src, dst)
+    x = rng.standard_normal((n, 4))
+    m = _random_model(rng, agg, dims)
+    full = O.full_recompute(g, x, m)
+    verts = rng.choice(n, 7, replace=False)
+    for layer in (1, 2, 3):
+        vs, hv = O.sampled_embeddings(g, x, m, verts, upto_layer=layer)
+        np.testing.assert_allclose(hv, full[layer][vs], rtol=1e-12, atol=1e-12)
+
+
+def test_row_relative_error_definition():
+    ref = np.array([[1.0, -2.0], [0.0, 0.0], [4.0, 0.5]])
+    got = ref + np.array([[0.0, 2e-4], [0.0, 0.0], [-4e-4, 0.0]])
+    # row 0: 2e-4 / 2 = 1e-4; row 2: 4e-4 / 4 = 1e-4
+    assert math.isclose(O.row_relative_error(got, ref), 1e-4, rel_tol=1e-9)
+    eps = 1e-3 * math.sqrt(np.mean(ref * ref))
+    got2 = ref.copy()
+    got2[1, 0] = 1e-6
+    assert math.isclose(O.row_relative_error(got2, ref), 1e-6 / eps, rel_tol=1e-9)
