@@ -1,0 +1,234 @@
+/*
+ * ripple.h -- C ABI of the MI355X library for exact incremental propagation of
+ * GNN embeddings on a streaming graph (Ripple, arXiv 2505.12112).
+ *
+ * The problem statement (Sec. IV-A, "Assumptions") has four parts, one call each:
+ *   1. a graph G(V,E) and a trained L-layer GNN with a linear aggregator
+ *      ............................................. ripple_load_graph, ripple_init_embeddings
+ *   2. initial embeddings H^1..H^L of every vertex, computed before updates arrive
+ *      ............................................. ripple_init_embeddings
+ *   3. a stream of edge inserts, edge deletes and vertex-feature replacements,
+ *      applied in fixed-size batches (no vertex inserts or deletes)
+ *      ............................................. ripple_apply_updates
+ *   4. after each batch, the exact embeddings of every affected vertex are
+ *      available at once (trigger-based inference, Sec. II-B; exact within
+ *      floating-point precision, Sec. VI)
+ *      ............................................. ripple_get_embeddings, ripple_get_affected
+ *
+ * The GNN layer is Eq. (1)-(2) of Sec. II-A with one of the linear aggregators of
+ * Sec. II-C: x_v = Aggregate({h_u : u in N_in(v)}), h_v = sigma(Update(h_v, x_v)).
+ *   RIPPLE_AGG_SUM   GraphSAGE-sum : h = sigma(W_self h_v + W_neigh sum_u h_u + b)
+ *   RIPPLE_AGG_MEAN  GraphSAGE-mean: h = sigma(W_self h_v + W_neigh mean_u h_u + b),
+ *                    the mean is 0 for a vertex without in-neighbours
+ *   RIPPLE_AGG_GCN   GCN, symmetric normalisation with an implicit self-loop:
+ *                    h = sigma(W sum_{u in N_in(v) + v} h_u / sqrt((dout(u)+1)(din(v)+1)) + b)
+ *
+ * Graph semantics: a simple directed graph on vertices 0..n-1 (int32 ids).
+ * Inserting a present arc, deleting an absent arc, and inserting or deleting a
+ * self-loop are counted no-ops. A batch has sequential semantics: its net effect
+ * is what applying its ops in order leaves (an insert sets an arc present, a
+ * delete sets it absent, the last feature write to a vertex wins). On an
+ * undirected graph every edge op acts on both arcs u->v and v->u.
+ *
+ * Conventions for every call:
+ *   - Every call returns a ripple_status; nothing else crosses the ABI. On an
+ *     error the message is in ripple_last_error(ctx), valid until the next call
+ *     on that context.
+ *   - Pointer arguments are HOST pointers owned by the caller. The library
+ *     copies what it needs during the call and keeps no caller pointer.
+ *   - The library owns all device memory (hipMalloc on the context's device).
+ *   - Inputs are validated before any state changes: RIPPLE_E_INVALID leaves the
+ *     context exactly as it was.
+ *   - A HIP runtime error poisons the context: that call returns RIPPLE_E_DEVICE
+ *     and every later call except ripple_last_error / ripple_destroy returns
+ *     RIPPLE_E_STATE.
+ *   - A context is used by one host thread at a time. Calls are synchronous:
+ *     they return after the device work they issued has finished.
+ */
+#ifndef RIPPLE_H
+#define RIPPLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__) || defined(__clang__)
+#define RIPPLE_API __attribute__((visibility("default")))
+#else
+#define RIPPLE_API
+#endif
+
+#define RIPPLE_MAX_LAYERS 8
+#define RIPPLE_MAX_DIM 1024
+
+typedef struct ripple_ctx ripple_ctx;
+
+typedef enum {
+  RIPPLE_OK = 0,
+  RIPPLE_E_INVALID = 1, /* bad argument; state unchanged */
+  RIPPLE_E_STATE = 2,   /* call out of order (e.g. apply before init) or poisoned context */
+  RIPPLE_E_OOM = 3,     /* device allocation failed or would exceed max_device_bytes */
+  RIPPLE_E_DEVICE = 4   /* HIP runtime error; the context is now poisoned */
+} ripple_status;
+
+typedef enum { RIPPLE_AGG_SUM = 0, RIPPLE_AGG_MEAN = 1, RIPPLE_AGG_GCN = 2 } ripple_agg;
+
+typedef enum { RIPPLE_GEMM_FP32 = 0, RIPPLE_GEMM_BF16 = 1 } ripple_gemm_prec;
+
+enum { RIPPLE_OP_INSERT = 1, RIPPLE_OP_DELETE = 2, RIPPLE_OP_FEATURE = 3 };
+
+/* One update (16 bytes). Edge ops: (kind, u, v, -1). Feature replacement:
+ * (RIPPLE_OP_FEATURE, u, -1, feat_row): vertex u's features become row feat_row
+ * of the batch's feature block. */
+typedef struct {
+  int32_t kind;
+  int32_t u;
+  int32_t v;
+  int32_t feat_row;
+} ripple_op;
+
+/* Graph snapshot (Sec. IV-A: the graph before any update arrives). */
+typedef struct {
+  int64_t num_vertices;   /* n >= 1; ids are int32 in [0, n) */
+  int64_t num_edges;      /* entries in src/dst */
+  const int32_t *src;     /* host, [num_edges] */
+  const int32_t *dst;     /* host, [num_edges] */
+  int32_t undirected;     /* 1: entry (u,v) stands for arcs u->v and v->u */
+  float slack;            /* spare slots per adjacency row, as a fraction of its degree (>= 0) */
+  int32_t min_slack;      /* spare slots per row at least (>= 0) */
+  int32_t device;         /* HIP device ordinal */
+  void *stream;           /* hipStream_t to run on, or NULL for a library-owned stream */
+  int64_t max_device_bytes; /* 0 = no cap; else allocations beyond it fail with RIPPLE_E_OOM */
+} ripple_graph_desc;
+
+/* Trained model (Sec. IV-A: a trained L-layer GNN with a linear aggregator). */
+typedef struct {
+  int32_t num_layers;            /* L in [1, RIPPLE_MAX_LAYERS] */
+  int32_t agg;                   /* ripple_agg */
+  const int32_t *dims;           /* [L+1]: d_0 (feature width) .. d_L, each in [1, RIPPLE_MAX_DIM] */
+  const float *const *w_self;    /* [L] row-major [d_l][d_{l-1}]; ignored (may be NULL) for GCN */
+  const float *const *w_neigh;   /* [L] row-major [d_l][d_{l-1}]; GCN: its single W */
+  const float *const *bias;      /* [L] [d_l]; NULL array or NULL entry = zero bias */
+  const int32_t *relu;           /* [L] 1 = ReLU after layer l, 0 = identity */
+  int32_t gemm_prec;             /* ripple_gemm_prec; RIPPLE_GEMM_FP32 only in this version */
+} ripple_model_desc;
+
+/* What one ripple_apply_updates call did. Arc counts count directed arcs (an
+ * undirected edge is two arcs). */
+typedef struct {
+  int64_t num_ops;              /* ops in the batch */
+  int64_t edge_keys;            /* distinct non-loop edges the batch named */
+  int64_t noop_edge_ops;        /* self-loop edge ops + named edges whose state did not change */
+  int64_t ins_arcs;             /* net inserted arcs */
+  int64_t del_arcs;             /* net deleted arcs */
+  int64_t features;             /* vertices whose features were replaced (|A^0|) */
+  int64_t dirty[RIPPLE_MAX_LAYERS + 1];     /* [l], l=1..L: vertices whose layer-(l-1) contribution changed */
+  int64_t affected[RIPPLE_MAX_LAYERS + 1];  /* [l]: |A^l|, l = 0..L */
+  int64_t pushed_arcs[RIPPLE_MAX_LAYERS + 1]; /* [l]: out-arcs of the dirty set pushed at layer l */
+  int64_t dest_rows[RIPPLE_MAX_LAYERS + 1];   /* [l]: distinct sinks of those arcs */
+  int64_t relocated_rows;       /* adjacency rows moved to the spare arena */
+  int64_t repacks;              /* adjacency re-layouts this call needed (spare arena full) */
+} ripple_batch_stats;
+
+/* Part 1 of the problem statement: copies the snapshot to the device as an
+ * out-adjacency (CSR) and in-adjacency (CSC) with spare slots per row.
+ * Rejects (RIPPLE_E_INVALID) out-of-range ids, self-loops and repeated arcs
+ * (for undirected graphs also (u,v) together with (v,u)). On success *out owns
+ * a new context; on failure *out is NULL. */
+RIPPLE_API ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out);
+
+/* Parts 1-2: uploads features X = H^0 (host [n][d_0] row-major) and the model,
+ * then computes H^1..H^L of every vertex layer by layer and caches, per layer,
+ * the un-normalised neighbour aggregate that the incremental path updates.
+ * May be called again to restart from new features or weights. */
+RIPPLE_API ripple_status ripple_init_embeddings(ripple_ctx *ctx, const float *x, const ripple_model_desc *model);
+
+/* Part 3-4: applies one batch (Sec. IV-A batching; Sec. IV-C incremental
+ * propagation) and returns when H^0..H^L are updated for every affected vertex.
+ * ops: host [num_ops]; feat_rows: host [num_feat_rows][d_0] (may be NULL when
+ * there is no feature op). Rejects the whole batch, with no state change, for an
+ * unknown op kind, a vertex id outside [0, n), or a feat_row outside
+ * [0, num_feat_rows). stats may be NULL. num_ops = 0 is a valid empty batch. */
+RIPPLE_API ripple_status ripple_apply_updates(ripple_ctx *ctx, const ripple_op *ops, int64_t num_ops,
+                                   const float *feat_rows, int64_t num_feat_rows,
+                                   ripple_batch_stats *stats);
+
+/* Part 4: copies rows of H^layer (layer 0 = current features) to host out
+ * [count][d_layer]. ids: host [count] vertex ids, or NULL for all n rows in id
+ * order (count must then be n). */
+RIPPLE_API ripple_status ripple_get_embeddings(ripple_ctx *ctx, int32_t layer, const int32_t *ids,
+                                    int64_t count, float *out);
+
+/* Trigger output of the last batch: A^layer, the vertices whose layer-`layer`
+ * embedding the batch recomputed, in ascending id order (A^0 = vertices whose
+ * features were replaced). Writes min(|A^layer|, capacity) ids to `ids` and
+ * |A^layer| to *count (always). */
+RIPPLE_API ripple_status ripple_get_affected(ripple_ctx *ctx, int32_t layer, int32_t *ids, int64_t capacity,
+                                  int64_t *count);
+
+/* The cached aggregate of layer `layer` (1..L) the incremental path maintains:
+ * S^l_v = sum over in-neighbours u of c_u h^{l-1}_u, with c_u = 1 (sum, mean)
+ * or 1/sqrt(dout(u)+1) (GCN). Host out [count][d_{l-1}]; ids as in
+ * ripple_get_embeddings. For checking only. */
+RIPPLE_API ripple_status ripple_get_aggregates(ripple_ctx *ctx, int32_t layer, const int32_t *ids,
+                                    int64_t count, float *out);
+
+/* Copies the current arc set as (src, dst) pairs read from the out-adjacency
+ * (direction 0) or the in-adjacency (direction 1), grouped by row in row order.
+ * Writes min(arcs, capacity) pairs and the arc count to *count (always). */
+RIPPLE_API ripple_status ripple_get_arcs(ripple_ctx *ctx, int32_t direction, int32_t *src, int32_t *dst,
+                              int64_t capacity, int64_t *count);
+
+/* Device bytes the context holds. */
+RIPPLE_API ripple_status ripple_device_bytes(ripple_ctx *ctx, int64_t *bytes);
+
+/* Kernel timing (for measurement). With enable = 1, every later
+ * ripple_apply_updates records HIP events around each kernel phase on the
+ * context's stream and accumulates per phase: event milliseconds, kernel launches,
+ * and the phase's algorithmic HBM bytes and flops computed from the batch's own
+ * counts (each input row read once, each output row written once):
+ *   SCATTER, per layer l with dirty set D, pushed arcs E_D, distinct sinks R,
+ *            width d = d_{l-1}:  4 E_D + 8 |D| + 4 d |D| + 8 d R  bytes
+ *   GEMM,    per layer l with |A^l| rows, K = 2 d_{l-1} (SAGE) or d_{l-1} (GCN),
+ *            N = d_l:  flops 2 |A^l| K N; bytes 4 |A^l| K + 4 N K
+ *            + 4 |A^l| N (2 if the layer is the last, else 3: old row, new row, delta)
+ *   COMPACT, per compaction over n vertices with W = ceil(n/32) bitmap words and
+ *            c ids out:  24 W + 4 c bytes
+ * Other phases report bytes = flops = 0. enable = 0 stops recording.
+ * ripple_get_phase_stats copies min(capacity, RIPPLE_NUM_PHASES) entries and
+ * resets the sums. */
+#define RIPPLE_NUM_PHASES 8
+enum {
+  RIPPLE_PHASE_NET = 0,      /* op netting (hash + membership) */
+  RIPPLE_PHASE_TOPO = 1,     /* pre-batch corrections + adjacency update */
+  RIPPLE_PHASE_LAYER0 = 2,   /* feature writes and layer-0 deltas */
+  RIPPLE_PHASE_SCATTER = 3,  /* delta scatter-add + frontier marking, all layers */
+  RIPPLE_PHASE_COMPACT = 4,  /* frontier bitmaps -> sorted lists, all layers */
+  RIPPLE_PHASE_GEMM = 5,     /* gather + transform + epilogue, all layers */
+  RIPPLE_PHASE_OTHER = 6,    /* scratch clean-up */
+  RIPPLE_PHASE_TOTAL = 7     /* first to last kernel of the batch */
+};
+typedef struct {
+  double ms;
+  int64_t launches;
+  double bytes;
+  double flops;
+} ripple_phase_stats;
+RIPPLE_API ripple_status ripple_set_profiling(ripple_ctx *ctx, int32_t enable);
+RIPPLE_API ripple_status ripple_get_phase_stats(ripple_ctx *ctx, ripple_phase_stats *out, int32_t capacity);
+RIPPLE_API const char *ripple_phase_name(int32_t phase);
+
+/* Message of the last failed call on ctx ("" after a success). With ctx NULL:
+ * the message of this thread's last failed ripple_load_graph. */
+RIPPLE_API const char *ripple_last_error(const ripple_ctx *ctx);
+
+/* Frees the context and its device memory. NULL is a no-op. */
+RIPPLE_API void ripple_destroy(ripple_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RIPPLE_H */

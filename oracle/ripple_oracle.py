@@ -133,10 +133,12 @@ class OracleGraph:
             return np.empty(0, np.int64)
         lo = np.searchsorted(self.keys, verts * self.n)
         hi = np.searchsorted(self.keys, (verts + 1) * self.n)
-        if int((hi - lo).sum()) == 0:
+        cnt = hi - lo
+        total = int(cnt.sum())
+        if total == 0:
             return np.empty(0, np.int64)
-        idx = np.concatenate([np.arange(a, b) for a, b in zip(lo, hi) if b > a])
-        return self.keys[idx] % self.n
+        starts = np.repeat(lo - (np.cumsum(cnt) - cnt), cnt)
+        return self.keys[starts + np.arange(total)] % self.n
 
     def in_adjacency(self, weights: Optional[np.ndarray] = None, dtype=np.float64) -> sp.csr_matrix:
         """Sparse A with A[v, u] = weight of arc u->v (1 by default): row v lists

@@ -1,0 +1,986 @@
+// Host side of libripple: the context, argument validation, the adjacency build,
+// the bootstrap forward pass and the per-batch kernel pipeline.
+//
+// Batch pipeline (one stream, counts stay on the device, one host sync at the end):
+//   net:     hash ops, decide winners against the pre-batch adjacency
+//   topo:    count per-row inserts/deletes, plan arena moves, check the arena,
+//            pre-batch corrections of every layer's aggregate, deletes, row moves,
+//            inserts
+//   layer 0: mark the dirty set (feature writes; GCN: out-degree changes), compact,
+//            form layer-0 deltas and write the new feature rows
+//   layer l: scatter deltas along post-batch out-arcs + mark A^l, compact A^l,
+//            gather + MFMA transform + epilogue (new rows, next deltas)
+//   cleanup: reset per-batch scratch
+// An aborted batch (arena too small) changes nothing; the host re-lays the
+// adjacency out with fresh spare slots and runs the batch again.
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <numeric>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "internal.h"
+
+using rp::u64;
+
+namespace {
+
+struct PhaseEv {
+  int phase;
+  hipEvent_t a;
+  hipEvent_t b;
+};
+
+}  // namespace
+
+struct ripple_ctx {
+  int device = 0;
+  hipStream_t stream = nullptr;
+  bool own_stream = false;
+  long long n = 0;
+  int undirected = 0;
+  float slack = 0.25f;
+  int min_slack = 4;
+  long long max_bytes = 0;
+  long long bytes = 0;
+  std::unordered_map<void *, size_t> allocs;
+  std::string err;
+  bool poisoned = false;
+  bool inited = false;
+
+  // adjacency: [0] out (CSR by source), [1] in (CSC by sink)
+  rp::Adj adj[2] = {};
+  long long col_capacity[2] = {0, 0};
+
+  // model
+  int L = 0, agg = 0;
+  int dims[rp::kMaxL + 1] = {};
+  int relu[rp::kMaxL] = {};
+  int K[rp::kMaxL] = {};
+  float *W[rp::kMaxL] = {};
+  float *bias[rp::kMaxL] = {};
+  float *H[rp::kMaxL + 1] = {};
+  float *S[rp::kMaxL + 1] = {};
+  int dmax_delta = 0;
+
+  // persistent scratch (n-sized)
+  int *fop = nullptr;
+  int *ddeg = nullptr;
+  unsigned *bm_out = nullptr;
+  unsigned *bm_x = nullptr;
+  int *blocksum = nullptr;
+  int *lists[rp::kMaxL + 1] = {};
+  float *delta[2] = {nullptr, nullptr};
+  rp::Counters *d_counters = nullptr;
+  rp::Persist *d_persist = nullptr;
+  rp::Counters *h_counters = nullptr;  // pinned
+
+  // per-batch scratch, sized for cap_ops ops
+  long long cap_ops = 0;
+  long long cap_feat_rows = 0;
+  ripple_op *d_ops = nullptr;
+  ripple_op *h_ops = nullptr;  // pinned
+  float *d_feat = nullptr;
+  float *h_feat = nullptr;     // pinned
+  u64 *ht_key = nullptr;
+  int *ht_val = nullptr;
+  unsigned ht_mask = 0;
+  int *op_slot = nullptr;
+  int *ins_src = nullptr, *ins_dst = nullptr, *del_src = nullptr, *del_dst = nullptr;
+  int *ins_rank = nullptr, *del_rank = nullptr, *del_pos = nullptr;
+  rp::RelocItem *reloc = nullptr;
+  int *flist = nullptr;
+
+  // last batch
+  bool has_batch = false;
+  long long last_count[rp::kMaxL + 1] = {};
+  long long last_nfeat = 0;
+
+  // profiling
+  bool prof = false;
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
+  std::vector<PhaseEv> ev_log;
+  double ph_ms[RIPPLE_NUM_PHASES] = {};
+  long long ph_launch[RIPPLE_NUM_PHASES] = {};
+  double ph_bytes[RIPPLE_NUM_PHASES] = {};
+  double ph_flops[RIPPLE_NUM_PHASES] = {};
+};
+
+namespace {
+
+const char *kNullCtxMsg = "ripple: context is NULL";
+thread_local std::string g_load_err;  // message of the last failed ripple_load_graph
+
+ripple_status fail(ripple_ctx *c, ripple_status st, const std::string &msg) {
+  c->err = msg;
+  return st;
+}
+
+ripple_status device_fail(ripple_ctx *c, hipError_t e, const char *what) {
+  c->poisoned = true;
+  c->err = std::string("ripple: HIP error in ") + what + ": " + hipGetErrorString(e);
+  return RIPPLE_E_DEVICE;
+}
+
+#define RP_HIP(ctx, expr)                                    \
+  do {                                                       \
+    hipError_t _e = (expr);                                  \
+    if (_e != hipSuccess) return device_fail(ctx, _e, #expr); \
+  } while (0)
+
+#define RP_TRY(expr)                      \
+  do {                                    \
+    ripple_status _s = (expr);            \
+    if (_s != RIPPLE_OK) return _s;       \
+  } while (0)
+
+ripple_status dalloc(ripple_ctx *c, void **p, size_t size) {
+  *p = nullptr;
+  if (size == 0) size = 4;
+  if (c->max_bytes > 0 && c->bytes + static_cast<long long>(size) > c->max_bytes)
+    return fail(c, RIPPLE_E_OOM, "ripple: device byte cap reached (requested " + std::to_string(size) +
+                                     " bytes, holding " + std::to_string(c->bytes) + ")");
+  hipError_t e = hipMalloc(p, size);
+  if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    return fail(c, RIPPLE_E_OOM, "ripple: hipMalloc of " + std::to_string(size) + " bytes failed");
+  }
+  if (e != hipSuccess) return device_fail(c, e, "hipMalloc");
+  c->allocs[*p] = size;
+  c->bytes += static_cast<long long>(size);
+  return RIPPLE_OK;
+}
+
+template <typename T>
+ripple_status dalloc_n(ripple_ctx *c, T **p, long long count) {
+  return dalloc(c, reinterpret_cast<void **>(p), static_cast<size_t>(count) * sizeof(T));
+}
+
+void dfree(ripple_ctx *c, void *p) {
+  if (p == nullptr) return;
+  auto it = c->allocs.find(p);
+  if (it != c->allocs.end()) {
+    c->bytes -= static_cast<long long>(it->second);
+    c->allocs.erase(it);
+  }
+  (void)hipFree(p);
+}
+
+template <typename T>
+void dfree_t(ripple_ctx *c, T *&p) {
+  dfree(c, reinterpret_cast<void *>(p));
+  p = nullptr;
+}
+
+ripple_status check_ctx(ripple_ctx *c) {
+  if (c == nullptr) return RIPPLE_E_INVALID;
+  if (c->poisoned) {
+    if (c->err.empty()) c->err = "ripple: context poisoned by an earlier device error";
+    return RIPPLE_E_STATE;
+  }
+  c->err.clear();
+  hipError_t e = hipSetDevice(c->device);
+  if (e != hipSuccess) return device_fail(c, e, "hipSetDevice");
+  return RIPPLE_OK;
+}
+
+long long row_cap(int len, float slack, int min_slack) {
+  long long extra = static_cast<long long>(std::ceil(static_cast<double>(len) * slack));
+  if (extra < min_slack) extra = min_slack;
+  return len + extra;
+}
+
+// Uploads one adjacency direction laid out with spare slots per row and a spare
+// arena of max(65536, total / 2) slots at the end.
+ripple_status upload_adj(ripple_ctx *c, int dir, const std::vector<int> &len, const std::vector<int> &col_packed,
+                         const std::vector<long long> &packed_off) {
+  const long long n = c->n;
+  std::vector<long long> off(n);
+  std::vector<int> cap(n);
+  long long total = 0;
+  for (long long u = 0; u < n; ++u) {
+    off[u] = total;
+    const long long cp = row_cap(len[u], c->slack, c->min_slack);
+    if (cp > INT32_MAX) return fail(c, RIPPLE_E_INVALID, "ripple: adjacency row too long");
+    cap[u] = static_cast<int>(cp);
+    total += cp;
+  }
+  long long arena = std::max<long long>(65536, total / 2);
+  const long long capacity = total + arena;
+  std::vector<int> col(static_cast<size_t>(total), -1);
+  for (long long u = 0; u < n; ++u)
+    std::copy(col_packed.begin() + packed_off[u], col_packed.begin() + packed_off[u] + len[u], col.begin() + off[u]);
+  rp::Adj &a = c->adj[dir];
+  RP_TRY(dalloc_n(c, &a.off, n));
+  RP_TRY(dalloc_n(c, &a.len, n));
+  RP_TRY(dalloc_n(c, &a.cap, n));
+  RP_TRY(dalloc_n(c, &a.col, capacity));
+  RP_TRY(dalloc_n(c, &a.inscnt, n));
+  RP_TRY(dalloc_n(c, &a.delcnt, n));
+  RP_TRY(dalloc_n(c, &a.fillcnt, n));
+  RP_HIP(c, hipMemcpyAsync(a.off, off.data(), n * sizeof(long long), hipMemcpyHostToDevice, c->stream));
+  RP_HIP(c, hipMemcpyAsync(a.len, len.data(), n * sizeof(int), hipMemcpyHostToDevice, c->stream));
+  RP_HIP(c, hipMemcpyAsync(a.cap, cap.data(), n * sizeof(int), hipMemcpyHostToDevice, c->stream));
+  if (total > 0)
+    RP_HIP(c, hipMemcpyAsync(a.col, col.data(), total * sizeof(int), hipMemcpyHostToDevice, c->stream));
+  rp::launch_fill_i32(c->stream, a.col + total, arena, -1);
+  RP_HIP(c, hipMemsetAsync(a.inscnt, 0, n * sizeof(int), c->stream));
+  RP_HIP(c, hipMemsetAsync(a.delcnt, 0, n * sizeof(int), c->stream));
+  RP_HIP(c, hipMemsetAsync(a.fillcnt, 0, n * sizeof(int), c->stream));
+  u64 top = static_cast<u64>(total);
+  RP_HIP(c, hipMemcpyAsync(&c->d_persist->top[dir], &top, sizeof(u64), hipMemcpyHostToDevice, c->stream));
+  RP_HIP(c, hipStreamSynchronize(c->stream));
+  c->col_capacity[dir] = capacity;
+  return RIPPLE_OK;
+}
+
+// Re-lays one direction out compactly with fresh spare slots (after the arena ran out).
+ripple_status repack_adj(ripple_ctx *c, int dir) {
+  const long long n = c->n;
+  rp::Adj &a = c->adj[dir];
+  std::vector<int> len(n);
+  RP_HIP(c, hipMemcpyAsync(len.data(), a.len, n * sizeof(int), hipMemcpyDeviceToHost, c->stream));
+  RP_HIP(c, hipStreamSynchronize(c->stream));
+  std::vector<long long> off(n);
+  std::vector<int> cap(n);
+  long long total = 0;
+  for (long long u = 0; u < n; ++u) {
+    off[u] = total;
+    cap[u] = static_cast<int>(row_cap(len[u], c->slack, std::max(c->min_slack, 4)));
+    total += cap[u];
+  }
+  const long long arena = std::max<long long>(65536, total / 2);
+  const long long capacity = total + arena;
+  int *new_col = nullptr;
+  long long *new_off = nullptr;
+  RP_TRY(dalloc_n(c, &new_col, capacity));
+  RP_TRY(dalloc_n(c, &new_off, n));
+  RP_HIP(c, hipMemcpyAsync(new_off, off.data(), n * sizeof(long long), hipMemcpyHostToDevice, c->stream));
+  rp::launch_fill_i32(c->stream, new_col, capacity, -1);
+  rp::launch_repack_copy(c->stream, n, a.col, a.off, a.len, new_col, new_off);
+  RP_HIP(c, hipMemcpyAsync(a.cap, cap.data(), n * sizeof(int), hipMemcpyHostToDevice, c->stream));
+  RP_HIP(c, hipGetLastError());
+  RP_HIP(c, hipStreamSynchronize(c->stream));
+  dfree(c, a.col);
+  dfree(c, a.off);
+  a.col = new_col;
+  a.off = new_off;
+  u64 top = static_cast<u64>(total);
+  RP_HIP(c, hipMemcpyAsync(&c->d_persist->top[dir], &top, sizeof(u64), hipMemcpyHostToDevice, c->stream));
+  RP_HIP(c, hipStreamSynchronize(c->stream));
+  c->col_capacity[dir] = capacity;
+  return RIPPLE_OK;
+}
+
+void free_batch_scratch(ripple_ctx *c) {
+  dfree_t(c, c->d_ops);
+  dfree_t(c, c->d_feat);
+  dfree_t(c, c->ht_key);
+  dfree_t(c, c->ht_val);
+  dfree_t(c, c->op_slot);
+  dfree_t(c, c->ins_src);
+  dfree_t(c, c->ins_dst);
+  dfree_t(c, c->del_src);
+  dfree_t(c, c->del_dst);
+  dfree_t(c, c->ins_rank);
+  dfree_t(c, c->del_rank);
+  dfree_t(c, c->del_pos);
+  dfree_t(c, c->reloc);
+  dfree_t(c, c->flist);
+  if (c->h_ops) (void)hipHostFree(c->h_ops);
+  if (c->h_feat) (void)hipHostFree(c->h_feat);
+  c->h_ops = nullptr;
+  c->h_feat = nullptr;
+  c->cap_ops = 0;
+  c->cap_feat_rows = 0;
+}
+
+// Grows per-batch scratch to hold `ops` ops and `frows` feature rows.
+ripple_status ensure_batch_scratch(ripple_ctx *c, long long ops, long long frows) {
+  if (ops <= c->cap_ops && frows <= c->cap_feat_rows && c->d_ops != nullptr) return RIPPLE_OK;
+  long long cap = std::max<long long>({ops, c->cap_ops, 256});
+  long long fcap = std::max<long long>({frows, c->cap_feat_rows, 64});
+  if (ops > c->cap_ops) cap = std::max(cap, 2 * c->cap_ops);
+  RP_HIP(c, hipStreamSynchronize(c->stream));
+  free_batch_scratch(c);
+  const long long arcs = 2 * cap;           // net arcs (undirected edges give two)
+  unsigned ht = 64;
+  while (ht < 4 * static_cast<unsigned long long>(cap)) ht <<= 1;
+  RP_TRY(dalloc_n(c, &c->d_ops, cap));
+  RP_TRY(dalloc_n(c, &c->d_feat, fcap * c->dims[0]));
+  RP_TRY(dalloc_n(c, &c->ht_key, ht));
+  RP_TRY(dalloc_n(c, &c->ht_val, ht));
+  RP_TRY(dalloc_n(c, &c->op_slot, cap));
+  RP_TRY(dalloc_n(c, &c->ins_src, arcs));
+  RP_TRY(dalloc_n(c, &c->ins_dst, arcs));
+  RP_TRY(dalloc_n(c, &c->del_src, arcs));
+  RP_TRY(dalloc_n(c, &c->del_dst, arcs));
+  RP_TRY(dalloc_n(c, &c->ins_rank, 2 * arcs));
+  RP_TRY(dalloc_n(c, &c->del_rank, 2 * arcs));
+  RP_TRY(dalloc_n(c, &c->del_pos, 2 * arcs));
+  RP_TRY(dalloc_n(c, &c->reloc, 2 * arcs));
+  RP_TRY(dalloc_n(c, &c->flist, cap));
+  RP_HIP(c, hipHostMalloc(reinterpret_cast<void **>(&c->h_ops), cap * sizeof(ripple_op), hipHostMallocDefault));
+  RP_HIP(c, hipHostMalloc(reinterpret_cast<void **>(&c->h_feat), fcap * c->dims[0] * sizeof(float),
+                          hipHostMallocDefault));
+  rp::launch_fill_u64(c->stream, c->ht_key, ht, rp::kEmptyKey);
+  rp::launch_fill_i32(c->stream, c->ht_val, ht, -1);
+  RP_HIP(c, hipGetLastError());
+  RP_HIP(c, hipStreamSynchronize(c->stream));
+  c->ht_mask = ht - 1;
+  c->cap_ops = cap;
+  c->cap_feat_rows = fcap;
+  return RIPPLE_OK;
+}
+
+void free_model(ripple_ctx *c) {
+  for (int l = 0; l < rp::kMaxL; ++l) {
+    dfree_t(c, c->W[l]);
+    dfree_t(c, c->bias[l]);
+  }
+  for (int l = 0; l <= rp::kMaxL; ++l) {
+    dfree_t(c, c->H[l]);
+    dfree_t(c, c->S[l]);
+    dfree_t(c, c->lists[l]);
+  }
+  dfree_t(c, c->delta[0]);
+  dfree_t(c, c->delta[1]);
+  free_batch_scratch(c);
+  c->inited = false;
+}
+
+rp::LayerPtrs layer_ptrs(const ripple_ctx *c) {
+  rp::LayerPtrs lp{};
+  for (int l = 0; l <= c->L; ++l) {
+    lp.H[l] = c->H[l];
+    lp.S[l] = c->S[l];
+    lp.dims[l] = c->dims[l];
+  }
+  lp.L = c->L;
+  return lp;
+}
+
+rp::GemmArgs gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 *count, long long count_fixed,
+                       float *delta) {
+  rp::GemmArgs g{};
+  g.rows = rows;
+  g.count = count;
+  g.count_fixed = count_fixed;
+  g.Hprev = c->H[l - 1];
+  g.dprev = c->dims[l - 1];
+  g.S = c->S[l];
+  g.in_len = c->adj[1].len;
+  g.out_len = c->adj[0].len;
+  g.ddeg = c->ddeg;
+  g.W = c->W[l - 1];
+  g.K = c->K[l - 1];
+  g.N = c->dims[l];
+  g.bias = c->bias[l - 1];
+  g.relu = c->relu[l - 1];
+  g.H = c->H[l];
+  g.delta = delta;
+  g.agg = c->agg;
+  g.abort = count != nullptr ? &c->d_counters->abort : nullptr;
+  return g;
+}
+
+// --- profiling helpers ---
+
+hipEvent_t next_event(ripple_ctx *c) {
+  if (c->ev_used == c->ev_pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    c->ev_pool.push_back(e);
+  }
+  return c->ev_pool[c->ev_used++];
+}
+
+struct PhaseScope {
+  ripple_ctx *c;
+  int phase;
+  hipEvent_t a = nullptr;
+  PhaseScope(ripple_ctx *cc, int ph) : c(cc), phase(ph) {
+    if (c->prof) {
+      a = next_event(c);
+      if (a) (void)hipEventRecord(a, c->stream);
+    }
+  }
+  ~PhaseScope() {
+    if (c->prof && a) {
+      hipEvent_t b = next_event(c);
+      if (b) {
+        (void)hipEventRecord(b, c->stream);
+        c->ev_log.push_back(PhaseEv{phase, a, b});
+      }
+    }
+  }
+};
+
+void add_launches(ripple_ctx *c, int phase, int k) {
+  if (c->prof) c->ph_launch[phase] += k;
+}
+
+// Issues one batch. Returns after queuing; the caller syncs.
+void issue_batch(ripple_ctx *c, int B) {
+  hipStream_t s = c->stream;
+  rp::Counters *dc = c->d_counters;
+  const int gcn = c->agg == rp::kGcn;
+  const int cap_arcs = static_cast<int>(2 * c->cap_ops);
+  rp::Adj out = c->adj[0], in = c->adj[1];
+  (void)hipMemsetAsync(dc, 0, sizeof(rp::Counters), s);
+  {
+    PhaseScope ps(c, RIPPLE_PHASE_NET);
+    rp::launch_net_hash(s, c->d_ops, B, c->undirected, c->n, c->ht_key, c->ht_val, c->ht_mask, c->op_slot, c->fop,
+                        dc);
+    rp::launch_net_decide(s, c->d_ops, B, c->undirected, c->ht_val, c->op_slot, c->fop, out, in, c->ins_src,
+                          c->ins_dst, c->del_src, c->del_dst, c->flist, dc);
+    add_launches(c, RIPPLE_PHASE_NET, 2);
+  }
+  {
+    PhaseScope ps(c, RIPPLE_PHASE_TOPO);
+    rp::launch_topo_count(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank,
+                          c->del_rank, dc);
+    rp::launch_topo_plan(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->ins_rank, c->reloc, dc);
+    rp::launch_topo_check(s, dc, c->d_persist, c->col_capacity[0], c->col_capacity[1]);
+    rp::launch_corrections(s, cap_arcs, c->agg, layer_ptrs(c), c->adj[0].len, c->ins_src, c->ins_dst, c->del_src,
+                           c->del_dst, dc);
+    rp::launch_del_apply(s, cap_arcs, out, in, c->del_src, c->del_dst, c->del_rank, c->del_pos, c->ddeg, dc);
+    rp::launch_reloc(s, 2 * cap_arcs, out, in, c->reloc, c->d_persist, dc);
+    rp::launch_ins_apply(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->ins_rank, c->ddeg, dc);
+    add_launches(c, RIPPLE_PHASE_TOPO, 10);
+  }
+  {
+    PhaseScope ps(c, RIPPLE_PHASE_LAYER0);
+    rp::launch_mark_dirty0(s, static_cast<int>(c->cap_ops), cap_arcs, gcn, c->flist, c->ins_src, c->del_src, c->ddeg,
+                           c->bm_x, dc);
+    rp::launch_compact(s, c->n, c->bm_out, c->bm_x, c->blocksum, c->lists[0], &dc->count[0]);
+    rp::launch_delta0(s, c->n, c->agg, c->dims[0], c->lists[0], &dc->count[0], c->d_ops, c->d_feat, c->fop,
+                      c->H[0], c->adj[0].len, c->ddeg, c->delta[0], dc);
+    add_launches(c, RIPPLE_PHASE_LAYER0, 4);
+  }
+  for (int l = 1; l <= c->L; ++l) {
+    float *din = c->delta[(l - 1) & 1];
+    float *dout = l < c->L ? c->delta[l & 1] : nullptr;
+    {
+      PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
+      rp::launch_scatter(s, c->n, c->dims[l - 1], c->lists[l - 1], &dc->count[l - 1], din, out, c->S[l], c->bm_out,
+                         c->bm_x, c->ins_dst, c->del_dst, cap_arcs, &dc->pushed[l], &dc->dest[l], dc);
+      add_launches(c, RIPPLE_PHASE_SCATTER, 1);
+    }
+    {
+      PhaseScope ps(c, RIPPLE_PHASE_COMPACT);
+      rp::launch_compact(s, c->n, c->bm_out, c->bm_x, c->blocksum, c->lists[l], &dc->count[l]);
+      add_launches(c, RIPPLE_PHASE_COMPACT, 2);
+    }
+    {
+      PhaseScope ps(c, RIPPLE_PHASE_GEMM);
+      rp::launch_gemm(s, gemm_args(c, l, c->lists[l], &dc->count[l], 0, dout), c->n);
+      add_launches(c, RIPPLE_PHASE_GEMM, 1);
+    }
+  }
+  {
+    PhaseScope ps(c, RIPPLE_PHASE_OTHER);
+    rp::launch_cleanup(s, B, cap_arcs, c->d_ops, c->op_slot, c->ht_key, c->ht_val, c->fop, out, in, c->ins_src,
+                       c->ins_dst, c->del_src, c->del_dst, c->ddeg, dc);
+    add_launches(c, RIPPLE_PHASE_OTHER, 1);
+  }
+  (void)hipMemcpyAsync(c->h_counters, dc, sizeof(rp::Counters), hipMemcpyDeviceToHost, s);
+}
+
+void account_phases(ripple_ctx *c) {
+  if (!c->prof) return;
+  const rp::Counters &k = *c->h_counters;
+  float total = 0.0f;
+  hipEvent_t first = nullptr, last = nullptr;
+  for (const PhaseEv &p : c->ev_log) {
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) c->ph_ms[p.phase] += ms;
+    if (!first) first = p.a;
+    last = p.b;
+  }
+  if (first && last && hipEventElapsedTime(&total, first, last) == hipSuccess) c->ph_ms[RIPPLE_PHASE_TOTAL] += total;
+  c->ph_launch[RIPPLE_PHASE_TOTAL] += 1;
+  const double words = static_cast<double>((c->n + 31) / 32);
+  for (int l = 1; l <= c->L; ++l) {
+    const double d = c->dims[l - 1];
+    const double nd = static_cast<double>(k.count[l - 1]);
+    c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * k.pushed[l] + 8.0 * nd + 4.0 * d * nd + 8.0 * d * k.dest[l];
+    const double m = static_cast<double>(k.count[l]);
+    const double K = c->K[l - 1], N = c->dims[l];
+    c->ph_flops[RIPPLE_PHASE_GEMM] += 2.0 * m * K * N;
+    c->ph_bytes[RIPPLE_PHASE_GEMM] += 4.0 * m * K + 4.0 * N * K + 4.0 * m * N * (l < c->L ? 3.0 : 2.0);
+    c->ph_bytes[RIPPLE_PHASE_COMPACT] += 24.0 * words + 4.0 * m;
+  }
+  c->ev_log.clear();
+  c->ev_used = 0;
+}
+
+bool validate_ops(ripple_ctx *c, const ripple_op *ops, long long num_ops, long long num_feat_rows) {
+  for (long long i = 0; i < num_ops; ++i) {
+    const ripple_op &o = ops[i];
+    if (o.kind == RIPPLE_OP_INSERT || o.kind == RIPPLE_OP_DELETE) {
+      if (o.u < 0 || o.u >= c->n || o.v < 0 || o.v >= c->n) {
+        c->err = "ripple: op " + std::to_string(i) + ": vertex id out of range";
+        return false;
+      }
+    } else if (o.kind == RIPPLE_OP_FEATURE) {
+      if (o.u < 0 || o.u >= c->n) {
+        c->err = "ripple: op " + std::to_string(i) + ": vertex id out of range";
+        return false;
+      }
+      if (o.feat_row < 0 || o.feat_row >= num_feat_rows) {
+        c->err = "ripple: op " + std::to_string(i) + ": feat_row out of range";
+        return false;
+      }
+    } else {
+      c->err = "ripple: op " + std::to_string(i) + ": unknown kind " + std::to_string(o.kind);
+      return false;
+    }
+  }
+  return true;
+}
+
+ripple_status read_rows(ripple_ctx *c, const float *src, int d, const int32_t *ids, long long count, float *out) {
+  if (count < 0) return fail(c, RIPPLE_E_INVALID, "ripple: negative count");
+  if (count == 0) return RIPPLE_OK;
+  if (out == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: out is NULL");
+  if (ids == nullptr) {
+    if (count != c->n) return fail(c, RIPPLE_E_INVALID, "ripple: ids NULL requires count == n");
+    RP_HIP(c, hipMemcpyAsync(out, src, static_cast<size_t>(count) * d * sizeof(float), hipMemcpyDeviceToHost,
+                             c->stream));
+    RP_HIP(c, hipStreamSynchronize(c->stream));
+    return RIPPLE_OK;
+  }
+  for (long long i = 0; i < count; ++i)
+    if (ids[i] < 0 || ids[i] >= c->n) return fail(c, RIPPLE_E_INVALID, "ripple: vertex id out of range");
+  int *d_ids = nullptr;
+  float *d_out = nullptr;
+  RP_TRY(dalloc_n(c, &d_ids, count));
+  ripple_status st = dalloc_n(c, &d_out, count * d);
+  if (st != RIPPLE_OK) {
+    dfree(c, d_ids);
+    return st;
+  }
+  hipError_t e = hipMemcpyAsync(d_ids, ids, count * sizeof(int), hipMemcpyHostToDevice, c->stream);
+  if (e == hipSuccess) {
+    rp::launch_gather_rows(c->stream, src, d, d_ids, count, d_out);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(out, d_out, static_cast<size_t>(count) * d * sizeof(float), hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  dfree(c, d_ids);
+  dfree(c, d_out);
+  if (e != hipSuccess) return device_fail(c, e, "read_rows");
+  return RIPPLE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
+  if (out == nullptr) return RIPPLE_E_INVALID;
+  *out = nullptr;
+  if (g == nullptr) return RIPPLE_E_INVALID;
+  ripple_ctx *c = new ripple_ctx();
+  g_load_err.clear();
+  auto bail = [&](ripple_status st) {
+    g_load_err = c->err;
+    ripple_destroy(c);
+    return st;
+  };
+  const long long n = g->num_vertices, m = g->num_edges;
+  if (n < 1 || n > INT32_MAX) {
+    c->err = "ripple: num_vertices must be in [1, 2^31)";
+    return bail(RIPPLE_E_INVALID);
+  }
+  if (m < 0 || (m > 0 && (g->src == nullptr || g->dst == nullptr))) {
+    c->err = "ripple: bad edge arrays";
+    return bail(RIPPLE_E_INVALID);
+  }
+  if (!(g->slack >= 0.0f) || g->min_slack < 0) {
+    c->err = "ripple: slack must be >= 0";
+    return bail(RIPPLE_E_INVALID);
+  }
+  c->n = n;
+  c->undirected = g->undirected ? 1 : 0;
+  c->slack = g->slack;
+  c->min_slack = g->min_slack;
+  c->device = g->device;
+  c->max_bytes = g->max_device_bytes;
+  // host-side validation and counting sort into CSR (by source) and CSC (by sink)
+  const long long arcs = c->undirected ? 2 * m : m;
+  std::vector<int> outdeg(n, 0), indeg(n, 0);
+  for (long long i = 0; i < m; ++i) {
+    const int u = g->src[i], v = g->dst[i];
+    if (u < 0 || u >= n || v < 0 || v >= n) {
+      c->err = "ripple: edge " + std::to_string(i) + ": vertex id out of range";
+      return bail(RIPPLE_E_INVALID);
+    }
+    if (u == v) {
+      c->err = "ripple: edge " + std::to_string(i) + ": self-loop";
+      return bail(RIPPLE_E_INVALID);
+    }
+    outdeg[u]++;
+    indeg[v]++;
+    if (c->undirected) {
+      outdeg[v]++;
+      indeg[u]++;
+    }
+  }
+  std::vector<long long> ooff(n + 1, 0), ioff(n + 1, 0);
+  for (long long u = 0; u < n; ++u) {
+    ooff[u + 1] = ooff[u] + outdeg[u];
+    ioff[u + 1] = ioff[u] + indeg[u];
+  }
+  std::vector<int> ocol(arcs), icol(arcs);
+  {
+    std::vector<long long> fo(ooff.begin(), ooff.end() - 1);
+    for (long long i = 0; i < m; ++i) {
+      const int u = g->src[i], v = g->dst[i];
+      ocol[fo[u]++] = v;
+      if (c->undirected) ocol[fo[v]++] = u;
+    }
+  }
+  for (long long u = 0; u < n; ++u) {
+    std::sort(ocol.begin() + ooff[u], ocol.begin() + ooff[u + 1]);
+    for (long long e = ooff[u] + 1; e < ooff[u + 1]; ++e)
+      if (ocol[e] == ocol[e - 1]) {
+        c->err = "ripple: repeated arc " + std::to_string(u) + "->" + std::to_string(ocol[e]);
+        return bail(RIPPLE_E_INVALID);
+      }
+  }
+  {
+    // stable over CSR order, so every in-row is sorted by source
+    std::vector<long long> fi(ioff.begin(), ioff.end() - 1);
+    for (long long u = 0; u < n; ++u)
+      for (long long e = ooff[u]; e < ooff[u + 1]; ++e) icol[fi[ocol[e]]++] = static_cast<int>(u);
+  }
+  hipError_t e = hipSetDevice(c->device);
+  if (e != hipSuccess) return bail(device_fail(c, e, "hipSetDevice"));
+  if (g->stream != nullptr) {
+    c->stream = static_cast<hipStream_t>(g->stream);
+  } else {
+    e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
+    if (e != hipSuccess) return bail(device_fail(c, e, "hipStreamCreate"));
+    c->own_stream = true;
+  }
+  ripple_status st;
+  if ((st = dalloc_n(c, &c->d_persist, 1)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->d_counters, 1)) != RIPPLE_OK) return bail(st);
+  e = hipHostMalloc(reinterpret_cast<void **>(&c->h_counters), sizeof(rp::Counters), hipHostMallocDefault);
+  if (e != hipSuccess) return bail(device_fail(c, e, "hipHostMalloc"));
+  std::vector<int> olen(outdeg), ilen(indeg);
+  if ((st = upload_adj(c, 0, olen, ocol, ooff)) != RIPPLE_OK) return bail(st);
+  if ((st = upload_adj(c, 1, ilen, icol, ioff)) != RIPPLE_OK) return bail(st);
+  // persistent per-vertex scratch
+  const long long words = (n + 31) / 32;
+  if ((st = dalloc_n(c, &c->fop, n)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->ddeg, n)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->bm_out, words)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->bm_x, words)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->blocksum, rp::compact_blocks(n) + 1)) != RIPPLE_OK) return bail(st);
+  rp::launch_fill_i32(c->stream, c->fop, n, -1);
+  e = hipMemsetAsync(c->ddeg, 0, n * sizeof(int), c->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(c->bm_out, 0, words * sizeof(unsigned), c->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(c->bm_x, 0, words * sizeof(unsigned), c->stream);
+  if (e == hipSuccess) e = hipGetLastError();
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return bail(device_fail(c, e, "load_graph init"));
+  *out = c;
+  return RIPPLE_OK;
+}
+
+ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple_model_desc *md) {
+  RP_TRY(check_ctx(c));
+  if (x == nullptr || md == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: x and model must be non-NULL");
+  const int L = md->num_layers;
+  if (L < 1 || L > rp::kMaxL) return fail(c, RIPPLE_E_INVALID, "ripple: num_layers out of range");
+  if (md->agg < 0 || md->agg > 2) return fail(c, RIPPLE_E_INVALID, "ripple: unknown aggregator");
+  if (md->gemm_prec != RIPPLE_GEMM_FP32) return fail(c, RIPPLE_E_INVALID, "ripple: only RIPPLE_GEMM_FP32 is built");
+  if (md->dims == nullptr || md->w_neigh == nullptr || md->relu == nullptr)
+    return fail(c, RIPPLE_E_INVALID, "ripple: dims, w_neigh and relu must be non-NULL");
+  if (md->agg != RIPPLE_AGG_GCN && md->w_self == nullptr)
+    return fail(c, RIPPLE_E_INVALID, "ripple: w_self must be non-NULL for GraphSAGE");
+  for (int l = 0; l <= L; ++l)
+    if (md->dims[l] < 1 || md->dims[l] > RIPPLE_MAX_DIM) return fail(c, RIPPLE_E_INVALID, "ripple: dim out of range");
+  for (int l = 0; l < L; ++l) {
+    if (md->w_neigh[l] == nullptr || (md->agg != RIPPLE_AGG_GCN && md->w_self[l] == nullptr))
+      return fail(c, RIPPLE_E_INVALID, "ripple: missing weight matrix");
+  }
+  free_model(c);
+  c->L = L;
+  c->agg = md->agg;
+  for (int l = 0; l <= L; ++l) c->dims[l] = md->dims[l];
+  c->dmax_delta = 0;
+  for (int l = 0; l < L; ++l) c->dmax_delta = std::max(c->dmax_delta, c->dims[l]);
+  const long long n = c->n;
+  // weights: SAGE W = [W_self | W_neigh] (K = 2 d_{l-1}); GCN W (K = d_{l-1})
+  for (int l = 1; l <= L; ++l) {
+    const int dp = c->dims[l - 1], dn = c->dims[l];
+    const int K = md->agg == RIPPLE_AGG_GCN ? dp : 2 * dp;
+    c->K[l - 1] = K;
+    c->relu[l - 1] = md->relu[l - 1] ? 1 : 0;
+    std::vector<float> w(static_cast<size_t>(dn) * K);
+    for (int j = 0; j < dn; ++j) {
+      if (md->agg == RIPPLE_AGG_GCN) {
+        std::memcpy(&w[static_cast<size_t>(j) * K], md->w_neigh[l - 1] + static_cast<size_t>(j) * dp,
+                    dp * sizeof(float));
+      } else {
+        std::memcpy(&w[static_cast<size_t>(j) * K], md->w_self[l - 1] + static_cast<size_t>(j) * dp,
+                    dp * sizeof(float));
+        std::memcpy(&w[static_cast<size_t>(j) * K + dp], md->w_neigh[l - 1] + static_cast<size_t>(j) * dp,
+                    dp * sizeof(float));
+      }
+    }
+    std::vector<float> b(dn, 0.0f);
+    if (md->bias != nullptr && md->bias[l - 1] != nullptr) std::memcpy(b.data(), md->bias[l - 1], dn * sizeof(float));
+    RP_TRY(dalloc_n(c, &c->W[l - 1], static_cast<long long>(dn) * K));
+    RP_TRY(dalloc_n(c, &c->bias[l - 1], dn));
+    RP_HIP(c, hipMemcpyAsync(c->W[l - 1], w.data(), w.size() * sizeof(float), hipMemcpyHostToDevice, c->stream));
+    RP_HIP(c, hipMemcpyAsync(c->bias[l - 1], b.data(), dn * sizeof(float), hipMemcpyHostToDevice, c->stream));
+    RP_HIP(c, hipStreamSynchronize(c->stream));
+  }
+  for (int l = 0; l <= L; ++l) {
+    RP_TRY(dalloc_n(c, &c->H[l], n * c->dims[l]));
+    RP_TRY(dalloc_n(c, &c->lists[l], n));
+    if (l >= 1) RP_TRY(dalloc_n(c, &c->S[l], n * c->dims[l - 1]));
+  }
+  RP_TRY(dalloc_n(c, &c->delta[0], n * c->dmax_delta));
+  RP_TRY(dalloc_n(c, &c->delta[1], n * c->dmax_delta));
+  RP_HIP(c, hipMemcpyAsync(c->H[0], x, static_cast<size_t>(n) * c->dims[0] * sizeof(float), hipMemcpyHostToDevice,
+                           c->stream));
+  // bootstrap: layer-wise full forward pass (pull aggregate over in-rows, then transform)
+  for (int l = 1; l <= L; ++l) {
+    rp::launch_pull(c->stream, n, c->dims[l - 1], c->agg, c->H[l - 1], c->adj[1], c->adj[0].len, c->S[l]);
+    rp::launch_gemm(c->stream, gemm_args(c, l, nullptr, nullptr, n, nullptr), n);
+    RP_HIP(c, hipGetLastError());
+  }
+  RP_HIP(c, hipStreamSynchronize(c->stream));
+  c->inited = true;
+  c->has_batch = false;
+  return RIPPLE_OK;
+}
+
+ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t num_ops, const float *feat_rows,
+                                   int64_t num_feat_rows, ripple_batch_stats *stats) {
+  RP_TRY(check_ctx(c));
+  if (!c->inited) return fail(c, RIPPLE_E_STATE, "ripple: ripple_init_embeddings has not run");
+  if (num_ops < 0 || num_feat_rows < 0) return fail(c, RIPPLE_E_INVALID, "ripple: negative count");
+  if (num_ops > (1LL << 26)) return fail(c, RIPPLE_E_INVALID, "ripple: batch larger than 2^26 ops");
+  if (num_ops > 0 && ops == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: ops is NULL");
+  if (num_feat_rows > 0 && feat_rows == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: feat_rows is NULL");
+  if (!validate_ops(c, ops, num_ops, num_feat_rows)) return RIPPLE_E_INVALID;
+  RP_TRY(ensure_batch_scratch(c, num_ops, num_feat_rows));
+  const int B = static_cast<int>(num_ops);
+  if (B > 0) {
+    std::memcpy(c->h_ops, ops, static_cast<size_t>(B) * sizeof(ripple_op));
+    RP_HIP(c, hipMemcpyAsync(c->d_ops, c->h_ops, static_cast<size_t>(B) * sizeof(ripple_op), hipMemcpyHostToDevice,
+                             c->stream));
+  }
+  if (num_feat_rows > 0) {
+    const size_t fb = static_cast<size_t>(num_feat_rows) * c->dims[0] * sizeof(float);
+    std::memcpy(c->h_feat, feat_rows, fb);
+    RP_HIP(c, hipMemcpyAsync(c->d_feat, c->h_feat, fb, hipMemcpyHostToDevice, c->stream));
+  }
+  long long repacks = 0;
+  for (int attempt = 0;; ++attempt) {
+    issue_batch(c, B);
+    RP_HIP(c, hipGetLastError());
+    RP_HIP(c, hipStreamSynchronize(c->stream));
+    if (!c->h_counters->abort) break;
+    // the spare arena cannot take this batch's row moves: nothing was mutated
+    c->ev_log.clear();
+    c->ev_used = 0;
+    if (attempt >= 2) {
+      c->poisoned = true;
+      return fail(c, RIPPLE_E_DEVICE, "ripple: adjacency re-layout did not make room for the batch");
+    }
+    RP_TRY(repack_adj(c, 0));
+    RP_TRY(repack_adj(c, 1));
+    ++repacks;
+  }
+  const rp::Counters &k = *c->h_counters;
+  if (k.err) {
+    c->poisoned = true;
+    return fail(c, RIPPLE_E_DEVICE, "ripple: device adjacency inconsistent (deleted arc not found)");
+  }
+  account_phases(c);
+  c->has_batch = true;
+  c->last_nfeat = static_cast<long long>(k.n_feat);
+  for (int l = 0; l <= c->L; ++l) c->last_count[l] = static_cast<long long>(k.count[l]);
+  if (stats != nullptr) {
+    std::memset(stats, 0, sizeof(*stats));
+    stats->num_ops = num_ops;
+    stats->edge_keys = static_cast<int64_t>(k.edge_keys);
+    stats->noop_edge_ops = static_cast<int64_t>(k.noop_edge);
+    stats->ins_arcs = static_cast<int64_t>(k.n_ins);
+    stats->del_arcs = static_cast<int64_t>(k.n_del);
+    stats->features = static_cast<int64_t>(k.n_feat);
+    stats->affected[0] = static_cast<int64_t>(k.n_feat);
+    for (int l = 1; l <= c->L; ++l) {
+      stats->dirty[l] = static_cast<int64_t>(k.count[l - 1]);
+      stats->affected[l] = static_cast<int64_t>(k.count[l]);
+      stats->pushed_arcs[l] = static_cast<int64_t>(k.pushed[l]);
+      stats->dest_rows[l] = static_cast<int64_t>(k.dest[l]);
+    }
+    stats->relocated_rows = static_cast<int64_t>(k.n_reloc);
+    stats->repacks = repacks;
+  }
+  return RIPPLE_OK;
+}
+
+ripple_status ripple_get_embeddings(ripple_ctx *c, int32_t layer, const int32_t *ids, int64_t count, float *out) {
+  RP_TRY(check_ctx(c));
+  if (!c->inited) return fail(c, RIPPLE_E_STATE, "ripple: ripple_init_embeddings has not run");
+  if (layer < 0 || layer > c->L) return fail(c, RIPPLE_E_INVALID, "ripple: layer out of range");
+  return read_rows(c, c->H[layer], c->dims[layer], ids, count, out);
+}
+
+ripple_status ripple_get_aggregates(ripple_ctx *c, int32_t layer, const int32_t *ids, int64_t count, float *out) {
+  RP_TRY(check_ctx(c));
+  if (!c->inited) return fail(c, RIPPLE_E_STATE, "ripple: ripple_init_embeddings has not run");
+  if (layer < 1 || layer > c->L) return fail(c, RIPPLE_E_INVALID, "ripple: layer out of range");
+  return read_rows(c, c->S[layer], c->dims[layer - 1], ids, count, out);
+}
+
+ripple_status ripple_get_affected(ripple_ctx *c, int32_t layer, int32_t *ids, int64_t capacity, int64_t *count) {
+  RP_TRY(check_ctx(c));
+  if (count == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: count is NULL");
+  *count = 0;
+  if (!c->inited) return fail(c, RIPPLE_E_STATE, "ripple: ripple_init_embeddings has not run");
+  if (layer < 0 || layer > c->L) return fail(c, RIPPLE_E_INVALID, "ripple: layer out of range");
+  if (capacity < 0 || (capacity > 0 && ids == nullptr)) return fail(c, RIPPLE_E_INVALID, "ripple: bad ids buffer");
+  if (!c->has_batch) return RIPPLE_OK;
+  if (layer == 0) {
+    const long long nf = c->last_nfeat;
+    std::vector<int> f(nf);
+    if (nf > 0) {
+      RP_HIP(c, hipMemcpyAsync(f.data(), c->flist, nf * sizeof(int), hipMemcpyDeviceToHost, c->stream));
+      RP_HIP(c, hipStreamSynchronize(c->stream));
+    }
+    std::sort(f.begin(), f.end());
+    *count = nf;
+    const long long w = std::min<long long>(nf, capacity);
+    if (w > 0) std::memcpy(ids, f.data(), w * sizeof(int));
+    return RIPPLE_OK;
+  }
+  const long long cnt = c->last_count[layer];
+  *count = cnt;
+  const long long w = std::min<long long>(cnt, capacity);
+  if (w > 0) {
+    RP_HIP(c, hipMemcpyAsync(ids, c->lists[layer], w * sizeof(int), hipMemcpyDeviceToHost, c->stream));
+    RP_HIP(c, hipStreamSynchronize(c->stream));
+  }
+  return RIPPLE_OK;
+}
+
+ripple_status ripple_get_arcs(ripple_ctx *c, int32_t direction, int32_t *src, int32_t *dst, int64_t capacity,
+                              int64_t *count) {
+  RP_TRY(check_ctx(c));
+  if (count == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: count is NULL");
+  *count = 0;
+  if (direction != 0 && direction != 1) return fail(c, RIPPLE_E_INVALID, "ripple: direction must be 0 or 1");
+  if (capacity < 0 || (capacity > 0 && (src == nullptr || dst == nullptr)))
+    return fail(c, RIPPLE_E_INVALID, "ripple: bad output buffers");
+  const long long n = c->n;
+  const rp::Adj &a = c->adj[direction];
+  std::vector<long long> off(n);
+  std::vector<int> len(n);
+  std::vector<int> col(c->col_capacity[direction]);
+  RP_HIP(c, hipMemcpyAsync(off.data(), a.off, n * sizeof(long long), hipMemcpyDeviceToHost, c->stream));
+  RP_HIP(c, hipMemcpyAsync(len.data(), a.len, n * sizeof(int), hipMemcpyDeviceToHost, c->stream));
+  RP_HIP(c, hipMemcpyAsync(col.data(), a.col, col.size() * sizeof(int), hipMemcpyDeviceToHost, c->stream));
+  RP_HIP(c, hipStreamSynchronize(c->stream));
+  long long k = 0;
+  for (long long u = 0; u < n; ++u) {
+    for (int e = 0; e < len[u]; ++e, ++k) {
+      if (k < capacity) {
+        const int w = col[off[u] + e];
+        src[k] = direction == 0 ? static_cast<int>(u) : w;
+        dst[k] = direction == 0 ? w : static_cast<int>(u);
+      }
+    }
+  }
+  *count = k;
+  return RIPPLE_OK;
+}
+
+ripple_status ripple_device_bytes(ripple_ctx *c, int64_t *bytes) {
+  if (c == nullptr || bytes == nullptr) return RIPPLE_E_INVALID;
+  *bytes = c->bytes;
+  return RIPPLE_OK;
+}
+
+ripple_status ripple_set_profiling(ripple_ctx *c, int32_t enable) {
+  RP_TRY(check_ctx(c));
+  c->prof = enable != 0;
+  c->ev_log.clear();
+  c->ev_used = 0;
+  return RIPPLE_OK;
+}
+
+ripple_status ripple_get_phase_stats(ripple_ctx *c, ripple_phase_stats *out, int32_t capacity) {
+  RP_TRY(check_ctx(c));
+  if (capacity < 0 || (capacity > 0 && out == nullptr)) return fail(c, RIPPLE_E_INVALID, "ripple: bad buffer");
+  for (int p = 0; p < RIPPLE_NUM_PHASES && p < capacity; ++p) {
+    out[p].ms = c->ph_ms[p];
+    out[p].launches = c->ph_launch[p];
+    out[p].bytes = c->ph_bytes[p];
+    out[p].flops = c->ph_flops[p];
+  }
+  for (int p = 0; p < RIPPLE_NUM_PHASES; ++p) {
+    c->ph_ms[p] = 0.0;
+    c->ph_launch[p] = 0;
+    c->ph_bytes[p] = 0.0;
+    c->ph_flops[p] = 0.0;
+  }
+  return RIPPLE_OK;
+}
+
+const char *ripple_phase_name(int32_t phase) {
+  static const char *names[RIPPLE_NUM_PHASES] = {"net", "topo", "layer0", "scatter", "compact", "gemm", "other",
+                                                 "total"};
+  if (phase < 0 || phase >= RIPPLE_NUM_PHASES) return "";
+  return names[phase];
+}
+
+const char *ripple_last_error(const ripple_ctx *c) {
+  if (c == nullptr) return g_load_err.empty() ? kNullCtxMsg : g_load_err.c_str();
+  return c->err.c_str();
+}
+
+void ripple_destroy(ripple_ctx *c) {
+  if (c == nullptr) return;
+  (void)hipSetDevice(c->device);
+  if (c->stream) (void)hipStreamSynchronize(c->stream);
+  for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
+  free_model(c);
+  for (int d = 0; d < 2; ++d) {
+    dfree_t(c, c->adj[d].off);
+    dfree_t(c, c->adj[d].len);
+    dfree_t(c, c->adj[d].cap);
+    dfree_t(c, c->adj[d].col);
+    dfree_t(c, c->adj[d].inscnt);
+    dfree_t(c, c->adj[d].delcnt);
+    dfree_t(c, c->adj[d].fillcnt);
+  }
+  dfree_t(c, c->fop);
+  dfree_t(c, c->ddeg);
+  dfree_t(c, c->bm_out);
+  dfree_t(c, c->bm_x);
+  dfree_t(c, c->blocksum);
+  dfree_t(c, c->d_counters);
+  dfree_t(c, c->d_persist);
+  if (c->h_counters) (void)hipHostFree(c->h_counters);
+  if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);
+  delete c;
+}
+
+}  // extern "C"

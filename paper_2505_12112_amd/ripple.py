@@ -1,0 +1,279 @@
+"""ctypes binding of libripple (the C ABI declared in include/ripple.h).
+
+Argument marshalling only: every step of the incremental propagation runs in the
+HIP library. Arrays are NumPy host arrays; the library copies them during each
+call. If the library is not built, importing this module works but creating a
+context raises ``RippleUnavailable`` (there is no fallback path).
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libripple.so")
+
+MAX_LAYERS = 8
+NUM_PHASES = 8
+
+OK, E_INVALID, E_STATE, E_OOM, E_DEVICE = 0, 1, 2, 3, 4
+AGG = {"sum": 0, "mean": 1, "gcn": 2}
+GEMM = {"fp32": 0, "bf16": 1}
+OP_INSERT, OP_DELETE, OP_FEATURE = 1, 2, 3
+PHASES = ["net", "topo", "layer0", "scatter", "compact", "gemm", "other", "total"]
+
+EXPORTED = [
+    "ripple_load_graph", "ripple_init_embeddings", "ripple_apply_updates", "ripple_get_embeddings",
+    "ripple_get_affected", "ripple_get_aggregates", "ripple_get_arcs", "ripple_device_bytes",
+    "ripple_set_profiling", "ripple_get_phase_stats", "ripple_phase_name", "ripple_last_error",
+    "ripple_destroy",
+]
+
+
+class RippleUnavailable(RuntimeError):
+    pass
+
+
+class RippleError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"[status {status}] {msg}")
+        self.status = status
+
+
+class GraphDesc(C.Structure):
+    _fields_ = [
+        ("num_vertices", C.c_int64), ("num_edges", C.c_int64),
+        ("src", C.POINTER(C.c_int32)), ("dst", C.POINTER(C.c_int32)),
+        ("undirected", C.c_int32), ("slack", C.c_float), ("min_slack", C.c_int32),
+        ("device", C.c_int32), ("stream", C.c_void_p), ("max_device_bytes", C.c_int64),
+    ]
+
+
+class ModelDesc(C.Structure):
+    _fields_ = [
+        ("num_layers", C.c_int32), ("agg", C.c_int32), ("dims", C.POINTER(C.c_int32)),
+        ("w_self", C.POINTER(C.POINTER(C.c_float))), ("w_neigh", C.POINTER(C.POINTER(C.c_float))),
+        ("bias", C.POINTER(C.POINTER(C.c_float))), ("relu", C.POINTER(C.c_int32)),
+        ("gemm_prec", C.c_int32),
+    ]
+
+
+class BatchStats(C.Structure):
+    _fields_ = [
+        ("num_ops", C.c_int64), ("edge_keys", C.c_int64), ("noop_edge_ops", C.c_int64),
+        ("ins_arcs", C.c_int64), ("del_arcs", C.c_int64), ("features", C.c_int64),
+        ("dirty", C.c_int64 * (MAX_LAYERS + 1)), ("affected", C.c_int64 * (MAX_LAYERS + 1)),
+        ("pushed_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("dest_rows", C.c_int64 * (MAX_LAYERS + 1)),
+        ("relocated_rows", C.c_int64), ("repacks", C.c_int64),
+    ]
+
+
+class PhaseStats(C.Structure):
+    _fields_ = [("ms", C.c_double), ("launches", C.c_int64), ("bytes", C.c_double), ("flops", C.c_double)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> C.CDLL:
+    """Loads libripple.so once; raises RippleUnavailable if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RippleUnavailable(f"{path} is not built (run __graft_entry__.build())")
+    lib = C.CDLL(path)
+    P = C.POINTER
+    vp = C.c_void_p
+    lib.ripple_load_graph.argtypes = [P(GraphDesc), P(vp)]
+    lib.ripple_init_embeddings.argtypes = [vp, P(C.c_float), P(ModelDesc)]
+    lib.ripple_apply_updates.argtypes = [vp, P(C.c_int32), C.c_int64, P(C.c_float), C.c_int64, P(BatchStats)]
+    lib.ripple_get_embeddings.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_float)]
+    lib.ripple_get_aggregates.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_float)]
+    lib.ripple_get_affected.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_int64)]
+    lib.ripple_get_arcs.argtypes = [vp, C.c_int32, P(C.c_int32), P(C.c_int32), C.c_int64, P(C.c_int64)]
+    lib.ripple_device_bytes.argtypes = [vp, P(C.c_int64)]
+    lib.ripple_set_profiling.argtypes = [vp, C.c_int32]
+    lib.ripple_get_phase_stats.argtypes = [vp, P(PhaseStats), C.c_int32]
+    lib.ripple_phase_name.argtypes = [C.c_int32]
+    lib.ripple_phase_name.restype = C.c_char_p
+    lib.ripple_last_error.argtypes = [vp]
+    lib.ripple_last_error.restype = C.c_char_p
+    lib.ripple_destroy.argtypes = [vp]
+    lib.ripple_destroy.restype = None
+    _lib = lib
+    return lib
+
+
+def _ptr(a: Optional[np.ndarray], ctype):
+    if a is None:
+        return None
+    return a.ctypes.data_as(C.POINTER(ctype))
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _f32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+class Ripple:
+    """One library context: graph + model state on one GPU."""
+
+    def __init__(self, n: int, src, dst, undirected: bool = False, slack: float = 0.25,
+                 min_slack: int = 4, device: int = 0, stream: Optional[int] = None,
+                 max_device_bytes: int = 0):
+        self._lib = load_library()
+        self._ctx = C.c_void_p()
+        src, dst = _i32(src), _i32(dst)
+        if src.shape != dst.shape:
+            raise ValueError("src and dst differ in length")
+        desc = GraphDesc(int(n), int(src.size), _ptr(src, C.c_int32), _ptr(dst, C.c_int32),
+                         int(bool(undirected)), float(slack), int(min_slack), int(device),
+                         C.c_void_p(stream) if stream else None, int(max_device_bytes))
+        st = self._lib.ripple_load_graph(C.byref(desc), C.byref(self._ctx))
+        if st != OK:
+            raise RippleError(st, self._lib.ripple_last_error(None).decode())
+        self.n = int(n)
+        self.undirected = bool(undirected)
+        self.dims: List[int] = []
+        self.num_layers = 0
+
+    # -- helpers --
+    def _check(self, st: int):
+        if st != OK:
+            raise RippleError(st, self._lib.ripple_last_error(self._ctx).decode())
+
+    def close(self):
+        if getattr(self, "_ctx", None) is not None and self._ctx.value:
+            self._lib.ripple_destroy(self._ctx)
+            self._ctx = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    # -- calls --
+    def init_embeddings(self, x, weights, gemm: str = "fp32"):
+        """weights: object with agg, dims, w_self, w_neigh, bias, relu (synth.ModelWeights)."""
+        x = _f32(x)
+        dims = _i32(weights.dims)
+        L = len(dims) - 1
+        keep = [x, dims]
+        ws = (C.POINTER(C.c_float) * L)()
+        wn = (C.POINTER(C.c_float) * L)()
+        bs = (C.POINTER(C.c_float) * L)()
+        for l in range(L):
+            if weights.w_self[l] is not None:
+                a = _f32(weights.w_self[l])
+                keep.append(a)
+                ws[l] = _ptr(a, C.c_float)
+            a = _f32(weights.w_neigh[l])
+            keep.append(a)
+            wn[l] = _ptr(a, C.c_float)
+            if weights.bias[l] is not None:
+                b = _f32(weights.bias[l])
+                keep.append(b)
+                bs[l] = _ptr(b, C.c_float)
+        relu = _i32([1 if r else 0 for r in weights.relu])
+        keep.append(relu)
+        md = ModelDesc(L, AGG[weights.agg], _ptr(dims, C.c_int32), ws, wn, bs, _ptr(relu, C.c_int32),
+                       GEMM[gemm])
+        self._check(self._lib.ripple_init_embeddings(self._ctx, _ptr(x, C.c_float), C.byref(md)))
+        self.dims = [int(d) for d in dims]
+        self.num_layers = L
+
+    def apply_updates(self, ops, feat_rows=None) -> Dict[str, object]:
+        ops = _i32(ops).reshape(-1, 4)
+        fr = None if feat_rows is None or len(feat_rows) == 0 else _f32(feat_rows)
+        st = BatchStats()
+        self._check(self._lib.ripple_apply_updates(
+            self._ctx, _ptr(ops, C.c_int32), int(ops.shape[0]), _ptr(fr, C.c_float),
+            0 if fr is None else int(fr.shape[0]), C.byref(st)))
+        L = self.num_layers
+        return {
+            "num_ops": st.num_ops, "edge_keys": st.edge_keys, "noop_edge_ops": st.noop_edge_ops,
+            "ins_arcs": st.ins_arcs, "del_arcs": st.del_arcs, "features": st.features,
+            "dirty": list(st.dirty[:L + 1]), "affected": list(st.affected[:L + 1]),
+            "pushed_arcs": list(st.pushed_arcs[:L + 1]), "dest_rows": list(st.dest_rows[:L + 1]),
+            "relocated_rows": st.relocated_rows, "repacks": st.repacks,
+        }
+
+    def apply_updates_raw(self, ops: np.ndarray, feat_rows: Optional[np.ndarray], stats: BatchStats) -> None:
+        """Lowest-overhead form for timing loops: contiguous int32 [B,4] ops and
+        float32 rows prepared by the caller; fills `stats` in place."""
+        self._check(self._lib.ripple_apply_updates(
+            self._ctx, ops.ctypes.data_as(C.POINTER(C.c_int32)), ops.shape[0],
+            None if feat_rows is None else feat_rows.ctypes.data_as(C.POINTER(C.c_float)),
+            0 if feat_rows is None else feat_rows.shape[0], C.byref(stats)))
+
+    def get_embeddings(self, layer: int, ids: Optional[Sequence[int]] = None) -> np.ndarray:
+        d = self.dims[layer]
+        if ids is None:
+            out = np.empty((self.n, d), np.float32)
+            self._check(self._lib.ripple_get_embeddings(self._ctx, layer, None, self.n, _ptr(out, C.c_float)))
+        else:
+            ids = _i32(ids)
+            out = np.empty((ids.size, d), np.float32)
+            self._check(self._lib.ripple_get_embeddings(self._ctx, layer, _ptr(ids, C.c_int32), ids.size,
+                                                        _ptr(out, C.c_float)))
+        return out
+
+    def get_aggregates(self, layer: int, ids: Optional[Sequence[int]] = None) -> np.ndarray:
+        d = self.dims[layer - 1]
+        if ids is None:
+            out = np.empty((self.n, d), np.float32)
+            self._check(self._lib.ripple_get_aggregates(self._ctx, layer, None, self.n, _ptr(out, C.c_float)))
+        else:
+            ids = _i32(ids)
+            out = np.empty((ids.size, d), np.float32)
+            self._check(self._lib.ripple_get_aggregates(self._ctx, layer, _ptr(ids, C.c_int32), ids.size,
+                                                        _ptr(out, C.c_float)))
+        return out
+
+    def get_affected(self, layer: int) -> np.ndarray:
+        cnt = C.c_int64()
+        self._check(self._lib.ripple_get_affected(self._ctx, layer, None, 0, C.byref(cnt)))
+        out = np.empty(cnt.value, np.int32)
+        if cnt.value:
+            self._check(self._lib.ripple_get_affected(self._ctx, layer, _ptr(out, C.c_int32), out.size,
+                                                      C.byref(cnt)))
+        return out
+
+    def get_arcs(self, direction: int = 0):
+        cnt = C.c_int64()
+        self._check(self._lib.ripple_get_arcs(self._ctx, direction, None, None, 0, C.byref(cnt)))
+        s = np.empty(cnt.value, np.int32)
+        d = np.empty(cnt.value, np.int32)
+        if cnt.value:
+            self._check(self._lib.ripple_get_arcs(self._ctx, direction, _ptr(s, C.c_int32), _ptr(d, C.c_int32),
+                                                  s.size, C.byref(cnt)))
+        return s, d
+
+    def device_bytes(self) -> int:
+        b = C.c_int64()
+        self._check(self._lib.ripple_device_bytes(self._ctx, C.byref(b)))
+        return b.value
+
+    def set_profiling(self, enable: bool):
+        self._check(self._lib.ripple_set_profiling(self._ctx, 1 if enable else 0))
+
+    def phase_stats(self) -> Dict[str, Dict[str, float]]:
+        arr = (PhaseStats * NUM_PHASES)()
+        self._check(self._lib.ripple_get_phase_stats(self._ctx, arr, NUM_PHASES))
+        return {PHASES[p]: {"ms": arr[p].ms, "launches": arr[p].launches, "bytes": arr[p].bytes,
+                            "flops": arr[p].flops} for p in range(NUM_PHASES)}
+

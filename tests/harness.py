@@ -1,0 +1,126 @@
+"""Test helpers: run the HIP library and the CPU oracle side by side on the same
+seeded inputs and compare what they produce."""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import ripple_oracle as O
+from paper_2505_12112_amd import synth
+from paper_2505_12112_amd.ripple import Ripple
+
+FP32_TOL = 1e-4   # max row-relative error for the fp32 path
+
+
+class Pair:
+    def __init__(self, n, src, dst, x, weights, undirected=False, **lib_kw):
+        self.lib = Ripple(n, src, dst, undirected=undirected, **lib_kw)
+        self.lib.init_embeddings(x, weights)
+        self.orc = O.OracleState(n, src, dst, x, O.OracleModel.from_weights(weights), undirected)
+        self.L = len(weights.dims) - 1
+        self.n = n
+
+    def close(self):
+        self.lib.close()
+
+    def step(self, batch, check_sets=True, check_stats=True):
+        st = self.lib.apply_updates(batch.ops, batch.feat_rows)
+        net, sets = self.orc.apply(batch.ops, batch.feat_rows)
+        if check_sets:
+            for l in range(self.L + 1):
+                got = self.lib.get_affected(l)
+                np.testing.assert_array_equal(got, sets[l].astype(np.int32), err_msg=f"A^{l}")
+        if check_stats:
+            assert st["ins_arcs"] == net.ins_src.size
+            assert st["del_arcs"] == net.del_src.size
+            assert st["features"] == net.features.size
+            assert st["edge_keys"] == net.edge_keys
+            assert st["noop_edge_ops"] == net.noop_edge_ops
+            for l in range(self.L + 1):
+                assert st["affected"][l] == sets[l].size
+        return st, net, sets
+
+    def embedding_errors(self):
+        ref = self.orc.embeddings()
+        return [O.row_relative_error(self.lib.get_embeddings(l), ref[l]) for l in range(self.L + 1)]
+
+    def check_embeddings(self, tol=FP32_TOL):
+        errs = self.embedding_errors()
+        assert max(errs) <= tol, errs
+        return errs
+
+    def check_arcs(self):
+        want = self.orc.graph.keys
+        for direction in (0, 1):
+            s, d = self.lib.get_arcs(direction)
+            got = np.sort(s.astype(np.int64) * self.n + d)
+            np.testing.assert_array_equal(got, want, err_msg=f"direction {direction}")
+
+    def check_aggregates(self, tol=FP32_TOL):
+        """The library's cached aggregates against their definition on oracle values:
+        S^l_v = sum over in-neighbours u of c_u h^{l-1}_u (c_u = 1, or 1/sqrt(dout+1) for GCN).
+
+        S is a running sum of deltas, so a row whose true value cancels to ~0 keeps
+        rounding residue of the order of the contributions that cancelled; the
+        error of each row is therefore measured against max(|S*_v|_inf, RMS(S*))."""
+        ref = self.orc.embeddings()
+        g = self.orc.graph
+        c = np.ones(self.n)
+        if self.orc.model.agg == "gcn":
+            c = 1.0 / np.sqrt(g.out_degree() + 1.0)
+        u, _ = g.arcs()
+        a = g.in_adjacency(weights=c[u])
+        errs = []
+        for l in range(1, self.L + 1):
+            want = a @ ref[l - 1]
+            got = self.lib.get_aggregates(l).astype(np.float64)
+            rms = float(np.sqrt(np.mean(want * want))) + 1e-30
+            num = np.max(np.abs(got - want), axis=1)
+            den = np.maximum(np.max(np.abs(want), axis=1), rms)
+            r = num / den
+            worst = int(np.argmax(r))
+            errs.append(float(r[worst]))
+            assert r[worst] <= tol, (l, worst, float(num[worst]), float(np.max(np.abs(want[worst]))), rms)
+        return errs
+
+
+def random_valid_batch(rng, orc: O.OracleState, bs: int, d0: int, mix=(1 / 3, 1 / 3, 1 / 3)) -> synth.Batch:
+    """Effective ops against the oracle's current graph: inserts of absent arcs,
+    deletes of present arcs, feature replacements (no two ops on one edge)."""
+    g = orc.graph
+    n = g.n
+    kinds = rng.choice([1, 2, 3], bs, p=np.array(mix) / np.sum(mix))
+    ops = np.full((bs, 4), -1, np.int32)
+    used = set()
+    nfeat = 0
+    keys = g.keys
+    for i, k in enumerate(kinds):
+        ops[i, 0] = k
+        if k == 3:
+            ops[i, 1] = rng.integers(0, n)
+            ops[i, 3] = nfeat
+            nfeat += 1
+            continue
+        placed = False
+        for _ in range(100):
+            if k == 1:
+                u, v = int(rng.integers(0, n)), int(rng.integers(0, n))
+                if u == v:
+                    continue
+            else:
+                if keys.size == 0:
+                    break
+                key = int(keys[rng.integers(0, keys.size)])
+                u, v = key // n, key % n
+            e = (min(u, v), max(u, v)) if g.undirected else (u, v)
+            present = bool(g.has_arcs(np.array([u * n + v]))[0])
+            if e in used or present != (k == 2):
+                continue
+            used.add(e)
+            ops[i, 1], ops[i, 2] = u, v
+            placed = True
+            break
+        if not placed:
+            ops[i] = (3, int(rng.integers(0, n)), -1, nfeat)
+            nfeat += 1
+    feats = rng.standard_normal((nfeat, d0), dtype=np.float32)
+    return synth.Batch(ops, feats)

@@ -1,0 +1,205 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Affected sets must match bit for bit after every batch; embeddings within a
+max row-relative error of 1e-4 (fp32 path); the adjacency must hold exactly the
+oracle's arc set. Inputs are seeded and synthetic."""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import ripple_oracle as O
+from paper_2505_12112_amd import synth
+from paper_2505_12112_amd.ripple import Ripple, RippleError, E_INVALID, E_STATE, E_OOM
+from tests.harness import Pair, random_valid_batch, FP32_TOL
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _small(rng, n, m, dims, agg, undirected=False, bias_std=0.1):
+    src, dst = synth.erdos_renyi(n, m, rng, undirected=undirected)
+    x = rng.standard_normal((n, dims[0])).astype(np.float32)
+    w = synth.model_weights(synth.ModelSpec(agg, tuple(dims)), rng, bias_std=bias_std)
+    return src, dst, x, w
+
+
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
+@pytest.mark.parametrize("dims", [(16, 16, 8), (5, 70, 33, 3), (100, 130, 47)])
+def test_bootstrap_matches_full_recompute(agg, dims):
+    _say("bootstrap", agg, dims)
+    rng = np.random.default_rng(hash((agg, dims)) % 2**32)
+    src, dst, x, w = _small(rng, 700, 4000, dims, agg)
+    p = Pair(700, src, dst, x, w)
+    try:
+        p.check_embeddings()
+        p.check_aggregates()
+        p.check_arcs()
+    finally:
+        p.close()
+
+
+def test_tiny_config_stream():
+    """The tiny workload as specified: 10 batches of 45 inserts, 45 deletes, 10 features."""
+    _say("tiny config")
+    wl = synth.build_workload("tiny")
+    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights)
+    try:
+        for b in range(10):
+            st, net, sets = p.step(wl.stream.next_batch(100))
+            assert st["ins_arcs"] == 45 and st["del_arcs"] == 45 and st["features"] == 10
+            p.check_embeddings()
+        p.check_arcs()
+        p.check_aggregates()
+    finally:
+        p.close()
+
+
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
+@pytest.mark.parametrize("undirected", [False, True])
+def test_adversarial_batches(agg, undirected):
+    """Colliding ops: repeated inserts/deletes of one edge, insert-then-delete,
+    absent deletes, self-loops, repeated feature writes (sequential semantics)."""
+    _say("adversarial", agg, undirected)
+    rng = np.random.default_rng(7 + 3 * ("sum", "mean", "gcn").index(agg) + undirected)
+    dims = (12, 40, 9)
+    src, dst, x, w = _small(rng, 300, 1200, dims, agg, undirected)
+    p = Pair(300, src, dst, x, w, undirected=undirected)
+    try:
+        for b in range(25):
+            a, bb = p.orc.graph.arcs()
+            batch = synth.adversarial_batch(rng, 300, dims[0], bs=int(rng.integers(1, 60)), hot=10,
+                                            existing=(a, bb))
+            p.step(batch)
+        p.check_embeddings()
+        p.check_arcs()
+        p.check_aggregates()
+    finally:
+        p.close()
+
+
+@pytest.mark.parametrize("agg", ["sum", "gcn"])
+def test_no_slack_forces_row_moves_and_relayouts(agg):
+    """slack 0: every insert outgrows its row, so rows move to the spare arena and
+    the arena fills up, which forces full re-layouts."""
+    _say("no slack", agg)
+    rng = np.random.default_rng(11)
+    dims = (8, 16, 4)
+    src, dst, x, w = _small(rng, 200, 600, dims, agg)
+    p = Pair(200, src, dst, x, w, slack=0.0, min_slack=0)
+    try:
+        moved = relayouts = 0
+        for b in range(60):
+            batch = random_valid_batch(rng, p.orc, 120, dims[0], mix=(0.7, 0.2, 0.1))
+            st, _, _ = p.step(batch)
+            moved += st["relocated_rows"]
+            relayouts += st["repacks"]
+        assert moved > 0
+        p.check_arcs()
+        p.check_embeddings()
+        _say("rows moved", moved, "re-layouts", relayouts)
+    finally:
+        p.close()
+
+
+def test_unaffected_rows_stay_bit_identical():
+    _say("unaffected rows")
+    rng = np.random.default_rng(12)
+    dims = (10, 20, 6)
+    src, dst, x, w = _small(rng, 500, 2500, dims, "sum")
+    p = Pair(500, src, dst, x, w)
+    try:
+        for b in range(5):
+            before = [p.lib.get_embeddings(l) for l in range(3)]
+            p.step(random_valid_batch(rng, p.orc, 8, dims[0]))
+            for l in range(3):
+                aff = np.zeros(500, bool)
+                aff[p.lib.get_affected(l)] = True
+                after = p.lib.get_embeddings(l)
+                np.testing.assert_array_equal(after[~aff], before[l][~aff])
+    finally:
+        p.close()
+
+
+def test_empty_and_noop_batches():
+    rng = np.random.default_rng(13)
+    dims = (6, 8, 3)
+    src, dst, x, w = _small(rng, 100, 300, dims, "mean")
+    p = Pair(100, src, dst, x, w)
+    try:
+        st, _, sets = p.step(synth.Batch(np.zeros((0, 4), np.int32), np.zeros((0, 6), np.float32)))
+        assert all(s.size == 0 for s in sets) and st["affected"] == [0, 0, 0]
+        u, v = p.orc.graph.arcs()
+        ops = np.array([[1, u[0], v[0], -1], [2, u[1], u[1], -1], [1, 5, 5, -1]], np.int32)
+        st, _, sets = p.step(synth.Batch(ops, np.zeros((0, 6), np.float32)))
+        assert st["noop_edge_ops"] == 3 and st["affected"] == [0, 0, 0]
+        p.check_embeddings()
+    finally:
+        p.close()
+
+
+def test_invalid_batch_changes_nothing():
+    rng = np.random.default_rng(14)
+    dims = (6, 8, 3)
+    src, dst, x, w = _small(rng, 100, 300, dims, "sum")
+    p = Pair(100, src, dst, x, w)
+    try:
+        before = [p.lib.get_embeddings(l) for l in range(3)]
+        for bad in ([[1, 0, 100, -1]], [[3, 1, -1, 0]], [[9, 1, 2, -1]], [[2, -1, 2, -1]]):
+            with pytest.raises(RippleError) as e:
+                p.lib.apply_updates(np.array(bad, np.int32), None)
+            assert e.value.status == E_INVALID
+        for l in range(3):
+            np.testing.assert_array_equal(p.lib.get_embeddings(l), before[l])
+        p.check_arcs()
+        p.step(random_valid_batch(rng, p.orc, 20, dims[0]))
+        p.check_embeddings()
+    finally:
+        p.close()
+
+
+def test_call_order_and_device_byte_cap():
+    rng = np.random.default_rng(15)
+    src, dst, x, w = _small(rng, 50, 100, (4, 64, 2), "sum")
+    lib = Ripple(50, src, dst)
+    try:
+        with pytest.raises(RippleError) as e:
+            lib.apply_updates(np.array([[3, 1, -1, 0]], np.int32), np.zeros((1, 4), np.float32))
+        assert e.value.status == E_STATE
+        load_bytes = lib.device_bytes()
+    finally:
+        lib.close()
+    with pytest.raises(RippleError) as e:
+        Ripple(50, src, dst, max_device_bytes=1000)
+    assert e.value.status == E_OOM
+    lib = Ripple(50, src, dst, max_device_bytes=load_bytes + 1000)
+    try:
+        with pytest.raises(RippleError) as e:
+            lib.init_embeddings(x, w)
+        assert e.value.status == E_OOM
+    finally:
+        lib.close()
+
+
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
+def test_thousand_batches_on_a_small_graph(agg):
+    """1000 consecutive batches: sets every batch, embeddings every 100 and at the end."""
+    _say("1000 batches", agg)
+    rng = np.random.default_rng(16 + ("sum", "mean", "gcn").index(agg))
+    dims = (16, 32, 8)
+    src, dst, x, w = _small(rng, 400, 2400, dims, agg)
+    p = Pair(400, src, dst, x, w)
+    try:
+        worst = 0.0
+        for b in range(1000):
+            p.step(random_valid_batch(rng, p.orc, 20, dims[0]))
+            if (b + 1) % 100 == 0:
+                worst = max(worst, max(p.check_embeddings()))
+                _say(f"  batch {b + 1}: worst row-relative error so far {worst:.2e}")
+        p.check_arcs()
+        p.check_aggregates()
+    finally:
+        p.close()
