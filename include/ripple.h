@@ -184,11 +184,13 @@ RIPPLE_API ripple_status ripple_get_arcs(ripple_ctx *ctx, int32_t direction, int
 /* Device bytes the context holds. */
 RIPPLE_API ripple_status ripple_device_bytes(ripple_ctx *ctx, int64_t *bytes);
 
-/* Kernel timing (for measurement). With enable = 1, every later
- * ripple_apply_updates records HIP events around each kernel phase on the
- * context's stream and accumulates per phase: event milliseconds, kernel launches,
- * and the phase's algorithmic HBM bytes and flops computed from the batch's own
- * counts (each input row read once, each output row written once):
+/* Kernel timing (for measurement). ripple_set_profiling(ctx, mask) makes every
+ * later ripple_apply_updates record a HIP event pair on the context's stream
+ * around each kernel phase p whose bit (1 << p) is set in mask (bit
+ * RIPPLE_PHASE_TOTAL: first to last kernel of the batch); mask 0 stops recording.
+ * Per phase the library accumulates event milliseconds, kernel launches, and the
+ * phase's algorithmic HBM bytes and flops computed from the batch's own counts
+ * (each input row read once, each output row written once):
  *   SCATTER, per layer l with dirty set D, pushed arcs E_D, distinct sinks R,
  *            width d = d_{l-1}:  4 E_D + 8 |D| + 4 d |D| + 8 d R  bytes
  *   GEMM,    per layer l with |A^l| rows, K = 2 d_{l-1} (SAGE) or d_{l-1} (GCN),
@@ -196,9 +198,8 @@ RIPPLE_API ripple_status ripple_device_bytes(ripple_ctx *ctx, int64_t *bytes);
  *            + 4 |A^l| N (2 if the layer is the last, else 3: old row, new row, delta)
  *   COMPACT, per compaction over n vertices with W = ceil(n/32) bitmap words and
  *            c ids out:  24 W + 4 c bytes
- * Other phases report bytes = flops = 0. enable = 0 stops recording.
- * ripple_get_phase_stats copies min(capacity, RIPPLE_NUM_PHASES) entries and
- * resets the sums. */
+ * Other phases report bytes = flops = 0. ripple_get_phase_stats copies
+ * min(capacity, RIPPLE_NUM_PHASES) entries and resets the sums. */
 #define RIPPLE_NUM_PHASES 8
 enum {
   RIPPLE_PHASE_NET = 0,      /* op netting (hash + membership) */
@@ -216,7 +217,7 @@ typedef struct {
   double bytes;
   double flops;
 } ripple_phase_stats;
-RIPPLE_API ripple_status ripple_set_profiling(ripple_ctx *ctx, int32_t enable);
+RIPPLE_API ripple_status ripple_set_profiling(ripple_ctx *ctx, int32_t mask);
 RIPPLE_API ripple_status ripple_get_phase_stats(ripple_ctx *ctx, ripple_phase_stats *out, int32_t capacity);
 RIPPLE_API const char *ripple_phase_name(int32_t phase);
 

@@ -36,6 +36,7 @@ struct Counters {
   u64 n_reloc;            // rows to move to the arena
   u64 arena_need[2];      // arena slots those moves need, per direction
   u64 err;                // device-detected inconsistency (bit 0: deleted arc not found)
+  u64 plan_done;          // blocks of the plan kernel that finished (last one checks the arena)
   u64 count[kMaxL + 1];   // [0] = |dirty set of layer 1|, [l] = |A^l|
   u64 pushed[kMaxL + 1];  // [l] = out-arcs pushed at layer l
   u64 dest[kMaxL + 1];    // [l] = distinct sinks of those arcs
@@ -53,14 +54,6 @@ struct Adj {
   int *col;
   int *inscnt;            // per-row scratch, zero between batches
   int *delcnt;
-  int *fillcnt;
-};
-
-struct RelocItem {
-  int row;
-  int dir;
-  int newcap;
-  int pad;
 };
 
 struct LayerPtrs {
@@ -74,50 +67,60 @@ enum Agg { kSum = 0, kMean = 1, kGcn = 2 };
 
 // --- launchers (each defined in the translation unit that holds its kernel) ---
 
-// netting
-void launch_net_hash(hipStream_t s, const ripple_op *ops, int B, int undirected, long long n,
+// netting: after these, the net arcs are listed and every (arc, direction) item
+// knows its rank among the row's inserts (ins_rank) or deletes (del_rank); the
+// hash slot of every named edge holds +1 (net insert), -1 (net delete) or 0.
+// host_ops: the batch in pinned host memory; copied to ops (device) on the way.
+void launch_net_hash(hipStream_t s, const ripple_op *host_ops, ripple_op *ops, int B, int undirected, long long n,
                      u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop, Counters *c);
 void launch_net_decide(hipStream_t s, const ripple_op *ops, int B, int undirected, const int *ht_val,
-                       const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src, int *ins_dst,
-                       int *del_src, int *del_dst, int *flist, Counters *c);
+                       int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src,
+                       int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank, int *flist,
+                       Counters *c);
 
-// topology (cap_arcs bounds n_ins and n_del)
-void launch_topo_count(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                       const int *del_src, const int *del_dst, int *ins_rank, int *del_rank, Counters *c);
+// topology (cap_arcs bounds n_ins and n_del): plan row moves and check the arena
+// (aborting before any mutation), then one owner wave per touched row removes its
+// deleted entries, moves the row if it must grow, and sets its new length; then
+// the inserts are written at their ranks.
 void launch_topo_plan(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                      const int *ins_rank, RelocItem *reloc, Counters *c);
-void launch_topo_check(hipStream_t s, Counters *c, const Persist *p, long long cap_out, long long cap_in);
-void launch_corrections(hipStream_t s, int cap_arcs, int agg, LayerPtrs lp, const int *out_len,
-                        const int *ins_src, const int *ins_dst, const int *del_src, const int *del_dst,
-                        Counters *c);
-void launch_del_apply(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *del_src, const int *del_dst,
-                      const int *del_rank, int *del_pos, int *ddeg, Counters *c);
-void launch_reloc(hipStream_t s, int cap_reloc, Adj out, Adj in, const RelocItem *reloc, Persist *p,
-                  Counters *c);
-void launch_ins_apply(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                      const int *ins_rank, int *ddeg, Counters *c);
+                      const int *ins_rank, Counters *c, const Persist *p, long long cap_out, long long cap_in);
+void launch_topo_rewrite(hipStream_t s, int cap_arcs, int undirected, long long n, Adj out, Adj in,
+                         const int *ins_src, const int *ins_dst, const int *del_src, const int *del_dst,
+                         const int *ins_rank, const int *del_rank, const u64 *ht_key, const int *ht_net,
+                         unsigned mask, Persist *p, int *ddeg, Counters *c);
+void launch_topo_put(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
+                     const int *ins_rank, Counters *c);
+// Also copies *c to host (pinned) and zeroes *next (the other counter buffer).
 void launch_cleanup(hipStream_t s, int B, int cap_arcs, const ripple_op *ops, const int *op_slot,
-                    u64 *ht_key, int *ht_val, int *fop, Adj out, Adj in, const int *ins_src,
+                    u64 *ht_key, int *ht_val, int *ht_net, int *fop, Adj out, Adj in, const int *ins_src,
                     const int *ins_dst, const int *del_src, const int *del_dst, int *ddeg,
-                    const Counters *c);
+                    const Counters *c, Counters *next, Counters *host);
 
-// frontier
-void launch_mark_dirty0(hipStream_t s, int cap_feat, int cap_arcs, int gcn, const int *flist,
-                        const int *ins_src, const int *del_src, const int *ddeg, unsigned *bm, Counters *c);
+// frontier. Pre-batch corrections of every layer's aggregate (an inserted arc
+// (u,v) adds u's pre-batch contribution to S^l_v, a deleted one removes it) run
+// after the adjacency update, with pre-batch coefficients recovered from ddeg;
+// the same kernel marks the layer-1 dirty set (feature writes; GCN: vertices whose
+// out-degree changed).
+void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerPtrs lp, const int *out_len,
+                      const int *ddeg, const int *flist, const int *ins_src, const int *ins_dst,
+                      const int *del_src, const int *del_dst, unsigned *bm, Counters *c);
 int compact_blocks(long long n);
+// bitmaps (a | b) -> ascending list, count, and, when deg != nullptr, doff[j] =
+// sum of deg over list[0..j) with doff[count] = total; both bitmaps are cleared.
 void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, int *blocksum,
-                    int *list_out, u64 *count_out);
+                    long long *blockdeg, const int *deg, int *list_out, long long *doff, u64 *count_out);
 
-// layer 0 deltas
+// layer 0 deltas (feat may be pinned host memory)
 void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list, const u64 *count,
                    const ripple_op *ops, const float *feat, const int *fop, float *X, const int *out_len,
                    const int *ddeg, float *delta, const Counters *c);
 
-// scatter: S^l[v] += delta[j] for every post-batch out-arc (list[j] -> v); marks sinks
-// in bm_out, the dirty vertices and the sinks of net arcs in bm_x.
-void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u64 *count, const float *delta,
-                    Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
-                    const int *del_dst, int cap_arcs, u64 *pushed, u64 *dest, const Counters *c);
+// scatter: S^l[v] += delta[j] for every post-batch out-arc (list[j] -> v), 64 arcs
+// per wave step (doff gives each listed vertex's first arc); marks the sinks in
+// bm_out, and the listed vertices and the sinks of net arcs in bm_x.
+void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *doff,
+                    const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
+                    const int *del_dst, u64 *pushed, u64 *dest, const Counters *c);
 
 // bootstrap pull: S[v] = sum over in-arcs c_u H[u]
 void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev, Adj in, const int *out_len,
@@ -148,7 +151,8 @@ struct GemmArgs {
   int agg;
   const u64 *abort;
 };
-void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows);
+// expected_rows picks the tile height (large tiles when many rows are expected).
+void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows, long long expected_rows);
 
 // re-layout of one adjacency direction
 void launch_repack_copy(hipStream_t s, long long n, const int *old_col, const long long *old_off, const int *len,

@@ -6,7 +6,9 @@
 // receiver adds it to its mailbox), and the affected set
 //   A^l = out(D^l) u sinks(net arcs) u D^l
 // is collected in two bitmaps (one for the out-arc sinks, so that their distinct
-// count is known exactly) and compacted into a sorted list by a popcount prefix sum.
+// count is known exactly) and compacted into a sorted list by a popcount prefix
+// sum, which also yields each listed vertex's first out-arc index for the next
+// layer's scatter.
 #include "internal.h"
 
 namespace rp {
@@ -14,6 +16,7 @@ namespace rp {
 namespace {
 
 constexpr int kCompactThreads = 256;
+constexpr int kCompactWaves = kCompactThreads / kWave;
 constexpr int kWordsPerThread = 4;
 constexpr int kWordsPerBlock = kCompactThreads * kWordsPerThread;
 
@@ -39,15 +42,65 @@ inline int blocks_for(long long items, int threads, int cap = 4096) {
   return static_cast<int>(b);
 }
 
-// Dirty set of layer 1: vertices with a feature write, and under GCN every vertex
-// whose out-degree changed (its coefficient 1/sqrt(dout+1) scales all it sends).
-__global__ void k_mark_dirty0(int gcn, const int *flist, const int *ins_src, const int *del_src,
-                              const int *ddeg, unsigned *bm, Counters *c) {
+// Exclusive scan of v over the block; *total receives the block sum.
+template <typename T>
+__device__ inline T block_exclusive_scan(T v, T *lds, T *total) {
+  const int lane = lane_id(), wave = threadIdx.x / kWave;
+  T x = v;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const T y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == kWave - 1) lds[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    T run = 0;
+    for (int w = 0; w < kCompactWaves; ++w) {
+      const T t = lds[w];
+      lds[w] = run;
+      run += t;
+    }
+    lds[kCompactWaves] = run;
+  }
+  __syncthreads();
+  const T excl = x - v + lds[wave];
+  *total = lds[kCompactWaves];
+  __syncthreads();
+  return excl;
+}
+
+template <typename T>
+__device__ inline T block_sum(T v, T *lds) {
+  T total;
+  block_exclusive_scan(v, lds, &total);
+  return total;
+}
+
+// Pre-batch corrections and the layer-1 dirty marks (see launch_corr_mark).
+__global__ void k_corr_mark(int agg, LayerPtrs lp, const int *out_len, const int *ddeg, const int *flist,
+                            const int *ins_src, const int *ins_dst, const int *del_src, const int *del_dst,
+                            unsigned *bm, Counters *c) {
   if (c->abort) return;
+  const int lane = lane_id();
   const long long nf = static_cast<long long>(c->n_feat);
   const long long ni = static_cast<long long>(c->n_ins);
-  const long long nd = static_cast<long long>(c->n_del);
-  const long long total = nf + (gcn ? ni + nd : 0);
+  const long long na = ni + static_cast<long long>(c->n_del);
+  const long long items = na * lp.L;
+  for (long long it = global_wave(); it < items; it += num_waves()) {
+    const long long arc = it / lp.L;
+    const int l = static_cast<int>(it % lp.L) + 1;
+    const bool ins = arc < ni;
+    const int u = ins ? ins_src[arc] : del_src[arc - ni];
+    const int v = ins ? ins_dst[arc] : del_dst[arc - ni];
+    float coef = ins ? 1.0f : -1.0f;
+    if (agg == kGcn) coef *= 1.0f / sqrtf(static_cast<float>(out_len[u] - ddeg[u]) + 1.0f);
+    const int d = lp.dims[l - 1];
+    const float *hu = lp.H[l - 1] + static_cast<long long>(u) * d;
+    float *sv = lp.S[l] + static_cast<long long>(v) * d;
+    for (int k = lane; k < d; k += kWave) unsafeAtomicAdd(&sv[k], coef * hu[k]);
+  }
+  const long long total = nf + (agg == kGcn ? na : 0);
   const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
   for (long long i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
     if (i < nf) {
@@ -60,71 +113,75 @@ __global__ void k_mark_dirty0(int gcn, const int *flist, const int *ins_src, con
   }
 }
 
-__device__ inline int block_reduce_sum(int v, int *red) {
-  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_down(v, o);
-  const int w = threadIdx.x / kWave;
-  if (lane_id() == 0) red[w] = v;
-  __syncthreads();
-  int t = 0;
-  if (threadIdx.x == 0) {
-    for (int i = 0; i < kCompactThreads / kWave; ++i) t += red[i];
-    red[kCompactThreads / kWave] = t;
+__device__ inline void word_stats(unsigned w, long long vbase, const int *deg, int &cnt, long long &dsum) {
+  cnt += __popc(w);
+  if (deg != nullptr) {
+    while (w) {
+      const int b = __ffs(w) - 1;
+      dsum += deg[vbase + b];
+      w &= w - 1;
+    }
   }
-  __syncthreads();
-  t = red[kCompactThreads / kWave];
-  __syncthreads();
-  return t;
 }
 
 __global__ __launch_bounds__(kCompactThreads) void k_compact_count(const unsigned *bm_a, const unsigned *bm_b,
-                                                                   long long words, int *blocksum) {
-  __shared__ int red[kCompactThreads / kWave + 1];
+                                                                   long long words, const int *deg,
+                                                                   int *blocksum, long long *blockdeg) {
+  __shared__ long long red[kCompactWaves + 1];
   const long long w0 = static_cast<long long>(blockIdx.x) * kWordsPerBlock + threadIdx.x * kWordsPerThread;
   int cnt = 0;
+  long long dsum = 0;
 #pragma unroll
   for (int i = 0; i < kWordsPerThread; ++i) {
     const long long w = w0 + i;
-    if (w < words) cnt += __popc(bm_a[w] | bm_b[w]);
+    if (w < words) word_stats(bm_a[w] | bm_b[w], w * 32, deg, cnt, dsum);
   }
-  const int t = block_reduce_sum(cnt, red);
-  if (threadIdx.x == 0) blocksum[blockIdx.x] = t;
+  const long long tc = block_sum<long long>(cnt, red);
+  const long long td = block_sum<long long>(dsum, red);
+  if (threadIdx.x == 0) {
+    blocksum[blockIdx.x] = static_cast<int>(tc);
+    blockdeg[blockIdx.x] = td;
+  }
 }
 
-__global__ __launch_bounds__(kCompactThreads) void k_compact_emit(unsigned *bm_a, unsigned *bm_b,
-                                                                  long long words, const int *blocksum,
-                                                                  int *list_out, u64 *count_out) {
-  __shared__ int red[kCompactThreads / kWave + 1];
-  __shared__ int scan[kCompactThreads];
-  // exclusive prefix of earlier blocks
-  int pre = 0;
-  for (int b = threadIdx.x; b < static_cast<int>(blockIdx.x); b += kCompactThreads) pre += blocksum[b];
-  const int base = block_reduce_sum(pre, red);
+__global__ __launch_bounds__(kCompactThreads) void k_compact_emit(unsigned *bm_a, unsigned *bm_b, long long words,
+                                                                  const int *deg, const int *blocksum,
+                                                                  const long long *blockdeg, int *list_out,
+                                                                  long long *doff, u64 *count_out) {
+  __shared__ long long red[kCompactWaves + 1];
+  long long pre = 0, pred = 0;
+  for (int b = threadIdx.x; b < static_cast<int>(blockIdx.x); b += kCompactThreads) {
+    pre += blocksum[b];
+    if (deg != nullptr) pred += blockdeg[b];
+  }
+  const long long base = block_sum<long long>(pre, red);
+  const long long dbase = block_sum<long long>(pred, red);
   const long long w0 = static_cast<long long>(blockIdx.x) * kWordsPerBlock + threadIdx.x * kWordsPerThread;
   unsigned wv[kWordsPerThread];
   int cnt = 0;
+  long long dsum = 0;
 #pragma unroll
   for (int i = 0; i < kWordsPerThread; ++i) {
     const long long w = w0 + i;
     wv[i] = w < words ? (bm_a[w] | bm_b[w]) : 0u;
-    cnt += __popc(wv[i]);
+    word_stats(wv[i], w * 32, deg, cnt, dsum);
   }
-  // block exclusive scan of cnt (Hillis-Steele in LDS)
-  scan[threadIdx.x] = cnt;
-  __syncthreads();
-  for (int o = 1; o < kCompactThreads; o <<= 1) {
-    const int v = threadIdx.x >= o ? scan[threadIdx.x - o] : 0;
-    __syncthreads();
-    scan[threadIdx.x] += v;
-    __syncthreads();
-  }
-  int pos = base + scan[threadIdx.x] - cnt;
+  long long tot_c, tot_d;
+  long long pos = base + block_exclusive_scan<long long>(cnt, red, &tot_c);
+  long long dpos = dbase + block_exclusive_scan<long long>(dsum, red, &tot_d);
 #pragma unroll
   for (int i = 0; i < kWordsPerThread; ++i) {
     unsigned m = wv[i];
     const long long vbase = (w0 + i) * 32;
     while (m) {
       const int b = __ffs(m) - 1;
-      list_out[pos++] = static_cast<int>(vbase + b);
+      const int v = static_cast<int>(vbase + b);
+      list_out[pos] = v;
+      if (deg != nullptr) {
+        doff[pos] = dpos;
+        dpos += deg[v];
+      }
+      ++pos;
       m &= m - 1;
     }
     const long long w = w0 + i;
@@ -133,8 +190,9 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact_emit(unsigned *bm_a
       bm_b[w] = 0u;
     }
   }
-  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == kCompactThreads - 1) {
-    *count_out = static_cast<u64>(base + scan[threadIdx.x]);
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
+    *count_out = static_cast<u64>(base + tot_c);
+    if (deg != nullptr) doff[base + tot_c] = dbase + tot_d;
   }
 }
 
@@ -167,60 +225,120 @@ __global__ void k_delta0(int agg, int d0, const int *list, const u64 *count, con
   }
 }
 
-// One wave per dirty vertex: its delta row sits in registers (NC floats per lane),
-// its out-row is read 64 ids at a time, and each id's row of S gets one coalesced
-// row of fp32 atomic adds.
-template <int NC>
-__global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u64 *count, const float *delta,
-                                                 Adj out, float *S, unsigned *bm_out, unsigned *bm_x,
-                                                 const int *ins_dst, const int *del_dst, u64 *pushed,
-                                                 u64 *dest, const Counters *c) {
+// First index i in [lo, hi) with a[i] > x (hi if none).
+__device__ inline long long upper_bound(const long long *a, long long lo, long long hi, long long x) {
+  while (lo < hi) {
+    const long long mid = (lo + hi) >> 1;
+    if (a[mid] <= x) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Last index j in [lo, hi) with a[j] <= x, for non-decreasing a with a[lo] <= x.
+// The whole wave searches together: each round probes 64 evenly spaced entries
+// with one load and keeps the gap after the last probe that is <= x, so a search
+// over m entries takes ceil(log64 m) dependent loads instead of log2 m.
+__device__ inline long long wave_last_le(const long long *a, long long lo, long long hi, long long x) {
+  const int lane = lane_id();
+  while (hi - lo > kWave) {
+    const long long step = (hi - lo + kWave - 1) / kWave;
+    const long long idx = lo + lane * step;
+    const bool le = idx < hi && a[idx] <= x;
+    const int last = __popcll(__ballot(le)) - 1;  // probes <= x form a prefix
+    lo = lo + last * step;
+    hi = lo + step < hi ? lo + step : hi;
+  }
+  const long long idx = lo + lane;
+  const bool le = idx < hi && a[idx] <= x;
+  return lo + __popcll(__ballot(le)) - 1;
+}
+
+// Edge-parallel scatter. Pushed arcs are numbered: arc e of listed vertex j has
+// index doff[j] + its position in j's out-row. A wave takes a chunk of C
+// consecutive arcs (C = 1 when there are few arcs, so that many waves run at
+// once; up to 64 when there are many), each lane resolves one arc's source slot
+// and sink and marks the sink, then G lanes per arc add the source's delta row
+// into the sink's row of S with fp32 atomics (coalesced across the G lanes). The
+// delta row stays in registers while consecutive arcs share a source, so a hub's
+// arcs cost one row load per chunk; hubs spread over many waves.
+template <int G, int NC>
+__global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u64 *count, const long long *doff,
+                                                 const float *delta, Adj out, float *S, unsigned *bm_out,
+                                                 unsigned *bm_x, const int *ins_dst, const int *del_dst,
+                                                 u64 *pushed, u64 *dest, const Counters *c) {
   if (c->abort) return;
   const int lane = lane_id();
-  // sinks of net arcs are affected at every layer
+  const long long nD = static_cast<long long>(*count);
+  const long long E = doff[nD];
   {
     const long long ni = static_cast<long long>(c->n_ins);
     const long long na = ni + static_cast<long long>(c->n_del);
     const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
-    for (long long i = blockIdx.x * blockDim.x + threadIdx.x; i < na; i += stride)
-      mark(bm_x, i < ni ? ins_dst[i] : del_dst[i - ni]);
+    const long long t0 = blockIdx.x * blockDim.x + threadIdx.x;
+    for (long long i = t0; i < na; i += stride) mark(bm_x, i < ni ? ins_dst[i] : del_dst[i - ni]);
+    for (long long j = t0; j < nD; j += stride) mark(bm_x, list[j]);
+    if (t0 == 0) *pushed = static_cast<u64>(E);
   }
-  const long long m = static_cast<long long>(*count);
-  u64 my_pushed = 0, my_dest = 0;
-  for (long long j = global_wave(); j < m; j += num_waves()) {
-    const int u = list[j];
-    if (lane == 0) mark(bm_x, u);
-    float dreg[NC];
-    const float *dj = delta + j * d;
-#pragma unroll
-    for (int q = 0; q < NC; ++q) {
-      const int k = lane + q * kWave;
-      dreg[q] = k < d ? dj[k] : 0.0f;
+  const long long waves = num_waves();
+  int C = 1;
+  while (C < kWave && static_cast<long long>(C) * waves < E) C <<= 1;
+  constexpr int kEdgesPerStep = kWave / G;
+  const int grp = lane / G, k0 = lane % G;
+  u64 my_dest = 0;
+  int cached = -1;
+  float dreg[NC];
+  const long long chunks = (E + C - 1) / C;
+  for (long long ch = global_wave(); ch < chunks; ch += waves) {
+    const long long e0 = ch * C;
+    const long long elast = e0 + C - 1 < E - 1 ? e0 + C - 1 : E - 1;
+    const long long ja = wave_last_le(doff, 0, nD + 1, e0);
+    const long long jb = C == 1 ? ja : wave_last_le(doff, ja, nD + 1, elast);
+    const long long e = e0 + lane;
+    const bool active = e <= elast;
+    int j = static_cast<int>(ja);
+    if (jb > ja) {
+      if (jb - ja < kWave) {
+        // the window's offsets, one per lane; every lane takes part in the shuffles
+        const long long mine = ja + lane <= jb ? doff[ja + lane] : (1LL << 62);
+        int cnt_le = 0;
+        for (int t = 0; t <= static_cast<int>(jb - ja); ++t) cnt_le += __shfl(mine, t) <= e ? 1 : 0;
+        j = static_cast<int>(ja) + cnt_le - 1;
+      } else if (active) {
+        j = static_cast<int>(upper_bound(doff, ja, jb + 1, e) - 1);
+      }
     }
-    const int deg = out.len[u];
-    const int *row = out.col + out.off[u];
-    my_pushed += deg;
-    for (int e0 = 0; e0 < deg; e0 += kWave) {
-      const int e = e0 + lane;
-      const int cidx = e < deg ? row[e] : -1;
-      const bool fresh = cidx >= 0 && mark(bm_out, cidx);
-      my_dest += __popcll(__ballot(fresh));
-      const int cnt = deg - e0 < kWave ? deg - e0 : kWave;
-      for (int i = 0; i < cnt; ++i) {
-        const int v = __shfl(cidx, i);
-        float *sv = S + static_cast<long long>(v) * d;
+    int v = -1;
+    if (active) {
+      const int u = list[j];
+      v = out.col[out.off[u] + (e - doff[j])];
+    }
+    const bool fresh = v >= 0 && mark(bm_out, v);
+    my_dest += __popcll(__ballot(fresh));
+    const int cnt = static_cast<int>(elast - e0 + 1);
+    for (int i = 0; i < cnt; i += kEdgesPerStep) {
+      const int vv = __shfl(v, i + grp);
+      const int jj = __shfl(j, i + grp);
+      if (vv >= 0) {
+        if (jj != cached) {
+          const float *dj = delta + static_cast<long long>(jj) * d;
+#pragma unroll
+          for (int q = 0; q < NC; ++q) {
+            const int k = k0 + q * G;
+            dreg[q] = k < d ? dj[k] : 0.0f;
+          }
+          cached = jj;
+        }
+        float *sv = S + static_cast<long long>(vv) * d;
 #pragma unroll
         for (int q = 0; q < NC; ++q) {
-          const int k = lane + q * kWave;
+          const int k = k0 + q * G;
           if (k < d) unsafeAtomicAdd(&sv[k], dreg[q]);
         }
       }
     }
   }
-  if (lane == 0 && (my_pushed | my_dest)) {
-    atomicAdd(pushed, my_pushed);
-    atomicAdd(dest, my_dest);
-  }
+  if (lane == 0 && my_dest) atomicAdd(dest, my_dest);
 }
 
 // Bootstrap: S[v] = sum over in-arcs (u -> v) of c_u H[u], one wave per vertex,
@@ -283,10 +401,14 @@ __global__ void k_gather_rows(const float *src, int d, const int *ids, long long
 
 }  // namespace
 
-void launch_mark_dirty0(hipStream_t s, int cap_feat, int cap_arcs, int gcn, const int *flist,
-                        const int *ins_src, const int *del_src, const int *ddeg, unsigned *bm, Counters *c) {
-  hipLaunchKernelGGL(k_mark_dirty0, dim3(blocks_for(static_cast<long long>(cap_feat) + 2LL * cap_arcs, 256)),
-                     dim3(256), 0, s, gcn, flist, ins_src, del_src, ddeg, bm, c);
+void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerPtrs lp, const int *out_len,
+                      const int *ddeg, const int *flist, const int *ins_src, const int *ins_dst, const int *del_src,
+                      const int *del_dst, unsigned *bm, Counters *c) {
+  const long long waves = 2LL * cap_arcs * lp.L;
+  const long long threads = static_cast<long long>(cap_feat) + 2LL * cap_arcs;
+  const long long items = waves * kWave > threads ? waves * kWave : threads;
+  hipLaunchKernelGGL(k_corr_mark, dim3(blocks_for(items, 256)), dim3(256), 0, s, agg, lp, out_len, ddeg, flist,
+                     ins_src, ins_dst, del_src, del_dst, bm, c);
 }
 
 int compact_blocks(long long n) {
@@ -294,13 +416,14 @@ int compact_blocks(long long n) {
   return static_cast<int>((words + kWordsPerBlock - 1) / kWordsPerBlock);
 }
 
-void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, int *blocksum, int *list_out,
-                    u64 *count_out) {
+void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, int *blocksum, long long *blockdeg,
+                    const int *deg, int *list_out, long long *doff, u64 *count_out) {
   const long long words = (n + 31) / 32;
   const int nb = compact_blocks(n);
-  hipLaunchKernelGGL(k_compact_count, dim3(nb), dim3(kCompactThreads), 0, s, bm_a, bm_b, words, blocksum);
-  hipLaunchKernelGGL(k_compact_emit, dim3(nb), dim3(kCompactThreads), 0, s, bm_a, bm_b, words, blocksum,
-                     list_out, count_out);
+  hipLaunchKernelGGL(k_compact_count, dim3(nb), dim3(kCompactThreads), 0, s, bm_a, bm_b, words, deg, blocksum,
+                     blockdeg);
+  hipLaunchKernelGGL(k_compact_emit, dim3(nb), dim3(kCompactThreads), 0, s, bm_a, bm_b, words, deg, blocksum,
+                     blockdeg, list_out, doff, count_out);
 }
 
 void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list, const u64 *count,
@@ -310,19 +433,20 @@ void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list,
                      ops, feat, fop, X, out_len, ddeg, delta, c);
 }
 
-void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u64 *count, const float *delta,
-                    Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst, const int *del_dst,
-                    int cap_arcs, u64 *pushed, u64 *dest, const Counters *c) {
-  const int blocks = blocks_for(n * kWave, 256, 2048);
-  const int nc = (d + kWave - 1) / kWave;
-#define RP_SCATTER(NCV)                                                                                  \
-  hipLaunchKernelGGL(k_scatter<NCV>, dim3(blocks), dim3(256), 0, s, d, list, count, delta, out, S, bm_out, \
-                     bm_x, ins_dst, del_dst, pushed, dest, c)
-  if (nc <= 1) RP_SCATTER(1);
-  else if (nc == 2) RP_SCATTER(2);
-  else if (nc <= 4) RP_SCATTER(4);
-  else if (nc <= 8) RP_SCATTER(8);
-  else RP_SCATTER(16);
+void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *doff,
+                    const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
+                    const int *del_dst, u64 *pushed, u64 *dest, const Counters *c) {
+  const int blocks = 2048;
+#define RP_SCATTER(GV, NCV)                                                                                     \
+  hipLaunchKernelGGL((k_scatter<GV, NCV>), dim3(blocks), dim3(256), 0, s, d, list, count, doff, delta, out, S, \
+                     bm_out, bm_x, ins_dst, del_dst, pushed, dest, c)
+  if (d <= 16) RP_SCATTER(16, 1);
+  else if (d <= 32) RP_SCATTER(32, 1);
+  else if (d <= 64) RP_SCATTER(64, 1);
+  else if (d <= 128) RP_SCATTER(64, 2);
+  else if (d <= 256) RP_SCATTER(64, 4);
+  else if (d <= 512) RP_SCATTER(64, 8);
+  else RP_SCATTER(64, 16);
 #undef RP_SCATTER
 }
 

@@ -1,13 +1,16 @@
 // Layer transform on the affected rows: Y = act(Z W^T + b) with fp32 MFMA
-// (v_mfma_f32_16x16x4_f32), where Z is gathered on the fly from the cached
-// aggregate and the previous layer's embeddings (Eq. (2): Update^l then sigma).
+// (v_mfma_f32_16x16x4_f32), where each row of Z is gathered on the fly from the
+// cached aggregate and the previous layer's embeddings (Eq. (2): Update^l then
+// sigma). SAGE: z_v = [h_v || t_v S_v]; GCN: z_v = t_v (S_v + s_v h_v).
 //
-// Block tile 64 x 64 over (rows of the affected list) x (output columns), K in
-// steps of 16 staged through LDS; four waves each own a 32 x 32 quarter as 2 x 2
-// MFMA tiles. The epilogue adds the bias, applies ReLU, forms the next layer's
-// delta row (new minus old contribution) and overwrites the embedding row.
-// Tiles are visited by a grid-stride loop so that the row count can stay on the
-// device.
+// A block of four waves owns a BM x BN output tile and walks K in steps of 32:
+// the next step's A (gathered rows) and B (weight rows) are loaded into registers
+// as float4 while the current step's MFMAs run from LDS, then stored into the
+// other half of a double buffer, so there is one barrier per K step. Tiles are
+// visited by a grid-stride loop so the row count can stay on the device. BN
+// follows the layer width (16, 32, 48, 64, 128) and BM the expected row count.
+// The epilogue adds the bias, applies ReLU, forms the next layer's delta row
+// (c'_v y - c_v h_old) and overwrites the embedding row.
 #include "internal.h"
 
 namespace rp {
@@ -16,44 +19,104 @@ namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int kBM = 64;
-constexpr int kBN = 64;
-constexpr int kBK = 16;
+constexpr int kBK = 32;
+constexpr int kLdk = kBK + 4;  // LDS row stride (floats)
 constexpr int kThreads = 256;
 
-template <int AGG>
-__global__ __launch_bounds__(kThreads) void k_gemm_f32(GemmArgs a) {
+template <int BM, int BN, int WM, int WN>
+struct Shape {
+  static constexpr int kWavesM = BM / (16 * WM);
+  static constexpr int kWavesN = BN / (16 * WN);
+  static_assert(kWavesM * kWavesN == 4, "four waves per block");
+  static constexpr int kAChunks = BM * (kBK / 4);  // float4 chunks per A tile
+  static constexpr int kBChunks = BN * (kBK / 4);
+  static constexpr int kAPer = (kAChunks + kThreads - 1) / kThreads;
+  static constexpr int kBPer = (kBChunks + kThreads - 1) / kThreads;
+};
+
+template <int AGG, bool VEC>
+__device__ inline float4 load_a(const GemmArgs &a, int v, float tv, float sv, int k) {
+  float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (v < 0 || k >= a.K) return r;
+  const int dp = a.dprev;
+  const long long base = static_cast<long long>(v) * dp;
+  if (VEC) {
+    if (AGG == kGcn) {
+      const float4 s = *reinterpret_cast<const float4 *>(a.S + base + k);
+      const float4 h = *reinterpret_cast<const float4 *>(a.Hprev + base + k);
+      r = make_float4(tv * (s.x + sv * h.x), tv * (s.y + sv * h.y), tv * (s.z + sv * h.z), tv * (s.w + sv * h.w));
+    } else if (k < dp) {
+      r = *reinterpret_cast<const float4 *>(a.Hprev + base + k);
+    } else {
+      const float4 s = *reinterpret_cast<const float4 *>(a.S + base + (k - dp));
+      r = make_float4(tv * s.x, tv * s.y, tv * s.z, tv * s.w);
+    }
+    return r;
+  }
+  float t[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int kk = k + i;
+    float val = 0.f;
+    if (kk < a.K) {
+      if (AGG == kGcn) {
+        val = tv * (a.S[base + kk] + sv * a.Hprev[base + kk]);
+      } else {
+        val = kk < dp ? a.Hprev[base + kk] : tv * a.S[base + (kk - dp)];
+      }
+    }
+    t[i] = val;
+  }
+  return make_float4(t[0], t[1], t[2], t[3]);
+}
+
+template <bool VEC>
+__device__ inline float4 load_b(const GemmArgs &a, int col, int k) {
+  if (col >= a.N || k >= a.K) return make_float4(0.f, 0.f, 0.f, 0.f);
+  const float *w = a.W + static_cast<long long>(col) * a.K + k;
+  if (VEC) return *reinterpret_cast<const float4 *>(w);
+  float t[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) t[i] = k + i < a.K ? w[i] : 0.f;
+  return make_float4(t[0], t[1], t[2], t[3]);
+}
+
+template <int BM, int BN, int WM, int WN, int AGG, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
+  using Sh = Shape<BM, BN, WM, WN>;
   if (a.abort != nullptr && *a.abort) return;
   const long long M = a.count != nullptr ? static_cast<long long>(*a.count) : a.count_fixed;
-  const int N = a.N, K = a.K, dp = a.dprev;
-  const long long tiles_n = (N + kBN - 1) / kBN;
-  const long long tiles = ((M + kBM - 1) / kBM) * tiles_n;
+  const int N = a.N, K = a.K;
+  const long long tiles_n = (N + BN - 1) / BN;
+  const long long tiles = ((M + BM - 1) / BM) * tiles_n;
 
-  __shared__ float As[kBK][kBM + 4];  // As[k][m] = Z[m0+m][k0+k]
-  __shared__ float Bs[kBK][kBN + 4];  // Bs[k][n] = W[n0+n][k0+k]
-  __shared__ int rv[kBM];             // vertex of each tile row, -1 past M
-  __shared__ float rt[kBM];           // aggregate scale t_v
-  __shared__ float rs[kBM];           // GCN self coefficient s_v (post-batch)
+  __shared__ float As[2][BM][kLdk];
+  __shared__ float Bs[2][BN][kLdk];
+  __shared__ int rv[BM];
+  __shared__ float rt[BM];
+  __shared__ float rs[BM];
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
-  const int wm = (wave >> 1) * 32;
-  const int wn = (wave & 1) * 32;
+  const int wm0 = (wave / Sh::kWavesN) * (16 * WM);
+  const int wn0 = (wave % Sh::kWavesN) * (16 * WN);
+  const int lr = lane & 15;      // row (A) / column (B) within a 16-wide MFMA tile
+  const int lk = lane >> 4;      // k within a 4-deep MFMA step
 
   for (long long t = blockIdx.x; t < tiles; t += gridDim.x) {
-    const long long m0 = (t / tiles_n) * kBM;
-    const int n0 = static_cast<int>(t % tiles_n) * kBN;
+    const long long m0 = (t / tiles_n) * BM;
+    const int n0 = static_cast<int>(t % tiles_n) * BN;
     __syncthreads();
-    if (tid < kBM) {
-      const long long r = m0 + tid;
+    for (int r = tid; r < BM; r += kThreads) {
+      const long long row = m0 + r;
       int v = -1;
-      float tv = 0.0f, sv = 0.0f;
-      if (r < M) {
-        v = a.rows != nullptr ? a.rows[r] : static_cast<int>(r);
+      float tv = 0.f, sv = 0.f;
+      if (row < M) {
+        v = a.rows != nullptr ? a.rows[row] : static_cast<int>(row);
         if (AGG == kMean) {
           const int din = a.in_len[v];
-          tv = din > 0 ? 1.0f / static_cast<float>(din) : 0.0f;
+          tv = din > 0 ? 1.0f / static_cast<float>(din) : 0.f;
         } else if (AGG == kGcn) {
           tv = 1.0f / sqrtf(static_cast<float>(a.in_len[v]) + 1.0f);
           sv = 1.0f / sqrtf(static_cast<float>(a.out_len[v]) + 1.0f);
@@ -61,79 +124,101 @@ __global__ __launch_bounds__(kThreads) void k_gemm_f32(GemmArgs a) {
           tv = 1.0f;
         }
       }
-      rv[tid] = v;
-      rt[tid] = tv;
-      rs[tid] = sv;
+      rv[r] = v;
+      rt[r] = tv;
+      rs[r] = sv;
     }
-    floatx4 acc[2][2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+    __syncthreads();
 
+    float4 ra[Sh::kAPer], rb[Sh::kBPer];
+    auto load_regs = [&](int k0) {
+#pragma unroll
+      for (int i = 0; i < Sh::kAPer; ++i) {
+        const int c = tid + i * kThreads;
+        if (c < Sh::kAChunks) {
+          const int m = c / (kBK / 4);
+          const int q = c % (kBK / 4);
+          ra[i] = load_a<AGG, VEC>(a, rv[m], rt[m], rs[m], k0 + 4 * q);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < Sh::kBPer; ++i) {
+        const int c = tid + i * kThreads;
+        if (c < Sh::kBChunks) {
+          const int nn = c / (kBK / 4);
+          const int q = c % (kBK / 4);
+          rb[i] = load_b<VEC>(a, n0 + nn, k0 + 4 * q);
+        }
+      }
+    };
+    auto store_lds = [&](int buf) {
+#pragma unroll
+      for (int i = 0; i < Sh::kAPer; ++i) {
+        const int c = tid + i * kThreads;
+        if (c < Sh::kAChunks) {
+          const int m = c / (kBK / 4);
+          const int q = c % (kBK / 4);
+          *reinterpret_cast<float4 *>(&As[buf][m][4 * q]) = ra[i];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < Sh::kBPer; ++i) {
+        const int c = tid + i * kThreads;
+        if (c < Sh::kBChunks) {
+          const int nn = c / (kBK / 4);
+          const int q = c % (kBK / 4);
+          *reinterpret_cast<float4 *>(&Bs[buf][nn][4 * q]) = rb[i];
+        }
+      }
+    };
+
+    floatx4 acc[WM][WN];
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    load_regs(0);
+    store_lds(0);
+    __syncthreads();
+    int buf = 0;
     for (int k0 = 0; k0 < K; k0 += kBK) {
-      __syncthreads();
-      {
-        const int m = tid >> 2;
-        const int kb = (tid & 3) * 4;
-        const int v = rv[m];
-        const long long rowoff = static_cast<long long>(v) * dp;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int k = k0 + kb + i;
-          float val = 0.0f;
-          if (v >= 0 && k < K) {
-            if (AGG == kGcn) {
-              val = rt[m] * (a.S[rowoff + k] + rs[m] * a.Hprev[rowoff + k]);
-            } else {
-              val = k < dp ? a.Hprev[rowoff + k] : rt[m] * a.S[rowoff + (k - dp)];
-            }
-          }
-          As[kb + i][m] = val;
-        }
-      }
-      {
-        const int nn = tid >> 2;
-        const int kb = (tid & 3) * 4;
-        const int col = n0 + nn;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int k = k0 + kb + i;
-          Bs[kb + i][nn] = (col < N && k < K) ? a.W[static_cast<long long>(col) * K + k] : 0.0f;
-        }
-      }
-      __syncthreads();
+      const bool more = k0 + kBK < K;
+      if (more) load_regs(k0 + kBK);
 #pragma unroll
       for (int kk = 0; kk < kBK; kk += 4) {
-        const int kr = kk + (lane >> 4);
-        float av[2], bv[2];
+        float av[WM], bv[WN];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) av[i] = As[kr][wm + i * 16 + (lane & 15)];
+        for (int i = 0; i < WM; ++i) av[i] = As[buf][wm0 + i * 16 + lr][kk + lk];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) bv[j] = Bs[kr][wn + j * 16 + (lane & 15)];
+        for (int j = 0; j < WN; ++j) bv[j] = Bs[buf][wn0 + j * 16 + lr][kk + lk];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < WM; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
+          for (int j = 0; j < WN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j], acc[i][j], 0, 0, 0);
       }
+      if (more) store_lds(buf ^ 1);
+      __syncthreads();
+      buf ^= 1;
     }
+
     // epilogue: lane holds C[4*(lane/16) + r][lane % 16] of each 16 x 16 tile
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < WM; ++i) {
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int col = n0 + wn + j * 16 + (lane & 15);
+      for (int j = 0; j < WN; ++j) {
+        const int col = n0 + wn0 + j * 16 + lr;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int ml = wm + i * 16 + (lane >> 4) * 4 + r;
+          const int ml = wm0 + i * 16 + lk * 4 + r;
           const int v = rv[ml];
           if (v < 0 || col >= N) continue;
-          float y = acc[i][j][r] + (a.bias != nullptr ? a.bias[col] : 0.0f);
-          if (a.relu) y = fmaxf(y, 0.0f);
+          float y = acc[i][j][r] + (a.bias != nullptr ? a.bias[col] : 0.f);
+          if (a.relu) y = fmaxf(y, 0.f);
           float *hp = a.H + static_cast<long long>(v) * N + col;
           if (a.delta != nullptr) {
-            float cn = 1.0f, co = 1.0f;
+            float cn = 1.f, co = 1.f;
             if (AGG == kGcn) {
               cn = rs[ml];
               co = 1.0f / sqrtf(static_cast<float>(a.out_len[v] - a.ddeg[v]) + 1.0f);
@@ -147,21 +232,219 @@ __global__ __launch_bounds__(kThreads) void k_gemm_f32(GemmArgs a) {
   }
 }
 
-}  // namespace
+// Small-row-count variant: a block owns a 16 x BN tile and its four waves split
+// each 128-deep K step between them (wave w takes the 4-deep sub-steps w, w+4,
+// ...), so a short row list still spreads over many waves and K = 512 takes four
+// steps; the partial tiles are summed through LDS before the epilogue.
+constexpr int kSmallBM = 16;
+constexpr int kSmallBK = 128;
+constexpr int kSmallLdk = kSmallBK + 4;
 
-void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows) {
-  const long long tiles = ((max_rows + kBM - 1) / kBM) * ((a.N + kBN - 1) / kBN);
+template <int BN, int AGG, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_gemm_small(GemmArgs a) {
+  constexpr int WN = BN / 16;
+  constexpr int kAChunks = kSmallBM * (kSmallBK / 4);
+  constexpr int kBChunks = BN * (kSmallBK / 4);
+  constexpr int kAPer = (kAChunks + kThreads - 1) / kThreads;
+  constexpr int kBPer = (kBChunks + kThreads - 1) / kThreads;
+  if (a.abort != nullptr && *a.abort) return;
+  const long long M = a.count != nullptr ? static_cast<long long>(*a.count) : a.count_fixed;
+  const int N = a.N, K = a.K;
+  const long long tiles_n = (N + BN - 1) / BN;
+  const long long tiles = ((M + kSmallBM - 1) / kSmallBM) * tiles_n;
+
+  __shared__ float As[2][kSmallBM][kSmallLdk];
+  __shared__ float Bs[2][BN][kSmallLdk];
+  __shared__ float red[4][kSmallBM][BN + 1];
+  __shared__ int rv[kSmallBM];
+  __shared__ float rt[kSmallBM];
+  __shared__ float rs[kSmallBM];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int lr = lane & 15;
+  const int lk = lane >> 4;
+
+  for (long long t = blockIdx.x; t < tiles; t += gridDim.x) {
+    const long long m0 = (t / tiles_n) * kSmallBM;
+    const int n0 = static_cast<int>(t % tiles_n) * BN;
+    __syncthreads();
+    if (tid < kSmallBM) {
+      const long long row = m0 + tid;
+      int v = -1;
+      float tv = 0.f, sv = 0.f;
+      if (row < M) {
+        v = a.rows != nullptr ? a.rows[row] : static_cast<int>(row);
+        if (AGG == kMean) {
+          const int din = a.in_len[v];
+          tv = din > 0 ? 1.0f / static_cast<float>(din) : 0.f;
+        } else if (AGG == kGcn) {
+          tv = 1.0f / sqrtf(static_cast<float>(a.in_len[v]) + 1.0f);
+          sv = 1.0f / sqrtf(static_cast<float>(a.out_len[v]) + 1.0f);
+        } else {
+          tv = 1.0f;
+        }
+      }
+      rv[tid] = v;
+      rt[tid] = tv;
+      rs[tid] = sv;
+    }
+    __syncthreads();
+
+    float4 ra[kAPer], rb[kBPer];
+    auto load_regs = [&](int k0) {
+#pragma unroll
+      for (int i = 0; i < kAPer; ++i) {
+        const int c = tid + i * kThreads;
+        if (c < kAChunks) {
+          const int m = c / (kSmallBK / 4);
+          const int q = c % (kSmallBK / 4);
+          ra[i] = load_a<AGG, VEC>(a, rv[m], rt[m], rs[m], k0 + 4 * q);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < kBPer; ++i) {
+        const int c = tid + i * kThreads;
+        if (c < kBChunks) {
+          const int nn = c / (kSmallBK / 4);
+          const int q = c % (kSmallBK / 4);
+          rb[i] = load_b<VEC>(a, n0 + nn, k0 + 4 * q);
+        }
+      }
+    };
+    auto store_lds = [&](int buf) {
+#pragma unroll
+      for (int i = 0; i < kAPer; ++i) {
+        const int c = tid + i * kThreads;
+        if (c < kAChunks) {
+          const int m = c / (kSmallBK / 4);
+          const int q = c % (kSmallBK / 4);
+          *reinterpret_cast<float4 *>(&As[buf][m][4 * q]) = ra[i];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < kBPer; ++i) {
+        const int c = tid + i * kThreads;
+        if (c < kBChunks) {
+          const int nn = c / (kSmallBK / 4);
+          const int q = c % (kSmallBK / 4);
+          *reinterpret_cast<float4 *>(&Bs[buf][nn][4 * q]) = rb[i];
+        }
+      }
+    };
+
+    floatx4 acc[WN];
+#pragma unroll
+    for (int j = 0; j < WN; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    load_regs(0);
+    store_lds(0);
+    __syncthreads();
+    int buf = 0;
+    for (int k0 = 0; k0 < K; k0 += kSmallBK) {
+      const bool more = k0 + kSmallBK < K;
+      if (more) load_regs(k0 + kSmallBK);
+#pragma unroll
+      for (int kk = 4 * wave; kk < kSmallBK; kk += 16) {
+        const float av = As[buf][lr][kk + lk];
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, Bs[buf][j * 16 + lr][kk + lk], acc[j], 0, 0, 0);
+      }
+      if (more) store_lds(buf ^ 1);
+      __syncthreads();
+      buf ^= 1;
+    }
+    // partial tiles -> LDS, summed by all threads
+#pragma unroll
+    for (int j = 0; j < WN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) red[wave][lk * 4 + r][j * 16 + lr] = acc[j][r];
+    __syncthreads();
+    for (int e = tid; e < kSmallBM * BN; e += kThreads) {
+      const int ml = e / BN, cl = e % BN;
+      const int col = n0 + cl;
+      const int v = rv[ml];
+      if (v < 0 || col >= N) continue;
+      float y = red[0][ml][cl] + red[1][ml][cl] + red[2][ml][cl] + red[3][ml][cl];
+      y += a.bias != nullptr ? a.bias[col] : 0.f;
+      if (a.relu) y = fmaxf(y, 0.f);
+      float *hp = a.H + static_cast<long long>(v) * N + col;
+      if (a.delta != nullptr) {
+        float cn = 1.f, co = 1.f;
+        if (AGG == kGcn) {
+          cn = rs[ml];
+          co = 1.0f / sqrtf(static_cast<float>(a.out_len[v] - a.ddeg[v]) + 1.0f);
+        }
+        a.delta[(m0 + ml) * N + col] = cn * y - co * (*hp);
+      }
+      *hp = y;
+    }
+  }
+}
+
+template <int BN, int AGG, bool VEC>
+void launch_small(hipStream_t s, const GemmArgs &a, long long max_rows) {
+  const long long tiles = ((max_rows + kSmallBM - 1) / kSmallBM) * ((a.N + BN - 1) / BN);
   long long blocks = tiles < 1 ? 1 : tiles;
   if (blocks > 2048) blocks = 2048;
+  hipLaunchKernelGGL((k_gemm_small<BN, AGG, VEC>), dim3(blocks), dim3(kThreads), 0, s, a);
+}
+
+template <int BM, int BN, int WM, int WN, int AGG, bool VEC>
+void launch_shape(hipStream_t s, const GemmArgs &a, long long max_rows) {
+  const long long tiles = ((max_rows + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  long long blocks = tiles < 1 ? 1 : tiles;
+  if (blocks > 2048) blocks = 2048;
+  hipLaunchKernelGGL((k_gemm<BM, BN, WM, WN, AGG, VEC>), dim3(blocks), dim3(kThreads), 0, s, a);
+}
+
+// BN follows N. Few expected rows: the 16-row split-K kernel; many: 128-row tiles.
+template <int AGG, bool VEC>
+void launch_agg(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) {
+  const int N = a.N;
+  if (!VEC) {
+    if (N <= 16) launch_shape<64, 16, 1, 1, AGG, VEC>(s, a, max_rows);
+    else if (N <= 32) launch_shape<64, 32, 2, 1, AGG, VEC>(s, a, max_rows);
+    else if (N <= 48) launch_shape<64, 48, 1, 3, AGG, VEC>(s, a, max_rows);
+    else if (N <= 64) launch_shape<32, 64, 1, 2, AGG, VEC>(s, a, max_rows);
+    else launch_shape<32, 128, 2, 2, AGG, VEC>(s, a, max_rows);
+    return;
+  }
+  if (!big) {
+    if (N <= 16) launch_small<16, AGG, VEC>(s, a, max_rows);
+    else if (N <= 32) launch_small<32, AGG, VEC>(s, a, max_rows);
+    else if (N <= 48) launch_small<48, AGG, VEC>(s, a, max_rows);
+    else launch_small<64, AGG, VEC>(s, a, max_rows);  // N > 64: several 64-wide column tiles
+    return;
+  }
+  if (N <= 16) launch_shape<64, 16, 1, 1, AGG, VEC>(s, a, max_rows);
+  else if (N <= 32) launch_shape<64, 32, 2, 1, AGG, VEC>(s, a, max_rows);
+  else if (N <= 48) launch_shape<128, 48, 2, 3, AGG, VEC>(s, a, max_rows);
+  else if (N <= 64) launch_shape<128, 64, 4, 2, AGG, VEC>(s, a, max_rows);
+  else launch_shape<128, 128, 4, 4, AGG, VEC>(s, a, max_rows);
+}
+
+template <int AGG>
+void launch_vec(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) {
+  const bool vec = (a.dprev % 4 == 0) && (a.K % 4 == 0);
+  if (vec) launch_agg<AGG, true>(s, a, max_rows, big);
+  else launch_agg<AGG, false>(s, a, max_rows, big);
+}
+
+}  // namespace
+
+void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows, long long expected_rows) {
+  const bool big = expected_rows >= 32768;
   switch (a.agg) {
     case kMean:
-      hipLaunchKernelGGL(k_gemm_f32<kMean>, dim3(blocks), dim3(kThreads), 0, s, a);
+      launch_vec<kMean>(s, a, max_rows, big);
       break;
     case kGcn:
-      hipLaunchKernelGGL(k_gemm_f32<kGcn>, dim3(blocks), dim3(kThreads), 0, s, a);
+      launch_vec<kGcn>(s, a, max_rows, big);
       break;
     default:
-      hipLaunchKernelGGL(k_gemm_f32<kSum>, dim3(blocks), dim3(kThreads), 0, s, a);
+      launch_vec<kSum>(s, a, max_rows, big);
       break;
   }
 }

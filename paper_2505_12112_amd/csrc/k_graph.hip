@@ -3,17 +3,18 @@
 // Netting (sequential semantics of a batch): an insert sets an arc present and a
 // delete sets it absent, so the last op naming an edge decides its final state.
 // One pass hashes every edge op and keeps the largest op index per edge; a second
-// pass lets each winning op compare the final state with the pre-batch adjacency
-// and emit the net inserted / deleted arcs. The last feature write per vertex is
-// found the same way with a per-vertex atomicMax.
+// pass lets each winning op compare the final state with the pre-batch adjacency,
+// emit the net inserted / deleted arcs, tag the edge's hash slot (+1 insert,
+// -1 delete) and take a rank among its rows' inserts or deletes. The last feature
+// write per vertex is found the same way with a per-vertex atomicMax.
 //
 // Adjacency update: row slots are [off, off+cap), the first len used, in no
-// particular order. Deletes tombstone their slot, then each hole in the part of
-// the row that survives is filled from the row's tail; inserts append at
-// len + rank. Rows that would overflow are first moved to the spare arena; the
-// arena demand is checked before anything is mutated, so an arena that is too
-// small aborts the batch with the state intact (the host then re-lays the rows
-// out and runs the batch again).
+// particular order. A plan pass sums the spare-arena slots that growing rows need
+// and the last block to finish checks them against the arena: a batch that does
+// not fit is aborted before anything is mutated (the host then re-lays the rows
+// out and runs the batch again). Then one owner wave per touched row drops its
+// net-deleted entries (hash lookups), moves the row to the arena if it must grow,
+// and sets the new length; finally every insert is written at its rank.
 #include "internal.h"
 
 namespace rp {
@@ -35,6 +36,26 @@ __device__ inline long long num_waves() {
   return static_cast<long long>(gridDim.x) * blockDim.x / kWave;
 }
 
+__device__ inline u64 edge_key(int a, int b, int undirected, long long n) {
+  if (undirected && a > b) {
+    const int t = a;
+    a = b;
+    b = t;
+  }
+  return static_cast<u64>(a) * static_cast<u64>(n) + static_cast<u64>(b);
+}
+
+// Slot holding `key`, or -1 (probing stops at the first empty slot).
+__device__ inline int hash_find(const u64 *ht_key, unsigned mask, u64 key) {
+  unsigned s = hash_slot(key, mask);
+  while (true) {
+    const u64 k = ht_key[s];
+    if (k == key) return static_cast<int>(s);
+    if (k == kEmptyKey) return -1;
+    s = (s + 1) & mask;
+  }
+}
+
 // Position of `target` in row[0, len) or -1; all lanes of the wave get the answer.
 __device__ inline int wave_find(const int *row, int len, int target) {
   const int lane = lane_id();
@@ -47,11 +68,32 @@ __device__ inline int wave_find(const int *row, int len, int target) {
   return -1;
 }
 
-__global__ void k_net_hash(const ripple_op *ops, int B, int undirected, long long n, u64 *ht_key,
-                           int *ht_val, unsigned mask, int *op_slot, int *fop, Counters *c) {
+__device__ inline int lanes_below(u64 mask) {
+  return static_cast<int>(__builtin_amdgcn_mbcnt_hi(static_cast<unsigned>(mask >> 32),
+                                                    __builtin_amdgcn_mbcnt_lo(static_cast<unsigned>(mask), 0u)));
+}
+
+__device__ inline int grow_cap(int newlen) {
+  const long long g = static_cast<long long>(newlen) + newlen / 2 + 4;
+  return static_cast<int>(((g + 3) / 4) * 4);
+}
+
+// Work items over arcs x directions: item w -> arc w >> 1, direction w & 1.
+// Direction 0 (out-adjacency): row = src, entry = dst; direction 1: row = dst, entry = src.
+__device__ inline void item_row(long long w, const int *src, const int *dst, int &dir, int &row, int &entry) {
+  const long long arc = w >> 1;
+  dir = static_cast<int>(w & 1);
+  row = dir == 0 ? src[arc] : dst[arc];
+  entry = dir == 0 ? dst[arc] : src[arc];
+}
+
+// Reads the ops from pinned host memory and keeps a device copy for later kernels.
+__global__ void k_net_hash(const ripple_op *host_ops, ripple_op *ops, int B, int undirected, long long n,
+                           u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop, Counters *c) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= B) return;
-  const ripple_op op = ops[i];
+  const ripple_op op = host_ops[i];
+  ops[i] = op;
   if (op.kind == RIPPLE_OP_FEATURE) {
     atomicMax(&fop[op.u], i);
     op_slot[i] = -1;
@@ -62,13 +104,7 @@ __global__ void k_net_hash(const ripple_op *ops, int B, int undirected, long lon
     op_slot[i] = -1;
     return;
   }
-  int a = op.u, b = op.v;
-  if (undirected && a > b) {
-    const int t = a;
-    a = b;
-    b = t;
-  }
-  const u64 key = static_cast<u64>(a) * static_cast<u64>(n) + static_cast<u64>(b);
+  const u64 key = edge_key(op.u, op.v, undirected, n);
   unsigned s = hash_slot(key, mask);
   while (true) {
     const u64 prev = atomicCAS(&ht_key[s], kEmptyKey, key);
@@ -79,9 +115,10 @@ __global__ void k_net_hash(const ripple_op *ops, int B, int undirected, long lon
   op_slot[i] = static_cast<int>(s);
 }
 
-__global__ void k_net_decide(const ripple_op *ops, int B, int undirected, const int *ht_val,
-                             const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src,
-                             int *ins_dst, int *del_src, int *del_dst, int *flist, Counters *c) {
+__global__ void k_net_decide(const ripple_op *ops, int B, int undirected, const int *ht_val, int *ht_net,
+                             const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src, int *ins_dst,
+                             int *del_src, int *del_dst, int *ins_rank, int *del_rank, int *flist,
+                             Counters *c) {
   const int lane = lane_id();
   for (long long i = global_wave(); i < B; i += num_waves()) {
     const ripple_op op = ops[i];
@@ -103,62 +140,34 @@ __global__ void k_net_decide(const ripple_op *ops, int B, int undirected, const 
     const int la = out.len[a], lb = in.len[b];
     const bool use_out = la <= lb;
     const int *row = use_out ? out.col + out.off[a] : in.col + in.off[b];
-    const int pos = wave_find(row, use_out ? la : lb, use_out ? b : a);
-    const bool present = pos >= 0;
+    const bool present = wave_find(row, use_out ? la : lb, use_out ? b : a) >= 0;
     const bool want = op.kind == RIPPLE_OP_INSERT;
     if (lane == 0) {
       atomicAdd(&c->edge_keys, 1ull);
       if (want == present) {
         atomicAdd(&c->noop_edge, 1ull);
+        ht_net[s] = 0;
       } else {
+        ht_net[s] = want ? 1 : -1;
         int *ps = want ? ins_src : del_src;
         int *pd = want ? ins_dst : del_dst;
-        const u64 j = atomicAdd(want ? &c->n_ins : &c->n_del, undirected ? 2ull : 1ull);
-        ps[j] = a;
-        pd[j] = b;
-        if (undirected) {
-          ps[j + 1] = b;
-          pd[j + 1] = a;
+        int *rank = want ? ins_rank : del_rank;
+        const int narcs = undirected ? 2 : 1;
+        const u64 j = atomicAdd(want ? &c->n_ins : &c->n_del, static_cast<u64>(narcs));
+        for (int t = 0; t < narcs; ++t) {
+          const int su = t == 0 ? a : b, sv = t == 0 ? b : a;
+          ps[j + t] = su;
+          pd[j + t] = sv;
+          rank[2 * (j + t)] = atomicAdd(want ? &out.inscnt[su] : &out.delcnt[su], 1);
+          rank[2 * (j + t) + 1] = atomicAdd(want ? &in.inscnt[sv] : &in.delcnt[sv], 1);
         }
       }
     }
   }
 }
 
-// Work items over arcs x directions: item w -> arc w >> 1, direction w & 1.
-// Direction 0 (out-adjacency): row = src, entry = dst; direction 1: row = dst, entry = src.
-__device__ inline void item_row(long long w, const int *src, const int *dst, int &dir, int &row, int &entry) {
-  const long long arc = w >> 1;
-  dir = static_cast<int>(w & 1);
-  row = dir == 0 ? src[arc] : dst[arc];
-  entry = dir == 0 ? dst[arc] : src[arc];
-}
-
-__global__ void k_topo_count(int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                             const int *del_src, const int *del_dst, int *ins_rank, int *del_rank,
-                             Counters *c) {
-  const long long ni = 2 * static_cast<long long>(c->n_ins);
-  const long long nd = 2 * static_cast<long long>(c->n_del);
-  const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
-  for (long long w = blockIdx.x * blockDim.x + threadIdx.x; w < ni + nd; w += stride) {
-    int dir, row, entry;
-    if (w < ni) {
-      item_row(w, ins_src, ins_dst, dir, row, entry);
-      ins_rank[w] = atomicAdd(&(dir ? in : out).inscnt[row], 1);
-    } else {
-      item_row(w - ni, del_src, del_dst, dir, row, entry);
-      del_rank[w - ni] = atomicAdd(&(dir ? in : out).delcnt[row], 1);
-    }
-  }
-}
-
-__device__ inline int grow_cap(int newlen) {
-  const long long g = static_cast<long long>(newlen) + newlen / 2 + 4;
-  return static_cast<int>(((g + 3) / 4) * 4);
-}
-
-__global__ void k_topo_plan(int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                            const int *ins_rank, RelocItem *reloc, Counters *c) {
+__global__ void k_topo_plan(Adj out, Adj in, const int *ins_src, const int *ins_dst, const int *ins_rank,
+                            Counters *c, const Persist *p, long long cap_out, long long cap_in) {
   const long long ni = 2 * static_cast<long long>(c->n_ins);
   const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
   for (long long w = blockIdx.x * blockDim.x + threadIdx.x; w < ni; w += stride) {
@@ -166,138 +175,92 @@ __global__ void k_topo_plan(int cap_arcs, Adj out, Adj in, const int *ins_src, c
     int dir, row, entry;
     item_row(w, ins_src, ins_dst, dir, row, entry);
     const Adj &a = dir ? in : out;
-    const int newlen = a.len[row] - a.delcnt[row] + a.inscnt[row];
-    if (newlen > a.cap[row]) {
-      const int nc = grow_cap(newlen);
-      const u64 j = atomicAdd(&c->n_reloc, 1ull);
-      reloc[j] = RelocItem{row, dir, nc, 0};
-      atomicAdd(&c->arena_need[dir], static_cast<u64>(nc));
+    const int need = a.len[row] - a.delcnt[row] + a.inscnt[row];
+    if (need > a.cap[row]) {
+      atomicAdd(&c->n_reloc, 1ull);
+      atomicAdd(&c->arena_need[dir], static_cast<u64>(grow_cap(need)));
     }
+  }
+  // the last block to finish compares the arena demand with the free arena
+  __threadfence();
+  __syncthreads();
+  __shared__ bool last;
+  if (threadIdx.x == 0) last = atomicAdd(&c->plan_done, 1ull) == gridDim.x - 1;
+  __syncthreads();
+  if (last && threadIdx.x == 0) {
+    __threadfence();
+    const u64 need0 = atomicAdd(&c->arena_need[0], 0ull);
+    const u64 need1 = atomicAdd(&c->arena_need[1], 0ull);
+    if (p->top[0] + need0 > static_cast<u64>(cap_out) || p->top[1] + need1 > static_cast<u64>(cap_in))
+      c->abort = 1;
   }
 }
 
-__global__ void k_topo_check(Counters *c, const Persist *p, long long cap_out, long long cap_in) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  const bool over0 = p->top[0] + c->arena_need[0] > static_cast<u64>(cap_out);
-  const bool over1 = p->top[1] + c->arena_need[1] > static_cast<u64>(cap_in);
-  if (over0 || over1) c->abort = 1;
-}
-
-// Pre-batch corrections, one per net arc (u,v) and layer l: an inserted arc adds
-// u's pre-batch contribution to S^l_v, a deleted arc removes it (an insert is a
-// message whose old embedding is zero, a delete one whose new embedding is zero).
-// Runs before any adjacency, feature or embedding write, so H and degrees are the
-// pre-batch ones.
-__global__ void k_corrections(int agg, LayerPtrs lp, const int *out_len, const int *ins_src,
-                              const int *ins_dst, const int *del_src, const int *del_dst, Counters *c) {
+// One wave per touched (row, direction): the row's owner is its rank-0 insert
+// item, or its rank-0 delete item when it has no inserts.
+__global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, const int *ins_src,
+                               const int *ins_dst, const int *del_src, const int *del_dst, const int *ins_rank,
+                               const int *del_rank, const u64 *ht_key, const int *ht_net, unsigned mask,
+                               Persist *p, int *ddeg, Counters *c) {
   if (c->abort) return;
   const int lane = lane_id();
-  const long long ni = static_cast<long long>(c->n_ins);
-  const long long na = ni + static_cast<long long>(c->n_del);
-  const long long items = na * lp.L;
-  for (long long it = global_wave(); it < items; it += num_waves()) {
-    const long long arc = it / lp.L;
-    const int l = static_cast<int>(it % lp.L) + 1;
-    const bool ins = arc < ni;
-    const int u = ins ? ins_src[arc] : del_src[arc - ni];
-    const int v = ins ? ins_dst[arc] : del_dst[arc - ni];
-    float coef = ins ? 1.0f : -1.0f;
-    if (agg == kGcn) coef *= 1.0f / sqrtf(static_cast<float>(out_len[u]) + 1.0f);
-    const int d = lp.dims[l - 1];
-    const float *hu = lp.H[l - 1] + static_cast<long long>(u) * d;
-    float *sv = lp.S[l] + static_cast<long long>(v) * d;
-    for (int k = lane; k < d; k += kWave) unsafeAtomicAdd(&sv[k], coef * hu[k]);
-  }
-}
-
-// Deletes: tombstone, fill surviving holes from the tail, shrink the row.
-__global__ void k_del_find(Adj out, Adj in, const int *del_src, const int *del_dst, int *del_pos,
-                           Counters *c) {
-  if (c->abort) return;
+  const long long ni = 2 * static_cast<long long>(c->n_ins);
   const long long nd = 2 * static_cast<long long>(c->n_del);
-  for (long long w = global_wave(); w < nd; w += num_waves()) {
+  for (long long w = global_wave(); w < ni + nd; w += num_waves()) {
     int dir, row, entry;
-    item_row(w, del_src, del_dst, dir, row, entry);
-    const Adj &a = dir ? in : out;
-    int *r = a.col + a.off[row];
-    const int pos = wave_find(r, a.len[row], entry);
-    if (lane_id() == 0) {
-      del_pos[w] = pos;
-      if (pos < 0) {
-        atomicOr(&c->err, 1ull);
-      } else {
-        r[pos] = -1;
-      }
+    if (w < ni) {
+      if (ins_rank[w] != 0) continue;
+      item_row(w, ins_src, ins_dst, dir, row, entry);
+    } else {
+      if (del_rank[w - ni] != 0) continue;
+      item_row(w - ni, del_src, del_dst, dir, row, entry);
+      if ((dir ? in : out).inscnt[row] != 0) continue;  // the insert owner handles this row
     }
-  }
-}
-
-__global__ void k_del_fill(Adj out, Adj in, const int *del_src, const int *del_dst, const int *del_pos,
-                           Counters *c) {
-  if (c->abort) return;
-  const long long nd = 2 * static_cast<long long>(c->n_del);
-  const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
-  for (long long w = blockIdx.x * blockDim.x + threadIdx.x; w < nd; w += stride) {
-    int dir, row, entry;
-    item_row(w, del_src, del_dst, dir, row, entry);
     const Adj &a = dir ? in : out;
-    const int p = del_pos[w];
-    const int len = a.len[row], k = a.delcnt[row];
-    if (p < 0 || p >= len - k) continue;  // hole lies in the part that is cut off
-    const int j = atomicAdd(&a.fillcnt[row], 1);
-    int *r = a.col + a.off[row];
-    int seen = 0;
-    for (int e = len - k; e < len; ++e) {
-      const int val = r[e];
-      if (val < 0) continue;
-      if (seen == j) {
-        r[p] = val;
-        break;
-      }
-      ++seen;
+    const int len0 = a.len[row], k = a.delcnt[row], nins = a.inscnt[row];
+    const int need = len0 - k + nins;
+    const bool move = nins > 0 && need > a.cap[row];
+    const long long src_off = a.off[row];
+    long long dst_off = src_off;
+    int nc = 0;
+    if (move) {
+      nc = grow_cap(need);
+      long long base = 0;
+      if (lane == 0) base = static_cast<long long>(atomicAdd(&p->top[dir], static_cast<u64>(nc)));
+      dst_off = __shfl(base, 0);
     }
-  }
-}
-
-__global__ void k_del_finish(Adj out, Adj in, const int *del_src, const int *del_dst, const int *del_rank,
-                             int *ddeg, Counters *c) {
-  if (c->abort) return;
-  const long long nd = 2 * static_cast<long long>(c->n_del);
-  const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
-  for (long long w = blockIdx.x * blockDim.x + threadIdx.x; w < nd; w += stride) {
-    if (del_rank[w] != 0) continue;
-    int dir, row, entry;
-    item_row(w, del_src, del_dst, dir, row, entry);
-    const Adj &a = dir ? in : out;
-    const int k = a.delcnt[row];
-    a.len[row] -= k;
-    if (dir == 0) ddeg[row] -= k;
-  }
-}
-
-__global__ void k_reloc(Adj out, Adj in, const RelocItem *reloc, Persist *p, Counters *c) {
-  if (c->abort) return;
-  const long long nr = static_cast<long long>(c->n_reloc);
-  const int lane = lane_id();
-  for (long long j = global_wave(); j < nr; j += num_waves()) {
-    const RelocItem it = reloc[j];
-    const Adj &a = it.dir ? in : out;
-    long long base = 0;
-    if (lane == 0) base = static_cast<long long>(atomicAdd(&p->top[it.dir], static_cast<u64>(it.newcap)));
-    base = __shfl(base, 0);
-    const int *src = a.col + a.off[it.row];
-    int *dst = a.col + base;
-    const int len = a.len[it.row];
-    for (int e = lane; e < len; e += kWave) dst[e] = src[e];
+    if (k > 0 || move) {
+      const int *src = a.col + src_off;
+      int *dst = a.col + dst_off;
+      int wpos = 0;
+      for (int base = 0; base < len0; base += kWave) {
+        const int e = base + lane;
+        const int x = e < len0 ? src[e] : -1;
+        bool keep = e < len0;
+        if (keep && k > 0) {
+          const int au = dir ? x : row, av = dir ? row : x;
+          const int slot = hash_find(ht_key, mask, edge_key(au, av, undirected, n));
+          keep = slot < 0 || ht_net[slot] != -1;
+        }
+        const u64 m = __ballot(keep);
+        if (keep) dst[wpos + lanes_below(m)] = x;  // in place: never past the entry read
+        wpos += __popcll(m);
+      }
+      if (lane == 0 && wpos != len0 - k) atomicOr(&c->err, 2ull);
+    }
     if (lane == 0) {
-      a.off[it.row] = base;
-      a.cap[it.row] = it.newcap;
+      if (move) {
+        a.off[row] = dst_off;
+        a.cap[row] = nc;
+      }
+      a.len[row] = need;
+      if (dir == 0) ddeg[row] = nins - k;
     }
   }
 }
 
-__global__ void k_ins_put(Adj out, Adj in, const int *ins_src, const int *ins_dst, const int *ins_rank,
-                          Counters *c) {
+__global__ void k_topo_put(Adj out, Adj in, const int *ins_src, const int *ins_dst, const int *ins_rank,
+                           Counters *c) {
   if (c->abort) return;
   const long long ni = 2 * static_cast<long long>(c->n_ins);
   const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
@@ -305,30 +268,26 @@ __global__ void k_ins_put(Adj out, Adj in, const int *ins_src, const int *ins_ds
     int dir, row, entry;
     item_row(w, ins_src, ins_dst, dir, row, entry);
     const Adj &a = dir ? in : out;
-    a.col[a.off[row] + a.len[row] + ins_rank[w]] = entry;
+    a.col[a.off[row] + (a.len[row] - a.inscnt[row]) + ins_rank[w]] = entry;
   }
 }
 
-__global__ void k_ins_finish(Adj out, Adj in, const int *ins_src, const int *ins_dst, const int *ins_rank,
-                             int *ddeg, Counters *c) {
-  if (c->abort) return;
-  const long long ni = 2 * static_cast<long long>(c->n_ins);
-  const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
-  for (long long w = blockIdx.x * blockDim.x + threadIdx.x; w < ni; w += stride) {
-    if (ins_rank[w] != 0) continue;
-    int dir, row, entry;
-    item_row(w, ins_src, ins_dst, dir, row, entry);
-    const Adj &a = dir ? in : out;
-    const int k = a.inscnt[row];
-    a.len[row] += k;
-    if (dir == 0) ddeg[row] += k;
+// Resets every per-batch scratch word the batch touched (runs even after an abort),
+// copies the batch's counters to pinned host memory and clears the other counter
+// buffer for the next batch.
+__global__ void k_cleanup(int B, const ripple_op *ops, const int *op_slot, u64 *ht_key, int *ht_val, int *ht_net,
+                          int *fop, Adj out, Adj in, const int *ins_src, const int *ins_dst, const int *del_src,
+                          const int *del_dst, int *ddeg, const Counters *c, Counters *next, Counters *host) {
+  if (blockIdx.x == 0) {
+    constexpr int words = static_cast<int>(sizeof(Counters) / sizeof(u64));
+    const u64 *src = reinterpret_cast<const u64 *>(c);
+    u64 *dst = reinterpret_cast<u64 *>(host);
+    u64 *nxt = reinterpret_cast<u64 *>(next);
+    for (int w = threadIdx.x; w < words; w += blockDim.x) {
+      dst[w] = src[w];
+      nxt[w] = 0ull;
+    }
   }
-}
-
-// Resets every per-batch scratch word the batch touched (runs even after an abort).
-__global__ void k_cleanup(int B, const ripple_op *ops, const int *op_slot, u64 *ht_key, int *ht_val,
-                          int *fop, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                          const int *del_src, const int *del_dst, int *ddeg, const Counters *c) {
   const long long ni = 2 * static_cast<long long>(c->n_ins);
   const long long nd = 2 * static_cast<long long>(c->n_del);
   const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
@@ -342,9 +301,7 @@ __global__ void k_cleanup(int B, const ripple_op *ops, const int *op_slot, u64 *
   for (long long w = t0; w < nd; w += stride) {
     int dir, row, entry;
     item_row(w, del_src, del_dst, dir, row, entry);
-    const Adj &a = dir ? in : out;
-    a.delcnt[row] = 0;
-    a.fillcnt[row] = 0;
+    (dir ? in : out).delcnt[row] = 0;
     if (dir == 0) ddeg[row] = 0;
   }
   for (long long i = t0; i < B; i += stride) {
@@ -352,8 +309,21 @@ __global__ void k_cleanup(int B, const ripple_op *ops, const int *op_slot, u64 *
     if (s >= 0) {
       ht_key[s] = kEmptyKey;
       ht_val[s] = -1;
+      ht_net[s] = 0;
     }
     if (ops[i].kind == RIPPLE_OP_FEATURE) fop[ops[i].u] = -1;
+  }
+}
+
+// Re-layout: row u's used entries move from old_col[old_off[u]..] to new_col[new_off[u]..].
+__global__ void k_repack_copy(long long n, const int *old_col, const long long *old_off, const int *len,
+                              int *new_col, const long long *new_off) {
+  const int lane = lane_id();
+  for (long long u = global_wave(); u < n; u += num_waves()) {
+    const int *src = old_col + old_off[u];
+    int *dst = new_col + new_off[u];
+    const int l = len[u];
+    for (int e = lane; e < l; e += kWave) dst[e] = src[e];
   }
 }
 
@@ -366,104 +336,56 @@ inline int blocks_for(long long items, int threads, int cap = 4096) {
 
 }  // namespace
 
-void launch_net_hash(hipStream_t s, const ripple_op *ops, int B, int undirected, long long n, u64 *ht_key,
-                     int *ht_val, unsigned mask, int *op_slot, int *fop, Counters *c) {
+void launch_net_hash(hipStream_t s, const ripple_op *host_ops, ripple_op *ops, int B, int undirected, long long n,
+                     u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop, Counters *c) {
   if (B <= 0) return;
-  hipLaunchKernelGGL(k_net_hash, dim3(blocks_for(B, 256, 1 << 20)), dim3(256), 0, s, ops, B, undirected, n,
-                     ht_key, ht_val, mask, op_slot, fop, c);
+  hipLaunchKernelGGL(k_net_hash, dim3(blocks_for(B, 256, 1 << 20)), dim3(256), 0, s, host_ops, ops, B, undirected,
+                     n, ht_key, ht_val, mask, op_slot, fop, c);
 }
 
-void launch_net_decide(hipStream_t s, const ripple_op *ops, int B, int undirected, const int *ht_val,
+void launch_net_decide(hipStream_t s, const ripple_op *ops, int B, int undirected, const int *ht_val, int *ht_net,
                        const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src, int *ins_dst,
-                       int *del_src, int *del_dst, int *flist, Counters *c) {
+                       int *del_src, int *del_dst, int *ins_rank, int *del_rank, int *flist, Counters *c) {
   if (B <= 0) return;
   hipLaunchKernelGGL(k_net_decide, dim3(blocks_for(static_cast<long long>(B) * kWave, 256)), dim3(256), 0, s,
-                     ops, B, undirected, ht_val, op_slot, fop, out, in, ins_src, ins_dst, del_src, del_dst,
-                     flist, c);
-}
-
-void launch_topo_count(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                       const int *del_src, const int *del_dst, int *ins_rank, int *del_rank, Counters *c) {
-  hipLaunchKernelGGL(k_topo_count, dim3(blocks_for(4LL * cap_arcs, 256)), dim3(256), 0, s, cap_arcs, out, in,
-                     ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank, c);
+                     ops, B, undirected, ht_val, ht_net, op_slot, fop, out, in, ins_src, ins_dst, del_src,
+                     del_dst, ins_rank, del_rank, flist, c);
 }
 
 void launch_topo_plan(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                      const int *ins_rank, RelocItem *reloc, Counters *c) {
-  hipLaunchKernelGGL(k_topo_plan, dim3(blocks_for(2LL * cap_arcs, 256)), dim3(256), 0, s, cap_arcs, out, in,
-                     ins_src, ins_dst, ins_rank, reloc, c);
+                      const int *ins_rank, Counters *c, const Persist *p, long long cap_out, long long cap_in) {
+  hipLaunchKernelGGL(k_topo_plan, dim3(blocks_for(2LL * cap_arcs, 256, 1024)), dim3(256), 0, s, out, in, ins_src,
+                     ins_dst, ins_rank, c, p, cap_out, cap_in);
 }
 
-void launch_topo_check(hipStream_t s, Counters *c, const Persist *p, long long cap_out, long long cap_in) {
-  hipLaunchKernelGGL(k_topo_check, dim3(1), dim3(64), 0, s, c, p, cap_out, cap_in);
+void launch_topo_rewrite(hipStream_t s, int cap_arcs, int undirected, long long n, Adj out, Adj in,
+                         const int *ins_src, const int *ins_dst, const int *del_src, const int *del_dst,
+                         const int *ins_rank, const int *del_rank, const u64 *ht_key, const int *ht_net,
+                         unsigned mask, Persist *p, int *ddeg, Counters *c) {
+  hipLaunchKernelGGL(k_topo_rewrite, dim3(blocks_for(4LL * cap_arcs * kWave, 256)), dim3(256), 0, s, undirected,
+                     n, out, in, ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank, ht_key, ht_net, mask, p,
+                     ddeg, c);
 }
 
-void launch_corrections(hipStream_t s, int cap_arcs, int agg, LayerPtrs lp, const int *out_len,
-                        const int *ins_src, const int *ins_dst, const int *del_src, const int *del_dst,
-                        Counters *c) {
-  hipLaunchKernelGGL(k_corrections, dim3(blocks_for(2LL * cap_arcs * lp.L * kWave, 256)), dim3(256), 0, s,
-                     agg, lp, out_len, ins_src, ins_dst, del_src, del_dst, c);
-}
-
-void launch_del_apply(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *del_src, const int *del_dst,
-                      const int *del_rank, int *del_pos, int *ddeg, Counters *c) {
-  hipLaunchKernelGGL(k_del_find, dim3(blocks_for(2LL * cap_arcs * kWave, 256)), dim3(256), 0, s, out, in,
-                     del_src, del_dst, del_pos, c);
-  hipLaunchKernelGGL(k_del_fill, dim3(blocks_for(2LL * cap_arcs, 256)), dim3(256), 0, s, out, in, del_src,
-                     del_dst, del_pos, c);
-  hipLaunchKernelGGL(k_del_finish, dim3(blocks_for(2LL * cap_arcs, 256)), dim3(256), 0, s, out, in, del_src,
-                     del_dst, del_rank, ddeg, c);
-}
-
-void launch_reloc(hipStream_t s, int cap_reloc, Adj out, Adj in, const RelocItem *reloc, Persist *p,
-                  Counters *c) {
-  hipLaunchKernelGGL(k_reloc, dim3(blocks_for(static_cast<long long>(cap_reloc) * kWave, 256)), dim3(256), 0, s,
-                     out, in, reloc, p, c);
-}
-
-void launch_ins_apply(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                      const int *ins_rank, int *ddeg, Counters *c) {
-  hipLaunchKernelGGL(k_ins_put, dim3(blocks_for(2LL * cap_arcs, 256)), dim3(256), 0, s, out, in, ins_src,
+void launch_topo_put(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
+                     const int *ins_rank, Counters *c) {
+  hipLaunchKernelGGL(k_topo_put, dim3(blocks_for(2LL * cap_arcs, 256)), dim3(256), 0, s, out, in, ins_src,
                      ins_dst, ins_rank, c);
-  hipLaunchKernelGGL(k_ins_finish, dim3(blocks_for(2LL * cap_arcs, 256)), dim3(256), 0, s, out, in, ins_src,
-                     ins_dst, ins_rank, ddeg, c);
 }
 
 void launch_cleanup(hipStream_t s, int B, int cap_arcs, const ripple_op *ops, const int *op_slot, u64 *ht_key,
-                    int *ht_val, int *fop, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                    const int *del_src, const int *del_dst, int *ddeg, const Counters *c) {
+                    int *ht_val, int *ht_net, int *fop, Adj out, Adj in, const int *ins_src, const int *ins_dst,
+                    const int *del_src, const int *del_dst, int *ddeg, const Counters *c, Counters *next,
+                    Counters *host) {
   const long long items = 2LL * cap_arcs > B ? 2LL * cap_arcs : B;
   hipLaunchKernelGGL(k_cleanup, dim3(blocks_for(items, 256)), dim3(256), 0, s, B, ops, op_slot, ht_key, ht_val,
-                     fop, out, in, ins_src, ins_dst, del_src, del_dst, ddeg, c);
+                     ht_net, fop, out, in, ins_src, ins_dst, del_src, del_dst, ddeg, c, next, host);
 }
-
-}  // namespace rp
-
-namespace rp {
-
-namespace {
-
-// Re-layout: row u's used entries move from old_col[old_off[u]..] to new_col[new_off[u]..].
-__global__ void k_repack_copy(long long n, const int *old_col, const long long *old_off, const int *len,
-                              int *new_col, const long long *new_off) {
-  const int lane = threadIdx.x & (kWave - 1);
-  const long long nw = static_cast<long long>(gridDim.x) * blockDim.x / kWave;
-  for (long long u = (static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x) / kWave; u < n; u += nw) {
-    const int *src = old_col + old_off[u];
-    int *dst = new_col + new_off[u];
-    const int l = len[u];
-    for (int e = lane; e < l; e += kWave) dst[e] = src[e];
-  }
-}
-
-}  // namespace
 
 void launch_repack_copy(hipStream_t s, long long n, const int *old_col, const long long *old_off, const int *len,
                         int *new_col, const long long *new_off) {
-  long long blocks = (n * kWave + 255) / 256;
-  if (blocks > 8192) blocks = 8192;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_repack_copy, dim3(blocks), dim3(256), 0, s, n, old_col, old_off, len, new_col, new_off);
+  hipLaunchKernelGGL(k_repack_copy, dim3(blocks_for(n * kWave, 256, 8192)), dim3(256), 0, s, n, old_col, old_off,
+                     len, new_col, new_off);
 }
 
 }  // namespace rp

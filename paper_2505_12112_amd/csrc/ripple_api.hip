@@ -72,9 +72,12 @@ struct ripple_ctx {
   unsigned *bm_out = nullptr;
   unsigned *bm_x = nullptr;
   int *blocksum = nullptr;
+  long long *blockdeg = nullptr;
   int *lists[rp::kMaxL + 1] = {};
+  long long *doff[rp::kMaxL + 1] = {};  // out-degree prefix of lists[l] (first arc index per vertex)
   float *delta[2] = {nullptr, nullptr};
-  rp::Counters *d_counters = nullptr;
+  rp::Counters *d_counters = nullptr;  // two buffers; batch parity picks one
+  int parity = 0;
   rp::Persist *d_persist = nullptr;
   rp::Counters *h_counters = nullptr;  // pinned
 
@@ -83,15 +86,14 @@ struct ripple_ctx {
   long long cap_feat_rows = 0;
   ripple_op *d_ops = nullptr;
   ripple_op *h_ops = nullptr;  // pinned
-  float *d_feat = nullptr;
   float *h_feat = nullptr;     // pinned
   u64 *ht_key = nullptr;
   int *ht_val = nullptr;
+  int *ht_net = nullptr;
   unsigned ht_mask = 0;
   int *op_slot = nullptr;
   int *ins_src = nullptr, *ins_dst = nullptr, *del_src = nullptr, *del_dst = nullptr;
-  int *ins_rank = nullptr, *del_rank = nullptr, *del_pos = nullptr;
-  rp::RelocItem *reloc = nullptr;
+  int *ins_rank = nullptr, *del_rank = nullptr;
   int *flist = nullptr;
 
   // last batch
@@ -99,7 +101,8 @@ struct ripple_ctx {
   long long last_count[rp::kMaxL + 1] = {};
   long long last_nfeat = 0;
 
-  // profiling
+  // profiling: bit p of prof_mask records phase p
+  unsigned prof_mask = 0;
   bool prof = false;
   std::vector<hipEvent_t> ev_pool;
   size_t ev_used = 0;
@@ -222,7 +225,6 @@ ripple_status upload_adj(ripple_ctx *c, int dir, const std::vector<int> &len, co
   RP_TRY(dalloc_n(c, &a.col, capacity));
   RP_TRY(dalloc_n(c, &a.inscnt, n));
   RP_TRY(dalloc_n(c, &a.delcnt, n));
-  RP_TRY(dalloc_n(c, &a.fillcnt, n));
   RP_HIP(c, hipMemcpyAsync(a.off, off.data(), n * sizeof(long long), hipMemcpyHostToDevice, c->stream));
   RP_HIP(c, hipMemcpyAsync(a.len, len.data(), n * sizeof(int), hipMemcpyHostToDevice, c->stream));
   RP_HIP(c, hipMemcpyAsync(a.cap, cap.data(), n * sizeof(int), hipMemcpyHostToDevice, c->stream));
@@ -231,7 +233,6 @@ ripple_status upload_adj(ripple_ctx *c, int dir, const std::vector<int> &len, co
   rp::launch_fill_i32(c->stream, a.col + total, arena, -1);
   RP_HIP(c, hipMemsetAsync(a.inscnt, 0, n * sizeof(int), c->stream));
   RP_HIP(c, hipMemsetAsync(a.delcnt, 0, n * sizeof(int), c->stream));
-  RP_HIP(c, hipMemsetAsync(a.fillcnt, 0, n * sizeof(int), c->stream));
   u64 top = static_cast<u64>(total);
   RP_HIP(c, hipMemcpyAsync(&c->d_persist->top[dir], &top, sizeof(u64), hipMemcpyHostToDevice, c->stream));
   RP_HIP(c, hipStreamSynchronize(c->stream));
@@ -279,9 +280,9 @@ ripple_status repack_adj(ripple_ctx *c, int dir) {
 
 void free_batch_scratch(ripple_ctx *c) {
   dfree_t(c, c->d_ops);
-  dfree_t(c, c->d_feat);
   dfree_t(c, c->ht_key);
   dfree_t(c, c->ht_val);
+  dfree_t(c, c->ht_net);
   dfree_t(c, c->op_slot);
   dfree_t(c, c->ins_src);
   dfree_t(c, c->ins_dst);
@@ -289,8 +290,6 @@ void free_batch_scratch(ripple_ctx *c) {
   dfree_t(c, c->del_dst);
   dfree_t(c, c->ins_rank);
   dfree_t(c, c->del_rank);
-  dfree_t(c, c->del_pos);
-  dfree_t(c, c->reloc);
   dfree_t(c, c->flist);
   if (c->h_ops) (void)hipHostFree(c->h_ops);
   if (c->h_feat) (void)hipHostFree(c->h_feat);
@@ -312,9 +311,9 @@ ripple_status ensure_batch_scratch(ripple_ctx *c, long long ops, long long frows
   unsigned ht = 64;
   while (ht < 4 * static_cast<unsigned long long>(cap)) ht <<= 1;
   RP_TRY(dalloc_n(c, &c->d_ops, cap));
-  RP_TRY(dalloc_n(c, &c->d_feat, fcap * c->dims[0]));
   RP_TRY(dalloc_n(c, &c->ht_key, ht));
   RP_TRY(dalloc_n(c, &c->ht_val, ht));
+  RP_TRY(dalloc_n(c, &c->ht_net, ht));
   RP_TRY(dalloc_n(c, &c->op_slot, cap));
   RP_TRY(dalloc_n(c, &c->ins_src, arcs));
   RP_TRY(dalloc_n(c, &c->ins_dst, arcs));
@@ -322,14 +321,13 @@ ripple_status ensure_batch_scratch(ripple_ctx *c, long long ops, long long frows
   RP_TRY(dalloc_n(c, &c->del_dst, arcs));
   RP_TRY(dalloc_n(c, &c->ins_rank, 2 * arcs));
   RP_TRY(dalloc_n(c, &c->del_rank, 2 * arcs));
-  RP_TRY(dalloc_n(c, &c->del_pos, 2 * arcs));
-  RP_TRY(dalloc_n(c, &c->reloc, 2 * arcs));
   RP_TRY(dalloc_n(c, &c->flist, cap));
   RP_HIP(c, hipHostMalloc(reinterpret_cast<void **>(&c->h_ops), cap * sizeof(ripple_op), hipHostMallocDefault));
   RP_HIP(c, hipHostMalloc(reinterpret_cast<void **>(&c->h_feat), fcap * c->dims[0] * sizeof(float),
                           hipHostMallocDefault));
   rp::launch_fill_u64(c->stream, c->ht_key, ht, rp::kEmptyKey);
   rp::launch_fill_i32(c->stream, c->ht_val, ht, -1);
+  rp::launch_fill_i32(c->stream, c->ht_net, ht, 0);
   RP_HIP(c, hipGetLastError());
   RP_HIP(c, hipStreamSynchronize(c->stream));
   c->ht_mask = ht - 1;
@@ -347,6 +345,7 @@ void free_model(ripple_ctx *c) {
     dfree_t(c, c->H[l]);
     dfree_t(c, c->S[l]);
     dfree_t(c, c->lists[l]);
+    dfree_t(c, c->doff[l]);
   }
   dfree_t(c, c->delta[0]);
   dfree_t(c, c->delta[1]);
@@ -405,20 +404,22 @@ struct PhaseScope {
   int phase;
   hipEvent_t a = nullptr;
   PhaseScope(ripple_ctx *cc, int ph) : c(cc), phase(ph) {
-    if (c->prof) {
+    if (c->prof && (c->prof_mask >> ph & 1u)) {
       a = next_event(c);
       if (a) (void)hipEventRecord(a, c->stream);
     }
   }
-  ~PhaseScope() {
-    if (c->prof && a) {
+  void close() {
+    if (a) {
       hipEvent_t b = next_event(c);
       if (b) {
         (void)hipEventRecord(b, c->stream);
         c->ev_log.push_back(PhaseEv{phase, a, b});
       }
+      a = nullptr;
     }
   }
+  ~PhaseScope() { close(); }
 };
 
 void add_launches(ripple_ctx *c, int phase, int k) {
@@ -428,38 +429,36 @@ void add_launches(ripple_ctx *c, int phase, int k) {
 // Issues one batch. Returns after queuing; the caller syncs.
 void issue_batch(ripple_ctx *c, int B) {
   hipStream_t s = c->stream;
-  rp::Counters *dc = c->d_counters;
-  const int gcn = c->agg == rp::kGcn;
+  rp::Counters *dc = c->d_counters + c->parity;  // zeroed by the previous batch's clean-up
+  rp::Counters *dnext = c->d_counters + (c->parity ^ 1);
   const int cap_arcs = static_cast<int>(2 * c->cap_ops);
   rp::Adj out = c->adj[0], in = c->adj[1];
-  (void)hipMemsetAsync(dc, 0, sizeof(rp::Counters), s);
+  PhaseScope total(c, RIPPLE_PHASE_TOTAL);
   {
     PhaseScope ps(c, RIPPLE_PHASE_NET);
-    rp::launch_net_hash(s, c->d_ops, B, c->undirected, c->n, c->ht_key, c->ht_val, c->ht_mask, c->op_slot, c->fop,
-                        dc);
-    rp::launch_net_decide(s, c->d_ops, B, c->undirected, c->ht_val, c->op_slot, c->fop, out, in, c->ins_src,
-                          c->ins_dst, c->del_src, c->del_dst, c->flist, dc);
+    rp::launch_net_hash(s, c->h_ops, c->d_ops, B, c->undirected, c->n, c->ht_key, c->ht_val, c->ht_mask,
+                        c->op_slot, c->fop, dc);
+    rp::launch_net_decide(s, c->d_ops, B, c->undirected, c->ht_val, c->ht_net, c->op_slot, c->fop, out, in,
+                          c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank, c->del_rank, c->flist, dc);
     add_launches(c, RIPPLE_PHASE_NET, 2);
   }
   {
     PhaseScope ps(c, RIPPLE_PHASE_TOPO);
-    rp::launch_topo_count(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank,
-                          c->del_rank, dc);
-    rp::launch_topo_plan(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->ins_rank, c->reloc, dc);
-    rp::launch_topo_check(s, dc, c->d_persist, c->col_capacity[0], c->col_capacity[1]);
-    rp::launch_corrections(s, cap_arcs, c->agg, layer_ptrs(c), c->adj[0].len, c->ins_src, c->ins_dst, c->del_src,
-                           c->del_dst, dc);
-    rp::launch_del_apply(s, cap_arcs, out, in, c->del_src, c->del_dst, c->del_rank, c->del_pos, c->ddeg, dc);
-    rp::launch_reloc(s, 2 * cap_arcs, out, in, c->reloc, c->d_persist, dc);
-    rp::launch_ins_apply(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->ins_rank, c->ddeg, dc);
-    add_launches(c, RIPPLE_PHASE_TOPO, 10);
+    rp::launch_topo_plan(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->ins_rank, dc, c->d_persist,
+                         c->col_capacity[0], c->col_capacity[1]);
+    rp::launch_topo_rewrite(s, cap_arcs, c->undirected, c->n, out, in, c->ins_src, c->ins_dst, c->del_src,
+                            c->del_dst, c->ins_rank, c->del_rank, c->ht_key, c->ht_net, c->ht_mask, c->d_persist,
+                            c->ddeg, dc);
+    rp::launch_topo_put(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->ins_rank, dc);
+    add_launches(c, RIPPLE_PHASE_TOPO, 3);
   }
   {
     PhaseScope ps(c, RIPPLE_PHASE_LAYER0);
-    rp::launch_mark_dirty0(s, static_cast<int>(c->cap_ops), cap_arcs, gcn, c->flist, c->ins_src, c->del_src, c->ddeg,
-                           c->bm_x, dc);
-    rp::launch_compact(s, c->n, c->bm_out, c->bm_x, c->blocksum, c->lists[0], &dc->count[0]);
-    rp::launch_delta0(s, c->n, c->agg, c->dims[0], c->lists[0], &dc->count[0], c->d_ops, c->d_feat, c->fop,
+    rp::launch_corr_mark(s, static_cast<int>(c->cap_ops), cap_arcs, c->agg, layer_ptrs(c), c->adj[0].len, c->ddeg,
+                         c->flist, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->bm_x, dc);
+    rp::launch_compact(s, c->n, c->bm_out, c->bm_x, c->blocksum, c->blockdeg, c->adj[0].len, c->lists[0],
+                       c->doff[0], &dc->count[0]);
+    rp::launch_delta0(s, c->n, c->agg, c->dims[0], c->lists[0], &dc->count[0], c->d_ops, c->h_feat, c->fop,
                       c->H[0], c->adj[0].len, c->ddeg, c->delta[0], dc);
     add_launches(c, RIPPLE_PHASE_LAYER0, 4);
   }
@@ -468,42 +467,40 @@ void issue_batch(ripple_ctx *c, int B) {
     float *dout = l < c->L ? c->delta[l & 1] : nullptr;
     {
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
-      rp::launch_scatter(s, c->n, c->dims[l - 1], c->lists[l - 1], &dc->count[l - 1], din, out, c->S[l], c->bm_out,
-                         c->bm_x, c->ins_dst, c->del_dst, cap_arcs, &dc->pushed[l], &dc->dest[l], dc);
+      rp::launch_scatter(s, c->n, c->dims[l - 1], c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], din, out,
+                         c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], &dc->dest[l], dc);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     {
       PhaseScope ps(c, RIPPLE_PHASE_COMPACT);
-      rp::launch_compact(s, c->n, c->bm_out, c->bm_x, c->blocksum, c->lists[l], &dc->count[l]);
+      rp::launch_compact(s, c->n, c->bm_out, c->bm_x, c->blocksum, c->blockdeg, l < c->L ? c->adj[0].len : nullptr,
+                         c->lists[l], c->doff[l], &dc->count[l]);
       add_launches(c, RIPPLE_PHASE_COMPACT, 2);
     }
     {
       PhaseScope ps(c, RIPPLE_PHASE_GEMM);
-      rp::launch_gemm(s, gemm_args(c, l, c->lists[l], &dc->count[l], 0, dout), c->n);
+      rp::launch_gemm(s, gemm_args(c, l, c->lists[l], &dc->count[l], 0, dout), c->n,
+                      c->has_batch ? c->last_count[l] : 0);
       add_launches(c, RIPPLE_PHASE_GEMM, 1);
     }
   }
   {
     PhaseScope ps(c, RIPPLE_PHASE_OTHER);
-    rp::launch_cleanup(s, B, cap_arcs, c->d_ops, c->op_slot, c->ht_key, c->ht_val, c->fop, out, in, c->ins_src,
-                       c->ins_dst, c->del_src, c->del_dst, c->ddeg, dc);
+    rp::launch_cleanup(s, B, cap_arcs, c->d_ops, c->op_slot, c->ht_key, c->ht_val, c->ht_net, c->fop, out, in,
+                       c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ddeg, dc, dnext, c->h_counters);
     add_launches(c, RIPPLE_PHASE_OTHER, 1);
   }
-  (void)hipMemcpyAsync(c->h_counters, dc, sizeof(rp::Counters), hipMemcpyDeviceToHost, s);
+  total.close();
+  c->parity ^= 1;
 }
 
 void account_phases(ripple_ctx *c) {
   if (!c->prof) return;
   const rp::Counters &k = *c->h_counters;
-  float total = 0.0f;
-  hipEvent_t first = nullptr, last = nullptr;
   for (const PhaseEv &p : c->ev_log) {
     float ms = 0.0f;
     if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) c->ph_ms[p.phase] += ms;
-    if (!first) first = p.a;
-    last = p.b;
   }
-  if (first && last && hipEventElapsedTime(&total, first, last) == hipSuccess) c->ph_ms[RIPPLE_PHASE_TOTAL] += total;
   c->ph_launch[RIPPLE_PHASE_TOTAL] += 1;
   const double words = static_cast<double>((c->n + 31) / 32);
   for (int l = 1; l <= c->L; ++l) {
@@ -673,7 +670,7 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   }
   ripple_status st;
   if ((st = dalloc_n(c, &c->d_persist, 1)) != RIPPLE_OK) return bail(st);
-  if ((st = dalloc_n(c, &c->d_counters, 1)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->d_counters, 2)) != RIPPLE_OK) return bail(st);
   e = hipHostMalloc(reinterpret_cast<void **>(&c->h_counters), sizeof(rp::Counters), hipHostMallocDefault);
   if (e != hipSuccess) return bail(device_fail(c, e, "hipHostMalloc"));
   std::vector<int> olen(outdeg), ilen(indeg);
@@ -686,10 +683,12 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   if ((st = dalloc_n(c, &c->bm_out, words)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->bm_x, words)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->blocksum, rp::compact_blocks(n) + 1)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->blockdeg, rp::compact_blocks(n) + 1)) != RIPPLE_OK) return bail(st);
   rp::launch_fill_i32(c->stream, c->fop, n, -1);
   e = hipMemsetAsync(c->ddeg, 0, n * sizeof(int), c->stream);
   if (e == hipSuccess) e = hipMemsetAsync(c->bm_out, 0, words * sizeof(unsigned), c->stream);
   if (e == hipSuccess) e = hipMemsetAsync(c->bm_x, 0, words * sizeof(unsigned), c->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(c->d_counters, 0, 2 * sizeof(rp::Counters), c->stream);
   if (e == hipSuccess) e = hipGetLastError();
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return bail(device_fail(c, e, "load_graph init"));
@@ -750,6 +749,7 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   for (int l = 0; l <= L; ++l) {
     RP_TRY(dalloc_n(c, &c->H[l], n * c->dims[l]));
     RP_TRY(dalloc_n(c, &c->lists[l], n));
+    RP_TRY(dalloc_n(c, &c->doff[l], n + 1));
     if (l >= 1) RP_TRY(dalloc_n(c, &c->S[l], n * c->dims[l - 1]));
   }
   RP_TRY(dalloc_n(c, &c->delta[0], n * c->dmax_delta));
@@ -759,7 +759,7 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   // bootstrap: layer-wise full forward pass (pull aggregate over in-rows, then transform)
   for (int l = 1; l <= L; ++l) {
     rp::launch_pull(c->stream, n, c->dims[l - 1], c->agg, c->H[l - 1], c->adj[1], c->adj[0].len, c->S[l]);
-    rp::launch_gemm(c->stream, gemm_args(c, l, nullptr, nullptr, n, nullptr), n);
+    rp::launch_gemm(c->stream, gemm_args(c, l, nullptr, nullptr, n, nullptr), n, n);
     RP_HIP(c, hipGetLastError());
   }
   RP_HIP(c, hipStreamSynchronize(c->stream));
@@ -778,17 +778,12 @@ ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t 
   if (num_feat_rows > 0 && feat_rows == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: feat_rows is NULL");
   if (!validate_ops(c, ops, num_ops, num_feat_rows)) return RIPPLE_E_INVALID;
   RP_TRY(ensure_batch_scratch(c, num_ops, num_feat_rows));
+  // the kernels read the batch straight from these pinned buffers (the previous
+  // call has synchronised, so nothing still reads them)
   const int B = static_cast<int>(num_ops);
-  if (B > 0) {
-    std::memcpy(c->h_ops, ops, static_cast<size_t>(B) * sizeof(ripple_op));
-    RP_HIP(c, hipMemcpyAsync(c->d_ops, c->h_ops, static_cast<size_t>(B) * sizeof(ripple_op), hipMemcpyHostToDevice,
-                             c->stream));
-  }
-  if (num_feat_rows > 0) {
-    const size_t fb = static_cast<size_t>(num_feat_rows) * c->dims[0] * sizeof(float);
-    std::memcpy(c->h_feat, feat_rows, fb);
-    RP_HIP(c, hipMemcpyAsync(c->d_feat, c->h_feat, fb, hipMemcpyHostToDevice, c->stream));
-  }
+  if (B > 0) std::memcpy(c->h_ops, ops, static_cast<size_t>(B) * sizeof(ripple_op));
+  if (num_feat_rows > 0)
+    std::memcpy(c->h_feat, feat_rows, static_cast<size_t>(num_feat_rows) * c->dims[0] * sizeof(float));
   long long repacks = 0;
   for (int attempt = 0;; ++attempt) {
     issue_batch(c, B);
@@ -809,7 +804,7 @@ ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t 
   const rp::Counters &k = *c->h_counters;
   if (k.err) {
     c->poisoned = true;
-    return fail(c, RIPPLE_E_DEVICE, "ripple: device adjacency inconsistent (deleted arc not found)");
+    return fail(c, RIPPLE_E_DEVICE, "ripple: device adjacency inconsistent (err bits " + std::to_string(k.err) + ")");
   }
   account_phases(c);
   c->has_batch = true;
@@ -918,9 +913,10 @@ ripple_status ripple_device_bytes(ripple_ctx *c, int64_t *bytes) {
   return RIPPLE_OK;
 }
 
-ripple_status ripple_set_profiling(ripple_ctx *c, int32_t enable) {
+ripple_status ripple_set_profiling(ripple_ctx *c, int32_t mask) {
   RP_TRY(check_ctx(c));
-  c->prof = enable != 0;
+  c->prof_mask = static_cast<unsigned>(mask) & ((1u << RIPPLE_NUM_PHASES) - 1u);
+  c->prof = c->prof_mask != 0;
   c->ev_log.clear();
   c->ev_used = 0;
   return RIPPLE_OK;
@@ -969,13 +965,13 @@ void ripple_destroy(ripple_ctx *c) {
     dfree_t(c, c->adj[d].col);
     dfree_t(c, c->adj[d].inscnt);
     dfree_t(c, c->adj[d].delcnt);
-    dfree_t(c, c->adj[d].fillcnt);
   }
   dfree_t(c, c->fop);
   dfree_t(c, c->ddeg);
   dfree_t(c, c->bm_out);
   dfree_t(c, c->bm_x);
   dfree_t(c, c->blocksum);
+  dfree_t(c, c->blockdeg);
   dfree_t(c, c->d_counters);
   dfree_t(c, c->d_persist);
   if (c->h_counters) (void)hipHostFree(c->h_counters);

@@ -268,8 +268,12 @@ class Ripple:
         self._check(self._lib.ripple_device_bytes(self._ctx, C.byref(b)))
         return b.value
 
-    def set_profiling(self, enable: bool):
-        self._check(self._lib.ripple_set_profiling(self._ctx, 1 if enable else 0))
+    def set_profiling(self, phases=()):
+        """Records HIP events around the named phases (see PHASES); () turns it off."""
+        mask = 0
+        for p in phases:
+            mask |= 1 << PHASES.index(p)
+        self._check(self._lib.ripple_set_profiling(self._ctx, mask))
 
     def phase_stats(self) -> Dict[str, Dict[str, float]]:
         arr = (PhaseStats * NUM_PHASES)()
