@@ -18,6 +18,7 @@ stream on this host.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import statistics
@@ -137,6 +138,11 @@ def main():
     lat = []
     aff = np.zeros(L + 1)
     pushed = np.zeros(L + 1)
+    repacks = relocated = 0
+    # the Python collector stays out of the timed region (a full collection with
+    # torch loaded takes tens of milliseconds and is not the library's work)
+    gc.collect()
+    gc.disable()
     torch.cuda.synchronize()
     t_region = time.perf_counter()
     for ops, fr in prepared[W:]:
@@ -145,8 +151,11 @@ def main():
         lat.append(time.perf_counter() - t1)
         aff += np.array(st.affected[:L + 1], dtype=np.float64)
         pushed += np.array(st.pushed_arcs[:L + 1], dtype=np.float64)
+        repacks += st.repacks
+        relocated += st.relocated_rows
     torch.cuda.synchronize()
     region_s = time.perf_counter() - t_region
+    gc.enable()
     ph = lib.phase_stats()
     lib.set_profiling(())
     log(f"[bench] {K} timed batches in {region_s:.3f}s")
@@ -222,6 +231,9 @@ def main():
         "cpu_baseline": cpu,
         "frontier_mean": {"affected": (aff / K).tolist(), "pushed_arcs": (pushed / K).tolist(),
                           "affected_frac": (aff / K / wl.n).tolist()},
+        "adjacency": {"rows_moved": int(relocated), "relayouts": int(repacks)},
+        "max_latency_ms": 1000 * max(lat),
+        "max_latency_batch": int(np.argmax(lat)),
         "phase_ms_per_batch": {k: v["ms"] / nb for k, v in breakdown.items()},
         "bootstrap_s": init_s,
         "device_gib": lib.device_bytes() / 2**30,

@@ -101,6 +101,10 @@ typedef struct {
   int32_t device;         /* HIP device ordinal */
   void *stream;           /* hipStream_t to run on, or NULL for a library-owned stream */
   int64_t max_device_bytes; /* 0 = no cap; else allocations beyond it fail with RIPPLE_E_OOM */
+  int64_t arena_slots;    /* spare slots per direction for rows that outgrow their own;
+                             0 = max(65536, half the laid-out slots). When the arena runs out,
+                             the direction is re-laid out (on the device if the fresh layout
+                             leaves a quarter of its buffer free, else into larger buffers). */
 } ripple_graph_desc;
 
 /* Trained model (Sec. IV-A: a trained L-layer GNN with a linear aggregator). */

@@ -167,8 +167,9 @@ class NetEffect:
 
 
 def apply_batch(graph: OracleGraph, x: np.ndarray, ops: np.ndarray,
-                feat_rows: np.ndarray) -> Tuple[OracleGraph, np.ndarray, NetEffect]:
-    """Applies `ops` in order to (graph, x) and returns (graph', x', net effect).
+                feat_rows: np.ndarray, inplace: bool = False) -> Tuple[OracleGraph, np.ndarray, NetEffect]:
+    """Applies `ops` in order to (graph, x) and returns (graph', x', net effect);
+    with inplace=True the feature matrix x itself is updated and returned.
 
     An insert sets an arc present and a delete sets it absent, so the final
     state of an arc is fixed by the last op naming it; comparing with the
@@ -176,7 +177,7 @@ def apply_batch(graph: OracleGraph, x: np.ndarray, ops: np.ndarray,
     each edge op to both arcs and count the unordered edge once."""
     n = graph.n
     ops = np.asarray(ops)
-    x_new = np.array(x, copy=True)
+    x_new = x if inplace else np.array(x, copy=True)
     final: Dict[Tuple[int, int], bool] = {}
     feat_vertices = set()
     selfloops = 0
@@ -210,9 +211,10 @@ def apply_batch(graph: OracleGraph, x: np.ndarray, ops: np.ndarray,
     g2 = graph.copy()
     keep = g2.keys
     if dels.size:
-        keep = np.setdiff1d(keep, dels[:, 0] * n + dels[:, 1], assume_unique=True)
+        keep = np.delete(keep, np.searchsorted(keep, dels[:, 0] * n + dels[:, 1]))
     if ins.size:
-        keep = np.union1d(keep, ins[:, 0] * n + ins[:, 1])
+        new_keys = np.sort(ins[:, 0] * n + ins[:, 1])
+        keep = np.insert(keep, np.searchsorted(keep, new_keys), new_keys)
     g2.keys = keep
     ch = np.concatenate([ins, dels]) if (ins.size or dels.size) else np.empty((0, 2), np.int64)
     od_change = np.zeros(n, np.int64)
@@ -372,10 +374,10 @@ class OracleState:
         self.x = np.asarray(x, np.float64).copy()
         self.model = model
 
-    def apply(self, ops, feat_rows):
-        g2, x2, net = apply_batch(self.graph, self.x, ops, np.asarray(feat_rows, np.float64))
+    def apply(self, ops, feat_rows, with_sets: bool = True):
+        g2, x2, net = apply_batch(self.graph, self.x, ops, np.asarray(feat_rows, np.float64), inplace=True)
         self.graph, self.x = g2, x2
-        sets = affected_sets(g2, net, self.model.agg, self.model.num_layers)
+        sets = affected_sets(g2, net, self.model.agg, self.model.num_layers) if with_sets else None
         return net, sets
 
     def embeddings(self, dtype=np.float64) -> List[np.ndarray]:

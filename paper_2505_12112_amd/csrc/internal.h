@@ -158,6 +158,18 @@ void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows, long long
 void launch_repack_copy(hipStream_t s, long long n, const int *old_col, const long long *old_off, const int *len,
                         int *new_col, const long long *new_off);
 
+// Device-side re-layout of one direction. relayout_sums leaves in blocksums[nb]
+// (nb = relayout_blocks(n)) the total slots a fresh layout needs (len + spare
+// slots per row); once the caller has checked that total + arena fits new_col,
+// relayout_apply writes the new offsets/capacities (scratch new_off[n],
+// new_cap[n]), copies the rows into new_col, installs the row table and sets the
+// arena top. The caller then swaps a.col and new_col.
+int relayout_blocks(long long n);
+void launch_relayout_sums(hipStream_t s, long long n, float slack, int min_slack, const int *len,
+                          long long *blocksums);
+void launch_relayout_apply(hipStream_t s, long long n, float slack, int min_slack, Adj a, int *new_col,
+                           const long long *blocksums, long long *new_off, int *new_cap, u64 *top);
+
 // utilities
 void launch_fill_i32(hipStream_t s, int *p, long long count, int value);
 void launch_fill_u64(hipStream_t s, u64 *p, long long count, u64 value);

@@ -389,3 +389,135 @@ void launch_repack_copy(hipStream_t s, long long n, const int *old_col, const lo
 }
 
 }  // namespace rp
+
+// Device-side re-layout of one adjacency direction: new capacities from the
+// current lengths, an exclusive scan for the new offsets, the rows copied into
+// the spare column buffer, then the row table and the arena top updated.
+namespace rp {
+
+namespace {
+
+constexpr int kScanThreads = 1024;
+constexpr int kScanPerThread = 4;
+constexpr int kScanPerBlock = kScanThreads * kScanPerThread;
+
+__device__ inline long long block_scan_excl(long long v, long long *lds, long long *total) {
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  constexpr int waves = kScanThreads / kWave;
+  long long x = v;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const long long y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == kWave - 1) lds[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    long long run = 0;
+    for (int w = 0; w < waves; ++w) {
+      const long long t = lds[w];
+      lds[w] = run;
+      run += t;
+    }
+    lds[waves] = run;
+  }
+  __syncthreads();
+  const long long excl = x - v + lds[wave];
+  *total = lds[waves];
+  __syncthreads();
+  return excl;
+}
+
+__device__ inline int relayout_cap(int len, float slack, int min_slack) {
+  long long extra = static_cast<long long>(ceilf(static_cast<float>(len) * slack));
+  if (extra < min_slack) extra = min_slack;
+  return static_cast<int>(len + extra);
+}
+
+// pass 1: per-block sums of the new capacities
+__global__ __launch_bounds__(kScanThreads) void k_relayout_sums(long long n, const int *len, float slack,
+                                                                int min_slack, long long *blocksums) {
+  __shared__ long long lds[kScanThreads / kWave + 1];
+  long long s = 0;
+  const long long base = static_cast<long long>(blockIdx.x) * kScanPerBlock + threadIdx.x * kScanPerThread;
+  for (int i = 0; i < kScanPerThread; ++i)
+    if (base + i < n) s += relayout_cap(len[base + i], slack, min_slack);
+  long long total;
+  block_scan_excl(s, lds, &total);
+  if (threadIdx.x == 0) blocksums[blockIdx.x] = total;
+}
+
+// pass 2: one block scans the block sums in place (exclusive); total to blocksums[nb]
+__global__ __launch_bounds__(kScanThreads) void k_relayout_scan_sums(long long *blocksums, int nb) {
+  __shared__ long long lds[kScanThreads / kWave + 1];
+  long long carry = 0;
+  for (int base = 0; base < nb; base += kScanThreads) {
+    const int i = base + threadIdx.x;
+    const long long v = i < nb ? blocksums[i] : 0;
+    long long total;
+    const long long ex = block_scan_excl(v, lds, &total);
+    if (i < nb) blocksums[i] = carry + ex;
+    carry += total;
+  }
+  if (threadIdx.x == 0) blocksums[nb] = carry;
+}
+
+// pass 3: new offsets and capacities
+__global__ __launch_bounds__(kScanThreads) void k_relayout_offsets(long long n, const int *len, float slack,
+                                                                   int min_slack, const long long *blocksums,
+                                                                   long long *new_off, int *new_cap) {
+  __shared__ long long lds[kScanThreads / kWave + 1];
+  const long long base = static_cast<long long>(blockIdx.x) * kScanPerBlock + threadIdx.x * kScanPerThread;
+  int caps[kScanPerThread];
+  long long s = 0;
+  for (int i = 0; i < kScanPerThread; ++i) {
+    caps[i] = base + i < n ? relayout_cap(len[base + i], slack, min_slack) : 0;
+    s += caps[i];
+  }
+  long long total;
+  long long pos = blocksums[blockIdx.x] + block_scan_excl(s, lds, &total);
+  for (int i = 0; i < kScanPerThread; ++i) {
+    if (base + i < n) {
+      new_off[base + i] = pos;
+      new_cap[base + i] = caps[i];
+      pos += caps[i];
+    }
+  }
+}
+
+// pass 5: install the new row table and arena top
+__global__ void k_relayout_install(long long n, const long long *new_off, const int *new_cap, long long *off,
+                                   int *cap, const long long *blocksums, int nb, u64 *top) {
+  const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
+  for (long long u = blockIdx.x * blockDim.x + threadIdx.x; u < n; u += stride) {
+    off[u] = new_off[u];
+    cap[u] = new_cap[u];
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *top = static_cast<u64>(blocksums[nb]);
+}
+
+}  // namespace
+
+int relayout_blocks(long long n) { return static_cast<int>((n + kScanPerBlock - 1) / kScanPerBlock); }
+
+void launch_relayout_sums(hipStream_t s, long long n, float slack, int min_slack, const int *len,
+                          long long *blocksums) {
+  const int nb = relayout_blocks(n);
+  hipLaunchKernelGGL(k_relayout_sums, dim3(nb), dim3(kScanThreads), 0, s, n, len, slack, min_slack, blocksums);
+  hipLaunchKernelGGL(k_relayout_scan_sums, dim3(1), dim3(kScanThreads), 0, s, blocksums, nb);
+}
+
+void launch_relayout_apply(hipStream_t s, long long n, float slack, int min_slack, Adj a, int *new_col,
+                           const long long *blocksums, long long *new_off, int *new_cap, u64 *top) {
+  const int nb = relayout_blocks(n);
+  hipLaunchKernelGGL(k_relayout_offsets, dim3(nb), dim3(kScanThreads), 0, s, n, a.len, slack, min_slack, blocksums,
+                     new_off, new_cap);
+  hipLaunchKernelGGL(k_repack_copy, dim3(blocks_for(n * kWave, 256, 8192)), dim3(256), 0, s, n, a.col, a.off, a.len,
+                     new_col, new_off);
+  long long ib = (n + 255) / 256;
+  if (ib > 4096) ib = 4096;
+  hipLaunchKernelGGL(k_relayout_install, dim3(ib), dim3(256), 0, s, n, new_off, new_cap, a.off, a.cap, blocksums, nb,
+                     top);
+}
+
+}  // namespace rp

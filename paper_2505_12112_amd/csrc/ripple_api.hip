@@ -14,6 +14,7 @@
 // An aborted batch (arena too small) changes nothing; the host re-lays the
 // adjacency out with fresh spare slots and runs the batch again.
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -45,6 +46,7 @@ struct ripple_ctx {
   float slack = 0.25f;
   int min_slack = 4;
   long long max_bytes = 0;
+  long long arena_slots = 0;  // 0 = default sizing
   long long bytes = 0;
   std::unordered_map<void *, size_t> allocs;
   std::string err;
@@ -54,6 +56,10 @@ struct ripple_ctx {
   // adjacency: [0] out (CSR by source), [1] in (CSC by sink)
   rp::Adj adj[2] = {};
   long long col_capacity[2] = {0, 0};
+  int *col_alt[2] = {nullptr, nullptr};   // spare column buffer per direction (same capacity)
+  long long *rl_blocksums = nullptr;      // re-layout scratch
+  long long *rl_off = nullptr;
+  int *rl_cap = nullptr;
 
   // model
   int L = 0, agg = 0;
@@ -198,8 +204,12 @@ long long row_cap(int len, float slack, int min_slack) {
   return len + extra;
 }
 
+long long arena_for(const ripple_ctx *c, long long total) {
+  return c->arena_slots > 0 ? c->arena_slots : std::max<long long>(65536, total / 2);
+}
+
 // Uploads one adjacency direction laid out with spare slots per row and a spare
-// arena of max(65536, total / 2) slots at the end.
+// arena at the end.
 ripple_status upload_adj(ripple_ctx *c, int dir, const std::vector<int> &len, const std::vector<int> &col_packed,
                          const std::vector<long long> &packed_off) {
   const long long n = c->n;
@@ -213,7 +223,7 @@ ripple_status upload_adj(ripple_ctx *c, int dir, const std::vector<int> &len, co
     cap[u] = static_cast<int>(cp);
     total += cp;
   }
-  long long arena = std::max<long long>(65536, total / 2);
+  const long long arena = arena_for(c, total);
   const long long capacity = total + arena;
   std::vector<int> col(static_cast<size_t>(total), -1);
   for (long long u = 0; u < n; ++u)
@@ -223,6 +233,7 @@ ripple_status upload_adj(ripple_ctx *c, int dir, const std::vector<int> &len, co
   RP_TRY(dalloc_n(c, &a.len, n));
   RP_TRY(dalloc_n(c, &a.cap, n));
   RP_TRY(dalloc_n(c, &a.col, capacity));
+  RP_TRY(dalloc_n(c, &c->col_alt[dir], capacity));
   RP_TRY(dalloc_n(c, &a.inscnt, n));
   RP_TRY(dalloc_n(c, &a.delcnt, n));
   RP_HIP(c, hipMemcpyAsync(a.off, off.data(), n * sizeof(long long), hipMemcpyHostToDevice, c->stream));
@@ -240,8 +251,9 @@ ripple_status upload_adj(ripple_ctx *c, int dir, const std::vector<int> &len, co
   return RIPPLE_OK;
 }
 
-// Re-lays one direction out compactly with fresh spare slots (after the arena ran out).
-ripple_status repack_adj(ripple_ctx *c, int dir) {
+// Re-lays one direction out with fresh spare slots into new, larger buffers (when the
+// device re-layout would not leave room for the arena).
+ripple_status repack_adj_grow(ripple_ctx *c, int dir) {
   const long long n = c->n;
   rp::Adj &a = c->adj[dir];
   std::vector<int> len(n);
@@ -255,10 +267,12 @@ ripple_status repack_adj(ripple_ctx *c, int dir) {
     cap[u] = static_cast<int>(row_cap(len[u], c->slack, std::max(c->min_slack, 4)));
     total += cap[u];
   }
-  const long long arena = std::max<long long>(65536, total / 2);
+  const long long arena = arena_for(c, total);
   const long long capacity = total + arena;
   int *new_col = nullptr;
   long long *new_off = nullptr;
+  dfree_t(c, c->col_alt[dir]);
+  RP_TRY(dalloc_n(c, &c->col_alt[dir], capacity));
   RP_TRY(dalloc_n(c, &new_col, capacity));
   RP_TRY(dalloc_n(c, &new_off, n));
   RP_HIP(c, hipMemcpyAsync(new_off, off.data(), n * sizeof(long long), hipMemcpyHostToDevice, c->stream));
@@ -275,6 +289,26 @@ ripple_status repack_adj(ripple_ctx *c, int dir) {
   RP_HIP(c, hipMemcpyAsync(&c->d_persist->top[dir], &top, sizeof(u64), hipMemcpyHostToDevice, c->stream));
   RP_HIP(c, hipStreamSynchronize(c->stream));
   c->col_capacity[dir] = capacity;
+  return RIPPLE_OK;
+}
+
+// Re-lays one direction out with fresh spare slots (after the spare arena ran out):
+// on the device, into the spare column buffer, when the fresh layout leaves at
+// least a quarter of the buffer as arena; otherwise into new, larger buffers.
+ripple_status repack_adj(ripple_ctx *c, int dir) {
+  const long long n = c->n;
+  rp::Adj &a = c->adj[dir];
+  const int smin = std::max(c->min_slack, 4);
+  rp::launch_relayout_sums(c->stream, n, c->slack, smin, a.len, c->rl_blocksums);
+  long long total = 0;
+  RP_HIP(c, hipMemcpyAsync(&total, c->rl_blocksums + rp::relayout_blocks(n), sizeof(long long),
+                           hipMemcpyDeviceToHost, c->stream));
+  RP_HIP(c, hipStreamSynchronize(c->stream));
+  if (total + c->col_capacity[dir] / 4 > c->col_capacity[dir]) return repack_adj_grow(c, dir);
+  rp::launch_relayout_apply(c->stream, n, c->slack, smin, a, c->col_alt[dir], c->rl_blocksums, c->rl_off, c->rl_cap,
+                            &c->d_persist->top[dir]);
+  RP_HIP(c, hipGetLastError());
+  std::swap(a.col, c->col_alt[dir]);
   return RIPPLE_OK;
 }
 
@@ -364,8 +398,9 @@ rp::LayerPtrs layer_ptrs(const ripple_ctx *c) {
   return lp;
 }
 
+// abort: the current batch's abort flag (nullptr outside a batch).
 rp::GemmArgs gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 *count, long long count_fixed,
-                       float *delta) {
+                       float *delta, const u64 *abort) {
   rp::GemmArgs g{};
   g.rows = rows;
   g.count = count;
@@ -384,7 +419,7 @@ rp::GemmArgs gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 *c
   g.H = c->H[l];
   g.delta = delta;
   g.agg = c->agg;
-  g.abort = count != nullptr ? &c->d_counters->abort : nullptr;
+  g.abort = abort;
   return g;
 }
 
@@ -479,7 +514,7 @@ void issue_batch(ripple_ctx *c, int B) {
     }
     {
       PhaseScope ps(c, RIPPLE_PHASE_GEMM);
-      rp::launch_gemm(s, gemm_args(c, l, c->lists[l], &dc->count[l], 0, dout), c->n,
+      rp::launch_gemm(s, gemm_args(c, l, c->lists[l], &dc->count[l], 0, dout, &dc->abort), c->n,
                       c->has_batch ? c->last_count[l] : 0);
       add_launches(c, RIPPLE_PHASE_GEMM, 1);
     }
@@ -515,6 +550,21 @@ void account_phases(ripple_ctx *c) {
   }
   c->ev_log.clear();
   c->ev_used = 0;
+}
+
+// Waits for the batch: polls the stream for up to ~20 ms (a batch usually takes
+// well under a millisecond, and polling keeps the thread from being descheduled
+// while it waits), then blocks.
+ripple_status wait_stream(ripple_ctx *c) {
+  const auto t0 = std::chrono::steady_clock::now();
+  while (true) {
+    const hipError_t e = hipStreamQuery(c->stream);
+    if (e == hipSuccess) return RIPPLE_OK;
+    if (e != hipErrorNotReady) return device_fail(c, e, "hipStreamQuery");
+    if (std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(20)) break;
+  }
+  RP_HIP(c, hipStreamSynchronize(c->stream));
+  return RIPPLE_OK;
 }
 
 bool validate_ops(ripple_ctx *c, const ripple_op *ops, long long num_ops, long long num_feat_rows) {
@@ -601,7 +651,7 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
     c->err = "ripple: bad edge arrays";
     return bail(RIPPLE_E_INVALID);
   }
-  if (!(g->slack >= 0.0f) || g->min_slack < 0) {
+  if (!(g->slack >= 0.0f) || g->min_slack < 0 || g->arena_slots < 0) {
     c->err = "ripple: slack must be >= 0";
     return bail(RIPPLE_E_INVALID);
   }
@@ -611,6 +661,7 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   c->min_slack = g->min_slack;
   c->device = g->device;
   c->max_bytes = g->max_device_bytes;
+  c->arena_slots = g->arena_slots;
   // host-side validation and counting sort into CSR (by source) and CSC (by sink)
   const long long arcs = c->undirected ? 2 * m : m;
   std::vector<int> outdeg(n, 0), indeg(n, 0);
@@ -684,6 +735,9 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   if ((st = dalloc_n(c, &c->bm_x, words)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->blocksum, rp::compact_blocks(n) + 1)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->blockdeg, rp::compact_blocks(n) + 1)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->rl_blocksums, rp::relayout_blocks(n) + 1)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->rl_off, n)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->rl_cap, n)) != RIPPLE_OK) return bail(st);
   rp::launch_fill_i32(c->stream, c->fop, n, -1);
   e = hipMemsetAsync(c->ddeg, 0, n * sizeof(int), c->stream);
   if (e == hipSuccess) e = hipMemsetAsync(c->bm_out, 0, words * sizeof(unsigned), c->stream);
@@ -759,7 +813,7 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   // bootstrap: layer-wise full forward pass (pull aggregate over in-rows, then transform)
   for (int l = 1; l <= L; ++l) {
     rp::launch_pull(c->stream, n, c->dims[l - 1], c->agg, c->H[l - 1], c->adj[1], c->adj[0].len, c->S[l]);
-    rp::launch_gemm(c->stream, gemm_args(c, l, nullptr, nullptr, n, nullptr), n, n);
+    rp::launch_gemm(c->stream, gemm_args(c, l, nullptr, nullptr, n, nullptr, nullptr), n, n);
     RP_HIP(c, hipGetLastError());
   }
   RP_HIP(c, hipStreamSynchronize(c->stream));
@@ -788,7 +842,7 @@ ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t 
   for (int attempt = 0;; ++attempt) {
     issue_batch(c, B);
     RP_HIP(c, hipGetLastError());
-    RP_HIP(c, hipStreamSynchronize(c->stream));
+    RP_TRY(wait_stream(c));
     if (!c->h_counters->abort) break;
     // the spare arena cannot take this batch's row moves: nothing was mutated
     c->ev_log.clear();
@@ -917,6 +971,13 @@ ripple_status ripple_set_profiling(ripple_ctx *c, int32_t mask) {
   RP_TRY(check_ctx(c));
   c->prof_mask = static_cast<unsigned>(mask) & ((1u << RIPPLE_NUM_PHASES) - 1u);
   c->prof = c->prof_mask != 0;
+  // create the events now so that the first recorded batch does not pay for it
+  const size_t want = 2 * (4 + 3 * static_cast<size_t>(rp::kMaxL));
+  while (c->prof && c->ev_pool.size() < want) {
+    hipEvent_t e;
+    RP_HIP(c, hipEventCreate(&e));
+    c->ev_pool.push_back(e);
+  }
   c->ev_log.clear();
   c->ev_used = 0;
   return RIPPLE_OK;
@@ -963,6 +1024,7 @@ void ripple_destroy(ripple_ctx *c) {
     dfree_t(c, c->adj[d].len);
     dfree_t(c, c->adj[d].cap);
     dfree_t(c, c->adj[d].col);
+    dfree_t(c, c->col_alt[d]);
     dfree_t(c, c->adj[d].inscnt);
     dfree_t(c, c->adj[d].delcnt);
   }
@@ -972,6 +1034,9 @@ void ripple_destroy(ripple_ctx *c) {
   dfree_t(c, c->bm_x);
   dfree_t(c, c->blocksum);
   dfree_t(c, c->blockdeg);
+  dfree_t(c, c->rl_blocksums);
+  dfree_t(c, c->rl_off);
+  dfree_t(c, c->rl_cap);
   dfree_t(c, c->d_counters);
   dfree_t(c, c->d_persist);
   if (c->h_counters) (void)hipHostFree(c->h_counters);

@@ -49,6 +49,7 @@ class GraphDesc(C.Structure):
         ("src", C.POINTER(C.c_int32)), ("dst", C.POINTER(C.c_int32)),
         ("undirected", C.c_int32), ("slack", C.c_float), ("min_slack", C.c_int32),
         ("device", C.c_int32), ("stream", C.c_void_p), ("max_device_bytes", C.c_int64),
+        ("arena_slots", C.c_int64),
     ]
 
 
@@ -127,7 +128,7 @@ class Ripple:
 
     def __init__(self, n: int, src, dst, undirected: bool = False, slack: float = 0.25,
                  min_slack: int = 4, device: int = 0, stream: Optional[int] = None,
-                 max_device_bytes: int = 0):
+                 max_device_bytes: int = 0, arena_slots: int = 0):
         self._lib = load_library()
         self._ctx = C.c_void_p()
         src, dst = _i32(src), _i32(dst)
@@ -135,7 +136,7 @@ class Ripple:
             raise ValueError("src and dst differ in length")
         desc = GraphDesc(int(n), int(src.size), _ptr(src, C.c_int32), _ptr(dst, C.c_int32),
                          int(bool(undirected)), float(slack), int(min_slack), int(device),
-                         C.c_void_p(stream) if stream else None, int(max_device_bytes))
+                         C.c_void_p(stream) if stream else None, int(max_device_bytes), int(arena_slots))
         st = self._lib.ripple_load_graph(C.byref(desc), C.byref(self._ctx))
         if st != OK:
             raise RippleError(st, self._lib.ripple_last_error(None).decode())

@@ -54,7 +54,7 @@ def _load(n, src, dst, **kw):
     src = np.ascontiguousarray(src, np.int32)
     dst = np.ascontiguousarray(dst, np.int32)
     desc = R.GraphDesc(n, src.size, src.ctypes.data_as(C.POINTER(C.c_int32)),
-                       dst.ctypes.data_as(C.POINTER(C.c_int32)), kw.get("undirected", 0), 0.25, 4, 0, None, 0)
+                       dst.ctypes.data_as(C.POINTER(C.c_int32)), kw.get("undirected", 0), 0.25, 4, 0, None, 0, 0)
     ctx = C.c_void_p(123)
     st = lib.ripple_load_graph(C.byref(desc), C.byref(ctx))
     return st, ctx, lib.ripple_last_error(None).decode()

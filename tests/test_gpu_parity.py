@@ -81,15 +81,16 @@ def test_adversarial_batches(agg, undirected):
         p.close()
 
 
-@pytest.mark.parametrize("agg", ["sum", "gcn"])
-def test_no_slack_forces_row_moves_and_relayouts(agg):
-    """slack 0: every insert outgrows its row, so rows move to the spare arena and
-    the arena fills up, which forces full re-layouts."""
-    _say("no slack", agg)
-    rng = np.random.default_rng(11)
+@pytest.mark.parametrize("agg,arena", [("sum", 0), ("gcn", 0), ("sum", 64), ("mean", 2000), ("sum", 2000)])
+def test_no_slack_forces_row_moves_and_relayouts(agg, arena):
+    """slack 0: every insert outgrows its row, so rows move to the spare arena; a
+    small arena runs out, which forces re-layouts (on the device, or into larger
+    buffers when the graph has outgrown them)."""
+    _say("no slack", agg, arena)
+    rng = np.random.default_rng(11 + arena)
     dims = (8, 16, 4)
     src, dst, x, w = _small(rng, 200, 600, dims, agg)
-    p = Pair(200, src, dst, x, w, slack=0.0, min_slack=0)
+    p = Pair(200, src, dst, x, w, slack=0.0, min_slack=0, arena_slots=arena)
     try:
         moved = relayouts = 0
         for b in range(60):
@@ -97,7 +98,12 @@ def test_no_slack_forces_row_moves_and_relayouts(agg):
             st, _, _ = p.step(batch)
             moved += st["relocated_rows"]
             relayouts += st["repacks"]
+            if st["repacks"] or b % 20 == 19:
+                p.check_arcs()
+                p.check_embeddings()
         assert moved > 0
+        if arena:
+            assert relayouts > 0
         p.check_arcs()
         p.check_embeddings()
         _say("rows moved", moved, "re-layouts", relayouts)
