@@ -106,6 +106,15 @@ class OracleGraph:
         g.n, g.undirected, g.keys = self.n, self.undirected, self.keys.copy()
         return g
 
+    def in_sorted(self) -> Tuple[np.ndarray, np.ndarray]:
+        """(sources, sinks) of all arcs ordered by sink, then source (cached)."""
+        cached = getattr(self, "_in_sorted", None)
+        if cached is None or cached[0] is not self.keys:
+            ik = np.sort((self.keys % self.n) * self.n + self.keys // self.n)
+            cached = (self.keys, ik % self.n, ik // self.n)
+            self._in_sorted = cached
+        return cached[1], cached[2]
+
     @property
     def num_arcs(self) -> int:
         return int(self.keys.size)
@@ -316,9 +325,7 @@ def sampled_embeddings(graph: OracleGraph, x: np.ndarray, model: OracleModel,
     Returns (sorted distinct vertices, their rows)."""
     L = model.num_layers if upto_layer is None else int(upto_layer)
     verts = np.unique(np.asarray(vertices, np.int64))
-    src, dst = graph.arcs()
-    order = np.argsort(dst, kind="stable")
-    s_sorted, d_sorted = src[order], dst[order]
+    s_sorted, d_sorted = graph.in_sorted()
     dout = graph.out_degree().astype(dtype)
     din = graph.in_degree().astype(dtype)
 

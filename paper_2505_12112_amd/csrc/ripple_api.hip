@@ -20,6 +20,7 @@
 #include <cstring>
 #include <numeric>
 #include <string>
+#include <thread>
 #include <unordered_map>
 #include <vector>
 
@@ -696,11 +697,33 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
       if (c->undirected) ocol[fo[v]++] = u;
     }
   }
-  for (long long u = 0; u < n; ++u) {
-    std::sort(ocol.begin() + ooff[u], ocol.begin() + ooff[u + 1]);
-    for (long long e = ooff[u] + 1; e < ooff[u + 1]; ++e)
-      if (ocol[e] == ocol[e - 1]) {
-        c->err = "ripple: repeated arc " + std::to_string(u) + "->" + std::to_string(ocol[e]);
+  {
+    // sort every out-row (host threads over row ranges of equal arc counts) and
+    // look for repeated arcs
+    const int nt = static_cast<int>(std::max(1u, std::min(16u, std::thread::hardware_concurrency())));
+    std::vector<long long> bad(nt, -1);
+    std::vector<std::thread> pool;
+    long long row0 = 0;
+    for (int t = 0; t < nt; ++t) {
+      const long long goal = arcs * (t + 1) / nt;
+      long long row1 = t == nt - 1 ? n : std::lower_bound(ooff.begin() + row0, ooff.end() - 1, goal) - ooff.begin();
+      if (row1 < row0) row1 = row0;
+      pool.emplace_back([&, t, row0, row1]() {
+        for (long long u = row0; u < row1; ++u) {
+          std::sort(ocol.begin() + ooff[u], ocol.begin() + ooff[u + 1]);
+          for (long long e = ooff[u] + 1; e < ooff[u + 1]; ++e)
+            if (ocol[e] == ocol[e - 1]) {
+              bad[t] = u;
+              return;
+            }
+        }
+      });
+      row0 = row1;
+    }
+    for (auto &th : pool) th.join();
+    for (int t = 0; t < nt; ++t)
+      if (bad[t] >= 0) {
+        c->err = "ripple: repeated arc out of vertex " + std::to_string(bad[t]);
         return bail(RIPPLE_E_INVALID);
       }
   }

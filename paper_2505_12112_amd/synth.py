@@ -28,6 +28,8 @@ feature-row block; ``v`` is -1 for feature ops and ``feat_row`` -1 for edge ops)
 from __future__ import annotations
 
 import dataclasses
+import os
+from concurrent.futures import ThreadPoolExecutor
 from typing import Dict, List, Optional, Tuple
 
 import numpy as np
@@ -135,7 +137,7 @@ def chung_lu_weights(n: int, total: float, gamma: float) -> np.ndarray:
     if w0(hi) > cap:          # cannot reach the cap: take the flattest admissible curve
         i0 = hi
     else:
-        for _ in range(200):
+        for _ in range(80):
             mid = np.sqrt(lo * hi)
             if w0(mid) > cap:
                 lo = mid
@@ -147,23 +149,65 @@ def chung_lu_weights(n: int, total: float, gamma: float) -> np.ndarray:
 
 
 def _draw(rng: np.random.Generator, cdf: np.ndarray, count: int) -> np.ndarray:
+    """`count` independent indices with P(i) proportional to cdf[i] - cdf[i-1]."""
     r = rng.random(count) * cdf[-1]
     return np.minimum(np.searchsorted(cdf, r, side="right"), len(cdf) - 1).astype(np.int64)
+
+
+def _draw_many(rng: np.random.Generator, p: np.ndarray, count: int, shuffle: bool = True) -> np.ndarray:
+    """`count` i.i.d. indices with probabilities p: multinomial counts per index,
+    laid out in a uniformly random order (same law as independent draws, without
+    a search per draw). With shuffle=False they come sorted; pairing a sorted
+    sample with a shuffled independent one still gives i.i.d. pairs."""
+    counts = rng.multinomial(count, p)
+    idx = np.repeat(np.arange(p.size, dtype=np.int64), counts)
+    if shuffle:
+        rng.shuffle(idx)
+    return idx
+
+
+_THREADS = max(1, min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else 4))
+
+
+def _unique_sorted_chunk(x: np.ndarray) -> np.ndarray:
+    x = np.sort(x)
+    if x.size == 0:
+        return x
+    keep = np.empty(x.size, bool)
+    keep[0] = True
+    np.not_equal(x[1:], x[:-1], out=keep[1:])
+    return x[keep]
+
+
+def _sorted_unique(x: np.ndarray) -> np.ndarray:
+    """Sorted distinct values (introsort; NumPy's stable sort of int64 is a much
+    slower merge sort)."""
+    return _unique_sorted_chunk(x)
 
 
 def _distinct(rng, n, target, sampler, undirected):
     """Draw arcs (or unordered pairs) until `target` distinct non-loop keys exist."""
     keys = np.empty(0, np.int64)
+    first = True
     while keys.size < target:
         need = target - keys.size
-        u, v = sampler(int(need * 1.2) + 1024)
+        u, v = sampler(int(need * (1.15 if first else 1.5)) + 1024)
         ok = u != v
         u, v = u[ok], v[ok]
         if undirected:
             u, v = np.minimum(u, v), np.maximum(u, v)
-        keys = np.unique(np.concatenate([keys, u * n + v]))
+        cand = _sorted_unique(u * n + v)
+        if first:
+            keys, first = cand, False
+            continue
+        pos = np.searchsorted(keys, cand)
+        hit = (pos < keys.size) & (keys[np.minimum(pos, keys.size - 1)] == cand)
+        new = cand[~hit]
+        keys = np.insert(keys, np.searchsorted(keys, new), new)
     if keys.size > target:
-        keys = np.sort(keys[rng.permutation(keys.size)[:target]])
+        drop = np.zeros(keys.size, bool)
+        drop[rng.choice(keys.size, keys.size - target, replace=False)] = True
+        keys = keys[~drop]
     return keys
 
 
@@ -181,39 +225,64 @@ def generate_graph(spec: GraphSpec, rng: np.random.Generator):
     elif spec.kind == "chung_lu":
         if spec.undirected:
             w = chung_lu_weights(n, 2.0 * total, spec.gamma)
-            perm = rng.permutation(n)
-            cdf = np.cumsum(w[np.argsort(perm)])
+            p = w[np.argsort(rng.permutation(n))]
+            p = p / p.sum()
 
             def sampler(c):
-                return _draw(rng, cdf, c), _draw(rng, cdf, c)
+                return _draw_many(rng, p, c, shuffle=False), _draw_many(rng, p, c)
         else:
             w = chung_lu_weights(n, float(total), spec.gamma)
-            cdf_out = np.cumsum(w[np.argsort(rng.permutation(n))])
-            cdf_in = np.cumsum(w[np.argsort(rng.permutation(n))])
+            p_out = w[np.argsort(rng.permutation(n))]
+            p_in = w[np.argsort(rng.permutation(n))]
+            p_out, p_in = p_out / p_out.sum(), p_in / p_in.sum()
 
             def sampler(c):
-                return _draw(rng, cdf_out, c), _draw(rng, cdf_in, c)
+                return _draw_many(rng, p_out, c, shuffle=False), _draw_many(rng, p_in, c)
     elif spec.kind == "rmat":
         scale = int(np.log2(n))
         assert (1 << scale) == n
         a, b, c_, _d = spec.rmat
         relabel = rng.permutation(n).astype(np.int64)
 
-        def sampler(c):
-            u = np.zeros(c, np.int64)
-            v = np.zeros(c, np.int64)
+        t1, t2, t3 = np.float32(a), np.float32(a + b), np.float32(a + b + c_)
+
+        def rmat_chunk(seed, k):
+            # quadrant per level from one uniform: a -> (0,0), b -> (0,1), c -> (1,0), d -> (1,1)
+            g = np.random.default_rng(seed)
+            u = np.zeros(k, np.int32)
+            v = np.zeros(k, np.int32)
+            r = np.empty(k, np.float32)
+            hi_half = np.empty(k, np.bool_)
+            vbit = np.empty(k, np.bool_)
+            dq = np.empty(k, np.bool_)
             for _ in range(scale):
-                r = rng.random(c)
-                ubit = r >= a + b
-                vbit = ((r >= a) & (r < a + b)) | (r >= a + b + c_)
-                u = (u << 1) | ubit
-                v = (v << 1) | vbit
+                g.random(out=r, dtype=np.float32)
+                np.greater_equal(r, t2, out=hi_half)          # c or d: source bit set
+                np.left_shift(u, 1, out=u)
+                np.bitwise_or(u, hi_half, out=u)
+                np.greater_equal(r, t1, out=vbit)
+                np.logical_xor(vbit, hi_half, out=vbit)       # b
+                np.greater_equal(r, t3, out=dq)               # d
+                np.logical_or(vbit, dq, out=vbit)             # b or d: sink bit set
+                np.left_shift(v, 1, out=v)
+                np.bitwise_or(v, vbit, out=v)
             return relabel[u], relabel[v]
+
+        def sampler(c):
+            # fixed-size chunks, each with its own generator seeded from rng, so the
+            # result does not depend on the thread count or scheduling
+            sizes = [min(1 << 22, c - lo) for lo in range(0, c, 1 << 22)]
+            chunk_seeds = rng.integers(0, 2**63 - 1, size=len(sizes))
+            with ThreadPoolExecutor(_THREADS) as ex:
+                parts = list(ex.map(rmat_chunk, chunk_seeds, sizes))
+            return np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts])
     else:
         raise ValueError(spec.kind)
     keys = _distinct(rng, n, total, sampler, spec.undirected)
-    keys = keys[rng.permutation(keys.size)]
-    snap, pool = np.sort(keys[:spec.m]), keys[spec.m:]
+    in_pool = np.zeros(keys.size, bool)
+    in_pool[rng.choice(keys.size, keys.size - spec.m, replace=False)] = True
+    snap, pool = keys[~in_pool], keys[in_pool]
+    rng.shuffle(pool)
     return ((snap // n).astype(np.int32), (snap % n).astype(np.int32),
             (pool // n).astype(np.int32), (pool % n).astype(np.int32))
 
@@ -304,7 +373,10 @@ class UpdateStream:
             assert out_deg is not None and in_deg is not None
             self._cdf_out = np.cumsum(out_deg.astype(np.float64) + 1.0)
             self._cdf_in = np.cumsum(in_deg.astype(np.float64) + 1.0)
-            self._keys = np.sort(snap_src.astype(np.int64) * n + snap_dst)
+            keys = snap_src.astype(np.int64) * n + snap_dst
+            if keys.size > 1 and not np.all(keys[1:] > keys[:-1]):
+                keys = np.sort(keys)     # generate_graph already returns the snapshot sorted
+            self._keys = keys
             self._inserted = set()
 
     def _kinds(self, bs: int) -> np.ndarray:

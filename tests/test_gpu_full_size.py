@@ -60,3 +60,76 @@ def test_sparse_mid_mean_thousand_batches():
         p.check_aggregates()
     finally:
         p.close()
+
+
+def _sample_vertices(rng, orc, affected, k, max_reach):
+    """Up to k affected and k other vertices whose two-hop in-neighbourhood (in arcs)
+    stays below max_reach, so the oracle can evaluate them one by one."""
+    src_s, dst_s = orc.graph.in_sorted()
+    indeg = np.bincount(dst_s, minlength=orc.graph.n)
+    picked = []
+    for pool in (affected, rng.integers(0, orc.graph.n, 50 * k)):
+        pool = np.asarray(pool)
+        got = 0
+        for v in rng.permutation(pool)[:50 * k]:
+            lo, hi = np.searchsorted(dst_s, [v, v + 1])
+            reach = int(indeg[src_s[lo:hi]].sum()) + (hi - lo)
+            if reach <= max_reach:
+                picked.append(int(v))
+                got += 1
+                if got == k:
+                    break
+    return np.unique(np.array(picked, np.int64))
+
+
+def _check_sampled(p, verts, layers, tol=1e-4):
+    errs = []
+    for l in layers:
+        vs, ref = O.sampled_embeddings(p.orc.graph, p.orc.x, p.orc.model, verts, upto_layer=l)
+        got = p.lib.get_embeddings(l, vs.astype(np.int32))
+        # row-relative error with the floor taken from the sampled reference rows
+        err = O.row_relative_error(got, ref)
+        errs.append(err)
+        assert err <= tol, (l, err)
+    return errs
+
+
+def test_dense_large_full_size():
+    """Products-shaped undirected graph at full size (2,449,029 vertices, 61,859,140
+    edges, GraphSAGE-sum 100-256-256-47): three batches of 100 with affected sets
+    compared bit for bit, then embeddings of sampled vertices at every layer."""
+    t0 = time.time()
+    wl = synth.build_workload("dense_large")
+    _say(f"dense_large generated in {time.time() - t0:.0f}s")
+    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, undirected=True)
+    try:
+        _say(f"  loaded + bootstrapped, oracle built ({time.time() - t0:.0f}s)")
+        rng = np.random.default_rng(5)
+        for b in range(3):
+            st, _, sets = p.step(wl.stream.next_batch(100))
+            _say(f"  batch {b}: |A| = {[s.size for s in sets]} ({time.time() - t0:.0f}s)")
+        verts = _sample_vertices(rng, p.orc, sets[3], 24, 400_000)
+        errs = _check_sampled(p, verts, (1, 2, 3))
+        _say(f"  {verts.size} sampled vertices, row-relative errors {errs} ({time.time() - t0:.0f}s)")
+    finally:
+        p.close()
+
+
+def test_stress_full_size():
+    """RMAT graph at full size (2^23 vertices, 200M arcs, GCN 64-256-64), one
+    hub-biased batch of 10,000 ops: affected sets bit for bit, embeddings of
+    sampled vertices at both layers."""
+    t0 = time.time()
+    wl = synth.build_workload("stress")
+    _say(f"stress generated in {time.time() - t0:.0f}s")
+    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights)
+    try:
+        _say(f"  loaded + bootstrapped, oracle built ({time.time() - t0:.0f}s)")
+        st, _, sets = p.step(wl.stream.next_batch(10_000))
+        _say(f"  batch: |A| = {[s.size for s in sets]}, pushed {st['pushed_arcs']} ({time.time() - t0:.0f}s)")
+        rng = np.random.default_rng(6)
+        verts = _sample_vertices(rng, p.orc, sets[2], 24, 2_000_000)
+        errs = _check_sampled(p, verts, (1, 2))
+        _say(f"  {verts.size} sampled vertices, row-relative errors {errs} ({time.time() - t0:.0f}s)")
+    finally:
+        p.close()
