@@ -117,6 +117,11 @@ typedef struct {
   const float *const *bias;      /* [L] [d_l]; NULL array or NULL entry = zero bias */
   const int32_t *relu;           /* [L] 1 = ReLU after layer l, 0 = identity */
   int32_t gemm_prec;             /* ripple_gemm_prec; RIPPLE_GEMM_FP32 only in this version */
+  int32_t transform_first;       /* per-layer choice of what the aggregate cache holds (see
+                                    ripple_get_aggregates): -1 = for layers with d_l < d_{l-1} when the
+                                    graph has at least 2^24 arcs (on smaller graphs the message step is
+                                    latency-bound and the extra transform does not pay), 0 = never,
+                                    1 = every layer. Results are the same up to rounding. */
 } ripple_model_desc;
 
 /* What one ripple_apply_updates call did. Arc counts count directed arcs (an
@@ -134,6 +139,9 @@ typedef struct {
   int64_t dest_rows[RIPPLE_MAX_LAYERS + 1];   /* [l]: distinct sinks of those arcs */
   int64_t relocated_rows;       /* adjacency rows moved to the spare arena */
   int64_t repacks;              /* adjacency re-layouts this call needed (spare arena full) */
+  int64_t in_arcs[RIPPLE_MAX_LAYERS + 1];   /* [l]: in-arcs of A^l (the pull form's work) */
+  int32_t pull_layers;          /* bit l set: layer l added its messages by pull, not push */
+  int32_t pad;
 } ripple_batch_stats;
 
 /* Part 1 of the problem statement: copies the snapshot to the device as an
@@ -174,16 +182,28 @@ RIPPLE_API ripple_status ripple_get_affected(ripple_ctx *ctx, int32_t layer, int
 
 /* The cached aggregate of layer `layer` (1..L) the incremental path maintains:
  * S^l_v = sum over in-neighbours u of c_u h^{l-1}_u, with c_u = 1 (sum, mean)
- * or 1/sqrt(dout(u)+1) (GCN). Host out [count][d_{l-1}]; ids as in
- * ripple_get_embeddings. For checking only. */
+ * or 1/sqrt(dout(u)+1) (GCN), width d_{l-1}; or, for a layer cached transformed
+ * (transform_first), T^l_v = W_neigh^l S^l_v (GCN: W^l S^l_v), width d_l. The
+ * messages of such a layer carry W_neigh times the change of the source's row,
+ * which is exact by linearity of the aggregators. Host out [count][width]; ids
+ * as in ripple_get_embeddings; *width (nullable) receives the row width. For
+ * checking only. */
 RIPPLE_API ripple_status ripple_get_aggregates(ripple_ctx *ctx, int32_t layer, const int32_t *ids,
-                                    int64_t count, float *out);
+                                    int64_t count, float *out, int32_t *width);
 
 /* Copies the current arc set as (src, dst) pairs read from the out-adjacency
  * (direction 0) or the in-adjacency (direction 1), grouped by row in row order.
  * Writes min(arcs, capacity) pairs and the arc count to *count (always). */
 RIPPLE_API ripple_status ripple_get_arcs(ripple_ctx *ctx, int32_t direction, int32_t *src, int32_t *dst,
                               int64_t capacity, int64_t *count);
+
+/* How each layer adds its messages to the cached aggregate (results agree up to
+ * rounding): RIPPLE_SCATTER_PUSH, one row of fp32 atomics per pushed arc;
+ * RIPPLE_SCATTER_PULL, each affected vertex sums the messages of its dirty
+ * in-neighbours and adds them once; RIPPLE_SCATTER_AUTO (default), per layer
+ * from the previous batch's counts (push on the first batch). */
+enum { RIPPLE_SCATTER_AUTO = 0, RIPPLE_SCATTER_PUSH = 1, RIPPLE_SCATTER_PULL = 2 };
+RIPPLE_API ripple_status ripple_set_scatter_mode(ripple_ctx *ctx, int32_t mode);
 
 /* Device bytes the context holds. */
 RIPPLE_API ripple_status ripple_device_bytes(ripple_ctx *ctx, int64_t *bytes);

@@ -40,6 +40,7 @@ struct Counters {
   u64 count[kMaxL + 1];   // [0] = |dirty set of layer 1|, [l] = |A^l|
   u64 pushed[kMaxL + 1];  // [l] = out-arcs pushed at layer l
   u64 dest[kMaxL + 1];    // [l] = distinct sinks of those arcs
+  u64 indeg[kMaxL + 1];   // [l] = sum of in-degrees over A^l (pull work), when computed
 };
 
 // Survives batches.
@@ -56,10 +57,13 @@ struct Adj {
   int *delcnt;
 };
 
+// Per layer l = 1..L: the rows whose contributions the aggregate S[l] sums
+// (src[l], width sw[l]): H[l-1] for a plain layer, or the cached P = W_neigh
+// H[l-1] (width d_l) for a transform-first layer.
 struct LayerPtrs {
-  float *H[kMaxL + 1];
+  const float *src[kMaxL + 1];
   float *S[kMaxL + 1];
-  int dims[kMaxL + 1];
+  int sw[kMaxL + 1];
   int L;
 };
 
@@ -105,22 +109,45 @@ void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerP
                       const int *ddeg, const int *flist, const int *ins_src, const int *ins_dst,
                       const int *del_src, const int *del_dst, unsigned *bm, Counters *c);
 int compact_blocks(long long n);
-// bitmaps (a | b) -> ascending list, count, and, when deg != nullptr, doff[j] =
-// sum of deg over list[0..j) with doff[count] = total; both bitmaps are cleared.
+// Outputs of one compaction of bitmaps (a | b) into an ascending list. Optional
+// (nullptr = skipped): doff[j] = sum of out_deg over list[0..j) (doff[count] =
+// total), ioff likewise over in_deg, keep = the compacted bitmap words, slot[v] =
+// position of v in the list. Both input bitmaps are cleared.
+struct CompactOut {
+  int *list;
+  u64 *count;
+  const int *out_deg;
+  long long *doff;
+  const int *in_deg;
+  long long *ioff;
+  u64 *in_total;       // receives the sum of in_deg over the list
+  unsigned *keep;
+  int *slot;
+};
+// in_total (nullable) receives the sum of in_deg over the list even without ioff.
+// Scratch: blocksum[compact_blocks(n)], blockdeg[2 * compact_blocks(n)].
+// single_block: one 1024-thread block walks all words (fewer launches; for small n).
 void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, int *blocksum,
-                    long long *blockdeg, const int *deg, int *list_out, long long *doff, u64 *count_out);
+                    long long *blockdeg, const CompactOut &o, bool single_block);
 
 // layer 0 deltas (feat may be pinned host memory)
 void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list, const u64 *count,
                    const ripple_op *ops, const float *feat, const int *fop, float *X, const int *out_len,
                    const int *ddeg, float *delta, const Counters *c);
 
-// scatter: S^l[v] += delta[j] for every post-batch out-arc (list[j] -> v), 64 arcs
-// per wave step (doff gives each listed vertex's first arc); marks the sinks in
-// bm_out, and the listed vertices and the sinks of net arcs in bm_x.
+// scatter: S^l[v] += delta[j] for every post-batch out-arc (list[j] -> v) (doff
+// gives each listed vertex's first arc); marks the sinks in bm_out, and the
+// listed vertices and the sinks of net arcs in bm_x. With push = false it only
+// marks (the pull kernel then adds the messages).
 void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
-                    const int *del_dst, u64 *pushed, u64 *dest, const Counters *c);
+                    const int *del_dst, u64 *pushed, u64 *dest, const Counters *c, bool push);
+
+// pull: for every vertex v of the sorted list A (in-arc prefix ioff), S[v] +=
+// sum of msg[slot[u]] over in-arcs (u -> v) whose source u is set in member.
+// One flush (row of fp32 atomics) per sink and wave; each in-arc is read once.
+void launch_pull_msgs(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *ioff,
+                      Adj in, const unsigned *member, const int *slot, const float *msg, float *S, const Counters *c);
 
 // bootstrap pull: S[v] = sum over in-arcs c_u H[u]
 void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev, Adj in, const int *out_len,
@@ -131,7 +158,15 @@ void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev,
 //   y = act(W t_v (S_v + s_v h_v) + b)   (GCN; t_v = 1/sqrt(din+1), s_v = 1/sqrt(dout+1))
 // then, when delta != nullptr, delta[r] = c'_v y - c_v H[v] (c = 1, or s_v post/pre
 // batch under GCN), and H[v] = y.
+// mode kLayer: the layer as above. kTransformFirst: S holds T = W_neigh S (width
+// N), Z = h_v (K = dprev), W = W_self (SAGE) or W (GCN), and the epilogue adds
+// t_v T_v (SAGE) or forms t_v (T_v + s_v y) (GCN). kPlain: y = h_v W^T (K =
+// dprev); with bias nullptr and relu 0 this computes the rows P_v = W_neigh h_v a
+// transform-first layer caches (H = P) and, with delta set, their messages
+// c'_v P'_v - c_v P_v.
+enum GemmMode { kLayer = 0, kTransformFirst = 1, kPlain = 2 };
 struct GemmArgs {
+  int mode;
   const int *rows;
   const u64 *count;
   long long count_fixed;

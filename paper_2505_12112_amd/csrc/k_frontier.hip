@@ -95,8 +95,8 @@ __global__ void k_corr_mark(int agg, LayerPtrs lp, const int *out_len, const int
     const int v = ins ? ins_dst[arc] : del_dst[arc - ni];
     float coef = ins ? 1.0f : -1.0f;
     if (agg == kGcn) coef *= 1.0f / sqrtf(static_cast<float>(out_len[u] - ddeg[u]) + 1.0f);
-    const int d = lp.dims[l - 1];
-    const float *hu = lp.H[l - 1] + static_cast<long long>(u) * d;
+    const int d = lp.sw[l];
+    const float *hu = lp.src[l] + static_cast<long long>(u) * d;
     float *sv = lp.S[l] + static_cast<long long>(v) * d;
     for (int k = lane; k < d; k += kWave) unsafeAtomicAdd(&sv[k], coef * hu[k]);
   }
@@ -113,62 +113,71 @@ __global__ void k_corr_mark(int agg, LayerPtrs lp, const int *out_len, const int
   }
 }
 
-__device__ inline void word_stats(unsigned w, long long vbase, const int *deg, int &cnt, long long &dsum) {
+__device__ inline void word_stats(unsigned w, long long vbase, const int *odeg, const int *ideg, int &cnt,
+                                  long long &dsum, long long &isum) {
   cnt += __popc(w);
-  if (deg != nullptr) {
+  if (odeg != nullptr || ideg != nullptr) {
     while (w) {
       const int b = __ffs(w) - 1;
-      dsum += deg[vbase + b];
+      if (odeg != nullptr) dsum += odeg[vbase + b];
+      if (ideg != nullptr) isum += ideg[vbase + b];
       w &= w - 1;
     }
   }
 }
 
 __global__ __launch_bounds__(kCompactThreads) void k_compact_count(const unsigned *bm_a, const unsigned *bm_b,
-                                                                   long long words, const int *deg,
-                                                                   int *blocksum, long long *blockdeg) {
+                                                                   long long words, const int *odeg,
+                                                                   const int *ideg, int *blocksum,
+                                                                   long long *blockdeg) {
   __shared__ long long red[kCompactWaves + 1];
   const long long w0 = static_cast<long long>(blockIdx.x) * kWordsPerBlock + threadIdx.x * kWordsPerThread;
   int cnt = 0;
-  long long dsum = 0;
+  long long dsum = 0, isum = 0;
 #pragma unroll
   for (int i = 0; i < kWordsPerThread; ++i) {
     const long long w = w0 + i;
-    if (w < words) word_stats(bm_a[w] | bm_b[w], w * 32, deg, cnt, dsum);
+    if (w < words) word_stats(bm_a[w] | bm_b[w], w * 32, odeg, ideg, cnt, dsum, isum);
   }
   const long long tc = block_sum<long long>(cnt, red);
   const long long td = block_sum<long long>(dsum, red);
+  const long long ti = block_sum<long long>(isum, red);
   if (threadIdx.x == 0) {
     blocksum[blockIdx.x] = static_cast<int>(tc);
-    blockdeg[blockIdx.x] = td;
+    blockdeg[2 * blockIdx.x] = td;
+    blockdeg[2 * blockIdx.x + 1] = ti;
   }
 }
 
 __global__ __launch_bounds__(kCompactThreads) void k_compact_emit(unsigned *bm_a, unsigned *bm_b, long long words,
-                                                                  const int *deg, const int *blocksum,
-                                                                  const long long *blockdeg, int *list_out,
-                                                                  long long *doff, u64 *count_out) {
+                                                                  const int *blocksum, const long long *blockdeg,
+                                                                  CompactOut o) {
   __shared__ long long red[kCompactWaves + 1];
-  long long pre = 0, pred = 0;
+  long long pre = 0, pred = 0, prei = 0;
   for (int b = threadIdx.x; b < static_cast<int>(blockIdx.x); b += kCompactThreads) {
     pre += blocksum[b];
-    if (deg != nullptr) pred += blockdeg[b];
+    pred += blockdeg[2 * b];
+    prei += blockdeg[2 * b + 1];
   }
   const long long base = block_sum<long long>(pre, red);
   const long long dbase = block_sum<long long>(pred, red);
+  const long long ibase = block_sum<long long>(prei, red);
   const long long w0 = static_cast<long long>(blockIdx.x) * kWordsPerBlock + threadIdx.x * kWordsPerThread;
+  const int *odeg = o.doff != nullptr ? o.out_deg : nullptr;
+  const int *ideg = o.ioff != nullptr ? o.in_deg : nullptr;  // prefix only when wanted
   unsigned wv[kWordsPerThread];
   int cnt = 0;
-  long long dsum = 0;
+  long long dsum = 0, isum = 0;
 #pragma unroll
   for (int i = 0; i < kWordsPerThread; ++i) {
     const long long w = w0 + i;
     wv[i] = w < words ? (bm_a[w] | bm_b[w]) : 0u;
-    word_stats(wv[i], w * 32, deg, cnt, dsum);
+    word_stats(wv[i], w * 32, odeg, ideg, cnt, dsum, isum);
   }
-  long long tot_c, tot_d;
+  long long tot_c, tot_d, tot_i;
   long long pos = base + block_exclusive_scan<long long>(cnt, red, &tot_c);
   long long dpos = dbase + block_exclusive_scan<long long>(dsum, red, &tot_d);
+  long long ipos = ibase + block_exclusive_scan<long long>(isum, red, &tot_i);
 #pragma unroll
   for (int i = 0; i < kWordsPerThread; ++i) {
     unsigned m = wv[i];
@@ -176,23 +185,124 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact_emit(unsigned *bm_a
     while (m) {
       const int b = __ffs(m) - 1;
       const int v = static_cast<int>(vbase + b);
-      list_out[pos] = v;
-      if (deg != nullptr) {
-        doff[pos] = dpos;
-        dpos += deg[v];
+      o.list[pos] = v;
+      if (odeg != nullptr) {
+        o.doff[pos] = dpos;
+        dpos += odeg[v];
       }
+      if (ideg != nullptr) {
+        o.ioff[pos] = ipos;
+        ipos += ideg[v];
+      }
+      if (o.slot != nullptr) o.slot[v] = static_cast<int>(pos);
       ++pos;
       m &= m - 1;
     }
     const long long w = w0 + i;
     if (w < words) {
+      if (o.keep != nullptr) o.keep[w] = wv[i];
       bm_a[w] = 0u;
       bm_b[w] = 0u;
     }
   }
   if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
-    *count_out = static_cast<u64>(base + tot_c);
-    if (deg != nullptr) doff[base + tot_c] = dbase + tot_d;
+    const long long total = base + tot_c;
+    *o.count = static_cast<u64>(total);
+    if (odeg != nullptr) o.doff[total] = dbase + tot_d;
+    if (ideg != nullptr) o.ioff[total] = ibase + tot_i;
+    // the count kernel summed in-degrees per block, also when no prefix is wanted
+    if (o.in_total != nullptr) *o.in_total = static_cast<u64>(ibase + blockdeg[2 * blockIdx.x + 1]);
+  }
+}
+
+// One-block form of the compaction for small graphs (one launch instead of two):
+// 1024 threads walk the bitmap words in rounds, carrying the running offsets.
+constexpr int kSingleThreads = 1024;
+constexpr int kSingleWaves = kSingleThreads / kWave;
+
+__device__ inline long long single_scan(long long v, long long *lds, long long *total) {
+  const int lane = lane_id(), wave = threadIdx.x / kWave;
+  long long x = v;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const long long y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == kWave - 1) lds[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    long long run = 0;
+    for (int w = 0; w < kSingleWaves; ++w) {
+      const long long t = lds[w];
+      lds[w] = run;
+      run += t;
+    }
+    lds[kSingleWaves] = run;
+  }
+  __syncthreads();
+  const long long excl = x - v + lds[wave];
+  *total = lds[kSingleWaves];
+  __syncthreads();
+  return excl;
+}
+
+__global__ __launch_bounds__(kSingleThreads) void k_compact_single(unsigned *bm_a, unsigned *bm_b, long long words,
+                                                                   CompactOut o) {
+  __shared__ long long red[kSingleWaves + 1];
+  const int *odeg = o.doff != nullptr ? o.out_deg : nullptr;
+  const int *ideg = (o.ioff != nullptr || o.in_total != nullptr) ? o.in_deg : nullptr;
+  long long pos = 0, dpos = 0, ipos = 0;
+  for (long long r0 = 0; r0 < words; r0 += static_cast<long long>(kSingleThreads) * kWordsPerThread) {
+    const long long w0 = r0 + static_cast<long long>(threadIdx.x) * kWordsPerThread;
+    unsigned wv[kWordsPerThread];
+    int cnt = 0;
+    long long dsum = 0, isum = 0;
+#pragma unroll
+    for (int i = 0; i < kWordsPerThread; ++i) {
+      const long long w = w0 + i;
+      wv[i] = w < words ? (bm_a[w] | bm_b[w]) : 0u;
+      word_stats(wv[i], w * 32, odeg, ideg, cnt, dsum, isum);
+    }
+    long long tc, td, ti;
+    long long p = pos + single_scan(cnt, red, &tc);
+    long long dp = dpos + single_scan(dsum, red, &td);
+    long long ip = ipos + single_scan(isum, red, &ti);
+#pragma unroll
+    for (int i = 0; i < kWordsPerThread; ++i) {
+      unsigned m = wv[i];
+      const long long vbase = (w0 + i) * 32;
+      while (m) {
+        const int b = __ffs(m) - 1;
+        const int v = static_cast<int>(vbase + b);
+        o.list[p] = v;
+        if (odeg != nullptr) {
+          o.doff[p] = dp;
+          dp += odeg[v];
+        }
+        if (o.ioff != nullptr) {
+          o.ioff[p] = ip;
+          ip += ideg[v];
+        }
+        if (o.slot != nullptr) o.slot[v] = static_cast<int>(p);
+        ++p;
+        m &= m - 1;
+      }
+      const long long w = w0 + i;
+      if (w < words) {
+        if (o.keep != nullptr) o.keep[w] = wv[i];
+        bm_a[w] = 0u;
+        bm_b[w] = 0u;
+      }
+    }
+    pos += tc;
+    dpos += td;
+    ipos += ti;
+  }
+  if (threadIdx.x == 0) {
+    *o.count = static_cast<u64>(pos);
+    if (odeg != nullptr) o.doff[pos] = dpos;
+    if (o.ioff != nullptr) o.ioff[pos] = ipos;
+    if (o.in_total != nullptr) *o.in_total = static_cast<u64>(ipos);
   }
 }
 
@@ -262,7 +372,7 @@ __device__ inline long long wave_last_le(const long long *a, long long lo, long 
 // into the sink's row of S with fp32 atomics (coalesced across the G lanes). The
 // delta row stays in registers while consecutive arcs share a source, so a hub's
 // arcs cost one row load per chunk; hubs spread over many waves.
-template <int G, int NC>
+template <int G, int NC, bool PUSH>
 __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u64 *count, const long long *doff,
                                                  const float *delta, Adj out, float *S, unsigned *bm_out,
                                                  unsigned *bm_x, const int *ins_dst, const int *del_dst,
@@ -315,7 +425,7 @@ __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u
     }
     const bool fresh = v >= 0 && mark(bm_out, v);
     my_dest += __popcll(__ballot(fresh));
-    const int cnt = static_cast<int>(elast - e0 + 1);
+    const int cnt = PUSH ? static_cast<int>(elast - e0 + 1) : 0;
     for (int i = 0; i < cnt; i += kEdgesPerStep) {
       const int vv = __shfl(v, i + grp);
       const int jj = __shfl(j, i + grp);
@@ -339,6 +449,90 @@ __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u
     }
   }
   if (lane == 0 && my_dest) atomicAdd(dest, my_dest);
+}
+
+// Pull form of the message step (for dense frontiers). In-arcs of the sorted
+// list A are numbered like the scatter's out-arcs (ioff gives each listed
+// vertex's first in-arc). A wave takes C consecutive in-arcs; each lane resolves
+// one arc's sink v and source u and keeps it if u is dirty (member bit), with the
+// source's message row msg[slot[u]]. The wave then walks its kept arcs in order,
+// summing message rows into registers while the sink stays the same, and adds
+// the sum to S[v] with one row of fp32 atomics per sink: a sink's messages cost
+// one read each and one row update per wave instead of one atomic row each.
+template <int NC>
+__global__ __launch_bounds__(256) void k_pull_msgs(int d, const int *list, const u64 *count, const long long *ioff,
+                                                   Adj in, const unsigned *member, const int *slot,
+                                                   const float *msg, float *S, const Counters *c) {
+  if (c->abort) return;
+  const int lane = lane_id();
+  const long long nA = static_cast<long long>(*count);
+  const long long E = ioff[nA];
+  const long long waves = num_waves();
+  int C = 1;
+  while (C < kWave && static_cast<long long>(C) * waves < E) C <<= 1;
+  const long long chunks = (E + C - 1) / C;
+  for (long long ch = global_wave(); ch < chunks; ch += waves) {
+    const long long e0 = ch * C;
+    const long long elast = e0 + C - 1 < E - 1 ? e0 + C - 1 : E - 1;
+    const long long ja = wave_last_le(ioff, 0, nA + 1, e0);
+    const long long jb = C == 1 ? ja : wave_last_le(ioff, ja, nA + 1, elast);
+    const long long e = e0 + lane;
+    const bool active = e <= elast;
+    int r = static_cast<int>(ja);
+    if (jb > ja) {
+      if (jb - ja < kWave) {
+        const long long mine = ja + lane <= jb ? ioff[ja + lane] : (1LL << 62);
+        int cnt_le = 0;
+        for (int t = 0; t <= static_cast<int>(jb - ja); ++t) cnt_le += __shfl(mine, t) <= e ? 1 : 0;
+        r = static_cast<int>(ja) + cnt_le - 1;
+      } else if (active) {
+        r = static_cast<int>(upper_bound(ioff, ja, jb + 1, e) - 1);
+      }
+    }
+    int v = -1, j = -1;
+    if (active) {
+      v = list[r];
+      const int u = in.col[in.off[v] + (e - ioff[r])];
+      if ((member[u >> 5] >> (u & 31)) & 1u) j = slot[u];
+    }
+    u64 keep = __ballot(j >= 0);
+    int cur = -1;
+    float acc[NC];
+#pragma unroll
+    for (int q = 0; q < NC; ++q) acc[q] = 0.0f;
+    while (keep) {
+      const int i = __ffsll(static_cast<long long>(keep)) - 1;
+      keep &= keep - 1;
+      const int vv = __shfl(v, i);
+      const int jj = __shfl(j, i);
+      if (vv != cur) {
+        if (cur >= 0) {
+          float *sv = S + static_cast<long long>(cur) * d;
+#pragma unroll
+          for (int q = 0; q < NC; ++q) {
+            const int k = lane + q * kWave;
+            if (k < d) unsafeAtomicAdd(&sv[k], acc[q]);
+            acc[q] = 0.0f;
+          }
+        }
+        cur = vv;
+      }
+      const float *mj = msg + static_cast<long long>(jj) * d;
+#pragma unroll
+      for (int q = 0; q < NC; ++q) {
+        const int k = lane + q * kWave;
+        if (k < d) acc[q] += mj[k];
+      }
+    }
+    if (cur >= 0) {
+      float *sv = S + static_cast<long long>(cur) * d;
+#pragma unroll
+      for (int q = 0; q < NC; ++q) {
+        const int k = lane + q * kWave;
+        if (k < d) unsafeAtomicAdd(&sv[k], acc[q]);
+      }
+    }
+  }
 }
 
 // Bootstrap: S[v] = sum over in-arcs (u -> v) of c_u H[u], one wave per vertex,
@@ -417,13 +611,17 @@ int compact_blocks(long long n) {
 }
 
 void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, int *blocksum, long long *blockdeg,
-                    const int *deg, int *list_out, long long *doff, u64 *count_out) {
+                    const CompactOut &o, bool single_block) {
   const long long words = (n + 31) / 32;
+  if (single_block) {
+    hipLaunchKernelGGL(k_compact_single, dim3(1), dim3(kSingleThreads), 0, s, bm_a, bm_b, words, o);
+    return;
+  }
   const int nb = compact_blocks(n);
-  hipLaunchKernelGGL(k_compact_count, dim3(nb), dim3(kCompactThreads), 0, s, bm_a, bm_b, words, deg, blocksum,
-                     blockdeg);
-  hipLaunchKernelGGL(k_compact_emit, dim3(nb), dim3(kCompactThreads), 0, s, bm_a, bm_b, words, deg, blocksum,
-                     blockdeg, list_out, doff, count_out);
+  hipLaunchKernelGGL(k_compact_count, dim3(nb), dim3(kCompactThreads), 0, s, bm_a, bm_b, words,
+                     o.doff != nullptr ? o.out_deg : nullptr,
+                     (o.ioff != nullptr || o.in_total != nullptr) ? o.in_deg : nullptr, blocksum, blockdeg);
+  hipLaunchKernelGGL(k_compact_emit, dim3(nb), dim3(kCompactThreads), 0, s, bm_a, bm_b, words, blocksum, blockdeg, o);
 }
 
 void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list, const u64 *count,
@@ -435,19 +633,34 @@ void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list,
 
 void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
-                    const int *del_dst, u64 *pushed, u64 *dest, const Counters *c) {
+                    const int *del_dst, u64 *pushed, u64 *dest, const Counters *c, bool push) {
   const int blocks = 2048;
-#define RP_SCATTER(GV, NCV)                                                                                     \
-  hipLaunchKernelGGL((k_scatter<GV, NCV>), dim3(blocks), dim3(256), 0, s, d, list, count, doff, delta, out, S, \
+#define RP_SCATTER(GV, NCV, P)                                                                                     \
+  hipLaunchKernelGGL((k_scatter<GV, NCV, P>), dim3(blocks), dim3(256), 0, s, d, list, count, doff, delta, out, S, \
                      bm_out, bm_x, ins_dst, del_dst, pushed, dest, c)
-  if (d <= 16) RP_SCATTER(16, 1);
-  else if (d <= 32) RP_SCATTER(32, 1);
-  else if (d <= 64) RP_SCATTER(64, 1);
-  else if (d <= 128) RP_SCATTER(64, 2);
-  else if (d <= 256) RP_SCATTER(64, 4);
-  else if (d <= 512) RP_SCATTER(64, 8);
-  else RP_SCATTER(64, 16);
+  if (!push) RP_SCATTER(64, 1, false);
+  else if (d <= 16) RP_SCATTER(16, 1, true);
+  else if (d <= 32) RP_SCATTER(32, 1, true);
+  else if (d <= 64) RP_SCATTER(64, 1, true);
+  else if (d <= 128) RP_SCATTER(64, 2, true);
+  else if (d <= 256) RP_SCATTER(64, 4, true);
+  else if (d <= 512) RP_SCATTER(64, 8, true);
+  else RP_SCATTER(64, 16, true);
 #undef RP_SCATTER
+}
+
+void launch_pull_msgs(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *ioff,
+                      Adj in, const unsigned *member, const int *slot, const float *msg, float *S, const Counters *c) {
+  const int blocks = 2048;
+#define RP_PULLM(NCV)                                                                                         \
+  hipLaunchKernelGGL((k_pull_msgs<NCV>), dim3(blocks), dim3(256), 0, s, d, list, count, ioff, in, member, slot, \
+                     msg, S, c)
+  if (d <= 64) RP_PULLM(1);
+  else if (d <= 128) RP_PULLM(2);
+  else if (d <= 256) RP_PULLM(4);
+  else if (d <= 512) RP_PULLM(8);
+  else RP_PULLM(16);
+#undef RP_PULLM
 }
 
 void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev, Adj in, const int *out_len,

@@ -11,6 +11,14 @@
 // follows the layer width (16, 32, 48, 64, 128) and BM the expected row count.
 // The epilogue adds the bias, applies ReLU, forms the next layer's delta row
 // (c'_v y - c_v h_old) and overwrites the embedding row.
+//
+// Modes. kLayer: Z = [h_v || t_v S_v] (SAGE) or t_v (S_v + s_v h_v) (GCN).
+// kTransformFirst: the layer caches T_v = W_neigh S_v (width N) instead of S_v,
+// Z is h_v (K = d_{l-1}) against W_self (SAGE) or W (GCN), and the epilogue adds
+// the cached part: y = Z W_self^T + t_v T_v (SAGE) or y = t_v (T_v + s_v Z W^T)
+// (GCN). kPlain: y = h_v W^T with no bias or activation; used for the rows
+// P_v = W_neigh h_v that a transform-first layer caches, and its messages
+// c'_v P'_v - c_v P_v formed by the same epilogue as the layer deltas.
 #include "internal.h"
 
 namespace rp {
@@ -34,12 +42,19 @@ struct Shape {
   static constexpr int kBPer = (kBChunks + kThreads - 1) / kThreads;
 };
 
-template <int AGG, bool VEC>
+template <int AGG, bool VEC, int MODE>
 __device__ inline float4 load_a(const GemmArgs &a, int v, float tv, float sv, int k) {
   float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
   if (v < 0 || k >= a.K) return r;
   const int dp = a.dprev;
   const long long base = static_cast<long long>(v) * dp;
+  if (MODE != kLayer) {  // plain rows of the previous layer (K == dprev)
+    if (VEC) return *reinterpret_cast<const float4 *>(a.Hprev + base + k);
+    float t[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) t[i] = k + i < a.K ? a.Hprev[base + k + i] : 0.f;
+    return make_float4(t[0], t[1], t[2], t[3]);
+  }
   if (VEC) {
     if (AGG == kGcn) {
       const float4 s = *reinterpret_cast<const float4 *>(a.S + base + k);
@@ -81,7 +96,30 @@ __device__ inline float4 load_b(const GemmArgs &a, int col, int k) {
   return make_float4(t[0], t[1], t[2], t[3]);
 }
 
-template <int BM, int BN, int WM, int WN, int AGG, bool VEC>
+// Bias, cached transformed aggregate (kTransformFirst), activation, delta and write-back for
+// output element (row slot m with vertex v, column col).
+template <int AGG, int MODE>
+__device__ inline void epilogue(const GemmArgs &a, long long m, int v, int col, float y, float tv, float sv) {
+  const int N = a.N;
+  if (MODE == kTransformFirst) {
+    const float Tv = a.S[static_cast<long long>(v) * N + col];
+    y = AGG == kGcn ? tv * (Tv + sv * y) : y + tv * Tv;
+  }
+  y += a.bias != nullptr ? a.bias[col] : 0.f;
+  if (a.relu) y = fmaxf(y, 0.f);
+  float *hp = a.H + static_cast<long long>(v) * N + col;
+  if (a.delta != nullptr) {
+    float cn = 1.f, co = 1.f;
+    if (AGG == kGcn) {
+      cn = sv;
+      co = 1.0f / sqrtf(static_cast<float>(a.out_len[v] - a.ddeg[v]) + 1.0f);
+    }
+    a.delta[m * N + col] = cn * y - co * (*hp);
+  }
+  *hp = y;
+}
+
+template <int BM, int BN, int WM, int WN, int AGG, bool VEC, int MODE>
 __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
   using Sh = Shape<BM, BN, WM, WN>;
   if (a.abort != nullptr && *a.abort) return;
@@ -138,7 +176,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
         if (c < Sh::kAChunks) {
           const int m = c / (kBK / 4);
           const int q = c % (kBK / 4);
-          ra[i] = load_a<AGG, VEC>(a, rv[m], rt[m], rs[m], k0 + 4 * q);
+          ra[i] = load_a<AGG, VEC, MODE>(a, rv[m], rt[m], rs[m], k0 + 4 * q);
         }
       }
 #pragma unroll
@@ -214,18 +252,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
           const int ml = wm0 + i * 16 + lk * 4 + r;
           const int v = rv[ml];
           if (v < 0 || col >= N) continue;
-          float y = acc[i][j][r] + (a.bias != nullptr ? a.bias[col] : 0.f);
-          if (a.relu) y = fmaxf(y, 0.f);
-          float *hp = a.H + static_cast<long long>(v) * N + col;
-          if (a.delta != nullptr) {
-            float cn = 1.f, co = 1.f;
-            if (AGG == kGcn) {
-              cn = rs[ml];
-              co = 1.0f / sqrtf(static_cast<float>(a.out_len[v] - a.ddeg[v]) + 1.0f);
-            }
-            a.delta[(m0 + ml) * N + col] = cn * y - co * (*hp);
-          }
-          *hp = y;
+          epilogue<AGG, MODE>(a, m0 + ml, v, col, acc[i][j][r], rt[ml], rs[ml]);
         }
       }
     }
@@ -240,7 +267,7 @@ constexpr int kSmallBM = 16;
 constexpr int kSmallBK = 128;
 constexpr int kSmallLdk = kSmallBK + 4;
 
-template <int BN, int AGG, bool VEC>
+template <int BN, int AGG, bool VEC, int MODE>
 __global__ __launch_bounds__(kThreads) void k_gemm_small(GemmArgs a) {
   constexpr int WN = BN / 16;
   constexpr int kAChunks = kSmallBM * (kSmallBK / 4);
@@ -300,7 +327,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_small(GemmArgs a) {
         if (c < kAChunks) {
           const int m = c / (kSmallBK / 4);
           const int q = c % (kSmallBK / 4);
-          ra[i] = load_a<AGG, VEC>(a, rv[m], rt[m], rs[m], k0 + 4 * q);
+          ra[i] = load_a<AGG, VEC, MODE>(a, rv[m], rt[m], rs[m], k0 + 4 * q);
         }
       }
 #pragma unroll
@@ -366,87 +393,83 @@ __global__ __launch_bounds__(kThreads) void k_gemm_small(GemmArgs a) {
       const int col = n0 + cl;
       const int v = rv[ml];
       if (v < 0 || col >= N) continue;
-      float y = red[0][ml][cl] + red[1][ml][cl] + red[2][ml][cl] + red[3][ml][cl];
-      y += a.bias != nullptr ? a.bias[col] : 0.f;
-      if (a.relu) y = fmaxf(y, 0.f);
-      float *hp = a.H + static_cast<long long>(v) * N + col;
-      if (a.delta != nullptr) {
-        float cn = 1.f, co = 1.f;
-        if (AGG == kGcn) {
-          cn = rs[ml];
-          co = 1.0f / sqrtf(static_cast<float>(a.out_len[v] - a.ddeg[v]) + 1.0f);
-        }
-        a.delta[(m0 + ml) * N + col] = cn * y - co * (*hp);
-      }
-      *hp = y;
+      const float y = red[0][ml][cl] + red[1][ml][cl] + red[2][ml][cl] + red[3][ml][cl];
+      epilogue<AGG, MODE>(a, m0 + ml, v, col, y, rt[ml], rs[ml]);
     }
   }
 }
 
-template <int BN, int AGG, bool VEC>
+template <int BN, int AGG, bool VEC, int MODE>
 void launch_small(hipStream_t s, const GemmArgs &a, long long max_rows) {
   const long long tiles = ((max_rows + kSmallBM - 1) / kSmallBM) * ((a.N + BN - 1) / BN);
   long long blocks = tiles < 1 ? 1 : tiles;
   if (blocks > 2048) blocks = 2048;
-  hipLaunchKernelGGL((k_gemm_small<BN, AGG, VEC>), dim3(blocks), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL((k_gemm_small<BN, AGG, VEC, MODE>), dim3(blocks), dim3(kThreads), 0, s, a);
 }
 
-template <int BM, int BN, int WM, int WN, int AGG, bool VEC>
+template <int BM, int BN, int WM, int WN, int AGG, bool VEC, int MODE>
 void launch_shape(hipStream_t s, const GemmArgs &a, long long max_rows) {
   const long long tiles = ((max_rows + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   long long blocks = tiles < 1 ? 1 : tiles;
   if (blocks > 2048) blocks = 2048;
-  hipLaunchKernelGGL((k_gemm<BM, BN, WM, WN, AGG, VEC>), dim3(blocks), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL((k_gemm<BM, BN, WM, WN, AGG, VEC, MODE>), dim3(blocks), dim3(kThreads), 0, s, a);
 }
 
 // BN follows N. Few expected rows: the 16-row split-K kernel; many: 128-row tiles.
-template <int AGG, bool VEC>
+template <int AGG, bool VEC, int MODE>
 void launch_agg(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) {
   const int N = a.N;
   if (!VEC) {
-    if (N <= 16) launch_shape<64, 16, 1, 1, AGG, VEC>(s, a, max_rows);
-    else if (N <= 32) launch_shape<64, 32, 2, 1, AGG, VEC>(s, a, max_rows);
-    else if (N <= 48) launch_shape<64, 48, 1, 3, AGG, VEC>(s, a, max_rows);
-    else if (N <= 64) launch_shape<32, 64, 1, 2, AGG, VEC>(s, a, max_rows);
-    else launch_shape<32, 128, 2, 2, AGG, VEC>(s, a, max_rows);
+    if (N <= 16) launch_shape<64, 16, 1, 1, AGG, VEC, MODE>(s, a, max_rows);
+    else if (N <= 32) launch_shape<64, 32, 2, 1, AGG, VEC, MODE>(s, a, max_rows);
+    else if (N <= 48) launch_shape<64, 48, 1, 3, AGG, VEC, MODE>(s, a, max_rows);
+    else if (N <= 64) launch_shape<32, 64, 1, 2, AGG, VEC, MODE>(s, a, max_rows);
+    else launch_shape<32, 128, 2, 2, AGG, VEC, MODE>(s, a, max_rows);
     return;
   }
   if (!big) {
-    if (N <= 16) launch_small<16, AGG, VEC>(s, a, max_rows);
-    else if (N <= 32) launch_small<32, AGG, VEC>(s, a, max_rows);
-    else if (N <= 48) launch_small<48, AGG, VEC>(s, a, max_rows);
-    else launch_small<64, AGG, VEC>(s, a, max_rows);  // N > 64: several 64-wide column tiles
+    if (N <= 16) launch_small<16, AGG, VEC, MODE>(s, a, max_rows);
+    else if (N <= 32) launch_small<32, AGG, VEC, MODE>(s, a, max_rows);
+    else if (N <= 48) launch_small<48, AGG, VEC, MODE>(s, a, max_rows);
+    else launch_small<64, AGG, VEC, MODE>(s, a, max_rows);  // N > 64: several 64-wide column tiles
     return;
   }
-  if (N <= 16) launch_shape<64, 16, 1, 1, AGG, VEC>(s, a, max_rows);
-  else if (N <= 32) launch_shape<64, 32, 2, 1, AGG, VEC>(s, a, max_rows);
-  else if (N <= 48) launch_shape<128, 48, 2, 3, AGG, VEC>(s, a, max_rows);
-  else if (N <= 64) launch_shape<128, 64, 4, 2, AGG, VEC>(s, a, max_rows);
-  else launch_shape<128, 128, 4, 4, AGG, VEC>(s, a, max_rows);
+  if (N <= 16) launch_shape<64, 16, 1, 1, AGG, VEC, MODE>(s, a, max_rows);
+  else if (N <= 32) launch_shape<64, 32, 2, 1, AGG, VEC, MODE>(s, a, max_rows);
+  else if (N <= 48) launch_shape<128, 48, 2, 3, AGG, VEC, MODE>(s, a, max_rows);
+  else if (N <= 64) launch_shape<128, 64, 4, 2, AGG, VEC, MODE>(s, a, max_rows);
+  else launch_shape<128, 128, 4, 4, AGG, VEC, MODE>(s, a, max_rows);
 }
 
-template <int AGG>
+template <int AGG, int MODE>
 void launch_vec(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) {
   const bool vec = (a.dprev % 4 == 0) && (a.K % 4 == 0);
-  if (vec) launch_agg<AGG, true>(s, a, max_rows, big);
-  else launch_agg<AGG, false>(s, a, max_rows, big);
+  if (vec) launch_agg<AGG, true, MODE>(s, a, max_rows, big);
+  else launch_agg<AGG, false, MODE>(s, a, max_rows, big);
+}
+
+template <int MODE>
+void launch_mode(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) {
+  switch (a.agg) {
+    case kMean:
+      launch_vec<kMean, MODE>(s, a, max_rows, big);
+      break;
+    case kGcn:
+      launch_vec<kGcn, MODE>(s, a, max_rows, big);
+      break;
+    default:
+      launch_vec<kSum, MODE>(s, a, max_rows, big);
+      break;
+  }
 }
 
 }  // namespace
 
 void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows, long long expected_rows) {
   const bool big = expected_rows >= 32768;
-  switch (a.agg) {
-    case kMean:
-      launch_vec<kMean>(s, a, max_rows, big);
-      break;
-    case kGcn:
-      launch_vec<kGcn>(s, a, max_rows, big);
-      break;
-    default:
-      launch_vec<kSum>(s, a, max_rows, big);
-      break;
-  }
+  if (a.mode == kTransformFirst) launch_mode<kTransformFirst>(s, a, max_rows, big);
+  else if (a.mode == kPlain) launch_mode<kPlain>(s, a, max_rows, big);
+  else launch_mode<kLayer>(s, a, max_rows, big);
 }
 
 }  // namespace rp

@@ -48,6 +48,7 @@ struct ripple_ctx {
   int min_slack = 4;
   long long max_bytes = 0;
   long long arena_slots = 0;  // 0 = default sizing
+  long long arcs_loaded = 0;  // arcs of the snapshot
   long long bytes = 0;
   std::unordered_map<void *, size_t> allocs;
   std::string err;
@@ -67,8 +68,13 @@ struct ripple_ctx {
   int dims[rp::kMaxL + 1] = {};
   int relu[rp::kMaxL] = {};
   int K[rp::kMaxL] = {};
-  float *W[rp::kMaxL] = {};
+  float *W[rp::kMaxL] = {};     // main transform [d_l][K]
+  float *Wn[rp::kMaxL] = {};    // transform-first layers: W_neigh [d_l][d_{l-1}] (GCN: W)
+  float *P[rp::kMaxL + 1] = {};  // [l], transform-first layers: P = W_neigh H^{l-1}, [n][d_l]
   float *bias[rp::kMaxL] = {};
+  int tf[rp::kMaxL + 1] = {};   // [l]: layer l caches T = W_neigh S (width d_l)
+  int sw[rp::kMaxL + 1] = {};   // [l]: width of the cached aggregate rows
+  float *msg = nullptr;         // [n][max d_l of transform-first layers]: message rows
   float *H[rp::kMaxL + 1] = {};
   float *S[rp::kMaxL + 1] = {};
   int dmax_delta = 0;
@@ -82,6 +88,13 @@ struct ripple_ctx {
   long long *blockdeg = nullptr;
   int *lists[rp::kMaxL + 1] = {};
   long long *doff[rp::kMaxL + 1] = {};  // out-degree prefix of lists[l] (first arc index per vertex)
+  long long *ioff = nullptr;            // in-degree prefix of the current layer's A^l (pull form)
+  unsigned *keep[2] = {nullptr, nullptr};  // bitmap of lists[k] for k = 0, 1 mod 2 (pull membership)
+  int *slot[2] = {nullptr, nullptr};       // position of each vertex in lists[k] (pull message rows)
+  int scatter_mode = RIPPLE_SCATTER_AUTO;
+  long long last_pushed[rp::kMaxL + 1] = {};
+  long long last_in[rp::kMaxL + 1] = {};
+  int last_pull = 0;
   float *delta[2] = {nullptr, nullptr};
   rp::Counters *d_counters = nullptr;  // two buffers; batch parity picks one
   int parity = 0;
@@ -374,8 +387,11 @@ ripple_status ensure_batch_scratch(ripple_ctx *c, long long ops, long long frows
 void free_model(ripple_ctx *c) {
   for (int l = 0; l < rp::kMaxL; ++l) {
     dfree_t(c, c->W[l]);
+    dfree_t(c, c->Wn[l]);
     dfree_t(c, c->bias[l]);
   }
+  dfree_t(c, c->msg);
+  for (int l = 0; l <= rp::kMaxL; ++l) dfree_t(c, c->P[l]);
   for (int l = 0; l <= rp::kMaxL; ++l) {
     dfree_t(c, c->H[l]);
     dfree_t(c, c->S[l]);
@@ -384,16 +400,21 @@ void free_model(ripple_ctx *c) {
   }
   dfree_t(c, c->delta[0]);
   dfree_t(c, c->delta[1]);
+  dfree_t(c, c->ioff);
+  for (int k = 0; k < 2; ++k) {
+    dfree_t(c, c->keep[k]);
+    dfree_t(c, c->slot[k]);
+  }
   free_batch_scratch(c);
   c->inited = false;
 }
 
 rp::LayerPtrs layer_ptrs(const ripple_ctx *c) {
   rp::LayerPtrs lp{};
-  for (int l = 0; l <= c->L; ++l) {
-    lp.H[l] = c->H[l];
+  for (int l = 1; l <= c->L; ++l) {
+    lp.src[l] = c->tf[l] ? c->P[l] : c->H[l - 1];
     lp.S[l] = c->S[l];
-    lp.dims[l] = c->dims[l];
+    lp.sw[l] = c->sw[l];
   }
   lp.L = c->L;
   return lp;
@@ -403,6 +424,7 @@ rp::LayerPtrs layer_ptrs(const ripple_ctx *c) {
 rp::GemmArgs gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 *count, long long count_fixed,
                        float *delta, const u64 *abort) {
   rp::GemmArgs g{};
+  g.mode = c->tf[l] ? rp::kTransformFirst : rp::kLayer;
   g.rows = rows;
   g.count = count;
   g.count_fixed = count_fixed;
@@ -419,6 +441,35 @@ rp::GemmArgs gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 *c
   g.relu = c->relu[l - 1];
   g.H = c->H[l];
   g.delta = delta;
+  g.agg = c->agg;
+  g.abort = abort;
+  return g;
+}
+
+// P rows of transform-first layer l: P_v = W_neigh h^{l-1}_v for the vertices of
+// `rows` (nullptr: all, count_fixed of them); with msg set, also the messages
+// msg[r] = c'_v P'_v - c_v P_v (c = 1, or the GCN source coefficient after / before
+// the batch), aligned with `rows`.
+rp::GemmArgs p_gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 *count, long long count_fixed,
+                         float *msg, const u64 *abort) {
+  rp::GemmArgs g{};
+  g.mode = rp::kPlain;
+  g.rows = rows;
+  g.count = count;
+  g.count_fixed = count_fixed;
+  g.Hprev = c->H[l - 1];
+  g.dprev = c->dims[l - 1];
+  g.S = nullptr;
+  g.in_len = c->adj[1].len;
+  g.out_len = c->adj[0].len;
+  g.ddeg = c->ddeg;
+  g.W = c->Wn[l - 1];
+  g.K = c->dims[l - 1];
+  g.N = c->dims[l];
+  g.bias = nullptr;
+  g.relu = 0;
+  g.H = c->P[l];
+  g.delta = msg;
   g.agg = c->agg;
   g.abort = abort;
   return g;
@@ -462,6 +513,29 @@ void add_launches(ripple_ctx *c, int phase, int k) {
   if (c->prof) c->ph_launch[phase] += k;
 }
 
+// Push or pull for layer l. Forced modes aside, estimate the bytes of each form
+// from the previous batch's counts for this layer: push moves every message as a
+// row of atomics (weighted 4x: atomics run at about a quarter of the read rate);
+// pull reads every in-arc of A^l, reads each message once and makes one atomic
+// row update per affected vertex.
+bool use_pull(const ripple_ctx *c, int l) {
+  if (c->scatter_mode == RIPPLE_SCATTER_PUSH) return false;
+  if (c->scatter_mode == RIPPLE_SCATTER_PULL) return true;
+  if (!c->has_batch) return false;
+  const double w = 4.0 * c->sw[l];
+  const double push = 4.0 * w * static_cast<double>(c->last_pushed[l]);
+  const double pull = 12.0 * static_cast<double>(c->last_in[l]) + w * static_cast<double>(c->last_pushed[l]) +
+                      4.0 * w * static_cast<double>(c->last_count[l]);
+  return pull < push;
+}
+
+// One-launch compaction for small graphs whose frontier stayed small last batch.
+bool single_compact(const ripple_ctx *c, int l) {
+  const long long words = (c->n + 31) / 32;
+  const long long hint = c->has_batch ? c->last_count[l] : c->n;
+  return words <= 16384 && hint <= 32768;
+}
+
 // Issues one batch. Returns after queuing; the caller syncs.
 void issue_batch(ripple_ctx *c, int B) {
   hipStream_t s = c->stream;
@@ -469,6 +543,7 @@ void issue_batch(ripple_ctx *c, int B) {
   rp::Counters *dnext = c->d_counters + (c->parity ^ 1);
   const int cap_arcs = static_cast<int>(2 * c->cap_ops);
   rp::Adj out = c->adj[0], in = c->adj[1];
+  c->last_pull = 0;
   PhaseScope total(c, RIPPLE_PHASE_TOTAL);
   {
     PhaseScope ps(c, RIPPLE_PHASE_NET);
@@ -492,8 +567,14 @@ void issue_batch(ripple_ctx *c, int B) {
     PhaseScope ps(c, RIPPLE_PHASE_LAYER0);
     rp::launch_corr_mark(s, static_cast<int>(c->cap_ops), cap_arcs, c->agg, layer_ptrs(c), c->adj[0].len, c->ddeg,
                          c->flist, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->bm_x, dc);
-    rp::launch_compact(s, c->n, c->bm_out, c->bm_x, c->blocksum, c->blockdeg, c->adj[0].len, c->lists[0],
-                       c->doff[0], &dc->count[0]);
+    rp::CompactOut co{};
+    co.list = c->lists[0];
+    co.count = &dc->count[0];
+    co.out_deg = c->adj[0].len;
+    co.doff = c->doff[0];
+    co.keep = use_pull(c, 1) ? c->keep[0] : nullptr;
+    co.slot = use_pull(c, 1) ? c->slot[0] : nullptr;
+    rp::launch_compact(s, c->n, c->bm_out, c->bm_x, c->blocksum, c->blockdeg, co, single_compact(c, 0));
     rp::launch_delta0(s, c->n, c->agg, c->dims[0], c->lists[0], &dc->count[0], c->d_ops, c->h_feat, c->fop,
                       c->H[0], c->adj[0].len, c->ddeg, c->delta[0], dc);
     add_launches(c, RIPPLE_PHASE_LAYER0, 4);
@@ -501,17 +582,46 @@ void issue_batch(ripple_ctx *c, int B) {
   for (int l = 1; l <= c->L; ++l) {
     float *din = c->delta[(l - 1) & 1];
     float *dout = l < c->L ? c->delta[l & 1] : nullptr;
+    const float *msg = din;
+    if (c->tf[l]) {
+      // transform-first layer: refresh P = W_neigh h for the dirty rows and form
+      // their messages c' P' - c P
+      PhaseScope ps(c, RIPPLE_PHASE_GEMM);
+      rp::launch_gemm(s, p_gemm_args(c, l, c->lists[l - 1], &dc->count[l - 1], 0, c->msg, &dc->abort), c->n,
+                      c->has_batch ? c->last_count[l - 1] : 0);
+      add_launches(c, RIPPLE_PHASE_GEMM, 1);
+      msg = c->msg;
+    }
+    const bool pull = use_pull(c, l);
+    if (pull) c->last_pull |= 1 << l;
     {
+      // push: marks + atomic adds; pull: marks only (the adds follow the compaction)
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
-      rp::launch_scatter(s, c->n, c->dims[l - 1], c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], din, out,
-                         c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], &dc->dest[l], dc);
+      rp::launch_scatter(s, c->n, c->sw[l], c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out, c->S[l],
+                         c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], &dc->dest[l], dc, !pull);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     {
       PhaseScope ps(c, RIPPLE_PHASE_COMPACT);
-      rp::launch_compact(s, c->n, c->bm_out, c->bm_x, c->blocksum, c->blockdeg, l < c->L ? c->adj[0].len : nullptr,
-                         c->lists[l], c->doff[l], &dc->count[l]);
+      rp::CompactOut co{};
+      co.list = c->lists[l];
+      co.count = &dc->count[l];
+      co.out_deg = c->adj[0].len;
+      co.doff = l < c->L ? c->doff[l] : nullptr;
+      co.in_deg = c->adj[1].len;
+      co.ioff = pull ? c->ioff : nullptr;
+      co.in_total = &dc->indeg[l];
+      const bool next_pull = l < c->L && use_pull(c, l + 1);
+      co.keep = next_pull ? c->keep[l & 1] : nullptr;
+      co.slot = next_pull ? c->slot[l & 1] : nullptr;
+      rp::launch_compact(s, c->n, c->bm_out, c->bm_x, c->blocksum, c->blockdeg, co, single_compact(c, l));
       add_launches(c, RIPPLE_PHASE_COMPACT, 2);
+    }
+    if (pull) {
+      PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
+      rp::launch_pull_msgs(s, c->n, c->sw[l], c->lists[l], &dc->count[l], c->ioff, in, c->keep[(l - 1) & 1],
+                           c->slot[(l - 1) & 1], msg, c->S[l], dc);
+      add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     {
       PhaseScope ps(c, RIPPLE_PHASE_GEMM);
@@ -540,9 +650,16 @@ void account_phases(ripple_ctx *c) {
   c->ph_launch[RIPPLE_PHASE_TOTAL] += 1;
   const double words = static_cast<double>((c->n + 31) / 32);
   for (int l = 1; l <= c->L; ++l) {
-    const double d = c->dims[l - 1];
+    const double d = c->sw[l];
     const double nd = static_cast<double>(k.count[l - 1]);
     c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * k.pushed[l] + 8.0 * nd + 4.0 * d * nd + 8.0 * d * k.dest[l];
+    if (c->last_pull >> l & 1)  // pull: every in-arc id of A^l and its in-row offset
+      c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * k.indeg[l] + 12.0 * k.count[l];
+    if (c->tf[l]) {
+      const double dp = c->dims[l - 1];
+      c->ph_flops[RIPPLE_PHASE_GEMM] += 2.0 * nd * dp * d;
+      c->ph_bytes[RIPPLE_PHASE_GEMM] += 4.0 * nd * dp + 4.0 * d * dp + 12.0 * nd * d;  // h rows, W, P old/new, msg
+    }
     const double m = static_cast<double>(k.count[l]);
     const double K = c->K[l - 1], N = c->dims[l];
     c->ph_flops[RIPPLE_PHASE_GEMM] += 2.0 * m * K * N;
@@ -665,6 +782,7 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   c->arena_slots = g->arena_slots;
   // host-side validation and counting sort into CSR (by source) and CSC (by sink)
   const long long arcs = c->undirected ? 2 * m : m;
+  c->arcs_loaded = arcs;
   std::vector<int> outdeg(n, 0), indeg(n, 0);
   for (long long i = 0; i < m; ++i) {
     const int u = g->src[i], v = g->dst[i];
@@ -757,7 +875,7 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   if ((st = dalloc_n(c, &c->bm_out, words)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->bm_x, words)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->blocksum, rp::compact_blocks(n) + 1)) != RIPPLE_OK) return bail(st);
-  if ((st = dalloc_n(c, &c->blockdeg, rp::compact_blocks(n) + 1)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->blockdeg, 2 * rp::compact_blocks(n) + 2)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->rl_blocksums, rp::relayout_blocks(n) + 1)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->rl_off, n)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->rl_cap, n)) != RIPPLE_OK) return bail(st);
@@ -790,6 +908,8 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
     if (md->w_neigh[l] == nullptr || (md->agg != RIPPLE_AGG_GCN && md->w_self[l] == nullptr))
       return fail(c, RIPPLE_E_INVALID, "ripple: missing weight matrix");
   }
+  if (md->transform_first < -1 || md->transform_first > 1)
+    return fail(c, RIPPLE_E_INVALID, "ripple: transform_first must be -1, 0 or 1");
   free_model(c);
   c->L = L;
   c->agg = md->agg;
@@ -797,23 +917,30 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   c->dmax_delta = 0;
   for (int l = 0; l < L; ++l) c->dmax_delta = std::max(c->dmax_delta, c->dims[l]);
   const long long n = c->n;
-  // weights: SAGE W = [W_self | W_neigh] (K = 2 d_{l-1}); GCN W (K = d_{l-1})
+  int msg_width = 0;
   for (int l = 1; l <= L; ++l) {
     const int dp = c->dims[l - 1], dn = c->dims[l];
-    const int K = md->agg == RIPPLE_AGG_GCN ? dp : 2 * dp;
+    const long long arcs = c->arcs_loaded;
+    c->tf[l] = md->transform_first == 1 || (md->transform_first == -1 && dn < dp && arcs >= (1LL << 24));
+    c->sw[l] = c->tf[l] ? dn : dp;
+    if (c->tf[l]) msg_width = std::max(msg_width, dn);
+  }
+  // weights. Plain layers: SAGE W = [W_self | W_neigh] (K = 2 d_{l-1}), GCN W
+  // (K = d_{l-1}). Transform-first layers: W = W_self (SAGE) or W (GCN), K =
+  // d_{l-1}, plus W_neigh (GCN: W) for the messages and corrections.
+  for (int l = 1; l <= L; ++l) {
+    const int dp = c->dims[l - 1], dn = c->dims[l];
+    const bool gcn = md->agg == RIPPLE_AGG_GCN;
+    const int K = (gcn || c->tf[l]) ? dp : 2 * dp;
     c->K[l - 1] = K;
     c->relu[l - 1] = md->relu[l - 1] ? 1 : 0;
+    const float *wmain = gcn ? md->w_neigh[l - 1] : md->w_self[l - 1];
     std::vector<float> w(static_cast<size_t>(dn) * K);
     for (int j = 0; j < dn; ++j) {
-      if (md->agg == RIPPLE_AGG_GCN) {
-        std::memcpy(&w[static_cast<size_t>(j) * K], md->w_neigh[l - 1] + static_cast<size_t>(j) * dp,
-                    dp * sizeof(float));
-      } else {
-        std::memcpy(&w[static_cast<size_t>(j) * K], md->w_self[l - 1] + static_cast<size_t>(j) * dp,
-                    dp * sizeof(float));
+      std::memcpy(&w[static_cast<size_t>(j) * K], wmain + static_cast<size_t>(j) * dp, dp * sizeof(float));
+      if (K == 2 * dp)
         std::memcpy(&w[static_cast<size_t>(j) * K + dp], md->w_neigh[l - 1] + static_cast<size_t>(j) * dp,
                     dp * sizeof(float));
-      }
     }
     std::vector<float> b(dn, 0.0f);
     if (md->bias != nullptr && md->bias[l - 1] != nullptr) std::memcpy(b.data(), md->bias[l - 1], dn * sizeof(float));
@@ -821,21 +948,41 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
     RP_TRY(dalloc_n(c, &c->bias[l - 1], dn));
     RP_HIP(c, hipMemcpyAsync(c->W[l - 1], w.data(), w.size() * sizeof(float), hipMemcpyHostToDevice, c->stream));
     RP_HIP(c, hipMemcpyAsync(c->bias[l - 1], b.data(), dn * sizeof(float), hipMemcpyHostToDevice, c->stream));
+    if (c->tf[l]) {
+      RP_TRY(dalloc_n(c, &c->Wn[l - 1], static_cast<long long>(dn) * dp));
+      RP_HIP(c, hipMemcpyAsync(c->Wn[l - 1], md->w_neigh[l - 1], static_cast<size_t>(dn) * dp * sizeof(float),
+                               hipMemcpyHostToDevice, c->stream));
+    }
     RP_HIP(c, hipStreamSynchronize(c->stream));
   }
   for (int l = 0; l <= L; ++l) {
     RP_TRY(dalloc_n(c, &c->H[l], n * c->dims[l]));
     RP_TRY(dalloc_n(c, &c->lists[l], n));
     RP_TRY(dalloc_n(c, &c->doff[l], n + 1));
-    if (l >= 1) RP_TRY(dalloc_n(c, &c->S[l], n * c->dims[l - 1]));
+    if (l >= 1) RP_TRY(dalloc_n(c, &c->S[l], n * c->sw[l]));
   }
   RP_TRY(dalloc_n(c, &c->delta[0], n * c->dmax_delta));
   RP_TRY(dalloc_n(c, &c->delta[1], n * c->dmax_delta));
+  RP_TRY(dalloc_n(c, &c->ioff, n + 1));
+  for (int k = 0; k < 2; ++k) {
+    RP_TRY(dalloc_n(c, &c->keep[k], (n + 31) / 32));
+    RP_TRY(dalloc_n(c, &c->slot[k], n));
+  }
+  if (msg_width > 0) RP_TRY(dalloc_n(c, &c->msg, n * msg_width));
+  for (int l = 1; l <= L; ++l)
+    if (c->tf[l]) RP_TRY(dalloc_n(c, &c->P[l], n * c->dims[l]));
   RP_HIP(c, hipMemcpyAsync(c->H[0], x, static_cast<size_t>(n) * c->dims[0] * sizeof(float), hipMemcpyHostToDevice,
                            c->stream));
-  // bootstrap: layer-wise full forward pass (pull aggregate over in-rows, then transform)
+  // bootstrap: layer-wise full forward pass. Plain layers pull the previous
+  // layer's rows over the in-rows, then transform; transform-first layers
+  // transform every row by W_neigh first and pull the narrower result.
   for (int l = 1; l <= L; ++l) {
-    rp::launch_pull(c->stream, n, c->dims[l - 1], c->agg, c->H[l - 1], c->adj[1], c->adj[0].len, c->S[l]);
+    if (c->tf[l]) {
+      rp::launch_gemm(c->stream, p_gemm_args(c, l, nullptr, nullptr, n, nullptr, nullptr), n, n);
+      rp::launch_pull(c->stream, n, c->dims[l], c->agg, c->P[l], c->adj[1], c->adj[0].len, c->S[l]);
+    } else {
+      rp::launch_pull(c->stream, n, c->dims[l - 1], c->agg, c->H[l - 1], c->adj[1], c->adj[0].len, c->S[l]);
+    }
     rp::launch_gemm(c->stream, gemm_args(c, l, nullptr, nullptr, n, nullptr, nullptr), n, n);
     RP_HIP(c, hipGetLastError());
   }
@@ -886,7 +1033,11 @@ ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t 
   account_phases(c);
   c->has_batch = true;
   c->last_nfeat = static_cast<long long>(k.n_feat);
-  for (int l = 0; l <= c->L; ++l) c->last_count[l] = static_cast<long long>(k.count[l]);
+  for (int l = 0; l <= c->L; ++l) {
+    c->last_count[l] = static_cast<long long>(k.count[l]);
+    c->last_pushed[l] = static_cast<long long>(k.pushed[l]);
+    c->last_in[l] = static_cast<long long>(k.indeg[l]);
+  }
   if (stats != nullptr) {
     std::memset(stats, 0, sizeof(*stats));
     stats->num_ops = num_ops;
@@ -904,6 +1055,8 @@ ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t 
     }
     stats->relocated_rows = static_cast<int64_t>(k.n_reloc);
     stats->repacks = repacks;
+    for (int l = 1; l <= c->L; ++l) stats->in_arcs[l] = static_cast<int64_t>(k.indeg[l]);
+    stats->pull_layers = c->last_pull;
   }
   return RIPPLE_OK;
 }
@@ -915,11 +1068,13 @@ ripple_status ripple_get_embeddings(ripple_ctx *c, int32_t layer, const int32_t 
   return read_rows(c, c->H[layer], c->dims[layer], ids, count, out);
 }
 
-ripple_status ripple_get_aggregates(ripple_ctx *c, int32_t layer, const int32_t *ids, int64_t count, float *out) {
+ripple_status ripple_get_aggregates(ripple_ctx *c, int32_t layer, const int32_t *ids, int64_t count, float *out,
+                                    int32_t *width) {
   RP_TRY(check_ctx(c));
   if (!c->inited) return fail(c, RIPPLE_E_STATE, "ripple: ripple_init_embeddings has not run");
   if (layer < 1 || layer > c->L) return fail(c, RIPPLE_E_INVALID, "ripple: layer out of range");
-  return read_rows(c, c->S[layer], c->dims[layer - 1], ids, count, out);
+  if (width != nullptr) *width = c->sw[layer];
+  return read_rows(c, c->S[layer], c->sw[layer], ids, count, out);
 }
 
 ripple_status ripple_get_affected(ripple_ctx *c, int32_t layer, int32_t *ids, int64_t capacity, int64_t *count) {
@@ -981,6 +1136,13 @@ ripple_status ripple_get_arcs(ripple_ctx *c, int32_t direction, int32_t *src, in
     }
   }
   *count = k;
+  return RIPPLE_OK;
+}
+
+ripple_status ripple_set_scatter_mode(ripple_ctx *c, int32_t mode) {
+  RP_TRY(check_ctx(c));
+  if (mode < RIPPLE_SCATTER_AUTO || mode > RIPPLE_SCATTER_PULL) return fail(c, RIPPLE_E_INVALID, "ripple: bad mode");
+  c->scatter_mode = mode;
   return RIPPLE_OK;
 }
 

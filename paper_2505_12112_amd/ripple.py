@@ -29,8 +29,9 @@ EXPORTED = [
     "ripple_load_graph", "ripple_init_embeddings", "ripple_apply_updates", "ripple_get_embeddings",
     "ripple_get_affected", "ripple_get_aggregates", "ripple_get_arcs", "ripple_device_bytes",
     "ripple_set_profiling", "ripple_get_phase_stats", "ripple_phase_name", "ripple_last_error",
-    "ripple_destroy",
+    "ripple_destroy", "ripple_set_scatter_mode",
 ]
+SCATTER = {"auto": 0, "push": 1, "pull": 2}
 
 
 class RippleUnavailable(RuntimeError):
@@ -58,7 +59,7 @@ class ModelDesc(C.Structure):
         ("num_layers", C.c_int32), ("agg", C.c_int32), ("dims", C.POINTER(C.c_int32)),
         ("w_self", C.POINTER(C.POINTER(C.c_float))), ("w_neigh", C.POINTER(C.POINTER(C.c_float))),
         ("bias", C.POINTER(C.POINTER(C.c_float))), ("relu", C.POINTER(C.c_int32)),
-        ("gemm_prec", C.c_int32),
+        ("gemm_prec", C.c_int32), ("transform_first", C.c_int32),
     ]
 
 
@@ -69,6 +70,7 @@ class BatchStats(C.Structure):
         ("dirty", C.c_int64 * (MAX_LAYERS + 1)), ("affected", C.c_int64 * (MAX_LAYERS + 1)),
         ("pushed_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("dest_rows", C.c_int64 * (MAX_LAYERS + 1)),
         ("relocated_rows", C.c_int64), ("repacks", C.c_int64),
+        ("in_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("pull_layers", C.c_int32), ("pad", C.c_int32),
     ]
 
 
@@ -93,11 +95,12 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.ripple_init_embeddings.argtypes = [vp, P(C.c_float), P(ModelDesc)]
     lib.ripple_apply_updates.argtypes = [vp, P(C.c_int32), C.c_int64, P(C.c_float), C.c_int64, P(BatchStats)]
     lib.ripple_get_embeddings.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_float)]
-    lib.ripple_get_aggregates.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_float)]
+    lib.ripple_get_aggregates.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_float), P(C.c_int32)]
     lib.ripple_get_affected.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_int64)]
     lib.ripple_get_arcs.argtypes = [vp, C.c_int32, P(C.c_int32), P(C.c_int32), C.c_int64, P(C.c_int64)]
     lib.ripple_device_bytes.argtypes = [vp, P(C.c_int64)]
     lib.ripple_set_profiling.argtypes = [vp, C.c_int32]
+    lib.ripple_set_scatter_mode.argtypes = [vp, C.c_int32]
     lib.ripple_get_phase_stats.argtypes = [vp, P(PhaseStats), C.c_int32]
     lib.ripple_phase_name.argtypes = [C.c_int32]
     lib.ripple_phase_name.restype = C.c_char_p
@@ -168,8 +171,9 @@ class Ripple:
         self.close()
 
     # -- calls --
-    def init_embeddings(self, x, weights, gemm: str = "fp32"):
-        """weights: object with agg, dims, w_self, w_neigh, bias, relu (synth.ModelWeights)."""
+    def init_embeddings(self, x, weights, gemm: str = "fp32", transform_first: int = -1):
+        """weights: object with agg, dims, w_self, w_neigh, bias, relu (synth.ModelWeights).
+        transform_first: -1 for layers that narrow (d_l < d_{l-1}), 0 never, 1 always."""
         x = _f32(x)
         dims = _i32(weights.dims)
         L = len(dims) - 1
@@ -192,7 +196,7 @@ class Ripple:
         relu = _i32([1 if r else 0 for r in weights.relu])
         keep.append(relu)
         md = ModelDesc(L, AGG[weights.agg], _ptr(dims, C.c_int32), ws, wn, bs, _ptr(relu, C.c_int32),
-                       GEMM[gemm])
+                       GEMM[gemm], int(transform_first))
         self._check(self._lib.ripple_init_embeddings(self._ctx, _ptr(x, C.c_float), C.byref(md)))
         self.dims = [int(d) for d in dims]
         self.num_layers = L
@@ -211,6 +215,7 @@ class Ripple:
             "dirty": list(st.dirty[:L + 1]), "affected": list(st.affected[:L + 1]),
             "pushed_arcs": list(st.pushed_arcs[:L + 1]), "dest_rows": list(st.dest_rows[:L + 1]),
             "relocated_rows": st.relocated_rows, "repacks": st.repacks,
+            "in_arcs": list(st.in_arcs[:L + 1]), "pull_layers": st.pull_layers,
         }
 
     def apply_updates_raw(self, ops: np.ndarray, feat_rows: Optional[np.ndarray], stats: BatchStats) -> None:
@@ -233,16 +238,23 @@ class Ripple:
                                                         _ptr(out, C.c_float)))
         return out
 
+    def aggregate_width(self, layer: int) -> int:
+        w = C.c_int32()
+        self._check(self._lib.ripple_get_aggregates(self._ctx, layer, None, 0, None, C.byref(w)))
+        return w.value
+
     def get_aggregates(self, layer: int, ids: Optional[Sequence[int]] = None) -> np.ndarray:
-        d = self.dims[layer - 1]
+        """The cached aggregate rows of a layer: S (width d_{l-1}) or, for a
+        transform-first layer, W_neigh S (width d_l)."""
+        d = self.aggregate_width(layer)
         if ids is None:
             out = np.empty((self.n, d), np.float32)
-            self._check(self._lib.ripple_get_aggregates(self._ctx, layer, None, self.n, _ptr(out, C.c_float)))
+            self._check(self._lib.ripple_get_aggregates(self._ctx, layer, None, self.n, _ptr(out, C.c_float), None))
         else:
             ids = _i32(ids)
             out = np.empty((ids.size, d), np.float32)
             self._check(self._lib.ripple_get_aggregates(self._ctx, layer, _ptr(ids, C.c_int32), ids.size,
-                                                        _ptr(out, C.c_float)))
+                                                        _ptr(out, C.c_float), None))
         return out
 
     def get_affected(self, layer: int) -> np.ndarray:
@@ -263,6 +275,10 @@ class Ripple:
             self._check(self._lib.ripple_get_arcs(self._ctx, direction, _ptr(s, C.c_int32), _ptr(d, C.c_int32),
                                                   s.size, C.byref(cnt)))
         return s, d
+
+    def set_scatter_mode(self, mode: str):
+        """"auto" (default), "push" or "pull": how layers add their messages."""
+        self._check(self._lib.ripple_set_scatter_mode(self._ctx, SCATTER[mode]))
 
     def device_bytes(self) -> int:
         b = C.c_int64()

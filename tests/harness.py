@@ -12,9 +12,10 @@ FP32_TOL = 1e-4   # max row-relative error for the fp32 path
 
 
 class Pair:
-    def __init__(self, n, src, dst, x, weights, undirected=False, **lib_kw):
+    def __init__(self, n, src, dst, x, weights, undirected=False, transform_first=-1, mode="auto", **lib_kw):
         self.lib = Ripple(n, src, dst, undirected=undirected, **lib_kw)
-        self.lib.init_embeddings(x, weights)
+        self.lib.init_embeddings(x, weights, transform_first=transform_first)
+        self.lib.set_scatter_mode(mode)
         self.orc = O.OracleState(n, src, dst, x, O.OracleModel.from_weights(weights), undirected)
         self.L = len(weights.dims) - 1
         self.n = n
@@ -73,6 +74,8 @@ class Pair:
         for l in range(1, self.L + 1):
             want = a @ ref[l - 1]
             got = self.lib.get_aggregates(l).astype(np.float64)
+            if got.shape[1] != want.shape[1]:   # cached transformed: W_neigh S
+                want = want @ self.orc.model.w_neigh[l - 1].T
             rms = float(np.sqrt(np.mean(want * want))) + 1e-30
             num = np.max(np.abs(got - want), axis=1)
             den = np.maximum(np.max(np.abs(want), axis=1), rms)

@@ -107,7 +107,9 @@ def test_dense_large_full_size():
         rng = np.random.default_rng(5)
         for b in range(3):
             st, _, sets = p.step(wl.stream.next_batch(100))
-            _say(f"  batch {b}: |A| = {[s.size for s in sets]} ({time.time() - t0:.0f}s)")
+            _say(f"  batch {b}: |A| = {[s.size for s in sets]}, pull layers {st['pull_layers']:b} "
+                 f"({time.time() - t0:.0f}s)")
+        assert st["pull_layers"] & 0b1000, "dense third layer should switch to the pull form"
         verts = _sample_vertices(rng, p.orc, sets[3], 24, 400_000)
         errs = _check_sampled(p, verts, (1, 2, 3))
         _say(f"  {verts.size} sampled vertices, row-relative errors {errs} ({time.time() - t0:.0f}s)")
@@ -122,10 +124,11 @@ def test_stress_full_size():
     t0 = time.time()
     wl = synth.build_workload("stress")
     _say(f"stress generated in {time.time() - t0:.0f}s")
-    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights)
+    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, mode="pull")
     try:
         _say(f"  loaded + bootstrapped, oracle built ({time.time() - t0:.0f}s)")
         st, _, sets = p.step(wl.stream.next_batch(10_000))
+        assert st["pull_layers"] == 0b110
         _say(f"  batch: |A| = {[s.size for s in sets]}, pushed {st['pushed_arcs']} ({time.time() - t0:.0f}s)")
         rng = np.random.default_rng(6)
         verts = _sample_vertices(rng, p.orc, sets[2], 24, 2_000_000)

@@ -42,11 +42,12 @@ def test_bootstrap_matches_full_recompute(agg, dims):
         p.close()
 
 
-def test_tiny_config_stream():
+@pytest.mark.parametrize("mode", ["push", "pull"])
+def test_tiny_config_stream(mode):
     """The tiny workload as specified: 10 batches of 45 inserts, 45 deletes, 10 features."""
-    _say("tiny config")
+    _say("tiny config", mode)
     wl = synth.build_workload("tiny")
-    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights)
+    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, mode=mode)
     try:
         for b in range(10):
             st, net, sets = p.step(wl.stream.next_batch(100))
@@ -60,14 +61,15 @@ def test_tiny_config_stream():
 
 @pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
 @pytest.mark.parametrize("undirected", [False, True])
-def test_adversarial_batches(agg, undirected):
+@pytest.mark.parametrize("mode", ["push", "pull"])
+def test_adversarial_batches(agg, undirected, mode):
     """Colliding ops: repeated inserts/deletes of one edge, insert-then-delete,
     absent deletes, self-loops, repeated feature writes (sequential semantics)."""
-    _say("adversarial", agg, undirected)
+    _say("adversarial", agg, undirected, mode)
     rng = np.random.default_rng(7 + 3 * ("sum", "mean", "gcn").index(agg) + undirected)
     dims = (12, 40, 9)
     src, dst, x, w = _small(rng, 300, 1200, dims, agg, undirected)
-    p = Pair(300, src, dst, x, w, undirected=undirected)
+    p = Pair(300, src, dst, x, w, undirected=undirected, mode=mode)
     try:
         for b in range(25):
             a, bb = p.orc.graph.arcs()
@@ -107,6 +109,34 @@ def test_no_slack_forces_row_moves_and_relayouts(agg, arena):
         p.check_arcs()
         p.check_embeddings()
         _say("rows moved", moved, "re-layouts", relayouts)
+    finally:
+        p.close()
+
+
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
+@pytest.mark.parametrize("tf", [0, 1])
+@pytest.mark.parametrize("mode", ["push", "pull"])
+def test_transform_first_choice_gives_the_same_results(agg, tf, mode):
+    """Caching W_neigh S instead of S (and pushing W_neigh times the deltas) on
+    every layer, or on none, matches the oracle like the default choice."""
+    _say("transform_first", tf, agg)
+    rng = np.random.default_rng(21 + tf + 3 * ("sum", "mean", "gcn").index(agg))
+    dims = (24, 40, 12, 20)
+    src, dst, x, w = _small(rng, 400, 2400, dims, agg)
+    p = Pair(400, src, dst, x, w, transform_first=tf, mode=mode)
+    try:
+        p.check_embeddings()
+        p.check_aggregates()
+        for b in range(40):
+            a, bb = p.orc.graph.arcs()
+            if b % 2:
+                batch = synth.adversarial_batch(rng, 400, dims[0], bs=30, hot=12, existing=(a, bb))
+            else:
+                batch = random_valid_batch(rng, p.orc, 25, dims[0])
+            p.step(batch)
+        p.check_embeddings()
+        p.check_aggregates()
+        p.check_arcs()
     finally:
         p.close()
 
@@ -191,13 +221,14 @@ def test_call_order_and_device_byte_cap():
 
 
 @pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
-def test_thousand_batches_on_a_small_graph(agg):
+@pytest.mark.parametrize("mode", ["auto", "pull"])
+def test_thousand_batches_on_a_small_graph(agg, mode):
     """1000 consecutive batches: sets every batch, embeddings every 100 and at the end."""
-    _say("1000 batches", agg)
+    _say("1000 batches", agg, mode)
     rng = np.random.default_rng(16 + ("sum", "mean", "gcn").index(agg))
     dims = (16, 32, 8)
     src, dst, x, w = _small(rng, 400, 2400, dims, agg)
-    p = Pair(400, src, dst, x, w)
+    p = Pair(400, src, dst, x, w, mode=mode)
     try:
         worst = 0.0
         for b in range(1000):
