@@ -39,9 +39,10 @@
  *   - The library owns all device memory (hipMalloc on the context's device).
  *   - Inputs are validated before any state changes: RIPPLE_E_INVALID leaves the
  *     context exactly as it was.
- *   - A HIP runtime error poisons the context: that call returns RIPPLE_E_DEVICE
- *     and every later call except ripple_last_error / ripple_destroy returns
- *     RIPPLE_E_STATE.
+ *   - A HIP runtime error, or a failed device-side consistency check (a deleted
+ *     arc missing from its row, a row length mismatch, a compaction wait that
+ *     timed out), poisons the context: that call returns RIPPLE_E_DEVICE and every
+ *     later call except ripple_last_error / ripple_destroy returns RIPPLE_E_STATE.
  *   - A context is used by one host thread at a time. Calls are synchronous:
  *     they return after the device work they issued has finished.
  */
@@ -70,7 +71,7 @@ typedef enum {
   RIPPLE_E_INVALID = 1, /* bad argument; state unchanged */
   RIPPLE_E_STATE = 2,   /* call out of order (e.g. apply before init) or poisoned context */
   RIPPLE_E_OOM = 3,     /* device allocation failed or would exceed max_device_bytes */
-  RIPPLE_E_DEVICE = 4   /* HIP runtime error; the context is now poisoned */
+  RIPPLE_E_DEVICE = 4   /* HIP error or device-side check failed; the context is now poisoned */
 } ripple_status;
 
 typedef enum { RIPPLE_AGG_SUM = 0, RIPPLE_AGG_MEAN = 1, RIPPLE_AGG_GCN = 2 } ripple_agg;

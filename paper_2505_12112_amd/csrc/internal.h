@@ -35,7 +35,8 @@ struct Counters {
   u64 abort;              // 1: the spare arena cannot hold this batch; nothing was mutated
   u64 n_reloc;            // rows to move to the arena
   u64 arena_need[2];      // arena slots those moves need, per direction
-  u64 err;                // device-detected inconsistency (bit 0: deleted arc not found)
+  u64 err;                // device-side check failed: bit 0 deleted arc not found, bit 1 row length
+                          // mismatch, bit 2 compaction wait timed out
   u64 plan_done;          // blocks of the plan kernel that finished (last one checks the arena)
   u64 count[kMaxL + 1];   // [0] = |dirty set of layer 1|, [l] = |A^l|
   u64 pushed[kMaxL + 1];  // [l] = out-arcs pushed at layer l
@@ -121,14 +122,23 @@ struct CompactOut {
   const int *in_deg;
   long long *ioff;
   u64 *in_total;       // receives the sum of in_deg over the list
+  u64 *out_total;      // receives the sum of out_deg over the list (the next scatter's arcs)
+  u64 *sinks_a;        // receives the number of bits set in the first bitmap
   unsigned *keep;
   int *slot;
 };
-// in_total (nullable) receives the sum of in_deg over the list even without ioff.
-// Scratch: blocksum[compact_blocks(n)], blockdeg[2 * compact_blocks(n)].
-// single_block: one 1024-thread block walks all words (fewer launches; for small n).
-void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, int *blocksum,
-                    long long *blockdeg, const CompactOut &o, bool single_block);
+// Tile sums published by the single-pass compaction: compact_scratch_words(n)
+// words, zero when first used; epoch cycles through 1..65535, one per launch.
+struct CompactScratch {
+  u64 *words;
+  u64 epoch;
+  u64 *err;  // bit 2 set if a wait for a predecessor tile timed out
+};
+long long compact_scratch_words(long long n);
+// Compacts bm_a | bm_b (both cleared) into o. in_total / out_total (nullable)
+// receive the degree sums over the list even when the prefix arrays are not wanted.
+void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, const CompactScratch &cs,
+                    const CompactOut &o);
 
 // layer 0 deltas (feat may be pinned host memory)
 void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list, const u64 *count,
@@ -139,9 +149,11 @@ void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list,
 // gives each listed vertex's first arc); marks the sinks in bm_out, and the
 // listed vertices and the sinks of net arcs in bm_x. With push = false it only
 // marks (the pull kernel then adds the messages).
+// pushed = the number of arcs to push (the out-degree sum over the list, written
+// by the compaction that built the list).
 void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
-                    const int *del_dst, u64 *pushed, u64 *dest, const Counters *c, bool push);
+                    const int *del_dst, const u64 *pushed, const Counters *c, bool push);
 
 // pull: for every vertex v of the sorted list A (in-arc prefix ioff), S[v] +=
 // sum of msg[slot[u]] over in-arcs (u -> v) whose source u is set in member.

@@ -30,51 +30,14 @@ __device__ inline long long num_waves() {
   return static_cast<long long>(gridDim.x) * blockDim.x / kWave;
 }
 
-__device__ inline bool mark(unsigned *bm, int v) {
-  const unsigned bit = 1u << (v & 31);
-  return (atomicOr(&bm[v >> 5], bit) & bit) == 0;
-}
+// Sets v's bit; the old word is not read back, so nothing waits on it.
+__device__ inline void mark_only(unsigned *bm, int v) { atomicOr(&bm[v >> 5], 1u << (v & 31)); }
 
 inline int blocks_for(long long items, int threads, int cap = 4096) {
   long long b = (items + threads - 1) / threads;
   if (b < 1) b = 1;
   if (b > cap) b = cap;
   return static_cast<int>(b);
-}
-
-// Exclusive scan of v over the block; *total receives the block sum.
-template <typename T>
-__device__ inline T block_exclusive_scan(T v, T *lds, T *total) {
-  const int lane = lane_id(), wave = threadIdx.x / kWave;
-  T x = v;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const T y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  if (lane == kWave - 1) lds[wave] = x;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    T run = 0;
-    for (int w = 0; w < kCompactWaves; ++w) {
-      const T t = lds[w];
-      lds[w] = run;
-      run += t;
-    }
-    lds[kCompactWaves] = run;
-  }
-  __syncthreads();
-  const T excl = x - v + lds[wave];
-  *total = lds[kCompactWaves];
-  __syncthreads();
-  return excl;
-}
-
-template <typename T>
-__device__ inline T block_sum(T v, T *lds) {
-  T total;
-  block_exclusive_scan(v, lds, &total);
-  return total;
 }
 
 // Pre-batch corrections and the layer-1 dirty marks (see launch_corr_mark).
@@ -104,100 +67,257 @@ __global__ void k_corr_mark(int agg, LayerPtrs lp, const int *out_len, const int
   const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
   for (long long i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
     if (i < nf) {
-      mark(bm, flist[i]);
+      mark_only(bm, flist[i]);
     } else {
       const long long a = i - nf;
       const int u = a < ni ? ins_src[a] : del_src[a - ni];
-      if (ddeg[u] != 0) mark(bm, u);
+      if (ddeg[u] != 0) mark_only(bm, u);
     }
   }
 }
 
-__device__ inline void word_stats(unsigned w, long long vbase, const int *odeg, const int *ideg, int &cnt,
-                                  long long &dsum, long long &isum) {
-  cnt += __popc(w);
-  if (odeg != nullptr || ideg != nullptr) {
-    while (w) {
-      const int b = __ffs(w) - 1;
-      if (odeg != nullptr) dsum += odeg[vbase + b];
-      if (ideg != nullptr) isum += ideg[vbase + b];
-      w &= w - 1;
+// The set bits of a thread's kWordsPerThread (= 4) bitmap words, walked in vertex
+// order from two 64-bit halves (no dynamically indexed register arrays).
+struct BitCursor {
+  unsigned long long lo, hi;
+  long long base;  // vertex id of bit 0
+  __device__ BitCursor(const unsigned (&w)[kWordsPerThread], long long first_word)
+      : lo(w[0] | static_cast<unsigned long long>(w[1]) << 32),
+        hi(w[2] | static_cast<unsigned long long>(w[3]) << 32), base(first_word * 32) {}
+  __device__ bool empty() const { return (lo | hi) == 0; }
+  __device__ int next() {  // -1 when exhausted
+    if (lo) {
+      const int b = __ffsll(lo) - 1;
+      lo &= lo - 1;
+      return static_cast<int>(base + b);
     }
+    if (hi) {
+      const int b = __ffsll(hi) - 1;
+      hi &= hi - 1;
+      return static_cast<int>(base + 64 + b);
+    }
+    return -1;
   }
-}
+};
+static_assert(kWordsPerThread == 4, "BitCursor covers four words");
 
-__global__ __launch_bounds__(kCompactThreads) void k_compact_count(const unsigned *bm_a, const unsigned *bm_b,
-                                                                   long long words, const int *odeg,
-                                                                   const int *ideg, int *blocksum,
-                                                                   long long *blockdeg) {
-  __shared__ long long red[kCompactWaves + 1];
-  const long long w0 = static_cast<long long>(blockIdx.x) * kWordsPerBlock + threadIdx.x * kWordsPerThread;
-  int cnt = 0;
-  long long dsum = 0, isum = 0;
+// Vertices and degrees are fetched kBatch at a time so that the loads of one
+// thread overlap instead of forming a chain of dependent round trips.
+constexpr int kBatch = 8;
+
+// Loads a thread's words of both bitmaps; pop_a counts the first bitmap's bits.
+__device__ inline void load_words(const unsigned *bm_a, const unsigned *bm_b, long long w0, long long words,
+                                  unsigned (&wv)[kWordsPerThread], int &pop_a) {
+  pop_a = 0;
 #pragma unroll
   for (int i = 0; i < kWordsPerThread; ++i) {
-    const long long w = w0 + i;
-    if (w < words) word_stats(bm_a[w] | bm_b[w], w * 32, odeg, ideg, cnt, dsum, isum);
+    const unsigned a = w0 + i < words ? bm_a[w0 + i] : 0u;
+    const unsigned b = w0 + i < words ? bm_b[w0 + i] : 0u;
+    wv[i] = a | b;
+    pop_a += __popc(a);
   }
-  const long long tc = block_sum<long long>(cnt, red);
-  const long long td = block_sum<long long>(dsum, red);
-  const long long ti = block_sum<long long>(isum, red);
+}
+
+// Sums of the out- and in-degrees (either may be null) over the cursor's bits.
+__device__ inline void degree_sums(BitCursor c, const int *odeg, const int *ideg, long long &dsum,
+                                   long long &isum) {
+  if (odeg == nullptr && ideg == nullptr) return;
+  while (!c.empty()) {
+    int v[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) v[j] = c.next();
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      if (v[j] >= 0) {
+        if (odeg != nullptr) dsum += odeg[v[j]];
+        if (ideg != nullptr) isum += ideg[v[j]];
+      }
+    }
+  }
+}
+
+// Per-tile sums carried by the compaction: marked vertices, their out-degrees,
+// their in-degrees, marked vertices of the first bitmap.
+constexpr int kVals = 4;
+
+// Exclusive block scan of kVals values at once (one LDS round).
+__device__ inline void block_scan(const long long (&v)[kVals], long long (&excl)[kVals], long long (&total)[kVals],
+                                  long long (*lds)[kVals]) {
+  const int lane = lane_id(), wave = threadIdx.x / kWave;
+  long long x[kVals];
+#pragma unroll
+  for (int k = 0; k < kVals; ++k) x[k] = v[k];
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+#pragma unroll
+    for (int k = 0; k < kVals; ++k) {
+      const long long y = __shfl_up(x[k], o);
+      if (lane >= o) x[k] += y;
+    }
+  }
+  if (lane == kWave - 1) {
+#pragma unroll
+    for (int k = 0; k < kVals; ++k) lds[wave][k] = x[k];
+  }
+  __syncthreads();
+  long long before[kVals] = {}, all[kVals] = {};
+  for (int w = 0; w < kCompactWaves; ++w) {
+#pragma unroll
+    for (int k = 0; k < kVals; ++k) {
+      const long long t = lds[w][k];
+      if (w < wave) before[k] += t;
+      all[k] += t;
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < kVals; ++k) {
+    excl[k] = before[k] + x[k] - v[k];
+    total[k] = all[k];
+  }
+  __syncthreads();
+}
+
+// Published tile sums: each 64-bit word holds the launch epoch (1..65535) above a
+// 48-bit value, so a word is valid on its own and words of earlier launches are
+// never mistaken for current ones (the tiles of every launch rewrite all words).
+constexpr int kEpochShift = 48;
+constexpr u64 kValueMask = (1ull << kEpochShift) - 1;
+constexpr int kSpinLimit = 1 << 20;
+
+__device__ inline void publish(u64 *p, u64 epoch, const long long (&v)[kVals]) {
+#pragma unroll
+  for (int k = 0; k < kVals; ++k)
+    __hip_atomic_store(p + k, epoch << kEpochShift | (static_cast<u64>(v[k]) & kValueMask), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ inline bool fetch(const u64 *p, u64 epoch, long long (&v)[kVals]) {
+  bool ok = true;
+#pragma unroll
+  for (int k = 0; k < kVals; ++k) {
+    const u64 w = __hip_atomic_load(p + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    ok = ok && (w >> kEpochShift) == epoch;
+    v[k] = static_cast<long long>(w & kValueMask);
+  }
+  return ok;
+}
+
+// Single-pass compaction (a decoupled look-back prefix scan). Blocks take tiles of
+// kWordsPerBlock bitmap words in ticket order, so a tile's predecessors are already
+// running. Each tile publishes its sums at once, then wave 0 walks back over the
+// predecessors (64 per step), adding their tile sums until it meets one that has
+// published its inclusive prefix. A tile publishes its own sums before it waits, so
+// every wait is for work that needs no waiting: all waits end. A wait that outlasts
+// kSpinLimit polls sets bit 2 of the error word and counts the tile as empty (the
+// batch then fails loudly instead of hanging).
+// Output: the marked vertices of both bitmaps as a sorted list with prefix sums of
+// their out- and in-degrees, membership words and slots; both bitmaps are cleared.
+__global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, unsigned *bm_b, long long words,
+                                                             CompactOut o, u64 *agg, u64 *inc, u64 *ticket,
+                                                             u64 epoch, u64 *err) {
+  __shared__ long long red[kCompactWaves][kVals];
+  __shared__ long long tile_s, base_s[kVals];
+  const long long tiles = gridDim.x;
   if (threadIdx.x == 0) {
-    blocksum[blockIdx.x] = static_cast<int>(tc);
-    blockdeg[2 * blockIdx.x] = td;
-    blockdeg[2 * blockIdx.x + 1] = ti;
+    const long long t = static_cast<long long>(atomicAdd(ticket, 1ull));
+    if (t == tiles - 1) __hip_atomic_store(ticket, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    tile_s = t;
   }
-}
-
-__global__ __launch_bounds__(kCompactThreads) void k_compact_emit(unsigned *bm_a, unsigned *bm_b, long long words,
-                                                                  const int *blocksum, const long long *blockdeg,
-                                                                  CompactOut o) {
-  __shared__ long long red[kCompactWaves + 1];
-  long long pre = 0, pred = 0, prei = 0;
-  for (int b = threadIdx.x; b < static_cast<int>(blockIdx.x); b += kCompactThreads) {
-    pre += blocksum[b];
-    pred += blockdeg[2 * b];
-    prei += blockdeg[2 * b + 1];
-  }
-  const long long base = block_sum<long long>(pre, red);
-  const long long dbase = block_sum<long long>(pred, red);
-  const long long ibase = block_sum<long long>(prei, red);
-  const long long w0 = static_cast<long long>(blockIdx.x) * kWordsPerBlock + threadIdx.x * kWordsPerThread;
-  const int *odeg = o.doff != nullptr ? o.out_deg : nullptr;
-  const int *ideg = o.ioff != nullptr ? o.in_deg : nullptr;  // prefix only when wanted
+  __syncthreads();
+  const long long tile = tile_s;
+  const long long w0 = tile * kWordsPerBlock + threadIdx.x * kWordsPerThread;
+  const int *odeg = o.doff != nullptr || o.out_total != nullptr ? o.out_deg : nullptr;
+  const int *ideg = o.ioff != nullptr || o.in_total != nullptr ? o.in_deg : nullptr;
   unsigned wv[kWordsPerThread];
-  int cnt = 0;
-  long long dsum = 0, isum = 0;
+  int pop_a;
+  load_words(bm_a, bm_b, w0, words, wv, pop_a);
+  long long st[kVals] = {0, 0, 0, pop_a};
 #pragma unroll
-  for (int i = 0; i < kWordsPerThread; ++i) {
-    const long long w = w0 + i;
-    wv[i] = w < words ? (bm_a[w] | bm_b[w]) : 0u;
-    word_stats(wv[i], w * 32, odeg, ideg, cnt, dsum, isum);
-  }
-  long long tot_c, tot_d, tot_i;
-  long long pos = base + block_exclusive_scan<long long>(cnt, red, &tot_c);
-  long long dpos = dbase + block_exclusive_scan<long long>(dsum, red, &tot_d);
-  long long ipos = ibase + block_exclusive_scan<long long>(isum, red, &tot_i);
+  for (int i = 0; i < kWordsPerThread; ++i) st[0] += __popc(wv[i]);
+  degree_sums(BitCursor(wv, w0), odeg, ideg, st[1], st[2]);
+  long long ex[kVals], tot[kVals];
+  block_scan(st, ex, tot, red);
+  if (threadIdx.x == 0) publish((tile == 0 ? inc : agg) + tile * kVals, epoch, tot);
+  if (threadIdx.x < kWave) {
+    const int lane = lane_id();
+    long long acc[kVals] = {};
+    bool timed_out = false;
+    for (long long j = tile - 1; j >= 0; j -= kWave) {
+      const long long p = j - lane;
+      long long v[kVals] = {};
+      bool incl = true;  // lanes before tile 0 end the walk with zeros
+      if (p >= 0) {
+        for (int it = 0;; ++it) {
+          if (fetch(inc + p * kVals, epoch, v)) break;
+          if (fetch(agg + p * kVals, epoch, v)) {
+            incl = false;
+            break;
+          }
+          if (it >= kSpinLimit) {
+            timed_out = true;
 #pragma unroll
-  for (int i = 0; i < kWordsPerThread; ++i) {
-    unsigned m = wv[i];
-    const long long vbase = (w0 + i) * 32;
-    while (m) {
-      const int b = __ffs(m) - 1;
-      const int v = static_cast<int>(vbase + b);
-      o.list[pos] = v;
-      if (odeg != nullptr) {
-        o.doff[pos] = dpos;
-        dpos += odeg[v];
+            for (int k = 0; k < kVals; ++k) v[k] = 0;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(2);
+        }
       }
-      if (ideg != nullptr) {
-        o.ioff[pos] = ipos;
-        ipos += ideg[v];
+      const u64 im = __ballot(incl);
+      const int first = im ? __ffsll(im) - 1 : kWave;  // nearest inclusive predecessor
+#pragma unroll
+      for (int k = 0; k < kVals; ++k) {
+        long long x = lane <= first ? v[k] : 0;
+#pragma unroll
+        for (int o2 = kWave / 2; o2 > 0; o2 >>= 1) x += __shfl_xor(x, o2);
+        acc[k] += x;
       }
-      if (o.slot != nullptr) o.slot[v] = static_cast<int>(pos);
-      ++pos;
-      m &= m - 1;
+      if (first < kWave) break;
     }
+    if (timed_out) atomicOr(err, 4ull);
+    if (lane == 0) {
+#pragma unroll
+      for (int k = 0; k < kVals; ++k) base_s[k] = acc[k];
+      if (tile > 0) {
+        long long incv[kVals];
+#pragma unroll
+        for (int k = 0; k < kVals; ++k) incv[k] = acc[k] + tot[k];
+        publish(inc + tile * kVals, epoch, incv);
+      }
+    }
+  }
+  __syncthreads();
+  long long base[kVals];
+#pragma unroll
+  for (int k = 0; k < kVals; ++k) base[k] = base_s[k];
+  long long pos = base[0] + ex[0], dpos = base[1] + ex[1], ipos = base[2] + ex[2];
+  BitCursor c(wv, w0);
+  while (!c.empty()) {
+    int v[kBatch], dv[kBatch], iv[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) v[j] = c.next();
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      dv[j] = o.doff != nullptr && v[j] >= 0 ? odeg[v[j]] : 0;
+      iv[j] = o.ioff != nullptr && v[j] >= 0 ? ideg[v[j]] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      if (v[j] < 0) continue;
+      o.list[pos] = v[j];
+      if (o.doff != nullptr) {
+        o.doff[pos] = dpos;
+        dpos += dv[j];
+      }
+      if (o.ioff != nullptr) {
+        o.ioff[pos] = ipos;
+        ipos += iv[j];
+      }
+      if (o.slot != nullptr) o.slot[v[j]] = static_cast<int>(pos);
+      ++pos;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kWordsPerThread; ++i) {
     const long long w = w0 + i;
     if (w < words) {
       if (o.keep != nullptr) o.keep[w] = wv[i];
@@ -205,110 +325,17 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact_emit(unsigned *bm_a
       bm_b[w] = 0u;
     }
   }
-  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
-    const long long total = base + tot_c;
+  if (tile == tiles - 1 && threadIdx.x == 0) {
+    const long long total = base[0] + tot[0];
     *o.count = static_cast<u64>(total);
-    if (odeg != nullptr) o.doff[total] = dbase + tot_d;
-    if (ideg != nullptr) o.ioff[total] = ibase + tot_i;
-    // the count kernel summed in-degrees per block, also when no prefix is wanted
-    if (o.in_total != nullptr) *o.in_total = static_cast<u64>(ibase + blockdeg[2 * blockIdx.x + 1]);
+    if (o.doff != nullptr) o.doff[total] = base[1] + tot[1];
+    if (o.ioff != nullptr) o.ioff[total] = base[2] + tot[2];
+    if (o.out_total != nullptr) *o.out_total = static_cast<u64>(base[1] + tot[1]);
+    if (o.in_total != nullptr) *o.in_total = static_cast<u64>(base[2] + tot[2]);
+    if (o.sinks_a != nullptr) *o.sinks_a = static_cast<u64>(base[3] + tot[3]);
   }
 }
 
-// One-block form of the compaction for small graphs (one launch instead of two):
-// 1024 threads walk the bitmap words in rounds, carrying the running offsets.
-constexpr int kSingleThreads = 1024;
-constexpr int kSingleWaves = kSingleThreads / kWave;
-
-__device__ inline long long single_scan(long long v, long long *lds, long long *total) {
-  const int lane = lane_id(), wave = threadIdx.x / kWave;
-  long long x = v;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const long long y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  if (lane == kWave - 1) lds[wave] = x;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    long long run = 0;
-    for (int w = 0; w < kSingleWaves; ++w) {
-      const long long t = lds[w];
-      lds[w] = run;
-      run += t;
-    }
-    lds[kSingleWaves] = run;
-  }
-  __syncthreads();
-  const long long excl = x - v + lds[wave];
-  *total = lds[kSingleWaves];
-  __syncthreads();
-  return excl;
-}
-
-__global__ __launch_bounds__(kSingleThreads) void k_compact_single(unsigned *bm_a, unsigned *bm_b, long long words,
-                                                                   CompactOut o) {
-  __shared__ long long red[kSingleWaves + 1];
-  const int *odeg = o.doff != nullptr ? o.out_deg : nullptr;
-  const int *ideg = (o.ioff != nullptr || o.in_total != nullptr) ? o.in_deg : nullptr;
-  long long pos = 0, dpos = 0, ipos = 0;
-  for (long long r0 = 0; r0 < words; r0 += static_cast<long long>(kSingleThreads) * kWordsPerThread) {
-    const long long w0 = r0 + static_cast<long long>(threadIdx.x) * kWordsPerThread;
-    unsigned wv[kWordsPerThread];
-    int cnt = 0;
-    long long dsum = 0, isum = 0;
-#pragma unroll
-    for (int i = 0; i < kWordsPerThread; ++i) {
-      const long long w = w0 + i;
-      wv[i] = w < words ? (bm_a[w] | bm_b[w]) : 0u;
-      word_stats(wv[i], w * 32, odeg, ideg, cnt, dsum, isum);
-    }
-    long long tc, td, ti;
-    long long p = pos + single_scan(cnt, red, &tc);
-    long long dp = dpos + single_scan(dsum, red, &td);
-    long long ip = ipos + single_scan(isum, red, &ti);
-#pragma unroll
-    for (int i = 0; i < kWordsPerThread; ++i) {
-      unsigned m = wv[i];
-      const long long vbase = (w0 + i) * 32;
-      while (m) {
-        const int b = __ffs(m) - 1;
-        const int v = static_cast<int>(vbase + b);
-        o.list[p] = v;
-        if (odeg != nullptr) {
-          o.doff[p] = dp;
-          dp += odeg[v];
-        }
-        if (o.ioff != nullptr) {
-          o.ioff[p] = ip;
-          ip += ideg[v];
-        }
-        if (o.slot != nullptr) o.slot[v] = static_cast<int>(p);
-        ++p;
-        m &= m - 1;
-      }
-      const long long w = w0 + i;
-      if (w < words) {
-        if (o.keep != nullptr) o.keep[w] = wv[i];
-        bm_a[w] = 0u;
-        bm_b[w] = 0u;
-      }
-    }
-    pos += tc;
-    dpos += td;
-    ipos += ti;
-  }
-  if (threadIdx.x == 0) {
-    *o.count = static_cast<u64>(pos);
-    if (odeg != nullptr) o.doff[pos] = dpos;
-    if (o.ioff != nullptr) o.ioff[pos] = ipos;
-    if (o.in_total != nullptr) *o.in_total = static_cast<u64>(ipos);
-  }
-}
-
-// Layer-0 deltas: for each dirty vertex u (slot j), the new feature row is the
-// last write of the batch (or the unchanged row), delta = c'_u x'_u - c_u x_u, and
-// the feature row is overwritten.
 __global__ void k_delta0(int agg, int d0, const int *list, const u64 *count, const ripple_op *ops,
                          const float *feat, const int *fop, float *X, const int *out_len, const int *ddeg,
                          float *delta, const Counters *c) {
@@ -376,26 +403,24 @@ template <int G, int NC, bool PUSH>
 __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u64 *count, const long long *doff,
                                                  const float *delta, Adj out, float *S, unsigned *bm_out,
                                                  unsigned *bm_x, const int *ins_dst, const int *del_dst,
-                                                 u64 *pushed, u64 *dest, const Counters *c) {
+                                                 const u64 *pushed, const Counters *c) {
   if (c->abort) return;
   const int lane = lane_id();
   const long long nD = static_cast<long long>(*count);
-  const long long E = doff[nD];
+  const long long E = static_cast<long long>(*pushed);
   {
     const long long ni = static_cast<long long>(c->n_ins);
     const long long na = ni + static_cast<long long>(c->n_del);
     const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
     const long long t0 = blockIdx.x * blockDim.x + threadIdx.x;
-    for (long long i = t0; i < na; i += stride) mark(bm_x, i < ni ? ins_dst[i] : del_dst[i - ni]);
-    for (long long j = t0; j < nD; j += stride) mark(bm_x, list[j]);
-    if (t0 == 0) *pushed = static_cast<u64>(E);
+    for (long long i = t0; i < na; i += stride) mark_only(bm_x, i < ni ? ins_dst[i] : del_dst[i - ni]);
+    for (long long j = t0; j < nD; j += stride) mark_only(bm_x, list[j]);
   }
   const long long waves = num_waves();
   int C = 1;
   while (C < kWave && static_cast<long long>(C) * waves < E) C <<= 1;
   constexpr int kEdgesPerStep = kWave / G;
   const int grp = lane / G, k0 = lane % G;
-  u64 my_dest = 0;
   int cached = -1;
   float dreg[NC];
   const long long chunks = (E + C - 1) / C;
@@ -403,6 +428,17 @@ __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u
     const long long e0 = ch * C;
     const long long elast = e0 + C - 1 < E - 1 ? e0 + C - 1 : E - 1;
     const long long ja = wave_last_le(doff, 0, nD + 1, e0);
+    if (PUSH && ja != cached) {
+      // the chunk's first source is known before its arcs are resolved: fetch its
+      // delta row now so that the load overlaps the list / offset / column reads
+      const float *dj = delta + ja * d;
+#pragma unroll
+      for (int q = 0; q < NC; ++q) {
+        const int k = k0 + q * G;
+        dreg[q] = k < d ? dj[k] : 0.0f;
+      }
+      cached = static_cast<int>(ja);
+    }
     const long long jb = C == 1 ? ja : wave_last_le(doff, ja, nD + 1, elast);
     const long long e = e0 + lane;
     const bool active = e <= elast;
@@ -423,8 +459,7 @@ __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u
       const int u = list[j];
       v = out.col[out.off[u] + (e - doff[j])];
     }
-    const bool fresh = v >= 0 && mark(bm_out, v);
-    my_dest += __popcll(__ballot(fresh));
+    if (v >= 0) mark_only(bm_out, v);
     const int cnt = PUSH ? static_cast<int>(elast - e0 + 1) : 0;
     for (int i = 0; i < cnt; i += kEdgesPerStep) {
       const int vv = __shfl(v, i + grp);
@@ -448,7 +483,6 @@ __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u
       }
     }
   }
-  if (lane == 0 && my_dest) atomicAdd(dest, my_dest);
 }
 
 // Pull form of the message step (for dense frontiers). In-arcs of the sorted
@@ -610,19 +644,16 @@ int compact_blocks(long long n) {
   return static_cast<int>((words + kWordsPerBlock - 1) / kWordsPerBlock);
 }
 
-void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, int *blocksum, long long *blockdeg,
-                    const CompactOut &o, bool single_block) {
+void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, const CompactScratch &cs,
+                    const CompactOut &o) {
   const long long words = (n + 31) / 32;
-  if (single_block) {
-    hipLaunchKernelGGL(k_compact_single, dim3(1), dim3(kSingleThreads), 0, s, bm_a, bm_b, words, o);
-    return;
-  }
-  const int nb = compact_blocks(n);
-  hipLaunchKernelGGL(k_compact_count, dim3(nb), dim3(kCompactThreads), 0, s, bm_a, bm_b, words,
-                     o.doff != nullptr ? o.out_deg : nullptr,
-                     (o.ioff != nullptr || o.in_total != nullptr) ? o.in_deg : nullptr, blocksum, blockdeg);
-  hipLaunchKernelGGL(k_compact_emit, dim3(nb), dim3(kCompactThreads), 0, s, bm_a, bm_b, words, blocksum, blockdeg, o);
+  const int tiles = compact_blocks(n);
+  hipLaunchKernelGGL(k_compact, dim3(tiles), dim3(kCompactThreads), 0, s, bm_a, bm_b, words, o, cs.words,
+                     cs.words + static_cast<long long>(tiles) * kVals, cs.words + 2LL * tiles * kVals, cs.epoch,
+                     cs.err);
 }
+
+long long compact_scratch_words(long long n) { return 2LL * compact_blocks(n) * kVals + 1; }
 
 void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list, const u64 *count,
                    const ripple_op *ops, const float *feat, const int *fop, float *X, const int *out_len,
@@ -633,11 +664,11 @@ void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list,
 
 void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
-                    const int *del_dst, u64 *pushed, u64 *dest, const Counters *c, bool push) {
+                    const int *del_dst, const u64 *pushed, const Counters *c, bool push) {
   const int blocks = 2048;
 #define RP_SCATTER(GV, NCV, P)                                                                                     \
   hipLaunchKernelGGL((k_scatter<GV, NCV, P>), dim3(blocks), dim3(256), 0, s, d, list, count, doff, delta, out, S, \
-                     bm_out, bm_x, ins_dst, del_dst, pushed, dest, c)
+                     bm_out, bm_x, ins_dst, del_dst, pushed, c)
   if (!push) RP_SCATTER(64, 1, false);
   else if (d <= 16) RP_SCATTER(16, 1, true);
   else if (d <= 32) RP_SCATTER(32, 1, true);

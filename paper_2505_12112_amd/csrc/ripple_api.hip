@@ -84,8 +84,8 @@ struct ripple_ctx {
   int *ddeg = nullptr;
   unsigned *bm_out = nullptr;
   unsigned *bm_x = nullptr;
-  int *blocksum = nullptr;
-  long long *blockdeg = nullptr;
+  rp::u64 *compact_lb = nullptr;  // tile sums of the single-pass compaction
+  rp::u64 compact_epoch = 0;
   int *lists[rp::kMaxL + 1] = {};
   long long *doff[rp::kMaxL + 1] = {};  // out-degree prefix of lists[l] (first arc index per vertex)
   long long *ioff = nullptr;            // in-degree prefix of the current layer's A^l (pull form)
@@ -529,11 +529,9 @@ bool use_pull(const ripple_ctx *c, int l) {
   return pull < push;
 }
 
-// One-launch compaction for small graphs whose frontier stayed small last batch.
-bool single_compact(const ripple_ctx *c, int l) {
-  const long long words = (c->n + 31) / 32;
-  const long long hint = c->has_batch ? c->last_count[l] : c->n;
-  return words <= 16384 && hint <= 32768;
+rp::CompactScratch compact_scratch(ripple_ctx *c, rp::Counters *dc) {
+  c->compact_epoch = c->compact_epoch % 65535 + 1;
+  return rp::CompactScratch{c->compact_lb, c->compact_epoch, &dc->err};
 }
 
 // Issues one batch. Returns after queuing; the caller syncs.
@@ -572,12 +570,13 @@ void issue_batch(ripple_ctx *c, int B) {
     co.count = &dc->count[0];
     co.out_deg = c->adj[0].len;
     co.doff = c->doff[0];
+    co.out_total = &dc->pushed[1];
     co.keep = use_pull(c, 1) ? c->keep[0] : nullptr;
     co.slot = use_pull(c, 1) ? c->slot[0] : nullptr;
-    rp::launch_compact(s, c->n, c->bm_out, c->bm_x, c->blocksum, c->blockdeg, co, single_compact(c, 0));
+    rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
     rp::launch_delta0(s, c->n, c->agg, c->dims[0], c->lists[0], &dc->count[0], c->d_ops, c->h_feat, c->fop,
                       c->H[0], c->adj[0].len, c->ddeg, c->delta[0], dc);
-    add_launches(c, RIPPLE_PHASE_LAYER0, 4);
+    add_launches(c, RIPPLE_PHASE_LAYER0, 3);
   }
   for (int l = 1; l <= c->L; ++l) {
     float *din = c->delta[(l - 1) & 1];
@@ -598,7 +597,7 @@ void issue_batch(ripple_ctx *c, int B) {
       // push: marks + atomic adds; pull: marks only (the adds follow the compaction)
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
       rp::launch_scatter(s, c->n, c->sw[l], c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out, c->S[l],
-                         c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], &dc->dest[l], dc, !pull);
+                         c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc, !pull);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     {
@@ -611,11 +610,13 @@ void issue_batch(ripple_ctx *c, int B) {
       co.in_deg = c->adj[1].len;
       co.ioff = pull ? c->ioff : nullptr;
       co.in_total = &dc->indeg[l];
+      co.out_total = l < c->L ? &dc->pushed[l + 1] : nullptr;
+      co.sinks_a = &dc->dest[l];  // distinct sinks of the arcs pushed at layer l
       const bool next_pull = l < c->L && use_pull(c, l + 1);
       co.keep = next_pull ? c->keep[l & 1] : nullptr;
       co.slot = next_pull ? c->slot[l & 1] : nullptr;
-      rp::launch_compact(s, c->n, c->bm_out, c->bm_x, c->blocksum, c->blockdeg, co, single_compact(c, l));
-      add_launches(c, RIPPLE_PHASE_COMPACT, 2);
+      rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
+      add_launches(c, RIPPLE_PHASE_COMPACT, 1);
     }
     if (pull) {
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
@@ -874,8 +875,7 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   if ((st = dalloc_n(c, &c->ddeg, n)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->bm_out, words)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->bm_x, words)) != RIPPLE_OK) return bail(st);
-  if ((st = dalloc_n(c, &c->blocksum, rp::compact_blocks(n) + 1)) != RIPPLE_OK) return bail(st);
-  if ((st = dalloc_n(c, &c->blockdeg, 2 * rp::compact_blocks(n) + 2)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->compact_lb, rp::compact_scratch_words(n))) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->rl_blocksums, rp::relayout_blocks(n) + 1)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->rl_off, n)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->rl_cap, n)) != RIPPLE_OK) return bail(st);
@@ -883,6 +883,8 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   e = hipMemsetAsync(c->ddeg, 0, n * sizeof(int), c->stream);
   if (e == hipSuccess) e = hipMemsetAsync(c->bm_out, 0, words * sizeof(unsigned), c->stream);
   if (e == hipSuccess) e = hipMemsetAsync(c->bm_x, 0, words * sizeof(unsigned), c->stream);
+  if (e == hipSuccess)
+    e = hipMemsetAsync(c->compact_lb, 0, rp::compact_scratch_words(n) * sizeof(rp::u64), c->stream);
   if (e == hipSuccess) e = hipMemsetAsync(c->d_counters, 0, 2 * sizeof(rp::Counters), c->stream);
   if (e == hipSuccess) e = hipGetLastError();
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
@@ -1028,7 +1030,9 @@ ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t 
   const rp::Counters &k = *c->h_counters;
   if (k.err) {
     c->poisoned = true;
-    return fail(c, RIPPLE_E_DEVICE, "ripple: device adjacency inconsistent (err bits " + std::to_string(k.err) + ")");
+    // bit 0: a net-deleted arc was not found; bit 1: a rewritten row's length did not
+    // match; bit 2: the compaction's wait for a predecessor tile timed out
+    return fail(c, RIPPLE_E_DEVICE, "ripple: device-side check failed (err bits " + std::to_string(k.err) + ")");
   }
   account_phases(c);
   c->has_batch = true;
@@ -1217,8 +1221,7 @@ void ripple_destroy(ripple_ctx *c) {
   dfree_t(c, c->ddeg);
   dfree_t(c, c->bm_out);
   dfree_t(c, c->bm_x);
-  dfree_t(c, c->blocksum);
-  dfree_t(c, c->blockdeg);
+  dfree_t(c, c->compact_lb);
   dfree_t(c, c->rl_blocksums);
   dfree_t(c, c->rl_off);
   dfree_t(c, c->rl_cap);
