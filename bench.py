@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-events", action="store_true",
                     help="no HIP events in the timed region (roofline then comes from the untimed pass)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-mebibyte device buffer into another (torch copy kernel), ten times: "
+                         "the reference reading for the HBM byte counters")
     return ap.parse_args()
 
 
@@ -103,6 +106,15 @@ def main():
         sys.exit(2)
     import numpy as np
     import torch
+    if args.copy_calibration:
+        n = args.copy_calibration * 2**20 // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(10):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": 4 * n, "copies": 10}))
+        return
     from paper_2505_12112_amd import synth
     from paper_2505_12112_amd.ripple import Ripple, BatchStats
 

@@ -141,8 +141,8 @@ typedef struct {
   int64_t relocated_rows;       /* adjacency rows moved to the spare arena */
   int64_t repacks;              /* adjacency re-layouts this call needed (spare arena full) */
   int64_t in_arcs[RIPPLE_MAX_LAYERS + 1];   /* [l]: in-arcs of A^l (the pull form's work) */
-  int32_t pull_layers;          /* bit l set: layer l added its messages by pull, not push */
-  int32_t pad;
+  int32_t pull_layers;          /* bit l set: layer l pulled over the in-arcs of A^l */
+  int32_t dense_layers;         /* bit l set: layer l pulled over every in-arc of the graph */
 } ripple_batch_stats;
 
 /* Part 1 of the problem statement: copies the snapshot to the device as an
@@ -201,9 +201,11 @@ RIPPLE_API ripple_status ripple_get_arcs(ripple_ctx *ctx, int32_t direction, int
 /* How each layer adds its messages to the cached aggregate (results agree up to
  * rounding): RIPPLE_SCATTER_PUSH, one row of fp32 atomics per pushed arc;
  * RIPPLE_SCATTER_PULL, each affected vertex sums the messages of its dirty
- * in-neighbours and adds them once; RIPPLE_SCATTER_AUTO (default), per layer
- * from the previous batch's counts (push on the first batch). */
-enum { RIPPLE_SCATTER_AUTO = 0, RIPPLE_SCATTER_PUSH = 1, RIPPLE_SCATTER_PULL = 2 };
+ * in-neighbours and adds them once; RIPPLE_SCATTER_DENSE, the pull form over every
+ * in-arc of the graph, which also finds the sinks (no per-arc marks; for layers
+ * where most arcs carry a message); RIPPLE_SCATTER_AUTO (default), per layer from
+ * the previous batch's counts (push on the first batch). */
+enum { RIPPLE_SCATTER_AUTO = 0, RIPPLE_SCATTER_PUSH = 1, RIPPLE_SCATTER_PULL = 2, RIPPLE_SCATTER_DENSE = 3 };
 RIPPLE_API ripple_status ripple_set_scatter_mode(ripple_ctx *ctx, int32_t mode);
 
 /* Device bytes the context holds. */

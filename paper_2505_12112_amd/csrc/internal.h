@@ -42,6 +42,8 @@ struct Counters {
   u64 pushed[kMaxL + 1];  // [l] = out-arcs pushed at layer l
   u64 dest[kMaxL + 1];    // [l] = distinct sinks of those arcs
   u64 indeg[kMaxL + 1];   // [l] = sum of in-degrees over A^l (pull work), when computed
+  u64 count_all;          // vertices listed by a full compaction (dense layers)
+  u64 zero;               // never written: an arc count of zero for kernels that only mark
 };
 
 // Survives batches.
@@ -111,10 +113,13 @@ void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerP
                       const int *del_src, const int *del_dst, unsigned *bm, Counters *c);
 int compact_blocks(long long n);
 // Outputs of one compaction of bitmaps (a | b) into an ascending list. Optional
-// (nullptr = skipped): doff[j] = sum of out_deg over list[0..j) (doff[count] =
-// total), ioff likewise over in_deg, keep = the compacted bitmap words, slot[v] =
-// position of v in the list. Both input bitmaps are cleared.
+// (nullptr = skipped): list, doff[j] = sum of out_deg over list[0..j) (doff[count]
+// = total), ioff likewise over in_deg, keep = the compacted bitmap words, wprefix[w]
+// = listed vertices in words before w (so the list position of a member u is
+// wprefix[u / 32] + the member bits of its word below u). Both input bitmaps are
+// cleared. full_n > 0: list all of 0..full_n-1 instead (the bitmaps are not read).
 struct CompactOut {
+  long long full_n;
   int *list;
   u64 *count;
   const int *out_deg;
@@ -125,7 +130,7 @@ struct CompactOut {
   u64 *out_total;      // receives the sum of out_deg over the list (the next scatter's arcs)
   u64 *sinks_a;        // receives the number of bits set in the first bitmap
   unsigned *keep;
-  int *slot;
+  int *wprefix;
 };
 // Tile sums published by the single-pass compaction: compact_scratch_words(n)
 // words, zero when first used; epoch cycles through 1..65535, one per launch.
@@ -155,11 +160,14 @@ void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u6
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
                     const int *del_dst, const u64 *pushed, const Counters *c, bool push);
 
-// pull: for every vertex v of the sorted list A (in-arc prefix ioff), S[v] +=
-// sum of msg[slot[u]] over in-arcs (u -> v) whose source u is set in member.
-// One flush (row of fp32 atomics) per sink and wave; each in-arc is read once.
+// pull: for every vertex v of the sorted list A (in-arc prefix ioff; list null =
+// the identity), S[v] += sum of msg[rank(u)] over in-arcs (u -> v) whose source u
+// is set in member, rank from wprefix (see CompactOut). One flush (row of fp32
+// atomics) per sink and lane group; each in-arc is read once. mark (nullable):
+// set the bit of every sink that received a message (the dense form's frontier).
 void launch_pull_msgs(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *ioff,
-                      Adj in, const unsigned *member, const int *slot, const float *msg, float *S, const Counters *c);
+                      Adj in, const unsigned *member, const int *wprefix, const float *msg, float *S,
+                      unsigned *mark, const Counters *c);
 
 // bootstrap pull: S[v] = sum over in-arcs c_u H[u]
 void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev, Adj in, const int *out_len,

@@ -211,7 +211,8 @@ __device__ inline bool fetch(const u64 *p, u64 epoch, long long (&v)[kVals]) {
 // kSpinLimit polls sets bit 2 of the error word and counts the tile as empty (the
 // batch then fails loudly instead of hanging).
 // Output: the marked vertices of both bitmaps as a sorted list with prefix sums of
-// their out- and in-degrees, membership words and slots; both bitmaps are cleared.
+// their out- and in-degrees, membership words and per-word prefix counts; both
+// bitmaps are cleared. A full compaction lists every vertex without reading them.
 __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, unsigned *bm_b, long long words,
                                                              CompactOut o, u64 *agg, u64 *inc, u64 *ticket,
                                                              u64 epoch, u64 *err) {
@@ -229,8 +230,17 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
   const int *odeg = o.doff != nullptr || o.out_total != nullptr ? o.out_deg : nullptr;
   const int *ideg = o.ioff != nullptr || o.in_total != nullptr ? o.in_deg : nullptr;
   unsigned wv[kWordsPerThread];
-  int pop_a;
-  load_words(bm_a, bm_b, w0, words, wv, pop_a);
+  int pop_a = 0;
+  if (o.full_n > 0) {
+#pragma unroll
+    for (int i = 0; i < kWordsPerThread; ++i) {
+      const long long w = w0 + i;
+      const long long left = o.full_n - w * 32;  // vertices from this word on
+      wv[i] = left >= 32 ? ~0u : left > 0 ? (1u << left) - 1u : 0u;
+    }
+  } else {
+    load_words(bm_a, bm_b, w0, words, wv, pop_a);
+  }
   long long st[kVals] = {0, 0, 0, pop_a};
 #pragma unroll
   for (int i = 0; i < kWordsPerThread; ++i) st[0] += __popc(wv[i]);
@@ -290,8 +300,16 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
 #pragma unroll
   for (int k = 0; k < kVals; ++k) base[k] = base_s[k];
   long long pos = base[0] + ex[0], dpos = base[1] + ex[1], ipos = base[2] + ex[2];
+  if (o.wprefix != nullptr) {
+    long long wp = pos;
+#pragma unroll
+    for (int i = 0; i < kWordsPerThread; ++i) {
+      if (w0 + i < words) o.wprefix[w0 + i] = static_cast<int>(wp);
+      wp += __popc(wv[i]);
+    }
+  }
   BitCursor c(wv, w0);
-  while (!c.empty()) {
+  while ((o.list != nullptr || o.doff != nullptr || o.ioff != nullptr) && !c.empty()) {
     int v[kBatch], dv[kBatch], iv[kBatch];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) v[j] = c.next();
@@ -303,7 +321,7 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       if (v[j] < 0) continue;
-      o.list[pos] = v[j];
+      if (o.list != nullptr) o.list[pos] = v[j];
       if (o.doff != nullptr) {
         o.doff[pos] = dpos;
         dpos += dv[j];
@@ -312,7 +330,6 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
         o.ioff[pos] = ipos;
         ipos += iv[j];
       }
-      if (o.slot != nullptr) o.slot[v[j]] = static_cast<int>(pos);
       ++pos;
     }
   }
@@ -321,8 +338,10 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
     const long long w = w0 + i;
     if (w < words) {
       if (o.keep != nullptr) o.keep[w] = wv[i];
-      bm_a[w] = 0u;
-      bm_b[w] = 0u;
+      if (o.full_n == 0) {
+        bm_a[w] = 0u;
+        bm_b[w] = 0u;
+      }
     }
   }
   if (tile == tiles - 1 && threadIdx.x == 0) {
@@ -391,6 +410,19 @@ __device__ inline long long wave_last_le(const long long *a, long long lo, long 
   return lo + __popcll(__ballot(le)) - 1;
 }
 
+// Same answer as wave_last_le(a, from, n1, x), for a lower bound `from` whose
+// answer is usually close: one round of 64 probes from `from`, and the full
+// search only when every probe is <= x. Used when a wave walks consecutive arcs.
+__device__ inline long long owner_from(const long long *a, long long from, long long n1, long long x) {
+  const int lane = lane_id();
+  const long long hi = from + kWave < n1 ? from + kWave : n1;
+  const long long idx = from + lane;
+  const bool le = idx < hi && a[idx] <= x;
+  const int cnt = __popcll(__ballot(le));
+  if (cnt == hi - from && hi < n1) return wave_last_le(a, hi - 1, n1, x);
+  return from + cnt - 1;
+}
+
 // Edge-parallel scatter. Pushed arcs are numbered: arc e of listed vertex j has
 // index doff[j] + its position in j's out-row. A wave takes a chunk of C
 // consecutive arcs (C = 1 when there are few arcs, so that many waves run at
@@ -424,10 +456,16 @@ __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u
   int cached = -1;
   float dreg[NC];
   const long long chunks = (E + C - 1) / C;
-  for (long long ch = global_wave(); ch < chunks; ch += waves) {
+  // a wave takes a contiguous run of chunks, so each chunk's first source is
+  // found from the previous chunk's
+  const long long per = (chunks + waves - 1) / waves;
+  const long long c0 = global_wave() * per;
+  const long long c1 = c0 + per < chunks ? c0 + per : chunks;
+  long long ja = -1;
+  for (long long ch = c0; ch < c1; ++ch) {
     const long long e0 = ch * C;
     const long long elast = e0 + C - 1 < E - 1 ? e0 + C - 1 : E - 1;
-    const long long ja = wave_last_le(doff, 0, nD + 1, e0);
+    ja = ja < 0 ? wave_last_le(doff, 0, nD + 1, e0) : owner_from(doff, ja, nD + 1, e0);
     if (PUSH && ja != cached) {
       // the chunk's first source is known before its arcs are resolved: fetch its
       // delta row now so that the load overlaps the list / offset / column reads
@@ -439,7 +477,7 @@ __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u
       }
       cached = static_cast<int>(ja);
     }
-    const long long jb = C == 1 ? ja : wave_last_le(doff, ja, nD + 1, elast);
+    const long long jb = C == 1 ? ja : owner_from(doff, ja, nD + 1, elast);
     const long long e = e0 + lane;
     const bool active = e <= elast;
     int j = static_cast<int>(ja);
@@ -487,29 +525,38 @@ __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u
 
 // Pull form of the message step (for dense frontiers). In-arcs of the sorted
 // list A are numbered like the scatter's out-arcs (ioff gives each listed
-// vertex's first in-arc). A wave takes C consecutive in-arcs; each lane resolves
-// one arc's sink v and source u and keeps it if u is dirty (member bit), with the
-// source's message row msg[slot[u]]. The wave then walks its kept arcs in order,
-// summing message rows into registers while the sink stays the same, and adds
-// the sum to S[v] with one row of fp32 atomics per sink: a sink's messages cost
-// one read each and one row update per wave instead of one atomic row each.
-template <int NC>
+// vertex's first in-arc). A wave takes C consecutive in-arcs (a contiguous run of
+// such chunks per wave); each lane resolves one arc's sink v and source u and
+// keeps it if u is dirty (member bit), with the source's message row: u's rank
+// among the members, from the member word and the count of members before it.
+// Groups of G lanes then walk the kept arcs of their own G-lane window in order,
+// U message rows in flight at a time, summing rows into registers while the sink
+// stays the same and adding each sum to S[v] with one row of fp32 atomics: a
+// sink's messages cost one read each and one row update per group instead of one
+// atomic row each. G = 16 for rows of at most 64 floats (four arcs per wave
+// instruction), else 64.
+template <int G, int NC, int U>
 __global__ __launch_bounds__(256) void k_pull_msgs(int d, const int *list, const u64 *count, const long long *ioff,
-                                                   Adj in, const unsigned *member, const int *slot,
-                                                   const float *msg, float *S, const Counters *c) {
+                                                   Adj in, const unsigned *member, const int *wprefix,
+                                                   const float *msg, float *S, unsigned *mark, const Counters *c) {
   if (c->abort) return;
   const int lane = lane_id();
+  const int grp = lane / G, k0 = lane % G;
   const long long nA = static_cast<long long>(*count);
   const long long E = ioff[nA];
   const long long waves = num_waves();
   int C = 1;
   while (C < kWave && static_cast<long long>(C) * waves < E) C <<= 1;
   const long long chunks = (E + C - 1) / C;
-  for (long long ch = global_wave(); ch < chunks; ch += waves) {
+  const long long per = (chunks + waves - 1) / waves;
+  const long long c0 = global_wave() * per;
+  const long long c1 = c0 + per < chunks ? c0 + per : chunks;
+  long long ja = -1;
+  for (long long ch = c0; ch < c1; ++ch) {
     const long long e0 = ch * C;
     const long long elast = e0 + C - 1 < E - 1 ? e0 + C - 1 : E - 1;
-    const long long ja = wave_last_le(ioff, 0, nA + 1, e0);
-    const long long jb = C == 1 ? ja : wave_last_le(ioff, ja, nA + 1, elast);
+    ja = ja < 0 ? wave_last_le(ioff, 0, nA + 1, e0) : owner_from(ioff, ja, nA + 1, e0);
+    const long long jb = C == 1 ? ja : owner_from(ioff, ja, nA + 1, elast);
     const long long e = e0 + lane;
     const bool active = e <= elast;
     int r = static_cast<int>(ja);
@@ -525,46 +572,74 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, const int *list, const
     }
     int v = -1, j = -1;
     if (active) {
-      v = list[r];
+      v = list != nullptr ? list[r] : r;
       const int u = in.col[in.off[v] + (e - ioff[r])];
-      if ((member[u >> 5] >> (u & 31)) & 1u) j = slot[u];
+      const unsigned word = member[u >> 5];
+      const int below = wprefix[u >> 5];  // issued with the member word: no dependent round trip
+      const unsigned bit = 1u << (u & 31);
+      if (word & bit) j = below + __popc(word & (bit - 1u));
     }
-    u64 keep = __ballot(j >= 0);
+    const u64 keep = __ballot(j >= 0);
+    u64 rem = G == kWave ? keep : (keep >> (grp * G)) & ((1ull << (G % kWave)) - 1);
+    int maxc = __popcll(rem);
+#pragma unroll
+    for (int o = G; o < kWave; o <<= 1) {
+      const int y = __shfl_xor(maxc, o);
+      maxc = y > maxc ? y : maxc;
+    }
     int cur = -1;
     float acc[NC];
 #pragma unroll
     for (int q = 0; q < NC; ++q) acc[q] = 0.0f;
-    while (keep) {
-      const int i = __ffsll(static_cast<long long>(keep)) - 1;
-      keep &= keep - 1;
-      const int vv = __shfl(v, i);
-      const int jj = __shfl(j, i);
-      if (vv != cur) {
-        if (cur >= 0) {
-          float *sv = S + static_cast<long long>(cur) * d;
+    for (int b = 0; b < maxc; b += U) {  // trip count is the same for the whole wave
+      int vv[U], jj[U];
 #pragma unroll
-          for (int q = 0; q < NC; ++q) {
-            const int k = lane + q * kWave;
-            if (k < d) unsafeAtomicAdd(&sv[k], acc[q]);
-            acc[q] = 0.0f;
-          }
-        }
-        cur = vv;
+      for (int t = 0; t < U; ++t) {
+        const bool ok = rem != 0;
+        const int src = ok ? grp * G + __ffsll(static_cast<long long>(rem)) - 1 : lane;
+        if (ok) rem &= rem - 1;
+        vv[t] = __shfl(v, src);
+        jj[t] = __shfl(j, src);
+        if (!ok) jj[t] = -1;
       }
-      const float *mj = msg + static_cast<long long>(jj) * d;
+      float row[U][NC];
 #pragma unroll
-      for (int q = 0; q < NC; ++q) {
-        const int k = lane + q * kWave;
-        if (k < d) acc[q] += mj[k];
+      for (int t = 0; t < U; ++t) {
+        const float *mj = msg + static_cast<long long>(jj[t]) * d;
+#pragma unroll
+        for (int q = 0; q < NC; ++q) {
+          const int k = k0 + q * G;
+          row[t][q] = jj[t] >= 0 && k < d ? mj[k] : 0.0f;
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < U; ++t) {
+        if (jj[t] < 0) continue;
+        if (vv[t] != cur) {
+          if (cur >= 0) {
+            float *sv = S + static_cast<long long>(cur) * d;
+#pragma unroll
+            for (int q = 0; q < NC; ++q) {
+              const int k = k0 + q * G;
+              if (k < d) unsafeAtomicAdd(&sv[k], acc[q]);
+              acc[q] = 0.0f;
+            }
+            if (mark != nullptr && k0 == 0) mark_only(mark, cur);
+          }
+          cur = vv[t];
+        }
+#pragma unroll
+        for (int q = 0; q < NC; ++q) acc[q] += row[t][q];
       }
     }
     if (cur >= 0) {
       float *sv = S + static_cast<long long>(cur) * d;
 #pragma unroll
       for (int q = 0; q < NC; ++q) {
-        const int k = lane + q * kWave;
+        const int k = k0 + q * G;
         if (k < d) unsafeAtomicAdd(&sv[k], acc[q]);
       }
+      if (mark != nullptr && k0 == 0) mark_only(mark, cur);
     }
   }
 }
@@ -681,16 +756,20 @@ void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u6
 }
 
 void launch_pull_msgs(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *ioff,
-                      Adj in, const unsigned *member, const int *slot, const float *msg, float *S, const Counters *c) {
+                      Adj in, const unsigned *member, const int *wprefix, const float *msg, float *S,
+                      unsigned *mark, const Counters *c) {
   const int blocks = 2048;
-#define RP_PULLM(NCV)                                                                                         \
-  hipLaunchKernelGGL((k_pull_msgs<NCV>), dim3(blocks), dim3(256), 0, s, d, list, count, ioff, in, member, slot, \
-                     msg, S, c)
-  if (d <= 64) RP_PULLM(1);
-  else if (d <= 128) RP_PULLM(2);
-  else if (d <= 256) RP_PULLM(4);
-  else if (d <= 512) RP_PULLM(8);
-  else RP_PULLM(16);
+#define RP_PULLM(GV, NCV, UV)                                                                                      \
+  hipLaunchKernelGGL((k_pull_msgs<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, list, count, ioff, in, member, \
+                     wprefix, msg, S, mark, c)
+  if (d <= 16) RP_PULLM(16, 1, 4);
+  else if (d <= 32) RP_PULLM(16, 2, 4);
+  else if (d <= 48) RP_PULLM(16, 3, 4);
+  else if (d <= 64) RP_PULLM(16, 4, 4);
+  else if (d <= 128) RP_PULLM(64, 2, 8);
+  else if (d <= 256) RP_PULLM(64, 4, 8);
+  else if (d <= 512) RP_PULLM(64, 8, 4);
+  else RP_PULLM(64, 16, 2);
 #undef RP_PULLM
 }
 

@@ -8,7 +8,9 @@
 // as float4 while the current step's MFMAs run from LDS, then stored into the
 // other half of a double buffer, so there is one barrier per K step. Tiles are
 // visited by a grid-stride loop so the row count can stay on the device. BN
-// follows the layer width (16, 32, 48, 64, 128) and BM the expected row count.
+// follows the layer width (16, 32, 48, 64, 128). Short row lists (the common
+// case for small batches) go to a 16-row kernel that loads operands straight
+// into registers and is bound by memory latency rather than throughput.
 // The epilogue adds the bias, applies ReLU, forms the next layer's delta row
 // (c'_v y - c_v h_old) and overwrites the embedding row.
 //
@@ -259,152 +261,190 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
   }
 }
 
-// Small-row-count variant: a block owns a 16 x BN tile and its four waves split
-// each 128-deep K step between them (wave w takes the 4-deep sub-steps w, w+4,
-// ...), so a short row list still spreads over many waves and K = 512 takes four
-// steps; the partial tiles are summed through LDS before the epilogue.
-constexpr int kSmallBM = 16;
-constexpr int kSmallBK = 128;
-constexpr int kSmallLdk = kSmallBK + 4;
+// Small-row-count variant, built for latency: a block owns a 16 x BN output tile
+// and its four waves split K into four contiguous ranges. Every lane loads its
+// operands straight from global memory into registers as float4: lane (r, q)
+// holds A row r and B column r at k = 16 f + 4 q .. 16 f + 4 q + 3 of its range,
+// and at MFMA sub-step i both operands give component i, the same permutation of
+// k on both sides. A range of up to 128 k values thus costs one round of loads and
+// no LDS staging. The epilogue's inputs (old embedding row, cached transform,
+// degrees, bias) are fetched as soon as the row ids are known, together with the
+// operands, so a tile takes three dependent rounds of memory access: row count,
+// row ids, then everything else. The four partial tiles meet in LDS.
+constexpr int kRowsBM = 16;
+constexpr int kRowsKC = 128;  // k values per wave per round of loads
 
-template <int BN, int AGG, bool VEC, int MODE>
-__global__ __launch_bounds__(kThreads) void k_gemm_small(GemmArgs a) {
+template <int BN, int AGG, int MODE>
+__global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
   constexpr int WN = BN / 16;
-  constexpr int kAChunks = kSmallBM * (kSmallBK / 4);
-  constexpr int kBChunks = BN * (kSmallBK / 4);
-  constexpr int kAPer = (kAChunks + kThreads - 1) / kThreads;
-  constexpr int kBPer = (kBChunks + kThreads - 1) / kThreads;
+  constexpr int kF = kRowsKC / 16;            // float4 per lane per operand row and round
+  constexpr int kEl = kRowsBM * BN / kThreads;  // output elements per thread
+  static_assert(kRowsBM * BN % kThreads == 0, "whole elements per thread");
   if (a.abort != nullptr && *a.abort) return;
   const long long M = a.count != nullptr ? static_cast<long long>(*a.count) : a.count_fixed;
-  const int N = a.N, K = a.K;
+  const int N = a.N, K = a.K, dp = a.dprev;
   const long long tiles_n = (N + BN - 1) / BN;
-  const long long tiles = ((M + kSmallBM - 1) / kSmallBM) * tiles_n;
+  const long long tiles = ((M + kRowsBM - 1) / kRowsBM) * tiles_n;
 
-  __shared__ float As[2][kSmallBM][kSmallLdk];
-  __shared__ float Bs[2][BN][kSmallLdk];
-  __shared__ float red[4][kSmallBM][BN + 1];
-  __shared__ int rv[kSmallBM];
-  __shared__ float rt[kSmallBM];
-  __shared__ float rs[kSmallBM];
+  __shared__ float red[4][kRowsBM][BN + 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
   const int lr = lane & 15;
-  const int lk = lane >> 4;
+  const int lq = lane >> 4;
+  const int kw = (K + 63) / 64 * 16;  // k values per wave, a multiple of 16
+  const int kb = wave * kw;
+  const int ke = K < kb + kw ? K : kb + kw;
 
   for (long long t = blockIdx.x; t < tiles; t += gridDim.x) {
-    const long long m0 = (t / tiles_n) * kSmallBM;
+    const long long m0 = (t / tiles_n) * kRowsBM;
     const int n0 = static_cast<int>(t % tiles_n) * BN;
-    __syncthreads();
-    if (tid < kSmallBM) {
-      const long long row = m0 + tid;
-      int v = -1;
-      float tv = 0.f, sv = 0.f;
-      if (row < M) {
-        v = a.rows != nullptr ? a.rows[row] : static_cast<int>(row);
+    // row ids: the lane's operand row and the rows of its output elements
+    const long long ar = m0 + lr;
+    const int va = ar < M ? (a.rows != nullptr ? a.rows[ar] : static_cast<int>(ar)) : -1;
+    int ve[kEl];
+#pragma unroll
+    for (int i = 0; i < kEl; ++i) {
+      const long long row = m0 + (tid + i * kThreads) / BN;
+      ve[i] = row < M ? (a.rows != nullptr ? a.rows[row] : static_cast<int>(row)) : -1;
+    }
+    // operand-row scales (layer mode): mean t = 1/deg_in; GCN t = (deg_in+1)^-1/2,
+    // s = (deg_out+1)^-1/2
+    float ta = 1.f, sa = 0.f;
+    if (MODE == kLayer && va >= 0) {
+      if (AGG == kMean) {
+        const int din = a.in_len[va];
+        ta = din > 0 ? 1.0f / static_cast<float>(din) : 0.f;
+      } else if (AGG == kGcn) {
+        ta = 1.0f / sqrtf(static_cast<float>(a.in_len[va]) + 1.0f);
+        sa = 1.0f / sqrtf(static_cast<float>(a.out_len[va]) + 1.0f);
+      }
+    }
+    // epilogue inputs
+    float e_old[kEl], e_t[kEl], e_tv[kEl], e_sv[kEl], e_co[kEl], e_b[kEl];
+#pragma unroll
+    for (int i = 0; i < kEl; ++i) {
+      const int col = n0 + (tid + i * kThreads) % BN;
+      const int v = ve[i];
+      e_old[i] = 0.f;
+      e_t[i] = 0.f;
+      e_tv[i] = 1.f;
+      e_sv[i] = 0.f;
+      e_co[i] = 1.f;
+      e_b[i] = 0.f;
+      if (v < 0 || col >= N) continue;
+      const long long idx = static_cast<long long>(v) * N + col;
+      if (a.delta != nullptr) e_old[i] = a.H[idx];
+      if (a.bias != nullptr) e_b[i] = a.bias[col];
+      if (MODE == kTransformFirst) {
+        e_t[i] = a.S[idx];
         if (AGG == kMean) {
           const int din = a.in_len[v];
-          tv = din > 0 ? 1.0f / static_cast<float>(din) : 0.f;
+          e_tv[i] = din > 0 ? 1.0f / static_cast<float>(din) : 0.f;
         } else if (AGG == kGcn) {
-          tv = 1.0f / sqrtf(static_cast<float>(a.in_len[v]) + 1.0f);
-          sv = 1.0f / sqrtf(static_cast<float>(a.out_len[v]) + 1.0f);
-        } else {
-          tv = 1.0f;
+          e_tv[i] = 1.0f / sqrtf(static_cast<float>(a.in_len[v]) + 1.0f);
         }
       }
-      rv[tid] = v;
-      rt[tid] = tv;
-      rs[tid] = sv;
+      if (AGG == kGcn) {
+        const int dout = a.out_len[v];
+        e_sv[i] = 1.0f / sqrtf(static_cast<float>(dout) + 1.0f);
+        e_co[i] = 1.0f / sqrtf(static_cast<float>(dout - a.ddeg[v]) + 1.0f);
+      }
     }
-    __syncthreads();
-
-    float4 ra[kAPer], rb[kBPer];
-    auto load_regs = [&](int k0) {
-#pragma unroll
-      for (int i = 0; i < kAPer; ++i) {
-        const int c = tid + i * kThreads;
-        if (c < kAChunks) {
-          const int m = c / (kSmallBK / 4);
-          const int q = c % (kSmallBK / 4);
-          ra[i] = load_a<AGG, VEC, MODE>(a, rv[m], rt[m], rs[m], k0 + 4 * q);
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < kBPer; ++i) {
-        const int c = tid + i * kThreads;
-        if (c < kBChunks) {
-          const int nn = c / (kSmallBK / 4);
-          const int q = c % (kSmallBK / 4);
-          rb[i] = load_b<VEC>(a, n0 + nn, k0 + 4 * q);
-        }
-      }
-    };
-    auto store_lds = [&](int buf) {
-#pragma unroll
-      for (int i = 0; i < kAPer; ++i) {
-        const int c = tid + i * kThreads;
-        if (c < kAChunks) {
-          const int m = c / (kSmallBK / 4);
-          const int q = c % (kSmallBK / 4);
-          *reinterpret_cast<float4 *>(&As[buf][m][4 * q]) = ra[i];
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < kBPer; ++i) {
-        const int c = tid + i * kThreads;
-        if (c < kBChunks) {
-          const int nn = c / (kSmallBK / 4);
-          const int q = c % (kSmallBK / 4);
-          *reinterpret_cast<float4 *>(&Bs[buf][nn][4 * q]) = rb[i];
-        }
-      }
-    };
 
     floatx4 acc[WN];
 #pragma unroll
     for (int j = 0; j < WN; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    load_regs(0);
-    store_lds(0);
-    __syncthreads();
-    int buf = 0;
-    for (int k0 = 0; k0 < K; k0 += kSmallBK) {
-      const bool more = k0 + kSmallBK < K;
-      if (more) load_regs(k0 + kSmallBK);
+    const long long abase = static_cast<long long>(va) * dp;
+    for (int kc = kb; kc < ke; kc += kRowsKC) {
+      float4 av[kF], ah[kF], bv[WN][kF];
 #pragma unroll
-      for (int kk = 4 * wave; kk < kSmallBK; kk += 16) {
-        const float av = As[buf][lr][kk + lk];
-#pragma unroll
-        for (int j = 0; j < WN; ++j)
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, Bs[buf][j * 16 + lr][kk + lk], acc[j], 0, 0, 0);
+      for (int f = 0; f < kF; ++f) {
+        const int k = kc + 16 * f + 4 * lq;
+        const bool ok = va >= 0 && k < ke;
+        float4 x = make_float4(0.f, 0.f, 0.f, 0.f), h = x;
+        if (ok) {
+          if (MODE != kLayer) {
+            x = *reinterpret_cast<const float4 *>(a.Hprev + abase + k);
+          } else if (AGG == kGcn) {  // K == dp: z = t (S + s h)
+            x = *reinterpret_cast<const float4 *>(a.S + abase + k);
+            h = *reinterpret_cast<const float4 *>(a.Hprev + abase + k);
+          } else {  // z = [h || t S]
+            x = k < dp ? *reinterpret_cast<const float4 *>(a.Hprev + abase + k)
+                       : *reinterpret_cast<const float4 *>(a.S + abase + (k - dp));
+          }
+        }
+        av[f] = x;
+        ah[f] = h;
       }
-      if (more) store_lds(buf ^ 1);
-      __syncthreads();
-      buf ^= 1;
+#pragma unroll
+      for (int j = 0; j < WN; ++j) {
+        const int col = n0 + 16 * j + lr;
+#pragma unroll
+        for (int f = 0; f < kF; ++f) {
+          const int k = kc + 16 * f + 4 * lq;
+          bv[j][f] = col < N && k < ke ? *reinterpret_cast<const float4 *>(a.W + static_cast<long long>(col) * K + k)
+                                       : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+      if (MODE == kLayer && AGG != kSum) {
+#pragma unroll
+        for (int f = 0; f < kF; ++f) {
+          const int k = kc + 16 * f + 4 * lq;
+          if (AGG == kGcn) {
+            av[f] = make_float4(ta * (av[f].x + sa * ah[f].x), ta * (av[f].y + sa * ah[f].y),
+                                ta * (av[f].z + sa * ah[f].z), ta * (av[f].w + sa * ah[f].w));
+          } else if (k >= dp) {
+            av[f] = make_float4(ta * av[f].x, ta * av[f].y, ta * av[f].z, ta * av[f].w);
+          }
+        }
+      }
+#pragma unroll
+      for (int f = 0; f < kF; ++f) {
+        const float ax[4] = {av[f].x, av[f].y, av[f].z, av[f].w};
+#pragma unroll
+        for (int j = 0; j < WN; ++j) {
+          const float bx[4] = {bv[j][f].x, bv[j][f].y, bv[j][f].z, bv[j][f].w};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ax[i], bx[i], acc[j], 0, 0, 0);
+        }
+      }
     }
-    // partial tiles -> LDS, summed by all threads
+    // lane holds C[4 q + r][r'] of each 16 x 16 tile (q = lane / 16, r' = lane % 16)
 #pragma unroll
     for (int j = 0; j < WN; ++j)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) red[wave][lk * 4 + r][j * 16 + lr] = acc[j][r];
+      for (int r = 0; r < 4; ++r) red[wave][lq * 4 + r][j * 16 + lr] = acc[j][r];
     __syncthreads();
-    for (int e = tid; e < kSmallBM * BN; e += kThreads) {
+#pragma unroll
+    for (int i = 0; i < kEl; ++i) {
+      const int e = tid + i * kThreads;
       const int ml = e / BN, cl = e % BN;
       const int col = n0 + cl;
-      const int v = rv[ml];
+      const int v = ve[i];
       if (v < 0 || col >= N) continue;
-      const float y = red[0][ml][cl] + red[1][ml][cl] + red[2][ml][cl] + red[3][ml][cl];
-      epilogue<AGG, MODE>(a, m0 + ml, v, col, y, rt[ml], rs[ml]);
+      float y = red[0][ml][cl] + red[1][ml][cl] + red[2][ml][cl] + red[3][ml][cl];
+      if (MODE == kTransformFirst) y = AGG == kGcn ? e_tv[i] * (e_t[i] + e_sv[i] * y) : y + e_tv[i] * e_t[i];
+      y += e_b[i];
+      if (a.relu) y = fmaxf(y, 0.f);
+      const long long idx = static_cast<long long>(v) * N + col;
+      if (a.delta != nullptr) {
+        const float cn = AGG == kGcn ? e_sv[i] : 1.f;
+        a.delta[(m0 + ml) * N + col] = cn * y - e_co[i] * e_old[i];
+      }
+      a.H[idx] = y;
     }
+    __syncthreads();  // red is reused by the next tile
   }
 }
 
-template <int BN, int AGG, bool VEC, int MODE>
-void launch_small(hipStream_t s, const GemmArgs &a, long long max_rows) {
-  const long long tiles = ((max_rows + kSmallBM - 1) / kSmallBM) * ((a.N + BN - 1) / BN);
+template <int BN, int AGG, int MODE>
+void launch_rows(hipStream_t s, const GemmArgs &a, long long max_rows) {
+  const long long tiles = ((max_rows + kRowsBM - 1) / kRowsBM) * ((a.N + BN - 1) / BN);
   long long blocks = tiles < 1 ? 1 : tiles;
   if (blocks > 2048) blocks = 2048;
-  hipLaunchKernelGGL((k_gemm_small<BN, AGG, VEC, MODE>), dim3(blocks), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL((k_gemm_rows<BN, AGG, MODE>), dim3(blocks), dim3(kThreads), 0, s, a);
 }
 
 template <int BM, int BN, int WM, int WN, int AGG, bool VEC, int MODE>
@@ -428,10 +468,10 @@ void launch_agg(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) 
     return;
   }
   if (!big) {
-    if (N <= 16) launch_small<16, AGG, VEC, MODE>(s, a, max_rows);
-    else if (N <= 32) launch_small<32, AGG, VEC, MODE>(s, a, max_rows);
-    else if (N <= 48) launch_small<48, AGG, VEC, MODE>(s, a, max_rows);
-    else launch_small<64, AGG, VEC, MODE>(s, a, max_rows);  // N > 64: several 64-wide column tiles
+    if (N <= 16) launch_rows<16, AGG, MODE>(s, a, max_rows);
+    else if (N <= 32) launch_rows<32, AGG, MODE>(s, a, max_rows);
+    else if (N <= 48) launch_rows<48, AGG, MODE>(s, a, max_rows);
+    else launch_rows<64, AGG, MODE>(s, a, max_rows);  // N > 64: several 64-wide column tiles
     return;
   }
   if (N <= 16) launch_shape<64, 16, 1, 1, AGG, VEC, MODE>(s, a, max_rows);

@@ -198,6 +198,8 @@ __global__ void k_topo_plan(Adj out, Adj in, const int *ins_src, const int *ins_
 
 // One wave per touched (row, direction): the row's owner is its rank-0 insert
 // item, or its rank-0 delete item when it has no inserts.
+constexpr int kRewriteU = 8;
+
 __global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, const int *ins_src,
                                const int *ins_dst, const int *del_src, const int *del_dst, const int *ins_rank,
                                const int *del_rank, const u64 *ht_key, const int *ht_net, unsigned mask,
@@ -233,18 +235,42 @@ __global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, con
       const int *src = a.col + src_off;
       int *dst = a.col + dst_off;
       int wpos = 0;
-      for (int base = 0; base < len0; base += kWave) {
-        const int e = base + lane;
-        const int x = e < len0 ? src[e] : -1;
-        bool keep = e < len0;
-        if (keep && k > 0) {
-          const int au = dir ? x : row, av = dir ? row : x;
-          const int slot = hash_find(ht_key, mask, edge_key(au, av, undirected, n));
-          keep = slot < 0 || ht_net[slot] != -1;
+      // kRewriteU entries per lane per step: the step's row reads, then its first
+      // hash probes, are all in flight together (a probe that meets another key
+      // continues alone); all reads of a step precede its writes, and a kept entry
+      // is written at or below its own position, so the in-place case is safe.
+      for (int base = 0; base < len0; base += kWave * kRewriteU) {
+        int x[kRewriteU];
+        bool keep[kRewriteU];
+#pragma unroll
+        for (int u = 0; u < kRewriteU; ++u) {
+          const int e = base + u * kWave + lane;
+          keep[u] = e < len0;
+          x[u] = keep[u] ? src[e] : -1;
         }
-        const u64 m = __ballot(keep);
-        if (keep) dst[wpos + lanes_below(m)] = x;  // in place: never past the entry read
-        wpos += __popcll(m);
+        if (k > 0) {
+          u64 key[kRewriteU], got[kRewriteU];
+          unsigned sl[kRewriteU];
+#pragma unroll
+          for (int u = 0; u < kRewriteU; ++u) {
+            key[u] = edge_key(dir ? x[u] : row, dir ? row : x[u], undirected, n);
+            sl[u] = hash_slot(key[u], mask);
+          }
+#pragma unroll
+          for (int u = 0; u < kRewriteU; ++u) got[u] = keep[u] ? ht_key[sl[u]] : kEmptyKey;
+#pragma unroll
+          for (int u = 0; u < kRewriteU; ++u) {
+            if (!keep[u] || got[u] == kEmptyKey) continue;
+            const int slot = got[u] == key[u] ? static_cast<int>(sl[u]) : hash_find(ht_key, mask, key[u]);
+            keep[u] = slot < 0 || ht_net[slot] != -1;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kRewriteU; ++u) {
+          const u64 m = __ballot(keep[u]);
+          if (keep[u]) dst[wpos + lanes_below(m)] = x[u];
+          wpos += __popcll(m);
+        }
       }
       if (lane == 0 && wpos != len0 - k) atomicOr(&c->err, 2ull);
     }

@@ -49,6 +49,7 @@ struct ripple_ctx {
   long long max_bytes = 0;
   long long arena_slots = 0;  // 0 = default sizing
   long long arcs_loaded = 0;  // arcs of the snapshot
+  long long arcs_now = 0;     // arcs stored now (snapshot + net inserts - net deletes)
   long long bytes = 0;
   std::unordered_map<void *, size_t> allocs;
   std::string err;
@@ -90,11 +91,12 @@ struct ripple_ctx {
   long long *doff[rp::kMaxL + 1] = {};  // out-degree prefix of lists[l] (first arc index per vertex)
   long long *ioff = nullptr;            // in-degree prefix of the current layer's A^l (pull form)
   unsigned *keep[2] = {nullptr, nullptr};  // bitmap of lists[k] for k = 0, 1 mod 2 (pull membership)
-  int *slot[2] = {nullptr, nullptr};       // position of each vertex in lists[k] (pull message rows)
+  int *wprefix[2] = {nullptr, nullptr};    // members of lists[k] before each bitmap word (message rows)
   int scatter_mode = RIPPLE_SCATTER_AUTO;
   long long last_pushed[rp::kMaxL + 1] = {};
   long long last_in[rp::kMaxL + 1] = {};
-  int last_pull = 0;
+  int last_pull = 0;   // layers that pulled over A^l's in-arcs (bit l)
+  int last_dense = 0;  // layers that pulled over every in-arc (bit l)
   float *delta[2] = {nullptr, nullptr};
   rp::Counters *d_counters = nullptr;  // two buffers; batch parity picks one
   int parity = 0;
@@ -403,7 +405,7 @@ void free_model(ripple_ctx *c) {
   dfree_t(c, c->ioff);
   for (int k = 0; k < 2; ++k) {
     dfree_t(c, c->keep[k]);
-    dfree_t(c, c->slot[k]);
+    dfree_t(c, c->wprefix[k]);
   }
   free_batch_scratch(c);
   c->inited = false;
@@ -513,20 +515,30 @@ void add_launches(ripple_ctx *c, int phase, int k) {
   if (c->prof) c->ph_launch[phase] += k;
 }
 
-// Push or pull for layer l. Forced modes aside, estimate the bytes of each form
-// from the previous batch's counts for this layer: push moves every message as a
-// row of atomics (weighted 4x: atomics run at about a quarter of the read rate);
-// pull reads every in-arc of A^l, reads each message once and makes one atomic
-// row update per affected vertex.
-bool use_pull(const ripple_ctx *c, int l) {
-  if (c->scatter_mode == RIPPLE_SCATTER_PUSH) return false;
-  if (c->scatter_mode == RIPPLE_SCATTER_PULL) return true;
-  if (!c->has_batch) return false;
+// How layer l adds its messages to S^l. Forced modes aside, estimate the bytes of
+// each form from the previous batch's counts for this layer (push on the first
+// batch). Push and pull both mark the sinks of every pushed arc with a bit atomic
+// (about 24 bytes of traffic each, as measured); push then moves every message as
+// a row of atomics (weighted 4x: atomics run at about a quarter of the read rate);
+// pull reads every in-arc of A^l, each message once and makes one atomic row
+// update per affected vertex; dense does the same over every in-arc of the graph
+// and needs no marks (a sink that receives a message is marked once).
+enum LayerMode { kPushLayer = 0, kPullLayer = 1, kDenseLayer = 2 };
+
+int layer_mode(const ripple_ctx *c, int l) {
+  if (c->scatter_mode == RIPPLE_SCATTER_PUSH) return kPushLayer;
+  if (c->scatter_mode == RIPPLE_SCATTER_PULL) return kPullLayer;
+  if (c->scatter_mode == RIPPLE_SCATTER_DENSE) return kDenseLayer;
+  if (!c->has_batch) return kPushLayer;
   const double w = 4.0 * c->sw[l];
-  const double push = 4.0 * w * static_cast<double>(c->last_pushed[l]);
-  const double pull = 12.0 * static_cast<double>(c->last_in[l]) + w * static_cast<double>(c->last_pushed[l]) +
-                      4.0 * w * static_cast<double>(c->last_count[l]);
-  return pull < push;
+  const double pushed = static_cast<double>(c->last_pushed[l]);
+  const double mark = 24.0 * pushed;
+  const double push = mark + 4.0 * w * pushed;
+  const double settle = w * pushed + 4.0 * w * static_cast<double>(c->last_count[l]);
+  const double pull = mark + 12.0 * static_cast<double>(c->last_in[l]) + settle;
+  const double dense = 12.0 * static_cast<double>(c->arcs_now + c->n) + settle;
+  if (push <= pull && push <= dense) return kPushLayer;
+  return pull <= dense ? kPullLayer : kDenseLayer;
 }
 
 rp::CompactScratch compact_scratch(ripple_ctx *c, rp::Counters *dc) {
@@ -542,6 +554,7 @@ void issue_batch(ripple_ctx *c, int B) {
   const int cap_arcs = static_cast<int>(2 * c->cap_ops);
   rp::Adj out = c->adj[0], in = c->adj[1];
   c->last_pull = 0;
+  c->last_dense = 0;
   PhaseScope total(c, RIPPLE_PHASE_TOTAL);
   {
     PhaseScope ps(c, RIPPLE_PHASE_NET);
@@ -571,8 +584,9 @@ void issue_batch(ripple_ctx *c, int B) {
     co.out_deg = c->adj[0].len;
     co.doff = c->doff[0];
     co.out_total = &dc->pushed[1];
-    co.keep = use_pull(c, 1) ? c->keep[0] : nullptr;
-    co.slot = use_pull(c, 1) ? c->slot[0] : nullptr;
+    const bool members = layer_mode(c, 1) != kPushLayer;  // layer 1 pulls: it needs A^0's membership
+    co.keep = members ? c->keep[0] : nullptr;
+    co.wprefix = members ? c->wprefix[0] : nullptr;
     rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
     rp::launch_delta0(s, c->n, c->agg, c->dims[0], c->lists[0], &dc->count[0], c->d_ops, c->h_feat, c->fop,
                       c->H[0], c->adj[0].len, c->ddeg, c->delta[0], dc);
@@ -591,13 +605,32 @@ void issue_batch(ripple_ctx *c, int B) {
       add_launches(c, RIPPLE_PHASE_GEMM, 1);
       msg = c->msg;
     }
-    const bool pull = use_pull(c, l);
-    if (pull) c->last_pull |= 1 << l;
-    {
+    const int mode = layer_mode(c, l);
+    if (mode == kPullLayer) c->last_pull |= 1 << l;
+    if (mode == kDenseLayer) c->last_dense |= 1 << l;
+    const unsigned *member = c->keep[(l - 1) & 1];
+    const int *wprefix = c->wprefix[(l - 1) & 1];
+    if (mode == kDenseLayer) {
+      // dense: mark the net arcs' heads and D (no arcs), list every vertex with its
+      // in-arc prefix, pull over every in-arc and mark the sinks that received a
+      // message
+      PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
+      rp::launch_scatter(s, c->n, c->sw[l], c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out, c->S[l],
+                         c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->zero, dc, false);
+      rp::CompactOut all{};
+      all.full_n = c->n;
+      all.count = &dc->count_all;
+      all.in_deg = c->adj[1].len;
+      all.ioff = c->ioff;
+      rp::launch_compact(s, c->n, nullptr, nullptr, compact_scratch(c, dc), all);
+      rp::launch_pull_msgs(s, c->n, c->sw[l], nullptr, &dc->count_all, c->ioff, in, member, wprefix, msg,
+                           c->S[l], c->bm_out, dc);
+      add_launches(c, RIPPLE_PHASE_SCATTER, 3);
+    } else {
       // push: marks + atomic adds; pull: marks only (the adds follow the compaction)
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
       rp::launch_scatter(s, c->n, c->sw[l], c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out, c->S[l],
-                         c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc, !pull);
+                         c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc, mode == kPushLayer);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     {
@@ -608,20 +641,20 @@ void issue_batch(ripple_ctx *c, int B) {
       co.out_deg = c->adj[0].len;
       co.doff = l < c->L ? c->doff[l] : nullptr;
       co.in_deg = c->adj[1].len;
-      co.ioff = pull ? c->ioff : nullptr;
+      co.ioff = mode == kPullLayer ? c->ioff : nullptr;
       co.in_total = &dc->indeg[l];
       co.out_total = l < c->L ? &dc->pushed[l + 1] : nullptr;
       co.sinks_a = &dc->dest[l];  // distinct sinks of the arcs pushed at layer l
-      const bool next_pull = l < c->L && use_pull(c, l + 1);
-      co.keep = next_pull ? c->keep[l & 1] : nullptr;
-      co.slot = next_pull ? c->slot[l & 1] : nullptr;
+      const bool members = l < c->L && layer_mode(c, l + 1) != kPushLayer;
+      co.keep = members ? c->keep[l & 1] : nullptr;
+      co.wprefix = members ? c->wprefix[l & 1] : nullptr;
       rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
       add_launches(c, RIPPLE_PHASE_COMPACT, 1);
     }
-    if (pull) {
+    if (mode == kPullLayer) {
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
-      rp::launch_pull_msgs(s, c->n, c->sw[l], c->lists[l], &dc->count[l], c->ioff, in, c->keep[(l - 1) & 1],
-                           c->slot[(l - 1) & 1], msg, c->S[l], dc);
+      rp::launch_pull_msgs(s, c->n, c->sw[l], c->lists[l], &dc->count[l], c->ioff, in, member, wprefix, msg,
+                           c->S[l], nullptr, dc);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     {
@@ -656,6 +689,8 @@ void account_phases(ripple_ctx *c) {
     c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * k.pushed[l] + 8.0 * nd + 4.0 * d * nd + 8.0 * d * k.dest[l];
     if (c->last_pull >> l & 1)  // pull: every in-arc id of A^l and its in-row offset
       c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * k.indeg[l] + 12.0 * k.count[l];
+    if (c->last_dense >> l & 1)  // dense: every in-arc id and every vertex's in-row offset
+      c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * static_cast<double>(c->arcs_now) + 12.0 * static_cast<double>(c->n);
     if (c->tf[l]) {
       const double dp = c->dims[l - 1];
       c->ph_flops[RIPPLE_PHASE_GEMM] += 2.0 * nd * dp * d;
@@ -784,6 +819,7 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   // host-side validation and counting sort into CSR (by source) and CSC (by sink)
   const long long arcs = c->undirected ? 2 * m : m;
   c->arcs_loaded = arcs;
+  c->arcs_now = arcs;
   std::vector<int> outdeg(n, 0), indeg(n, 0);
   for (long long i = 0; i < m; ++i) {
     const int u = g->src[i], v = g->dst[i];
@@ -968,7 +1004,7 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   RP_TRY(dalloc_n(c, &c->ioff, n + 1));
   for (int k = 0; k < 2; ++k) {
     RP_TRY(dalloc_n(c, &c->keep[k], (n + 31) / 32));
-    RP_TRY(dalloc_n(c, &c->slot[k], n));
+    RP_TRY(dalloc_n(c, &c->wprefix[k], (n + 31) / 32));
   }
   if (msg_width > 0) RP_TRY(dalloc_n(c, &c->msg, n * msg_width));
   for (int l = 1; l <= L; ++l)
@@ -1034,6 +1070,7 @@ ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t 
     // match; bit 2: the compaction's wait for a predecessor tile timed out
     return fail(c, RIPPLE_E_DEVICE, "ripple: device-side check failed (err bits " + std::to_string(k.err) + ")");
   }
+  c->arcs_now += static_cast<long long>(k.n_ins) - static_cast<long long>(k.n_del);
   account_phases(c);
   c->has_batch = true;
   c->last_nfeat = static_cast<long long>(k.n_feat);
@@ -1061,6 +1098,7 @@ ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t 
     stats->repacks = repacks;
     for (int l = 1; l <= c->L; ++l) stats->in_arcs[l] = static_cast<int64_t>(k.indeg[l]);
     stats->pull_layers = c->last_pull;
+    stats->dense_layers = c->last_dense;
   }
   return RIPPLE_OK;
 }
@@ -1145,7 +1183,7 @@ ripple_status ripple_get_arcs(ripple_ctx *c, int32_t direction, int32_t *src, in
 
 ripple_status ripple_set_scatter_mode(ripple_ctx *c, int32_t mode) {
   RP_TRY(check_ctx(c));
-  if (mode < RIPPLE_SCATTER_AUTO || mode > RIPPLE_SCATTER_PULL) return fail(c, RIPPLE_E_INVALID, "ripple: bad mode");
+  if (mode < RIPPLE_SCATTER_AUTO || mode > RIPPLE_SCATTER_DENSE) return fail(c, RIPPLE_E_INVALID, "ripple: bad mode");
   c->scatter_mode = mode;
   return RIPPLE_OK;
 }

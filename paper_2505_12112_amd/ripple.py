@@ -31,7 +31,7 @@ EXPORTED = [
     "ripple_set_profiling", "ripple_get_phase_stats", "ripple_phase_name", "ripple_last_error",
     "ripple_destroy", "ripple_set_scatter_mode",
 ]
-SCATTER = {"auto": 0, "push": 1, "pull": 2}
+SCATTER = {"auto": 0, "push": 1, "pull": 2, "dense": 3}
 
 
 class RippleUnavailable(RuntimeError):
@@ -70,7 +70,7 @@ class BatchStats(C.Structure):
         ("dirty", C.c_int64 * (MAX_LAYERS + 1)), ("affected", C.c_int64 * (MAX_LAYERS + 1)),
         ("pushed_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("dest_rows", C.c_int64 * (MAX_LAYERS + 1)),
         ("relocated_rows", C.c_int64), ("repacks", C.c_int64),
-        ("in_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("pull_layers", C.c_int32), ("pad", C.c_int32),
+        ("in_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("pull_layers", C.c_int32), ("dense_layers", C.c_int32),
     ]
 
 
@@ -215,7 +215,7 @@ class Ripple:
             "dirty": list(st.dirty[:L + 1]), "affected": list(st.affected[:L + 1]),
             "pushed_arcs": list(st.pushed_arcs[:L + 1]), "dest_rows": list(st.dest_rows[:L + 1]),
             "relocated_rows": st.relocated_rows, "repacks": st.repacks,
-            "in_arcs": list(st.in_arcs[:L + 1]), "pull_layers": st.pull_layers,
+            "in_arcs": list(st.in_arcs[:L + 1]), "pull_layers": st.pull_layers, "dense_layers": st.dense_layers,
         }
 
     def apply_updates_raw(self, ops: np.ndarray, feat_rows: Optional[np.ndarray], stats: BatchStats) -> None:

@@ -107,9 +107,9 @@ def test_dense_large_full_size():
         rng = np.random.default_rng(5)
         for b in range(3):
             st, _, sets = p.step(wl.stream.next_batch(100))
-            _say(f"  batch {b}: |A| = {[s.size for s in sets]}, pull layers {st['pull_layers']:b} "
-                 f"({time.time() - t0:.0f}s)")
-        assert st["pull_layers"] & 0b1000, "dense third layer should switch to the pull form"
+            _say(f"  batch {b}: |A| = {[s.size for s in sets]}, pull layers {st['pull_layers']:b}, "
+                 f"dense layers {st['dense_layers']:b} ({time.time() - t0:.0f}s)")
+        assert (st["pull_layers"] | st["dense_layers"]) & 0b1000, "the third layer should switch to a pull form"
         verts = _sample_vertices(rng, p.orc, sets[3], 24, 400_000)
         errs = _check_sampled(p, verts, (1, 2, 3))
         _say(f"  {verts.size} sampled vertices, row-relative errors {errs} ({time.time() - t0:.0f}s)")
@@ -117,18 +117,19 @@ def test_dense_large_full_size():
         p.close()
 
 
-def test_stress_full_size():
+@pytest.mark.parametrize("mode", ["pull", "dense"])
+def test_stress_full_size(mode):
     """RMAT graph at full size (2^23 vertices, 200M arcs, GCN 64-256-64), one
     hub-biased batch of 10,000 ops: affected sets bit for bit, embeddings of
     sampled vertices at both layers."""
     t0 = time.time()
     wl = synth.build_workload("stress")
-    _say(f"stress generated in {time.time() - t0:.0f}s")
-    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, mode="pull")
+    _say(f"stress generated in {time.time() - t0:.0f}s ({mode})")
+    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, mode=mode)
     try:
         _say(f"  loaded + bootstrapped, oracle built ({time.time() - t0:.0f}s)")
         st, _, sets = p.step(wl.stream.next_batch(10_000))
-        assert st["pull_layers"] == 0b110
+        assert st["pull_layers" if mode == "pull" else "dense_layers"] == 0b110
         _say(f"  batch: |A| = {[s.size for s in sets]}, pushed {st['pushed_arcs']} ({time.time() - t0:.0f}s)")
         rng = np.random.default_rng(6)
         verts = _sample_vertices(rng, p.orc, sets[2], 24, 2_000_000)

@@ -42,7 +42,7 @@ def test_bootstrap_matches_full_recompute(agg, dims):
         p.close()
 
 
-@pytest.mark.parametrize("mode", ["push", "pull"])
+@pytest.mark.parametrize("mode", ["push", "pull", "dense"])
 def test_tiny_config_stream(mode):
     """The tiny workload as specified: 10 batches of 45 inserts, 45 deletes, 10 features."""
     _say("tiny config", mode)
@@ -61,7 +61,7 @@ def test_tiny_config_stream(mode):
 
 @pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
 @pytest.mark.parametrize("undirected", [False, True])
-@pytest.mark.parametrize("mode", ["push", "pull"])
+@pytest.mark.parametrize("mode", ["push", "pull", "dense"])
 def test_adversarial_batches(agg, undirected, mode):
     """Colliding ops: repeated inserts/deletes of one edge, insert-then-delete,
     absent deletes, self-loops, repeated feature writes (sequential semantics)."""
@@ -115,7 +115,7 @@ def test_no_slack_forces_row_moves_and_relayouts(agg, arena):
 
 @pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
 @pytest.mark.parametrize("tf", [0, 1])
-@pytest.mark.parametrize("mode", ["push", "pull"])
+@pytest.mark.parametrize("mode", ["push", "pull", "dense"])
 def test_transform_first_choice_gives_the_same_results(agg, tf, mode):
     """Caching W_neigh S instead of S (and pushing W_neigh times the deltas) on
     every layer, or on none, matches the oracle like the default choice."""
@@ -221,7 +221,7 @@ def test_call_order_and_device_byte_cap():
 
 
 @pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
-@pytest.mark.parametrize("mode", ["auto", "pull"])
+@pytest.mark.parametrize("mode", ["auto", "pull", "dense"])
 def test_thousand_batches_on_a_small_graph(agg, mode):
     """1000 consecutive batches: sets every batch, embeddings every 100 and at the end."""
     _say("1000 batches", agg, mode)
