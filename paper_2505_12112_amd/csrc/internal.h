@@ -146,7 +146,7 @@ void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, 
                     const CompactOut &o);
 
 // layer 0 deltas (feat may be pinned host memory)
-void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list, const u64 *count,
+void launch_delta0(hipStream_t s, long long n, int agg, int d0, int ld, const int *list, const u64 *count,
                    const ripple_op *ops, const float *feat, const int *fop, float *X, const int *out_len,
                    const int *ddeg, float *delta, const Counters *c);
 
@@ -156,7 +156,7 @@ void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list,
 // marks (the pull kernel then adds the messages).
 // pushed = the number of arcs to push (the out-degree sum over the list, written
 // by the compaction that built the list).
-void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *doff,
+void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
                     const int *del_dst, const u64 *pushed, const Counters *c, bool push);
 
@@ -165,7 +165,7 @@ void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u6
 // is set in member, rank from wprefix (see CompactOut). One flush (row of fp32
 // atomics) per sink and lane group; each in-arc is read once. mark (nullable):
 // set the bit of every sink that received a message (the dense form's frontier).
-void launch_pull_msgs(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *ioff,
+void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *ioff,
                       Adj in, const unsigned *member, const int *wprefix, const float *msg, float *S,
                       unsigned *mark, const Counters *c);
 
@@ -185,6 +185,10 @@ void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev,
 // transform-first layer caches (H = P) and, with delta set, their messages
 // c'_v P'_v - c_v P_v.
 enum GemmMode { kLayer = 0, kTransformFirst = 1, kPlain = 2 };
+// Row stride (floats) of message and delta rows of width w: rows start on 64-byte
+// boundaries, so a row read touches the fewest memory segments.
+inline int row_ld(int w) { return (w + 15) / 16 * 16; }
+
 struct GemmArgs {
   int mode;
   const int *rows;
@@ -203,6 +207,7 @@ struct GemmArgs {
   int relu;
   float *H;
   float *delta;
+  int dld;  // row stride of delta (floats)
   int agg;
   const u64 *abort;
 };

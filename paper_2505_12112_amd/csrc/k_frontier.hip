@@ -355,7 +355,7 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
   }
 }
 
-__global__ void k_delta0(int agg, int d0, const int *list, const u64 *count, const ripple_op *ops,
+__global__ void k_delta0(int agg, int d0, int ld, const int *list, const u64 *count, const ripple_op *ops,
                          const float *feat, const int *fop, float *X, const int *out_len, const int *ddeg,
                          float *delta, const Counters *c) {
   if (c->abort) return;
@@ -371,7 +371,7 @@ __global__ void k_delta0(int agg, int d0, const int *list, const u64 *count, con
     }
     float *xu = X + static_cast<long long>(u) * d0;
     const float *xn = fo >= 0 ? feat + static_cast<long long>(ops[fo].feat_row) * d0 : xu;
-    float *dj = delta + j * d0;
+    float *dj = delta + j * ld;
     for (int k = lane; k < d0; k += kWave) {
       const float xo = xu[k];
       const float x1 = xn[k];
@@ -432,7 +432,7 @@ __device__ inline long long owner_from(const long long *a, long long from, long 
 // delta row stays in registers while consecutive arcs share a source, so a hub's
 // arcs cost one row load per chunk; hubs spread over many waves.
 template <int G, int NC, bool PUSH>
-__global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u64 *count, const long long *doff,
+__global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list, const u64 *count, const long long *doff,
                                                  const float *delta, Adj out, float *S, unsigned *bm_out,
                                                  unsigned *bm_x, const int *ins_dst, const int *del_dst,
                                                  const u64 *pushed, const Counters *c) {
@@ -469,7 +469,7 @@ __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u
     if (PUSH && ja != cached) {
       // the chunk's first source is known before its arcs are resolved: fetch its
       // delta row now so that the load overlaps the list / offset / column reads
-      const float *dj = delta + ja * d;
+      const float *dj = delta + ja * ld;
 #pragma unroll
       for (int q = 0; q < NC; ++q) {
         const int k = k0 + q * G;
@@ -504,7 +504,7 @@ __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u
       const int jj = __shfl(j, i + grp);
       if (vv >= 0) {
         if (jj != cached) {
-          const float *dj = delta + static_cast<long long>(jj) * d;
+          const float *dj = delta + static_cast<long long>(jj) * ld;
 #pragma unroll
           for (int q = 0; q < NC; ++q) {
             const int k = k0 + q * G;
@@ -525,28 +525,37 @@ __global__ __launch_bounds__(256) void k_scatter(int d, const int *list, const u
 
 // Pull form of the message step (for dense frontiers). In-arcs of the sorted
 // list A are numbered like the scatter's out-arcs (ioff gives each listed
-// vertex's first in-arc). A wave takes C consecutive in-arcs (a contiguous run of
-// such chunks per wave); each lane resolves one arc's sink v and source u and
-// keeps it if u is dirty (member bit), with the source's message row: u's rank
-// among the members, from the member word and the count of members before it.
-// Groups of G lanes then walk the kept arcs of their own G-lane window in order,
-// U message rows in flight at a time, summing rows into registers while the sink
-// stays the same and adding each sum to S[v] with one row of fp32 atomics: a
-// sink's messages cost one read each and one row update per group instead of one
-// atomic row each. G = 16 for rows of at most 64 floats (four arcs per wave
-// instruction), else 64.
+// vertex's first in-arc). A wave takes chunks of up to 256 consecutive in-arcs (a
+// contiguous run of chunks per wave), each lane up to four consecutive arcs: it
+// resolves their sinks v and sources u, all loads of its arcs in flight together,
+// and keeps an arc if u is dirty (member bit), with the source's message row (u's
+// rank among the members, from the member word and the count of members before
+// it). The (sink, row) pairs go to LDS in arc order. Groups of G lanes then walk
+// the arcs of their own window (a quarter of the chunk when G = 16, all of it when
+// G = 64), U message rows in flight at a time, summing rows into registers while
+// the sink stays the same and adding each sum to S[v] with one row of fp32
+// atomics: a sink's messages cost one read each, and one row update per window it
+// spans. G = 16 for rows of at most 64 floats (four rows per wave instruction).
+constexpr int kPullArcs = 4;  // arcs per lane per chunk
+constexpr int kPullChunk = kWave * kPullArcs;
+
 template <int G, int NC, int U>
-__global__ __launch_bounds__(256) void k_pull_msgs(int d, const int *list, const u64 *count, const long long *ioff,
-                                                   Adj in, const unsigned *member, const int *wprefix,
-                                                   const float *msg, float *S, unsigned *mark, const Counters *c) {
+__global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *list, const u64 *count,
+                                                   const long long *ioff, Adj in, const unsigned *member,
+                                                   const int *wprefix, const float *msg, float *S, unsigned *mark,
+                                                   const Counters *c) {
+  __shared__ int2 pairs[256 / kWave][kPullChunk];
   if (c->abort) return;
   const int lane = lane_id();
   const int grp = lane / G, k0 = lane % G;
+  int2 *wp = pairs[threadIdx.x / kWave];
   const long long nA = static_cast<long long>(*count);
   const long long E = ioff[nA];
   const long long waves = num_waves();
   int C = 1;
-  while (C < kWave && static_cast<long long>(C) * waves < E) C <<= 1;
+  while (C < kPullChunk && static_cast<long long>(C) * waves < E) C <<= 1;
+  const int per_lane = C > kWave ? C / kWave : 1;  // arcs per lane
+  const int window = C / (kWave / G) > 0 ? C / (kWave / G) : 1;  // chunk positions per group
   const long long chunks = (E + C - 1) / C;
   const long long per = (chunks + waves - 1) / waves;
   const long long c0 = global_wave() * per;
@@ -557,55 +566,75 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, const int *list, const
     const long long elast = e0 + C - 1 < E - 1 ? e0 + C - 1 : E - 1;
     ja = ja < 0 ? wave_last_le(ioff, 0, nA + 1, e0) : owner_from(ioff, ja, nA + 1, e0);
     const long long jb = C == 1 ? ja : owner_from(ioff, ja, nA + 1, elast);
-    const long long e = e0 + lane;
-    const bool active = e <= elast;
-    int r = static_cast<int>(ja);
+    // this lane's arcs: chunk positions lane * per_lane + a
+    long long e[kPullArcs];
+    int r[kPullArcs];
+#pragma unroll
+    for (int a = 0; a < kPullArcs; ++a) {
+      e[a] = e0 + static_cast<long long>(lane) * per_lane + a;
+      r[a] = static_cast<int>(ja);
+    }
     if (jb > ja) {
       if (jb - ja < kWave) {
+        // the window's offsets, one per lane; every lane takes part in the shuffles
         const long long mine = ja + lane <= jb ? ioff[ja + lane] : (1LL << 62);
-        int cnt_le = 0;
-        for (int t = 0; t <= static_cast<int>(jb - ja); ++t) cnt_le += __shfl(mine, t) <= e ? 1 : 0;
-        r = static_cast<int>(ja) + cnt_le - 1;
-      } else if (active) {
-        r = static_cast<int>(upper_bound(ioff, ja, jb + 1, e) - 1);
+        int cnt[kPullArcs] = {};
+        for (int t = 0; t <= static_cast<int>(jb - ja); ++t) {
+          const long long o = __shfl(mine, t);
+#pragma unroll
+          for (int a = 0; a < kPullArcs; ++a) cnt[a] += o <= e[a] ? 1 : 0;
+        }
+#pragma unroll
+        for (int a = 0; a < kPullArcs; ++a) r[a] = static_cast<int>(ja) + cnt[a] - 1;
+      } else {
+#pragma unroll
+        for (int a = 0; a < kPullArcs; ++a)
+          if (a < per_lane && e[a] <= elast) r[a] = static_cast<int>(upper_bound(ioff, ja, jb + 1, e[a]) - 1);
       }
     }
-    int v = -1, j = -1;
-    if (active) {
-      v = list != nullptr ? list[r] : r;
-      const int u = in.col[in.off[v] + (e - ioff[r])];
-      const unsigned word = member[u >> 5];
-      const int below = wprefix[u >> 5];  // issued with the member word: no dependent round trip
-      const unsigned bit = 1u << (u & 31);
-      if (word & bit) j = below + __popc(word & (bit - 1u));
-    }
-    const u64 keep = __ballot(j >= 0);
-    u64 rem = G == kWave ? keep : (keep >> (grp * G)) & ((1ull << (G % kWave)) - 1);
-    int maxc = __popcll(rem);
+    int v[kPullArcs], u[kPullArcs];
 #pragma unroll
-    for (int o = G; o < kWave; o <<= 1) {
-      const int y = __shfl_xor(maxc, o);
-      maxc = y > maxc ? y : maxc;
+    for (int a = 0; a < kPullArcs; ++a) {
+      const bool active = a < per_lane && e[a] <= elast;
+      v[a] = active ? (list != nullptr ? list[r[a]] : r[a]) : -1;
     }
+#pragma unroll
+    for (int a = 0; a < kPullArcs; ++a)
+      u[a] = v[a] >= 0 ? __builtin_nontemporal_load(in.col + in.off[v[a]] + (e[a] - ioff[r[a]])) : -1;
+#pragma unroll
+    for (int a = 0; a < kPullArcs; ++a) {
+      int j = -1;
+      if (u[a] >= 0) {
+        const unsigned word = member[u[a] >> 5];
+        const int below = wprefix[u[a] >> 5];  // issued with the member word
+        const unsigned bit = 1u << (u[a] & 31);
+        if (word & bit) j = below + __popc(word & (bit - 1u));
+      }
+      if (a < per_lane) wp[lane * per_lane + a] = make_int2(v[a], j);
+    }
+    // the pairs are read back by other lanes of this wave only
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     int cur = -1;
     float acc[NC];
 #pragma unroll
     for (int q = 0; q < NC; ++q) acc[q] = 0.0f;
-    for (int b = 0; b < maxc; b += U) {  // trip count is the same for the whole wave
+    const int base = grp * window;
+    for (int t0 = 0; t0 < window; t0 += U) {  // trip count is the same for the whole wave
       int vv[U], jj[U];
 #pragma unroll
       for (int t = 0; t < U; ++t) {
-        const bool ok = rem != 0;
-        const int src = ok ? grp * G + __ffsll(static_cast<long long>(rem)) - 1 : lane;
-        if (ok) rem &= rem - 1;
-        vv[t] = __shfl(v, src);
-        jj[t] = __shfl(j, src);
-        if (!ok) jj[t] = -1;
+        const int pos = t0 + t;
+        int2 pr = make_int2(-1, -1);
+        if (pos < window && base + pos < C) pr = wp[base + pos];
+        vv[t] = pr.x;
+        jj[t] = pr.y;
       }
       float row[U][NC];
 #pragma unroll
       for (int t = 0; t < U; ++t) {
-        const float *mj = msg + static_cast<long long>(jj[t]) * d;
+        const float *mj = msg + static_cast<long long>(jj[t]) * ld;
 #pragma unroll
         for (int q = 0; q < NC; ++q) {
           const int k = k0 + q * G;
@@ -641,6 +670,10 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, const int *list, const
       }
       if (mark != nullptr && k0 == 0) mark_only(mark, cur);
     }
+    // the next chunk overwrites the pairs only after every lane has read them
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 }
 
@@ -730,19 +763,19 @@ void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, 
 
 long long compact_scratch_words(long long n) { return 2LL * compact_blocks(n) * kVals + 1; }
 
-void launch_delta0(hipStream_t s, long long n, int agg, int d0, const int *list, const u64 *count,
+void launch_delta0(hipStream_t s, long long n, int agg, int d0, int ld, const int *list, const u64 *count,
                    const ripple_op *ops, const float *feat, const int *fop, float *X, const int *out_len,
                    const int *ddeg, float *delta, const Counters *c) {
-  hipLaunchKernelGGL(k_delta0, dim3(blocks_for(n * kWave, 256, 2048)), dim3(256), 0, s, agg, d0, list, count,
+  hipLaunchKernelGGL(k_delta0, dim3(blocks_for(n * kWave, 256, 2048)), dim3(256), 0, s, agg, d0, ld, list, count,
                      ops, feat, fop, X, out_len, ddeg, delta, c);
 }
 
-void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *doff,
+void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
                     const int *del_dst, const u64 *pushed, const Counters *c, bool push) {
   const int blocks = 2048;
 #define RP_SCATTER(GV, NCV, P)                                                                                     \
-  hipLaunchKernelGGL((k_scatter<GV, NCV, P>), dim3(blocks), dim3(256), 0, s, d, list, count, doff, delta, out, S, \
+  hipLaunchKernelGGL((k_scatter<GV, NCV, P>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, doff, delta, out, S, \
                      bm_out, bm_x, ins_dst, del_dst, pushed, c)
   if (!push) RP_SCATTER(64, 1, false);
   else if (d <= 16) RP_SCATTER(16, 1, true);
@@ -755,17 +788,17 @@ void launch_scatter(hipStream_t s, long long n, int d, const int *list, const u6
 #undef RP_SCATTER
 }
 
-void launch_pull_msgs(hipStream_t s, long long n, int d, const int *list, const u64 *count, const long long *ioff,
-                      Adj in, const unsigned *member, const int *wprefix, const float *msg, float *S,
-                      unsigned *mark, const Counters *c) {
+void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count,
+                      const long long *ioff, Adj in, const unsigned *member, const int *wprefix, const float *msg,
+                      float *S, unsigned *mark, const Counters *c) {
   const int blocks = 2048;
-#define RP_PULLM(GV, NCV, UV)                                                                                      \
-  hipLaunchKernelGGL((k_pull_msgs<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, list, count, ioff, in, member, \
-                     wprefix, msg, S, mark, c)
-  if (d <= 16) RP_PULLM(16, 1, 4);
-  else if (d <= 32) RP_PULLM(16, 2, 4);
-  else if (d <= 48) RP_PULLM(16, 3, 4);
-  else if (d <= 64) RP_PULLM(16, 4, 4);
+#define RP_PULLM(GV, NCV, UV)                                                                                    \
+  hipLaunchKernelGGL((k_pull_msgs<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, ioff, in, \
+                     member, wprefix, msg, S, mark, c)
+  if (d <= 16) RP_PULLM(16, 1, 8);
+  else if (d <= 32) RP_PULLM(16, 2, 8);
+  else if (d <= 48) RP_PULLM(16, 3, 8);
+  else if (d <= 64) RP_PULLM(16, 4, 8);
   else if (d <= 128) RP_PULLM(64, 2, 8);
   else if (d <= 256) RP_PULLM(64, 4, 8);
   else if (d <= 512) RP_PULLM(64, 8, 4);

@@ -116,7 +116,7 @@ __device__ inline void epilogue(const GemmArgs &a, long long m, int v, int col, 
       cn = sv;
       co = 1.0f / sqrtf(static_cast<float>(a.out_len[v] - a.ddeg[v]) + 1.0f);
     }
-    a.delta[m * N + col] = cn * y - co * (*hp);
+    a.delta[m * a.dld + col] = cn * y - co * (*hp);
   }
   *hp = y;
 }
@@ -431,7 +431,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
       const long long idx = static_cast<long long>(v) * N + col;
       if (a.delta != nullptr) {
         const float cn = AGG == kGcn ? e_sv[i] : 1.f;
-        a.delta[(m0 + ml) * N + col] = cn * y - e_co[i] * e_old[i];
+        a.delta[(m0 + ml) * a.dld + col] = cn * y - e_co[i] * e_old[i];
       }
       a.H[idx] = y;
     }

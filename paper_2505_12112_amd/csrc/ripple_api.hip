@@ -443,6 +443,7 @@ rp::GemmArgs gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 *c
   g.relu = c->relu[l - 1];
   g.H = c->H[l];
   g.delta = delta;
+  g.dld = rp::row_ld(c->dims[l]);
   g.agg = c->agg;
   g.abort = abort;
   return g;
@@ -472,6 +473,7 @@ rp::GemmArgs p_gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 
   g.relu = 0;
   g.H = c->P[l];
   g.delta = msg;
+  g.dld = rp::row_ld(c->dims[l]);
   g.agg = c->agg;
   g.abort = abort;
   return g;
@@ -588,13 +590,15 @@ void issue_batch(ripple_ctx *c, int B) {
     co.keep = members ? c->keep[0] : nullptr;
     co.wprefix = members ? c->wprefix[0] : nullptr;
     rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
-    rp::launch_delta0(s, c->n, c->agg, c->dims[0], c->lists[0], &dc->count[0], c->d_ops, c->h_feat, c->fop,
-                      c->H[0], c->adj[0].len, c->ddeg, c->delta[0], dc);
+    rp::launch_delta0(s, c->n, c->agg, c->dims[0], rp::row_ld(c->dims[0]), c->lists[0], &dc->count[0], c->d_ops,
+                      c->h_feat, c->fop, c->H[0], c->adj[0].len, c->ddeg, c->delta[0], dc);
     add_launches(c, RIPPLE_PHASE_LAYER0, 3);
   }
   for (int l = 1; l <= c->L; ++l) {
     float *din = c->delta[(l - 1) & 1];
-    float *dout = l < c->L ? c->delta[l & 1] : nullptr;
+    // the next layer's messages: this layer's delta rows, unless it transforms first
+    // (its messages then come from its own P rows)
+    float *dout = l < c->L && !c->tf[l + 1] ? c->delta[l & 1] : nullptr;
     const float *msg = din;
     if (c->tf[l]) {
       // transform-first layer: refresh P = W_neigh h for the dirty rows and form
@@ -606,6 +610,7 @@ void issue_batch(ripple_ctx *c, int B) {
       msg = c->msg;
     }
     const int mode = layer_mode(c, l);
+    const int ld = rp::row_ld(c->sw[l]);  // message row stride
     if (mode == kPullLayer) c->last_pull |= 1 << l;
     if (mode == kDenseLayer) c->last_dense |= 1 << l;
     const unsigned *member = c->keep[(l - 1) & 1];
@@ -615,22 +620,23 @@ void issue_batch(ripple_ctx *c, int B) {
       // in-arc prefix, pull over every in-arc and mark the sinks that received a
       // message
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
-      rp::launch_scatter(s, c->n, c->sw[l], c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out, c->S[l],
-                         c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->zero, dc, false);
+      rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out,
+                         c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->zero, dc, false);
       rp::CompactOut all{};
       all.full_n = c->n;
       all.count = &dc->count_all;
       all.in_deg = c->adj[1].len;
       all.ioff = c->ioff;
       rp::launch_compact(s, c->n, nullptr, nullptr, compact_scratch(c, dc), all);
-      rp::launch_pull_msgs(s, c->n, c->sw[l], nullptr, &dc->count_all, c->ioff, in, member, wprefix, msg,
+      rp::launch_pull_msgs(s, c->n, c->sw[l], ld, nullptr, &dc->count_all, c->ioff, in, member, wprefix, msg,
                            c->S[l], c->bm_out, dc);
       add_launches(c, RIPPLE_PHASE_SCATTER, 3);
     } else {
       // push: marks + atomic adds; pull: marks only (the adds follow the compaction)
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
-      rp::launch_scatter(s, c->n, c->sw[l], c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out, c->S[l],
-                         c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc, mode == kPushLayer);
+      rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out,
+                         c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc,
+                         mode == kPushLayer);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     {
@@ -653,7 +659,7 @@ void issue_batch(ripple_ctx *c, int B) {
     }
     if (mode == kPullLayer) {
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
-      rp::launch_pull_msgs(s, c->n, c->sw[l], c->lists[l], &dc->count[l], c->ioff, in, member, wprefix, msg,
+      rp::launch_pull_msgs(s, c->n, c->sw[l], ld, c->lists[l], &dc->count[l], c->ioff, in, member, wprefix, msg,
                            c->S[l], nullptr, dc);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
@@ -699,7 +705,7 @@ void account_phases(ripple_ctx *c) {
     const double m = static_cast<double>(k.count[l]);
     const double K = c->K[l - 1], N = c->dims[l];
     c->ph_flops[RIPPLE_PHASE_GEMM] += 2.0 * m * K * N;
-    c->ph_bytes[RIPPLE_PHASE_GEMM] += 4.0 * m * K + 4.0 * N * K + 4.0 * m * N * (l < c->L ? 3.0 : 2.0);
+    c->ph_bytes[RIPPLE_PHASE_GEMM] += 4.0 * m * K + 4.0 * N * K + 4.0 * m * N * (l < c->L && !c->tf[l + 1] ? 3.0 : 2.0);
     c->ph_bytes[RIPPLE_PHASE_COMPACT] += 24.0 * words + 4.0 * m;
   }
   c->ev_log.clear();
@@ -999,14 +1005,14 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
     RP_TRY(dalloc_n(c, &c->doff[l], n + 1));
     if (l >= 1) RP_TRY(dalloc_n(c, &c->S[l], n * c->sw[l]));
   }
-  RP_TRY(dalloc_n(c, &c->delta[0], n * c->dmax_delta));
-  RP_TRY(dalloc_n(c, &c->delta[1], n * c->dmax_delta));
+  RP_TRY(dalloc_n(c, &c->delta[0], n * rp::row_ld(c->dmax_delta)));
+  RP_TRY(dalloc_n(c, &c->delta[1], n * rp::row_ld(c->dmax_delta)));
   RP_TRY(dalloc_n(c, &c->ioff, n + 1));
   for (int k = 0; k < 2; ++k) {
     RP_TRY(dalloc_n(c, &c->keep[k], (n + 31) / 32));
     RP_TRY(dalloc_n(c, &c->wprefix[k], (n + 31) / 32));
   }
-  if (msg_width > 0) RP_TRY(dalloc_n(c, &c->msg, n * msg_width));
+  if (msg_width > 0) RP_TRY(dalloc_n(c, &c->msg, n * rp::row_ld(msg_width)));
   for (int l = 1; l <= L; ++l)
     if (c->tf[l]) RP_TRY(dalloc_n(c, &c->P[l], n * c->dims[l]));
   RP_HIP(c, hipMemcpyAsync(c->H[0], x, static_cast<size_t>(n) * c->dims[0] * sizeof(float), hipMemcpyHostToDevice,
