@@ -49,6 +49,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-events", action="store_true",
                     help="no HIP events in the timed region (roofline then comes from the untimed pass)")
+    ap.add_argument("--scatter-mode", default="auto", choices=["auto", "push", "pull", "dense"],
+                    help="how every layer adds its messages (default: chosen per layer by the library)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-mebibyte device buffer into another (torch copy kernel), ten times: "
                          "the reference reading for the HBM byte counters")
@@ -66,8 +68,12 @@ def percentile(xs, q):
 
 
 def cpu_baseline(wl_name, seed, batches, bs):
-    """The oracle as it stands, on the first len(batches) batches of the stream:
-    apply the batch, recompute every layer in float64, derive the affected sets."""
+    """The oracle as it stands, in its float32 mode, on the first batches of the
+    stream: apply the batch (with the affected sets), then recompute every layer
+    over the whole graph. On graphs of more than 20M arcs one batch is timed and
+    only its first layer is recomputed; the other layers are scaled from it by
+    their share of the work (2 m d_{l-1} aggregation flops + 2 n K_l d_l GEMM
+    flops per layer), which keeps the sample to tens of seconds."""
     import numpy as np
     from oracle import ripple_oracle as O
     from paper_2505_12112_amd import synth
@@ -77,24 +83,37 @@ def cpu_baseline(wl_name, seed, batches, bs):
     except Exception:
         blas_threads = 1
     wl = synth.build_workload(wl_name, seed=seed)
-    st = O.OracleState(wl.n, wl.src, wl.dst, wl.x, O.OracleModel.from_weights(wl.weights),
-                       wl.spec.graph.undirected)
+    model = O.OracleModel.from_weights(wl.weights)
+    st = O.OracleState(wl.n, wl.src, wl.dst, wl.x, model, wl.spec.graph.undirected)
+    big = wl.src.size * (2 if wl.spec.graph.undirected else 1) > 20_000_000
+    dims = list(wl.weights.dims)
+    m = st.graph.num_arcs
+    gcn = wl.spec.model.agg == "gcn"
+    work = [2.0 * m * dims[l - 1] + 2.0 * wl.n * (1 if gcn else 2) * dims[l - 1] * dims[l]
+            for l in range(1, len(dims))]
     times = []
-    for b in batches:
+    for b in batches[:1] if big else batches:
         t0 = time.perf_counter()
         st.apply(b.ops, b.feat_rows)
-        st.embeddings()
-        times.append(time.perf_counter() - t0)
+        if big:
+            t1 = time.perf_counter()
+            O.layer(st.graph, st.x.astype(np.float32), O.OracleModel.from_weights(model, np.float32), 1)
+            t2 = time.perf_counter()
+            times.append((t1 - t0) + (t2 - t1) * sum(work) / work[0])
+        else:
+            st.embeddings(np.float32)
+            times.append(time.perf_counter() - t0)
     med = statistics.median(times)
+    how = ("apply + first-layer float32 recompute over all vertices, scaled by the layers' work "
+           f"({sum(work) / work[0]:.2f}x)" if big else "apply + full float32 layer-wise recompute")
     return {
         "value": bs / med,
         "unit": "updates/s",
         "cores": int(blas_threads),
         "kind": "oracle",
-        "sample": (f"first {len(batches)} batches of {bs} ops of the {wl_name} stream; per batch: apply, "
-                   f"full float64 layer-wise recompute (scipy sparse product, single thread; numpy BLAS, "
-                   f"{blas_threads} threads), affected sets; median {med:.3f} s/batch; "
-                   f"host has {len(os.sched_getaffinity(0))} cores available"),
+        "sample": (f"first {1 if big else len(batches)} batch(es) of {bs} ops of the {wl_name} stream; per batch: "
+                   f"{how} (scipy sparse product, single thread; numpy BLAS, {blas_threads} threads), affected "
+                   f"sets; median {med:.3f} s/batch; host has {len(os.sched_getaffinity(0))} cores available"),
     }
 
 
@@ -117,6 +136,7 @@ def main():
         return
     from paper_2505_12112_amd import synth
     from paper_2505_12112_amd.ripple import Ripple, BatchStats
+    from paper_2505_12112_amd.profiling import read_traffic
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
@@ -126,6 +146,7 @@ def main():
     log(f"[bench] generated {args.config}: n={wl.n} edges={wl.src.size} in {time.perf_counter() - t0:.1f}s")
     stream = torch.cuda.current_stream().cuda_stream
     lib = Ripple(wl.n, wl.src, wl.dst, undirected=spec.graph.undirected, device=0, stream=stream or None)
+    lib.set_scatter_mode(args.scatter_mode)
     t0 = time.perf_counter()
     lib.init_embeddings(wl.x, wl.weights)
     torch.cuda.synchronize()
@@ -150,6 +171,8 @@ def main():
     lat = []
     aff = np.zeros(L + 1)
     pushed = np.zeros(L + 1)
+    in_arcs = np.zeros(L + 1)
+    pull_layers = dense_layers = 0
     repacks = relocated = 0
     # the Python collector stays out of the timed region (a full collection with
     # torch loaded takes tens of milliseconds and is not the library's work)
@@ -163,6 +186,9 @@ def main():
         lat.append(time.perf_counter() - t1)
         aff += np.array(st.affected[:L + 1], dtype=np.float64)
         pushed += np.array(st.pushed_arcs[:L + 1], dtype=np.float64)
+        in_arcs += np.array(st.in_arcs[:L + 1], dtype=np.float64)
+        pull_layers |= st.pull_layers
+        dense_layers |= st.dense_layers
         repacks += st.repacks
         relocated += st.relocated_rows
     torch.cuda.synchronize()
@@ -187,21 +213,27 @@ def main():
     value = K * bs / sum(lat)
     ms_per_step = 1000.0 * sum(lat) / K
 
+    workload_key = f"{args.config}_b{bs}"
+
     def roof(name):
         p = ph[name]
         if p["launches"] == 0 or p["ms"] <= 0:
             return None
+        # HBM bytes per launch from the committed rocprofv3 counters (null when the
+        # kernels changed since they were taken)
+        traffic = read_traffic(workload_key, name)
+        common = {"traffic": traffic, "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
+                  "calibrated on a plain copy)", "launches": p["launches"],
+                  "avg_launch_us": 1000.0 * p["ms"] / p["launches"]}
         if name == "gemm":
             ach = p["flops"] / (p["ms"] * 1e-3) / 1e12
-            return {"kernel": "k_gemm_f32 (gather + fp32 MFMA + epilogue)", "bound": "mfma", "achieved": ach,
+            return {"kernel": "k_gemm (gather + fp32 MFMA + epilogue)", "bound": "mfma", "achieved": ach,
                     "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": ach / FP32_MFMA_PEAK_TFLOPS,
-                    "traffic": None, "launches": p["launches"], "avg_launch_us": 1000.0 * p["ms"] / p["launches"],
-                    "algorithmic_per_launch": p["flops"] / p["launches"]}
+                    "algorithmic_per_launch": p["flops"] / p["launches"], **common}
         ach = p["bytes"] / (p["ms"] * 1e-3) / 1e9
-        return {"kernel": "k_scatter (delta scatter-add + frontier marks)", "bound": "hbm", "achieved": ach,
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "traffic": None,
-                "launches": p["launches"], "avg_launch_us": 1000.0 * p["ms"] / p["launches"],
-                "algorithmic_per_launch": p["bytes"] / p["launches"]}
+        return {"kernel": "k_scatter / k_pull_msgs (message step)", "bound": "hbm", "achieved": ach,
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
+                "algorithmic_per_launch": p["bytes"] / p["launches"], **common}
 
     r_scatter, r_gemm = roof("scatter"), roof("gemm")
     dominant = "gemm" if ph["gemm"]["ms"] >= ph["scatter"]["ms"] else "scatter"
@@ -242,7 +274,10 @@ def main():
         "roofline_other": other,
         "cpu_baseline": cpu,
         "frontier_mean": {"affected": (aff / K).tolist(), "pushed_arcs": (pushed / K).tolist(),
+                          "in_arcs_of_affected": (in_arcs / K).tolist(),
                           "affected_frac": (aff / K / wl.n).tolist()},
+        "message_form": {"mode": args.scatter_mode, "pull_layers_seen": pull_layers,
+                         "dense_layers_seen": dense_layers},
         "adjacency": {"rows_moved": int(relocated), "relayouts": int(repacks)},
         "max_latency_ms": 1000 * max(lat),
         "max_latency_batch": int(np.argmax(lat)),

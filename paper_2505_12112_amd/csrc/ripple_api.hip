@@ -517,14 +517,16 @@ void add_launches(ripple_ctx *c, int phase, int k) {
   if (c->prof) c->ph_launch[phase] += k;
 }
 
-// How layer l adds its messages to S^l. Forced modes aside, estimate the bytes of
-// each form from the previous batch's counts for this layer (push on the first
-// batch). Push and pull both mark the sinks of every pushed arc with a bit atomic
-// (about 24 bytes of traffic each, as measured); push then moves every message as
-// a row of atomics (weighted 4x: atomics run at about a quarter of the read rate);
-// pull reads every in-arc of A^l, each message once and makes one atomic row
-// update per affected vertex; dense does the same over every in-arc of the graph
-// and needs no marks (a sink that receives a message is marked once).
+// How layer l adds its messages to S^l. Forced modes aside, the form with the
+// least estimated time for the previous batch's counts at this layer (push on the
+// first batch). The rates are fits to MI355X kernel traces of the three forms on
+// the dense_large and stress workloads:
+//   push   per pushed arc: a fixed 90 ps plus its row of fp32 atomics at 1.3 TB/s;
+//   pull   a bit atomic per pushed arc to mark its sink (38 ps), 35 ps per in-arc
+//          of A^l scanned, every message read once at 10 TB/s (the rows are mostly
+//          cache hits), one row of atomics per affected vertex at 1.3 TB/s;
+//   dense  25 ps per in-arc of the whole graph and 20 ps per vertex (the full
+//          listing) instead of the marks and A^l's in-arcs, reads and flushes as pull.
 enum LayerMode { kPushLayer = 0, kPullLayer = 1, kDenseLayer = 2 };
 
 int layer_mode(const ripple_ctx *c, int l) {
@@ -532,13 +534,14 @@ int layer_mode(const ripple_ctx *c, int l) {
   if (c->scatter_mode == RIPPLE_SCATTER_PULL) return kPullLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_DENSE) return kDenseLayer;
   if (!c->has_batch) return kPushLayer;
-  const double w = 4.0 * c->sw[l];
+  constexpr double kArc = 90e-12, kAtomicRate = 1.3e12, kMark = 38e-12, kPullScan = 35e-12;
+  constexpr double kDenseScan = 25e-12, kDenseVertex = 20e-12, kReadRate = 10e12;
+  const double w = 4.0 * c->sw[l];  // message row bytes
   const double pushed = static_cast<double>(c->last_pushed[l]);
-  const double mark = 24.0 * pushed;
-  const double push = mark + 4.0 * w * pushed;
-  const double settle = w * pushed + 4.0 * w * static_cast<double>(c->last_count[l]);
-  const double pull = mark + 12.0 * static_cast<double>(c->last_in[l]) + settle;
-  const double dense = 12.0 * static_cast<double>(c->arcs_now + c->n) + settle;
+  const double push = pushed * (kArc + w / kAtomicRate);
+  const double settle = pushed * w / kReadRate + static_cast<double>(c->last_count[l]) * w / kAtomicRate;
+  const double pull = pushed * kMark + static_cast<double>(c->last_in[l]) * kPullScan + settle;
+  const double dense = static_cast<double>(c->arcs_now) * kDenseScan + static_cast<double>(c->n) * kDenseVertex + settle;
   if (push <= pull && push <= dense) return kPushLayer;
   return pull <= dense ? kPullLayer : kDenseLayer;
 }

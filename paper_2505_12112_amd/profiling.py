@@ -1,0 +1,172 @@
+"""Summaries of rocprofv3 output for the committed profiles, and the HBM traffic
+figures bench.py reports beside its roofline.
+
+Two kinds of input, both CSV as rocprofv3 writes them with --output-format csv:
+
+* a kernel-trace statistics file (``*_kernel_stats.csv``): calls and durations
+  per kernel;
+* counter-collection files (``*_counter_collection.csv``) of two separate
+  ``--pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE`` runs, per dispatch, in KiB.
+
+The byte counters are scaled by what they read for a plain device-to-device copy
+of known size (``bench.py --copy-calibration MIB``): on gfx950 FETCH_SIZE reads
+half of the bytes such a copy moves and WRITE_SIZE all of them; the factors are
+measured, not assumed, and written into the summary.
+
+The traffic table carries a hash of the HIP sources it was measured on; bench.py
+reports the figures only while the sources still hash the same (a changed kernel
+makes them stale, and then the field is null).
+
+    python -m paper_2505_12112_amd.profiling stats TRACE_DIR TITLE COMMAND > profiles/x.txt
+    python -m paper_2505_12112_amd.profiling traffic OUT.md COPY_DIR WORKLOAD=FETCH_DIR,WRITE_DIR,BATCHES,CMD ...
+"""
+from __future__ import annotations
+
+import csv
+import glob
+import hashlib
+import os
+import re
+import sys
+from collections import defaultdict
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+TRAFFIC_MD = os.path.join(ROOT, "profiles", "hbm_traffic_counters.md")
+
+# kernels whose launches make up each rooflined phase of bench.py
+PHASE_KERNELS = {"scatter": ("k_scatter", "k_pull_msgs"), "gemm": ("k_gemm",)}
+
+
+def source_hash() -> str:
+    """sha256 over the HIP sources and headers the library is built from."""
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")) + glob.glob(os.path.join(HERE, "csrc", "*.h"))
+                   + [os.path.join(ROOT, "include", "ripple.h")])
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def kernel_name(full: str) -> str:
+    m = re.search(r"(k_\w+(<[^>]*>)?)", full)
+    return m.group(1) if m else full.split("(")[0][:48]
+
+
+def _one(dirpath: str, pattern: str) -> str:
+    hits = sorted(glob.glob(os.path.join(dirpath, "**", pattern), recursive=True))
+    if not hits:
+        raise FileNotFoundError(f"no {pattern} under {dirpath}")
+    return hits[0]
+
+
+def stats_table(trace_dir: str, title: str, command: str, top: int = 24) -> str:
+    rows = list(csv.DictReader(open(_one(trace_dir, "*kernel_stats.csv"))))
+    out = [f"# {title}", "", f"command: {command}", "",
+           " calls     avg_us     min_us     max_us   total_ms    pct  kernel"]
+    for r in rows[:top]:
+        out.append(f"{int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:10.2f} {int(r['MinNs']) / 1e3:10.2f} "
+                   f"{int(r['MaxNs']) / 1e3:10.2f} {float(r['TotalDurationNs']) / 1e6:10.3f} "
+                   f"{float(r['Percentage']):6.2f}  {kernel_name(r['Name'])}")
+    return "\n".join(out) + "\n"
+
+
+def _counter(dirpath: str, batches_only: bool = False):
+    """kernel -> list of (value KiB, duration ns) per dispatch; batches_only keeps
+    the dispatches from the first batch on (the first k_net_hash), leaving out the
+    bootstrap."""
+    rows = list(csv.DictReader(open(_one(dirpath, "*counter_collection.csv"))))
+    t0 = 0
+    if batches_only:
+        starts = [int(r["Start_Timestamp"]) for r in rows if kernel_name(r["Kernel_Name"]) == "k_net_hash"]
+        t0 = min(starts) if starts else 0
+    d = defaultdict(list)
+    for r in rows:
+        if int(r["Start_Timestamp"]) < t0:
+            continue
+        d[kernel_name(r["Kernel_Name"])].append(
+            (float(r["Counter_Value"]), int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
+    return d
+
+
+def _copy_factor(copy_dir: str, size_kib: float) -> float:
+    vals = [v for k, lst in _counter(copy_dir).items() if "copyBuffer" in k for v, _ in lst]
+    if not vals:
+        raise ValueError(f"no copy kernel in {copy_dir}")
+    return size_kib / (sum(vals) / len(vals))
+
+
+def traffic_md(copy_fetch: str, copy_write: str, copy_mib: int, workloads) -> str:
+    """workloads: list of (name, fetch_dir, write_dir, batches, command)."""
+    kib = copy_mib * 1024.0
+    ff, fw = _copy_factor(copy_fetch, kib), _copy_factor(copy_write, kib)
+    out = ["# HBM traffic per dispatch (rocprofv3 FETCH_SIZE and WRITE_SIZE, separate runs)", "",
+           f"source-hash: {source_hash()}", "",
+           f"Calibration: a {copy_mib} MiB device-to-device copy (bench.py --copy-calibration {copy_mib}) reads "
+           f"FETCH_SIZE x {ff:.4f} and WRITE_SIZE x {fw:.4f} of the bytes it moves; the calibrated columns "
+           f"below apply these factors.", ""]
+    for name, fdir, wdir, batches, cmd in workloads:
+        f, w = _counter(fdir, True), _counter(wdir, True)
+        out += [f"## {name}", "", f"command (one run per counter): {cmd.replace('COUNTER', 'FETCH_SIZE')} ; "
+                f"{cmd.replace('COUNTER', 'WRITE_SIZE')}", "",
+                f"Dispatches from the first of {batches} update batches on (the bootstrap is left out).", "",
+                "| kernel | dispatches | FETCH KiB/disp | WRITE KiB/disp | HBM MB/disp (calibrated) |",
+                "|---|---|---|---|---|"]
+        for k in sorted(f, key=lambda k: -sum(v for v, _ in f[k])):
+            fv = [v for v, _ in f[k]]
+            wv = [v for v, _ in w.get(k, [])]
+            fa = sum(fv) / len(fv)
+            wa = sum(wv) / len(wv) if wv else 0.0
+            out.append(f"| {k} | {len(fv)} | {fa:.1f} | {wa:.1f} | {(ff * fa + fw * wa) * 1024 / 1e6:.3f} |")
+        out.append("")
+        # per-launch traffic of each rooflined phase over the timed batches' kernels
+        for phase, prefixes in PHASE_KERNELS.items():
+            tot = n = 0.0
+            for k in f:
+                if k.startswith(prefixes):
+                    fv = [v for v, _ in f[k]]
+                    wv = [v for v, _ in w.get(k, [])]
+                    tot += ff * sum(fv) + (fw * sum(wv) if wv else 0.0)
+                    n += len(fv)
+            if n:
+                out.append(f"traffic {name} {phase} {tot * 1024 / n:.0f}")
+        out.append("")
+    return "\n".join(out) + "\n"
+
+
+def read_traffic(workload: str, phase: str):
+    """Calibrated HBM bytes per launch of `phase` on `workload` from the committed
+    table, or None when there is none or it predates the current sources."""
+    try:
+        text = open(TRAFFIC_MD).read()
+    except OSError:
+        return None
+    m = re.search(r"source-hash: (\w+)", text)
+    if not m or m.group(1) != source_hash():
+        return None
+    m = re.search(rf"^traffic {re.escape(workload)} {phase} (\d+)$", text, re.M)
+    return float(m.group(1)) if m else None
+
+
+def main(argv):
+    if argv[:1] == ["stats"]:
+        sys.stdout.write(stats_table(argv[1], argv[2], argv[3]))
+    elif argv[:1] == ["traffic"]:
+        out, copy_mib, cf, cw = argv[1], int(argv[2]), argv[3], argv[4]
+        wls = []
+        for spec in argv[5:]:
+            name, rest = spec.split("=", 1)
+            fdir, wdir, batches, cmd = rest.split(",", 3)
+            wls.append((name, fdir, wdir, int(batches), cmd))
+        with open(out, "w") as fh:
+            fh.write(traffic_md(cf, cw, copy_mib, wls))
+    else:
+        print(__doc__)
+        return 2
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main(sys.argv[1:]))

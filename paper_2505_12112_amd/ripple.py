@@ -277,7 +277,7 @@ class Ripple:
         return s, d
 
     def set_scatter_mode(self, mode: str):
-        """"auto" (default), "push" or "pull": how layers add their messages."""
+        """"auto" (default), "push", "pull" or "dense": how layers add their messages."""
         self._check(self._lib.ripple_set_scatter_mode(self._ctx, SCATTER[mode]))
 
     def device_bytes(self) -> int:
