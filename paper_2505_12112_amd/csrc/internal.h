@@ -43,6 +43,7 @@ struct Counters {
   u64 dest[kMaxL + 1];    // [l] = distinct sinks of those arcs
   u64 indeg[kMaxL + 1];   // [l] = sum of in-degrees over A^l (pull work), when computed
   u64 count_all;          // vertices listed by a full compaction (dense layers)
+  u64 bad_op;             // B - i for the first op i that failed the device-side check, else 0
   u64 zero;               // never written: an arc count of zero for kernels that only mark
 };
 
@@ -77,9 +78,12 @@ enum Agg { kSum = 0, kMean = 1, kGcn = 2 };
 // netting: after these, the net arcs are listed and every (arc, direction) item
 // knows its rank among the row's inserts (ins_rank) or deletes (del_rank); the
 // hash slot of every named edge holds +1 (net insert), -1 (net delete) or 0.
-// host_ops: the batch in pinned host memory; copied to ops (device) on the way.
-void launch_net_hash(hipStream_t s, const ripple_op *host_ops, ripple_op *ops, int B, int undirected, long long n,
-                     u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop, Counters *c);
+// src_ops: the batch in pinned host or device memory; copied to ops (device) on the
+// way and checked (ids and feature rows in range, known kind): a failing op sets
+// bad_op and abort, and is copied as a self-loop no-op.
+void launch_net_hash(hipStream_t s, const ripple_op *src_ops, ripple_op *ops, int B, long long num_feat_rows,
+                     int undirected, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop,
+                     Counters *c);
 void launch_net_decide(hipStream_t s, const ripple_op *ops, int B, int undirected, const int *ht_val,
                        int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src,
                        int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank, int *flist,

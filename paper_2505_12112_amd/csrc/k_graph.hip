@@ -88,11 +88,27 @@ __device__ inline void item_row(long long w, const int *src, const int *dst, int
 }
 
 // Reads the ops from pinned host memory and keeps a device copy for later kernels.
-__global__ void k_net_hash(const ripple_op *host_ops, ripple_op *ops, int B, int undirected, long long n,
-                           u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop, Counters *c) {
+__global__ void k_net_hash(const ripple_op *src_ops, ripple_op *ops, int B, long long num_feat_rows, int undirected,
+                           long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop,
+                           Counters *c) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= B) return;
-  const ripple_op op = host_ops[i];
+  ripple_op op = src_ops[i];
+  // the same checks as the host's: an op that fails them aborts the batch before
+  // anything is mutated, and is replaced by a harmless self-loop so that no kernel
+  // indexes with its fields
+  bool bad;
+  if (op.kind == RIPPLE_OP_INSERT || op.kind == RIPPLE_OP_DELETE)
+    bad = op.u < 0 || op.u >= n || op.v < 0 || op.v >= n;
+  else if (op.kind == RIPPLE_OP_FEATURE)
+    bad = op.u < 0 || op.u >= n || op.feat_row < 0 || op.feat_row >= num_feat_rows;
+  else
+    bad = true;
+  if (bad) {
+    atomicMax(&c->bad_op, static_cast<u64>(B - i));
+    c->abort = 1;
+    op = ripple_op{RIPPLE_OP_INSERT, 0, 0, -1};
+  }
   ops[i] = op;
   if (op.kind == RIPPLE_OP_FEATURE) {
     atomicMax(&fop[op.u], i);
@@ -362,11 +378,12 @@ inline int blocks_for(long long items, int threads, int cap = 4096) {
 
 }  // namespace
 
-void launch_net_hash(hipStream_t s, const ripple_op *host_ops, ripple_op *ops, int B, int undirected, long long n,
-                     u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop, Counters *c) {
+void launch_net_hash(hipStream_t s, const ripple_op *src_ops, ripple_op *ops, int B, long long num_feat_rows,
+                     int undirected, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop,
+                     Counters *c) {
   if (B <= 0) return;
-  hipLaunchKernelGGL(k_net_hash, dim3(blocks_for(B, 256, 1 << 20)), dim3(256), 0, s, host_ops, ops, B, undirected,
-                     n, ht_key, ht_val, mask, op_slot, fop, c);
+  hipLaunchKernelGGL(k_net_hash, dim3(blocks_for(B, 256, 1 << 20)), dim3(256), 0, s, src_ops, ops, B, num_feat_rows,
+                     undirected, n, ht_key, ht_val, mask, op_slot, fop, c);
 }
 
 void launch_net_decide(hipStream_t s, const ripple_op *ops, int B, int undirected, const int *ht_val, int *ht_net,

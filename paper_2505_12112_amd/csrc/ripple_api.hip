@@ -50,6 +50,7 @@ struct ripple_ctx {
   long long arena_slots = 0;  // 0 = default sizing
   long long arcs_loaded = 0;  // arcs of the snapshot
   long long arcs_now = 0;     // arcs stored now (snapshot + net inserts - net deletes)
+  std::vector<std::pair<uintptr_t, uintptr_t>> dev_ranges;  // device allocations seen by apply_updates_device
   long long bytes = 0;
   std::unordered_map<void *, size_t> allocs;
   std::string err;
@@ -552,7 +553,7 @@ rp::CompactScratch compact_scratch(ripple_ctx *c, rp::Counters *dc) {
 }
 
 // Issues one batch. Returns after queuing; the caller syncs.
-void issue_batch(ripple_ctx *c, int B) {
+void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op *src_ops, const float *src_feat) {
   hipStream_t s = c->stream;
   rp::Counters *dc = c->d_counters + c->parity;  // zeroed by the previous batch's clean-up
   rp::Counters *dnext = c->d_counters + (c->parity ^ 1);
@@ -563,8 +564,8 @@ void issue_batch(ripple_ctx *c, int B) {
   PhaseScope total(c, RIPPLE_PHASE_TOTAL);
   {
     PhaseScope ps(c, RIPPLE_PHASE_NET);
-    rp::launch_net_hash(s, c->h_ops, c->d_ops, B, c->undirected, c->n, c->ht_key, c->ht_val, c->ht_mask,
-                        c->op_slot, c->fop, dc);
+    rp::launch_net_hash(s, src_ops, c->d_ops, B, num_feat_rows, c->undirected, c->n, c->ht_key, c->ht_val,
+                        c->ht_mask, c->op_slot, c->fop, dc);
     rp::launch_net_decide(s, c->d_ops, B, c->undirected, c->ht_val, c->ht_net, c->op_slot, c->fop, out, in,
                           c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank, c->del_rank, c->flist, dc);
     add_launches(c, RIPPLE_PHASE_NET, 2);
@@ -594,7 +595,7 @@ void issue_batch(ripple_ctx *c, int B) {
     co.wprefix = members ? c->wprefix[0] : nullptr;
     rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
     rp::launch_delta0(s, c->n, c->agg, c->dims[0], rp::row_ld(c->dims[0]), c->lists[0], &dc->count[0], c->d_ops,
-                      c->h_feat, c->fop, c->H[0], c->adj[0].len, c->ddeg, c->delta[0], dc);
+                      src_feat, c->fop, c->H[0], c->adj[0].len, c->ddeg, c->delta[0], dc);
     add_launches(c, RIPPLE_PHASE_LAYER0, 3);
   }
   for (int l = 1; l <= c->L; ++l) {
@@ -1039,27 +1040,31 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   return RIPPLE_OK;
 }
 
-ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t num_ops, const float *feat_rows,
-                                   int64_t num_feat_rows, ripple_batch_stats *stats) {
-  RP_TRY(check_ctx(c));
-  if (!c->inited) return fail(c, RIPPLE_E_STATE, "ripple: ripple_init_embeddings has not run");
-  if (num_ops < 0 || num_feat_rows < 0) return fail(c, RIPPLE_E_INVALID, "ripple: negative count");
-  if (num_ops > (1LL << 26)) return fail(c, RIPPLE_E_INVALID, "ripple: batch larger than 2^26 ops");
-  if (num_ops > 0 && ops == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: ops is NULL");
-  if (num_feat_rows > 0 && feat_rows == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: feat_rows is NULL");
-  if (!validate_ops(c, ops, num_ops, num_feat_rows)) return RIPPLE_E_INVALID;
-  RP_TRY(ensure_batch_scratch(c, num_ops, num_feat_rows));
-  // the kernels read the batch straight from these pinned buffers (the previous
-  // call has synchronised, so nothing still reads them)
-  const int B = static_cast<int>(num_ops);
-  if (B > 0) std::memcpy(c->h_ops, ops, static_cast<size_t>(B) * sizeof(ripple_op));
-  if (num_feat_rows > 0)
-    std::memcpy(c->h_feat, feat_rows, static_cast<size_t>(num_feat_rows) * c->dims[0] * sizeof(float));
+namespace {
+
+// Runs one batch whose ops and feature rows the kernels read from src_ops /
+// src_feat (pinned host or device memory). The kernels check every op again; a
+// batch they reject is invalid, reported from caller_ops (the caller's device
+// copy), and nothing was mutated.
+ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op *src_ops,
+                        const float *src_feat, const ripple_op *caller_ops, ripple_batch_stats *stats) {
   long long repacks = 0;
   for (int attempt = 0;; ++attempt) {
-    issue_batch(c, B);
+    issue_batch(c, B, num_feat_rows, src_ops, src_feat);
     RP_HIP(c, hipGetLastError());
     RP_TRY(wait_stream(c));
+    if (c->h_counters->bad_op) {
+      // rejected on the device before anything was mutated: name the first bad op
+      c->ev_log.clear();
+      c->ev_used = 0;
+      const long long i = B - static_cast<long long>(c->h_counters->bad_op);
+      ripple_op o{};
+      RP_HIP(c, hipMemcpy(&o, caller_ops + i, sizeof(o), hipMemcpyDeviceToHost));
+      if (validate_ops(c, &o, 1, num_feat_rows)) c->err = "ripple: op 0: failed the device-side check";
+      const size_t at = c->err.find("op 0:");
+      if (at != std::string::npos) c->err.replace(at, 5, "op " + std::to_string(i) + ":");
+      return RIPPLE_E_INVALID;
+    }
     if (!c->h_counters->abort) break;
     // the spare arena cannot take this batch's row moves: nothing was mutated
     c->ev_log.clear();
@@ -1090,7 +1095,7 @@ ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t 
   }
   if (stats != nullptr) {
     std::memset(stats, 0, sizeof(*stats));
-    stats->num_ops = num_ops;
+    stats->num_ops = B;
     stats->edge_keys = static_cast<int64_t>(k.edge_keys);
     stats->noop_edge_ops = static_cast<int64_t>(k.noop_edge);
     stats->ins_arcs = static_cast<int64_t>(k.n_ins);
@@ -1110,6 +1115,70 @@ ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t 
     stats->dense_layers = c->last_dense;
   }
   return RIPPLE_OK;
+}
+
+// True if [p, p + bytes) lies inside one device allocation of the context's
+// device. Allocations already seen are remembered (the runtime query costs
+// microseconds, and callers reuse their buffers), so a repeat check is a lookup.
+// This refuses host pointers; it cannot tell a freed device range.
+bool device_range(ripple_ctx *c, const void *p, long long bytes) {
+  if (p == nullptr || bytes <= 0) return true;
+  const uintptr_t lo = reinterpret_cast<uintptr_t>(p), hi = lo + static_cast<uintptr_t>(bytes);
+  for (const auto &r : c->dev_ranges)
+    if (lo >= r.first && hi <= r.second) return true;
+  hipPointerAttribute_t at{};
+  if (hipPointerGetAttributes(&at, p) != hipSuccess || at.type != hipMemoryTypeDevice || at.device != c->device) {
+    (void)hipGetLastError();
+    return false;
+  }
+  void *base = nullptr;
+  size_t size = 0;
+  if (hipMemGetAddressRange(reinterpret_cast<hipDeviceptr_t *>(&base), &size, const_cast<void *>(p)) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  const uintptr_t b = reinterpret_cast<uintptr_t>(base);
+  if (hi > b + size) return false;
+  if (c->dev_ranges.size() >= 64) c->dev_ranges.erase(c->dev_ranges.begin());
+  c->dev_ranges.emplace_back(b, b + size);
+  return true;
+}
+
+ripple_status check_batch_args(ripple_ctx *c, const ripple_op *ops, int64_t num_ops, const float *feat_rows,
+                               int64_t num_feat_rows) {
+  RP_TRY(check_ctx(c));
+  if (!c->inited) return fail(c, RIPPLE_E_STATE, "ripple: ripple_init_embeddings has not run");
+  if (num_ops < 0 || num_feat_rows < 0) return fail(c, RIPPLE_E_INVALID, "ripple: negative count");
+  if (num_ops > (1LL << 26)) return fail(c, RIPPLE_E_INVALID, "ripple: batch larger than 2^26 ops");
+  if (num_ops > 0 && ops == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: ops is NULL");
+  if (num_feat_rows > 0 && feat_rows == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: feat_rows is NULL");
+  return RIPPLE_OK;
+}
+
+}  // namespace
+
+ripple_status ripple_apply_updates(ripple_ctx *c, const ripple_op *ops, int64_t num_ops, const float *feat_rows,
+                                   int64_t num_feat_rows, ripple_batch_stats *stats) {
+  RP_TRY(check_batch_args(c, ops, num_ops, feat_rows, num_feat_rows));
+  if (!validate_ops(c, ops, num_ops, num_feat_rows)) return RIPPLE_E_INVALID;
+  RP_TRY(ensure_batch_scratch(c, num_ops, num_feat_rows));
+  // the kernels read the batch straight from these pinned buffers (the previous
+  // call has synchronised, so nothing still reads them)
+  const int B = static_cast<int>(num_ops);
+  if (B > 0) std::memcpy(c->h_ops, ops, static_cast<size_t>(B) * sizeof(ripple_op));
+  if (num_feat_rows > 0)
+    std::memcpy(c->h_feat, feat_rows, static_cast<size_t>(num_feat_rows) * c->dims[0] * sizeof(float));
+  return run_batch(c, B, num_feat_rows, c->h_ops, c->h_feat, nullptr, stats);
+}
+
+ripple_status ripple_apply_updates_device(ripple_ctx *c, const ripple_op *ops, int64_t num_ops,
+                                          const float *feat_rows, int64_t num_feat_rows, ripple_batch_stats *stats) {
+  RP_TRY(check_batch_args(c, ops, num_ops, feat_rows, num_feat_rows));
+  if (!device_range(c, ops, num_ops * sizeof(ripple_op)) ||
+      !device_range(c, feat_rows, num_feat_rows * c->dims[0] * sizeof(float)))
+    return fail(c, RIPPLE_E_INVALID, "ripple: ops / feat_rows must be device memory of the context's device");
+  RP_TRY(ensure_batch_scratch(c, num_ops, num_feat_rows));
+  return run_batch(c, static_cast<int>(num_ops), num_feat_rows, ops, feat_rows, ops, stats);
 }
 
 ripple_status ripple_get_embeddings(ripple_ctx *c, int32_t layer, const int32_t *ids, int64_t count, float *out) {
@@ -1208,7 +1277,7 @@ ripple_status ripple_set_profiling(ripple_ctx *c, int32_t mask) {
   c->prof_mask = static_cast<unsigned>(mask) & ((1u << RIPPLE_NUM_PHASES) - 1u);
   c->prof = c->prof_mask != 0;
   // create the events now so that the first recorded batch does not pay for it
-  const size_t want = 2 * (4 + 3 * static_cast<size_t>(rp::kMaxL));
+  const size_t want = 2 * (4 + 6 * static_cast<size_t>(rp::kMaxL));  // every scope of a batch
   while (c->prof && c->ev_pool.size() < want) {
     hipEvent_t e;
     RP_HIP(c, hipEventCreate(&e));

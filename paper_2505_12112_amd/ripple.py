@@ -29,7 +29,7 @@ EXPORTED = [
     "ripple_load_graph", "ripple_init_embeddings", "ripple_apply_updates", "ripple_get_embeddings",
     "ripple_get_affected", "ripple_get_aggregates", "ripple_get_arcs", "ripple_device_bytes",
     "ripple_set_profiling", "ripple_get_phase_stats", "ripple_phase_name", "ripple_last_error",
-    "ripple_destroy", "ripple_set_scatter_mode",
+    "ripple_destroy", "ripple_set_scatter_mode", "ripple_apply_updates_device",
 ]
 SCATTER = {"auto": 0, "push": 1, "pull": 2, "dense": 3}
 
@@ -94,6 +94,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.ripple_load_graph.argtypes = [P(GraphDesc), P(vp)]
     lib.ripple_init_embeddings.argtypes = [vp, P(C.c_float), P(ModelDesc)]
     lib.ripple_apply_updates.argtypes = [vp, P(C.c_int32), C.c_int64, P(C.c_float), C.c_int64, P(BatchStats)]
+    lib.ripple_apply_updates_device.argtypes = [vp, vp, C.c_int64, vp, C.c_int64, P(BatchStats)]
     lib.ripple_get_embeddings.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_float)]
     lib.ripple_get_aggregates.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_float), P(C.c_int32)]
     lib.ripple_get_affected.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_int64)]
@@ -208,6 +209,20 @@ class Ripple:
         self._check(self._lib.ripple_apply_updates(
             self._ctx, _ptr(ops, C.c_int32), int(ops.shape[0]), _ptr(fr, C.c_float),
             0 if fr is None else int(fr.shape[0]), C.byref(st)))
+        return self._stats_dict(st)
+
+    def apply_updates_device(self, ops_ptr: int, num_ops: int, feat_ptr: int, num_feat_rows: int,
+                             stats: Optional[BatchStats] = None) -> Dict[str, object]:
+        """The batch already in device memory: ops_ptr -> int32 [num_ops, 4] and
+        feat_ptr -> float32 [num_feat_rows, d_0] on the context's device (raw
+        addresses, e.g. a torch tensor's data_ptr(); 0 for none)."""
+        st = BatchStats() if stats is None else stats
+        self._check(self._lib.ripple_apply_updates_device(
+            self._ctx, C.c_void_p(ops_ptr or None), int(num_ops), C.c_void_p(feat_ptr or None),
+            int(num_feat_rows), C.byref(st)))
+        return st if stats is not None else self._stats_dict(st)
+
+    def _stats_dict(self, st: BatchStats) -> Dict[str, object]:
         L = self.num_layers
         return {
             "num_ops": st.num_ops, "edge_keys": st.edge_keys, "noop_edge_ops": st.noop_edge_ops,

@@ -2,6 +2,8 @@
 seeded inputs and compare what they produce."""
 from __future__ import annotations
 
+import ctypes as C
+
 import numpy as np
 
 from oracle import ripple_oracle as O
@@ -11,11 +13,54 @@ from paper_2505_12112_amd.ripple import Ripple
 FP32_TOL = 1e-4   # max row-relative error for the fp32 path
 
 
+class DeviceCopy:
+    """A host array copied into device memory (hipMalloc + hipMemcpy) through the
+    HIP runtime the library itself runs on, so that tests need no other GPU
+    framework; freed on exit. ptr is 0 for None or an empty array."""
+
+    def __init__(self, arr):
+        self.arr = arr
+        self.ptr = 0
+
+    def __enter__(self):
+        if self.arr is not None and self.arr.nbytes:
+            hip = _hip()
+            p = C.c_void_p()
+            if hip.hipMalloc(C.byref(p), C.c_size_t(self.arr.nbytes)) != 0:
+                raise RuntimeError("hipMalloc failed")
+            self.ptr = p.value
+            if hip.hipMemcpy(C.c_void_p(self.ptr), self.arr.ctypes.data_as(C.c_void_p),
+                             C.c_size_t(self.arr.nbytes), 1) != 0:  # host to device
+                raise RuntimeError("hipMemcpy failed")
+        return self
+
+    def __exit__(self, *exc):
+        if self.ptr:
+            _hip().hipFree(C.c_void_p(self.ptr))
+            self.ptr = 0
+        return False
+
+
+_HIP = None
+
+
+def _hip():
+    global _HIP
+    if _HIP is None:
+        _HIP = C.CDLL("libamdhip64.so.7")  # the runtime libripple.so is linked against
+        _HIP.hipMalloc.argtypes = [C.POINTER(C.c_void_p), C.c_size_t]
+        _HIP.hipMemcpy.argtypes = [C.c_void_p, C.c_void_p, C.c_size_t, C.c_int]
+        _HIP.hipFree.argtypes = [C.c_void_p]
+    return _HIP
+
+
 class Pair:
-    def __init__(self, n, src, dst, x, weights, undirected=False, transform_first=-1, mode="auto", **lib_kw):
+    def __init__(self, n, src, dst, x, weights, undirected=False, transform_first=-1, mode="auto", inputs="host",
+                 **lib_kw):
         self.lib = Ripple(n, src, dst, undirected=undirected, **lib_kw)
         self.lib.init_embeddings(x, weights, transform_first=transform_first)
         self.lib.set_scatter_mode(mode)
+        self.inputs = inputs  # "host": ripple_apply_updates; "device": the batch staged in HBM first
         self.orc = O.OracleState(n, src, dst, x, O.OracleModel.from_weights(weights), undirected)
         self.L = len(weights.dims) - 1
         self.n = n
@@ -23,8 +68,17 @@ class Pair:
     def close(self):
         self.lib.close()
 
+    def apply(self, ops, feat_rows):
+        """The batch through the library, from host memory or staged in device memory."""
+        if self.inputs == "host":
+            return self.lib.apply_updates(ops, feat_rows)
+        o = np.ascontiguousarray(np.asarray(ops, np.int32).reshape(-1, 4))
+        f = None if feat_rows is None or len(feat_rows) == 0 else np.ascontiguousarray(feat_rows, np.float32)
+        with DeviceCopy(o) as do, DeviceCopy(f) as df:
+            return self.lib.apply_updates_device(do.ptr, o.shape[0], df.ptr, 0 if f is None else f.shape[0])
+
     def step(self, batch, check_sets=True, check_stats=True):
-        st = self.lib.apply_updates(batch.ops, batch.feat_rows)
+        st = self.apply(batch.ops, batch.feat_rows)
         net, sets = self.orc.apply(batch.ops, batch.feat_rows)
         if check_sets:
             for l in range(self.L + 1):

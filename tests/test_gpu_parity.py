@@ -42,12 +42,14 @@ def test_bootstrap_matches_full_recompute(agg, dims):
         p.close()
 
 
+@pytest.mark.parametrize("inputs", ["host", "device"])
 @pytest.mark.parametrize("mode", ["push", "pull", "dense"])
-def test_tiny_config_stream(mode):
-    """The tiny workload as specified: 10 batches of 45 inserts, 45 deletes, 10 features."""
-    _say("tiny config", mode)
+def test_tiny_config_stream(mode, inputs):
+    """The tiny workload as specified: 10 batches of 45 inserts, 45 deletes, 10
+    features, handed over from host memory or already resident in device memory."""
+    _say("tiny config", mode, inputs)
     wl = synth.build_workload("tiny")
-    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, mode=mode)
+    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, mode=mode, inputs=inputs)
     try:
         for b in range(10):
             st, net, sets = p.step(wl.stream.next_batch(100))
@@ -193,6 +195,39 @@ def test_invalid_batch_changes_nothing():
         p.check_arcs()
         p.step(random_valid_batch(rng, p.orc, 20, dims[0]))
         p.check_embeddings()
+    finally:
+        p.close()
+
+
+def test_device_resident_batch_is_checked_on_the_device():
+    """A batch in device memory with a bad op is rejected by the kernels before
+    anything changes, naming the first bad op; a host pointer is refused; the next
+    valid batch goes through."""
+    import torch
+    rng = np.random.default_rng(18)
+    dims = (6, 8, 3)
+    src, dst, x, w = _small(rng, 100, 300, dims, "mean")
+    p = Pair(100, src, dst, x, w, inputs="device")
+    try:
+        p.step(random_valid_batch(rng, p.orc, 20, dims[0]))
+        before = [p.lib.get_embeddings(l) for l in range(3)]
+        good = random_valid_batch(rng, p.orc, 12, dims[0])
+        for bad_op in ([1, 0, 100, -1], [3, 1, -1, 1000], [9, 1, 2, -1], [2, -1, 2, -1]):
+            ops = np.array(good.ops, np.int32).copy()
+            ops[7] = bad_op
+            with pytest.raises(RippleError) as e:
+                p.apply(ops, good.feat_rows if len(good.feat_rows) else np.zeros((1, dims[0]), np.float32))
+            assert e.value.status == E_INVALID and "op 7:" in str(e.value), str(e.value)
+        with pytest.raises(RippleError) as e:  # host memory is not device memory
+            host = np.array(good.ops, np.int32)
+            p.lib.apply_updates_device(host.ctypes.data, host.shape[0], 0, 0)
+        assert e.value.status == E_INVALID
+        for l in range(3):
+            np.testing.assert_array_equal(p.lib.get_embeddings(l), before[l])
+        p.check_arcs()
+        p.step(good)
+        p.check_embeddings()
+        p.check_arcs()
     finally:
         p.close()
 
