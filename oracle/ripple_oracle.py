@@ -38,6 +38,11 @@ design notes of the repository):
   mean (0 when the in-degree is 0);
 * GCN with symmetric normalisation: implicit self-loop,
   alpha_uv = 1/sqrt((d_out(u)+1)(d_in(v)+1));
+* GraphConv with sum or mean (the evaluation's GC-S and GC-M workloads, Sec.
+  VII-A): h = sigma(W agg + b), no self term and no self-loop, so a vertex whose
+  own embedding changed is not affected at the next hop unless a neighbour is;
+* GINConv with sum (GI-S): h = sigma(MLP((1 + eps) h_self + sum)), the MLP a
+  linear layer, a ReLU and a second linear layer;
 * ReLU after every layer but the last.
 
 Arithmetic is float64 by default; the aggregation uses a scipy sparse product
@@ -61,14 +66,30 @@ OP_FEATURE = 3
 # model
 # ----------------------------------------------------------------------------
 
+# GraphSAGE (self weight + neighbour weight): "sum", "mean"; GCN: "gcn";
+# GraphConv (neighbour weight only, no self term): "gc_sum", "gc_mean";
+# GINConv: "gin" (sum, (1 + eps) self term, two-layer MLP).
+AGGREGATORS = ("sum", "mean", "gcn", "gc_sum", "gc_mean", "gin")
+
+
+def has_self_term(agg: str) -> bool:
+    """Whether a vertex's own previous embedding enters its update."""
+    return agg not in ("gc_sum", "gc_mean")
+
+
 @dataclasses.dataclass
 class OracleModel:
-    """agg in {"sum", "mean", "gcn"}; weights are [d_l, d_{l-1}] (y = W x)."""
+    """Weights are [out, in] (y = W x). SAGE: w_self, w_neigh [d_l, d_{l-1}];
+    GCN / GraphConv: w_neigh only. GIN: w_neigh [hidden, d_{l-1}] and bias [hidden]
+    are the MLP's first layer, w_out [d_l, hidden] and b_out [d_l] its second."""
     agg: str
     w_self: List[Optional[np.ndarray]]
     w_neigh: List[np.ndarray]
     bias: List[np.ndarray]
     relu: List[bool]
+    w_out: List[np.ndarray] = dataclasses.field(default_factory=list)
+    b_out: List[np.ndarray] = dataclasses.field(default_factory=list)
+    gin_eps: float = 0.0
 
     @property
     def num_layers(self) -> int:
@@ -76,13 +97,17 @@ class OracleModel:
 
     @staticmethod
     def from_weights(mw, dtype=np.float64) -> "OracleModel":
-        """Accepts any object with agg / w_self / w_neigh / bias / relu attributes."""
+        """Accepts any object with agg / w_self / w_neigh / bias / relu attributes
+        (and w_out / b_out / gin_eps for GIN)."""
         return OracleModel(
             mw.agg,
             [None if w is None else np.asarray(w, dtype) for w in mw.w_self],
             [np.asarray(w, dtype) for w in mw.w_neigh],
             [np.asarray(b, dtype) for b in mw.bias],
-            list(mw.relu))
+            list(mw.relu),
+            [np.asarray(w, dtype) for w in (getattr(mw, "w_out", None) or [])],
+            [np.asarray(b, dtype) for b in (getattr(mw, "b_out", None) or [])],
+            float(getattr(mw, "gin_eps", 0.0)))
 
 
 # ----------------------------------------------------------------------------
@@ -246,9 +271,9 @@ def aggregate(graph: OracleGraph, h: np.ndarray, agg: str) -> np.ndarray:
     """x_v = Aggregate({h_u : u in N_in(v)}) for every v (table of linear
     aggregators). GCN's weighted sum includes v itself (implicit self-loop)."""
     h = np.asarray(h)
-    if agg == "sum":
+    if agg in ("sum", "gc_sum", "gin"):
         return graph.in_adjacency(dtype=h.dtype) @ h
-    if agg == "mean":
+    if agg in ("mean", "gc_mean"):
         s = graph.in_adjacency(dtype=h.dtype) @ h
         deg = graph.in_degree()
         out = np.zeros_like(s)
@@ -266,17 +291,25 @@ def aggregate(graph: OracleGraph, h: np.ndarray, agg: str) -> np.ndarray:
     raise ValueError(agg)
 
 
-def layer(graph: OracleGraph, h_prev: np.ndarray, model: OracleModel, l: int) -> np.ndarray:
-    """One layer l (1-based): Update^l then sigma (Eq. (2))."""
-    agg = aggregate(graph, h_prev, model.agg)
+def update(model: OracleModel, l: int, h_self: np.ndarray, agg: np.ndarray) -> np.ndarray:
+    """Update^l then sigma (Eq. (2)) for rows with own embedding h_self and
+    aggregate agg."""
     wn, b = model.w_neigh[l - 1], model.bias[l - 1]
-    if model.agg == "gcn":
+    if model.agg in ("gcn", "gc_sum", "gc_mean"):
         out = agg @ wn.T + b
+    elif model.agg == "gin":
+        hidden = np.maximum(((1.0 + model.gin_eps) * h_self + agg) @ wn.T + b, 0.0)
+        out = hidden @ model.w_out[l - 1].T + model.b_out[l - 1]
     else:
-        out = h_prev @ model.w_self[l - 1].T + agg @ wn.T + b
+        out = h_self @ model.w_self[l - 1].T + agg @ wn.T + b
     if model.relu[l - 1]:
         out = np.maximum(out, 0.0)
     return out
+
+
+def layer(graph: OracleGraph, h_prev: np.ndarray, model: OracleModel, l: int) -> np.ndarray:
+    """One layer l (1-based) for every vertex (Eq. (1)-(2))."""
+    return update(model, l, h_prev, aggregate(graph, h_prev, model.agg))
 
 
 def full_recompute(graph: OracleGraph, x: np.ndarray, model: OracleModel,
@@ -302,13 +335,16 @@ def affected_sets(graph_post: OracleGraph, net: NetEffect, agg: str,
     vertex whose out-degree changed (its normalisation scales all its outgoing
     contributions and its own self-loop). A^l holds D^l's post-batch
     out-neighbours, every sink of a net-changed arc (its neighbourhood changed),
-    and D^l itself (its own previous embedding enters its update)."""
+    and, for models with a self term, D^l itself (its own previous embedding
+    enters its update; GraphConv has none)."""
     sets = [np.unique(net.features)]
     for _ in range(num_layers):
         d = sets[-1]
         if agg == "gcn":
             d = np.union1d(d, net.out_deg_changed)
-        a = np.union1d(np.union1d(graph_post.out_neighbours(d), net.heads), d)
+        a = np.union1d(graph_post.out_neighbours(d), net.heads)
+        if has_self_term(agg):
+            a = np.union1d(a, d)
         sets.append(a.astype(np.int64))
     return sets
 
@@ -338,6 +374,7 @@ def sampled_embeddings(graph: OracleGraph, x: np.ndarray, model: OracleModel,
         idx = start + np.arange(int(cnt.sum()))
         return row_of, s_sorted[idx]
 
+    m = model if dtype == np.float64 else OracleModel.from_weights(model, dtype)
     need = [None] * (L + 1)
     need[L] = verts
     for l in range(L, 0, -1):
@@ -350,22 +387,15 @@ def sampled_embeddings(graph: OracleGraph, x: np.ndarray, model: OracleModel,
         col = np.searchsorted(prev, us)
         if model.agg == "gcn":
             w = 1.0 / np.sqrt((dout[us] + 1.0) * (din[rows][row_of] + 1.0))
-        elif model.agg == "mean":
+        elif model.agg in ("mean", "gc_mean"):
             w = 1.0 / din[rows][row_of]
         else:
             w = np.ones(us.size, dtype)
         agg = sp.csr_matrix((w, (row_of, col)), shape=(rows.size, prev.size)) @ h
         self_rows = h[np.searchsorted(prev, rows)]
-        wn = np.asarray(model.w_neigh[l - 1], dtype)
-        b = np.asarray(model.bias[l - 1], dtype)
         if model.agg == "gcn":
-            a_self = 1.0 / np.sqrt((dout[rows] + 1.0) * (din[rows] + 1.0))
-            out = (agg + a_self[:, None] * self_rows) @ wn.T + b
-        else:
-            out = self_rows @ np.asarray(model.w_self[l - 1], dtype).T + agg @ wn.T + b
-        if model.relu[l - 1]:
-            out = np.maximum(out, 0.0)
-        h = out
+            agg = agg + (1.0 / np.sqrt((dout[rows] + 1.0) * (din[rows] + 1.0)))[:, None] * self_rows
+        h = update(m, l, self_rows, agg)
     return verts, h
 
 

@@ -41,6 +41,9 @@ OP_FEATURE = 3
 AGG_SUM = "sum"
 AGG_MEAN = "mean"
 AGG_GCN = "gcn"
+AGG_GC_SUM = "gc_sum"    # GraphConv, sum aggregator (no self term)
+AGG_GC_MEAN = "gc_mean"  # GraphConv, mean aggregator (no self term)
+AGG_GIN = "gin"          # GINConv, sum aggregator, two-layer MLP
 
 
 @dataclasses.dataclass(frozen=True)
@@ -56,8 +59,9 @@ class GraphSpec:
 
 @dataclasses.dataclass(frozen=True)
 class ModelSpec:
-    agg: str                  # "sum" | "mean" | "gcn"
+    agg: str                  # "sum" | "mean" | "gcn" | "gc_sum" | "gc_mean" | "gin"
     dims: Tuple[int, ...]     # d_0 .. d_L
+    gin_eps: float = 0.0      # GIN: weight 1 + eps of the own embedding
 
 
 @dataclasses.dataclass(frozen=True)
@@ -306,10 +310,14 @@ def features(n: int, d: int, rng: np.random.Generator) -> np.ndarray:
 class ModelWeights:
     agg: str
     dims: Tuple[int, ...]
-    w_self: List[Optional[np.ndarray]]   # [d_l, d_{l-1}] float32, None for GCN
-    w_neigh: List[np.ndarray]            # [d_l, d_{l-1}] float32 (GCN: the single W)
-    bias: List[np.ndarray]               # [d_l] float32
+    w_self: List[Optional[np.ndarray]]   # [d_l, d_{l-1}] float32, None for GCN / GraphConv / GIN
+    w_neigh: List[np.ndarray]            # [d_l, d_{l-1}] float32 (GCN, GraphConv: the single W;
+                                         # GIN: the MLP's first layer, [d_l, d_{l-1}])
+    bias: List[np.ndarray]               # [d_l] float32 (GIN: the MLP's first bias)
     relu: List[bool]                     # activation after each layer
+    w_out: List[np.ndarray] = dataclasses.field(default_factory=list)  # GIN: MLP second layer [d_l, d_l]
+    b_out: List[np.ndarray] = dataclasses.field(default_factory=list)  # GIN: its bias [d_l]
+    gin_eps: float = 0.0
 
     @property
     def num_layers(self) -> int:
@@ -326,20 +334,26 @@ def model_weights(spec: ModelSpec, rng: np.random.Generator, bias_std: float = 0
     """Glorot-uniform weights (gain 1), drawn separately for the self and neighbour
     matrices; ReLU after every layer but the last; bias zero unless bias_std > 0."""
     L = len(spec.dims) - 1
-    ws, wn, bs, act = [], [], [], []
+    ws, wn, bs, act, wo, bo = [], [], [], [], [], []
+
+    def bias(d):
+        if bias_std > 0:
+            return (rng.standard_normal(d) * bias_std).astype(np.float32)
+        return np.zeros(d, np.float32)
+
     for l in range(1, L + 1):
         din, dout = spec.dims[l - 1], spec.dims[l]
-        if spec.agg == AGG_GCN:
+        if spec.agg in (AGG_GCN, AGG_GC_SUM, AGG_GC_MEAN, AGG_GIN):
             ws.append(None)
         else:
             ws.append(glorot(rng, dout, din))
         wn.append(glorot(rng, dout, din))
-        if bias_std > 0:
-            bs.append((rng.standard_normal(dout) * bias_std).astype(np.float32))
-        else:
-            bs.append(np.zeros(dout, np.float32))
+        bs.append(bias(dout))
+        if spec.agg == AGG_GIN:  # the MLP's second layer (hidden width d_l)
+            wo.append(glorot(rng, dout, dout))
+            bo.append(bias(dout))
         act.append(l < L or last_relu)
-    return ModelWeights(spec.agg, tuple(spec.dims), ws, wn, bs, act)
+    return ModelWeights(spec.agg, tuple(spec.dims), ws, wn, bs, act, wo, bo, spec.gin_eps)
 
 
 # ----------------------------------------------------------------------------

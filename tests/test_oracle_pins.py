@@ -15,24 +15,30 @@ from paper_2505_12112_amd import synth
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
-def _model(agg, w_self, w_neigh, bias, relu):
+def _model(agg, w_self, w_neigh, bias, relu, w_out=(), b_out=(), gin_eps=0.0):
     return O.OracleModel(
         agg,
         [None if w is None else np.array(w, np.float64) for w in w_self],
         [np.array(w, np.float64) for w in w_neigh],
         [np.array(b, np.float64) for b in bias],
-        list(relu))
+        list(relu),
+        [np.array(w, np.float64) for w in w_out],
+        [np.array(b, np.float64) for b in b_out],
+        float(gin_eps))
 
 
-def _random_model(rng, agg, dims, relu_all=False, relu_none=False):
-    ws, wn, bs, act = [], [], [], []
+def _random_model(rng, agg, dims, relu_all=False, relu_none=False, gin_eps=0.3):
+    ws, wn, bs, act, wo, bo = [], [], [], [], [], []
     L = len(dims) - 1
     for l in range(1, L + 1):
-        ws.append(None if agg == "gcn" else rng.standard_normal((dims[l], dims[l - 1])))
+        ws.append(rng.standard_normal((dims[l], dims[l - 1])) if agg in ("sum", "mean") else None)
         wn.append(rng.standard_normal((dims[l], dims[l - 1])))
         bs.append(rng.standard_normal(dims[l]) * 0.1)
+        if agg == "gin":
+            wo.append(rng.standard_normal((dims[l], dims[l])))
+            bo.append(rng.standard_normal(dims[l]) * 0.1)
         act.append(False if relu_none else (True if relu_all else l < L))
-    return O.OracleModel(agg, ws, wn, bs, act)
+    return O.OracleModel(agg, ws, wn, bs, act, wo, bo, gin_eps if agg == "gin" else 0.0)
 
 
 def _eval_expr(s):
@@ -43,13 +49,15 @@ def _eval_expr(s):
 # hand-derived closed forms
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("case", ["sage_sum_2layer", "sage_mean_1layer", "gcn_directed_1layer"])
+@pytest.mark.parametrize("case", ["sage_sum_2layer", "sage_mean_1layer", "gcn_directed_1layer", "gc_sum_2layer",
+                                  "gc_mean_1layer", "gin_1layer"])
 def test_hand_derived_values(case):
     fx = json.load(open(os.path.join(GOLDEN, "hand_small_graph.json")))
     arcs = np.array(fx["arcs"])
     c = fx["cases"][case]
     g = O.OracleGraph(fx["n"], arcs[:, 0], arcs[:, 1])
-    m = _model(c["agg"], c["w_self"], c["w_neigh"], c["bias"], c["relu"])
+    m = _model(c["agg"], c["w_self"], c["w_neigh"], c["bias"], c["relu"], c.get("w_out", ()),
+               c.get("b_out", ()), c.get("gin_eps", 0.0))
     hs = O.full_recompute(g, np.array(fx["x"], np.float64), m)
     for layer, rows in c["expected"].items():
         want = np.array([[_eval_expr(e) for e in r] for r in rows])
@@ -159,12 +167,14 @@ def _changed_rows(h_pre, h_post):
     return np.nonzero(np.any(h_pre != h_post, axis=1))[0]
 
 
-@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn", "gc_sum", "gc_mean"])
 @pytest.mark.parametrize("undirected", [False, True])
 def test_affected_sets_equal_changed_rows_without_activation(agg, undirected):
     """With no activation and generic values, a vertex's embedding changes iff it
-    is structurally affected (Sec. IV-C: no pruning, and nothing else changes)."""
-    rng = np.random.default_rng(10 + ("sum", "mean", "gcn").index(agg) + 7 * undirected)
+    is structurally affected (Sec. IV-C: no pruning, and nothing else changes).
+    For GraphConv this includes that a vertex whose own embedding changed, with no
+    changed in-neighbour and no changed arc, keeps its next-layer embedding."""
+    rng = np.random.default_rng(10 + O.AGGREGATORS.index(agg) + 7 * undirected)
     n, L = 30, 3
     dims = (3, 4, 3, 2)
     for trial in range(12):
@@ -182,7 +192,7 @@ def test_affected_sets_equal_changed_rows_without_activation(agg, undirected):
                                           err_msg=f"trial {trial} layer {l}")
 
 
-@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn", "gc_sum", "gc_mean", "gin"])
 def test_changed_rows_within_affected_sets_with_relu(agg):
     rng = np.random.default_rng(30)
     n, dims = 40, (4, 5, 3)
@@ -317,7 +327,7 @@ def test_permutation_equivariance():
             np.testing.assert_allclose(hp[l][perm], h[l], rtol=1e-12, atol=1e-12)
 
 
-@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn", "gc_sum", "gc_mean", "gin"])
 def test_sampled_embeddings_match_full_recompute(agg):
     rng = np.random.default_rng(70)
     n, dims = 200, (4, 6, 5, 3)
@@ -341,3 +351,48 @@ def test_row_relative_error_definition():
     got2 = ref.copy()
     got2[1, 0] = 1e-6
     assert math.isclose(O.row_relative_error(got2, ref), 1e-6 / eps, rel_tol=1e-9)
+
+
+# ---------------------------------------------------------------------------
+# GraphConv and GIN against other definitions
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("agg,sage", [("gc_sum", "sum"), ("gc_mean", "mean")])
+def test_graphconv_is_graphsage_without_self_weight(agg, sage):
+    """GraphConv's update is GraphSAGE's with the self weight set to zero."""
+    rng = np.random.default_rng(80)
+    n, dims = 60, (5, 7, 3)
+    src, dst = synth.erdos_renyi(n, 200, rng)
+    g = O.OracleGraph(n, src, dst)
+    x = rng.standard_normal((n, dims[0]))
+    gc = _random_model(rng, agg, dims)
+    sg = O.OracleModel(sage, [np.zeros((dims[l], dims[l - 1])) for l in (1, 2)], gc.w_neigh, gc.bias, gc.relu)
+    for a, b in zip(O.full_recompute(g, x, gc), O.full_recompute(g, x, sg)):
+        np.testing.assert_allclose(a, b, rtol=1e-13, atol=1e-13)
+
+
+def test_gin_matches_a_per_vertex_loop():
+    """GIN by brute force: for each vertex, (1 + eps) times its row plus a Python
+    loop over its in-neighbours, then the two-layer MLP written out per vertex."""
+    rng = np.random.default_rng(81)
+    n, dims, eps = 25, (3, 4, 2), 0.25
+    src, dst = synth.erdos_renyi(n, 70, rng)
+    g = O.OracleGraph(n, src, dst)
+    x = rng.standard_normal((n, dims[0]))
+    m = _random_model(rng, "gin", dims, gin_eps=eps)
+    hs = O.full_recompute(g, x, m)
+    a, b = g.arcs()
+    h = x
+    for l in (1, 2):
+        out = np.zeros((n, dims[l]))
+        for v in range(n):
+            z = (1.0 + eps) * h[v]
+            for u in a[b == v]:
+                z = z + h[u]
+            hid = [max(sum(m.w_neigh[l - 1][i, k] * z[k] for k in range(z.size)) + m.bias[l - 1][i], 0.0)
+                   for i in range(dims[l])]
+            for j in range(dims[l]):
+                y = sum(m.w_out[l - 1][j, i] * hid[i] for i in range(dims[l])) + m.b_out[l - 1][j]
+                out[v, j] = max(y, 0.0) if m.relu[l - 1] else y
+        np.testing.assert_allclose(hs[l], out, rtol=1e-12, atol=1e-12)
+        h = out
