@@ -22,6 +22,13 @@
  *                    the mean is 0 for a vertex without in-neighbours
  *   RIPPLE_AGG_GCN   GCN, symmetric normalisation with an implicit self-loop:
  *                    h = sigma(W sum_{u in N_in(v) + v} h_u / sqrt((dout(u)+1)(din(v)+1)) + b)
+ *   RIPPLE_AGG_GC_SUM, RIPPLE_AGG_GC_MEAN  GraphConv with sum or mean (the
+ *                    evaluation's GC-S and GC-M workloads, Sec. VII-A):
+ *                    h = sigma(W agg_u h_u + b), no self term; a vertex whose own
+ *                    embedding changed is affected at the next hop only through a
+ *                    changed in-neighbour or arc
+ *   RIPPLE_AGG_GIN   GINConv with sum (GI-S): h = sigma(W2 ReLU(W1 ((1 + eps) h_v
+ *                    + sum_u h_u) + b1) + b2)
  *
  * Graph semantics: a simple directed graph on vertices 0..n-1 (int32 ids).
  * Inserting a present arc, deleting an absent arc, and inserting or deleting a
@@ -74,7 +81,14 @@ typedef enum {
   RIPPLE_E_DEVICE = 4   /* HIP error or device-side check failed; the context is now poisoned */
 } ripple_status;
 
-typedef enum { RIPPLE_AGG_SUM = 0, RIPPLE_AGG_MEAN = 1, RIPPLE_AGG_GCN = 2 } ripple_agg;
+typedef enum {
+  RIPPLE_AGG_SUM = 0,     /* GraphSAGE-sum */
+  RIPPLE_AGG_MEAN = 1,    /* GraphSAGE-mean */
+  RIPPLE_AGG_GCN = 2,     /* GCN, symmetric normalisation, implicit self-loop */
+  RIPPLE_AGG_GC_SUM = 3,  /* GraphConv-sum (no self term) */
+  RIPPLE_AGG_GC_MEAN = 4, /* GraphConv-mean (no self term) */
+  RIPPLE_AGG_GIN = 5      /* GINConv-sum with a two-layer MLP */
+} ripple_agg;
 
 typedef enum { RIPPLE_GEMM_FP32 = 0, RIPPLE_GEMM_BF16 = 1 } ripple_gemm_prec;
 
@@ -113,16 +127,22 @@ typedef struct {
   int32_t num_layers;            /* L in [1, RIPPLE_MAX_LAYERS] */
   int32_t agg;                   /* ripple_agg */
   const int32_t *dims;           /* [L+1]: d_0 (feature width) .. d_L, each in [1, RIPPLE_MAX_DIM] */
-  const float *const *w_self;    /* [L] row-major [d_l][d_{l-1}]; ignored (may be NULL) for GCN */
-  const float *const *w_neigh;   /* [L] row-major [d_l][d_{l-1}]; GCN: its single W */
-  const float *const *bias;      /* [L] [d_l]; NULL array or NULL entry = zero bias */
+  const float *const *w_self;    /* [L] row-major [d_l][d_{l-1}]; GraphSAGE only (may be NULL otherwise) */
+  const float *const *w_neigh;   /* [L] row-major [d_l][d_{l-1}]; GCN, GraphConv: the single W;
+                                    GIN: the MLP's first layer W1 */
+  const float *const *bias;      /* [L] [d_l]; NULL array or NULL entry = zero bias (GIN: b1) */
   const int32_t *relu;           /* [L] 1 = ReLU after layer l, 0 = identity */
   int32_t gemm_prec;             /* ripple_gemm_prec; RIPPLE_GEMM_FP32 only in this version */
   int32_t transform_first;       /* per-layer choice of what the aggregate cache holds (see
                                     ripple_get_aggregates): -1 = for layers with d_l < d_{l-1} when the
                                     graph has at least 2^24 arcs (on smaller graphs the message step is
                                     latency-bound and the extra transform does not pay), 0 = never,
-                                    1 = every layer. Results are the same up to rounding. */
+                                    1 = every layer. Results are the same up to rounding. GraphSAGE and
+                                    GCN only: GraphConv and GIN models require -1 or 0 (never). */
+  const float *const *w_out;     /* GIN: [L] row-major [d_l][d_l], the MLP's second layer W2; else NULL */
+  const float *const *b_out;     /* GIN: [L] [d_l] b2; NULL array or NULL entry = zero */
+  float gin_eps;                 /* GIN: the own embedding enters as (1 + gin_eps) h_v */
+  int32_t reserved;              /* 0 */
 } ripple_model_desc;
 
 /* What one ripple_apply_updates call did. Arc counts count directed arcs (an

@@ -71,7 +71,10 @@ struct LayerPtrs {
   int L;
 };
 
-enum Agg { kSum = 0, kMean = 1, kGcn = 2 };
+// Same values as ripple_agg. GraphConv (kGcSum, kGcMean) has no self term; GIN's
+// update is a two-layer MLP on (1 + eps) h_v + S_v.
+enum Agg { kSum = 0, kMean = 1, kGcn = 2, kGcSum = 3, kGcMean = 4, kGin = 5 };
+inline bool has_self_term(int agg) { return agg != kGcSum && agg != kGcMean; }
 
 // --- launchers (each defined in the translation unit that holds its kernel) ---
 
@@ -160,9 +163,11 @@ void launch_delta0(hipStream_t s, long long n, int agg, int d0, int ld, const in
 // marks (the pull kernel then adds the messages).
 // pushed = the number of arcs to push (the out-degree sum over the list, written
 // by the compaction that built the list).
+// mark_list: also mark the listed (dirty) vertices themselves in bm_x (models with
+// a self term).
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
-                    const int *del_dst, const u64 *pushed, const Counters *c, bool push);
+                    const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list);
 
 // pull: for every vertex v of the sorted list A (in-arc prefix ioff; list null =
 // the identity), S[v] += sum of msg[rank(u)] over in-arcs (u -> v) whose source u
@@ -188,7 +193,11 @@ void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev,
 // dprev); with bias nullptr and relu 0 this computes the rows P_v = W_neigh h_v a
 // transform-first layer caches (H = P) and, with delta set, their messages
 // c'_v P'_v - c_v P_v.
-enum GemmMode { kLayer = 0, kTransformFirst = 1, kPlain = 2 };
+// GraphConv layers (agg kGcSum / kGcMean) use kLayer with Z = t_v S_v (K = dprev).
+// GIN layers run two GEMMs: kGin1, Z = S_v + eps1 h_v (K = dprev), y = ReLU(Z W1^T
+// + b1) written to H[m] (a row buffer indexed by list position, no delta); then
+// kGin2, Z = Hprev[m] (that buffer, K = dprev = its width), the epilogue of kLayer.
+enum GemmMode { kLayer = 0, kTransformFirst = 1, kPlain = 2, kGin1 = 3, kGin2 = 4 };
 // Row stride (floats) of message and delta rows of width w: rows start on 64-byte
 // boundaries, so a row read touches the fewest memory segments.
 inline int row_ld(int w) { return (w + 15) / 16 * 16; }
@@ -214,6 +223,7 @@ struct GemmArgs {
   int dld;  // row stride of delta (floats)
   int agg;
   const u64 *abort;
+  float eps1;  // GIN: 1 + eps
 };
 // expected_rows picks the tile height (large tiles when many rows are expected).
 void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows, long long expected_rows);

@@ -435,7 +435,7 @@ template <int G, int NC, bool PUSH>
 __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list, const u64 *count, const long long *doff,
                                                  const float *delta, Adj out, float *S, unsigned *bm_out,
                                                  unsigned *bm_x, const int *ins_dst, const int *del_dst,
-                                                 const u64 *pushed, const Counters *c) {
+                                                 const u64 *pushed, const Counters *c, int mark_list) {
   if (c->abort) return;
   const int lane = lane_id();
   const long long nD = static_cast<long long>(*count);
@@ -446,7 +446,8 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
     const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
     const long long t0 = blockIdx.x * blockDim.x + threadIdx.x;
     for (long long i = t0; i < na; i += stride) mark_only(bm_x, i < ni ? ins_dst[i] : del_dst[i - ni]);
-    for (long long j = t0; j < nD; j += stride) mark_only(bm_x, list[j]);
+    if (mark_list)
+      for (long long j = t0; j < nD; j += stride) mark_only(bm_x, list[j]);
   }
   const long long waves = num_waves();
   int C = 1;
@@ -772,11 +773,11 @@ void launch_delta0(hipStream_t s, long long n, int agg, int d0, int ld, const in
 
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
-                    const int *del_dst, const u64 *pushed, const Counters *c, bool push) {
+                    const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list) {
   const int blocks = 2048;
 #define RP_SCATTER(GV, NCV, P)                                                                                     \
   hipLaunchKernelGGL((k_scatter<GV, NCV, P>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, doff, delta, out, S, \
-                     bm_out, bm_x, ins_dst, del_dst, pushed, c)
+                     bm_out, bm_x, ins_dst, del_dst, pushed, c, mark_list ? 1 : 0)
   if (!push) RP_SCATTER(64, 1, false);
   else if (d <= 16) RP_SCATTER(16, 1, true);
   else if (d <= 32) RP_SCATTER(32, 1, true);

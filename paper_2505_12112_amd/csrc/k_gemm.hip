@@ -21,6 +21,10 @@
 // (GCN). kPlain: y = h_v W^T with no bias or activation; used for the rows
 // P_v = W_neigh h_v that a transform-first layer caches, and its messages
 // c'_v P'_v - c_v P_v formed by the same epilogue as the layer deltas.
+// GraphConv (no self term): kLayer with z_v = t_v S_v (t = 1, or 1/d_in for the
+// mean). GIN: kGin1 forms z_v = S_v + (1 + eps) h_v and writes ReLU(z W1^T + b1)
+// to a buffer row per list position; kGin2 reads those rows as its operand and
+// finishes with W2, b2 and the kLayer epilogue (the MLP of GINConv).
 #include "internal.h"
 
 namespace rp {
@@ -44,13 +48,36 @@ struct Shape {
   static constexpr int kBPer = (kBChunks + kThreads - 1) / kThreads;
 };
 
+// True when Z = t (S + s h) with K = dprev: GCN (t, s from degrees) and GIN's
+// first GEMM (t = 1, s = 1 + eps).
+template <int AGG, int MODE>
+__device__ constexpr bool sum_form() {
+  return (MODE == kLayer && AGG == kGcn) || MODE == kGin1;
+}
+// True when Z = t S with K = dprev (GraphConv).
+template <int AGG, int MODE>
+__device__ constexpr bool neigh_only() {
+  return MODE == kLayer && (AGG == kGcSum || AGG == kGcMean);
+}
+
+// Operand row v (kGin2: list position v), columns k .. k+3.
 template <int AGG, bool VEC, int MODE>
-__device__ inline float4 load_a(const GemmArgs &a, int v, float tv, float sv, int k) {
+__device__ inline float4 load_a(const GemmArgs &a, long long v, float tv, float sv, int k) {
   float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
   if (v < 0 || k >= a.K) return r;
   const int dp = a.dprev;
-  const long long base = static_cast<long long>(v) * dp;
-  if (MODE != kLayer) {  // plain rows of the previous layer (K == dprev)
+  const long long base = v * dp;
+  if (neigh_only<AGG, MODE>()) {
+    if (VEC) {
+      const float4 q = *reinterpret_cast<const float4 *>(a.S + base + k);
+      return make_float4(tv * q.x, tv * q.y, tv * q.z, tv * q.w);
+    }
+    float t[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) t[i] = k + i < a.K ? tv * a.S[base + k + i] : 0.f;
+    return make_float4(t[0], t[1], t[2], t[3]);
+  }
+  if (MODE != kLayer && MODE != kGin1) {  // plain rows of the previous layer (K == dprev)
     if (VEC) return *reinterpret_cast<const float4 *>(a.Hprev + base + k);
     float t[4];
 #pragma unroll
@@ -58,7 +85,7 @@ __device__ inline float4 load_a(const GemmArgs &a, int v, float tv, float sv, in
     return make_float4(t[0], t[1], t[2], t[3]);
   }
   if (VEC) {
-    if (AGG == kGcn) {
+    if (sum_form<AGG, MODE>()) {
       const float4 s = *reinterpret_cast<const float4 *>(a.S + base + k);
       const float4 h = *reinterpret_cast<const float4 *>(a.Hprev + base + k);
       r = make_float4(tv * (s.x + sv * h.x), tv * (s.y + sv * h.y), tv * (s.z + sv * h.z), tv * (s.w + sv * h.w));
@@ -76,7 +103,7 @@ __device__ inline float4 load_a(const GemmArgs &a, int v, float tv, float sv, in
     const int kk = k + i;
     float val = 0.f;
     if (kk < a.K) {
-      if (AGG == kGcn) {
+      if (sum_form<AGG, MODE>()) {
         val = tv * (a.S[base + kk] + sv * a.Hprev[base + kk]);
       } else {
         val = kk < dp ? a.Hprev[base + kk] : tv * a.S[base + (kk - dp)];
@@ -109,8 +136,8 @@ __device__ inline void epilogue(const GemmArgs &a, long long m, int v, int col, 
   }
   y += a.bias != nullptr ? a.bias[col] : 0.f;
   if (a.relu) y = fmaxf(y, 0.f);
-  float *hp = a.H + static_cast<long long>(v) * N + col;
-  if (a.delta != nullptr) {
+  float *hp = a.H + (MODE == kGin1 ? m : static_cast<long long>(v)) * N + col;
+  if (MODE != kGin1 && a.delta != nullptr) {
     float cn = 1.f, co = 1.f;
     if (AGG == kGcn) {
       cn = sv;
@@ -154,7 +181,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
       float tv = 0.f, sv = 0.f;
       if (row < M) {
         v = a.rows != nullptr ? a.rows[row] : static_cast<int>(row);
-        if (AGG == kMean) {
+        if (AGG == kMean || AGG == kGcMean) {
           const int din = a.in_len[v];
           tv = din > 0 ? 1.0f / static_cast<float>(din) : 0.f;
         } else if (AGG == kGcn) {
@@ -162,6 +189,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
           sv = 1.0f / sqrtf(static_cast<float>(a.out_len[v]) + 1.0f);
         } else {
           tv = 1.0f;
+          if (MODE == kGin1) sv = a.eps1;
         }
       }
       rv[r] = v;
@@ -178,7 +206,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
         if (c < Sh::kAChunks) {
           const int m = c / (kBK / 4);
           const int q = c % (kBK / 4);
-          ra[i] = load_a<AGG, VEC, MODE>(a, rv[m], rt[m], rs[m], k0 + 4 * q);
+          const long long arow = MODE == kGin2 ? (rv[m] >= 0 ? m0 + m : -1) : rv[m];
+          ra[i] = load_a<AGG, VEC, MODE>(a, arow, rt[m], rs[m], k0 + 4 * q);
         }
       }
 #pragma unroll
@@ -303,6 +332,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
     // row ids: the lane's operand row and the rows of its output elements
     const long long ar = m0 + lr;
     const int va = ar < M ? (a.rows != nullptr ? a.rows[ar] : static_cast<int>(ar)) : -1;
+    const long long arow = MODE == kGin2 ? (ar < M ? ar : -1) : va;  // operand row (kGin2: list position)
     int ve[kEl];
 #pragma unroll
     for (int i = 0; i < kEl; ++i) {
@@ -313,7 +343,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
     // s = (deg_out+1)^-1/2
     float ta = 1.f, sa = 0.f;
     if (MODE == kLayer && va >= 0) {
-      if (AGG == kMean) {
+      if (AGG == kMean || AGG == kGcMean) {
         const int din = a.in_len[va];
         ta = din > 0 ? 1.0f / static_cast<float>(din) : 0.f;
       } else if (AGG == kGcn) {
@@ -321,6 +351,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
         sa = 1.0f / sqrtf(static_cast<float>(a.out_len[va]) + 1.0f);
       }
     }
+    if (MODE == kGin1) sa = a.eps1;
     // epilogue inputs
     float e_old[kEl], e_t[kEl], e_tv[kEl], e_sv[kEl], e_co[kEl], e_b[kEl];
 #pragma unroll
@@ -335,7 +366,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
       e_b[i] = 0.f;
       if (v < 0 || col >= N) continue;
       const long long idx = static_cast<long long>(v) * N + col;
-      if (a.delta != nullptr) e_old[i] = a.H[idx];
+      if (MODE != kGin1 && a.delta != nullptr) e_old[i] = a.H[idx];
       if (a.bias != nullptr) e_b[i] = a.bias[col];
       if (MODE == kTransformFirst) {
         e_t[i] = a.S[idx];
@@ -356,20 +387,22 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
     floatx4 acc[WN];
 #pragma unroll
     for (int j = 0; j < WN; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const long long abase = static_cast<long long>(va) * dp;
+    const long long abase = arow * dp;
     for (int kc = kb; kc < ke; kc += kRowsKC) {
       float4 av[kF], ah[kF], bv[WN][kF];
 #pragma unroll
       for (int f = 0; f < kF; ++f) {
         const int k = kc + 16 * f + 4 * lq;
-        const bool ok = va >= 0 && k < ke;
+        const bool ok = arow >= 0 && k < ke;
         float4 x = make_float4(0.f, 0.f, 0.f, 0.f), h = x;
         if (ok) {
-          if (MODE != kLayer) {
-            x = *reinterpret_cast<const float4 *>(a.Hprev + abase + k);
-          } else if (AGG == kGcn) {  // K == dp: z = t (S + s h)
+          if (neigh_only<AGG, MODE>()) {  // K == dp: z = t S
+            x = *reinterpret_cast<const float4 *>(a.S + abase + k);
+          } else if (sum_form<AGG, MODE>()) {  // K == dp: z = t (S + s h)
             x = *reinterpret_cast<const float4 *>(a.S + abase + k);
             h = *reinterpret_cast<const float4 *>(a.Hprev + abase + k);
+          } else if (MODE != kLayer) {  // plain rows (kGin2: the first GEMM's rows)
+            x = *reinterpret_cast<const float4 *>(a.Hprev + abase + k);
           } else {  // z = [h || t S]
             x = k < dp ? *reinterpret_cast<const float4 *>(a.Hprev + abase + k)
                        : *reinterpret_cast<const float4 *>(a.S + abase + (k - dp));
@@ -388,14 +421,14 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
                                        : make_float4(0.f, 0.f, 0.f, 0.f);
         }
       }
-      if (MODE == kLayer && AGG != kSum) {
+      if ((MODE == kLayer && AGG != kSum && AGG != kGcSum) || MODE == kGin1) {
 #pragma unroll
         for (int f = 0; f < kF; ++f) {
           const int k = kc + 16 * f + 4 * lq;
-          if (AGG == kGcn) {
+          if (sum_form<AGG, MODE>()) {
             av[f] = make_float4(ta * (av[f].x + sa * ah[f].x), ta * (av[f].y + sa * ah[f].y),
                                 ta * (av[f].z + sa * ah[f].z), ta * (av[f].w + sa * ah[f].w));
-          } else if (k >= dp) {
+          } else if (neigh_only<AGG, MODE>() || k >= dp) {
             av[f] = make_float4(ta * av[f].x, ta * av[f].y, ta * av[f].z, ta * av[f].w);
           }
         }
@@ -428,8 +461,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
       if (MODE == kTransformFirst) y = AGG == kGcn ? e_tv[i] * (e_t[i] + e_sv[i] * y) : y + e_tv[i] * e_t[i];
       y += e_b[i];
       if (a.relu) y = fmaxf(y, 0.f);
-      const long long idx = static_cast<long long>(v) * N + col;
-      if (a.delta != nullptr) {
+      const long long idx = (MODE == kGin1 ? m0 + ml : static_cast<long long>(v)) * N + col;
+      if (MODE != kGin1 && a.delta != nullptr) {
         const float cn = AGG == kGcn ? e_sv[i] : 1.f;
         a.delta[(m0 + ml) * a.dld + col] = cn * y - e_co[i] * e_old[i];
       }
@@ -490,16 +523,26 @@ void launch_vec(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) 
 
 template <int MODE>
 void launch_mode(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) {
-  switch (a.agg) {
-    case kMean:
-      launch_vec<kMean, MODE>(s, a, max_rows, big);
-      break;
-    case kGcn:
-      launch_vec<kGcn, MODE>(s, a, max_rows, big);
-      break;
-    default:
-      launch_vec<kSum, MODE>(s, a, max_rows, big);
-      break;
+  if constexpr (MODE == kGin1 || MODE == kGin2) {
+    launch_vec<kSum, MODE>(s, a, max_rows, big);  // GIN sums with coefficient 1
+  } else {
+    switch (a.agg) {
+      case kMean:
+        launch_vec<kMean, MODE>(s, a, max_rows, big);
+        break;
+      case kGcn:
+        launch_vec<kGcn, MODE>(s, a, max_rows, big);
+        break;
+      case kGcSum:
+        if constexpr (MODE == kLayer) launch_vec<kGcSum, MODE>(s, a, max_rows, big);
+        break;
+      case kGcMean:
+        if constexpr (MODE == kLayer) launch_vec<kGcMean, MODE>(s, a, max_rows, big);
+        break;
+      default:
+        launch_vec<kSum, MODE>(s, a, max_rows, big);
+        break;
+    }
   }
 }
 
@@ -509,6 +552,8 @@ void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows, long long
   const bool big = expected_rows >= 32768;
   if (a.mode == kTransformFirst) launch_mode<kTransformFirst>(s, a, max_rows, big);
   else if (a.mode == kPlain) launch_mode<kPlain>(s, a, max_rows, big);
+  else if (a.mode == kGin1) launch_mode<kGin1>(s, a, max_rows, big);
+  else if (a.mode == kGin2) launch_mode<kGin2>(s, a, max_rows, big);
   else launch_mode<kLayer>(s, a, max_rows, big);
 }
 

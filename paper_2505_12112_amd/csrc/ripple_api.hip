@@ -74,6 +74,10 @@ struct ripple_ctx {
   float *Wn[rp::kMaxL] = {};    // transform-first layers: W_neigh [d_l][d_{l-1}] (GCN: W)
   float *P[rp::kMaxL + 1] = {};  // [l], transform-first layers: P = W_neigh H^{l-1}, [n][d_l]
   float *bias[rp::kMaxL] = {};
+  float *W2[rp::kMaxL] = {};     // GIN: the MLP's second layer [d_l][d_l]
+  float *b2[rp::kMaxL] = {};
+  float gin_eps1 = 1.0f;         // GIN: 1 + eps
+  float *gin_rows = nullptr;     // GIN: the MLP's hidden rows, one per list position [n][max d_l]
   int tf[rp::kMaxL + 1] = {};   // [l]: layer l caches T = W_neigh S (width d_l)
   int sw[rp::kMaxL + 1] = {};   // [l]: width of the cached aggregate rows
   float *msg = nullptr;         // [n][max d_l of transform-first layers]: message rows
@@ -392,7 +396,10 @@ void free_model(ripple_ctx *c) {
     dfree_t(c, c->W[l]);
     dfree_t(c, c->Wn[l]);
     dfree_t(c, c->bias[l]);
+    dfree_t(c, c->W2[l]);
+    dfree_t(c, c->b2[l]);
   }
+  dfree_t(c, c->gin_rows);
   dfree_t(c, c->msg);
   for (int l = 0; l <= rp::kMaxL; ++l) dfree_t(c, c->P[l]);
   for (int l = 0; l <= rp::kMaxL; ++l) {
@@ -447,6 +454,7 @@ rp::GemmArgs gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 *c
   g.dld = rp::row_ld(c->dims[l]);
   g.agg = c->agg;
   g.abort = abort;
+  g.eps1 = c->gin_eps1;
   return g;
 }
 
@@ -478,6 +486,34 @@ rp::GemmArgs p_gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 
   g.agg = c->agg;
   g.abort = abort;
   return g;
+}
+
+// Layer l's transform on `rows` (nullptr: all, count_fixed of them): one GEMM, or
+// GIN's two (the MLP's hidden rows go through gin_rows). Returns the launches.
+int launch_layer_gemm(const ripple_ctx *c, hipStream_t s, int l, const int *rows, const u64 *count,
+                      long long count_fixed, float *delta, const u64 *abort, long long max_rows,
+                      long long expected_rows) {
+  rp::GemmArgs g = gemm_args(c, l, rows, count, count_fixed, delta, abort);
+  if (c->agg != rp::kGin) {
+    rp::launch_gemm(s, g, max_rows, expected_rows);
+    return 1;
+  }
+  rp::GemmArgs g1 = g;  // hidden = ReLU(W1 ((1 + eps) h + S) + b1), one row per list position
+  g1.mode = rp::kGin1;
+  g1.relu = 1;
+  g1.H = c->gin_rows;
+  g1.delta = nullptr;
+  rp::launch_gemm(s, g1, max_rows, expected_rows);
+  rp::GemmArgs g2 = g;  // y = W2 hidden + b2, then the layer's activation, delta and write-back
+  g2.mode = rp::kGin2;
+  g2.Hprev = c->gin_rows;
+  g2.dprev = c->dims[l];
+  g2.S = nullptr;
+  g2.W = c->W2[l - 1];
+  g2.K = c->dims[l];
+  g2.bias = c->b2[l - 1];
+  rp::launch_gemm(s, g2, max_rows, expected_rows);
+  return 2;
 }
 
 // --- profiling helpers ---
@@ -625,7 +661,8 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
       // message
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
       rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out,
-                         c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->zero, dc, false);
+                         c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->zero, dc, false,
+                         rp::has_self_term(c->agg));
       rp::CompactOut all{};
       all.full_n = c->n;
       all.count = &dc->count_all;
@@ -640,7 +677,7 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
       rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out,
                          c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc,
-                         mode == kPushLayer);
+                         mode == kPushLayer, rp::has_self_term(c->agg));
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     {
@@ -669,9 +706,8 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
     }
     {
       PhaseScope ps(c, RIPPLE_PHASE_GEMM);
-      rp::launch_gemm(s, gemm_args(c, l, c->lists[l], &dc->count[l], 0, dout, &dc->abort), c->n,
-                      c->has_batch ? c->last_count[l] : 0);
-      add_launches(c, RIPPLE_PHASE_GEMM, 1);
+      add_launches(c, RIPPLE_PHASE_GEMM, launch_layer_gemm(c, s, l, c->lists[l], &dc->count[l], 0, dout,
+                                                          &dc->abort, c->n, c->has_batch ? c->last_count[l] : 0));
     }
   }
   {
@@ -709,6 +745,10 @@ void account_phases(ripple_ctx *c) {
     const double m = static_cast<double>(k.count[l]);
     const double K = c->K[l - 1], N = c->dims[l];
     c->ph_flops[RIPPLE_PHASE_GEMM] += 2.0 * m * K * N;
+    if (c->agg == rp::kGin) {  // the MLP's second layer: hidden rows in and out once more
+      c->ph_flops[RIPPLE_PHASE_GEMM] += 2.0 * m * N * N;
+      c->ph_bytes[RIPPLE_PHASE_GEMM] += 8.0 * m * N + 4.0 * N * N;
+    }
     c->ph_bytes[RIPPLE_PHASE_GEMM] += 4.0 * m * K + 4.0 * N * K + 4.0 * m * N * (l < c->L && !c->tf[l + 1] ? 3.0 : 2.0);
     c->ph_bytes[RIPPLE_PHASE_COMPACT] += 24.0 * words + 4.0 * m;
   }
@@ -944,16 +984,20 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   if (x == nullptr || md == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: x and model must be non-NULL");
   const int L = md->num_layers;
   if (L < 1 || L > rp::kMaxL) return fail(c, RIPPLE_E_INVALID, "ripple: num_layers out of range");
-  if (md->agg < 0 || md->agg > 2) return fail(c, RIPPLE_E_INVALID, "ripple: unknown aggregator");
+  if (md->agg < RIPPLE_AGG_SUM || md->agg > RIPPLE_AGG_GIN) return fail(c, RIPPLE_E_INVALID, "ripple: unknown aggregator");
+  const bool sage = md->agg == RIPPLE_AGG_SUM || md->agg == RIPPLE_AGG_MEAN;
+  const bool gin = md->agg == RIPPLE_AGG_GIN;
+  if (!sage && md->agg != RIPPLE_AGG_GCN && md->transform_first == 1)
+    return fail(c, RIPPLE_E_INVALID, "ripple: transform_first = 1 needs a GraphSAGE or GCN model");
+  if (gin && md->w_out == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: w_out must be non-NULL for GIN");
   if (md->gemm_prec != RIPPLE_GEMM_FP32) return fail(c, RIPPLE_E_INVALID, "ripple: only RIPPLE_GEMM_FP32 is built");
   if (md->dims == nullptr || md->w_neigh == nullptr || md->relu == nullptr)
     return fail(c, RIPPLE_E_INVALID, "ripple: dims, w_neigh and relu must be non-NULL");
-  if (md->agg != RIPPLE_AGG_GCN && md->w_self == nullptr)
-    return fail(c, RIPPLE_E_INVALID, "ripple: w_self must be non-NULL for GraphSAGE");
+  if (sage && md->w_self == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: w_self must be non-NULL for GraphSAGE");
   for (int l = 0; l <= L; ++l)
     if (md->dims[l] < 1 || md->dims[l] > RIPPLE_MAX_DIM) return fail(c, RIPPLE_E_INVALID, "ripple: dim out of range");
   for (int l = 0; l < L; ++l) {
-    if (md->w_neigh[l] == nullptr || (md->agg != RIPPLE_AGG_GCN && md->w_self[l] == nullptr))
+    if (md->w_neigh[l] == nullptr || (sage && md->w_self[l] == nullptr) || (gin && md->w_out[l] == nullptr))
       return fail(c, RIPPLE_E_INVALID, "ripple: missing weight matrix");
   }
   if (md->transform_first < -1 || md->transform_first > 1)
@@ -969,20 +1013,22 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   for (int l = 1; l <= L; ++l) {
     const int dp = c->dims[l - 1], dn = c->dims[l];
     const long long arcs = c->arcs_loaded;
-    c->tf[l] = md->transform_first == 1 || (md->transform_first == -1 && dn < dp && arcs >= (1LL << 24));
+    c->tf[l] = (sage || md->agg == RIPPLE_AGG_GCN) &&
+               (md->transform_first == 1 || (md->transform_first == -1 && dn < dp && arcs >= (1LL << 24)));
     c->sw[l] = c->tf[l] ? dn : dp;
     if (c->tf[l]) msg_width = std::max(msg_width, dn);
   }
-  // weights. Plain layers: SAGE W = [W_self | W_neigh] (K = 2 d_{l-1}), GCN W
-  // (K = d_{l-1}). Transform-first layers: W = W_self (SAGE) or W (GCN), K =
-  // d_{l-1}, plus W_neigh (GCN: W) for the messages and corrections.
+  // weights. Plain layers: SAGE W = [W_self | W_neigh] (K = 2 d_{l-1}); GCN and
+  // GraphConv W, GIN W1 (K = d_{l-1}). Transform-first layers: W = W_self (SAGE)
+  // or W (GCN), K = d_{l-1}, plus W_neigh (GCN: W) for the messages and
+  // corrections. GIN also keeps W2 [d_l][d_l] and b2.
+  c->gin_eps1 = 1.0f + (gin ? md->gin_eps : 0.0f);
   for (int l = 1; l <= L; ++l) {
     const int dp = c->dims[l - 1], dn = c->dims[l];
-    const bool gcn = md->agg == RIPPLE_AGG_GCN;
-    const int K = (gcn || c->tf[l]) ? dp : 2 * dp;
+    const int K = (!sage || c->tf[l]) ? dp : 2 * dp;
     c->K[l - 1] = K;
     c->relu[l - 1] = md->relu[l - 1] ? 1 : 0;
-    const float *wmain = gcn ? md->w_neigh[l - 1] : md->w_self[l - 1];
+    const float *wmain = sage ? md->w_self[l - 1] : md->w_neigh[l - 1];
     std::vector<float> w(static_cast<size_t>(dn) * K);
     for (int j = 0; j < dn; ++j) {
       std::memcpy(&w[static_cast<size_t>(j) * K], wmain + static_cast<size_t>(j) * dp, dp * sizeof(float));
@@ -1001,6 +1047,15 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
       RP_HIP(c, hipMemcpyAsync(c->Wn[l - 1], md->w_neigh[l - 1], static_cast<size_t>(dn) * dp * sizeof(float),
                                hipMemcpyHostToDevice, c->stream));
     }
+    if (gin) {
+      std::vector<float> b2(dn, 0.0f);
+      if (md->b_out != nullptr && md->b_out[l - 1] != nullptr) std::memcpy(b2.data(), md->b_out[l - 1], dn * sizeof(float));
+      RP_TRY(dalloc_n(c, &c->W2[l - 1], static_cast<long long>(dn) * dn));
+      RP_TRY(dalloc_n(c, &c->b2[l - 1], dn));
+      RP_HIP(c, hipMemcpyAsync(c->W2[l - 1], md->w_out[l - 1], static_cast<size_t>(dn) * dn * sizeof(float),
+                               hipMemcpyHostToDevice, c->stream));
+      RP_HIP(c, hipMemcpyAsync(c->b2[l - 1], b2.data(), dn * sizeof(float), hipMemcpyHostToDevice, c->stream));
+    }
     RP_HIP(c, hipStreamSynchronize(c->stream));
   }
   for (int l = 0; l <= L; ++l) {
@@ -1017,6 +1072,11 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
     RP_TRY(dalloc_n(c, &c->wprefix[k], (n + 31) / 32));
   }
   if (msg_width > 0) RP_TRY(dalloc_n(c, &c->msg, n * rp::row_ld(msg_width)));
+  if (gin) {
+    int dmax = 0;
+    for (int l = 1; l <= L; ++l) dmax = std::max(dmax, c->dims[l]);
+    RP_TRY(dalloc_n(c, &c->gin_rows, n * dmax));
+  }
   for (int l = 1; l <= L; ++l)
     if (c->tf[l]) RP_TRY(dalloc_n(c, &c->P[l], n * c->dims[l]));
   RP_HIP(c, hipMemcpyAsync(c->H[0], x, static_cast<size_t>(n) * c->dims[0] * sizeof(float), hipMemcpyHostToDevice,
@@ -1031,7 +1091,7 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
     } else {
       rp::launch_pull(c->stream, n, c->dims[l - 1], c->agg, c->H[l - 1], c->adj[1], c->adj[0].len, c->S[l]);
     }
-    rp::launch_gemm(c->stream, gemm_args(c, l, nullptr, nullptr, n, nullptr, nullptr), n, n);
+    launch_layer_gemm(c, c->stream, l, nullptr, nullptr, n, nullptr, nullptr, n, n);
     RP_HIP(c, hipGetLastError());
   }
   RP_HIP(c, hipStreamSynchronize(c->stream));

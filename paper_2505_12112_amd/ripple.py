@@ -20,7 +20,7 @@ MAX_LAYERS = 8
 NUM_PHASES = 8
 
 OK, E_INVALID, E_STATE, E_OOM, E_DEVICE = 0, 1, 2, 3, 4
-AGG = {"sum": 0, "mean": 1, "gcn": 2}
+AGG = {"sum": 0, "mean": 1, "gcn": 2, "gc_sum": 3, "gc_mean": 4, "gin": 5}
 GEMM = {"fp32": 0, "bf16": 1}
 OP_INSERT, OP_DELETE, OP_FEATURE = 1, 2, 3
 PHASES = ["net", "topo", "layer0", "scatter", "compact", "gemm", "other", "total"]
@@ -60,6 +60,8 @@ class ModelDesc(C.Structure):
         ("w_self", C.POINTER(C.POINTER(C.c_float))), ("w_neigh", C.POINTER(C.POINTER(C.c_float))),
         ("bias", C.POINTER(C.POINTER(C.c_float))), ("relu", C.POINTER(C.c_int32)),
         ("gemm_prec", C.c_int32), ("transform_first", C.c_int32),
+        ("w_out", C.POINTER(C.POINTER(C.c_float))), ("b_out", C.POINTER(C.POINTER(C.c_float))),
+        ("gin_eps", C.c_float), ("reserved", C.c_int32),
     ]
 
 
@@ -173,8 +175,9 @@ class Ripple:
 
     # -- calls --
     def init_embeddings(self, x, weights, gemm: str = "fp32", transform_first: int = -1):
-        """weights: object with agg, dims, w_self, w_neigh, bias, relu (synth.ModelWeights).
-        transform_first: -1 for layers that narrow (d_l < d_{l-1}), 0 never, 1 always."""
+        """weights: object with agg, dims, w_self, w_neigh, bias, relu (and for GIN
+        w_out, b_out, gin_eps), e.g. synth.ModelWeights. transform_first: -1 for
+        layers that narrow (d_l < d_{l-1}), 0 never, 1 always (GraphSAGE and GCN)."""
         x = _f32(x)
         dims = _i32(weights.dims)
         L = len(dims) - 1
@@ -196,8 +199,20 @@ class Ripple:
                 bs[l] = _ptr(b, C.c_float)
         relu = _i32([1 if r else 0 for r in weights.relu])
         keep.append(relu)
+        wo = bo = None
+        if getattr(weights, "w_out", None):  # GIN: the MLP's second layer
+            wo = (C.POINTER(C.c_float) * L)()
+            bo = (C.POINTER(C.c_float) * L)()
+            for l in range(L):
+                a = _f32(weights.w_out[l])
+                keep.append(a)
+                wo[l] = _ptr(a, C.c_float)
+                if weights.b_out and weights.b_out[l] is not None:
+                    b = _f32(weights.b_out[l])
+                    keep.append(b)
+                    bo[l] = _ptr(b, C.c_float)
         md = ModelDesc(L, AGG[weights.agg], _ptr(dims, C.c_int32), ws, wn, bs, _ptr(relu, C.c_int32),
-                       GEMM[gemm], int(transform_first))
+                       GEMM[gemm], int(transform_first), wo, bo, float(getattr(weights, "gin_eps", 0.0)), 0)
         self._check(self._lib.ripple_init_embeddings(self._ctx, _ptr(x, C.c_float), C.byref(md)))
         self.dims = [int(d) for d in dims]
         self.num_layers = L

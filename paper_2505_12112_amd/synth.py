@@ -11,6 +11,9 @@ Table "Graph datasets used in experiments"), which are not available here:
 * ``sparse_mid``      directed Chung-Lu power law (exponent 2.1) shaped like
                       ogbn-arxiv: 169,343 vertices, 1,166,243 arcs, 128 features.
 * ``sparse_mid_mean`` the same graph with a 3-layer GraphSAGE-mean model.
+* ``sparse_mid_gc_sum``, ``sparse_mid_gc_mean``, ``sparse_mid_gin``  the same
+                      graph with the evaluation's GraphConv-sum, GraphConv-mean
+                      and GIN-sum workloads (2 layers, 128-256-40).
 * ``dense_large``     undirected Chung-Lu (exponent 2.1) shaped like
                       ogbn-products: 2,449,029 vertices, 61,859,140 edges, 100 features.
 * ``dense_large_2l``  the same graph with a 2-layer model (the paper's 2-layer
@@ -98,6 +101,23 @@ CONFIGS: Dict[str, WorkloadSpec] = {
         GraphSpec("chung_lu", 169_343, 1_166_243),
         ModelSpec(AGG_MEAN, (128, 256, 256, 40)),
         StreamSpec((100,), (1 / 3, 1 / 3, 1 / 3))),
+    # the evaluation's other workloads (Sec. VII-A: GC-S, GC-M, GI-S) on the
+    # Arxiv-shaped graph, 2 layers like sparse_mid (which is GS-S)
+    "sparse_mid_gc_sum": WorkloadSpec(
+        "sparse_mid_gc_sum",
+        GraphSpec("chung_lu", 169_343, 1_166_243),
+        ModelSpec(AGG_GC_SUM, (128, 256, 40)),
+        StreamSpec((1, 10, 100, 1000), (1 / 3, 1 / 3, 1 / 3))),
+    "sparse_mid_gc_mean": WorkloadSpec(
+        "sparse_mid_gc_mean",
+        GraphSpec("chung_lu", 169_343, 1_166_243),
+        ModelSpec(AGG_GC_MEAN, (128, 256, 40)),
+        StreamSpec((1, 10, 100, 1000), (1 / 3, 1 / 3, 1 / 3))),
+    "sparse_mid_gin": WorkloadSpec(
+        "sparse_mid_gin",
+        GraphSpec("chung_lu", 169_343, 1_166_243),
+        ModelSpec(AGG_GIN, (128, 256, 40), gin_eps=0.1),
+        StreamSpec((1, 10, 100, 1000), (1 / 3, 1 / 3, 1 / 3))),
     "dense_large": WorkloadSpec(
         "dense_large",
         GraphSpec("chung_lu", 2_449_029, 61_859_140, undirected=True),

@@ -37,6 +37,26 @@ def test_sparse_mid_full_size(bs):
         p.close()
 
 
+@pytest.mark.parametrize("config", ["sparse_mid_gc_sum", "sparse_mid_gc_mean", "sparse_mid_gin"])
+def test_evaluation_workloads_on_the_arxiv_shaped_graph(config):
+    """GraphConv-sum, GraphConv-mean and GIN-sum (2 layers, 128-256-40) at full size:
+    20 batches of 100 with affected sets every batch, then all embeddings against a
+    float64 full recompute."""
+    wl = synth.build_workload(config)
+    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights)
+    try:
+        p.check_embeddings()
+        t0 = time.time()
+        for b in range(20):
+            st, _, sets = p.step(wl.stream.next_batch(100))
+        errs = p.check_embeddings()
+        _say(f"{config}: 20 batches in {time.time() - t0:.1f}s, last |A| = {[s.size for s in sets]}, "
+             f"row-relative errors {errs}")
+        p.check_arcs()
+    finally:
+        p.close()
+
+
 def test_sparse_mid_mean_thousand_batches():
     """The 3-layer mean workload: 1000 consecutive batches of 100, affected sets
     checked every 10th batch, embeddings against full recompute after 500 and 1000."""

@@ -20,14 +20,18 @@ def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+AGGS = ["sum", "mean", "gcn", "gc_sum", "gc_mean", "gin"]
+
+
 def _small(rng, n, m, dims, agg, undirected=False, bias_std=0.1):
     src, dst = synth.erdos_renyi(n, m, rng, undirected=undirected)
     x = rng.standard_normal((n, dims[0])).astype(np.float32)
-    w = synth.model_weights(synth.ModelSpec(agg, tuple(dims)), rng, bias_std=bias_std)
+    w = synth.model_weights(synth.ModelSpec(agg, tuple(dims), gin_eps=0.2 if agg == "gin" else 0.0), rng,
+                            bias_std=bias_std)
     return src, dst, x, w
 
 
-@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
+@pytest.mark.parametrize("agg", AGGS)
 @pytest.mark.parametrize("dims", [(16, 16, 8), (5, 70, 33, 3), (100, 130, 47)])
 def test_bootstrap_matches_full_recompute(agg, dims):
     _say("bootstrap", agg, dims)
@@ -61,14 +65,14 @@ def test_tiny_config_stream(mode, inputs):
         p.close()
 
 
-@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
+@pytest.mark.parametrize("agg", AGGS)
 @pytest.mark.parametrize("undirected", [False, True])
 @pytest.mark.parametrize("mode", ["push", "pull", "dense"])
 def test_adversarial_batches(agg, undirected, mode):
     """Colliding ops: repeated inserts/deletes of one edge, insert-then-delete,
     absent deletes, self-loops, repeated feature writes (sequential semantics)."""
     _say("adversarial", agg, undirected, mode)
-    rng = np.random.default_rng(7 + 3 * ("sum", "mean", "gcn").index(agg) + undirected)
+    rng = np.random.default_rng(7 + 3 * AGGS.index(agg) + undirected)
     dims = (12, 40, 9)
     src, dst, x, w = _small(rng, 300, 1200, dims, agg, undirected)
     p = Pair(300, src, dst, x, w, undirected=undirected, mode=mode)
@@ -255,12 +259,12 @@ def test_call_order_and_device_byte_cap():
         lib.close()
 
 
-@pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
-@pytest.mark.parametrize("mode", ["auto", "pull", "dense"])
+@pytest.mark.parametrize("agg,mode", [(a, m) for a in ("sum", "mean", "gcn") for m in ("auto", "pull", "dense")]
+                         + [(a, m) for a in ("gc_sum", "gc_mean", "gin") for m in ("auto", "dense")])
 def test_thousand_batches_on_a_small_graph(agg, mode):
     """1000 consecutive batches: sets every batch, embeddings every 100 and at the end."""
     _say("1000 batches", agg, mode)
-    rng = np.random.default_rng(16 + ("sum", "mean", "gcn").index(agg))
+    rng = np.random.default_rng(16 + AGGS.index(agg))
     dims = (16, 32, 8)
     src, dst, x, w = _small(rng, 400, 2400, dims, agg)
     p = Pair(400, src, dst, x, w, mode=mode)
