@@ -43,6 +43,10 @@ design notes of the repository):
   own embedding changed is not affected at the next hop unless a neighbour is;
 * GINConv with sum (GI-S): h = sigma(MLP((1 + eps) h_self + sum)), the MLP a
   linear layer, a ReLU and a second linear layer;
+* GraphConv with weighted sum (GC-W): the arcs carry stored weights alpha_uv
+  and agg = sum_u alpha_uv h_u (Sec. II-C table; Sec. IV-C.1: each message is
+  scaled by the weight of its arc); an insert carries the new arc's weight and
+  an insert of a present arc sets its weight;
 * ReLU after every layer but the last.
 
 Arithmetic is float64 by default; the aggregation uses a scipy sparse product
@@ -67,14 +71,15 @@ OP_FEATURE = 3
 # ----------------------------------------------------------------------------
 
 # GraphSAGE (self weight + neighbour weight): "sum", "mean"; GCN: "gcn";
-# GraphConv (neighbour weight only, no self term): "gc_sum", "gc_mean";
+# GraphConv (neighbour weight only, no self term): "gc_sum", "gc_mean", and
+# "gc_wsum" (the sum weighted by the arcs' stored weights);
 # GINConv: "gin" (sum, (1 + eps) self term, two-layer MLP).
-AGGREGATORS = ("sum", "mean", "gcn", "gc_sum", "gc_mean", "gin")
+AGGREGATORS = ("sum", "mean", "gcn", "gc_sum", "gc_mean", "gin", "gc_wsum")
 
 
 def has_self_term(agg: str) -> bool:
     """Whether a vertex's own previous embedding enters its update."""
-    return agg not in ("gc_sum", "gc_mean")
+    return agg not in ("gc_sum", "gc_mean", "gc_wsum")
 
 
 @dataclasses.dataclass
@@ -115,30 +120,45 @@ class OracleModel:
 # ----------------------------------------------------------------------------
 
 class OracleGraph:
-    def __init__(self, n: int, src, dst, undirected: bool = False):
+    """Arcs as sorted keys u * n + v; on a weighted graph `w` holds each arc's
+    weight (float64, aligned with `keys`), else None."""
+
+    def __init__(self, n: int, src, dst, undirected: bool = False, weights=None):
         self.n = int(n)
         self.undirected = bool(undirected)
         src = np.asarray(src, np.int64)
         dst = np.asarray(dst, np.int64)
+        w = None if weights is None else np.asarray(weights, np.float64)
         if undirected:
             src, dst = np.concatenate([src, dst]), np.concatenate([dst, src])
+            w = None if w is None else np.concatenate([w, w])
         keys = src * self.n + dst
-        keys = keys[src != dst]
-        self.keys = np.unique(keys)
+        ok = src != dst
+        keys = keys[ok]
+        self.keys, first = np.unique(keys, return_index=True)
+        self.w = None if w is None else w[ok][first]
 
     def copy(self) -> "OracleGraph":
         g = OracleGraph.__new__(OracleGraph)
         g.n, g.undirected, g.keys = self.n, self.undirected, self.keys.copy()
+        g.w = None if self.w is None else self.w.copy()
         return g
 
     def in_sorted(self) -> Tuple[np.ndarray, np.ndarray]:
         """(sources, sinks) of all arcs ordered by sink, then source (cached)."""
+        s, d, _ = self.in_sorted_weighted()
+        return s, d
+
+    def in_sorted_weighted(self):
+        """(sources, sinks, weights or None) ordered by sink, then source (cached)."""
         cached = getattr(self, "_in_sorted", None)
         if cached is None or cached[0] is not self.keys:
-            ik = np.sort((self.keys % self.n) * self.n + self.keys // self.n)
-            cached = (self.keys, ik % self.n, ik // self.n)
+            ik = (self.keys % self.n) * self.n + self.keys // self.n
+            order = np.argsort(ik, kind="stable")
+            ik = ik[order]
+            cached = (self.keys, ik % self.n, ik // self.n, None if self.w is None else self.w[order])
             self._in_sorted = cached
-        return cached[1], cached[2]
+        return cached[1], cached[2], cached[3]
 
     @property
     def num_arcs(self) -> int:
@@ -174,6 +194,12 @@ class OracleGraph:
         starts = np.repeat(lo - (np.cumsum(cnt) - cnt), cnt)
         return self.keys[starts + np.arange(total)] % self.n
 
+    def weight_of(self, keys: np.ndarray) -> np.ndarray:
+        """Weights of present arcs given by key (1 on an unweighted graph)."""
+        if self.w is None:
+            return np.ones(np.asarray(keys).shape)
+        return self.w[np.searchsorted(self.keys, keys)]
+
     def in_adjacency(self, weights: Optional[np.ndarray] = None, dtype=np.float64) -> sp.csr_matrix:
         """Sparse A with A[v, u] = weight of arc u->v (1 by default): row v lists
         v's in-neighbours, so A @ H sums in-neighbour rows (Eq. (1))."""
@@ -198,6 +224,9 @@ class NetEffect:
     out_deg_changed: np.ndarray  # sorted vertices whose out-degree changed
     edge_keys: int             # distinct non-loop edge keys the batch touched
     noop_edge_ops: int         # self-loop edge ops + touched keys with no net change
+    rew_src: np.ndarray = dataclasses.field(default_factory=lambda: np.empty(0, np.int64))
+    rew_dst: np.ndarray = dataclasses.field(default_factory=lambda: np.empty(0, np.int64))
+    # arcs present before and after whose weight changed (weighted graphs)
 
 
 def apply_batch(graph: OracleGraph, x: np.ndarray, ops: np.ndarray,
@@ -208,14 +237,20 @@ def apply_batch(graph: OracleGraph, x: np.ndarray, ops: np.ndarray,
     An insert sets an arc present and a delete sets it absent, so the final
     state of an arc is fixed by the last op naming it; comparing with the
     pre-batch state gives the net inserts and deletes. Undirected graphs apply
-    each edge op to both arcs and count the unordered edge once."""
+    each edge op to both arcs and count the unordered edge once. On a weighted
+    graph an insert carries the arc's weight (the op's fourth field, as float32
+    bits) and also sets the weight of an arc already present, so the last op
+    fixes the weight too; an arc present before and after with another weight is
+    reweighted (its sink's neighbourhood changed)."""
     n = graph.n
-    ops = np.asarray(ops)
+    ops = np.asarray(ops, np.int32).reshape(-1, 4)
+    op_w = ops[:, 3].copy().view(np.float32).astype(np.float64)
+    weighted = graph.w is not None
     x_new = x if inplace else np.array(x, copy=True)
-    final: Dict[Tuple[int, int], bool] = {}
+    final: Dict[Tuple[int, int], Tuple[bool, float]] = {}
     feat_vertices = set()
     selfloops = 0
-    for kind, u, v, f in ops.tolist():
+    for (kind, u, v, f), wt in zip(ops.tolist(), op_w.tolist()):
         if kind == OP_FEATURE:
             x_new[u] = feat_rows[f]
             feat_vertices.add(u)
@@ -226,31 +261,52 @@ def apply_batch(graph: OracleGraph, x: np.ndarray, ops: np.ndarray,
             selfloops += 1
             continue
         key = (min(u, v), max(u, v)) if graph.undirected else (u, v)
-        final[key] = (kind == OP_INSERT)
+        final[key] = (kind == OP_INSERT, wt if weighted else 1.0)
     keys_touched = list(final.keys())
-    ins, dels = [], []
+    ins, dels, rew, ins_w, rew_w = [], [], [], [], []
     noop_keys = 0
     if keys_touched:
         arr = np.array(keys_touched, np.int64)
-        present = graph.has_arcs(arr[:, 0] * n + arr[:, 1])
-        for (a, b), was in zip(keys_touched, present.tolist()):
-            now = final[(a, b)]
+        karr = arr[:, 0] * n + arr[:, 1]
+        present = graph.has_arcs(karr)
+        old_w = np.ones(karr.size)
+        if weighted and present.any():
+            old_w[present] = graph.weight_of(karr[present])
+        for (a, b), was, ow in zip(keys_touched, present.tolist(), old_w.tolist()):
+            now, nw = final[(a, b)]
+            pairs = [(a, b), (b, a)] if graph.undirected else [(a, b)]
+            if now and was:
+                if weighted and nw != ow:
+                    rew.extend(pairs)
+                    rew_w.extend([nw] * len(pairs))
+                else:
+                    noop_keys += 1
+                continue
             if now == was:
                 noop_keys += 1
                 continue
-            pairs = [(a, b), (b, a)] if graph.undirected else [(a, b)]
             (ins if now else dels).extend(pairs)
+            if now:
+                ins_w.extend([nw] * len(pairs))
     ins = np.array(ins, np.int64).reshape(-1, 2)
     dels = np.array(dels, np.int64).reshape(-1, 2)
+    rew = np.array(rew, np.int64).reshape(-1, 2)
     g2 = graph.copy()
-    keep = g2.keys
+    keep, kw = g2.keys, g2.w
     if dels.size:
-        keep = np.delete(keep, np.searchsorted(keep, dels[:, 0] * n + dels[:, 1]))
+        at = np.searchsorted(keep, dels[:, 0] * n + dels[:, 1])
+        keep = np.delete(keep, at)
+        kw = None if kw is None else np.delete(kw, at)
+    if rew.size:
+        kw[np.searchsorted(keep, rew[:, 0] * n + rew[:, 1])] = rew_w
     if ins.size:
-        new_keys = np.sort(ins[:, 0] * n + ins[:, 1])
-        keep = np.insert(keep, np.searchsorted(keep, new_keys), new_keys)
-    g2.keys = keep
-    ch = np.concatenate([ins, dels]) if (ins.size or dels.size) else np.empty((0, 2), np.int64)
+        nk = ins[:, 0] * n + ins[:, 1]
+        order = np.argsort(nk)
+        at = np.searchsorted(keep, nk[order])
+        keep = np.insert(keep, at, nk[order])
+        kw = None if kw is None else np.insert(kw, at, np.asarray(ins_w)[order])
+    g2.keys, g2.w = keep, kw
+    ch = np.concatenate([ins, dels, rew]) if (ins.size or dels.size or rew.size) else np.empty((0, 2), np.int64)
     od_change = np.zeros(n, np.int64)
     np.add.at(od_change, ins[:, 0], 1)
     np.add.at(od_change, dels[:, 0], -1)
@@ -259,7 +315,7 @@ def apply_batch(graph: OracleGraph, x: np.ndarray, ops: np.ndarray,
         np.array(sorted(feat_vertices), np.int64),
         np.unique(ch[:, 1]), np.unique(ch[:, 0]),
         np.nonzero(od_change)[0].astype(np.int64),
-        len(keys_touched), noop_keys + selfloops)
+        len(keys_touched), noop_keys + selfloops, rew[:, 0], rew[:, 1])
     return g2, x_new, net
 
 
@@ -273,6 +329,8 @@ def aggregate(graph: OracleGraph, h: np.ndarray, agg: str) -> np.ndarray:
     h = np.asarray(h)
     if agg in ("sum", "gc_sum", "gin"):
         return graph.in_adjacency(dtype=h.dtype) @ h
+    if agg == "gc_wsum":
+        return graph.in_adjacency(graph.w, dtype=h.dtype) @ h
     if agg in ("mean", "gc_mean"):
         s = graph.in_adjacency(dtype=h.dtype) @ h
         deg = graph.in_degree()
@@ -295,7 +353,7 @@ def update(model: OracleModel, l: int, h_self: np.ndarray, agg: np.ndarray) -> n
     """Update^l then sigma (Eq. (2)) for rows with own embedding h_self and
     aggregate agg."""
     wn, b = model.w_neigh[l - 1], model.bias[l - 1]
-    if model.agg in ("gcn", "gc_sum", "gc_mean"):
+    if model.agg in ("gcn", "gc_sum", "gc_mean", "gc_wsum"):
         out = agg @ wn.T + b
     elif model.agg == "gin":
         hidden = np.maximum(((1.0 + model.gin_eps) * h_self + agg) @ wn.T + b, 0.0)
@@ -361,7 +419,7 @@ def sampled_embeddings(graph: OracleGraph, x: np.ndarray, model: OracleModel,
     Returns (sorted distinct vertices, their rows)."""
     L = model.num_layers if upto_layer is None else int(upto_layer)
     verts = np.unique(np.asarray(vertices, np.int64))
-    s_sorted, d_sorted = graph.in_sorted()
+    s_sorted, d_sorted, w_sorted = graph.in_sorted_weighted()
     dout = graph.out_degree().astype(dtype)
     din = graph.in_degree().astype(dtype)
 
@@ -372,20 +430,22 @@ def sampled_embeddings(graph: OracleGraph, x: np.ndarray, model: OracleModel,
         row_of = np.repeat(np.arange(rows.size), cnt)
         start = np.repeat(lo - np.concatenate([[0], np.cumsum(cnt)[:-1]]), cnt)
         idx = start + np.arange(int(cnt.sum()))
-        return row_of, s_sorted[idx]
+        return row_of, s_sorted[idx], (None if w_sorted is None else w_sorted[idx])
 
     m = model if dtype == np.float64 else OracleModel.from_weights(model, dtype)
     need = [None] * (L + 1)
     need[L] = verts
     for l in range(L, 0, -1):
-        _, us = in_arcs(need[l])
+        _, us, _ = in_arcs(need[l])
         need[l - 1] = np.union1d(need[l], us)
     h = np.asarray(x, dtype)[need[0]]
     for l in range(1, L + 1):
         rows, prev = need[l], need[l - 1]
-        row_of, us = in_arcs(rows)
+        row_of, us, ws = in_arcs(rows)
         col = np.searchsorted(prev, us)
-        if model.agg == "gcn":
+        if model.agg == "gc_wsum":
+            w = ws.astype(dtype)
+        elif model.agg == "gcn":
             w = 1.0 / np.sqrt((dout[us] + 1.0) * (din[rows][row_of] + 1.0))
         elif model.agg in ("mean", "gc_mean"):
             w = 1.0 / din[rows][row_of]
@@ -406,8 +466,8 @@ def sampled_embeddings(graph: OracleGraph, x: np.ndarray, model: OracleModel,
 class OracleState:
     """Graph + features + model; applies batches and recomputes on demand."""
 
-    def __init__(self, n, src, dst, x, model: OracleModel, undirected=False):
-        self.graph = OracleGraph(n, src, dst, undirected)
+    def __init__(self, n, src, dst, x, model: OracleModel, undirected=False, weights=None):
+        self.graph = OracleGraph(n, src, dst, undirected, weights)
         self.x = np.asarray(x, np.float64).copy()
         self.model = model
 

@@ -11,9 +11,11 @@ Table "Graph datasets used in experiments"), which are not available here:
 * ``sparse_mid``      directed Chung-Lu power law (exponent 2.1) shaped like
                       ogbn-arxiv: 169,343 vertices, 1,166,243 arcs, 128 features.
 * ``sparse_mid_mean`` the same graph with a 3-layer GraphSAGE-mean model.
-* ``sparse_mid_gc_sum``, ``sparse_mid_gc_mean``, ``sparse_mid_gin``  the same
-                      graph with the evaluation's GraphConv-sum, GraphConv-mean
-                      and GIN-sum workloads (2 layers, 128-256-40).
+* ``sparse_mid_gc_sum``, ``sparse_mid_gc_mean``, ``sparse_mid_gin``,
+  ``sparse_mid_gc_wsum``  the same graph with the evaluation's GraphConv-sum,
+                      GraphConv-mean, GIN-sum and GraphConv-weighted-sum workloads
+                      (2 layers, 128-256-40; the last on arcs weighted uniformly in
+                      [0.5, 1.5), inserts carrying their weights).
 * ``dense_large``     undirected Chung-Lu (exponent 2.1) shaped like
                       ogbn-products: 2,449,029 vertices, 61,859,140 edges, 100 features.
 * ``dense_large_2l``  the same graph with a 2-layer model (the paper's 2-layer
@@ -47,6 +49,7 @@ AGG_GCN = "gcn"
 AGG_GC_SUM = "gc_sum"    # GraphConv, sum aggregator (no self term)
 AGG_GC_MEAN = "gc_mean"  # GraphConv, mean aggregator (no self term)
 AGG_GIN = "gin"          # GINConv, sum aggregator, two-layer MLP
+AGG_GC_WSUM = "gc_wsum"  # GraphConv, sum weighted by stored arc weights (no self term)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -58,6 +61,7 @@ class GraphSpec:
     gamma: float = 2.1        # power-law exponent (chung_lu)
     rmat: Tuple[float, float, float, float] = (0.57, 0.19, 0.19, 0.05)
     holdout: float = 0.10     # extra edges drawn and held out as the insert pool
+    weighted: bool = False    # arcs carry weights, uniform in [0.5, 1.5) (inserts too)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -113,6 +117,11 @@ CONFIGS: Dict[str, WorkloadSpec] = {
         GraphSpec("chung_lu", 169_343, 1_166_243),
         ModelSpec(AGG_GC_MEAN, (128, 256, 40)),
         StreamSpec((1, 10, 100, 1000), (1 / 3, 1 / 3, 1 / 3))),
+    "sparse_mid_gc_wsum": WorkloadSpec(
+        "sparse_mid_gc_wsum",
+        GraphSpec("chung_lu", 169_343, 1_166_243, weighted=True),
+        ModelSpec(AGG_GC_WSUM, (128, 256, 40)),
+        StreamSpec((1, 10, 100, 1000), (1 / 3, 1 / 3, 1 / 3))),
     "sparse_mid_gin": WorkloadSpec(
         "sparse_mid_gin",
         GraphSpec("chung_lu", 169_343, 1_166_243),
@@ -139,6 +148,21 @@ CONFIGS: Dict[str, WorkloadSpec] = {
 def seeds(seed: int) -> List[np.random.Generator]:
     """Four independent generators: graph, features, weights, stream."""
     return [np.random.default_rng(s) for s in np.random.SeedSequence(seed).spawn(4)]
+
+
+def edge_weights_rng(seed: int) -> np.random.Generator:
+    """A fifth independent generator, for arc weights (the first four of the same
+    spawn are those of seeds(), so unweighted workloads are unchanged)."""
+    return np.random.default_rng(np.random.SeedSequence(seed).spawn(5)[4])
+
+
+def arc_weights(rng: np.random.Generator, count: int) -> np.ndarray:
+    return rng.uniform(0.5, 1.5, count).astype(np.float32)
+
+
+def weight_bits(w) -> np.ndarray:
+    """Float32 weights as the int32 bit patterns an insert op carries in its fourth field."""
+    return np.ascontiguousarray(np.asarray(w, np.float32)).view(np.int32)
 
 
 # ----------------------------------------------------------------------------
@@ -363,7 +387,7 @@ def model_weights(spec: ModelSpec, rng: np.random.Generator, bias_std: float = 0
 
     for l in range(1, L + 1):
         din, dout = spec.dims[l - 1], spec.dims[l]
-        if spec.agg in (AGG_GCN, AGG_GC_SUM, AGG_GC_MEAN, AGG_GIN):
+        if spec.agg in (AGG_GCN, AGG_GC_SUM, AGG_GC_MEAN, AGG_GC_WSUM, AGG_GIN):
             ws.append(None)
         else:
             ws.append(glorot(rng, dout, din))
@@ -396,8 +420,9 @@ class UpdateStream:
     updates pick uniform vertices with fresh N(0,1) rows. Every op is effective."""
 
     def __init__(self, n: int, d0: int, snap_src, snap_dst, pool_src, pool_dst,
-                 spec: StreamSpec, rng: np.random.Generator, out_deg=None, in_deg=None):
+                 spec: StreamSpec, rng: np.random.Generator, out_deg=None, in_deg=None, pool_w=None):
         self.n, self.d0, self.spec, self.rng = n, d0, spec, rng
+        self.pool_w = pool_w  # weighted graphs: each pool edge's weight
         self.snap_src, self.snap_dst = snap_src, snap_dst
         self.pool_src, self.pool_dst = pool_src, pool_dst
         self._del_order = rng.permutation(snap_src.size)
@@ -452,6 +477,8 @@ class UpdateStream:
                     j = self._ins_next
                     self._ins_next += 1
                     ops[i, 1], ops[i, 2] = self.pool_src[j], self.pool_dst[j]
+                    if self.pool_w is not None:
+                        ops[i, 3] = weight_bits(self.pool_w[j : j + 1])[0]
             elif k == OP_DELETE:
                 if self._del_next >= self._del_order.size:
                     raise RuntimeError("delete pool exhausted")
@@ -470,11 +497,12 @@ class UpdateStream:
 
 def adversarial_batch(rng: np.random.Generator, n: int, d0: int, bs: int,
                       hot: int = 12, existing: Optional[Tuple[np.ndarray, np.ndarray]] = None,
-                      p_selfloop: float = 0.05) -> Batch:
+                      p_selfloop: float = 0.05, weighted: bool = False) -> Batch:
     """A batch designed to collide: ops mostly touch a small hot vertex set, so it
     holds repeated inserts/deletes of one edge, insert-then-delete, deletes of
     absent edges, self-loops and repeated feature writes. Sequential semantics
-    decide the outcome."""
+    decide the outcome. weighted: inserts carry weights from a few values, so
+    inserts of present arcs sometimes keep and sometimes change their weight."""
     hot_set = rng.choice(n, size=min(hot, n), replace=False)
     ops = np.full((bs, 4), -1, np.int32)
     nfeat = 0
@@ -501,7 +529,12 @@ def adversarial_batch(rng: np.random.Generator, n: int, d0: int, bs: int,
             u, v = int(rng.choice(hot_set)), int(rng.choice(hot_set))
             if rng.random() < 0.3:
                 v = int(rng.integers(0, n))
+        if kind == OP_INSERT and existing is not None and existing[0].size and rng.random() < 0.25:
+            j = rng.integers(0, existing[0].size)  # an arc that may be present: a weight update
+            u, v = int(existing[0][j]), int(existing[1][j])
         ops[i, 1], ops[i, 2] = u, v
+        if weighted and kind == OP_INSERT:
+            ops[i, 3] = weight_bits([rng.choice([0.5, 1.0, 1.25])])[0]
     feat_rows = rng.standard_normal((nfeat, d0), dtype=np.float32)
     return Batch(ops, feat_rows)
 
@@ -520,6 +553,7 @@ class Workload:
     x: np.ndarray
     weights: ModelWeights
     stream: UpdateStream
+    edge_w: Optional[np.ndarray] = None   # weighted graphs: float32 weight per snapshot edge
 
     @property
     def n(self) -> int:
@@ -543,6 +577,11 @@ def build_workload(name_or_spec, seed: Optional[int] = None, bias_std: float = 0
         in_deg = np.bincount(dst, minlength=spec.graph.n)
         if spec.graph.undirected:
             out_deg = in_deg = out_deg + in_deg
+    edge_w = pool_w = None
+    if spec.graph.weighted:
+        e_rng = edge_weights_rng(spec.seed)
+        edge_w = arc_weights(e_rng, src.size)
+        pool_w = arc_weights(e_rng, psrc.size)
     stream = UpdateStream(spec.graph.n, spec.model.dims[0], src, dst, psrc, pdst,
-                          spec.stream, s_rng, out_deg, in_deg)
-    return Workload(spec, src, dst, psrc, pdst, x, w, stream)
+                          spec.stream, s_rng, out_deg, in_deg, pool_w)
+    return Workload(spec, src, dst, psrc, pdst, x, w, stream, edge_w)

@@ -50,12 +50,12 @@ def _eval_expr(s):
 # ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("case", ["sage_sum_2layer", "sage_mean_1layer", "gcn_directed_1layer", "gc_sum_2layer",
-                                  "gc_mean_1layer", "gin_1layer"])
+                                  "gc_mean_1layer", "gin_1layer", "gc_wsum_1layer"])
 def test_hand_derived_values(case):
     fx = json.load(open(os.path.join(GOLDEN, "hand_small_graph.json")))
     arcs = np.array(fx["arcs"])
     c = fx["cases"][case]
-    g = O.OracleGraph(fx["n"], arcs[:, 0], arcs[:, 1])
+    g = O.OracleGraph(fx["n"], arcs[:, 0], arcs[:, 1], weights=c.get("arc_weights"))
     m = _model(c["agg"], c["w_self"], c["w_neigh"], c["bias"], c["relu"], c.get("w_out", ()),
                c.get("b_out", ()), c.get("gin_eps", 0.0))
     hs = O.full_recompute(g, np.array(fx["x"], np.float64), m)
@@ -167,7 +167,11 @@ def _changed_rows(h_pre, h_post):
     return np.nonzero(np.any(h_pre != h_post, axis=1))[0]
 
 
-@pytest.mark.parametrize("agg", ["sum", "mean", "gcn", "gc_sum", "gc_mean"])
+def _weights_for(agg, rng, m):
+    return rng.uniform(0.5, 1.5, m).astype(np.float32) if agg == "gc_wsum" else None
+
+
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn", "gc_sum", "gc_mean", "gc_wsum"])
 @pytest.mark.parametrize("undirected", [False, True])
 def test_affected_sets_equal_changed_rows_without_activation(agg, undirected):
     """With no activation and generic values, a vertex's embedding changes iff it
@@ -180,11 +184,12 @@ def test_affected_sets_equal_changed_rows_without_activation(agg, undirected):
     for trial in range(12):
         src, dst = synth.erdos_renyi(n, 45 if undirected else 70, rng, undirected=undirected)
         st = O.OracleState(n, src, dst, rng.standard_normal((n, dims[0])),
-                           _random_model(rng, agg, dims, relu_none=True), undirected)
+                           _random_model(rng, agg, dims, relu_none=True), undirected,
+                           _weights_for(agg, rng, src.size))
         pre = st.embeddings()
         a, b = st.graph.arcs()
         batch = synth.adversarial_batch(rng, n, dims[0], bs=int(rng.integers(1, 10)),
-                                        hot=6, existing=(a, b))
+                                        hot=6, existing=(a, b), weighted=agg == "gc_wsum")
         net, sets = st.apply(batch.ops, batch.feat_rows)
         post = st.embeddings()
         for l in range(1, L + 1):
@@ -192,17 +197,17 @@ def test_affected_sets_equal_changed_rows_without_activation(agg, undirected):
                                           err_msg=f"trial {trial} layer {l}")
 
 
-@pytest.mark.parametrize("agg", ["sum", "mean", "gcn", "gc_sum", "gc_mean", "gin"])
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn", "gc_sum", "gc_mean", "gin", "gc_wsum"])
 def test_changed_rows_within_affected_sets_with_relu(agg):
     rng = np.random.default_rng(30)
     n, dims = 40, (4, 5, 3)
     for _ in range(8):
         src, dst = synth.erdos_renyi(n, 90, rng)
         st = O.OracleState(n, src, dst, rng.standard_normal((n, dims[0])),
-                           _random_model(rng, agg, dims, relu_all=True))
+                           _random_model(rng, agg, dims, relu_all=True), weights=_weights_for(agg, rng, src.size))
         pre = st.embeddings()
         a, b = st.graph.arcs()
-        batch = synth.adversarial_batch(rng, n, dims[0], bs=8, hot=8, existing=(a, b))
+        batch = synth.adversarial_batch(rng, n, dims[0], bs=8, hot=8, existing=(a, b), weighted=agg == "gc_wsum")
         _, sets = st.apply(batch.ops, batch.feat_rows)
         post = st.embeddings()
         for l in range(1, 3):
@@ -327,12 +332,12 @@ def test_permutation_equivariance():
             np.testing.assert_allclose(hp[l][perm], h[l], rtol=1e-12, atol=1e-12)
 
 
-@pytest.mark.parametrize("agg", ["sum", "mean", "gcn", "gc_sum", "gc_mean", "gin"])
+@pytest.mark.parametrize("agg", ["sum", "mean", "gcn", "gc_sum", "gc_mean", "gin", "gc_wsum"])
 def test_sampled_embeddings_match_full_recompute(agg):
     rng = np.random.default_rng(70)
     n, dims = 200, (4, 6, 5, 3)
     src, dst = synth.erdos_renyi(n, 900, rng)
-    g = O.OracleGraph(n, src, dst)
+    g = O.OracleGraph(n, src, dst, weights=_weights_for(agg, rng, src.size))
     x = rng.standard_normal((n, 4))
     m = _random_model(rng, agg, dims)
     full = O.full_recompute(g, x, m)
@@ -396,3 +401,96 @@ def test_gin_matches_a_per_vertex_loop():
                 out[v, j] = max(y, 0.0) if m.relu[l - 1] else y
         np.testing.assert_allclose(hs[l], out, rtol=1e-12, atol=1e-12)
         h = out
+
+
+# ---------------------------------------------------------------------------
+# weighted graphs (GC-W)
+# ---------------------------------------------------------------------------
+
+def _brute_apply_weighted(n, arcs, x, ops, rows, undirected):
+    """Op-by-op on a dict arc -> weight: an insert sets the arc present with the
+    op's weight (also when present), a delete removes it."""
+    arcs = dict(arcs)
+    x = x.copy()
+    wts = np.asarray(ops, np.int32)[:, 3].copy().view(np.float32)
+    for (kind, u, v, f), w in zip(np.asarray(ops).tolist(), wts.tolist()):
+        if kind == O.OP_FEATURE:
+            x[u] = rows[f]
+            continue
+        if u == v:
+            continue
+        for p in ([(u, v), (v, u)] if undirected else [(u, v)]):
+            if kind == O.OP_INSERT:
+                arcs[p] = w
+            else:
+                arcs.pop(p, None)
+    return arcs, x
+
+
+@pytest.mark.parametrize("undirected", [False, True])
+def test_weighted_batch_equals_op_by_op_application(undirected):
+    """Weights follow the same sequential semantics: the last insert of an arc
+    sets its weight; the net effect splits into inserts, deletes and reweights."""
+    rng = np.random.default_rng(90 + undirected)
+    n, d = 25, 3
+    for _ in range(20):
+        src, dst = synth.erdos_renyi(n, 40, rng, undirected=undirected)
+        w = rng.uniform(0.5, 1.5, src.size).astype(np.float32)
+        g = O.OracleGraph(n, src, dst, undirected, w)
+        x = rng.standard_normal((n, d))
+        a, b = g.arcs()
+        batch = synth.adversarial_batch(rng, n, d, bs=15, hot=5, existing=(a, b), weighted=True)
+        g2, x2, net = O.apply_batch(g, x, batch.ops, batch.feat_rows)
+        pre = {(u, v): float(wt) for u, v, wt in zip(a.tolist(), b.tolist(), g.w.tolist())}
+        want, want_x = _brute_apply_weighted(n, pre, x, batch.ops, batch.feat_rows, undirected)
+        u2, v2 = g2.arcs()
+        got = {(u, v): float(wt) for u, v, wt in zip(u2.tolist(), v2.tolist(), g2.w.tolist())}
+        assert got == want
+        np.testing.assert_array_equal(x2, want_x)
+        rew = set(zip(net.rew_src.tolist(), net.rew_dst.tolist()))
+        assert rew == {k for k in set(pre) & set(got) if pre[k] != got[k]}
+        assert set(zip(net.ins_src.tolist(), net.ins_dst.tolist())) == set(got) - set(pre)
+        assert set(zip(net.del_src.tolist(), net.del_dst.tolist())) == set(pre) - set(got)
+        for u, v in rew:
+            assert v in net.heads
+
+
+def test_weighted_sum_with_unit_weights_is_graphconv_sum():
+    rng = np.random.default_rng(91)
+    n, dims = 50, (4, 6, 3)
+    src, dst = synth.erdos_renyi(n, 180, rng)
+    x = rng.standard_normal((n, dims[0]))
+    m = _random_model(rng, "gc_wsum", dims)
+    unit = O.full_recompute(O.OracleGraph(n, src, dst, weights=np.ones(src.size)), x, m)
+    m.agg = "gc_sum"
+    plain = O.full_recompute(O.OracleGraph(n, src, dst), x, m)
+    for a, b in zip(unit, plain):
+        np.testing.assert_allclose(a, b, rtol=1e-13, atol=1e-13)
+
+
+def test_weighted_sum_matches_a_per_vertex_loop():
+    rng = np.random.default_rng(92)
+    n, dims = 20, (3, 2)
+    src, dst = synth.erdos_renyi(n, 60, rng)
+    w = rng.uniform(0.5, 1.5, src.size)
+    g = O.OracleGraph(n, src, dst, weights=w)
+    x = rng.standard_normal((n, dims[0]))
+    m = _random_model(rng, "gc_wsum", dims)
+    h1 = O.full_recompute(g, x, m)[1]
+    for v in range(n):
+        agg = np.zeros(dims[0])
+        for u, t, wt in zip(src.tolist(), dst.tolist(), w.tolist()):
+            if t == v:
+                agg = agg + wt * x[u]
+        np.testing.assert_allclose(h1[v], m.w_neigh[0] @ agg + m.bias[0], rtol=1e-12, atol=1e-12)
+
+
+def test_reinserting_a_present_arc_with_its_own_weight_is_a_noop():
+    g = O.OracleGraph(3, [0, 1], [1, 2], weights=[0.75, 1.25])
+    ops = np.array([[O.OP_INSERT, 0, 1, 0], [O.OP_INSERT, 1, 2, 0]], np.int32)
+    ops[:, 3] = synth.weight_bits([0.75, 2.0])
+    g2, _, net = O.apply_batch(g, np.zeros((3, 1)), ops, np.zeros((0, 1)))
+    assert net.noop_edge_ops == 1 and net.edge_keys == 2
+    np.testing.assert_array_equal(net.rew_src, [1])
+    np.testing.assert_array_equal(net.heads, [2])
+    np.testing.assert_array_equal(g2.w, [0.75, 2.0])
