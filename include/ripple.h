@@ -29,6 +29,9 @@
  *                    changed in-neighbour or arc
  *   RIPPLE_AGG_GIN   GINConv with sum (GI-S): h = sigma(W2 ReLU(W1 ((1 + eps) h_v
  *                    + sum_u h_u) + b1) + b2)
+ *   RIPPLE_AGG_GC_WSUM  GraphConv with weighted sum (GC-W): h = sigma(W sum_u
+ *                    alpha_uv h_u + b), alpha_uv the arc's stored weight (each
+ *                    message is scaled by the weight of its arc, Sec. IV-C.1)
  *
  * Graph semantics: a simple directed graph on vertices 0..n-1 (int32 ids).
  * Inserting a present arc, deleting an absent arc, and inserting or deleting a
@@ -87,7 +90,8 @@ typedef enum {
   RIPPLE_AGG_GCN = 2,     /* GCN, symmetric normalisation, implicit self-loop */
   RIPPLE_AGG_GC_SUM = 3,  /* GraphConv-sum (no self term) */
   RIPPLE_AGG_GC_MEAN = 4, /* GraphConv-mean (no self term) */
-  RIPPLE_AGG_GIN = 5      /* GINConv-sum with a two-layer MLP */
+  RIPPLE_AGG_GIN = 5,     /* GINConv-sum with a two-layer MLP */
+  RIPPLE_AGG_GC_WSUM = 6  /* GraphConv with the arcs' stored weights (a graph loaded with weights) */
 } ripple_agg;
 
 typedef enum { RIPPLE_GEMM_FP32 = 0, RIPPLE_GEMM_BF16 = 1 } ripple_gemm_prec;
@@ -96,12 +100,18 @@ enum { RIPPLE_OP_INSERT = 1, RIPPLE_OP_DELETE = 2, RIPPLE_OP_FEATURE = 3 };
 
 /* One update (16 bytes). Edge ops: (kind, u, v, -1). Feature replacement:
  * (RIPPLE_OP_FEATURE, u, -1, feat_row): vertex u's features become row feat_row
- * of the batch's feature block. */
+ * of the batch's feature block. On a graph loaded with weights an insert carries
+ * the arc's weight in the last field, (RIPPLE_OP_INSERT, u, v, weight), and an
+ * insert of a present arc sets its weight (the last op on an arc fixes both its
+ * presence and its weight; an unchanged weight is a no-op). */
 typedef struct {
   int32_t kind;
   int32_t u;
   int32_t v;
-  int32_t feat_row;
+  union {
+    int32_t feat_row;  /* feature ops */
+    float weight;      /* inserts on a weighted graph (finite) */
+  };
 } ripple_op;
 
 /* Graph snapshot (Sec. IV-A: the graph before any update arrives). */
@@ -120,6 +130,9 @@ typedef struct {
                              0 = max(65536, half the laid-out slots). When the arena runs out,
                              the direction is re-laid out (on the device if the fresh layout
                              leaves a quarter of its buffer free, else into larger buffers). */
+  const float *weight;    /* [num_edges] arc weights (finite; an undirected edge's weight is both
+                             arcs'), or NULL for an unweighted graph. Only RIPPLE_AGG_GC_WSUM uses
+                             them; host memory, copied. */
 } ripple_graph_desc;
 
 /* Trained model (Sec. IV-A: a trained L-layer GNN with a linear aggregator). */
@@ -163,6 +176,7 @@ typedef struct {
   int64_t in_arcs[RIPPLE_MAX_LAYERS + 1];   /* [l]: in-arcs of A^l (the pull form's work) */
   int32_t pull_layers;          /* bit l set: layer l pulled over the in-arcs of A^l */
   int32_t dense_layers;         /* bit l set: layer l pulled over every in-arc of the graph */
+  int64_t reweighted_arcs;      /* weighted graphs: arcs present before and after whose weight changed */
 } ripple_batch_stats;
 
 /* Part 1 of the problem statement: copies the snapshot to the device as an
@@ -228,6 +242,12 @@ RIPPLE_API ripple_status ripple_get_aggregates(ripple_ctx *ctx, int32_t layer, c
  * Writes min(arcs, capacity) pairs and the arc count to *count (always). */
 RIPPLE_API ripple_status ripple_get_arcs(ripple_ctx *ctx, int32_t direction, int32_t *src, int32_t *dst,
                               int64_t capacity, int64_t *count);
+
+/* Weighted graphs: the arcs' weights in the order ripple_get_arcs lists them
+ * (same direction); *count always receives the arc count. RIPPLE_E_INVALID on an
+ * unweighted graph. */
+RIPPLE_API ripple_status ripple_get_arc_weights(ripple_ctx *ctx, int32_t direction, float *weights, int64_t capacity,
+                                                int64_t *count);
 
 /* How each layer adds its messages to the cached aggregate (results agree up to
  * rounding): RIPPLE_SCATTER_PUSH, one row of fp32 atomics per pushed arc;

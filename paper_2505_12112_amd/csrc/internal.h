@@ -44,6 +44,7 @@ struct Counters {
   u64 indeg[kMaxL + 1];   // [l] = sum of in-degrees over A^l (pull work), when computed
   u64 count_all;          // vertices listed by a full compaction (dense layers)
   u64 bad_op;             // B - i for the first op i that failed the device-side check, else 0
+  u64 n_rew;              // reweighted arcs (weighted graphs; each also counted in n_ins and n_del)
   u64 zero;               // never written: an arc count of zero for kernels that only mark
 };
 
@@ -57,6 +58,7 @@ struct Adj {
   int *len;
   int *cap;
   int *col;
+  float *wt;              // weighted graphs: the weight of the arc in each slot of col; else nullptr
   int *inscnt;            // per-row scratch, zero between batches
   int *delcnt;
 };
@@ -73,8 +75,9 @@ struct LayerPtrs {
 
 // Same values as ripple_agg. GraphConv (kGcSum, kGcMean) has no self term; GIN's
 // update is a two-layer MLP on (1 + eps) h_v + S_v.
-enum Agg { kSum = 0, kMean = 1, kGcn = 2, kGcSum = 3, kGcMean = 4, kGin = 5 };
-inline bool has_self_term(int agg) { return agg != kGcSum && agg != kGcMean; }
+// kGcWsum: GraphConv with the arcs' stored weights (weighted graphs).
+enum Agg { kSum = 0, kMean = 1, kGcn = 2, kGcSum = 3, kGcMean = 4, kGin = 5, kGcWsum = 6 };
+inline bool has_self_term(int agg) { return agg != kGcSum && agg != kGcMean && agg != kGcWsum; }
 
 // --- launchers (each defined in the translation unit that holds its kernel) ---
 
@@ -82,15 +85,18 @@ inline bool has_self_term(int agg) { return agg != kGcSum && agg != kGcMean; }
 // knows its rank among the row's inserts (ins_rank) or deletes (del_rank); the
 // hash slot of every named edge holds +1 (net insert), -1 (net delete) or 0.
 // src_ops: the batch in pinned host or device memory; copied to ops (device) on the
-// way and checked (ids and feature rows in range, known kind): a failing op sets
-// bad_op and abort, and is copied as a self-loop no-op.
+// way and checked (ids and feature rows in range, known kind, finite insert weights
+// on a weighted graph): a failing op sets bad_op and abort, and is copied as a
+// self-loop no-op. On a weighted graph (out.wt set) an insert of a present arc
+// with another weight is a reweight: listed as a delete (old weight, del_w) and an
+// insert (new weight, ins_w) of the same arc, counted in n_rew.
 void launch_net_hash(hipStream_t s, const ripple_op *src_ops, ripple_op *ops, int B, long long num_feat_rows,
-                     int undirected, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop,
-                     Counters *c);
+                     int undirected, int weighted, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot,
+                     int *fop, Counters *c);
 void launch_net_decide(hipStream_t s, const ripple_op *ops, int B, int undirected, const int *ht_val,
                        int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src,
-                       int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank, int *flist,
-                       Counters *c);
+                       int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w,
+                       float *del_w, int *flist, Counters *c);
 
 // topology (cap_arcs bounds n_ins and n_del): plan row moves and check the arena
 // (aborting before any mutation), then one owner wave per touched row removes its
@@ -103,7 +109,7 @@ void launch_topo_rewrite(hipStream_t s, int cap_arcs, int undirected, long long 
                          const int *ins_rank, const int *del_rank, const u64 *ht_key, const int *ht_net,
                          unsigned mask, Persist *p, int *ddeg, Counters *c);
 void launch_topo_put(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                     const int *ins_rank, Counters *c);
+                     const int *ins_rank, const float *ins_w, Counters *c);
 // Also copies *c to host (pinned) and zeroes *next (the other counter buffer).
 void launch_cleanup(hipStream_t s, int B, int cap_arcs, const ripple_op *ops, const int *op_slot,
                     u64 *ht_key, int *ht_val, int *ht_net, int *fop, Adj out, Adj in, const int *ins_src,
@@ -115,9 +121,11 @@ void launch_cleanup(hipStream_t s, int B, int cap_arcs, const ripple_op *ops, co
 // after the adjacency update, with pre-batch coefficients recovered from ddeg;
 // the same kernel marks the layer-1 dirty set (feature writes; GCN: vertices whose
 // out-degree changed).
+// ins_w / del_w (nullable): the arcs' weights (weighted graphs).
 void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerPtrs lp, const int *out_len,
                       const int *ddeg, const int *flist, const int *ins_src, const int *ins_dst,
-                      const int *del_src, const int *del_dst, unsigned *bm, Counters *c);
+                      const int *del_src, const int *del_dst, const float *ins_w, const float *del_w, unsigned *bm,
+                      Counters *c);
 int compact_blocks(long long n);
 // Outputs of one compaction of bitmaps (a | b) into an ascending list. Optional
 // (nullptr = skipped): list, doff[j] = sum of out_deg over list[0..j) (doff[count]
@@ -229,8 +237,9 @@ struct GemmArgs {
 void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows, long long expected_rows);
 
 // re-layout of one adjacency direction
+// old_wt / new_wt (nullable): the slots' weights move with them.
 void launch_repack_copy(hipStream_t s, long long n, const int *old_col, const long long *old_off, const int *len,
-                        int *new_col, const long long *new_off);
+                        int *new_col, const long long *new_off, const float *old_wt, float *new_wt);
 
 // Device-side re-layout of one direction. relayout_sums leaves in blocksums[nb]
 // (nb = relayout_blocks(n)) the total slots a fresh layout needs (len + spare
@@ -242,7 +251,7 @@ int relayout_blocks(long long n);
 void launch_relayout_sums(hipStream_t s, long long n, float slack, int min_slack, const int *len,
                           long long *blocksums);
 void launch_relayout_apply(hipStream_t s, long long n, float slack, int min_slack, Adj a, int *new_col,
-                           const long long *blocksums, long long *new_off, int *new_cap, u64 *top);
+                           float *new_wt, const long long *blocksums, long long *new_off, int *new_cap, u64 *top);
 
 // utilities
 void launch_fill_i32(hipStream_t s, int *p, long long count, int value);

@@ -43,7 +43,7 @@ inline int blocks_for(long long items, int threads, int cap = 4096) {
 // Pre-batch corrections and the layer-1 dirty marks (see launch_corr_mark).
 __global__ void k_corr_mark(int agg, LayerPtrs lp, const int *out_len, const int *ddeg, const int *flist,
                             const int *ins_src, const int *ins_dst, const int *del_src, const int *del_dst,
-                            unsigned *bm, Counters *c) {
+                            const float *ins_w, const float *del_w, unsigned *bm, Counters *c) {
   if (c->abort) return;
   const int lane = lane_id();
   const long long nf = static_cast<long long>(c->n_feat);
@@ -58,6 +58,7 @@ __global__ void k_corr_mark(int agg, LayerPtrs lp, const int *out_len, const int
     const int v = ins ? ins_dst[arc] : del_dst[arc - ni];
     float coef = ins ? 1.0f : -1.0f;
     if (agg == kGcn) coef *= 1.0f / sqrtf(static_cast<float>(out_len[u] - ddeg[u]) + 1.0f);
+    if (ins_w != nullptr) coef *= ins ? ins_w[arc] : del_w[arc - ni];  // the arc's weight
     const int d = lp.sw[l];
     const float *hu = lp.src[l] + static_cast<long long>(u) * d;
     float *sv = lp.S[l] + static_cast<long long>(v) * d;
@@ -494,15 +495,19 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
       }
     }
     int v = -1;
+    float wv = 1.0f;  // the arc's weight (weighted graphs)
     if (active) {
       const int u = list[j];
-      v = out.col[out.off[u] + (e - doff[j])];
+      const long long slot = out.off[u] + (e - doff[j]);
+      v = out.col[slot];
+      if (PUSH && out.wt != nullptr) wv = out.wt[slot];
     }
     if (v >= 0) mark_only(bm_out, v);
     const int cnt = PUSH ? static_cast<int>(elast - e0 + 1) : 0;
     for (int i = 0; i < cnt; i += kEdgesPerStep) {
       const int vv = __shfl(v, i + grp);
       const int jj = __shfl(j, i + grp);
+      const float ww = __shfl(wv, i + grp);
       if (vv >= 0) {
         if (jj != cached) {
           const float *dj = delta + static_cast<long long>(jj) * ld;
@@ -517,7 +522,7 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
 #pragma unroll
         for (int q = 0; q < NC; ++q) {
           const int k = k0 + q * G;
-          if (k < d) unsafeAtomicAdd(&sv[k], dreg[q]);
+          if (k < d) unsafeAtomicAdd(&sv[k], ww * dreg[q]);
         }
       }
     }
@@ -546,10 +551,13 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
                                                    const int *wprefix, const float *msg, float *S, unsigned *mark,
                                                    const Counters *c) {
   __shared__ int2 pairs[256 / kWave][kPullChunk];
+  __shared__ float pair_w[256 / kWave][kPullChunk];  // the in-arcs' weights (weighted graphs)
   if (c->abort) return;
   const int lane = lane_id();
   const int grp = lane / G, k0 = lane % G;
   int2 *wp = pairs[threadIdx.x / kWave];
+  float *ww = pair_w[threadIdx.x / kWave];
+  const bool weighted = in.wt != nullptr;
   const long long nA = static_cast<long long>(*count);
   const long long E = ioff[nA];
   const long long waves = num_waves();
@@ -594,14 +602,18 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
       }
     }
     int v[kPullArcs], u[kPullArcs];
+    float w[kPullArcs];
 #pragma unroll
     for (int a = 0; a < kPullArcs; ++a) {
       const bool active = a < per_lane && e[a] <= elast;
       v[a] = active ? (list != nullptr ? list[r[a]] : r[a]) : -1;
     }
 #pragma unroll
-    for (int a = 0; a < kPullArcs; ++a)
-      u[a] = v[a] >= 0 ? __builtin_nontemporal_load(in.col + in.off[v[a]] + (e[a] - ioff[r[a]])) : -1;
+    for (int a = 0; a < kPullArcs; ++a) {
+      const long long slot = v[a] >= 0 ? in.off[v[a]] + (e[a] - ioff[r[a]]) : 0;
+      u[a] = v[a] >= 0 ? __builtin_nontemporal_load(in.col + slot) : -1;
+      w[a] = weighted && v[a] >= 0 ? __builtin_nontemporal_load(in.wt + slot) : 1.0f;
+    }
 #pragma unroll
     for (int a = 0; a < kPullArcs; ++a) {
       int j = -1;
@@ -611,7 +623,10 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
         const unsigned bit = 1u << (u[a] & 31);
         if (word & bit) j = below + __popc(word & (bit - 1u));
       }
-      if (a < per_lane) wp[lane * per_lane + a] = make_int2(v[a], j);
+      if (a < per_lane) {
+        wp[lane * per_lane + a] = make_int2(v[a], j);
+        if (weighted) ww[lane * per_lane + a] = w[a];
+      }
     }
     // the pairs are read back by other lanes of this wave only
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -624,13 +639,19 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
     const int base = grp * window;
     for (int t0 = 0; t0 < window; t0 += U) {  // trip count is the same for the whole wave
       int vv[U], jj[U];
+      float wt[U];
 #pragma unroll
       for (int t = 0; t < U; ++t) {
         const int pos = t0 + t;
         int2 pr = make_int2(-1, -1);
-        if (pos < window && base + pos < C) pr = wp[base + pos];
+        float pw = 1.0f;
+        if (pos < window && base + pos < C) {
+          pr = wp[base + pos];
+          if (weighted) pw = ww[base + pos];
+        }
         vv[t] = pr.x;
         jj[t] = pr.y;
+        wt[t] = pw;
       }
       float row[U][NC];
 #pragma unroll
@@ -659,7 +680,7 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
           cur = vv[t];
         }
 #pragma unroll
-        for (int q = 0; q < NC; ++q) acc[q] += row[t][q];
+        for (int q = 0; q < NC; ++q) acc[q] += wt[t] * row[t][q];
       }
     }
     if (cur >= 0) {
@@ -695,6 +716,7 @@ __global__ __launch_bounds__(256) void k_pull(long long n, int d, int agg, const
       const int uid = e < deg ? row[e] : 0;
       float cu = 1.0f;
       if (agg == kGcn && e < deg) cu = 1.0f / sqrtf(static_cast<float>(out_len[uid]) + 1.0f);
+      if (in.wt != nullptr && e < deg) cu *= in.wt[in.off[v] + e];  // the arc's weight
       const int cnt = deg - e0 < kWave ? deg - e0 : kWave;
       for (int i = 0; i < cnt; ++i) {
         const int u = __shfl(uid, i);
@@ -740,12 +762,12 @@ __global__ void k_gather_rows(const float *src, int d, const int *ids, long long
 
 void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerPtrs lp, const int *out_len,
                       const int *ddeg, const int *flist, const int *ins_src, const int *ins_dst, const int *del_src,
-                      const int *del_dst, unsigned *bm, Counters *c) {
+                      const int *del_dst, const float *ins_w, const float *del_w, unsigned *bm, Counters *c) {
   const long long waves = 2LL * cap_arcs * lp.L;
   const long long threads = static_cast<long long>(cap_feat) + 2LL * cap_arcs;
   const long long items = waves * kWave > threads ? waves * kWave : threads;
   hipLaunchKernelGGL(k_corr_mark, dim3(blocks_for(items, 256)), dim3(256), 0, s, agg, lp, out_len, ddeg, flist,
-                     ins_src, ins_dst, del_src, del_dst, bm, c);
+                     ins_src, ins_dst, del_src, del_dst, ins_w, del_w, bm, c);
 }
 
 int compact_blocks(long long n) {

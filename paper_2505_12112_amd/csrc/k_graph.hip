@@ -89,7 +89,7 @@ __device__ inline void item_row(long long w, const int *src, const int *dst, int
 
 // Reads the ops from pinned host memory and keeps a device copy for later kernels.
 __global__ void k_net_hash(const ripple_op *src_ops, ripple_op *ops, int B, long long num_feat_rows, int undirected,
-                           long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop,
+                           int weighted, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop,
                            Counters *c) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= B) return;
@@ -99,7 +99,8 @@ __global__ void k_net_hash(const ripple_op *src_ops, ripple_op *ops, int B, long
   // indexes with its fields
   bool bad;
   if (op.kind == RIPPLE_OP_INSERT || op.kind == RIPPLE_OP_DELETE)
-    bad = op.u < 0 || op.u >= n || op.v < 0 || op.v >= n;
+    bad = op.u < 0 || op.u >= n || op.v < 0 || op.v >= n ||
+          (weighted && op.kind == RIPPLE_OP_INSERT && !isfinite(op.weight));
   else if (op.kind == RIPPLE_OP_FEATURE)
     bad = op.u < 0 || op.u >= n || op.feat_row < 0 || op.feat_row >= num_feat_rows;
   else
@@ -133,8 +134,8 @@ __global__ void k_net_hash(const ripple_op *src_ops, ripple_op *ops, int B, long
 
 __global__ void k_net_decide(const ripple_op *ops, int B, int undirected, const int *ht_val, int *ht_net,
                              const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src, int *ins_dst,
-                             int *del_src, int *del_dst, int *ins_rank, int *del_rank, int *flist,
-                             Counters *c) {
+                             int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w, float *del_w,
+                             int *flist, Counters *c) {
   const int lane = lane_id();
   for (long long i = global_wave(); i < B; i += num_waves()) {
     const ripple_op op = ops[i];
@@ -155,27 +156,40 @@ __global__ void k_net_decide(const ripple_op *ops, int B, int undirected, const 
     }
     const int la = out.len[a], lb = in.len[b];
     const bool use_out = la <= lb;
-    const int *row = use_out ? out.col + out.off[a] : in.col + in.off[b];
-    const bool present = wave_find(row, use_out ? la : lb, use_out ? b : a) >= 0;
+    const long long row0 = use_out ? out.off[a] : in.off[b];
+    const int pos = wave_find((use_out ? out.col : in.col) + row0, use_out ? la : lb, use_out ? b : a);
+    const bool present = pos >= 0;
     const bool want = op.kind == RIPPLE_OP_INSERT;
+    const bool weighted = out.wt != nullptr;
+    const float w_old = weighted && present ? (use_out ? out.wt : in.wt)[row0 + pos] : 1.0f;
+    const float w_new = weighted ? op.weight : 1.0f;
+    const bool reweight = want && present && w_old != w_new;
     if (lane == 0) {
       atomicAdd(&c->edge_keys, 1ull);
-      if (want == present) {
+      if (want == present && !reweight) {
         atomicAdd(&c->noop_edge, 1ull);
         ht_net[s] = 0;
       } else {
-        ht_net[s] = want ? 1 : -1;
-        int *ps = want ? ins_src : del_src;
-        int *pd = want ? ins_dst : del_dst;
-        int *rank = want ? ins_rank : del_rank;
+        // a reweight drops the old entry (as a delete) and puts the arc back with its
+        // new weight (as an insert)
+        ht_net[s] = want && !reweight ? 1 : -1;
         const int narcs = undirected ? 2 : 1;
-        const u64 j = atomicAdd(want ? &c->n_ins : &c->n_del, static_cast<u64>(narcs));
-        for (int t = 0; t < narcs; ++t) {
-          const int su = t == 0 ? a : b, sv = t == 0 ? b : a;
-          ps[j + t] = su;
-          pd[j + t] = sv;
-          rank[2 * (j + t)] = atomicAdd(want ? &out.inscnt[su] : &out.delcnt[su], 1);
-          rank[2 * (j + t) + 1] = atomicAdd(want ? &in.inscnt[sv] : &in.delcnt[sv], 1);
+        if (reweight) atomicAdd(&c->n_rew, static_cast<u64>(narcs));
+        for (int kind = 0; kind < 2; ++kind) {  // 0: delete item, 1: insert item
+          if (kind == 0 ? !present : !want) continue;
+          const bool ins = kind == 1;
+          int *ps = ins ? ins_src : del_src;
+          int *pd = ins ? ins_dst : del_dst;
+          int *rank = ins ? ins_rank : del_rank;
+          const u64 j = atomicAdd(ins ? &c->n_ins : &c->n_del, static_cast<u64>(narcs));
+          for (int t = 0; t < narcs; ++t) {
+            const int su = t == 0 ? a : b, sv = t == 0 ? b : a;
+            ps[j + t] = su;
+            pd[j + t] = sv;
+            (ins ? ins_w : del_w)[j + t] = ins ? w_new : w_old;
+            rank[2 * (j + t)] = atomicAdd(ins ? &out.inscnt[su] : &out.delcnt[su], 1);
+            rank[2 * (j + t) + 1] = atomicAdd(ins ? &in.inscnt[sv] : &in.delcnt[sv], 1);
+          }
         }
       }
     }
@@ -250,6 +264,8 @@ __global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, con
     if (k > 0 || move) {
       const int *src = a.col + src_off;
       int *dst = a.col + dst_off;
+      const float *srcw = a.wt != nullptr ? a.wt + src_off : nullptr;  // weights move with their slots
+      float *dstw = a.wt != nullptr ? a.wt + dst_off : nullptr;
       int wpos = 0;
       // kRewriteU entries per lane per step: the step's row reads, then its first
       // hash probes, are all in flight together (a probe that meets another key
@@ -257,12 +273,14 @@ __global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, con
       // is written at or below its own position, so the in-place case is safe.
       for (int base = 0; base < len0; base += kWave * kRewriteU) {
         int x[kRewriteU];
+        float xw[kRewriteU];
         bool keep[kRewriteU];
 #pragma unroll
         for (int u = 0; u < kRewriteU; ++u) {
           const int e = base + u * kWave + lane;
           keep[u] = e < len0;
           x[u] = keep[u] ? src[e] : -1;
+          xw[u] = keep[u] && srcw != nullptr ? srcw[e] : 0.0f;
         }
         if (k > 0) {
           u64 key[kRewriteU], got[kRewriteU];
@@ -284,7 +302,10 @@ __global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, con
 #pragma unroll
         for (int u = 0; u < kRewriteU; ++u) {
           const u64 m = __ballot(keep[u]);
-          if (keep[u]) dst[wpos + lanes_below(m)] = x[u];
+          if (keep[u]) {
+            dst[wpos + lanes_below(m)] = x[u];
+            if (dstw != nullptr) dstw[wpos + lanes_below(m)] = xw[u];
+          }
           wpos += __popcll(m);
         }
       }
@@ -302,7 +323,7 @@ __global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, con
 }
 
 __global__ void k_topo_put(Adj out, Adj in, const int *ins_src, const int *ins_dst, const int *ins_rank,
-                           Counters *c) {
+                           const float *ins_w, Counters *c) {
   if (c->abort) return;
   const long long ni = 2 * static_cast<long long>(c->n_ins);
   const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
@@ -310,7 +331,9 @@ __global__ void k_topo_put(Adj out, Adj in, const int *ins_src, const int *ins_d
     int dir, row, entry;
     item_row(w, ins_src, ins_dst, dir, row, entry);
     const Adj &a = dir ? in : out;
-    a.col[a.off[row] + (a.len[row] - a.inscnt[row]) + ins_rank[w]] = entry;
+    const long long slot = a.off[row] + (a.len[row] - a.inscnt[row]) + ins_rank[w];
+    a.col[slot] = entry;
+    if (a.wt != nullptr) a.wt[slot] = ins_w[w >> 1];
   }
 }
 
@@ -359,13 +382,15 @@ __global__ void k_cleanup(int B, const ripple_op *ops, const int *op_slot, u64 *
 
 // Re-layout: row u's used entries move from old_col[old_off[u]..] to new_col[new_off[u]..].
 __global__ void k_repack_copy(long long n, const int *old_col, const long long *old_off, const int *len,
-                              int *new_col, const long long *new_off) {
+                              int *new_col, const long long *new_off, const float *old_wt, float *new_wt) {
   const int lane = lane_id();
   for (long long u = global_wave(); u < n; u += num_waves()) {
     const int *src = old_col + old_off[u];
     int *dst = new_col + new_off[u];
     const int l = len[u];
     for (int e = lane; e < l; e += kWave) dst[e] = src[e];
+    if (new_wt != nullptr)
+      for (int e = lane; e < l; e += kWave) new_wt[new_off[u] + e] = old_wt[old_off[u] + e];
   }
 }
 
@@ -379,20 +404,21 @@ inline int blocks_for(long long items, int threads, int cap = 4096) {
 }  // namespace
 
 void launch_net_hash(hipStream_t s, const ripple_op *src_ops, ripple_op *ops, int B, long long num_feat_rows,
-                     int undirected, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop,
-                     Counters *c) {
+                     int undirected, int weighted, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot,
+                     int *fop, Counters *c) {
   if (B <= 0) return;
   hipLaunchKernelGGL(k_net_hash, dim3(blocks_for(B, 256, 1 << 20)), dim3(256), 0, s, src_ops, ops, B, num_feat_rows,
-                     undirected, n, ht_key, ht_val, mask, op_slot, fop, c);
+                     undirected, weighted, n, ht_key, ht_val, mask, op_slot, fop, c);
 }
 
 void launch_net_decide(hipStream_t s, const ripple_op *ops, int B, int undirected, const int *ht_val, int *ht_net,
                        const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src, int *ins_dst,
-                       int *del_src, int *del_dst, int *ins_rank, int *del_rank, int *flist, Counters *c) {
+                       int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w, float *del_w,
+                       int *flist, Counters *c) {
   if (B <= 0) return;
   hipLaunchKernelGGL(k_net_decide, dim3(blocks_for(static_cast<long long>(B) * kWave, 256)), dim3(256), 0, s,
                      ops, B, undirected, ht_val, ht_net, op_slot, fop, out, in, ins_src, ins_dst, del_src,
-                     del_dst, ins_rank, del_rank, flist, c);
+                     del_dst, ins_rank, del_rank, ins_w, del_w, flist, c);
 }
 
 void launch_topo_plan(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
@@ -411,9 +437,9 @@ void launch_topo_rewrite(hipStream_t s, int cap_arcs, int undirected, long long 
 }
 
 void launch_topo_put(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                     const int *ins_rank, Counters *c) {
+                     const int *ins_rank, const float *ins_w, Counters *c) {
   hipLaunchKernelGGL(k_topo_put, dim3(blocks_for(2LL * cap_arcs, 256)), dim3(256), 0, s, out, in, ins_src,
-                     ins_dst, ins_rank, c);
+                     ins_dst, ins_rank, ins_w, c);
 }
 
 void launch_cleanup(hipStream_t s, int B, int cap_arcs, const ripple_op *ops, const int *op_slot, u64 *ht_key,
@@ -426,9 +452,9 @@ void launch_cleanup(hipStream_t s, int B, int cap_arcs, const ripple_op *ops, co
 }
 
 void launch_repack_copy(hipStream_t s, long long n, const int *old_col, const long long *old_off, const int *len,
-                        int *new_col, const long long *new_off) {
+                        int *new_col, const long long *new_off, const float *old_wt, float *new_wt) {
   hipLaunchKernelGGL(k_repack_copy, dim3(blocks_for(n * kWave, 256, 8192)), dim3(256), 0, s, n, old_col, old_off,
-                     len, new_col, new_off);
+                     len, new_col, new_off, old_wt, new_wt);
 }
 
 }  // namespace rp
@@ -551,12 +577,12 @@ void launch_relayout_sums(hipStream_t s, long long n, float slack, int min_slack
 }
 
 void launch_relayout_apply(hipStream_t s, long long n, float slack, int min_slack, Adj a, int *new_col,
-                           const long long *blocksums, long long *new_off, int *new_cap, u64 *top) {
+                           float *new_wt, const long long *blocksums, long long *new_off, int *new_cap, u64 *top) {
   const int nb = relayout_blocks(n);
   hipLaunchKernelGGL(k_relayout_offsets, dim3(nb), dim3(kScanThreads), 0, s, n, a.len, slack, min_slack, blocksums,
                      new_off, new_cap);
   hipLaunchKernelGGL(k_repack_copy, dim3(blocks_for(n * kWave, 256, 8192)), dim3(256), 0, s, n, a.col, a.off, a.len,
-                     new_col, new_off);
+                     new_col, new_off, a.wt, new_wt);
   long long ib = (n + 255) / 256;
   if (ib > 4096) ib = 4096;
   hipLaunchKernelGGL(k_relayout_install, dim3(ib), dim3(256), 0, s, n, new_off, new_cap, a.off, a.cap, blocksums, nb,

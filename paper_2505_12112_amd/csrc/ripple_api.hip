@@ -61,6 +61,8 @@ struct ripple_ctx {
   rp::Adj adj[2] = {};
   long long col_capacity[2] = {0, 0};
   int *col_alt[2] = {nullptr, nullptr};   // spare column buffer per direction (same capacity)
+  float *wt_alt[2] = {nullptr, nullptr};  // weighted graphs: the spare buffer of the slots' weights
+  bool weighted = false;                  // the arcs carry weights
   long long *rl_blocksums = nullptr;      // re-layout scratch
   long long *rl_off = nullptr;
   int *rl_cap = nullptr;
@@ -121,6 +123,7 @@ struct ripple_ctx {
   int *op_slot = nullptr;
   int *ins_src = nullptr, *ins_dst = nullptr, *del_src = nullptr, *del_dst = nullptr;
   int *ins_rank = nullptr, *del_rank = nullptr;
+  float *ins_w = nullptr, *del_w = nullptr;  // the net arcs' weights (weighted graphs)
   int *flist = nullptr;
 
   // last batch
@@ -232,7 +235,7 @@ long long arena_for(const ripple_ctx *c, long long total) {
 // Uploads one adjacency direction laid out with spare slots per row and a spare
 // arena at the end.
 ripple_status upload_adj(ripple_ctx *c, int dir, const std::vector<int> &len, const std::vector<int> &col_packed,
-                         const std::vector<long long> &packed_off) {
+                         const std::vector<long long> &packed_off, const std::vector<float> &wt_packed) {
   const long long n = c->n;
   std::vector<long long> off(n);
   std::vector<int> cap(n);
@@ -249,12 +252,24 @@ ripple_status upload_adj(ripple_ctx *c, int dir, const std::vector<int> &len, co
   std::vector<int> col(static_cast<size_t>(total), -1);
   for (long long u = 0; u < n; ++u)
     std::copy(col_packed.begin() + packed_off[u], col_packed.begin() + packed_off[u] + len[u], col.begin() + off[u]);
+  std::vector<float> wt;
+  if (c->weighted) {
+    wt.assign(static_cast<size_t>(total), 0.0f);
+    for (long long u = 0; u < n; ++u)
+      std::copy(wt_packed.begin() + packed_off[u], wt_packed.begin() + packed_off[u] + len[u], wt.begin() + off[u]);
+  }
   rp::Adj &a = c->adj[dir];
   RP_TRY(dalloc_n(c, &a.off, n));
   RP_TRY(dalloc_n(c, &a.len, n));
   RP_TRY(dalloc_n(c, &a.cap, n));
   RP_TRY(dalloc_n(c, &a.col, capacity));
   RP_TRY(dalloc_n(c, &c->col_alt[dir], capacity));
+  if (c->weighted) {
+    RP_TRY(dalloc_n(c, &a.wt, capacity));
+    RP_TRY(dalloc_n(c, &c->wt_alt[dir], capacity));
+    if (total > 0)
+      RP_HIP(c, hipMemcpyAsync(a.wt, wt.data(), total * sizeof(float), hipMemcpyHostToDevice, c->stream));
+  }
   RP_TRY(dalloc_n(c, &a.inscnt, n));
   RP_TRY(dalloc_n(c, &a.delcnt, n));
   RP_HIP(c, hipMemcpyAsync(a.off, off.data(), n * sizeof(long long), hipMemcpyHostToDevice, c->stream));
@@ -291,14 +306,20 @@ ripple_status repack_adj_grow(ripple_ctx *c, int dir) {
   const long long arena = arena_for(c, total);
   const long long capacity = total + arena;
   int *new_col = nullptr;
+  float *new_wt = nullptr;
   long long *new_off = nullptr;
   dfree_t(c, c->col_alt[dir]);
   RP_TRY(dalloc_n(c, &c->col_alt[dir], capacity));
   RP_TRY(dalloc_n(c, &new_col, capacity));
+  if (c->weighted) {
+    dfree_t(c, c->wt_alt[dir]);
+    RP_TRY(dalloc_n(c, &c->wt_alt[dir], capacity));
+    RP_TRY(dalloc_n(c, &new_wt, capacity));
+  }
   RP_TRY(dalloc_n(c, &new_off, n));
   RP_HIP(c, hipMemcpyAsync(new_off, off.data(), n * sizeof(long long), hipMemcpyHostToDevice, c->stream));
   rp::launch_fill_i32(c->stream, new_col, capacity, -1);
-  rp::launch_repack_copy(c->stream, n, a.col, a.off, a.len, new_col, new_off);
+  rp::launch_repack_copy(c->stream, n, a.col, a.off, a.len, new_col, new_off, a.wt, new_wt);
   RP_HIP(c, hipMemcpyAsync(a.cap, cap.data(), n * sizeof(int), hipMemcpyHostToDevice, c->stream));
   RP_HIP(c, hipGetLastError());
   RP_HIP(c, hipStreamSynchronize(c->stream));
@@ -306,6 +327,10 @@ ripple_status repack_adj_grow(ripple_ctx *c, int dir) {
   dfree(c, a.off);
   a.col = new_col;
   a.off = new_off;
+  if (c->weighted) {
+    dfree(c, a.wt);
+    a.wt = new_wt;
+  }
   u64 top = static_cast<u64>(total);
   RP_HIP(c, hipMemcpyAsync(&c->d_persist->top[dir], &top, sizeof(u64), hipMemcpyHostToDevice, c->stream));
   RP_HIP(c, hipStreamSynchronize(c->stream));
@@ -326,10 +351,11 @@ ripple_status repack_adj(ripple_ctx *c, int dir) {
                            hipMemcpyDeviceToHost, c->stream));
   RP_HIP(c, hipStreamSynchronize(c->stream));
   if (total + c->col_capacity[dir] / 4 > c->col_capacity[dir]) return repack_adj_grow(c, dir);
-  rp::launch_relayout_apply(c->stream, n, c->slack, smin, a, c->col_alt[dir], c->rl_blocksums, c->rl_off, c->rl_cap,
-                            &c->d_persist->top[dir]);
+  rp::launch_relayout_apply(c->stream, n, c->slack, smin, a, c->col_alt[dir], c->wt_alt[dir], c->rl_blocksums,
+                            c->rl_off, c->rl_cap, &c->d_persist->top[dir]);
   RP_HIP(c, hipGetLastError());
   std::swap(a.col, c->col_alt[dir]);
+  if (c->weighted) std::swap(a.wt, c->wt_alt[dir]);
   return RIPPLE_OK;
 }
 
@@ -345,6 +371,8 @@ void free_batch_scratch(ripple_ctx *c) {
   dfree_t(c, c->del_dst);
   dfree_t(c, c->ins_rank);
   dfree_t(c, c->del_rank);
+  dfree_t(c, c->ins_w);
+  dfree_t(c, c->del_w);
   dfree_t(c, c->flist);
   if (c->h_ops) (void)hipHostFree(c->h_ops);
   if (c->h_feat) (void)hipHostFree(c->h_feat);
@@ -375,6 +403,8 @@ ripple_status ensure_batch_scratch(ripple_ctx *c, long long ops, long long frows
   RP_TRY(dalloc_n(c, &c->del_src, arcs));
   RP_TRY(dalloc_n(c, &c->del_dst, arcs));
   RP_TRY(dalloc_n(c, &c->ins_rank, 2 * arcs));
+  RP_TRY(dalloc_n(c, &c->ins_w, arcs));
+  RP_TRY(dalloc_n(c, &c->del_w, arcs));
   RP_TRY(dalloc_n(c, &c->del_rank, 2 * arcs));
   RP_TRY(dalloc_n(c, &c->flist, cap));
   RP_HIP(c, hipHostMalloc(reinterpret_cast<void **>(&c->h_ops), cap * sizeof(ripple_op), hipHostMallocDefault));
@@ -452,7 +482,7 @@ rp::GemmArgs gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 *c
   g.H = c->H[l];
   g.delta = delta;
   g.dld = rp::row_ld(c->dims[l]);
-  g.agg = c->agg;
+  g.agg = c->agg == rp::kGcWsum ? rp::kGcSum : c->agg;  // the weights are already in S
   g.abort = abort;
   g.eps1 = c->gin_eps1;
   return g;
@@ -595,15 +625,20 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
   rp::Counters *dnext = c->d_counters + (c->parity ^ 1);
   const int cap_arcs = static_cast<int>(2 * c->cap_ops);
   rp::Adj out = c->adj[0], in = c->adj[1];
+  // the message kernels see the arcs' weights only under the weighted-sum model
+  // (the topology kernels always keep them)
+  rp::Adj out_msg = out, in_msg = in;
+  if (c->agg != rp::kGcWsum) out_msg.wt = in_msg.wt = nullptr;
   c->last_pull = 0;
   c->last_dense = 0;
   PhaseScope total(c, RIPPLE_PHASE_TOTAL);
   {
     PhaseScope ps(c, RIPPLE_PHASE_NET);
-    rp::launch_net_hash(s, src_ops, c->d_ops, B, num_feat_rows, c->undirected, c->n, c->ht_key, c->ht_val,
-                        c->ht_mask, c->op_slot, c->fop, dc);
+    rp::launch_net_hash(s, src_ops, c->d_ops, B, num_feat_rows, c->undirected, c->weighted ? 1 : 0, c->n, c->ht_key,
+                        c->ht_val, c->ht_mask, c->op_slot, c->fop, dc);
     rp::launch_net_decide(s, c->d_ops, B, c->undirected, c->ht_val, c->ht_net, c->op_slot, c->fop, out, in,
-                          c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank, c->del_rank, c->flist, dc);
+                          c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank, c->del_rank, c->ins_w,
+                          c->del_w, c->flist, dc);
     add_launches(c, RIPPLE_PHASE_NET, 2);
   }
   {
@@ -613,13 +648,14 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
     rp::launch_topo_rewrite(s, cap_arcs, c->undirected, c->n, out, in, c->ins_src, c->ins_dst, c->del_src,
                             c->del_dst, c->ins_rank, c->del_rank, c->ht_key, c->ht_net, c->ht_mask, c->d_persist,
                             c->ddeg, dc);
-    rp::launch_topo_put(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->ins_rank, dc);
+    rp::launch_topo_put(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->ins_rank, c->ins_w, dc);
     add_launches(c, RIPPLE_PHASE_TOPO, 3);
   }
   {
     PhaseScope ps(c, RIPPLE_PHASE_LAYER0);
     rp::launch_corr_mark(s, static_cast<int>(c->cap_ops), cap_arcs, c->agg, layer_ptrs(c), c->adj[0].len, c->ddeg,
-                         c->flist, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->bm_x, dc);
+                         c->flist, c->ins_src, c->ins_dst, c->del_src, c->del_dst,
+                         c->agg == rp::kGcWsum ? c->ins_w : nullptr, c->del_w, c->bm_x, dc);
     rp::CompactOut co{};
     co.list = c->lists[0];
     co.count = &dc->count[0];
@@ -660,7 +696,7 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
       // in-arc prefix, pull over every in-arc and mark the sinks that received a
       // message
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
-      rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out,
+      rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out_msg,
                          c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->zero, dc, false,
                          rp::has_self_term(c->agg));
       rp::CompactOut all{};
@@ -669,13 +705,13 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
       all.in_deg = c->adj[1].len;
       all.ioff = c->ioff;
       rp::launch_compact(s, c->n, nullptr, nullptr, compact_scratch(c, dc), all);
-      rp::launch_pull_msgs(s, c->n, c->sw[l], ld, nullptr, &dc->count_all, c->ioff, in, member, wprefix, msg,
+      rp::launch_pull_msgs(s, c->n, c->sw[l], ld, nullptr, &dc->count_all, c->ioff, in_msg, member, wprefix, msg,
                            c->S[l], c->bm_out, dc);
       add_launches(c, RIPPLE_PHASE_SCATTER, 3);
     } else {
       // push: marks + atomic adds; pull: marks only (the adds follow the compaction)
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
-      rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out,
+      rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out_msg,
                          c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc,
                          mode == kPushLayer, rp::has_self_term(c->agg));
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
@@ -700,7 +736,7 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
     }
     if (mode == kPullLayer) {
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
-      rp::launch_pull_msgs(s, c->n, c->sw[l], ld, c->lists[l], &dc->count[l], c->ioff, in, member, wprefix, msg,
+      rp::launch_pull_msgs(s, c->n, c->sw[l], ld, c->lists[l], &dc->count[l], c->ioff, in_msg, member, wprefix, msg,
                            c->S[l], nullptr, dc);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
@@ -777,6 +813,10 @@ bool validate_ops(ripple_ctx *c, const ripple_op *ops, long long num_ops, long l
     if (o.kind == RIPPLE_OP_INSERT || o.kind == RIPPLE_OP_DELETE) {
       if (o.u < 0 || o.u >= c->n || o.v < 0 || o.v >= c->n) {
         c->err = "ripple: op " + std::to_string(i) + ": vertex id out of range";
+        return false;
+      }
+      if (c->weighted && o.kind == RIPPLE_OP_INSERT && !std::isfinite(o.weight)) {
+        c->err = "ripple: op " + std::to_string(i) + ": insert weight is not finite";
         return false;
       }
     } else if (o.kind == RIPPLE_OP_FEATURE) {
@@ -861,6 +901,12 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   }
   c->n = n;
   c->undirected = g->undirected ? 1 : 0;
+  c->weighted = g->weight != nullptr;
+  for (long long i = 0; c->weighted && i < m; ++i)
+    if (!std::isfinite(g->weight[i])) {
+      c->err = "ripple: edge " + std::to_string(i) + ": weight is not finite";
+      return bail(RIPPLE_E_INVALID);
+    }
   c->slack = g->slack;
   c->min_slack = g->min_slack;
   c->device = g->device;
@@ -894,10 +940,23 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
     ioff[u + 1] = ioff[u] + indeg[u];
   }
   std::vector<int> ocol(arcs), icol(arcs);
+  std::vector<float> ow, iw;  // weighted graphs: the arcs' weights in the same order
+  // weighted rows are sorted as (column, weight bits) pairs packed in 64 bits
+  std::vector<unsigned long long> okey;
+  auto pack = [](int v, float w) {
+    unsigned bits;
+    std::memcpy(&bits, &w, sizeof(bits));
+    return static_cast<unsigned long long>(static_cast<unsigned>(v)) << 32 | bits;
+  };
   {
     std::vector<long long> fo(ooff.begin(), ooff.end() - 1);
+    if (c->weighted) okey.resize(arcs);
     for (long long i = 0; i < m; ++i) {
       const int u = g->src[i], v = g->dst[i];
+      if (c->weighted) {
+        okey[fo[u]] = pack(v, g->weight[i]);
+        if (c->undirected) okey[fo[v]] = pack(u, g->weight[i]);
+      }
       ocol[fo[u]++] = v;
       if (c->undirected) ocol[fo[v]++] = u;
     }
@@ -915,7 +974,12 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
       if (row1 < row0) row1 = row0;
       pool.emplace_back([&, t, row0, row1]() {
         for (long long u = row0; u < row1; ++u) {
-          std::sort(ocol.begin() + ooff[u], ocol.begin() + ooff[u + 1]);
+          if (c->weighted) {
+            std::sort(okey.begin() + ooff[u], okey.begin() + ooff[u + 1]);
+            for (long long e = ooff[u]; e < ooff[u + 1]; ++e) ocol[e] = static_cast<int>(okey[e] >> 32);
+          } else {
+            std::sort(ocol.begin() + ooff[u], ocol.begin() + ooff[u + 1]);
+          }
           for (long long e = ooff[u] + 1; e < ooff[u + 1]; ++e)
             if (ocol[e] == ocol[e - 1]) {
               bad[t] = u;
@@ -935,8 +999,20 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   {
     // stable over CSR order, so every in-row is sorted by source
     std::vector<long long> fi(ioff.begin(), ioff.end() - 1);
+    if (c->weighted) {
+      ow.resize(arcs);
+      iw.resize(arcs);
+      for (long long e = 0; e < arcs; ++e) {
+        const unsigned bits = static_cast<unsigned>(okey[e] & 0xffffffffull);
+        std::memcpy(&ow[e], &bits, sizeof(float));
+      }
+      std::vector<unsigned long long>().swap(okey);
+    }
     for (long long u = 0; u < n; ++u)
-      for (long long e = ooff[u]; e < ooff[u + 1]; ++e) icol[fi[ocol[e]]++] = static_cast<int>(u);
+      for (long long e = ooff[u]; e < ooff[u + 1]; ++e) {
+        if (c->weighted) iw[fi[ocol[e]]] = ow[e];
+        icol[fi[ocol[e]]++] = static_cast<int>(u);
+      }
   }
   hipError_t e = hipSetDevice(c->device);
   if (e != hipSuccess) return bail(device_fail(c, e, "hipSetDevice"));
@@ -953,8 +1029,8 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   e = hipHostMalloc(reinterpret_cast<void **>(&c->h_counters), sizeof(rp::Counters), hipHostMallocDefault);
   if (e != hipSuccess) return bail(device_fail(c, e, "hipHostMalloc"));
   std::vector<int> olen(outdeg), ilen(indeg);
-  if ((st = upload_adj(c, 0, olen, ocol, ooff)) != RIPPLE_OK) return bail(st);
-  if ((st = upload_adj(c, 1, ilen, icol, ioff)) != RIPPLE_OK) return bail(st);
+  if ((st = upload_adj(c, 0, olen, ocol, ooff, ow)) != RIPPLE_OK) return bail(st);
+  if ((st = upload_adj(c, 1, ilen, icol, ioff, iw)) != RIPPLE_OK) return bail(st);
   // persistent per-vertex scratch
   const long long words = (n + 31) / 32;
   if ((st = dalloc_n(c, &c->fop, n)) != RIPPLE_OK) return bail(st);
@@ -984,7 +1060,10 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   if (x == nullptr || md == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: x and model must be non-NULL");
   const int L = md->num_layers;
   if (L < 1 || L > rp::kMaxL) return fail(c, RIPPLE_E_INVALID, "ripple: num_layers out of range");
-  if (md->agg < RIPPLE_AGG_SUM || md->agg > RIPPLE_AGG_GIN) return fail(c, RIPPLE_E_INVALID, "ripple: unknown aggregator");
+  if (md->agg < RIPPLE_AGG_SUM || md->agg > RIPPLE_AGG_GC_WSUM)
+    return fail(c, RIPPLE_E_INVALID, "ripple: unknown aggregator");
+  if (md->agg == RIPPLE_AGG_GC_WSUM && !c->weighted)
+    return fail(c, RIPPLE_E_INVALID, "ripple: RIPPLE_AGG_GC_WSUM needs a graph loaded with weights");
   const bool sage = md->agg == RIPPLE_AGG_SUM || md->agg == RIPPLE_AGG_MEAN;
   const bool gin = md->agg == RIPPLE_AGG_GIN;
   if (!sage && md->agg != RIPPLE_AGG_GCN && md->transform_first == 1)
@@ -1081,15 +1160,17 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
     if (c->tf[l]) RP_TRY(dalloc_n(c, &c->P[l], n * c->dims[l]));
   RP_HIP(c, hipMemcpyAsync(c->H[0], x, static_cast<size_t>(n) * c->dims[0] * sizeof(float), hipMemcpyHostToDevice,
                            c->stream));
+  rp::Adj pull_adj = c->adj[1];  // arc weights only under the weighted-sum model
+  if (c->agg != rp::kGcWsum) pull_adj.wt = nullptr;
   // bootstrap: layer-wise full forward pass. Plain layers pull the previous
   // layer's rows over the in-rows, then transform; transform-first layers
   // transform every row by W_neigh first and pull the narrower result.
   for (int l = 1; l <= L; ++l) {
     if (c->tf[l]) {
       rp::launch_gemm(c->stream, p_gemm_args(c, l, nullptr, nullptr, n, nullptr, nullptr), n, n);
-      rp::launch_pull(c->stream, n, c->dims[l], c->agg, c->P[l], c->adj[1], c->adj[0].len, c->S[l]);
+      rp::launch_pull(c->stream, n, c->dims[l], c->agg, c->P[l], pull_adj, c->adj[0].len, c->S[l]);
     } else {
-      rp::launch_pull(c->stream, n, c->dims[l - 1], c->agg, c->H[l - 1], c->adj[1], c->adj[0].len, c->S[l]);
+      rp::launch_pull(c->stream, n, c->dims[l - 1], c->agg, c->H[l - 1], pull_adj, c->adj[0].len, c->S[l]);
     }
     launch_layer_gemm(c, c->stream, l, nullptr, nullptr, n, nullptr, nullptr, n, n);
     RP_HIP(c, hipGetLastError());
@@ -1158,8 +1239,9 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
     stats->num_ops = B;
     stats->edge_keys = static_cast<int64_t>(k.edge_keys);
     stats->noop_edge_ops = static_cast<int64_t>(k.noop_edge);
-    stats->ins_arcs = static_cast<int64_t>(k.n_ins);
-    stats->del_arcs = static_cast<int64_t>(k.n_del);
+    stats->ins_arcs = static_cast<int64_t>(k.n_ins - k.n_rew);
+    stats->del_arcs = static_cast<int64_t>(k.n_del - k.n_rew);
+    stats->reweighted_arcs = static_cast<int64_t>(k.n_rew);
     stats->features = static_cast<int64_t>(k.n_feat);
     stats->affected[0] = static_cast<int64_t>(k.n_feat);
     for (int l = 1; l <= c->L; ++l) {
@@ -1319,6 +1401,31 @@ ripple_status ripple_get_arcs(ripple_ctx *c, int32_t direction, int32_t *src, in
   return RIPPLE_OK;
 }
 
+ripple_status ripple_get_arc_weights(ripple_ctx *c, int32_t direction, float *weights, int64_t capacity,
+                                     int64_t *count) {
+  RP_TRY(check_ctx(c));
+  if (count == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: count is NULL");
+  *count = 0;
+  if (!c->weighted) return fail(c, RIPPLE_E_INVALID, "ripple: the graph has no weights");
+  if (direction != 0 && direction != 1) return fail(c, RIPPLE_E_INVALID, "ripple: direction must be 0 or 1");
+  if (capacity < 0 || (capacity > 0 && weights == nullptr)) return fail(c, RIPPLE_E_INVALID, "ripple: bad output buffer");
+  const long long n = c->n;
+  const rp::Adj &a = c->adj[direction];
+  std::vector<long long> off(n);
+  std::vector<int> len(n);
+  std::vector<float> wt(c->col_capacity[direction]);
+  RP_HIP(c, hipMemcpyAsync(off.data(), a.off, n * sizeof(long long), hipMemcpyDeviceToHost, c->stream));
+  RP_HIP(c, hipMemcpyAsync(len.data(), a.len, n * sizeof(int), hipMemcpyDeviceToHost, c->stream));
+  RP_HIP(c, hipMemcpyAsync(wt.data(), a.wt, wt.size() * sizeof(float), hipMemcpyDeviceToHost, c->stream));
+  RP_HIP(c, hipStreamSynchronize(c->stream));
+  long long k = 0;
+  for (long long u = 0; u < n; ++u)
+    for (int e = 0; e < len[u]; ++e, ++k)
+      if (k < capacity) weights[k] = wt[off[u] + e];
+  *count = k;
+  return RIPPLE_OK;
+}
+
 ripple_status ripple_set_scatter_mode(ripple_ctx *c, int32_t mode) {
   RP_TRY(check_ctx(c));
   if (mode < RIPPLE_SCATTER_AUTO || mode > RIPPLE_SCATTER_DENSE) return fail(c, RIPPLE_E_INVALID, "ripple: bad mode");
@@ -1390,6 +1497,8 @@ void ripple_destroy(ripple_ctx *c) {
     dfree_t(c, c->adj[d].cap);
     dfree_t(c, c->adj[d].col);
     dfree_t(c, c->col_alt[d]);
+    dfree_t(c, c->adj[d].wt);
+    dfree_t(c, c->wt_alt[d]);
     dfree_t(c, c->adj[d].inscnt);
     dfree_t(c, c->adj[d].delcnt);
   }

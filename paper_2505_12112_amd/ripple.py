@@ -20,7 +20,7 @@ MAX_LAYERS = 8
 NUM_PHASES = 8
 
 OK, E_INVALID, E_STATE, E_OOM, E_DEVICE = 0, 1, 2, 3, 4
-AGG = {"sum": 0, "mean": 1, "gcn": 2, "gc_sum": 3, "gc_mean": 4, "gin": 5}
+AGG = {"sum": 0, "mean": 1, "gcn": 2, "gc_sum": 3, "gc_mean": 4, "gin": 5, "gc_wsum": 6}
 GEMM = {"fp32": 0, "bf16": 1}
 OP_INSERT, OP_DELETE, OP_FEATURE = 1, 2, 3
 PHASES = ["net", "topo", "layer0", "scatter", "compact", "gemm", "other", "total"]
@@ -29,7 +29,7 @@ EXPORTED = [
     "ripple_load_graph", "ripple_init_embeddings", "ripple_apply_updates", "ripple_get_embeddings",
     "ripple_get_affected", "ripple_get_aggregates", "ripple_get_arcs", "ripple_device_bytes",
     "ripple_set_profiling", "ripple_get_phase_stats", "ripple_phase_name", "ripple_last_error",
-    "ripple_destroy", "ripple_set_scatter_mode", "ripple_apply_updates_device",
+    "ripple_destroy", "ripple_set_scatter_mode", "ripple_apply_updates_device", "ripple_get_arc_weights",
 ]
 SCATTER = {"auto": 0, "push": 1, "pull": 2, "dense": 3}
 
@@ -50,7 +50,7 @@ class GraphDesc(C.Structure):
         ("src", C.POINTER(C.c_int32)), ("dst", C.POINTER(C.c_int32)),
         ("undirected", C.c_int32), ("slack", C.c_float), ("min_slack", C.c_int32),
         ("device", C.c_int32), ("stream", C.c_void_p), ("max_device_bytes", C.c_int64),
-        ("arena_slots", C.c_int64),
+        ("arena_slots", C.c_int64), ("weight", C.POINTER(C.c_float)),
     ]
 
 
@@ -73,6 +73,7 @@ class BatchStats(C.Structure):
         ("pushed_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("dest_rows", C.c_int64 * (MAX_LAYERS + 1)),
         ("relocated_rows", C.c_int64), ("repacks", C.c_int64),
         ("in_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("pull_layers", C.c_int32), ("dense_layers", C.c_int32),
+        ("reweighted_arcs", C.c_int64),
     ]
 
 
@@ -101,6 +102,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.ripple_get_aggregates.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_float), P(C.c_int32)]
     lib.ripple_get_affected.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_int64)]
     lib.ripple_get_arcs.argtypes = [vp, C.c_int32, P(C.c_int32), P(C.c_int32), C.c_int64, P(C.c_int64)]
+    lib.ripple_get_arc_weights.argtypes = [vp, C.c_int32, P(C.c_float), C.c_int64, P(C.c_int64)]
     lib.ripple_device_bytes.argtypes = [vp, P(C.c_int64)]
     lib.ripple_set_profiling.argtypes = [vp, C.c_int32]
     lib.ripple_set_scatter_mode.argtypes = [vp, C.c_int32]
@@ -134,15 +136,20 @@ class Ripple:
 
     def __init__(self, n: int, src, dst, undirected: bool = False, slack: float = 0.25,
                  min_slack: int = 4, device: int = 0, stream: Optional[int] = None,
-                 max_device_bytes: int = 0, arena_slots: int = 0):
+                 max_device_bytes: int = 0, arena_slots: int = 0, weights=None):
+        """weights: one float per edge for a weighted graph (RIPPLE_AGG_GC_WSUM), else None."""
         self._lib = load_library()
         self._ctx = C.c_void_p()
         src, dst = _i32(src), _i32(dst)
         if src.shape != dst.shape:
             raise ValueError("src and dst differ in length")
+        w = None if weights is None else _f32(weights)
+        if w is not None and w.shape != src.shape:
+            raise ValueError("one weight per edge")
         desc = GraphDesc(int(n), int(src.size), _ptr(src, C.c_int32), _ptr(dst, C.c_int32),
                          int(bool(undirected)), float(slack), int(min_slack), int(device),
-                         C.c_void_p(stream) if stream else None, int(max_device_bytes), int(arena_slots))
+                         C.c_void_p(stream) if stream else None, int(max_device_bytes), int(arena_slots),
+                         _ptr(w, C.c_float))
         st = self._lib.ripple_load_graph(C.byref(desc), C.byref(self._ctx))
         if st != OK:
             raise RippleError(st, self._lib.ripple_last_error(None).decode())
@@ -246,6 +253,7 @@ class Ripple:
             "pushed_arcs": list(st.pushed_arcs[:L + 1]), "dest_rows": list(st.dest_rows[:L + 1]),
             "relocated_rows": st.relocated_rows, "repacks": st.repacks,
             "in_arcs": list(st.in_arcs[:L + 1]), "pull_layers": st.pull_layers, "dense_layers": st.dense_layers,
+            "reweighted_arcs": st.reweighted_arcs,
         }
 
     def apply_updates_raw(self, ops: np.ndarray, feat_rows: Optional[np.ndarray], stats: BatchStats) -> None:
@@ -305,6 +313,16 @@ class Ripple:
             self._check(self._lib.ripple_get_arcs(self._ctx, direction, _ptr(s, C.c_int32), _ptr(d, C.c_int32),
                                                   s.size, C.byref(cnt)))
         return s, d
+
+    def get_arc_weights(self, direction: int = 0) -> np.ndarray:
+        """Weighted graphs: the arcs' weights in get_arcs order."""
+        cnt = C.c_int64()
+        self._check(self._lib.ripple_get_arc_weights(self._ctx, direction, None, 0, C.byref(cnt)))
+        w = np.empty(cnt.value, np.float32)
+        if cnt.value:
+            self._check(self._lib.ripple_get_arc_weights(self._ctx, direction, _ptr(w, C.c_float), w.size,
+                                                         C.byref(cnt)))
+        return w
 
     def set_scatter_mode(self, mode: str):
         """"auto" (default), "push", "pull" or "dense": how layers add their messages."""

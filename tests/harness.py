@@ -56,12 +56,12 @@ def _hip():
 
 class Pair:
     def __init__(self, n, src, dst, x, weights, undirected=False, transform_first=-1, mode="auto", inputs="host",
-                 **lib_kw):
-        self.lib = Ripple(n, src, dst, undirected=undirected, **lib_kw)
+                 edge_w=None, **lib_kw):
+        self.lib = Ripple(n, src, dst, undirected=undirected, weights=edge_w, **lib_kw)
         self.lib.init_embeddings(x, weights, transform_first=transform_first)
         self.lib.set_scatter_mode(mode)
         self.inputs = inputs  # "host": ripple_apply_updates; "device": the batch staged in HBM first
-        self.orc = O.OracleState(n, src, dst, x, O.OracleModel.from_weights(weights), undirected)
+        self.orc = O.OracleState(n, src, dst, x, O.OracleModel.from_weights(weights), undirected, edge_w)
         self.L = len(weights.dims) - 1
         self.n = n
 
@@ -87,6 +87,7 @@ class Pair:
         if check_stats:
             assert st["ins_arcs"] == net.ins_src.size
             assert st["del_arcs"] == net.del_src.size
+            assert st["reweighted_arcs"] == net.rew_src.size
             assert st["features"] == net.features.size
             assert st["edge_keys"] == net.edge_keys
             assert st["noop_edge_ops"] == net.noop_edge_ops
@@ -104,11 +105,16 @@ class Pair:
         return errs
 
     def check_arcs(self):
+        """The arc set in both directions, and on a weighted graph every arc's weight."""
         want = self.orc.graph.keys
         for direction in (0, 1):
             s, d = self.lib.get_arcs(direction)
-            got = np.sort(s.astype(np.int64) * self.n + d)
-            np.testing.assert_array_equal(got, want, err_msg=f"direction {direction}")
+            keys = s.astype(np.int64) * self.n + d
+            order = np.argsort(keys)
+            np.testing.assert_array_equal(keys[order], want, err_msg=f"direction {direction}")
+            if self.orc.graph.w is not None:
+                w = self.lib.get_arc_weights(direction)[order]
+                np.testing.assert_array_equal(w.astype(np.float64), self.orc.graph.w, err_msg=f"weights {direction}")
 
     def check_aggregates(self, tol=FP32_TOL):
         """The library's cached aggregates against their definition on oracle values:
@@ -123,7 +129,7 @@ class Pair:
         if self.orc.model.agg == "gcn":
             c = 1.0 / np.sqrt(g.out_degree() + 1.0)
         u, _ = g.arcs()
-        a = g.in_adjacency(weights=c[u])
+        a = g.in_adjacency(weights=c[u] * (g.w if self.orc.model.agg == "gc_wsum" else 1.0))
         errs = []
         for l in range(1, self.L + 1):
             want = a @ ref[l - 1]
@@ -174,6 +180,8 @@ def random_valid_batch(rng, orc: O.OracleState, bs: int, d0: int, mix=(1 / 3, 1 
                 continue
             used.add(e)
             ops[i, 1], ops[i, 2] = u, v
+            if k == 1 and g.w is not None:  # weighted graph: the new arc's weight
+                ops[i, 3] = synth.weight_bits([rng.uniform(0.5, 1.5)])[0]
             placed = True
             break
         if not placed:

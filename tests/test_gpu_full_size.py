@@ -37,13 +37,13 @@ def test_sparse_mid_full_size(bs):
         p.close()
 
 
-@pytest.mark.parametrize("config", ["sparse_mid_gc_sum", "sparse_mid_gc_mean", "sparse_mid_gin"])
+@pytest.mark.parametrize("config", ["sparse_mid_gc_sum", "sparse_mid_gc_mean", "sparse_mid_gin", "sparse_mid_gc_wsum"])
 def test_evaluation_workloads_on_the_arxiv_shaped_graph(config):
-    """GraphConv-sum, GraphConv-mean and GIN-sum (2 layers, 128-256-40) at full size:
-    20 batches of 100 with affected sets every batch, then all embeddings against a
-    float64 full recompute."""
+    """GraphConv-sum, GraphConv-mean, GIN-sum and GraphConv-weighted-sum (2 layers,
+    128-256-40) at full size: 20 batches of 100 with affected sets every batch, then
+    all embeddings against a float64 full recompute."""
     wl = synth.build_workload(config)
-    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights)
+    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, edge_w=wl.edge_w)
     try:
         p.check_embeddings()
         t0 = time.time()

@@ -20,7 +20,7 @@ def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-AGGS = ["sum", "mean", "gcn", "gc_sum", "gc_mean", "gin"]
+AGGS = ["sum", "mean", "gcn", "gc_sum", "gc_mean", "gin", "gc_wsum"]
 
 
 def _small(rng, n, m, dims, agg, undirected=False, bias_std=0.1):
@@ -31,13 +31,18 @@ def _small(rng, n, m, dims, agg, undirected=False, bias_std=0.1):
     return src, dst, x, w
 
 
+def _edge_w(rng, agg, m):
+    """Arc weights for the weighted-sum model, else None."""
+    return synth.arc_weights(rng, m) if agg == "gc_wsum" else None
+
+
 @pytest.mark.parametrize("agg", AGGS)
 @pytest.mark.parametrize("dims", [(16, 16, 8), (5, 70, 33, 3), (100, 130, 47)])
 def test_bootstrap_matches_full_recompute(agg, dims):
     _say("bootstrap", agg, dims)
     rng = np.random.default_rng(hash((agg, dims)) % 2**32)
     src, dst, x, w = _small(rng, 700, 4000, dims, agg)
-    p = Pair(700, src, dst, x, w)
+    p = Pair(700, src, dst, x, w, edge_w=_edge_w(rng, agg, src.size))
     try:
         p.check_embeddings()
         p.check_aggregates()
@@ -75,12 +80,12 @@ def test_adversarial_batches(agg, undirected, mode):
     rng = np.random.default_rng(7 + 3 * AGGS.index(agg) + undirected)
     dims = (12, 40, 9)
     src, dst, x, w = _small(rng, 300, 1200, dims, agg, undirected)
-    p = Pair(300, src, dst, x, w, undirected=undirected, mode=mode)
+    p = Pair(300, src, dst, x, w, undirected=undirected, mode=mode, edge_w=_edge_w(rng, agg, src.size))
     try:
         for b in range(25):
             a, bb = p.orc.graph.arcs()
             batch = synth.adversarial_batch(rng, 300, dims[0], bs=int(rng.integers(1, 60)), hot=10,
-                                            existing=(a, bb))
+                                            existing=(a, bb), weighted=agg == "gc_wsum")
             p.step(batch)
         p.check_embeddings()
         p.check_arcs()
@@ -89,7 +94,8 @@ def test_adversarial_batches(agg, undirected, mode):
         p.close()
 
 
-@pytest.mark.parametrize("agg,arena", [("sum", 0), ("gcn", 0), ("sum", 64), ("mean", 2000), ("sum", 2000)])
+@pytest.mark.parametrize("agg,arena", [("sum", 0), ("gcn", 0), ("sum", 64), ("mean", 2000), ("sum", 2000),
+                                       ("gc_wsum", 0), ("gc_wsum", 64)])
 def test_no_slack_forces_row_moves_and_relayouts(agg, arena):
     """slack 0: every insert outgrows its row, so rows move to the spare arena; a
     small arena runs out, which forces re-layouts (on the device, or into larger
@@ -98,7 +104,7 @@ def test_no_slack_forces_row_moves_and_relayouts(agg, arena):
     rng = np.random.default_rng(11 + arena)
     dims = (8, 16, 4)
     src, dst, x, w = _small(rng, 200, 600, dims, agg)
-    p = Pair(200, src, dst, x, w, slack=0.0, min_slack=0, arena_slots=arena)
+    p = Pair(200, src, dst, x, w, slack=0.0, min_slack=0, arena_slots=arena, edge_w=_edge_w(rng, agg, src.size))
     try:
         moved = relayouts = 0
         for b in range(60):
@@ -260,14 +266,14 @@ def test_call_order_and_device_byte_cap():
 
 
 @pytest.mark.parametrize("agg,mode", [(a, m) for a in ("sum", "mean", "gcn") for m in ("auto", "pull", "dense")]
-                         + [(a, m) for a in ("gc_sum", "gc_mean", "gin") for m in ("auto", "dense")])
+                         + [(a, m) for a in ("gc_sum", "gc_mean", "gin", "gc_wsum") for m in ("auto", "dense")])
 def test_thousand_batches_on_a_small_graph(agg, mode):
     """1000 consecutive batches: sets every batch, embeddings every 100 and at the end."""
     _say("1000 batches", agg, mode)
     rng = np.random.default_rng(16 + AGGS.index(agg))
     dims = (16, 32, 8)
     src, dst, x, w = _small(rng, 400, 2400, dims, agg)
-    p = Pair(400, src, dst, x, w, mode=mode)
+    p = Pair(400, src, dst, x, w, mode=mode, edge_w=_edge_w(rng, agg, src.size))
     try:
         worst = 0.0
         for b in range(1000):
