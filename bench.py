@@ -87,7 +87,7 @@ def cpu_baseline(wl_name, seed, batches, bs):
         blas_threads = 1
     wl = synth.build_workload(wl_name, seed=seed)
     model = O.OracleModel.from_weights(wl.weights)
-    st = O.OracleState(wl.n, wl.src, wl.dst, wl.x, model, wl.spec.graph.undirected)
+    st = O.OracleState(wl.n, wl.src, wl.dst, wl.x, model, wl.spec.graph.undirected, wl.edge_w)
     big = wl.src.size * (2 if wl.spec.graph.undirected else 1) > 20_000_000
     dims = list(wl.weights.dims)
     m = st.graph.num_arcs
@@ -148,7 +148,8 @@ def main():
     spec = wl.spec
     log(f"[bench] generated {args.config}: n={wl.n} edges={wl.src.size} in {time.perf_counter() - t0:.1f}s")
     stream = torch.cuda.current_stream().cuda_stream
-    lib = Ripple(wl.n, wl.src, wl.dst, undirected=spec.graph.undirected, device=0, stream=stream or None)
+    lib = Ripple(wl.n, wl.src, wl.dst, undirected=spec.graph.undirected, device=0, stream=stream or None,
+                 weights=wl.edge_w)
     lib.set_scatter_mode(args.scatter_mode)
     t0 = time.perf_counter()
     lib.init_embeddings(wl.x, wl.weights)
