@@ -177,6 +177,8 @@ typedef struct {
   int32_t pull_layers;          /* bit l set: layer l pulled over the in-arcs of A^l */
   int32_t dense_layers;         /* bit l set: layer l pulled over every in-arc of the graph */
   int64_t reweighted_arcs;      /* weighted graphs: arcs present before and after whose weight changed */
+  int64_t graph_replay;         /* 1: the batch ran as one replay of a captured HIP graph (see
+                                   ripple_set_graphs); 0: its kernels were queued one by one */
 } ripple_batch_stats;
 
 /* Part 1 of the problem statement: copies the snapshot to the device as an
@@ -258,6 +260,18 @@ RIPPLE_API ripple_status ripple_get_arc_weights(ripple_ctx *ctx, int32_t directi
  * the previous batch's counts (push on the first batch). */
 enum { RIPPLE_SCATTER_AUTO = 0, RIPPLE_SCATTER_PUSH = 1, RIPPLE_SCATTER_PULL = 2, RIPPLE_SCATTER_DENSE = 3 };
 RIPPLE_API ripple_status ripple_set_scatter_mode(ripple_ctx *ctx, int32_t mode);
+
+/* How a batch's kernels reach the GPU. enable = 1: the first batch of each launch
+ * plan (message form and GEMM tile per layer) is captured as a HIP graph on the
+ * context's stream and later batches with that plan replay it, so the host
+ * thread queues one graph instead of some fifteen kernels. Batch sizes and input
+ * pointers are not part of a plan: the first kernel reads them from a pinned block
+ * the library fills per call. enable = 0 (default, the lower batch latency on
+ * MI355X): every kernel is queued on its own, as are batches that record phase
+ * events. A capture that the runtime refuses switches the context to direct
+ * launches for good. The same kernels run either way. RIPPLE_E_INVALID for other
+ * values. */
+RIPPLE_API ripple_status ripple_set_graphs(ripple_ctx *ctx, int32_t enable);
 
 /* Device bytes the context holds. */
 RIPPLE_API ripple_status ripple_device_bytes(ripple_ctx *ctx, int64_t *bytes);

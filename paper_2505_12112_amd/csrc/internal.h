@@ -48,6 +48,18 @@ struct Counters {
   u64 zero;               // never written: an arc count of zero for kernels that only mark
 };
 
+// One batch's inputs as the host hands them over, in pinned host memory written
+// before the launch: the first kernel of the batch reads it (system scope, so a
+// replayed launch sees the new values) and keeps a device copy for the later
+// kernels. Every launch of a batch is therefore the same for batches of any size
+// up to the scratch capacity, which lets a batch be replayed as one graph.
+struct BatchIn {
+  const ripple_op *ops;    // pinned host or device memory
+  const float *feat;       // feature rows, [num_feat_rows][d_0], pinned host or device memory
+  long long num_ops;
+  long long num_feat_rows;
+};
+
 // Survives batches.
 struct Persist {
   u64 top[2];             // next free arena slot per direction
@@ -73,6 +85,73 @@ struct LayerPtrs {
   int L;
 };
 
+// The per-batch scratch a batch touched, reset by its last kernel (see
+// batch_cleanup).
+struct CleanupArgs {
+  const BatchIn *in;  // device copy of the batch's inputs
+  const ripple_op *ops;
+  const int *op_slot;
+  u64 *ht_key;
+  int *ht_val;
+  int *ht_net;
+  int *fop;
+  int *out_inscnt, *out_delcnt, *in_inscnt, *in_delcnt;
+  const int *ins_src, *ins_dst, *del_src, *del_dst;
+  int *ddeg;
+  const Counters *c;  // this batch's counters, copied to host
+  Counters *next;     // the other counter buffer, zeroed for the next batch
+  Counters *host;     // pinned
+};
+
+// Resets every per-batch scratch word the batch touched (also after an abort),
+// copies the batch's counters to pinned host memory and clears the other counter
+// buffer. Thread t of `threads` (t = 0 also copies the counters, with the rest of
+// its block: block is the calling block's index among the cleanup blocks). Runs in
+// the batch's last kernel beside work that reads none of this scratch.
+__device__ inline void batch_cleanup(const CleanupArgs &a, int block, long long t0, long long threads) {
+  if (block == 0) {
+    constexpr int words = static_cast<int>(sizeof(Counters) / sizeof(u64));
+    const u64 *src = reinterpret_cast<const u64 *>(a.c);
+    u64 *dst = reinterpret_cast<u64 *>(a.host);
+    u64 *nxt = reinterpret_cast<u64 *>(a.next);
+    for (int w = threadIdx.x; w < words; w += blockDim.x) {
+      dst[w] = src[w];
+      nxt[w] = 0ull;
+    }
+  }
+  // item w = 2 * arc + direction (0: the source's out-row, 1: the sink's in-row)
+  const long long ni = 2 * static_cast<long long>(a.c->n_ins);
+  const long long nd = 2 * static_cast<long long>(a.c->n_del);
+  const long long B = a.in->num_ops;
+  for (long long w = t0; w < ni; w += threads) {
+    if (w & 1) {
+      a.in_inscnt[a.ins_dst[w >> 1]] = 0;
+    } else {
+      const int u = a.ins_src[w >> 1];
+      a.out_inscnt[u] = 0;
+      a.ddeg[u] = 0;
+    }
+  }
+  for (long long w = t0; w < nd; w += threads) {
+    if (w & 1) {
+      a.in_delcnt[a.del_dst[w >> 1]] = 0;
+    } else {
+      const int u = a.del_src[w >> 1];
+      a.out_delcnt[u] = 0;
+      a.ddeg[u] = 0;
+    }
+  }
+  for (long long i = t0; i < B; i += threads) {
+    const int s = a.op_slot[i];
+    if (s >= 0) {
+      a.ht_key[s] = kEmptyKey;
+      a.ht_val[s] = -1;
+      a.ht_net[s] = 0;
+    }
+    if (a.ops[i].kind == RIPPLE_OP_FEATURE) a.fop[a.ops[i].u] = -1;
+  }
+}
+
 // Same values as ripple_agg. GraphConv (kGcSum, kGcMean) has no self term; GIN's
 // update is a two-layer MLP on (1 + eps) h_v + S_v.
 // kGcWsum: GraphConv with the arcs' stored weights (weighted graphs).
@@ -84,48 +163,46 @@ inline bool has_self_term(int agg) { return agg != kGcSum && agg != kGcMean && a
 // netting: after these, the net arcs are listed and every (arc, direction) item
 // knows its rank among the row's inserts (ins_rank) or deletes (del_rank); the
 // hash slot of every named edge holds +1 (net insert), -1 (net delete) or 0.
-// src_ops: the batch in pinned host or device memory; copied to ops (device) on the
-// way and checked (ids and feature rows in range, known kind, finite insert weights
-// on a weighted graph): a failing op sets bad_op and abort, and is copied as a
+// host_in: the batch's inputs (BatchIn, pinned host memory); dev_in receives a copy
+// for the later kernels. The ops are copied to ops (device) on the way and
+// checked (ids and feature rows in range, known kind, finite insert weights on a
+// weighted graph): a failing op sets bad_op and abort, and is copied as a
 // self-loop no-op. On a weighted graph (out.wt set) an insert of a present arc
 // with another weight is a reweight: listed as a delete (old weight, del_w) and an
 // insert (new weight, ins_w) of the same arc, counted in n_rew.
-void launch_net_hash(hipStream_t s, const ripple_op *src_ops, ripple_op *ops, int B, long long num_feat_rows,
+// cap_ops bounds num_ops (the grids are sized for it).
+void launch_net_hash(hipStream_t s, int cap_ops, const BatchIn *host_in, BatchIn *dev_in, ripple_op *ops,
                      int undirected, int weighted, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot,
                      int *fop, Counters *c);
-void launch_net_decide(hipStream_t s, const ripple_op *ops, int B, int undirected, const int *ht_val,
-                       int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src,
-                       int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w,
-                       float *del_w, int *flist, Counters *c);
+void launch_net_decide(hipStream_t s, int cap_ops, const BatchIn *in, const ripple_op *ops, int undirected,
+                       const int *ht_val, int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in_adj,
+                       int *ins_src, int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank,
+                       float *ins_w, float *del_w, int *flist, Counters *c);
 
 // topology (cap_arcs bounds n_ins and n_del): plan row moves and check the arena
 // (aborting before any mutation), then one owner wave per touched row removes its
-// deleted entries, moves the row if it must grow, and sets its new length; then
-// the inserts are written at their ranks.
+// deleted entries, moves the row if it must grow, and sets its new length (the
+// inserts are written at their ranks by launch_corr_mark).
 void launch_topo_plan(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
                       const int *ins_rank, Counters *c, const Persist *p, long long cap_out, long long cap_in);
 void launch_topo_rewrite(hipStream_t s, int cap_arcs, int undirected, long long n, Adj out, Adj in,
                          const int *ins_src, const int *ins_dst, const int *del_src, const int *del_dst,
                          const int *ins_rank, const int *del_rank, const u64 *ht_key, const int *ht_net,
                          unsigned mask, Persist *p, int *ddeg, Counters *c);
-void launch_topo_put(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                     const int *ins_rank, const float *ins_w, Counters *c);
-// Also copies *c to host (pinned) and zeroes *next (the other counter buffer).
-void launch_cleanup(hipStream_t s, int B, int cap_arcs, const ripple_op *ops, const int *op_slot,
-                    u64 *ht_key, int *ht_val, int *ht_net, int *fop, Adj out, Adj in, const int *ins_src,
-                    const int *ins_dst, const int *del_src, const int *del_dst, int *ddeg,
-                    const Counters *c, Counters *next, Counters *host);
 
 // frontier. Pre-batch corrections of every layer's aggregate (an inserted arc
 // (u,v) adds u's pre-batch contribution to S^l_v, a deleted one removes it) run
 // after the adjacency update, with pre-batch coefficients recovered from ddeg;
 // the same kernel marks the layer-1 dirty set (feature writes; GCN: vertices whose
-// out-degree changed).
-// ins_w / del_w (nullable): the arcs' weights (weighted graphs).
-void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerPtrs lp, const int *out_len,
-                      const int *ddeg, const int *flist, const int *ins_src, const int *ins_dst,
-                      const int *del_src, const int *del_dst, const float *ins_w, const float *del_w, unsigned *bm,
-                      Counters *c);
+// out-degree changed) and writes every inserted arc into the slot of its row given
+// by its rank among the row's inserts (with arc_w[arc], the slot's weight, when
+// the adjacency keeps weights).
+// ins_w / del_w (nullable): the arcs' weights as the corrections use them
+// (weighted-sum model).
+void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerPtrs lp, Adj out, Adj in,
+                      const int *ins_rank, const float *arc_w, const int *ddeg, const int *flist, const int *ins_src,
+                      const int *ins_dst, const int *del_src, const int *del_dst, const float *ins_w,
+                      const float *del_w, unsigned *bm, Counters *c);
 int compact_blocks(long long n);
 // Outputs of one compaction of bitmaps (a | b) into an ascending list. Optional
 // (nullptr = skipped): list, doff[j] = sum of out_deg over list[0..j) (doff[count]
@@ -148,22 +225,37 @@ struct CompactOut {
   int *wprefix;
 };
 // Tile sums published by the single-pass compaction: compact_scratch_words(n)
-// words, zero when first used; epoch cycles through 1..65535, one per launch.
+// words, zero when first used, then owned by the compactions of one vertex count
+// (each launch finds its epoch from a ticket counter kept there).
 struct CompactScratch {
   u64 *words;
-  u64 epoch;
   u64 *err;  // bit 2 set if a wait for a predecessor tile timed out
 };
 long long compact_scratch_words(long long n);
+// Layer-0 deltas of the listed (dirty) vertices u at list position j:
+// delta[j] = c'_u x'_u - c_u x_u (c = 1, or 1/sqrt(dout+1) post/pre batch under
+// GCN), where x'_u is u's last feature row of the batch (in->feat, which may be
+// pinned host memory, row ops[fop[u]].feat_row) or x_u when u has none; then
+// X[u] = x'_u. Skipped when the batch aborted.
+struct Delta0Args {
+  int agg;
+  int d0;
+  int ld;  // row stride of delta (floats)
+  const ripple_op *ops;
+  const BatchIn *in;
+  const int *fop;
+  float *X;
+  const int *out_len;
+  const int *ddeg;
+  float *delta;
+  const Counters *c;
+};
 // Compacts bm_a | bm_b (both cleared) into o. in_total / out_total (nullable)
 // receive the degree sums over the list even when the prefix arrays are not wanted.
 void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, const CompactScratch &cs,
                     const CompactOut &o);
-
-// layer 0 deltas (feat may be pinned host memory)
-void launch_delta0(hipStream_t s, long long n, int agg, int d0, int ld, const int *list, const u64 *count,
-                   const ripple_op *ops, const float *feat, const int *fop, float *X, const int *out_len,
-                   const int *ddeg, float *delta, const Counters *c);
+// The layer-0 deltas of list[0 .. *count) (n bounds the count).
+void launch_delta0(hipStream_t s, long long n, const Delta0Args &z, const int *list, const u64 *count);
 
 // scatter: S^l[v] += delta[j] for every post-batch out-arc (list[j] -> v) (doff
 // gives each listed vertex's first arc); marks the sinks in bm_out, and the
@@ -232,9 +324,18 @@ struct GemmArgs {
   int agg;
   const u64 *abort;
   float eps1;  // GIN: 1 + eps
+  // cleanup_blocks > 0: the launch has that many extra blocks which run
+  // batch_cleanup(cleanup) instead (the batch's last GEMM)
+  int cleanup_blocks;
+  CleanupArgs cleanup;
 };
-// expected_rows picks the tile height (large tiles when many rows are expected).
+// Blocks a batch's clean-up takes for cap_ops ops.
+int cleanup_blocks_for(long long cap_ops);
+// expected_rows picks the tile height (large tiles when many rows are expected);
+// gemm_variant(expected_rows) names the choice (launches with the same variant
+// and arguments are the same launch).
 void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows, long long expected_rows);
+int gemm_variant(long long expected_rows);
 
 // re-layout of one adjacency direction
 // old_wt / new_wt (nullable): the slots' weights move with them.

@@ -40,15 +40,33 @@ inline int blocks_for(long long items, int threads, int cap = 4096) {
   return static_cast<int>(b);
 }
 
-// Pre-batch corrections and the layer-1 dirty marks (see launch_corr_mark).
-__global__ void k_corr_mark(int agg, LayerPtrs lp, const int *out_len, const int *ddeg, const int *flist,
-                            const int *ins_src, const int *ins_dst, const int *del_src, const int *del_dst,
-                            const float *ins_w, const float *del_w, unsigned *bm, Counters *c) {
+// The inserted arcs' slots, the pre-batch corrections and the layer-1 dirty marks
+// (see launch_corr_mark).
+__global__ void k_corr_mark(int agg, LayerPtrs lp, Adj out, Adj in, const int *ins_rank, const float *arc_w,
+                            const int *ddeg, const int *flist, const int *ins_src, const int *ins_dst,
+                            const int *del_src, const int *del_dst, const float *ins_w, const float *del_w,
+                            unsigned *bm, Counters *c) {
   if (c->abort) return;
   const int lane = lane_id();
+  const int *out_len = out.len;
   const long long nf = static_cast<long long>(c->n_feat);
   const long long ni = static_cast<long long>(c->n_ins);
   const long long na = ni + static_cast<long long>(c->n_del);
+  {
+    // item w = 2 * arc + direction: its row's inserts follow the kept entries, in
+    // rank order
+    const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
+    for (long long w = blockIdx.x * blockDim.x + threadIdx.x; w < 2 * ni; w += stride) {
+      const long long arc = w >> 1;
+      const int dir = static_cast<int>(w & 1);
+      const int row = dir == 0 ? ins_src[arc] : ins_dst[arc];
+      const int entry = dir == 0 ? ins_dst[arc] : ins_src[arc];
+      const Adj &a = dir ? in : out;
+      const long long slot = a.off[row] + (a.len[row] - a.inscnt[row]) + ins_rank[w];
+      a.col[slot] = entry;
+      if (a.wt != nullptr) a.wt[slot] = arc_w[arc];
+    }
+  }
   const long long items = na * lp.L;
   for (long long it = global_wave(); it < items; it += num_waves()) {
     const long long arc = it / lp.L;
@@ -120,20 +138,28 @@ __device__ inline void load_words(const unsigned *bm_a, const unsigned *bm_b, lo
 }
 
 // Sums of the out- and in-degrees (either may be null) over the cursor's bits.
-__device__ inline void degree_sums(BitCursor c, const int *odeg, const int *ideg, long long &dsum,
-                                   long long &isum) {
+// The degrees of the first kBatch bits are kept in d0 / i0 (most threads have no
+// more), so the pass that writes the offsets need not fetch them again.
+__device__ inline void degree_sums(BitCursor c, const int *odeg, const int *ideg, long long &dsum, long long &isum,
+                                   int (&d0)[kBatch], int (&i0)[kBatch]) {
   if (odeg == nullptr && ideg == nullptr) return;
+  bool first = true;
   while (!c.empty()) {
     int v[kBatch];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) v[j] = c.next();
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
-      if (v[j] >= 0) {
-        if (odeg != nullptr) dsum += odeg[v[j]];
-        if (ideg != nullptr) isum += ideg[v[j]];
+      const int dv = odeg != nullptr && v[j] >= 0 ? odeg[v[j]] : 0;
+      const int iv = ideg != nullptr && v[j] >= 0 ? ideg[v[j]] : 0;
+      dsum += dv;
+      isum += iv;
+      if (first) {
+        d0[j] = dv;
+        i0[j] = iv;
       }
     }
+    first = false;
   }
 }
 
@@ -216,17 +242,22 @@ __device__ inline bool fetch(const u64 *p, u64 epoch, long long (&v)[kVals]) {
 // bitmaps are cleared. A full compaction lists every vertex without reading them.
 __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, unsigned *bm_b, long long words,
                                                              CompactOut o, u64 *agg, u64 *inc, u64 *ticket,
-                                                             u64 epoch, u64 *err) {
+                                                             u64 *err) {
   __shared__ long long red[kCompactWaves][kVals];
   __shared__ long long tile_s, base_s[kVals];
+  __shared__ u64 epoch_s;
   const long long tiles = gridDim.x;
   if (threadIdx.x == 0) {
-    const long long t = static_cast<long long>(atomicAdd(ticket, 1ull));
-    if (t == tiles - 1) __hip_atomic_store(ticket, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    tile_s = t;
+    // The ticket counter only grows and every launch on this scratch has the same
+    // number of tiles, each taking one ticket, so launch k holds tickets k * tiles
+    // .. k * tiles + tiles - 1: the ticket names both the tile and the launch.
+    const u64 t = atomicAdd(ticket, 1ull);
+    tile_s = static_cast<long long>(t % static_cast<u64>(tiles));
+    epoch_s = t / static_cast<u64>(tiles) % 65535 + 1;
   }
   __syncthreads();
   const long long tile = tile_s;
+  const u64 epoch = epoch_s;
   const long long w0 = tile * kWordsPerBlock + threadIdx.x * kWordsPerThread;
   const int *odeg = o.doff != nullptr || o.out_total != nullptr ? o.out_deg : nullptr;
   const int *ideg = o.ioff != nullptr || o.in_total != nullptr ? o.in_deg : nullptr;
@@ -245,7 +276,8 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
   long long st[kVals] = {0, 0, 0, pop_a};
 #pragma unroll
   for (int i = 0; i < kWordsPerThread; ++i) st[0] += __popc(wv[i]);
-  degree_sums(BitCursor(wv, w0), odeg, ideg, st[1], st[2]);
+  int d0[kBatch], i0[kBatch];
+  degree_sums(BitCursor(wv, w0), odeg, ideg, st[1], st[2], d0, i0);
   long long ex[kVals], tot[kVals];
   block_scan(st, ex, tot, red);
   if (threadIdx.x == 0) publish((tile == 0 ? inc : agg) + tile * kVals, epoch, tot);
@@ -310,15 +342,17 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
     }
   }
   BitCursor c(wv, w0);
+  bool first = true;  // the cursor repeats the first pass's order: its first batch is cached
   while ((o.list != nullptr || o.doff != nullptr || o.ioff != nullptr) && !c.empty()) {
     int v[kBatch], dv[kBatch], iv[kBatch];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) v[j] = c.next();
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
-      dv[j] = o.doff != nullptr && v[j] >= 0 ? odeg[v[j]] : 0;
-      iv[j] = o.ioff != nullptr && v[j] >= 0 ? ideg[v[j]] : 0;
+      dv[j] = o.doff == nullptr || v[j] < 0 ? 0 : first ? d0[j] : odeg[v[j]];
+      iv[j] = o.ioff == nullptr || v[j] < 0 ? 0 : first ? i0[j] : ideg[v[j]];
     }
+    first = false;
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       if (v[j] < 0) continue;
@@ -353,32 +387,6 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
     if (o.out_total != nullptr) *o.out_total = static_cast<u64>(base[1] + tot[1]);
     if (o.in_total != nullptr) *o.in_total = static_cast<u64>(base[2] + tot[2]);
     if (o.sinks_a != nullptr) *o.sinks_a = static_cast<u64>(base[3] + tot[3]);
-  }
-}
-
-__global__ void k_delta0(int agg, int d0, int ld, const int *list, const u64 *count, const ripple_op *ops,
-                         const float *feat, const int *fop, float *X, const int *out_len, const int *ddeg,
-                         float *delta, const Counters *c) {
-  if (c->abort) return;
-  const long long m = static_cast<long long>(*count);
-  const int lane = lane_id();
-  for (long long j = global_wave(); j < m; j += num_waves()) {
-    const int u = list[j];
-    const int fo = fop[u];
-    float cn = 1.0f, co = 1.0f;
-    if (agg == kGcn) {
-      cn = 1.0f / sqrtf(static_cast<float>(out_len[u]) + 1.0f);
-      co = 1.0f / sqrtf(static_cast<float>(out_len[u] - ddeg[u]) + 1.0f);
-    }
-    float *xu = X + static_cast<long long>(u) * d0;
-    const float *xn = fo >= 0 ? feat + static_cast<long long>(ops[fo].feat_row) * d0 : xu;
-    float *dj = delta + j * ld;
-    for (int k = lane; k < d0; k += kWave) {
-      const float xo = xu[k];
-      const float x1 = xn[k];
-      dj[k] = cn * x1 - co * xo;
-      xu[k] = x1;
-    }
   }
 }
 
@@ -422,6 +430,33 @@ __device__ inline long long owner_from(const long long *a, long long from, long 
   const int cnt = __popcll(__ballot(le));
   if (cnt == hi - from && hi < n1) return wave_last_le(a, hi - 1, n1, x);
   return from + cnt - 1;
+}
+
+// One wave per listed vertex (see Delta0Args).
+__global__ void k_delta0(Delta0Args z, const int *list, const u64 *count) {
+  if (z.c->abort) return;
+  const long long m = static_cast<long long>(*count);
+  const int lane = lane_id();
+  const float *feat = z.in->feat;
+  for (long long j = global_wave(); j < m; j += num_waves()) {
+    const int u = list[j];
+    const int fo = z.fop[u];
+    float cn = 1.0f, co = 1.0f;
+    if (z.agg == kGcn) {
+      const int dout = z.out_len[u];
+      cn = 1.0f / sqrtf(static_cast<float>(dout) + 1.0f);
+      co = 1.0f / sqrtf(static_cast<float>(dout - z.ddeg[u]) + 1.0f);
+    }
+    float *xu = z.X + static_cast<long long>(u) * z.d0;
+    const float *xn = fo >= 0 ? feat + static_cast<long long>(z.ops[fo].feat_row) * z.d0 : xu;
+    float *dj = z.delta + j * z.ld;
+    for (int k = lane; k < z.d0; k += kWave) {
+      const float xo = xu[k];
+      const float x1 = xn[k];
+      dj[k] = cn * x1 - co * xo;
+      xu[k] = x1;
+    }
+  }
 }
 
 // Edge-parallel scatter. Pushed arcs are numbered: arc e of listed vertex j has
@@ -760,14 +795,15 @@ __global__ void k_gather_rows(const float *src, int d, const int *ids, long long
 
 }  // namespace
 
-void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerPtrs lp, const int *out_len,
-                      const int *ddeg, const int *flist, const int *ins_src, const int *ins_dst, const int *del_src,
-                      const int *del_dst, const float *ins_w, const float *del_w, unsigned *bm, Counters *c) {
+void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerPtrs lp, Adj out, Adj in,
+                      const int *ins_rank, const float *arc_w, const int *ddeg, const int *flist, const int *ins_src,
+                      const int *ins_dst, const int *del_src, const int *del_dst, const float *ins_w,
+                      const float *del_w, unsigned *bm, Counters *c) {
   const long long waves = 2LL * cap_arcs * lp.L;
   const long long threads = static_cast<long long>(cap_feat) + 2LL * cap_arcs;
   const long long items = waves * kWave > threads ? waves * kWave : threads;
-  hipLaunchKernelGGL(k_corr_mark, dim3(blocks_for(items, 256)), dim3(256), 0, s, agg, lp, out_len, ddeg, flist,
-                     ins_src, ins_dst, del_src, del_dst, ins_w, del_w, bm, c);
+  hipLaunchKernelGGL(k_corr_mark, dim3(blocks_for(items, 256)), dim3(256), 0, s, agg, lp, out, in, ins_rank, arc_w,
+                     ddeg, flist, ins_src, ins_dst, del_src, del_dst, ins_w, del_w, bm, c);
 }
 
 int compact_blocks(long long n) {
@@ -780,18 +816,14 @@ void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, 
   const long long words = (n + 31) / 32;
   const int tiles = compact_blocks(n);
   hipLaunchKernelGGL(k_compact, dim3(tiles), dim3(kCompactThreads), 0, s, bm_a, bm_b, words, o, cs.words,
-                     cs.words + static_cast<long long>(tiles) * kVals, cs.words + 2LL * tiles * kVals, cs.epoch,
-                     cs.err);
+                     cs.words + static_cast<long long>(tiles) * kVals, cs.words + 2LL * tiles * kVals, cs.err);
+}
+
+void launch_delta0(hipStream_t s, long long n, const Delta0Args &z, const int *list, const u64 *count) {
+  hipLaunchKernelGGL(k_delta0, dim3(blocks_for(n * kWave, 256, 2048)), dim3(256), 0, s, z, list, count);
 }
 
 long long compact_scratch_words(long long n) { return 2LL * compact_blocks(n) * kVals + 1; }
-
-void launch_delta0(hipStream_t s, long long n, int agg, int d0, int ld, const int *list, const u64 *count,
-                   const ripple_op *ops, const float *feat, const int *fop, float *X, const int *out_len,
-                   const int *ddeg, float *delta, const Counters *c) {
-  hipLaunchKernelGGL(k_delta0, dim3(blocks_for(n * kWave, 256, 2048)), dim3(256), 0, s, agg, d0, ld, list, count,
-                     ops, feat, fop, X, out_len, ddeg, delta, c);
-}
 
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,

@@ -148,9 +148,22 @@ __device__ inline void epilogue(const GemmArgs &a, long long m, int v, int col, 
   *hp = y;
 }
 
+// The launch's last a.cleanup_blocks blocks reset the batch's scratch instead of
+// computing tiles (true for them); the others take tiles with stride gemm_grid.
+__device__ inline bool cleanup_role(const GemmArgs &a, unsigned &gemm_grid) {
+  gemm_grid = gridDim.x - static_cast<unsigned>(a.cleanup_blocks);
+  if (blockIdx.x < gemm_grid) return false;
+  const int b = static_cast<int>(blockIdx.x - gemm_grid);
+  batch_cleanup(a.cleanup, b, static_cast<long long>(b) * blockDim.x + threadIdx.x,
+                static_cast<long long>(a.cleanup_blocks) * blockDim.x);
+  return true;
+}
+
 template <int BM, int BN, int WM, int WN, int AGG, bool VEC, int MODE>
 __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
   using Sh = Shape<BM, BN, WM, WN>;
+  unsigned gemm_grid;
+  if (cleanup_role(a, gemm_grid)) return;
   if (a.abort != nullptr && *a.abort) return;
   const long long M = a.count != nullptr ? static_cast<long long>(*a.count) : a.count_fixed;
   const int N = a.N, K = a.K;
@@ -171,7 +184,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
   const int lr = lane & 15;      // row (A) / column (B) within a 16-wide MFMA tile
   const int lk = lane >> 4;      // k within a 4-deep MFMA step
 
-  for (long long t = blockIdx.x; t < tiles; t += gridDim.x) {
+  for (long long t = blockIdx.x; t < tiles; t += gemm_grid) {
     const long long m0 = (t / tiles_n) * BM;
     const int n0 = static_cast<int>(t % tiles_n) * BN;
     __syncthreads();
@@ -309,6 +322,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
   constexpr int kF = kRowsKC / 16;            // float4 per lane per operand row and round
   constexpr int kEl = kRowsBM * BN / kThreads;  // output elements per thread
   static_assert(kRowsBM * BN % kThreads == 0, "whole elements per thread");
+  unsigned gemm_grid;
+  if (cleanup_role(a, gemm_grid)) return;
   if (a.abort != nullptr && *a.abort) return;
   const long long M = a.count != nullptr ? static_cast<long long>(*a.count) : a.count_fixed;
   const int N = a.N, K = a.K, dp = a.dprev;
@@ -326,7 +341,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
   const int kb = wave * kw;
   const int ke = K < kb + kw ? K : kb + kw;
 
-  for (long long t = blockIdx.x; t < tiles; t += gridDim.x) {
+  for (long long t = blockIdx.x; t < tiles; t += gemm_grid) {
     const long long m0 = (t / tiles_n) * kRowsBM;
     const int n0 = static_cast<int>(t % tiles_n) * BN;
     // row ids: the lane's operand row and the rows of its output elements
@@ -477,7 +492,7 @@ void launch_rows(hipStream_t s, const GemmArgs &a, long long max_rows) {
   const long long tiles = ((max_rows + kRowsBM - 1) / kRowsBM) * ((a.N + BN - 1) / BN);
   long long blocks = tiles < 1 ? 1 : tiles;
   if (blocks > 2048) blocks = 2048;
-  hipLaunchKernelGGL((k_gemm_rows<BN, AGG, MODE>), dim3(blocks), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL((k_gemm_rows<BN, AGG, MODE>), dim3(blocks + a.cleanup_blocks), dim3(kThreads), 0, s, a);
 }
 
 template <int BM, int BN, int WM, int WN, int AGG, bool VEC, int MODE>
@@ -485,7 +500,8 @@ void launch_shape(hipStream_t s, const GemmArgs &a, long long max_rows) {
   const long long tiles = ((max_rows + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   long long blocks = tiles < 1 ? 1 : tiles;
   if (blocks > 2048) blocks = 2048;
-  hipLaunchKernelGGL((k_gemm<BM, BN, WM, WN, AGG, VEC, MODE>), dim3(blocks), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL((k_gemm<BM, BN, WM, WN, AGG, VEC, MODE>), dim3(blocks + a.cleanup_blocks), dim3(kThreads), 0, s,
+                     a);
 }
 
 // BN follows N. Few expected rows: the 16-row split-K kernel; many: 128-row tiles.
@@ -548,8 +564,16 @@ void launch_mode(hipStream_t s, const GemmArgs &a, long long max_rows, bool big)
 
 }  // namespace
 
+int gemm_variant(long long expected_rows) { return expected_rows >= 32768 ? 1 : 0; }
+
+int cleanup_blocks_for(long long cap_ops) {
+  // up to 4 * cap_ops (arc, direction) items and cap_ops ops, grid-strided
+  const long long b = (4 * cap_ops + kThreads - 1) / kThreads;
+  return static_cast<int>(b < 1 ? 1 : b > 256 ? 256 : b);
+}
+
 void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows, long long expected_rows) {
-  const bool big = expected_rows >= 32768;
+  const bool big = gemm_variant(expected_rows) == 1;
   if (a.mode == kTransformFirst) launch_mode<kTransformFirst>(s, a, max_rows, big);
   else if (a.mode == kPlain) launch_mode<kPlain>(s, a, max_rows, big);
   else if (a.mode == kGin1) launch_mode<kGin1>(s, a, max_rows, big);

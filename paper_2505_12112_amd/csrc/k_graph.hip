@@ -87,11 +87,24 @@ __device__ inline void item_row(long long w, const int *src, const int *dst, int
   entry = dir == 0 ? dst[arc] : src[arc];
 }
 
-// Reads the ops from pinned host memory and keeps a device copy for later kernels.
-__global__ void k_net_hash(const ripple_op *src_ops, ripple_op *ops, int B, long long num_feat_rows, int undirected,
-                           int weighted, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop,
-                           Counters *c) {
+// Reads the batch's inputs from pinned host memory at system scope (the host
+// rewrites them before every launch, so no cached copy may be used), hands them
+// to the later kernels in dev_in, and keeps a device copy of the ops.
+__global__ void k_net_hash(const BatchIn *host_in, BatchIn *dev_in, ripple_op *ops, int undirected, int weighted,
+                           long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop, Counters *c) {
+  const auto word = [&](const void *f) {
+    return __hip_atomic_load(static_cast<const u64 *>(f), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  };
+  const ripple_op *src_ops = reinterpret_cast<const ripple_op *>(word(&host_in->ops));
+  const long long B = static_cast<long long>(word(&host_in->num_ops));
+  const long long num_feat_rows = static_cast<long long>(word(&host_in->num_feat_rows));
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) {
+    dev_in->ops = src_ops;
+    dev_in->feat = reinterpret_cast<const float *>(word(&host_in->feat));
+    dev_in->num_ops = B;
+    dev_in->num_feat_rows = num_feat_rows;
+  }
   if (i >= B) return;
   ripple_op op = src_ops[i];
   // the same checks as the host's: an op that fails them aborts the batch before
@@ -132,11 +145,12 @@ __global__ void k_net_hash(const ripple_op *src_ops, ripple_op *ops, int B, long
   op_slot[i] = static_cast<int>(s);
 }
 
-__global__ void k_net_decide(const ripple_op *ops, int B, int undirected, const int *ht_val, int *ht_net,
-                             const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src, int *ins_dst,
-                             int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w, float *del_w,
-                             int *flist, Counters *c) {
+__global__ void k_net_decide(const BatchIn *bin, const ripple_op *ops, int undirected, const int *ht_val,
+                             int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src,
+                             int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w,
+                             float *del_w, int *flist, Counters *c) {
   const int lane = lane_id();
+  const long long B = bin->num_ops;
   for (long long i = global_wave(); i < B; i += num_waves()) {
     const ripple_op op = ops[i];
     if (op.kind == RIPPLE_OP_FEATURE) {
@@ -322,64 +336,6 @@ __global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, con
   }
 }
 
-__global__ void k_topo_put(Adj out, Adj in, const int *ins_src, const int *ins_dst, const int *ins_rank,
-                           const float *ins_w, Counters *c) {
-  if (c->abort) return;
-  const long long ni = 2 * static_cast<long long>(c->n_ins);
-  const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
-  for (long long w = blockIdx.x * blockDim.x + threadIdx.x; w < ni; w += stride) {
-    int dir, row, entry;
-    item_row(w, ins_src, ins_dst, dir, row, entry);
-    const Adj &a = dir ? in : out;
-    const long long slot = a.off[row] + (a.len[row] - a.inscnt[row]) + ins_rank[w];
-    a.col[slot] = entry;
-    if (a.wt != nullptr) a.wt[slot] = ins_w[w >> 1];
-  }
-}
-
-// Resets every per-batch scratch word the batch touched (runs even after an abort),
-// copies the batch's counters to pinned host memory and clears the other counter
-// buffer for the next batch.
-__global__ void k_cleanup(int B, const ripple_op *ops, const int *op_slot, u64 *ht_key, int *ht_val, int *ht_net,
-                          int *fop, Adj out, Adj in, const int *ins_src, const int *ins_dst, const int *del_src,
-                          const int *del_dst, int *ddeg, const Counters *c, Counters *next, Counters *host) {
-  if (blockIdx.x == 0) {
-    constexpr int words = static_cast<int>(sizeof(Counters) / sizeof(u64));
-    const u64 *src = reinterpret_cast<const u64 *>(c);
-    u64 *dst = reinterpret_cast<u64 *>(host);
-    u64 *nxt = reinterpret_cast<u64 *>(next);
-    for (int w = threadIdx.x; w < words; w += blockDim.x) {
-      dst[w] = src[w];
-      nxt[w] = 0ull;
-    }
-  }
-  const long long ni = 2 * static_cast<long long>(c->n_ins);
-  const long long nd = 2 * static_cast<long long>(c->n_del);
-  const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
-  const long long t0 = blockIdx.x * blockDim.x + threadIdx.x;
-  for (long long w = t0; w < ni; w += stride) {
-    int dir, row, entry;
-    item_row(w, ins_src, ins_dst, dir, row, entry);
-    (dir ? in : out).inscnt[row] = 0;
-    if (dir == 0) ddeg[row] = 0;
-  }
-  for (long long w = t0; w < nd; w += stride) {
-    int dir, row, entry;
-    item_row(w, del_src, del_dst, dir, row, entry);
-    (dir ? in : out).delcnt[row] = 0;
-    if (dir == 0) ddeg[row] = 0;
-  }
-  for (long long i = t0; i < B; i += stride) {
-    const int s = op_slot[i];
-    if (s >= 0) {
-      ht_key[s] = kEmptyKey;
-      ht_val[s] = -1;
-      ht_net[s] = 0;
-    }
-    if (ops[i].kind == RIPPLE_OP_FEATURE) fop[ops[i].u] = -1;
-  }
-}
-
 // Re-layout: row u's used entries move from old_col[old_off[u]..] to new_col[new_off[u]..].
 __global__ void k_repack_copy(long long n, const int *old_col, const long long *old_off, const int *len,
                               int *new_col, const long long *new_off, const float *old_wt, float *new_wt) {
@@ -403,21 +359,19 @@ inline int blocks_for(long long items, int threads, int cap = 4096) {
 
 }  // namespace
 
-void launch_net_hash(hipStream_t s, const ripple_op *src_ops, ripple_op *ops, int B, long long num_feat_rows,
+void launch_net_hash(hipStream_t s, int cap_ops, const BatchIn *host_in, BatchIn *dev_in, ripple_op *ops,
                      int undirected, int weighted, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot,
                      int *fop, Counters *c) {
-  if (B <= 0) return;
-  hipLaunchKernelGGL(k_net_hash, dim3(blocks_for(B, 256, 1 << 20)), dim3(256), 0, s, src_ops, ops, B, num_feat_rows,
+  hipLaunchKernelGGL(k_net_hash, dim3(blocks_for(cap_ops, 256, 1 << 20)), dim3(256), 0, s, host_in, dev_in, ops,
                      undirected, weighted, n, ht_key, ht_val, mask, op_slot, fop, c);
 }
 
-void launch_net_decide(hipStream_t s, const ripple_op *ops, int B, int undirected, const int *ht_val, int *ht_net,
-                       const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src, int *ins_dst,
-                       int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w, float *del_w,
-                       int *flist, Counters *c) {
-  if (B <= 0) return;
-  hipLaunchKernelGGL(k_net_decide, dim3(blocks_for(static_cast<long long>(B) * kWave, 256)), dim3(256), 0, s,
-                     ops, B, undirected, ht_val, ht_net, op_slot, fop, out, in, ins_src, ins_dst, del_src,
+void launch_net_decide(hipStream_t s, int cap_ops, const BatchIn *in, const ripple_op *ops, int undirected,
+                       const int *ht_val, int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in_adj,
+                       int *ins_src, int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank,
+                       float *ins_w, float *del_w, int *flist, Counters *c) {
+  hipLaunchKernelGGL(k_net_decide, dim3(blocks_for(static_cast<long long>(cap_ops) * kWave, 256)), dim3(256), 0, s,
+                     in, ops, undirected, ht_val, ht_net, op_slot, fop, out, in_adj, ins_src, ins_dst, del_src,
                      del_dst, ins_rank, del_rank, ins_w, del_w, flist, c);
 }
 
@@ -434,21 +388,6 @@ void launch_topo_rewrite(hipStream_t s, int cap_arcs, int undirected, long long 
   hipLaunchKernelGGL(k_topo_rewrite, dim3(blocks_for(4LL * cap_arcs * kWave, 256)), dim3(256), 0, s, undirected,
                      n, out, in, ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank, ht_key, ht_net, mask, p,
                      ddeg, c);
-}
-
-void launch_topo_put(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                     const int *ins_rank, const float *ins_w, Counters *c) {
-  hipLaunchKernelGGL(k_topo_put, dim3(blocks_for(2LL * cap_arcs, 256)), dim3(256), 0, s, out, in, ins_src,
-                     ins_dst, ins_rank, ins_w, c);
-}
-
-void launch_cleanup(hipStream_t s, int B, int cap_arcs, const ripple_op *ops, const int *op_slot, u64 *ht_key,
-                    int *ht_val, int *ht_net, int *fop, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                    const int *del_src, const int *del_dst, int *ddeg, const Counters *c, Counters *next,
-                    Counters *host) {
-  const long long items = 2LL * cap_arcs > B ? 2LL * cap_arcs : B;
-  hipLaunchKernelGGL(k_cleanup, dim3(blocks_for(items, 256)), dim3(256), 0, s, B, ops, op_slot, ht_key, ht_val,
-                     ht_net, fop, out, in, ins_src, ins_dst, del_src, del_dst, ddeg, c, next, host);
 }
 
 void launch_repack_copy(hipStream_t s, long long n, const int *old_col, const long long *old_off, const int *len,

@@ -2,17 +2,24 @@
 // the bootstrap forward pass and the per-batch kernel pipeline.
 //
 // Batch pipeline (one stream, counts stay on the device, one host sync at the end):
-//   net:     hash ops, decide winners against the pre-batch adjacency
-//   topo:    count per-row inserts/deletes, plan arena moves, check the arena,
-//            pre-batch corrections of every layer's aggregate, deletes, row moves,
-//            inserts
-//   layer 0: mark the dirty set (feature writes; GCN: out-degree changes), compact,
-//            form layer-0 deltas and write the new feature rows
+//   net:     hash ops, decide winners against the pre-batch adjacency, count
+//            per-row inserts/deletes
+//   topo:    plan arena moves and check the arena, then per touched row: deletes,
+//            row move, new length
+//   layer 0: inserts into their slots, pre-batch corrections of every layer's
+//            aggregate, mark the dirty set (feature writes; GCN: out-degree
+//            changes), compact, form layer-0 deltas and write the new feature rows
 //   layer l: scatter deltas along post-batch out-arcs + mark A^l, compact A^l,
 //            gather + MFMA transform + epilogue (new rows, next deltas)
 //   cleanup: reset per-batch scratch
 // An aborted batch (arena too small) changes nothing; the host re-lays the
 // adjacency out with fresh spare slots and runs the batch again.
+// Every launch of a batch depends only on its plan (message form and GEMM tile
+// per layer, counter parity): the batch's own sizes and input pointers reach the
+// kernels through a pinned block the first kernel reads. So a batch can be
+// captured once per plan as a HIP graph and later batches with that plan replay
+// it (ripple_set_graphs), which takes the queueing of some fifteen dependent
+// kernels off the host thread.
 #include <algorithm>
 #include <chrono>
 #include <cmath>
@@ -34,6 +41,13 @@ struct PhaseEv {
   int phase;
   hipEvent_t a;
   hipEvent_t b;
+};
+
+// One captured batch: the executable graph of the plan with this key.
+struct GraphSlot {
+  unsigned long long key;
+  hipGraphExec_t exec;
+  unsigned long long used;  // last use, for eviction
 };
 
 }  // namespace
@@ -93,7 +107,6 @@ struct ripple_ctx {
   unsigned *bm_out = nullptr;
   unsigned *bm_x = nullptr;
   rp::u64 *compact_lb = nullptr;  // tile sums of the single-pass compaction
-  rp::u64 compact_epoch = 0;
   int *lists[rp::kMaxL + 1] = {};
   long long *doff[rp::kMaxL + 1] = {};  // out-degree prefix of lists[l] (first arc index per vertex)
   long long *ioff = nullptr;            // in-degree prefix of the current layer's A^l (pull form)
@@ -109,6 +122,16 @@ struct ripple_ctx {
   int parity = 0;
   rp::Persist *d_persist = nullptr;
   rp::Counters *h_counters = nullptr;  // pinned
+  rp::BatchIn *h_in = nullptr;         // pinned: the batch's sizes and input pointers
+  rp::BatchIn *d_in = nullptr;         // device copy made by the first kernel of a batch
+
+  // batches replayed from captured graphs, one per plan key; dropped whenever a
+  // device buffer is allocated or freed or the adjacency's row table moves
+  bool use_graphs = false;
+  bool graphs_failed = false;  // a capture failed: launch kernel by kernel from then on
+  std::vector<GraphSlot> graphs;
+  unsigned long long graph_clock = 0;
+  bool last_graph = false;     // the last batch ran as a graph replay
 
   // per-batch scratch, sized for cap_ops ops
   long long cap_ops = 0;
@@ -171,7 +194,16 @@ ripple_status device_fail(ripple_ctx *c, hipError_t e, const char *what) {
     if (_s != RIPPLE_OK) return _s;       \
   } while (0)
 
-ripple_status dalloc(ripple_ctx *c, void **p, size_t size) {
+void drop_graphs(ripple_ctx *c) {
+  for (GraphSlot &g : c->graphs) (void)hipGraphExecDestroy(g.exec);
+  c->graphs.clear();
+}
+
+// Device allocation counted against the context's byte cap. Temporary buffers that
+// no batch launch names (keep_graphs) leave the captured graphs alone; any other
+// allocation or free may change an address a captured launch holds.
+ripple_status dalloc(ripple_ctx *c, void **p, size_t size, bool keep_graphs = false) {
+  if (!keep_graphs) drop_graphs(c);
   *p = nullptr;
   if (size == 0) size = 4;
   if (c->max_bytes > 0 && c->bytes + static_cast<long long>(size) > c->max_bytes)
@@ -190,12 +222,13 @@ ripple_status dalloc(ripple_ctx *c, void **p, size_t size) {
 }
 
 template <typename T>
-ripple_status dalloc_n(ripple_ctx *c, T **p, long long count) {
-  return dalloc(c, reinterpret_cast<void **>(p), static_cast<size_t>(count) * sizeof(T));
+ripple_status dalloc_n(ripple_ctx *c, T **p, long long count, bool keep_graphs = false) {
+  return dalloc(c, reinterpret_cast<void **>(p), static_cast<size_t>(count) * sizeof(T), keep_graphs);
 }
 
-void dfree(ripple_ctx *c, void *p) {
+void dfree(ripple_ctx *c, void *p, bool keep_graphs = false) {
   if (p == nullptr) return;
+  if (!keep_graphs) drop_graphs(c);
   auto it = c->allocs.find(p);
   if (it != c->allocs.end()) {
     c->bytes -= static_cast<long long>(it->second);
@@ -354,6 +387,7 @@ ripple_status repack_adj(ripple_ctx *c, int dir) {
   rp::launch_relayout_apply(c->stream, n, c->slack, smin, a, c->col_alt[dir], c->wt_alt[dir], c->rl_blocksums,
                             c->rl_off, c->rl_cap, &c->d_persist->top[dir]);
   RP_HIP(c, hipGetLastError());
+  drop_graphs(c);  // the launches name the row table's buffers
   std::swap(a.col, c->col_alt[dir]);
   if (c->weighted) std::swap(a.wt, c->wt_alt[dir]);
   return RIPPLE_OK;
@@ -519,12 +553,17 @@ rp::GemmArgs p_gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 
 }
 
 // Layer l's transform on `rows` (nullptr: all, count_fixed of them): one GEMM, or
-// GIN's two (the MLP's hidden rows go through gin_rows). Returns the launches.
+// GIN's two (the MLP's hidden rows go through gin_rows). cleanup (nullable): the
+// batch's clean-up, run by extra blocks of the last launch. Returns the launches.
 int launch_layer_gemm(const ripple_ctx *c, hipStream_t s, int l, const int *rows, const u64 *count,
                       long long count_fixed, float *delta, const u64 *abort, long long max_rows,
-                      long long expected_rows) {
+                      long long expected_rows, const rp::CleanupArgs *cleanup = nullptr) {
   rp::GemmArgs g = gemm_args(c, l, rows, count, count_fixed, delta, abort);
   if (c->agg != rp::kGin) {
+    if (cleanup != nullptr) {
+      g.cleanup = *cleanup;
+      g.cleanup_blocks = rp::cleanup_blocks_for(c->cap_ops);
+    }
     rp::launch_gemm(s, g, max_rows, expected_rows);
     return 1;
   }
@@ -542,6 +581,10 @@ int launch_layer_gemm(const ripple_ctx *c, hipStream_t s, int l, const int *rows
   g2.W = c->W2[l - 1];
   g2.K = c->dims[l];
   g2.bias = c->b2[l - 1];
+  if (cleanup != nullptr) {
+    g2.cleanup = *cleanup;
+    g2.cleanup_blocks = rp::cleanup_blocks_for(c->cap_ops);
+  }
   rp::launch_gemm(s, g2, max_rows, expected_rows);
   return 2;
 }
@@ -614,13 +657,39 @@ int layer_mode(const ripple_ctx *c, int l) {
 }
 
 rp::CompactScratch compact_scratch(ripple_ctx *c, rp::Counters *dc) {
-  c->compact_epoch = c->compact_epoch % 65535 + 1;
-  return rp::CompactScratch{c->compact_lb, c->compact_epoch, &dc->err};
+  return rp::CompactScratch{c->compact_lb, &dc->err};
 }
 
-// Issues one batch. Returns after queuing; the caller syncs.
-void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op *src_ops, const float *src_feat) {
+// The launch plan of the next batch: every host decision its launches depend on.
+struct BatchPlan {
+  int mode[rp::kMaxL + 1];             // [l]: message form of layer l
+  long long tf_rows[rp::kMaxL + 1];    // [l]: expected rows of layer l's transform-first GEMM
+  long long rows[rp::kMaxL + 1];       // [l]: expected rows of layer l's GEMM
+  unsigned long long key;              // the above as GEMM variants, and the counter parity
+};
+
+BatchPlan make_plan(const ripple_ctx *c) {
+  BatchPlan p{};
+  unsigned long long key = static_cast<unsigned long long>(c->parity);
+  int bit = 1;
+  for (int l = 1; l <= c->L; ++l) {
+    p.mode[l] = layer_mode(c, l);
+    p.tf_rows[l] = c->has_batch ? c->last_count[l - 1] : 0;
+    p.rows[l] = c->has_batch ? c->last_count[l] : 0;
+    key |= static_cast<unsigned long long>(p.mode[l]) << bit;
+    key |= static_cast<unsigned long long>(rp::gemm_variant(p.tf_rows[l])) << (bit + 2);
+    key |= static_cast<unsigned long long>(rp::gemm_variant(p.rows[l])) << (bit + 3);
+    bit += 4;
+  }
+  p.key = key;
+  return p;
+}
+
+// Issues one batch's launches (the inputs are in c->h_in). Returns after queuing;
+// the caller syncs. Launches only: the same calls are captured as a graph.
+void issue_batch(ripple_ctx *c, const BatchPlan &p) {
   hipStream_t s = c->stream;
+  const int cap_ops = static_cast<int>(c->cap_ops);
   rp::Counters *dc = c->d_counters + c->parity;  // zeroed by the previous batch's clean-up
   rp::Counters *dnext = c->d_counters + (c->parity ^ 1);
   const int cap_arcs = static_cast<int>(2 * c->cap_ops);
@@ -629,15 +698,17 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
   // (the topology kernels always keep them)
   rp::Adj out_msg = out, in_msg = in;
   if (c->agg != rp::kGcWsum) out_msg.wt = in_msg.wt = nullptr;
-  c->last_pull = 0;
-  c->last_dense = 0;
+  rp::CleanupArgs cleanup{c->d_in,      c->d_ops,      c->op_slot,   c->ht_key,    c->ht_val,    c->ht_net,
+                          c->fop,       out.inscnt,    out.delcnt,   in.inscnt,    in.delcnt,    c->ins_src,
+                          c->ins_dst,   c->del_src,    c->del_dst,   c->ddeg,      dc,           dnext,
+                          c->h_counters};
   PhaseScope total(c, RIPPLE_PHASE_TOTAL);
   {
     PhaseScope ps(c, RIPPLE_PHASE_NET);
-    rp::launch_net_hash(s, src_ops, c->d_ops, B, num_feat_rows, c->undirected, c->weighted ? 1 : 0, c->n, c->ht_key,
+    rp::launch_net_hash(s, cap_ops, c->h_in, c->d_in, c->d_ops, c->undirected, c->weighted ? 1 : 0, c->n, c->ht_key,
                         c->ht_val, c->ht_mask, c->op_slot, c->fop, dc);
-    rp::launch_net_decide(s, c->d_ops, B, c->undirected, c->ht_val, c->ht_net, c->op_slot, c->fop, out, in,
-                          c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank, c->del_rank, c->ins_w,
+    rp::launch_net_decide(s, cap_ops, c->d_in, c->d_ops, c->undirected, c->ht_val, c->ht_net, c->op_slot, c->fop, out,
+                          in, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank, c->del_rank, c->ins_w,
                           c->del_w, c->flist, dc);
     add_launches(c, RIPPLE_PHASE_NET, 2);
   }
@@ -648,12 +719,12 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
     rp::launch_topo_rewrite(s, cap_arcs, c->undirected, c->n, out, in, c->ins_src, c->ins_dst, c->del_src,
                             c->del_dst, c->ins_rank, c->del_rank, c->ht_key, c->ht_net, c->ht_mask, c->d_persist,
                             c->ddeg, dc);
-    rp::launch_topo_put(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->ins_rank, c->ins_w, dc);
-    add_launches(c, RIPPLE_PHASE_TOPO, 3);
+    add_launches(c, RIPPLE_PHASE_TOPO, 2);
   }
   {
     PhaseScope ps(c, RIPPLE_PHASE_LAYER0);
-    rp::launch_corr_mark(s, static_cast<int>(c->cap_ops), cap_arcs, c->agg, layer_ptrs(c), c->adj[0].len, c->ddeg,
+    // also writes the inserted arcs into their slots
+    rp::launch_corr_mark(s, cap_ops, cap_arcs, c->agg, layer_ptrs(c), out, in, c->ins_rank, c->ins_w, c->ddeg,
                          c->flist, c->ins_src, c->ins_dst, c->del_src, c->del_dst,
                          c->agg == rp::kGcWsum ? c->ins_w : nullptr, c->del_w, c->bm_x, dc);
     rp::CompactOut co{};
@@ -662,12 +733,13 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
     co.out_deg = c->adj[0].len;
     co.doff = c->doff[0];
     co.out_total = &dc->pushed[1];
-    const bool members = layer_mode(c, 1) != kPushLayer;  // layer 1 pulls: it needs A^0's membership
+    const bool members = p.mode[1] != kPushLayer;  // layer 1 pulls: it needs A^0's membership
     co.keep = members ? c->keep[0] : nullptr;
     co.wprefix = members ? c->wprefix[0] : nullptr;
     rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
-    rp::launch_delta0(s, c->n, c->agg, c->dims[0], rp::row_ld(c->dims[0]), c->lists[0], &dc->count[0], c->d_ops,
-                      src_feat, c->fop, c->H[0], c->adj[0].len, c->ddeg, c->delta[0], dc);
+    const rp::Delta0Args z{c->agg, c->dims[0], rp::row_ld(c->dims[0]), c->d_ops, c->d_in, c->fop, c->H[0],
+                           c->adj[0].len, c->ddeg, c->delta[0], dc};
+    rp::launch_delta0(s, c->n, z, c->lists[0], &dc->count[0]);
     add_launches(c, RIPPLE_PHASE_LAYER0, 3);
   }
   for (int l = 1; l <= c->L; ++l) {
@@ -681,14 +753,12 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
       // their messages c' P' - c P
       PhaseScope ps(c, RIPPLE_PHASE_GEMM);
       rp::launch_gemm(s, p_gemm_args(c, l, c->lists[l - 1], &dc->count[l - 1], 0, c->msg, &dc->abort), c->n,
-                      c->has_batch ? c->last_count[l - 1] : 0);
+                      p.tf_rows[l]);
       add_launches(c, RIPPLE_PHASE_GEMM, 1);
       msg = c->msg;
     }
-    const int mode = layer_mode(c, l);
+    const int mode = p.mode[l];
     const int ld = rp::row_ld(c->sw[l]);  // message row stride
-    if (mode == kPullLayer) c->last_pull |= 1 << l;
-    if (mode == kDenseLayer) c->last_dense |= 1 << l;
     const unsigned *member = c->keep[(l - 1) & 1];
     const int *wprefix = c->wprefix[(l - 1) & 1];
     if (mode == kDenseLayer) {
@@ -728,7 +798,7 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
       co.in_total = &dc->indeg[l];
       co.out_total = l < c->L ? &dc->pushed[l + 1] : nullptr;
       co.sinks_a = &dc->dest[l];  // distinct sinks of the arcs pushed at layer l
-      const bool members = l < c->L && layer_mode(c, l + 1) != kPushLayer;
+      const bool members = l < c->L && p.mode[l + 1] != kPushLayer;
       co.keep = members ? c->keep[l & 1] : nullptr;
       co.wprefix = members ? c->wprefix[l & 1] : nullptr;
       rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
@@ -741,19 +811,73 @@ void issue_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op 
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     {
+      // the last layer's GEMM also resets the batch's scratch (extra blocks)
       PhaseScope ps(c, RIPPLE_PHASE_GEMM);
-      add_launches(c, RIPPLE_PHASE_GEMM, launch_layer_gemm(c, s, l, c->lists[l], &dc->count[l], 0, dout,
-                                                          &dc->abort, c->n, c->has_batch ? c->last_count[l] : 0));
+      add_launches(c, RIPPLE_PHASE_GEMM,
+                   launch_layer_gemm(c, s, l, c->lists[l], &dc->count[l], 0, dout, &dc->abort, c->n, p.rows[l],
+                                     l == c->L ? &cleanup : nullptr));
     }
   }
-  {
-    PhaseScope ps(c, RIPPLE_PHASE_OTHER);
-    rp::launch_cleanup(s, B, cap_arcs, c->d_ops, c->op_slot, c->ht_key, c->ht_val, c->ht_net, c->fop, out, in,
-                       c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ddeg, dc, dnext, c->h_counters);
-    add_launches(c, RIPPLE_PHASE_OTHER, 1);
-  }
   total.close();
+}
+
+// The executable graph of plan p: a cached one, else a new capture of the batch's
+// launches (nullptr if capturing fails; the caller then launches directly).
+hipGraphExec_t plan_graph(ripple_ctx *c, const BatchPlan &p) {
+  constexpr size_t kMaxGraphs = 16;
+  for (GraphSlot &g : c->graphs) {
+    if (g.key == p.key) {
+      g.used = ++c->graph_clock;
+      return g.exec;
+    }
+  }
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+  hipError_t e = hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal);
+  if (e == hipSuccess) {
+    issue_batch(c, p);
+    e = hipStreamEndCapture(c->stream, &graph);
+  }
+  if (e == hipSuccess) e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  if (e == hipSuccess) e = hipGraphUpload(exec, c->stream);
+  if (graph != nullptr) (void)hipGraphDestroy(graph);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    if (exec != nullptr) (void)hipGraphExecDestroy(exec);
+    c->graphs_failed = true;
+    return nullptr;
+  }
+  if (c->graphs.size() >= kMaxGraphs) {
+    auto old = std::min_element(c->graphs.begin(), c->graphs.end(),
+                                [](const GraphSlot &a, const GraphSlot &b) { return a.used < b.used; });
+    (void)hipGraphExecDestroy(old->exec);
+    c->graphs.erase(old);
+  }
+  c->graphs.push_back(GraphSlot{p.key, exec, ++c->graph_clock});
+  return exec;
+}
+
+// Queues one batch whose inputs are in c->h_in: as a graph replay unless graphs
+// are off or this batch records phase events.
+ripple_status launch_batch(ripple_ctx *c) {
+  const BatchPlan p = make_plan(c);
+  c->last_pull = 0;
+  c->last_dense = 0;
+  for (int l = 1; l <= c->L; ++l) {
+    if (p.mode[l] == kPullLayer) c->last_pull |= 1 << l;
+    if (p.mode[l] == kDenseLayer) c->last_dense |= 1 << l;
+  }
+  c->last_graph = false;
+  hipGraphExec_t g = c->use_graphs && !c->graphs_failed && !c->prof ? plan_graph(c, p) : nullptr;
+  if (g != nullptr) {
+    RP_HIP(c, hipGraphLaunch(g, c->stream));
+    c->last_graph = true;
+  } else {
+    issue_batch(c, p);
+    RP_HIP(c, hipGetLastError());
+  }
   c->parity ^= 1;
+  return RIPPLE_OK;
 }
 
 void account_phases(ripple_ctx *c) {
@@ -851,10 +975,10 @@ ripple_status read_rows(ripple_ctx *c, const float *src, int d, const int32_t *i
     if (ids[i] < 0 || ids[i] >= c->n) return fail(c, RIPPLE_E_INVALID, "ripple: vertex id out of range");
   int *d_ids = nullptr;
   float *d_out = nullptr;
-  RP_TRY(dalloc_n(c, &d_ids, count));
-  ripple_status st = dalloc_n(c, &d_out, count * d);
+  RP_TRY(dalloc_n(c, &d_ids, count, true));
+  ripple_status st = dalloc_n(c, &d_out, count * d, true);
   if (st != RIPPLE_OK) {
-    dfree(c, d_ids);
+    dfree(c, d_ids, true);
     return st;
   }
   hipError_t e = hipMemcpyAsync(d_ids, ids, count * sizeof(int), hipMemcpyHostToDevice, c->stream);
@@ -865,8 +989,8 @@ ripple_status read_rows(ripple_ctx *c, const float *src, int d, const int32_t *i
   if (e == hipSuccess)
     e = hipMemcpyAsync(out, d_out, static_cast<size_t>(count) * d * sizeof(float), hipMemcpyDeviceToHost, c->stream);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
-  dfree(c, d_ids);
-  dfree(c, d_out);
+  dfree(c, d_ids, true);
+  dfree(c, d_out, true);
   if (e != hipSuccess) return device_fail(c, e, "read_rows");
   return RIPPLE_OK;
 }
@@ -1026,8 +1150,11 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   ripple_status st;
   if ((st = dalloc_n(c, &c->d_persist, 1)) != RIPPLE_OK) return bail(st);
   if ((st = dalloc_n(c, &c->d_counters, 2)) != RIPPLE_OK) return bail(st);
+  if ((st = dalloc_n(c, &c->d_in, 1)) != RIPPLE_OK) return bail(st);
   e = hipHostMalloc(reinterpret_cast<void **>(&c->h_counters), sizeof(rp::Counters), hipHostMallocDefault);
+  if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void **>(&c->h_in), sizeof(rp::BatchIn), hipHostMallocDefault);
   if (e != hipSuccess) return bail(device_fail(c, e, "hipHostMalloc"));
+  *c->h_in = rp::BatchIn{};
   std::vector<int> olen(outdeg), ilen(indeg);
   if ((st = upload_adj(c, 0, olen, ocol, ooff, ow)) != RIPPLE_OK) return bail(st);
   if ((st = upload_adj(c, 1, ilen, icol, ioff, iw)) != RIPPLE_OK) return bail(st);
@@ -1190,9 +1317,13 @@ namespace {
 ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op *src_ops,
                         const float *src_feat, const ripple_op *caller_ops, ripple_batch_stats *stats) {
   long long repacks = 0;
+  // the previous call has synchronised, so no kernel still reads the block
+  c->h_in->ops = src_ops;
+  c->h_in->feat = src_feat;
+  c->h_in->num_ops = B;
+  c->h_in->num_feat_rows = num_feat_rows;
   for (int attempt = 0;; ++attempt) {
-    issue_batch(c, B, num_feat_rows, src_ops, src_feat);
-    RP_HIP(c, hipGetLastError());
+    RP_TRY(launch_batch(c));
     RP_TRY(wait_stream(c));
     if (c->h_counters->bad_op) {
       // rejected on the device before anything was mutated: name the first bad op
@@ -1255,6 +1386,7 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
     for (int l = 1; l <= c->L; ++l) stats->in_arcs[l] = static_cast<int64_t>(k.indeg[l]);
     stats->pull_layers = c->last_pull;
     stats->dense_layers = c->last_dense;
+    stats->graph_replay = c->last_graph ? 1 : 0;
   }
   return RIPPLE_OK;
 }
@@ -1433,6 +1565,14 @@ ripple_status ripple_set_scatter_mode(ripple_ctx *c, int32_t mode) {
   return RIPPLE_OK;
 }
 
+ripple_status ripple_set_graphs(ripple_ctx *c, int32_t enable) {
+  RP_TRY(check_ctx(c));
+  if (enable != 0 && enable != 1) return fail(c, RIPPLE_E_INVALID, "ripple: enable must be 0 or 1");
+  c->use_graphs = enable == 1;
+  if (!c->use_graphs) drop_graphs(c);
+  return RIPPLE_OK;
+}
+
 ripple_status ripple_device_bytes(ripple_ctx *c, int64_t *bytes) {
   if (c == nullptr || bytes == nullptr) return RIPPLE_E_INVALID;
   *bytes = c->bytes;
@@ -1489,6 +1629,7 @@ void ripple_destroy(ripple_ctx *c) {
   if (c == nullptr) return;
   (void)hipSetDevice(c->device);
   if (c->stream) (void)hipStreamSynchronize(c->stream);
+  drop_graphs(c);
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
   free_model(c);
   for (int d = 0; d < 2; ++d) {
@@ -1512,7 +1653,9 @@ void ripple_destroy(ripple_ctx *c) {
   dfree_t(c, c->rl_cap);
   dfree_t(c, c->d_counters);
   dfree_t(c, c->d_persist);
+  dfree_t(c, c->d_in);
   if (c->h_counters) (void)hipHostFree(c->h_counters);
+  if (c->h_in) (void)hipHostFree(c->h_in);
   if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);
   delete c;
 }

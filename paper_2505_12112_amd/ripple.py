@@ -30,6 +30,7 @@ EXPORTED = [
     "ripple_get_affected", "ripple_get_aggregates", "ripple_get_arcs", "ripple_device_bytes",
     "ripple_set_profiling", "ripple_get_phase_stats", "ripple_phase_name", "ripple_last_error",
     "ripple_destroy", "ripple_set_scatter_mode", "ripple_apply_updates_device", "ripple_get_arc_weights",
+    "ripple_set_graphs",
 ]
 SCATTER = {"auto": 0, "push": 1, "pull": 2, "dense": 3}
 
@@ -73,7 +74,7 @@ class BatchStats(C.Structure):
         ("pushed_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("dest_rows", C.c_int64 * (MAX_LAYERS + 1)),
         ("relocated_rows", C.c_int64), ("repacks", C.c_int64),
         ("in_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("pull_layers", C.c_int32), ("dense_layers", C.c_int32),
-        ("reweighted_arcs", C.c_int64),
+        ("reweighted_arcs", C.c_int64), ("graph_replay", C.c_int64),
     ]
 
 
@@ -106,6 +107,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.ripple_device_bytes.argtypes = [vp, P(C.c_int64)]
     lib.ripple_set_profiling.argtypes = [vp, C.c_int32]
     lib.ripple_set_scatter_mode.argtypes = [vp, C.c_int32]
+    lib.ripple_set_graphs.argtypes = [vp, C.c_int32]
     lib.ripple_get_phase_stats.argtypes = [vp, P(PhaseStats), C.c_int32]
     lib.ripple_phase_name.argtypes = [C.c_int32]
     lib.ripple_phase_name.restype = C.c_char_p
@@ -253,7 +255,7 @@ class Ripple:
             "pushed_arcs": list(st.pushed_arcs[:L + 1]), "dest_rows": list(st.dest_rows[:L + 1]),
             "relocated_rows": st.relocated_rows, "repacks": st.repacks,
             "in_arcs": list(st.in_arcs[:L + 1]), "pull_layers": st.pull_layers, "dense_layers": st.dense_layers,
-            "reweighted_arcs": st.reweighted_arcs,
+            "reweighted_arcs": st.reweighted_arcs, "graph_replay": st.graph_replay,
         }
 
     def apply_updates_raw(self, ops: np.ndarray, feat_rows: Optional[np.ndarray], stats: BatchStats) -> None:
@@ -327,6 +329,10 @@ class Ripple:
     def set_scatter_mode(self, mode: str):
         """"auto" (default), "push", "pull" or "dense": how layers add their messages."""
         self._check(self._lib.ripple_set_scatter_mode(self._ctx, SCATTER[mode]))
+
+    def set_graphs(self, enable: bool):
+        """True: batches replay captured HIP graphs; False (default): kernels are queued one by one."""
+        self._check(self._lib.ripple_set_graphs(self._ctx, 1 if enable else 0))
 
     def device_bytes(self) -> int:
         b = C.c_int64()

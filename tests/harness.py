@@ -56,10 +56,12 @@ def _hip():
 
 class Pair:
     def __init__(self, n, src, dst, x, weights, undirected=False, transform_first=-1, mode="auto", inputs="host",
-                 edge_w=None, **lib_kw):
+                 edge_w=None, graphs=False, **lib_kw):
         self.lib = Ripple(n, src, dst, undirected=undirected, weights=edge_w, **lib_kw)
         self.lib.init_embeddings(x, weights, transform_first=transform_first)
         self.lib.set_scatter_mode(mode)
+        self.lib.set_graphs(graphs)
+        self.graphs = graphs  # batches replay captured HIP graphs, else kernels are queued one by one
         self.inputs = inputs  # "host": ripple_apply_updates; "device": the batch staged in HBM first
         self.orc = O.OracleState(n, src, dst, x, O.OracleModel.from_weights(weights), undirected, edge_w)
         self.L = len(weights.dims) - 1
@@ -88,6 +90,7 @@ class Pair:
             assert st["ins_arcs"] == net.ins_src.size
             assert st["del_arcs"] == net.del_src.size
             assert st["reweighted_arcs"] == net.rew_src.size
+            assert st["graph_replay"] == int(self.graphs), "the batch did not run the way the test asked"
             assert st["features"] == net.features.size
             assert st["edge_keys"] == net.edge_keys
             assert st["noop_edge_ops"] == net.noop_edge_ops

@@ -10,7 +10,7 @@ import pytest
 
 from oracle import ripple_oracle as O
 from paper_2505_12112_amd import synth
-from paper_2505_12112_amd.ripple import Ripple, RippleError, E_INVALID, E_STATE, E_OOM
+from paper_2505_12112_amd.ripple import PHASES, Ripple, RippleError, E_INVALID, E_STATE, E_OOM
 from tests.harness import Pair, random_valid_batch, FP32_TOL
 
 pytestmark = pytest.mark.gpu
@@ -51,14 +51,16 @@ def test_bootstrap_matches_full_recompute(agg, dims):
         p.close()
 
 
+@pytest.mark.parametrize("launch", ["graph", "direct"])
 @pytest.mark.parametrize("inputs", ["host", "device"])
 @pytest.mark.parametrize("mode", ["push", "pull", "dense"])
-def test_tiny_config_stream(mode, inputs):
+def test_tiny_config_stream(mode, inputs, launch):
     """The tiny workload as specified: 10 batches of 45 inserts, 45 deletes, 10
-    features, handed over from host memory or already resident in device memory."""
-    _say("tiny config", mode, inputs)
+    features, handed over from host memory or already resident in device memory,
+    replayed as captured graphs or queued kernel by kernel."""
+    _say("tiny config", mode, inputs, launch)
     wl = synth.build_workload("tiny")
-    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, mode=mode, inputs=inputs)
+    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, mode=mode, inputs=inputs, graphs=launch == "graph")
     try:
         for b in range(10):
             st, net, sets = p.step(wl.stream.next_batch(100))
@@ -172,6 +174,41 @@ def test_unaffected_rows_stay_bit_identical():
         p.close()
 
 
+def test_graph_replays_follow_sizes_pointers_and_plans():
+    """One context, graphs on: batch sizes from 0 to 300 (the scratch grows, which
+    drops the captured graphs), inputs alternating between host memory and fresh
+    device buffers (new pointers every batch, same graphs), the message form
+    switched between batches (new plans), a slack-free adjacency whose spare arena
+    fills (re-layouts move the row table, which drops the graphs), embedding reads
+    in between, and a few batches that record phase events (queued kernel by
+    kernel). Every batch is checked against the oracle."""
+    rng = np.random.default_rng(21)
+    dims = (10, 24, 7)
+    src, dst, x, w = _small(rng, 250, 900, dims, "gcn")
+    p = Pair(250, src, dst, x, w, slack=0.0, min_slack=0, arena_slots=64, graphs=True)
+    try:
+        sizes = [0, 1, 3, 17, 60, 5, 300, 2, 40, 40, 40, 1, 120]
+        modes = ["auto", "push", "pull", "dense"]
+        relayouts = 0
+        for b in range(52):
+            p.inputs = "device" if b % 2 else "host"
+            p.lib.set_scatter_mode(modes[(b // 5) % 4])
+            prof = b % 13 == 12
+            p.lib.set_profiling(PHASES if prof else ())
+            p.graphs = not prof
+            batch = random_valid_batch(rng, p.orc, sizes[b % len(sizes)], dims[0], mix=(0.6, 0.3, 0.1))
+            st, _, _ = p.step(batch)
+            relayouts += st["repacks"]
+            if b % 4 == 3:
+                p.check_embeddings()
+        assert relayouts > 0, "the arena never filled: the re-layout path was not exercised"
+        p.check_embeddings()
+        p.check_arcs()
+        p.check_aggregates()
+    finally:
+        p.close()
+
+
 def test_empty_and_noop_batches():
     rng = np.random.default_rng(13)
     dims = (6, 8, 3)
@@ -265,15 +302,18 @@ def test_call_order_and_device_byte_cap():
         lib.close()
 
 
-@pytest.mark.parametrize("agg,mode", [(a, m) for a in ("sum", "mean", "gcn") for m in ("auto", "pull", "dense")]
-                         + [(a, m) for a in ("gc_sum", "gc_mean", "gin", "gc_wsum") for m in ("auto", "dense")])
-def test_thousand_batches_on_a_small_graph(agg, mode):
-    """1000 consecutive batches: sets every batch, embeddings every 100 and at the end."""
-    _say("1000 batches", agg, mode)
+@pytest.mark.parametrize("agg,mode,launch",
+                         [(a, m, "direct") for a in ("sum", "mean", "gcn") for m in ("auto", "pull", "dense")]
+                         + [(a, m, "direct") for a in ("gc_sum", "gc_mean", "gin", "gc_wsum") for m in ("auto", "dense")]
+                         + [("sum", "auto", "graph"), ("gcn", "dense", "graph"), ("gin", "auto", "graph")])
+def test_thousand_batches_on_a_small_graph(agg, mode, launch):
+    """1000 consecutive batches: sets every batch, embeddings every 100 and at the
+    end; with launch "graph" every batch replays a captured graph."""
+    _say("1000 batches", agg, mode, launch)
     rng = np.random.default_rng(16 + AGGS.index(agg))
     dims = (16, 32, 8)
     src, dst, x, w = _small(rng, 400, 2400, dims, agg)
-    p = Pair(400, src, dst, x, w, mode=mode, edge_w=_edge_w(rng, agg, src.size))
+    p = Pair(400, src, dst, x, w, mode=mode, edge_w=_edge_w(rng, agg, src.size), graphs=launch == "graph")
     try:
         worst = 0.0
         for b in range(1000):
