@@ -85,6 +85,15 @@ struct LayerPtrs {
   int L;
 };
 
+// True if the batch aborted (ab = its abort flag). The counts a kernel loads with
+// the flag join the test (none is negative, so they never change its outcome):
+// then every one of those loads is issued before the branch and the kernel waits
+// for them once, instead of waiting for the flag before it loads the rest.
+template <typename... T>
+__device__ inline bool aborted_with(u64 ab, T... counts) {
+  return (ab | static_cast<u64>((static_cast<long long>(counts) | ... | 0LL)) >> 63) != 0;
+}
+
 // The per-batch scratch a batch touched, reset by its last kernel (see
 // batch_cleanup).
 struct CleanupArgs {

@@ -46,12 +46,12 @@ __global__ void k_corr_mark(int agg, LayerPtrs lp, Adj out, Adj in, const int *i
                             const int *ddeg, const int *flist, const int *ins_src, const int *ins_dst,
                             const int *del_src, const int *del_dst, const float *ins_w, const float *del_w,
                             unsigned *bm, Counters *c) {
-  if (c->abort) return;
-  const int lane = lane_id();
-  const int *out_len = out.len;
   const long long nf = static_cast<long long>(c->n_feat);
   const long long ni = static_cast<long long>(c->n_ins);
   const long long na = ni + static_cast<long long>(c->n_del);
+  if (aborted_with(c->abort, nf, na)) return;
+  const int lane = lane_id();
+  const int *out_len = out.len;
   {
     // item w = 2 * arc + direction: its row's inserts follow the kept entries, in
     // rank order
@@ -229,13 +229,14 @@ __device__ inline bool fetch(const u64 *p, u64 epoch, long long (&v)[kVals]) {
   return ok;
 }
 
-// Single-pass compaction (a decoupled look-back prefix scan). Blocks take tiles of
-// kWordsPerBlock bitmap words in ticket order, so a tile's predecessors are already
-// running. Each tile publishes its sums at once, then wave 0 walks back over the
-// predecessors (64 per step), adding their tile sums until it meets one that has
-// published its inclusive prefix. A tile publishes its own sums before it waits, so
-// every wait is for work that needs no waiting: all waits end. A wait that outlasts
-// kSpinLimit polls sets bit 2 of the error word and counts the tile as empty (the
+// Single-pass compaction (a decoupled look-back prefix scan). Block b takes tile b
+// of kWordsPerBlock bitmap words; blocks are dispatched in index order, so a
+// tile's predecessors are running or done. Each tile publishes its sums at once,
+// then wave 0 walks back over the predecessors (64 per step), adding their tile
+// sums until it meets one that has published its inclusive prefix. A tile
+// publishes its own sums before it waits, so every wait is for work that needs no
+// waiting: all waits end. A wait that outlasts kSpinLimit polls (a predecessor
+// that never ran) sets bit 2 of the error word and counts the tile as empty (the
 // batch then fails loudly instead of hanging).
 // Output: the marked vertices of both bitmaps as a sorted list with prefix sums of
 // their out- and in-degrees, membership words and per-word prefix counts; both
@@ -244,20 +245,10 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
                                                              CompactOut o, u64 *agg, u64 *inc, u64 *ticket,
                                                              u64 *err) {
   __shared__ long long red[kCompactWaves][kVals];
-  __shared__ long long tile_s, base_s[kVals];
+  __shared__ long long base_s[kVals];
   __shared__ u64 epoch_s;
   const long long tiles = gridDim.x;
-  if (threadIdx.x == 0) {
-    // The ticket counter only grows and every launch on this scratch has the same
-    // number of tiles, each taking one ticket, so launch k holds tickets k * tiles
-    // .. k * tiles + tiles - 1: the ticket names both the tile and the launch.
-    const u64 t = atomicAdd(ticket, 1ull);
-    tile_s = static_cast<long long>(t % static_cast<u64>(tiles));
-    epoch_s = t / static_cast<u64>(tiles) % 65535 + 1;
-  }
-  __syncthreads();
-  const long long tile = tile_s;
-  const u64 epoch = epoch_s;
+  const long long tile = blockIdx.x;
   const long long w0 = tile * kWordsPerBlock + threadIdx.x * kWordsPerThread;
   const int *odeg = o.doff != nullptr || o.out_total != nullptr ? o.out_deg : nullptr;
   const int *ideg = o.ioff != nullptr || o.in_total != nullptr ? o.in_deg : nullptr;
@@ -273,13 +264,20 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
   } else {
     load_words(bm_a, bm_b, w0, words, wv, pop_a);
   }
+  u64 ticket_no = 0;
+  if (threadIdx.x == 0) ticket_no = atomicAdd(ticket, 1ull);  // in flight beside the loads
   long long st[kVals] = {0, 0, 0, pop_a};
 #pragma unroll
   for (int i = 0; i < kWordsPerThread; ++i) st[0] += __popc(wv[i]);
   int d0[kBatch], i0[kBatch];
   degree_sums(BitCursor(wv, w0), odeg, ideg, st[1], st[2], d0, i0);
+  // The ticket counter only grows and every launch on this scratch has the same
+  // number of blocks, each taking one ticket, so launch k holds tickets k * tiles
+  // .. k * tiles + tiles - 1: the ticket's quotient names the launch.
+  if (threadIdx.x == 0) epoch_s = ticket_no / static_cast<u64>(tiles) % 65535 + 1;
   long long ex[kVals], tot[kVals];
-  block_scan(st, ex, tot, red);
+  block_scan(st, ex, tot, red);  // its barriers also publish epoch_s
+  const u64 epoch = epoch_s;
   if (threadIdx.x == 0) publish((tile == 0 ? inc : agg) + tile * kVals, epoch, tot);
   if (threadIdx.x < kWave) {
     const int lane = lane_id();
@@ -434,10 +432,10 @@ __device__ inline long long owner_from(const long long *a, long long from, long 
 
 // One wave per listed vertex (see Delta0Args).
 __global__ void k_delta0(Delta0Args z, const int *list, const u64 *count) {
-  if (z.c->abort) return;
   const long long m = static_cast<long long>(*count);
-  const int lane = lane_id();
   const float *feat = z.in->feat;
+  if (aborted_with(z.c->abort, m)) return;
+  const int lane = lane_id();
   for (long long j = global_wave(); j < m; j += num_waves()) {
     const int u = list[j];
     const int fo = z.fop[u];
@@ -472,13 +470,13 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
                                                  const float *delta, Adj out, float *S, unsigned *bm_out,
                                                  unsigned *bm_x, const int *ins_dst, const int *del_dst,
                                                  const u64 *pushed, const Counters *c, int mark_list) {
-  if (c->abort) return;
-  const int lane = lane_id();
   const long long nD = static_cast<long long>(*count);
   const long long E = static_cast<long long>(*pushed);
+  const long long ni = static_cast<long long>(c->n_ins);
+  const long long na = ni + static_cast<long long>(c->n_del);
+  if (aborted_with(c->abort, nD, E, na)) return;
+  const int lane = lane_id();
   {
-    const long long ni = static_cast<long long>(c->n_ins);
-    const long long na = ni + static_cast<long long>(c->n_del);
     const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
     const long long t0 = blockIdx.x * blockDim.x + threadIdx.x;
     for (long long i = t0; i < na; i += stride) mark_only(bm_x, i < ni ? ins_dst[i] : del_dst[i - ni]);
@@ -587,13 +585,13 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
                                                    const Counters *c) {
   __shared__ int2 pairs[256 / kWave][kPullChunk];
   __shared__ float pair_w[256 / kWave][kPullChunk];  // the in-arcs' weights (weighted graphs)
-  if (c->abort) return;
+  const long long nA = static_cast<long long>(*count);
+  if (aborted_with(c->abort, nA)) return;
   const int lane = lane_id();
   const int grp = lane / G, k0 = lane % G;
   int2 *wp = pairs[threadIdx.x / kWave];
   float *ww = pair_w[threadIdx.x / kWave];
   const bool weighted = in.wt != nullptr;
-  const long long nA = static_cast<long long>(*count);
   const long long E = ioff[nA];
   const long long waves = num_waves();
   int C = 1;

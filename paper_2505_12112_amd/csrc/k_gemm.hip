@@ -148,6 +148,18 @@ __device__ inline void epilogue(const GemmArgs &a, long long m, int v, int col, 
   *hp = y;
 }
 
+// Reads the abort flag and the row count (batch launches have both, bootstrap
+// launches neither) in one round of loads; true if the batch aborted.
+__device__ inline bool abort_or_rows(const GemmArgs &a, long long &M) {
+  if (a.abort != nullptr && a.count != nullptr) {
+    const u64 ab = *a.abort;
+    M = static_cast<long long>(*a.count);
+    return aborted_with(ab, M);
+  }
+  M = a.count_fixed;
+  return a.abort != nullptr && *a.abort != 0;
+}
+
 // The launch's last a.cleanup_blocks blocks reset the batch's scratch instead of
 // computing tiles (true for them); the others take tiles with stride gemm_grid.
 __device__ inline bool cleanup_role(const GemmArgs &a, unsigned &gemm_grid) {
@@ -164,8 +176,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
   using Sh = Shape<BM, BN, WM, WN>;
   unsigned gemm_grid;
   if (cleanup_role(a, gemm_grid)) return;
-  if (a.abort != nullptr && *a.abort) return;
-  const long long M = a.count != nullptr ? static_cast<long long>(*a.count) : a.count_fixed;
+  long long M;
+  if (abort_or_rows(a, M)) return;
   const int N = a.N, K = a.K;
   const long long tiles_n = (N + BN - 1) / BN;
   const long long tiles = ((M + BM - 1) / BM) * tiles_n;
@@ -324,8 +336,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
   static_assert(kRowsBM * BN % kThreads == 0, "whole elements per thread");
   unsigned gemm_grid;
   if (cleanup_role(a, gemm_grid)) return;
-  if (a.abort != nullptr && *a.abort) return;
-  const long long M = a.count != nullptr ? static_cast<long long>(*a.count) : a.count_fixed;
+  long long M;
+  if (abort_or_rows(a, M)) return;
   const int N = a.N, K = a.K, dp = a.dprev;
   const long long tiles_n = (N + BN - 1) / BN;
   const long long tiles = ((M + kRowsBM - 1) / kRowsBM) * tiles_n;

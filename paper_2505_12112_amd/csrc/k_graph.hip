@@ -153,6 +153,7 @@ __global__ void k_net_decide(const BatchIn *bin, const ripple_op *ops, int undir
   const long long B = bin->num_ops;
   for (long long i = global_wave(); i < B; i += num_waves()) {
     const ripple_op op = ops[i];
+    const int s = op_slot[i];
     if (op.kind == RIPPLE_OP_FEATURE) {
       if (lane == 0 && fop[op.u] == i) {
         const u64 j = atomicAdd(&c->n_feat, 1ull);
@@ -160,17 +161,23 @@ __global__ void k_net_decide(const BatchIn *bin, const ripple_op *ops, int undir
       }
       continue;
     }
-    const int s = op_slot[i];
-    if (s < 0 || ht_val[s] != i) continue;  // self-loop, or a later op names this edge
     int a = op.u, b = op.v;
     if (undirected && a > b) {
       const int t = a;
       a = b;
       b = t;
     }
+    // what the decision needs from the op's slot and rows, in one round of loads
+    // (ids are in range: failing ops became self-loops); the non-negative values
+    // join the test so that no load waits behind it
+    const int winner = s >= 0 ? ht_val[s] : -1;
     const int la = out.len[a], lb = in.len[b];
+    const long long oa = out.off[a], ob = in.off[b];
+    if (static_cast<int>(s < 0 || winner != i) |
+        (la | lb | static_cast<int>(oa >> 32) | static_cast<int>(ob >> 32)) >> 31)
+      continue;  // self-loop, or a later op names this edge
     const bool use_out = la <= lb;
-    const long long row0 = use_out ? out.off[a] : in.off[b];
+    const long long row0 = use_out ? oa : ob;
     const int pos = wave_find((use_out ? out.col : in.col) + row0, use_out ? la : lb, use_out ? b : a);
     const bool present = pos >= 0;
     const bool want = op.kind == RIPPLE_OP_INSERT;
@@ -215,9 +222,9 @@ __global__ void k_topo_plan(Adj out, Adj in, const int *ins_src, const int *ins_
   const long long ni = 2 * static_cast<long long>(c->n_ins);
   const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
   for (long long w = blockIdx.x * blockDim.x + threadIdx.x; w < ni; w += stride) {
-    if (ins_rank[w] != 0) continue;  // one planner per row
     int dir, row, entry;
     item_row(w, ins_src, ins_dst, dir, row, entry);
+    if ((ins_rank[w] | row >> 31) != 0) continue;  // one planner per row (row >= 0: see k_topo_rewrite)
     const Adj &a = dir ? in : out;
     const int need = a.len[row] - a.delcnt[row] + a.inscnt[row];
     if (need > a.cap[row]) {
@@ -248,25 +255,26 @@ __global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, con
                                const int *ins_dst, const int *del_src, const int *del_dst, const int *ins_rank,
                                const int *del_rank, const u64 *ht_key, const int *ht_net, unsigned mask,
                                Persist *p, int *ddeg, Counters *c) {
-  if (c->abort) return;
-  const int lane = lane_id();
   const long long ni = 2 * static_cast<long long>(c->n_ins);
   const long long nd = 2 * static_cast<long long>(c->n_del);
+  if (aborted_with(c->abort, ni, nd)) return;
+  const int lane = lane_id();
   for (long long w = global_wave(); w < ni + nd; w += num_waves()) {
+    const bool ins_item = w < ni;
+    const long long x = ins_item ? w : w - ni;
     int dir, row, entry;
-    if (w < ni) {
-      if (ins_rank[w] != 0) continue;
-      item_row(w, ins_src, ins_dst, dir, row, entry);
-    } else {
-      if (del_rank[w - ni] != 0) continue;
-      item_row(w - ni, del_src, del_dst, dir, row, entry);
-      if ((dir ? in : out).inscnt[row] != 0) continue;  // the insert owner handles this row
-    }
+    item_row(x, ins_item ? ins_src : del_src, ins_item ? ins_dst : del_dst, dir, row, entry);
+    const int rank = (ins_item ? ins_rank : del_rank)[x];
+    if ((rank | row >> 31) != 0) continue;  // not the row's first item (row >= 0 joins the test,
+                                            // so its load is not held back behind the rank's)
     const Adj &a = dir ? in : out;
-    const int len0 = a.len[row], k = a.delcnt[row], nins = a.inscnt[row];
-    const int need = len0 - k + nins;
-    const bool move = nins > 0 && need > a.cap[row];
+    const int len0 = a.len[row], k = a.delcnt[row], nins = a.inscnt[row], cap0 = a.cap[row];
     const long long src_off = a.off[row];
+    // a row with inserts belongs to its first insert item (cap0, src_off >= 0 join
+    // the test so that their loads go out with the others)
+    if (static_cast<int>(!ins_item && nins != 0) | (cap0 | static_cast<int>(src_off >> 32)) >> 31) continue;
+    const int need = len0 - k + nins;
+    const bool move = nins > 0 && need > cap0;
     long long dst_off = src_off;
     int nc = 0;
     if (move) {
