@@ -86,7 +86,8 @@ struct LayerPtrs {
 };
 
 // True if the batch aborted (ab = its abort flag). The counts a kernel loads with
-// the flag join the test (none is negative, so they never change its outcome):
+// the flag join the test (callers pass only values that cannot be negative, so
+// they never change its outcome):
 // then every one of those loads is issued before the branch and the kernel waits
 // for them once, instead of waiting for the flag before it loads the rest.
 template <typename... T>
@@ -337,6 +338,7 @@ struct GemmArgs {
   // batch_cleanup(cleanup) instead (the batch's last GEMM)
   int cleanup_blocks;
   CleanupArgs cleanup;
+  long long max_rows;  // rows (list entries) the launch may read; set by launch_gemm
 };
 // Blocks a batch's clean-up takes for cap_ops ops.
 int cleanup_blocks_for(long long cap_ops);

@@ -430,14 +430,19 @@ __device__ inline long long owner_from(const long long *a, long long from, long 
   return from + cnt - 1;
 }
 
-// One wave per listed vertex (see Delta0Args).
-__global__ void k_delta0(Delta0Args z, const int *list, const u64 *count) {
+// One wave per listed vertex (see Delta0Args). list holds cap entries: the wave's
+// first vertex is fetched with the count (an entry past the count is dropped).
+__global__ void k_delta0(Delta0Args z, const int *list, const u64 *count, long long cap) {
+  const long long j0 = global_wave();
+  const int u0 = j0 < cap ? list[j0] : 0;
   const long long m = static_cast<long long>(*count);
   const float *feat = z.in->feat;
-  if (aborted_with(z.c->abort, m)) return;
+  // (an entry past the count may hold anything: it joins the test as an unsigned
+  // half, which is never negative)
+  if (aborted_with(z.c->abort, m, static_cast<unsigned>(u0) >> 1)) return;
   const int lane = lane_id();
-  for (long long j = global_wave(); j < m; j += num_waves()) {
-    const int u = list[j];
+  for (long long j = j0; j < m; j += num_waves()) {
+    const int u = j == j0 ? u0 : list[j];
     const int fo = z.fop[u];
     float cn = 1.0f, co = 1.0f;
     if (z.agg == kGcn) {
@@ -818,7 +823,7 @@ void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, 
 }
 
 void launch_delta0(hipStream_t s, long long n, const Delta0Args &z, const int *list, const u64 *count) {
-  hipLaunchKernelGGL(k_delta0, dim3(blocks_for(n * kWave, 256, 2048)), dim3(256), 0, s, z, list, count);
+  hipLaunchKernelGGL(k_delta0, dim3(blocks_for(n * kWave, 256, 2048)), dim3(256), 0, s, z, list, count, n);
 }
 
 long long compact_scratch_words(long long n) { return 2LL * compact_blocks(n) * kVals + 1; }

@@ -149,12 +149,14 @@ __device__ inline void epilogue(const GemmArgs &a, long long m, int v, int col, 
 }
 
 // Reads the abort flag and the row count (batch launches have both, bootstrap
-// launches neither) in one round of loads; true if the batch aborted.
-__device__ inline bool abort_or_rows(const GemmArgs &a, long long &M) {
+// launches neither) in one round of loads, together with whatever loads produced
+// `more` (non-negative values); true if the batch aborted.
+template <typename... T>
+__device__ inline bool abort_or_rows(const GemmArgs &a, long long &M, T... more) {
   if (a.abort != nullptr && a.count != nullptr) {
     const u64 ab = *a.abort;
     M = static_cast<long long>(*a.count);
-    return aborted_with(ab, M);
+    return aborted_with(ab, M, more...);
   }
   M = a.count_fixed;
   return a.abort != nullptr && *a.abort != 0;
@@ -336,19 +338,37 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
   static_assert(kRowsBM * BN % kThreads == 0, "whole elements per thread");
   unsigned gemm_grid;
   if (cleanup_role(a, gemm_grid)) return;
-  long long M;
-  if (abort_or_rows(a, M)) return;
   const int N = a.N, K = a.K, dp = a.dprev;
   const long long tiles_n = (N + BN - 1) / BN;
-  const long long tiles = ((M + kRowsBM - 1) / kRowsBM) * tiles_n;
-
-  __shared__ float red[4][kRowsBM][BN + 1];
-
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
   const int lr = lane & 15;
   const int lq = lane >> 4;
+  // row ids of tile t up to `limit`: the lane's operand row and the rows of its
+  // output elements (-1 past the limit)
+  int va, ve[kEl];
+  const auto row_ids = [&](long long t, long long limit) {
+    const long long m0 = (t / tiles_n) * kRowsBM;
+    const long long ar = m0 + lr;
+    va = ar < limit ? (a.rows != nullptr ? a.rows[ar] : static_cast<int>(ar)) : -1;
+#pragma unroll
+    for (int i = 0; i < kEl; ++i) {
+      const long long row = m0 + (tid + i * kThreads) / BN;
+      ve[i] = row < limit ? (a.rows != nullptr ? a.rows[row] : static_cast<int>(row)) : -1;
+    }
+  };
+  // The first tile's ids are fetched with the row count: the list holds max_rows
+  // ids, so ids read past the count stay in bounds; they are dropped below.
+  row_ids(blockIdx.x, a.max_rows);
+  long long M;
+  // (ids past the count may hold anything: they join the test as unsigned halves,
+  // which are never negative)
+  if (abort_or_rows(a, M, static_cast<unsigned>(va) >> 1, static_cast<unsigned>(ve[0]) >> 1)) return;
+  const long long tiles = ((M + kRowsBM - 1) / kRowsBM) * tiles_n;
+
+  __shared__ float red[4][kRowsBM][BN + 1];
+
   const int kw = (K + 63) / 64 * 16;  // k values per wave, a multiple of 16
   const int kb = wave * kw;
   const int ke = K < kb + kw ? K : kb + kw;
@@ -356,16 +376,16 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
   for (long long t = blockIdx.x; t < tiles; t += gemm_grid) {
     const long long m0 = (t / tiles_n) * kRowsBM;
     const int n0 = static_cast<int>(t % tiles_n) * BN;
-    // row ids: the lane's operand row and the rows of its output elements
-    const long long ar = m0 + lr;
-    const int va = ar < M ? (a.rows != nullptr ? a.rows[ar] : static_cast<int>(ar)) : -1;
-    const long long arow = MODE == kGin2 ? (ar < M ? ar : -1) : va;  // operand row (kGin2: list position)
-    int ve[kEl];
+    if (t == blockIdx.x) {  // the prefetched ids: drop those past the count
+      if (m0 + lr >= M) va = -1;
 #pragma unroll
-    for (int i = 0; i < kEl; ++i) {
-      const long long row = m0 + (tid + i * kThreads) / BN;
-      ve[i] = row < M ? (a.rows != nullptr ? a.rows[row] : static_cast<int>(row)) : -1;
+      for (int i = 0; i < kEl; ++i)
+        if (m0 + (tid + i * kThreads) / BN >= M) ve[i] = -1;
+    } else {
+      row_ids(t, M);
     }
+    const long long ar = m0 + lr;
+    const long long arow = MODE == kGin2 ? (ar < M ? ar : -1) : va;  // operand row (kGin2: list position)
     // operand-row scales (layer mode): mean t = 1/deg_in; GCN t = (deg_in+1)^-1/2,
     // s = (deg_out+1)^-1/2
     float ta = 1.f, sa = 0.f;
@@ -584,7 +604,9 @@ int cleanup_blocks_for(long long cap_ops) {
   return static_cast<int>(b < 1 ? 1 : b > 256 ? 256 : b);
 }
 
-void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows, long long expected_rows) {
+void launch_gemm(hipStream_t s, const GemmArgs &args, long long max_rows, long long expected_rows) {
+  GemmArgs a = args;
+  a.max_rows = max_rows;
   const bool big = gemm_variant(expected_rows) == 1;
   if (a.mode == kTransformFirst) launch_mode<kTransformFirst>(s, a, max_rows, big);
   else if (a.mode == kPlain) launch_mode<kPlain>(s, a, max_rows, big);
