@@ -764,20 +764,28 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p) {
     if (mode == kDenseLayer) {
       // dense: mark the net arcs' heads and D (no arcs), list every vertex with its
       // in-arc prefix, pull over every in-arc and mark the sinks that received a
-      // message
+      // message (the listing is timed with the compactions)
+      {
+        PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
+        rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out_msg,
+                           c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->zero, dc, false,
+                           rp::has_self_term(c->agg));
+        add_launches(c, RIPPLE_PHASE_SCATTER, 1);
+      }
+      {
+        PhaseScope ps(c, RIPPLE_PHASE_COMPACT);
+        rp::CompactOut all{};
+        all.full_n = c->n;
+        all.count = &dc->count_all;
+        all.in_deg = c->adj[1].len;
+        all.ioff = c->ioff;
+        rp::launch_compact(s, c->n, nullptr, nullptr, compact_scratch(c, dc), all);
+        add_launches(c, RIPPLE_PHASE_COMPACT, 1);
+      }
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
-      rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out_msg,
-                         c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->zero, dc, false,
-                         rp::has_self_term(c->agg));
-      rp::CompactOut all{};
-      all.full_n = c->n;
-      all.count = &dc->count_all;
-      all.in_deg = c->adj[1].len;
-      all.ioff = c->ioff;
-      rp::launch_compact(s, c->n, nullptr, nullptr, compact_scratch(c, dc), all);
       rp::launch_pull_msgs(s, c->n, c->sw[l], ld, nullptr, &dc->count_all, c->ioff, in_msg, member, wprefix, msg,
                            c->S[l], c->bm_out, dc);
-      add_launches(c, RIPPLE_PHASE_SCATTER, 3);
+      add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     } else {
       // push: marks + atomic adds; pull: marks only (the adds follow the compaction)
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
@@ -895,8 +903,12 @@ void account_phases(ripple_ctx *c) {
     c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * k.pushed[l] + 8.0 * nd + 4.0 * d * nd + 8.0 * d * k.dest[l];
     if (c->last_pull >> l & 1)  // pull: every in-arc id of A^l and its in-row offset
       c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * k.indeg[l] + 12.0 * k.count[l];
-    if (c->last_dense >> l & 1)  // dense: every in-arc id and every vertex's in-row offset
-      c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * static_cast<double>(c->arcs_now) + 12.0 * static_cast<double>(c->n);
+    if (c->last_dense >> l & 1) {
+      // dense: every in-arc id and every vertex's in-row offset (the pull); the
+      // listing reads every in-degree and writes the offsets
+      c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * static_cast<double>(c->arcs_now) + 8.0 * static_cast<double>(c->n);
+      c->ph_bytes[RIPPLE_PHASE_COMPACT] += 12.0 * static_cast<double>(c->n);
+    }
     if (c->tf[l]) {
       const double dp = c->dims[l - 1];
       c->ph_flops[RIPPLE_PHASE_GEMM] += 2.0 * nd * dp * d;
