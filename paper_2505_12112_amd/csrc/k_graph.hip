@@ -45,25 +45,25 @@ __device__ inline u64 edge_key(int a, int b, int undirected, long long n) {
   return static_cast<u64>(a) * static_cast<u64>(n) + static_cast<u64>(b);
 }
 
-// Slot holding `key`, or -1 (probing stops at the first empty slot).
-__device__ inline int hash_find(const u64 *ht_key, unsigned mask, u64 key) {
-  unsigned s = hash_slot(key, mask);
-  while (true) {
-    const u64 k = ht_key[s];
-    if (k == key) return static_cast<int>(s);
-    if (k == kEmptyKey) return -1;
-    s = (s + 1) & mask;
-  }
-}
-
 // Position of `target` in row[0, len) or -1; all lanes of the wave get the answer.
+// Reads kFindU entries per lane per round, all in flight together, so a row of up
+// to 512 entries costs one round trip.
+constexpr int kFindU = 8;
+
 __device__ inline int wave_find(const int *row, int len, int target) {
   const int lane = lane_id();
-  for (int base = 0; base < len; base += kWave) {
-    const int e = base + lane;
-    const bool hit = e < len && row[e] == target;
-    const u64 m = __ballot(hit);
-    if (m) return base + __ffsll(static_cast<long long>(m)) - 1;
+  for (int base = 0; base < len; base += kWave * kFindU) {
+    int x[kFindU];
+#pragma unroll
+    for (int u = 0; u < kFindU; ++u) {
+      const int e = base + u * kWave + lane;
+      x[u] = e < len ? row[e] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < kFindU; ++u) {
+      const u64 m = __ballot(x[u] == target);
+      if (m) return base + u * kWave + __ffsll(static_cast<long long>(m)) - 1;
+    }
   }
   return -1;
 }
@@ -249,9 +249,9 @@ __global__ void k_topo_plan(Adj out, Adj in, const int *ins_src, const int *ins_
 
 // One wave per touched (row, direction): the row's owner is its rank-0 insert
 // item, or its rank-0 delete item when it has no inserts.
-constexpr int kRewriteU = 8;
+constexpr int kRewriteU = 16;
 
-__global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, const int *ins_src,
+__global__ __launch_bounds__(256) void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, const int *ins_src,
                                const int *ins_dst, const int *del_src, const int *del_dst, const int *ins_rank,
                                const int *del_rank, const u64 *ht_key, const int *ht_net, unsigned mask,
                                Persist *p, int *ddeg, Counters *c) {
@@ -275,24 +275,21 @@ __global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, con
     if (static_cast<int>(!ins_item && nins != 0) | (cap0 | static_cast<int>(src_off >> 32)) >> 31) continue;
     const int need = len0 - k + nins;
     const bool move = nins > 0 && need > cap0;
+    const int nc = move ? grow_cap(need) : 0;
+    // a moving row's arena slots: the returning atomic stays in flight while the
+    // row is read (its value is needed only for the writes)
+    long long moved_to = 0;
+    if (move && lane == 0) moved_to = static_cast<long long>(atomicAdd(&p->top[dir], static_cast<u64>(nc)));
     long long dst_off = src_off;
-    int nc = 0;
-    if (move) {
-      nc = grow_cap(need);
-      long long base = 0;
-      if (lane == 0) base = static_cast<long long>(atomicAdd(&p->top[dir], static_cast<u64>(nc)));
-      dst_off = __shfl(base, 0);
-    }
     if (k > 0 || move) {
       const int *src = a.col + src_off;
-      int *dst = a.col + dst_off;
       const float *srcw = a.wt != nullptr ? a.wt + src_off : nullptr;  // weights move with their slots
-      float *dstw = a.wt != nullptr ? a.wt + dst_off : nullptr;
       int wpos = 0;
-      // kRewriteU entries per lane per step: the step's row reads, then its first
-      // hash probes, are all in flight together (a probe that meets another key
-      // continues alone); all reads of a step precede its writes, and a kept entry
-      // is written at or below its own position, so the in-place case is safe.
+      // kRewriteU entries per lane per step (rows up to 1024 entries take one step):
+      // the step's row reads, then its hash probes together with the net decisions
+      // of the probed slots, are all in flight at once (a probe that meets another
+      // key continues alone); all reads of a step precede its writes, and a kept
+      // entry is written at or below its own position, so the in-place case is safe.
       for (int base = 0; base < len0; base += kWave * kRewriteU) {
         int x[kRewriteU];
         float xw[kRewriteU];
@@ -307,20 +304,51 @@ __global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, con
         if (k > 0) {
           u64 key[kRewriteU], got[kRewriteU];
           unsigned sl[kRewriteU];
+          int net[kRewriteU];
 #pragma unroll
           for (int u = 0; u < kRewriteU; ++u) {
             key[u] = edge_key(dir ? x[u] : row, dir ? row : x[u], undirected, n);
             sl[u] = hash_slot(key[u], mask);
           }
 #pragma unroll
-          for (int u = 0; u < kRewriteU; ++u) got[u] = keep[u] ? ht_key[sl[u]] : kEmptyKey;
+          for (int u = 0; u < kRewriteU; ++u) {
+            got[u] = keep[u] ? ht_key[sl[u]] : kEmptyKey;
+            net[u] = keep[u] ? ht_net[sl[u]] : 0;
+          }
+          // keys found in their first slot are decided; the others walk their probe
+          // chains one slot per round, all of a lane's walks in the same round (the
+          // table is at most an eighth full, so every chain meets an empty slot)
+          unsigned pend = 0;
 #pragma unroll
           for (int u = 0; u < kRewriteU; ++u) {
             if (!keep[u] || got[u] == kEmptyKey) continue;
-            const int slot = got[u] == key[u] ? static_cast<int>(sl[u]) : hash_find(ht_key, mask, key[u]);
-            keep[u] = slot < 0 || ht_net[slot] != -1;
+            if (got[u] == key[u]) keep[u] = net[u] != -1;
+            else pend |= 1u << u;
+          }
+          for (unsigned j = 1; pend != 0; ++j) {
+#pragma unroll
+            for (int u = 0; u < kRewriteU; ++u) {
+              if (pend >> u & 1u) {
+                const unsigned s2 = (sl[u] + j) & mask;
+                got[u] = ht_key[s2];
+                net[u] = ht_net[s2];
+              }
+            }
+#pragma unroll
+            for (int u = 0; u < kRewriteU; ++u) {
+              if (!(pend >> u & 1u)) continue;
+              if (got[u] == key[u]) {
+                keep[u] = net[u] != -1;
+                pend &= ~(1u << u);
+              } else if (got[u] == kEmptyKey) {
+                pend &= ~(1u << u);  // not named by the batch: kept
+              }
+            }
           }
         }
+        if (base == 0 && move) dst_off = __shfl(moved_to, 0);
+        int *dst = a.col + dst_off;
+        float *dstw = a.wt != nullptr ? a.wt + dst_off : nullptr;
 #pragma unroll
         for (int u = 0; u < kRewriteU; ++u) {
           const u64 m = __ballot(keep[u]);
@@ -331,6 +359,7 @@ __global__ void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, con
           wpos += __popcll(m);
         }
       }
+      if (move && len0 == 0) dst_off = __shfl(moved_to, 0);  // no step ran
       if (lane == 0 && wpos != len0 - k) atomicOr(&c->err, 2ull);
     }
     if (lane == 0) {

@@ -425,8 +425,8 @@ ripple_status ensure_batch_scratch(ripple_ctx *c, long long ops, long long frows
   RP_HIP(c, hipStreamSynchronize(c->stream));
   free_batch_scratch(c);
   const long long arcs = 2 * cap;           // net arcs (undirected edges give two)
-  unsigned ht = 64;
-  while (ht < 4 * static_cast<unsigned long long>(cap)) ht <<= 1;
+  unsigned ht = 64;  // at most an eighth full: probe chains stay short
+  while (ht < 8 * static_cast<unsigned long long>(cap)) ht <<= 1;
   RP_TRY(dalloc_n(c, &c->d_ops, cap));
   RP_TRY(dalloc_n(c, &c->ht_key, ht));
   RP_TRY(dalloc_n(c, &c->ht_val, ht));
