@@ -48,11 +48,12 @@ struct Counters {
   u64 zero;               // never written: an arc count of zero for kernels that only mark
 };
 
-// One batch's inputs as the host hands them over, in pinned host memory written
-// before the launch: the first kernel of the batch reads it (system scope, so a
-// replayed launch sees the new values) and keeps a device copy for the later
-// kernels. Every launch of a batch is therefore the same for batches of any size
-// up to the scratch capacity, which lets a batch be replayed as one graph.
+// One batch's inputs as the host hands them over. The first kernel of the batch
+// takes them as an argument, or, in a launch captured for replay, reads them from
+// pinned host memory written before each replay (system scope, so a replay sees
+// the new values); it keeps a device copy for the later kernels. Every other
+// launch of a batch is therefore the same for batches of any size up to the
+// scratch capacity, which lets a batch be replayed as one graph.
 struct BatchIn {
   const ripple_op *ops;    // pinned host or device memory
   const float *feat;       // feature rows, [num_feat_rows][d_0], pinned host or device memory
@@ -173,7 +174,8 @@ inline bool has_self_term(int agg) { return agg != kGcSum && agg != kGcMean && a
 // netting: after these, the net arcs are listed and every (arc, direction) item
 // knows its rank among the row's inserts (ins_rank) or deletes (del_rank); the
 // hash slot of every named edge holds +1 (net insert), -1 (net delete) or 0.
-// host_in: the batch's inputs (BatchIn, pinned host memory); dev_in receives a copy
+// The batch's inputs are `now`, or, when host_in (pinned host memory) is set,
+// whatever it holds when the kernel runs (graph replays); dev_in receives a copy
 // for the later kernels. The ops are copied to ops (device) on the way and
 // checked (ids and feature rows in range, known kind, finite insert weights on a
 // weighted graph): a failing op sets bad_op and abort, and is copied as a
@@ -181,7 +183,8 @@ inline bool has_self_term(int agg) { return agg != kGcSum && agg != kGcMean && a
 // with another weight is a reweight: listed as a delete (old weight, del_w) and an
 // insert (new weight, ins_w) of the same arc, counted in n_rew.
 // cap_ops bounds num_ops (the grids are sized for it).
-void launch_net_hash(hipStream_t s, int cap_ops, const BatchIn *host_in, BatchIn *dev_in, ripple_op *ops,
+void launch_net_hash(hipStream_t s, int cap_ops, const BatchIn *host_in, const BatchIn &now, BatchIn *dev_in,
+                     ripple_op *ops,
                      int undirected, int weighted, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot,
                      int *fop, Counters *c);
 void launch_net_decide(hipStream_t s, int cap_ops, const BatchIn *in, const ripple_op *ops, int undirected,

@@ -87,24 +87,28 @@ __device__ inline void item_row(long long w, const int *src, const int *dst, int
   entry = dir == 0 ? dst[arc] : src[arc];
 }
 
-// Reads the batch's inputs from pinned host memory at system scope (the host
-// rewrites them before every launch, so no cached copy may be used), hands them
-// to the later kernels in dev_in, and keeps a device copy of the ops.
-__global__ void k_net_hash(const BatchIn *host_in, BatchIn *dev_in, ripple_op *ops, int undirected, int weighted,
-                           long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop, Counters *c) {
-  const auto word = [&](const void *f) {
-    return __hip_atomic_load(static_cast<const u64 *>(f), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-  };
-  const ripple_op *src_ops = reinterpret_cast<const ripple_op *>(word(&host_in->ops));
-  const long long B = static_cast<long long>(word(&host_in->num_ops));
-  const long long num_feat_rows = static_cast<long long>(word(&host_in->num_feat_rows));
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i == 0) {
-    dev_in->ops = src_ops;
-    dev_in->feat = reinterpret_cast<const float *>(word(&host_in->feat));
-    dev_in->num_ops = B;
-    dev_in->num_feat_rows = num_feat_rows;
+// Takes the batch's inputs from `now` (a launch for this batch alone) or, when
+// host_in is set (a launch replayed for later batches), from pinned host memory
+// at system scope (the host rewrites them before every replay, so no cached copy
+// may be used); hands them to the later kernels in dev_in, and keeps a device
+// copy of the ops.
+__global__ void k_net_hash(const BatchIn *host_in, BatchIn now, BatchIn *dev_in, ripple_op *ops, int undirected,
+                           int weighted, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot, int *fop,
+                           Counters *c) {
+  if (host_in != nullptr) {
+    const auto word = [&](const void *f) {
+      return __hip_atomic_load(static_cast<const u64 *>(f), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    };
+    now.ops = reinterpret_cast<const ripple_op *>(word(&host_in->ops));
+    now.feat = reinterpret_cast<const float *>(word(&host_in->feat));
+    now.num_ops = static_cast<long long>(word(&host_in->num_ops));
+    now.num_feat_rows = static_cast<long long>(word(&host_in->num_feat_rows));
   }
+  const ripple_op *src_ops = now.ops;
+  const long long B = now.num_ops;
+  const long long num_feat_rows = now.num_feat_rows;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) *dev_in = now;
   if (i >= B) return;
   ripple_op op = src_ops[i];
   // the same checks as the host's: an op that fails them aborts the batch before
@@ -396,10 +400,11 @@ inline int blocks_for(long long items, int threads, int cap = 4096) {
 
 }  // namespace
 
-void launch_net_hash(hipStream_t s, int cap_ops, const BatchIn *host_in, BatchIn *dev_in, ripple_op *ops,
+void launch_net_hash(hipStream_t s, int cap_ops, const BatchIn *host_in, const BatchIn &now, BatchIn *dev_in,
+                     ripple_op *ops,
                      int undirected, int weighted, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot,
                      int *fop, Counters *c) {
-  hipLaunchKernelGGL(k_net_hash, dim3(blocks_for(cap_ops, 256, 1 << 20)), dim3(256), 0, s, host_in, dev_in, ops,
+  hipLaunchKernelGGL(k_net_hash, dim3(blocks_for(cap_ops, 256, 1 << 20)), dim3(256), 0, s, host_in, now, dev_in, ops,
                      undirected, weighted, n, ht_key, ht_val, mask, op_slot, fop, c);
 }
 

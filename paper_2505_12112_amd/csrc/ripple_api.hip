@@ -686,8 +686,9 @@ BatchPlan make_plan(const ripple_ctx *c) {
 }
 
 // Issues one batch's launches (the inputs are in c->h_in). Returns after queuing;
-// the caller syncs. Launches only: the same calls are captured as a graph.
-void issue_batch(ripple_ctx *c, const BatchPlan &p) {
+// the caller syncs. Launches only: the same calls are captured as a graph, and
+// then (replay) the first kernel reads the inputs from c->h_in when it runs.
+void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
   hipStream_t s = c->stream;
   const int cap_ops = static_cast<int>(c->cap_ops);
   rp::Counters *dc = c->d_counters + c->parity;  // zeroed by the previous batch's clean-up
@@ -705,8 +706,8 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p) {
   PhaseScope total(c, RIPPLE_PHASE_TOTAL);
   {
     PhaseScope ps(c, RIPPLE_PHASE_NET);
-    rp::launch_net_hash(s, cap_ops, c->h_in, c->d_in, c->d_ops, c->undirected, c->weighted ? 1 : 0, c->n, c->ht_key,
-                        c->ht_val, c->ht_mask, c->op_slot, c->fop, dc);
+    rp::launch_net_hash(s, cap_ops, replay ? c->h_in : nullptr, *c->h_in, c->d_in, c->d_ops, c->undirected,
+                        c->weighted ? 1 : 0, c->n, c->ht_key, c->ht_val, c->ht_mask, c->op_slot, c->fop, dc);
     rp::launch_net_decide(s, cap_ops, c->d_in, c->d_ops, c->undirected, c->ht_val, c->ht_net, c->op_slot, c->fop, out,
                           in, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank, c->del_rank, c->ins_w,
                           c->del_w, c->flist, dc);
@@ -843,7 +844,7 @@ hipGraphExec_t plan_graph(ripple_ctx *c, const BatchPlan &p) {
   hipGraphExec_t exec = nullptr;
   hipError_t e = hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal);
   if (e == hipSuccess) {
-    issue_batch(c, p);
+    issue_batch(c, p, true);
     e = hipStreamEndCapture(c->stream, &graph);
   }
   if (e == hipSuccess) e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
@@ -881,7 +882,7 @@ ripple_status launch_batch(ripple_ctx *c) {
     RP_HIP(c, hipGraphLaunch(g, c->stream));
     c->last_graph = true;
   } else {
-    issue_batch(c, p);
+    issue_batch(c, p, false);
     RP_HIP(c, hipGetLastError());
   }
   c->parity ^= 1;
