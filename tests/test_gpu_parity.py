@@ -209,6 +209,45 @@ def test_graph_replays_follow_sizes_pointers_and_plans():
         p.close()
 
 
+@pytest.mark.parametrize("case", ["one_vertex", "no_arcs", "max_layers_sum", "max_layers_gcn", "max_width",
+                                  "width_one"])
+def test_degenerate_and_extreme_shapes(case):
+    """A one-vertex graph (only feature writes and self-loop no-ops can act), a graph
+    that starts with no arcs (every insert outgrows its row), the most layers the ABI
+    takes (RIPPLE_MAX_LAYERS = 8), the widest rows it takes (RIPPLE_MAX_DIM = 1024,
+    so K = 2048 for GraphSAGE) and rows of width 1."""
+    _say("extreme shape", case)
+    rng = np.random.default_rng(41 + ["one_vertex", "no_arcs", "max_layers_sum", "max_layers_gcn", "max_width",
+                                      "width_one"].index(case))
+    agg, n, m, dims = {
+        "one_vertex": ("sum", 1, 0, (3, 5, 2)),
+        "no_arcs": ("mean", 40, 0, (6, 9, 4)),
+        "max_layers_sum": ("sum", 120, 500, (6,) * 9),
+        "max_layers_gcn": ("gcn", 120, 500, (6,) * 9),
+        "max_width": ("sum", 64, 256, (1024, 1024, 1)),
+        "width_one": ("gcn", 80, 300, (1, 1, 1)),
+    }[case]
+    src, dst, x, w = _small(rng, n, m, dims, agg) if m else (np.zeros(0, np.int32), np.zeros(0, np.int32),
+                                                                rng.standard_normal((n, dims[0])).astype(np.float32),
+                                                                synth.model_weights(synth.ModelSpec(agg, dims), rng,
+                                                                                    bias_std=0.1))
+    p = Pair(n, src, dst, x, w)
+    try:
+        for b in range(12):
+            if case == "one_vertex" and b % 3 == 2:
+                batch = synth.Batch(np.array([[1, 0, 0, -1], [2, 0, 0, -1], [3, 0, -1, 0]], np.int32),
+                                    rng.standard_normal((1, dims[0])).astype(np.float32))
+            else:
+                mix = (0.6, 0.2, 0.2) if case == "no_arcs" else (1 / 3, 1 / 3, 1 / 3)
+                batch = random_valid_batch(rng, p.orc, int(rng.integers(1, 40)), dims[0], mix=mix)
+            p.step(batch)
+        p.check_embeddings()
+        p.check_arcs()
+        p.check_aggregates()
+    finally:
+        p.close()
+
+
 def test_empty_and_noop_batches():
     rng = np.random.default_rng(13)
     dims = (6, 8, 3)
