@@ -267,7 +267,12 @@ def main():
         ach = p["bytes"] / (p["ms"] * 1e-3) / 1e9
         return {"kernel": "k_scatter / k_pull_msgs (message step)", "bound": "hbm", "achieved": ach,
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
-                "algorithmic_per_launch": p["bytes"] / p["launches"], **common}
+                "algorithmic_per_launch": p["bytes"] / p["launches"],
+                "no_reuse_per_launch": p["bytes_no_reuse"] / p["launches"],
+                "bytes_note": "algorithmic: each message row read once, each sink row of S read and written once; "
+                              "no_reuse: a message row read per arc that carries it (and, pushed, a row of atomics "
+                              "per arc); the counters' traffic falls between the two by the L2 / MALL reuse",
+                **common}
 
     r_scatter, r_gemm = roof("scatter"), roof("gemm")
     dominant = "gemm" if ph["gemm"]["ms"] >= ph["scatter"]["ms"] else "scatter"

@@ -306,8 +306,11 @@ enum {
 typedef struct {
   double ms;
   int64_t launches;
-  double bytes;
+  double bytes;          /* algorithmic bytes: each row the phase needs read or written once */
   double flops;
+  double bytes_no_reuse; /* the same work with no on-chip reuse: in the message step every
+                            message row is read once per arc that carries it and, in the push
+                            form, every arc's row of atomics goes to memory; other phases: bytes */
 } ripple_phase_stats;
 RIPPLE_API ripple_status ripple_set_profiling(ripple_ctx *ctx, int32_t mask);
 RIPPLE_API ripple_status ripple_get_phase_stats(ripple_ctx *ctx, ripple_phase_stats *out, int32_t capacity);

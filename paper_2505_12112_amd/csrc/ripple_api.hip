@@ -163,6 +163,7 @@ struct ripple_ctx {
   double ph_ms[RIPPLE_NUM_PHASES] = {};
   long long ph_launch[RIPPLE_NUM_PHASES] = {};
   double ph_bytes[RIPPLE_NUM_PHASES] = {};
+  double ph_extra[RIPPLE_NUM_PHASES] = {};  // bytes_no_reuse - bytes
   double ph_flops[RIPPLE_NUM_PHASES] = {};
 };
 
@@ -902,6 +903,13 @@ void account_phases(ripple_ctx *c) {
     const double d = c->sw[l];
     const double nd = static_cast<double>(k.count[l - 1]);
     c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * k.pushed[l] + 8.0 * nd + 4.0 * d * nd + 8.0 * d * k.dest[l];
+    // without on-chip reuse: a message row read per arc that carries it, and under
+    // push a row of atomics per arc rather than per sink
+    const double per_arc = static_cast<double>(k.pushed[l]);
+    const double sinks = static_cast<double>(k.dest[l]);
+    c->ph_extra[RIPPLE_PHASE_SCATTER] += 4.0 * d * std::max(per_arc - nd, 0.0);
+    if (!((c->last_pull | c->last_dense) >> l & 1))
+      c->ph_extra[RIPPLE_PHASE_SCATTER] += 8.0 * d * std::max(per_arc - sinks, 0.0);
     if (c->last_pull >> l & 1)  // pull: every in-arc id of A^l and its in-row offset
       c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * k.indeg[l] + 12.0 * k.count[l];
     if (c->last_dense >> l & 1) {
@@ -1326,7 +1334,7 @@ namespace {
 // Runs one batch whose ops and feature rows the kernels read from src_ops /
 // src_feat (pinned host or device memory). The kernels check every op again; a
 // batch they reject is invalid, reported from caller_ops (the caller's device
-// copy), and nothing was mutated.
+// copy; nullptr when src_ops is the pinned host copy), and nothing was mutated.
 ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const ripple_op *src_ops,
                         const float *src_feat, const ripple_op *caller_ops, ripple_batch_stats *stats) {
   long long repacks = 0;
@@ -1344,7 +1352,10 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
       c->ev_used = 0;
       const long long i = B - static_cast<long long>(c->h_counters->bad_op);
       ripple_op o{};
-      RP_HIP(c, hipMemcpy(&o, caller_ops + i, sizeof(o), hipMemcpyDeviceToHost));
+      if (caller_ops != nullptr)
+        RP_HIP(c, hipMemcpy(&o, caller_ops + i, sizeof(o), hipMemcpyDeviceToHost));
+      else
+        o = src_ops[i];  // the batch came through pinned host memory
       if (validate_ops(c, &o, 1, num_feat_rows)) c->err = "ripple: op 0: failed the device-side check";
       const size_t at = c->err.find("op 0:");
       if (at != std::string::npos) c->err.replace(at, 5, "op " + std::to_string(i) + ":");
@@ -1615,12 +1626,14 @@ ripple_status ripple_get_phase_stats(ripple_ctx *c, ripple_phase_stats *out, int
     out[p].ms = c->ph_ms[p];
     out[p].launches = c->ph_launch[p];
     out[p].bytes = c->ph_bytes[p];
+    out[p].bytes_no_reuse = c->ph_bytes[p] + c->ph_extra[p];
     out[p].flops = c->ph_flops[p];
   }
   for (int p = 0; p < RIPPLE_NUM_PHASES; ++p) {
     c->ph_ms[p] = 0.0;
     c->ph_launch[p] = 0;
     c->ph_bytes[p] = 0.0;
+    c->ph_extra[p] = 0.0;
     c->ph_flops[p] = 0.0;
   }
   return RIPPLE_OK;

@@ -79,7 +79,8 @@ class BatchStats(C.Structure):
 
 
 class PhaseStats(C.Structure):
-    _fields_ = [("ms", C.c_double), ("launches", C.c_int64), ("bytes", C.c_double), ("flops", C.c_double)]
+    _fields_ = [("ms", C.c_double), ("launches", C.c_int64), ("bytes", C.c_double), ("flops", C.c_double),
+                ("bytes_no_reuse", C.c_double)]
 
 
 _lib = None
@@ -350,5 +351,6 @@ class Ripple:
         arr = (PhaseStats * NUM_PHASES)()
         self._check(self._lib.ripple_get_phase_stats(self._ctx, arr, NUM_PHASES))
         return {PHASES[p]: {"ms": arr[p].ms, "launches": arr[p].launches, "bytes": arr[p].bytes,
-                            "flops": arr[p].flops} for p in range(NUM_PHASES)}
+                            "flops": arr[p].flops, "bytes_no_reuse": arr[p].bytes_no_reuse}
+                for p in range(NUM_PHASES)}
 

@@ -248,6 +248,39 @@ def test_degenerate_and_extreme_shapes(case):
         p.close()
 
 
+@pytest.mark.parametrize("mode", ["push", "pull", "dense"])
+def test_phase_stats_count_launches_and_bytes(mode):
+    """Phase events: every phase of a profiled batch is timed, the launches are
+    counted per phase (two netting, two topology, three layer-0 launches per
+    batch; per layer one message launch when pushing, two when pulling; the dense
+    form's full listing counts with the compactions), and the no-reuse byte bound
+    of the message step is at least its algorithmic bytes."""
+    rng = np.random.default_rng(51)
+    dims = (8, 16, 4)
+    src, dst, x, w = _small(rng, 300, 1500, dims, "sum")
+    p = Pair(300, src, dst, x, w, mode=mode)
+    try:
+        p.lib.set_profiling(PHASES)
+        p.lib.phase_stats()
+        nb = 3
+        for _ in range(nb):
+            p.step(random_valid_batch(rng, p.orc, 30, dims[0]))
+        ph = p.lib.phase_stats()
+        L = len(dims) - 1
+        assert ph["net"]["launches"] == 2 * nb and ph["topo"]["launches"] == 2 * nb
+        assert ph["layer0"]["launches"] == 3 * nb
+        assert ph["scatter"]["launches"] == (1 if mode == "push" else 2) * L * nb
+        assert ph["compact"]["launches"] == (2 if mode == "dense" else 1) * L * nb
+        assert ph["gemm"]["launches"] == L * nb and ph["total"]["launches"] == nb
+        for name in ("net", "topo", "layer0", "scatter", "compact", "gemm", "total"):
+            assert ph[name]["ms"] > 0, name
+        assert ph["scatter"]["bytes"] > 0 and ph["scatter"]["bytes_no_reuse"] >= ph["scatter"]["bytes"]
+        assert ph["gemm"]["flops"] > 0
+        p.check_embeddings()
+    finally:
+        p.close()
+
+
 def test_empty_and_noop_batches():
     rng = np.random.default_rng(13)
     dims = (6, 8, 3)
