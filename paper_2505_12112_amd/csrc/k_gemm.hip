@@ -162,6 +162,44 @@ __device__ inline bool abort_or_rows(const GemmArgs &a, long long &M, T... more)
   return a.abort != nullptr && *a.abort != 0;
 }
 
+// The epilogue for four consecutive columns col .. col+3 of row slot m (vertex v),
+// all inside the layer (N % 4 == 0, so every row of H, S and delta is 16-byte
+// aligned there): the scalar epilogue's arithmetic with float4 loads and stores.
+template <int AGG, int MODE>
+__device__ inline void epilogue4(const GemmArgs &a, long long m, int v, int col, float4 y, float tv, float sv) {
+  const int N = a.N;
+  float yy[4] = {y.x, y.y, y.z, y.w};
+  if (MODE == kTransformFirst) {
+    const float4 T = *reinterpret_cast<const float4 *>(a.S + static_cast<long long>(v) * N + col);
+    const float tt[4] = {T.x, T.y, T.z, T.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) yy[i] = AGG == kGcn ? tv * (tt[i] + sv * yy[i]) : yy[i] + tv * tt[i];
+  }
+  if (a.bias != nullptr) {
+    const float4 b = *reinterpret_cast<const float4 *>(a.bias + col);
+    yy[0] += b.x;
+    yy[1] += b.y;
+    yy[2] += b.z;
+    yy[3] += b.w;
+  }
+  if (a.relu) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) yy[i] = fmaxf(yy[i], 0.f);
+  }
+  float4 *hp = reinterpret_cast<float4 *>(a.H + (MODE == kGin1 ? m : static_cast<long long>(v)) * N + col);
+  if (MODE != kGin1 && a.delta != nullptr) {
+    float cn = 1.f, co = 1.f;
+    if (AGG == kGcn) {
+      cn = sv;
+      co = 1.0f / sqrtf(static_cast<float>(a.out_len[v] - a.ddeg[v]) + 1.0f);
+    }
+    const float4 o = *hp;
+    *reinterpret_cast<float4 *>(a.delta + m * a.dld + col) =
+        make_float4(cn * yy[0] - co * o.x, cn * yy[1] - co * o.y, cn * yy[2] - co * o.z, cn * yy[3] - co * o.w);
+  }
+  *hp = make_float4(yy[0], yy[1], yy[2], yy[3]);
+}
+
 // The launch's last a.cleanup_blocks blocks reset the batch's scratch instead of
 // computing tiles (true for them); the others take tiles with stride gemm_grid.
 __device__ inline bool cleanup_role(const GemmArgs &a, unsigned &gemm_grid) {
@@ -184,8 +222,13 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
   const long long tiles_n = (N + BN - 1) / BN;
   const long long tiles = ((M + BM - 1) / BM) * tiles_n;
 
-  __shared__ float As[2][BM][kLdk];
-  __shared__ float Bs[2][BN][kLdk];
+  // the double-buffered operand tiles, and after the K loop the output tile (row
+  // stride BN + 4 floats keeps its rows 16-byte aligned), share one LDS block
+  constexpr int kAsz = 2 * BM * kLdk, kBsz = 2 * BN * kLdk, kLdo = BN + 4;
+  constexpr int kSmem = kAsz + kBsz > BM * kLdo ? kAsz + kBsz : BM * kLdo;
+  __shared__ __attribute__((aligned(16))) float smem[kSmem];
+  float(*As)[BM][kLdk] = reinterpret_cast<float(*)[BM][kLdk]>(smem);
+  float(*Bs)[BN][kLdk] = reinterpret_cast<float(*)[BN][kLdk]>(smem + kAsz);
   __shared__ int rv[BM];
   __shared__ float rt[BM];
   __shared__ float rs[BM];
@@ -300,17 +343,38 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
     }
 
     // epilogue: lane holds C[4*(lane/16) + r][lane % 16] of each 16 x 16 tile
+    if (VEC && N % 4 == 0) {
+      // through LDS, so that each row's outputs are read, written and loaded as
+      // float4 runs of up to BN columns (the K loop's last barrier has released the
+      // operand tiles)
 #pragma unroll
-    for (int i = 0; i < WM; ++i) {
+      for (int i = 0; i < WM; ++i)
 #pragma unroll
-      for (int j = 0; j < WN; ++j) {
-        const int col = n0 + wn0 + j * 16 + lr;
+        for (int j = 0; j < WN; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int ml = wm0 + i * 16 + lk * 4 + r;
-          const int v = rv[ml];
-          if (v < 0 || col >= N) continue;
-          epilogue<AGG, MODE>(a, m0 + ml, v, col, acc[i][j][r], rt[ml], rs[ml]);
+          for (int r = 0; r < 4; ++r) smem[(wm0 + i * 16 + lk * 4 + r) * kLdo + wn0 + j * 16 + lr] = acc[i][j][r];
+      __syncthreads();
+      for (int q = tid; q < BM * (BN / 4); q += kThreads) {
+        const int ml = q / (BN / 4), c4 = q % (BN / 4);
+        const int col = n0 + 4 * c4;
+        const int v = rv[ml];
+        if (v < 0 || col >= N) continue;
+        const float4 y = *reinterpret_cast<const float4 *>(&smem[ml * kLdo + 4 * c4]);
+        epilogue4<AGG, MODE>(a, m0 + ml, v, col, y, rt[ml], rs[ml]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < WM; ++i) {
+#pragma unroll
+        for (int j = 0; j < WN; ++j) {
+          const int col = n0 + wn0 + j * 16 + lr;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int ml = wm0 + i * 16 + lk * 4 + r;
+            const int v = rv[ml];
+            if (v < 0 || col >= N) continue;
+            epilogue<AGG, MODE>(a, m0 + ml, v, col, acc[i][j][r], rt[ml], rs[ml]);
+          }
         }
       }
     }
