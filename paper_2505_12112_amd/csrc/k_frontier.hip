@@ -19,6 +19,10 @@ constexpr int kCompactThreads = 256;
 constexpr int kCompactWaves = kCompactThreads / kWave;
 constexpr int kWordsPerThread = 4;
 constexpr int kWordsPerBlock = kCompactThreads * kWordsPerThread;
+// Tiles that are placed by block index: far fewer than the compute units, so all are
+// resident at once (graphs up to 2M vertices; larger ones, whose compactions take
+// long enough not to notice a round trip, go in ticket order).
+constexpr long long kIndexTiles = 64;
 
 __device__ inline int lane_id() { return threadIdx.x & (kWave - 1); }
 
@@ -229,9 +233,10 @@ __device__ inline bool fetch(const u64 *p, u64 epoch, long long (&v)[kVals]) {
   return ok;
 }
 
-// Single-pass compaction (a decoupled look-back prefix scan). Block b takes tile b
-// of kWordsPerBlock bitmap words; blocks are dispatched in index order, so a
-// tile's predecessors are running or done. Each tile publishes its sums at once,
+// Single-pass compaction (a decoupled look-back prefix scan). Tiles of
+// kWordsPerBlock bitmap words go to blocks by index when all tiles fit on the GPU at
+// once, else in ticket order; either way a tile's predecessors are running or done
+// when it waits for them. Each tile publishes its sums at once,
 // then wave 0 walks back over the predecessors (64 per step), adding their tile
 // sums until it meets one that has published its inclusive prefix. A tile
 // publishes its own sums before it waits, so every wait is for work that needs no
@@ -246,9 +251,20 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
                                                              u64 *err) {
   __shared__ long long red[kCompactWaves][kVals];
   __shared__ long long base_s[kVals];
-  __shared__ u64 epoch_s;
+  __shared__ u64 epoch_s, ticket_s;
   const long long tiles = gridDim.x;
-  const long long tile = blockIdx.x;
+  // Up to kIndexTiles tiles all fit on the GPU at once, so block b takes tile b and
+  // its ticket (for the epoch) is in flight beside the bitmap loads. Beyond that,
+  // tiles go in ticket order, so a tile's predecessors are running or done however
+  // the blocks are dispatched.
+  const bool by_ticket = tiles > kIndexTiles;
+  u64 ticket_no = 0;
+  if (by_ticket) {
+    if (threadIdx.x == 0) ticket_s = atomicAdd(ticket, 1ull);
+    __syncthreads();
+    ticket_no = ticket_s;
+  }
+  const long long tile = by_ticket ? static_cast<long long>(ticket_no % static_cast<u64>(tiles)) : blockIdx.x;
   const long long w0 = tile * kWordsPerBlock + threadIdx.x * kWordsPerThread;
   const int *odeg = o.doff != nullptr || o.out_total != nullptr ? o.out_deg : nullptr;
   const int *ideg = o.ioff != nullptr || o.in_total != nullptr ? o.in_deg : nullptr;
@@ -264,8 +280,7 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
   } else {
     load_words(bm_a, bm_b, w0, words, wv, pop_a);
   }
-  u64 ticket_no = 0;
-  if (threadIdx.x == 0) ticket_no = atomicAdd(ticket, 1ull);  // in flight beside the loads
+  if (!by_ticket && threadIdx.x == 0) ticket_no = atomicAdd(ticket, 1ull);  // in flight beside the loads
   long long st[kVals] = {0, 0, 0, pop_a};
 #pragma unroll
   for (int i = 0; i < kWordsPerThread; ++i) st[0] += __popc(wv[i]);

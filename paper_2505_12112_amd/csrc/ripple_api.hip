@@ -1206,6 +1206,7 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
 ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple_model_desc *md) {
   RP_TRY(check_ctx(c));
   if (x == nullptr || md == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: x and model must be non-NULL");
+  drop_graphs(c);  // a new model changes the launches of every plan
   const int L = md->num_layers;
   if (L < 1 || L > rp::kMaxL) return fail(c, RIPPLE_E_INVALID, "ripple: num_layers out of range");
   if (md->agg < RIPPLE_AGG_SUM || md->agg > RIPPLE_AGG_GC_WSUM)
