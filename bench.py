@@ -125,8 +125,8 @@ def cpu_baseline(wl_name, seed, batches, bs):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
-                          "(multi-GPU sharding is designed but not built)"}))
+        print(json.dumps({"error": "the library runs on one GPU; --gpus must be 1 "
+                          "(sharding over several GPUs is not implemented)"}))
         sys.exit(2)
     import numpy as np
     import torch
