@@ -179,6 +179,8 @@ typedef struct {
   int64_t reweighted_arcs;      /* weighted graphs: arcs present before and after whose weight changed */
   int64_t graph_replay;         /* 1: the batch ran as one replay of a captured HIP graph (see
                                    ripple_set_graphs); 0: its kernels were queued one by one */
+  int64_t long_rows;            /* adjacency rows of at least 16384 entries whose deletes were swept by
+                                   many waves in chunks (graphs whose snapshot has rows of 8192 or more) */
 } ripple_batch_stats;
 
 /* Part 1 of the problem statement: copies the snapshot to the device as an

@@ -46,6 +46,24 @@ struct Counters {
   u64 bad_op;             // B - i for the first op i that failed the device-side check, else 0
   u64 n_rew;              // reweighted arcs (weighted graphs; each also counted in n_ins and n_del)
   u64 zero;               // never written: an arc count of zero for kernels that only mark
+  u64 long_rows;          // long rows swept in chunks: count << 40 | chunks handed out
+  u64 long_pool;          // pool slots handed out to them
+};
+
+// Rows at least kLongRow entries long from which a batch deletes entries (and that
+// keep their slots) are swept by many waves, kLongChunk entries each: the sweeps
+// record the positions of deleted entries below the row's new length (holes) and
+// of kept entries at or above it (movers), and a fill pass moves the movers into
+// the holes (rows are unordered, so a swap-remove keeps them valid).
+constexpr int kLongRow = 16384;
+constexpr int kLongChunk = 4096;
+struct LongRow {
+  int dir, row, len0, k;  // direction, row, pre-batch length, entries deleted
+  long long off;          // the row's first slot
+  long long chunk0;       // its first chunk number
+  long long pool;         // holes at pool[0 .. k), movers at pool[k .. 2k)
+  int holes, movers, found;  // filled in by the sweeps (found: deleted entries seen)
+  int pad;
 };
 
 // One batch's inputs as the host hands them over. The first kernel of the batch
@@ -196,12 +214,18 @@ void launch_net_decide(hipStream_t s, int cap_ops, const BatchIn *in, const ripp
 // (aborting before any mutation), then one owner wave per touched row removes its
 // deleted entries, moves the row if it must grow, and sets its new length (the
 // inserts are written at their ranks by launch_corr_mark).
+// long_ok: rows may be long (tab / pool hold up to 2 cap_arcs rows / 4 cap_arcs
+// slots); then the plan lists the long rows, the rewrite's waves also sweep their
+// chunks, and launch_topo_fill must follow the rewrite.
 void launch_topo_plan(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                      const int *ins_rank, Counters *c, const Persist *p, long long cap_out, long long cap_in);
+                      const int *del_src, const int *del_dst, const int *ins_rank, const int *del_rank,
+                      int long_ok, LongRow *tab, Counters *c, const Persist *p, long long cap_out, long long cap_in);
 void launch_topo_rewrite(hipStream_t s, int cap_arcs, int undirected, long long n, Adj out, Adj in,
                          const int *ins_src, const int *ins_dst, const int *del_src, const int *del_dst,
                          const int *ins_rank, const int *del_rank, const u64 *ht_key, const int *ht_net,
-                         unsigned mask, Persist *p, int *ddeg, Counters *c);
+                         unsigned mask, Persist *p, int *ddeg, int long_ok, LongRow *tab, int *pool, Counters *c);
+void launch_topo_fill(hipStream_t s, int cap_arcs, Adj out, Adj in, const LongRow *tab, const int *pool,
+                      Counters *c);
 
 // frontier. Pre-batch corrections of every layer's aggregate (an inserted arc
 // (u,v) adds u's pre-batch contribution to S^l_v, a deleted one removes it) run

@@ -221,19 +221,40 @@ __global__ void k_net_decide(const BatchIn *bin, const ripple_op *ops, int undir
   }
 }
 
-__global__ void k_topo_plan(Adj out, Adj in, const int *ins_src, const int *ins_dst, const int *ins_rank,
+__global__ void k_topo_plan(Adj out, Adj in, const int *ins_src, const int *ins_dst, const int *del_src,
+                            const int *del_dst, const int *ins_rank, const int *del_rank, int long_ok, LongRow *tab,
                             Counters *c, const Persist *p, long long cap_out, long long cap_in) {
   const long long ni = 2 * static_cast<long long>(c->n_ins);
+  const long long nd = long_ok ? 2 * static_cast<long long>(c->n_del) : 0;
   const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
-  for (long long w = blockIdx.x * blockDim.x + threadIdx.x; w < ni; w += stride) {
+  for (long long w = blockIdx.x * blockDim.x + threadIdx.x; w < ni + nd; w += stride) {
+    // one planner per touched row: its first insert item, else its first delete item
+    const bool ins_item = w < ni;
+    const long long x = ins_item ? w : w - ni;
     int dir, row, entry;
-    item_row(w, ins_src, ins_dst, dir, row, entry);
-    if ((ins_rank[w] | row >> 31) != 0) continue;  // one planner per row (row >= 0: see k_topo_rewrite)
+    item_row(x, ins_item ? ins_src : del_src, ins_item ? ins_dst : del_dst, dir, row, entry);
+    if (((ins_item ? ins_rank : del_rank)[x] | row >> 31) != 0) continue;  // (row >= 0: see k_topo_rewrite)
     const Adj &a = dir ? in : out;
-    const int need = a.len[row] - a.delcnt[row] + a.inscnt[row];
-    if (need > a.cap[row]) {
+    const int len0 = a.len[row], k = a.delcnt[row], nins = a.inscnt[row], cap = a.cap[row];
+    if (!ins_item && nins != 0) continue;
+    const int need = len0 - k + nins;
+    if (need > cap) {
       atomicAdd(&c->n_reloc, 1ull);
       atomicAdd(&c->arena_need[dir], static_cast<u64>(grow_cap(need)));
+    } else if (long_ok && k > 0 && len0 >= kLongRow) {
+      // a long row that keeps its slots: list it for the chunked sweep
+      const long long chunks = (len0 + kLongChunk - 1) / kLongChunk;
+      const u64 old = atomicAdd(&c->long_rows, (1ull << 40) | static_cast<u64>(chunks));
+      const long long at = static_cast<long long>(old >> 40);
+      LongRow t{};
+      t.dir = dir;
+      t.row = row;
+      t.len0 = len0;
+      t.k = k;
+      t.off = a.off[row];
+      t.chunk0 = static_cast<long long>(old & ((1ull << 40) - 1));
+      t.pool = static_cast<long long>(atomicAdd(&c->long_pool, 2ull * static_cast<u64>(k)));
+      tab[at] = t;
     }
   }
   // the last block to finish compares the arena demand with the free arena
@@ -251,19 +272,142 @@ __global__ void k_topo_plan(Adj out, Adj in, const int *ins_src, const int *ins_
   }
 }
 
-// One wave per touched (row, direction): the row's owner is its rank-0 insert
-// item, or its rank-0 delete item when it has no inserts.
-constexpr int kRewriteU = 16;
+constexpr int kRewriteU = 16;  // row entries per lane per step: 1024 per wave
 
+// Clears keep[u] for the entries x[u] of `row` (direction dir) that the batch
+// deletes. Each entry's edge-key slot is probed together with the slot's net
+// decision; probes that meet another key walk their chains one slot per round, all
+// of a lane's chains in the same round (the table is at most an eighth full, so
+// every chain meets an empty slot).
+__device__ inline void drop_deleted(const int (&x)[kRewriteU], bool (&keep)[kRewriteU], int row, int dir,
+                                    int undirected, long long n, const u64 *ht_key, const int *ht_net,
+                                    unsigned mask) {
+  u64 key[kRewriteU], got[kRewriteU];
+  unsigned sl[kRewriteU];
+  int net[kRewriteU];
+#pragma unroll
+  for (int u = 0; u < kRewriteU; ++u) {
+    key[u] = edge_key(dir ? x[u] : row, dir ? row : x[u], undirected, n);
+    sl[u] = hash_slot(key[u], mask);
+  }
+#pragma unroll
+  for (int u = 0; u < kRewriteU; ++u) {
+    got[u] = keep[u] ? ht_key[sl[u]] : kEmptyKey;
+    net[u] = keep[u] ? ht_net[sl[u]] : 0;
+  }
+  unsigned pend = 0;
+#pragma unroll
+  for (int u = 0; u < kRewriteU; ++u) {
+    if (!keep[u] || got[u] == kEmptyKey) continue;
+    if (got[u] == key[u]) keep[u] = net[u] != -1;
+    else pend |= 1u << u;
+  }
+  for (unsigned j = 1; pend != 0; ++j) {
+#pragma unroll
+    for (int u = 0; u < kRewriteU; ++u) {
+      if (pend >> u & 1u) {
+        const unsigned s2 = (sl[u] + j) & mask;
+        got[u] = ht_key[s2];
+        net[u] = ht_net[s2];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kRewriteU; ++u) {
+      if (!(pend >> u & 1u)) continue;
+      if (got[u] == key[u]) {
+        keep[u] = net[u] != -1;
+        pend &= ~(1u << u);
+      } else if (got[u] == kEmptyKey) {
+        pend &= ~(1u << u);  // not named by the batch: kept
+      }
+    }
+  }
+}
+
+// The entry of tab[0 .. n_long) holding chunk j (the last one whose chunk0 <= j;
+// chunk0 grows with the index): at most two rounds of 64 loads for up to 4096 rows,
+// then a plain search.
+__device__ inline long long find_long(const LongRow *tab, long long n_long, long long j) {
+  const int lane = lane_id();
+  long long lo = 0, hi = n_long;  // answer in [lo, hi)
+  while (hi - lo > 1) {
+    const long long step = (hi - lo + kWave - 1) / kWave;
+    const long long at = lo + lane * step;
+    const bool le = at < hi && tab[at].chunk0 <= j;
+    const int cnt = __popcll(__ballot(le));  // entries lo, lo + step, ... up to cnt - 1 qualify
+    const long long nlo = lo + (cnt - 1) * step;
+    hi = nlo + step < hi ? nlo + step : hi;
+    lo = nlo;
+  }
+  return lo;
+}
+
+// Appends position e of every lane with flag set to list[*count ..] (at most cap
+// entries; past that the check bit is set instead).
+__device__ inline void append_positions(bool flag, int e, int *list, int *count, int cap, Counters *c) {
+  const u64 m = __ballot(flag);
+  if (m == 0) return;
+  int b0 = 0;
+  if (lane_id() == 0) b0 = atomicAdd(count, __popcll(m));
+  b0 = __shfl(b0, 0);
+  const int at = b0 + lanes_below(m);
+  if (flag) {
+    if (at < cap) list[at] = e;
+    else atomicOr(&c->err, 2ull);
+  }
+}
+
+// One wave per touched (row, direction): the row's owner is its rank-0 insert
+// item, or its rank-0 delete item when it has no inserts. Long rows listed by the
+// plan are left to the chunk sweeps, which follow the items in the same grid.
 __global__ __launch_bounds__(256) void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, const int *ins_src,
                                const int *ins_dst, const int *del_src, const int *del_dst, const int *ins_rank,
                                const int *del_rank, const u64 *ht_key, const int *ht_net, unsigned mask,
-                               Persist *p, int *ddeg, Counters *c) {
+                               Persist *p, int *ddeg, int long_ok, LongRow *tab, int *pool, Counters *c) {
   const long long ni = 2 * static_cast<long long>(c->n_ins);
   const long long nd = 2 * static_cast<long long>(c->n_del);
-  if (aborted_with(c->abort, ni, nd)) return;
+  const u64 lr = c->long_rows;
+  if (aborted_with(c->abort, ni, nd, static_cast<long long>(lr >> 1))) return;
+  const long long n_long = static_cast<long long>(lr >> 40);
+  const long long chunks = static_cast<long long>(lr & ((1ull << 40) - 1));
   const int lane = lane_id();
-  for (long long w = global_wave(); w < ni + nd; w += num_waves()) {
+  for (long long w = global_wave(); w < ni + nd + chunks; w += num_waves()) {
+    if (w >= ni + nd) {
+      // chunk sweep of a long row: its deleted entries below the new length are
+      // holes, its kept entries at or above it are movers
+      const long long j = w - ni - nd;
+      const long long at = find_long(tab, n_long, j);
+      const LongRow t = tab[at];
+      const Adj &a = t.dir ? in : out;
+      const int *src = a.col + t.off;
+      const int e0 = static_cast<int>((j - t.chunk0) * kLongChunk);
+      const int e1 = e0 + kLongChunk < t.len0 ? e0 + kLongChunk : t.len0;
+      const int new_len = t.len0 - t.k;
+      int found = 0;
+      for (int base = e0; base < e1; base += kWave * kRewriteU) {
+        int x[kRewriteU];
+        bool keep[kRewriteU], live[kRewriteU];
+#pragma unroll
+        for (int u = 0; u < kRewriteU; ++u) {
+          const int e = base + u * kWave + lane;
+          live[u] = e < e1;
+          keep[u] = live[u];
+          x[u] = live[u] ? src[e] : -1;
+        }
+        drop_deleted(x, keep, t.row, t.dir, undirected, n, ht_key, ht_net, mask);
+#pragma unroll
+        for (int u = 0; u < kRewriteU; ++u) {
+          const int e = base + u * kWave + lane;
+          found += live[u] && !keep[u] ? 1 : 0;
+          append_positions(live[u] && !keep[u] && e < new_len, e, pool + t.pool, &tab[at].holes, t.k, c);
+          append_positions(live[u] && keep[u] && e >= new_len, e, pool + t.pool + t.k, &tab[at].movers, t.k, c);
+        }
+      }
+#pragma unroll
+      for (int o = kWave / 2; o > 0; o >>= 1) found += __shfl_xor(found, o);
+      if (lane == 0 && found != 0) atomicAdd(&tab[at].found, found);
+      continue;
+    }
     const bool ins_item = w < ni;
     const long long x = ins_item ? w : w - ni;
     int dir, row, entry;
@@ -279,21 +423,21 @@ __global__ __launch_bounds__(256) void k_topo_rewrite(int undirected, long long 
     if (static_cast<int>(!ins_item && nins != 0) | (cap0 | static_cast<int>(src_off >> 32)) >> 31) continue;
     const int need = len0 - k + nins;
     const bool move = nins > 0 && need > cap0;
+    const bool swept = long_ok && k > 0 && !move && len0 >= kLongRow;  // listed by the plan
     const int nc = move ? grow_cap(need) : 0;
     // a moving row's arena slots: the returning atomic stays in flight while the
     // row is read (its value is needed only for the writes)
     long long moved_to = 0;
     if (move && lane == 0) moved_to = static_cast<long long>(atomicAdd(&p->top[dir], static_cast<u64>(nc)));
     long long dst_off = src_off;
-    if (k > 0 || move) {
+    if (!swept && (k > 0 || move)) {
       const int *src = a.col + src_off;
       const float *srcw = a.wt != nullptr ? a.wt + src_off : nullptr;  // weights move with their slots
       int wpos = 0;
       // kRewriteU entries per lane per step (rows up to 1024 entries take one step):
-      // the step's row reads, then its hash probes together with the net decisions
-      // of the probed slots, are all in flight at once (a probe that meets another
-      // key continues alone); all reads of a step precede its writes, and a kept
-      // entry is written at or below its own position, so the in-place case is safe.
+      // the step's row reads, then its hash probes, are all in flight at once; all
+      // reads of a step precede its writes, and a kept entry is written at or below
+      // its own position, so the in-place case is safe.
       for (int base = 0; base < len0; base += kWave * kRewriteU) {
         int x[kRewriteU];
         float xw[kRewriteU];
@@ -305,51 +449,7 @@ __global__ __launch_bounds__(256) void k_topo_rewrite(int undirected, long long 
           x[u] = keep[u] ? src[e] : -1;
           xw[u] = keep[u] && srcw != nullptr ? srcw[e] : 0.0f;
         }
-        if (k > 0) {
-          u64 key[kRewriteU], got[kRewriteU];
-          unsigned sl[kRewriteU];
-          int net[kRewriteU];
-#pragma unroll
-          for (int u = 0; u < kRewriteU; ++u) {
-            key[u] = edge_key(dir ? x[u] : row, dir ? row : x[u], undirected, n);
-            sl[u] = hash_slot(key[u], mask);
-          }
-#pragma unroll
-          for (int u = 0; u < kRewriteU; ++u) {
-            got[u] = keep[u] ? ht_key[sl[u]] : kEmptyKey;
-            net[u] = keep[u] ? ht_net[sl[u]] : 0;
-          }
-          // keys found in their first slot are decided; the others walk their probe
-          // chains one slot per round, all of a lane's walks in the same round (the
-          // table is at most an eighth full, so every chain meets an empty slot)
-          unsigned pend = 0;
-#pragma unroll
-          for (int u = 0; u < kRewriteU; ++u) {
-            if (!keep[u] || got[u] == kEmptyKey) continue;
-            if (got[u] == key[u]) keep[u] = net[u] != -1;
-            else pend |= 1u << u;
-          }
-          for (unsigned j = 1; pend != 0; ++j) {
-#pragma unroll
-            for (int u = 0; u < kRewriteU; ++u) {
-              if (pend >> u & 1u) {
-                const unsigned s2 = (sl[u] + j) & mask;
-                got[u] = ht_key[s2];
-                net[u] = ht_net[s2];
-              }
-            }
-#pragma unroll
-            for (int u = 0; u < kRewriteU; ++u) {
-              if (!(pend >> u & 1u)) continue;
-              if (got[u] == key[u]) {
-                keep[u] = net[u] != -1;
-                pend &= ~(1u << u);
-              } else if (got[u] == kEmptyKey) {
-                pend &= ~(1u << u);  // not named by the batch: kept
-              }
-            }
-          }
-        }
+        if (k > 0) drop_deleted(x, keep, row, dir, undirected, n, ht_key, ht_net, mask);
         if (base == 0 && move) dst_off = __shfl(moved_to, 0);
         int *dst = a.col + dst_off;
         float *dstw = a.wt != nullptr ? a.wt + dst_off : nullptr;
@@ -373,6 +473,28 @@ __global__ __launch_bounds__(256) void k_topo_rewrite(int undirected, long long 
       }
       a.len[row] = need;
       if (dir == 0) ddeg[row] = nins - k;
+    }
+  }
+}
+
+// The fill pass of the long rows: each hole takes one mover's entry (and weight).
+// The sweeps found as many holes as movers and every deleted entry, else the
+// check bit is set.
+__global__ void k_topo_fill(Adj out, Adj in, const LongRow *tab, const int *pool, Counters *c) {
+  const u64 lr = c->long_rows;
+  if (aborted_with(c->abort, static_cast<long long>(lr >> 1))) return;
+  const long long n_long = static_cast<long long>(lr >> 40);
+  const int lane = lane_id();
+  for (long long r = global_wave(); r < n_long; r += num_waves()) {
+    const LongRow t = tab[r];
+    if (lane == 0 && (t.holes != t.movers || t.found != t.k)) atomicOr(&c->err, 2ull);
+    int pairs = t.holes < t.movers ? t.holes : t.movers;
+    if (pairs > t.k) pairs = t.k;  // the sweeps record at most k of each
+    const Adj &a = t.dir ? in : out;
+    for (int i = lane; i < pairs; i += kWave) {
+      const long long hole = t.off + pool[t.pool + i], mover = t.off + pool[t.pool + t.k + i];
+      a.col[hole] = a.col[mover];
+      if (a.wt != nullptr) a.wt[hole] = a.wt[mover];
     }
   }
 }
@@ -418,18 +540,26 @@ void launch_net_decide(hipStream_t s, int cap_ops, const BatchIn *in, const ripp
 }
 
 void launch_topo_plan(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
-                      const int *ins_rank, Counters *c, const Persist *p, long long cap_out, long long cap_in) {
-  hipLaunchKernelGGL(k_topo_plan, dim3(blocks_for(2LL * cap_arcs, 256, 1024)), dim3(256), 0, s, out, in, ins_src,
-                     ins_dst, ins_rank, c, p, cap_out, cap_in);
+                      const int *del_src, const int *del_dst, const int *ins_rank, const int *del_rank,
+                      int long_ok, LongRow *tab, Counters *c, const Persist *p, long long cap_out, long long cap_in) {
+  hipLaunchKernelGGL(k_topo_plan, dim3(blocks_for((long_ok ? 4LL : 2LL) * cap_arcs, 256, 1024)), dim3(256), 0, s,
+                     out, in, ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank, long_ok, tab, c, p, cap_out,
+                     cap_in);
 }
 
 void launch_topo_rewrite(hipStream_t s, int cap_arcs, int undirected, long long n, Adj out, Adj in,
                          const int *ins_src, const int *ins_dst, const int *del_src, const int *del_dst,
                          const int *ins_rank, const int *del_rank, const u64 *ht_key, const int *ht_net,
-                         unsigned mask, Persist *p, int *ddeg, Counters *c) {
+                         unsigned mask, Persist *p, int *ddeg, int long_ok, LongRow *tab, int *pool, Counters *c) {
   hipLaunchKernelGGL(k_topo_rewrite, dim3(blocks_for(4LL * cap_arcs * kWave, 256)), dim3(256), 0, s, undirected,
                      n, out, in, ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank, ht_key, ht_net, mask, p,
-                     ddeg, c);
+                     ddeg, long_ok, tab, pool, c);
+}
+
+void launch_topo_fill(hipStream_t s, int cap_arcs, Adj out, Adj in, const LongRow *tab, const int *pool,
+                      Counters *c) {
+  hipLaunchKernelGGL(k_topo_fill, dim3(blocks_for(2LL * cap_arcs * kWave, 256, 1024)), dim3(256), 0, s, out, in,
+                     tab, pool, c);
 }
 
 void launch_repack_copy(hipStream_t s, long long n, const int *old_col, const long long *old_off, const int *len,

@@ -148,6 +148,11 @@ struct ripple_ctx {
   int *ins_rank = nullptr, *del_rank = nullptr;
   float *ins_w = nullptr, *del_w = nullptr;  // the net arcs' weights (weighted graphs)
   int *flist = nullptr;
+  // rows long enough for the chunked delete sweep exist (or may, once rows grow):
+  // the plan lists such rows in long_tab, their sweeps record positions in long_pool
+  int long_ok = 0;
+  rp::LongRow *long_tab = nullptr;
+  int *long_pool = nullptr;
 
   // last batch
   bool has_batch = false;
@@ -395,6 +400,8 @@ ripple_status repack_adj(ripple_ctx *c, int dir) {
 }
 
 void free_batch_scratch(ripple_ctx *c) {
+  dfree_t(c, c->long_tab);
+  dfree_t(c, c->long_pool);
   dfree_t(c, c->d_ops);
   dfree_t(c, c->ht_key);
   dfree_t(c, c->ht_val);
@@ -442,6 +449,10 @@ ripple_status ensure_batch_scratch(ripple_ctx *c, long long ops, long long frows
   RP_TRY(dalloc_n(c, &c->del_w, arcs));
   RP_TRY(dalloc_n(c, &c->del_rank, 2 * arcs));
   RP_TRY(dalloc_n(c, &c->flist, cap));
+  if (c->long_ok) {  // at most one long row per (net arc, direction), and two slots per deleted entry
+    RP_TRY(dalloc_n(c, &c->long_tab, 2 * arcs));
+    RP_TRY(dalloc_n(c, &c->long_pool, 4 * arcs));
+  }
   RP_HIP(c, hipHostMalloc(reinterpret_cast<void **>(&c->h_ops), cap * sizeof(ripple_op), hipHostMallocDefault));
   RP_HIP(c, hipHostMalloc(reinterpret_cast<void **>(&c->h_feat), fcap * c->dims[0] * sizeof(float),
                           hipHostMallocDefault));
@@ -716,12 +727,14 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
   }
   {
     PhaseScope ps(c, RIPPLE_PHASE_TOPO);
-    rp::launch_topo_plan(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->ins_rank, dc, c->d_persist,
-                         c->col_capacity[0], c->col_capacity[1]);
+    rp::launch_topo_plan(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank,
+                         c->del_rank, c->long_ok, c->long_tab, dc, c->d_persist, c->col_capacity[0],
+                         c->col_capacity[1]);
     rp::launch_topo_rewrite(s, cap_arcs, c->undirected, c->n, out, in, c->ins_src, c->ins_dst, c->del_src,
                             c->del_dst, c->ins_rank, c->del_rank, c->ht_key, c->ht_net, c->ht_mask, c->d_persist,
-                            c->ddeg, dc);
-    add_launches(c, RIPPLE_PHASE_TOPO, 2);
+                            c->ddeg, c->long_ok, c->long_tab, c->long_pool, dc);
+    if (c->long_ok) rp::launch_topo_fill(s, cap_arcs, out, in, c->long_tab, c->long_pool, dc);
+    add_launches(c, RIPPLE_PHASE_TOPO, c->long_ok ? 3 : 2);
   }
   {
     PhaseScope ps(c, RIPPLE_PHASE_LAYER0);
@@ -1177,6 +1190,10 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   if (e != hipSuccess) return bail(device_fail(c, e, "hipHostMalloc"));
   *c->h_in = rp::BatchIn{};
   std::vector<int> olen(outdeg), ilen(indeg);
+  // hubs of half the long-row length or more: their rows may need the chunked sweep
+  const int max_len = std::max(olen.empty() ? 0 : *std::max_element(olen.begin(), olen.end()),
+                               ilen.empty() ? 0 : *std::max_element(ilen.begin(), ilen.end()));
+  c->long_ok = max_len >= rp::kLongRow / 2 ? 1 : 0;
   if ((st = upload_adj(c, 0, olen, ocol, ooff, ow)) != RIPPLE_OK) return bail(st);
   if ((st = upload_adj(c, 1, ilen, icol, ioff, iw)) != RIPPLE_OK) return bail(st);
   // persistent per-vertex scratch
@@ -1412,6 +1429,7 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
     stats->pull_layers = c->last_pull;
     stats->dense_layers = c->last_dense;
     stats->graph_replay = c->last_graph ? 1 : 0;
+    stats->long_rows = static_cast<int64_t>(k.long_rows >> 40);
   }
   return RIPPLE_OK;
 }

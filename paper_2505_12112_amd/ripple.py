@@ -74,7 +74,7 @@ class BatchStats(C.Structure):
         ("pushed_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("dest_rows", C.c_int64 * (MAX_LAYERS + 1)),
         ("relocated_rows", C.c_int64), ("repacks", C.c_int64),
         ("in_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("pull_layers", C.c_int32), ("dense_layers", C.c_int32),
-        ("reweighted_arcs", C.c_int64), ("graph_replay", C.c_int64),
+        ("reweighted_arcs", C.c_int64), ("graph_replay", C.c_int64), ("long_rows", C.c_int64),
     ]
 
 
@@ -256,7 +256,7 @@ class Ripple:
             "pushed_arcs": list(st.pushed_arcs[:L + 1]), "dest_rows": list(st.dest_rows[:L + 1]),
             "relocated_rows": st.relocated_rows, "repacks": st.repacks,
             "in_arcs": list(st.in_arcs[:L + 1]), "pull_layers": st.pull_layers, "dense_layers": st.dense_layers,
-            "reweighted_arcs": st.reweighted_arcs, "graph_replay": st.graph_replay,
+            "reweighted_arcs": st.reweighted_arcs, "graph_replay": st.graph_replay, "long_rows": st.long_rows,
         }
 
     def apply_updates_raw(self, ops: np.ndarray, feat_rows: Optional[np.ndarray], stats: BatchStats) -> None:

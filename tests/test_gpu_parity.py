@@ -96,6 +96,63 @@ def test_adversarial_batches(agg, undirected, mode):
         p.close()
 
 
+def _hub_graph(rng, n, hub_in, hub_out, extra, undirected):
+    """Vertex 0 is a hub: arcs from 1..hub_in into it and (directed graphs) from it to
+    1..hub_out, plus `extra` random arcs among the other vertices."""
+    if undirected:
+        src = np.zeros(hub_in, np.int64)
+        dst = np.arange(1, hub_in + 1, dtype=np.int64)
+    else:
+        src = np.concatenate([np.arange(1, hub_in + 1), np.zeros(hub_out, np.int64)])
+        dst = np.concatenate([np.zeros(hub_in, np.int64), np.arange(1, hub_out + 1)])
+    es, ed = synth.erdos_renyi(n - 1, extra, rng, undirected=undirected)
+    src = np.concatenate([src, es.astype(np.int64) + 1]).astype(np.int32)
+    dst = np.concatenate([dst, ed.astype(np.int64) + 1]).astype(np.int32)
+    return src, dst
+
+
+@pytest.mark.parametrize("agg,slack,undirected", [("sum", 0.25, False), ("gcn", 0.25, False), ("sum", 0.0, False),
+                                                  ("mean", 0.25, True)])
+def test_long_rows_swept_in_chunks(agg, slack, undirected):
+    """A hub with ~20,000 in- and out-arcs: batches that delete and insert hub arcs.
+    Rows of 16384 entries or more that keep their slots have their deletes swept by
+    many waves and filled from their tails (with slack 0 every insert moves its row,
+    so rows with inserts take the one-wave path and delete-only rows the sweep); the
+    arc set, aggregates and embeddings must match the oracle exactly as elsewhere."""
+    _say("long rows", agg, slack, undirected)
+    rng = np.random.default_rng(61 + int(slack * 4) + 2 * undirected)
+    # 24,000 rows: a hidden width of 32 keeps rows whose every component sits near
+    # zero (where the error floor of the row-relative measure bites) out of the test
+    n, dims = 24000, (8, 32, 6)
+    src, dst = _hub_graph(rng, n, 20000, 18000, 16000, undirected)
+    x = rng.standard_normal((n, dims[0])).astype(np.float32)
+    w = synth.model_weights(synth.ModelSpec(agg, dims), rng, bias_std=0.1)
+    p = Pair(n, src, dst, x, w, undirected=undirected, slack=slack, min_slack=0 if slack == 0 else 4)
+    try:
+        swept = 0
+        for b in range(8):
+            a_src, a_dst = p.orc.graph.arcs()
+            hub = np.flatnonzero((a_src == 0) | (a_dst == 0))
+            pick = rng.choice(hub, 40, replace=False)
+            dels = np.stack([np.full(40, 2), a_src[pick], a_dst[pick], np.full(40, -1)], 1)
+            fresh = rng.integers(20001, n, 12)
+            ins = np.stack([np.ones(12, np.int64), fresh, np.zeros(12, np.int64), np.full(12, -1)], 1)
+            if not undirected:
+                ins[6:, 1], ins[6:, 2] = 0, rng.integers(18001, n, 6)
+            rest = random_valid_batch(rng, p.orc, 20, dims[0])
+            ops = np.concatenate([dels, ins, np.asarray(rest.ops, np.int64)]).astype(np.int32)
+            st, _, _ = p.step(synth.Batch(ops, rest.feat_rows))
+            swept += st["long_rows"]
+            if b % 3 == 2:
+                p.check_arcs()
+        assert swept > 0, "no row took the chunked sweep"
+        p.check_arcs()
+        p.check_embeddings()
+        p.check_aggregates()
+    finally:
+        p.close()
+
+
 @pytest.mark.parametrize("agg,arena", [("sum", 0), ("gcn", 0), ("sum", 64), ("mean", 2000), ("sum", 2000),
                                        ("gc_wsum", 0), ("gc_wsum", 64)])
 def test_no_slack_forces_row_moves_and_relayouts(agg, arena):
