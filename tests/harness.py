@@ -51,7 +51,25 @@ def _hip():
         _HIP.hipMalloc.argtypes = [C.POINTER(C.c_void_p), C.c_size_t]
         _HIP.hipMemcpy.argtypes = [C.c_void_p, C.c_void_p, C.c_size_t, C.c_int]
         _HIP.hipFree.argtypes = [C.c_void_p]
+        _HIP.hipStreamCreateWithFlags.argtypes = [C.POINTER(C.c_void_p), C.c_uint]
+        _HIP.hipStreamDestroy.argtypes = [C.c_void_p]
     return _HIP
+
+
+class CallerStream:
+    """A stream the caller owns (hipStreamCreateWithFlags, default priority), for
+    contexts that run on a stream they did not create; destroyed on exit."""
+
+    def __enter__(self):
+        p = C.c_void_p()
+        if _hip().hipStreamCreateWithFlags(C.byref(p), 1) != 0:  # non-blocking
+            raise RuntimeError("hipStreamCreateWithFlags failed")
+        self.handle = p.value
+        return self
+
+    def __exit__(self, *exc):
+        _hip().hipStreamDestroy(C.c_void_p(self.handle))
+        return False
 
 
 class Pair:

@@ -11,7 +11,7 @@ import pytest
 from oracle import ripple_oracle as O
 from paper_2505_12112_amd import synth
 from paper_2505_12112_amd.ripple import PHASES, Ripple, RippleError, E_INVALID, E_STATE, E_OOM
-from tests.harness import Pair, random_valid_batch, FP32_TOL
+from tests.harness import CallerStream, Pair, random_valid_batch, FP32_TOL
 
 pytestmark = pytest.mark.gpu
 
@@ -336,6 +336,40 @@ def test_phase_stats_count_launches_and_bytes(mode):
         p.check_embeddings()
     finally:
         p.close()
+
+
+@pytest.mark.parametrize("launch", ["direct", "graph"])
+def test_two_contexts_on_a_caller_stream(launch):
+    """Two contexts on one GPU, one on a stream the caller created and one on its
+    own, fed interleaved batches: each keeps its own graph, caches, scratch and
+    counters, and both match their oracles."""
+    rng = np.random.default_rng(71)
+    dims = (8, 20, 5)
+    s1, d1, x1, w1 = _small(rng, 500, 2500, dims, "sum")
+    s2, d2, x2, w2 = _small(rng, 400, 1600, dims, "gcn", undirected=True)
+    with CallerStream() as stream:
+        _two_contexts(rng, dims, launch, stream.handle, (s1, d1, x1, w1), (s2, d2, x2, w2))
+
+
+def _two_contexts(rng, dims, launch, stream, a, b_):
+    s1, d1, x1, w1 = a
+    s2, d2, x2, w2 = b_
+    pa = Pair(500, s1, d1, x1, w1, graphs=launch == "graph", stream=stream)
+    pb = Pair(400, s2, d2, x2, w2, undirected=True, graphs=launch == "graph")
+    try:
+        for b in range(30):
+            pa.step(random_valid_batch(rng, pa.orc, int(rng.integers(1, 60)), dims[0]))
+            pb.step(random_valid_batch(rng, pb.orc, int(rng.integers(1, 60)), dims[0]))
+            if b % 10 == 9:
+                pa.check_embeddings()
+                pb.check_embeddings()
+        pa.check_arcs()
+        pb.check_arcs()
+        pa.check_aggregates()
+        pb.check_aggregates()
+    finally:
+        pa.close()
+        pb.close()
 
 
 def test_empty_and_noop_batches():
