@@ -243,10 +243,10 @@ void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerP
 int compact_blocks(long long n);
 // Outputs of one compaction of bitmaps (a | b) into an ascending list. Optional
 // (nullptr = skipped): list, doff[j] = sum of out_deg over list[0..j) (doff[count]
-// = total), ioff likewise over in_deg, keep = the compacted bitmap words, wprefix[w]
-// = listed vertices in words before w (so the list position of a member u is
-// wprefix[u / 32] + the member bits of its word below u). Both input bitmaps are
-// cleared. full_n > 0: list all of 0..full_n-1 instead (the bitmaps are not read).
+// = total), ioff likewise over in_deg, memb[w] = (the compacted bitmap word w,
+// listed vertices in words before w), so the list position of a member u is
+// memb[u / 32].y + the member bits of its word below u, and one 8-byte load
+// answers both questions. Both input bitmaps are cleared. full_n > 0: list all of 0..full_n-1 instead (the bitmaps are not read).
 struct CompactOut {
   long long full_n;
   int *list;
@@ -258,8 +258,7 @@ struct CompactOut {
   u64 *in_total;       // receives the sum of in_deg over the list
   u64 *out_total;      // receives the sum of out_deg over the list (the next scatter's arcs)
   u64 *sinks_a;        // receives the number of bits set in the first bitmap
-  unsigned *keep;
-  int *wprefix;
+  uint2 *memb;
 };
 // Tile sums published by the single-pass compaction: compact_scratch_words(n)
 // words, zero when first used, then owned by the compactions of one vertex count
@@ -308,12 +307,11 @@ void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, 
 
 // pull: for every vertex v of the sorted list A (in-arc prefix ioff; list null =
 // the identity), S[v] += sum of msg[rank(u)] over in-arcs (u -> v) whose source u
-// is set in member, rank from wprefix (see CompactOut). One flush (row of fp32
+// is a member by memb, its rank from memb too (see CompactOut). One flush (row of fp32
 // atomics) per sink and lane group; each in-arc is read once. mark (nullable):
 // set the bit of every sink that received a message (the dense form's frontier).
 void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *ioff,
-                      Adj in, const unsigned *member, const int *wprefix, const float *msg, float *S,
-                      unsigned *mark, const Counters *c);
+                      Adj in, const uint2 *memb, const float *msg, float *S, unsigned *mark, const Counters *c);
 
 // bootstrap pull: S[v] = sum over in-arcs c_u H[u]
 void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev, Adj in, const int *out_len,

@@ -346,11 +346,11 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
 #pragma unroll
   for (int k = 0; k < kVals; ++k) base[k] = base_s[k];
   long long pos = base[0] + ex[0], dpos = base[1] + ex[1], ipos = base[2] + ex[2];
-  if (o.wprefix != nullptr) {
+  if (o.memb != nullptr) {
     long long wp = pos;
 #pragma unroll
     for (int i = 0; i < kWordsPerThread; ++i) {
-      if (w0 + i < words) o.wprefix[w0 + i] = static_cast<int>(wp);
+      if (w0 + i < words) o.memb[w0 + i] = make_uint2(wv[i], static_cast<unsigned>(wp));
       wp += __popc(wv[i]);
     }
   }
@@ -385,7 +385,6 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
   for (int i = 0; i < kWordsPerThread; ++i) {
     const long long w = w0 + i;
     if (w < words) {
-      if (o.keep != nullptr) o.keep[w] = wv[i];
       if (o.full_n == 0) {
         bm_a[w] = 0u;
         bm_b[w] = 0u;
@@ -600,8 +599,8 @@ constexpr int kPullChunk = kWave * kPullArcs;
 
 template <int G, int NC, int U>
 __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *list, const u64 *count,
-                                                   const long long *ioff, Adj in, const unsigned *member,
-                                                   const int *wprefix, const float *msg, float *S, unsigned *mark,
+                                                   const long long *ioff, Adj in, const uint2 *memb,
+                                                   const float *msg, float *S, unsigned *mark,
                                                    const Counters *c) {
   __shared__ int2 pairs[256 / kWave][kPullChunk];
   __shared__ float pair_w[256 / kWave][kPullChunk];  // the in-arcs' weights (weighted graphs)
@@ -671,10 +670,9 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
     for (int a = 0; a < kPullArcs; ++a) {
       int j = -1;
       if (u[a] >= 0) {
-        const unsigned word = member[u[a] >> 5];
-        const int below = wprefix[u[a] >> 5];  // issued with the member word
+        const uint2 mw = memb[u[a] >> 5];  // the member word and the members before it
         const unsigned bit = 1u << (u[a] & 31);
-        if (word & bit) j = below + __popc(word & (bit - 1u));
+        if (mw.x & bit) j = static_cast<int>(mw.y) + __popc(mw.x & (bit - 1u));
       }
       if (a < per_lane) {
         wp[lane * per_lane + a] = make_int2(v[a], j);
@@ -862,12 +860,12 @@ void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, 
 }
 
 void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count,
-                      const long long *ioff, Adj in, const unsigned *member, const int *wprefix, const float *msg,
+                      const long long *ioff, Adj in, const uint2 *memb, const float *msg,
                       float *S, unsigned *mark, const Counters *c) {
   const int blocks = 2048;
 #define RP_PULLM(GV, NCV, UV)                                                                                    \
   hipLaunchKernelGGL((k_pull_msgs<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, ioff, in, \
-                     member, wprefix, msg, S, mark, c)
+                     memb, msg, S, mark, c)
   if (d <= 16) RP_PULLM(16, 1, 8);
   else if (d <= 32) RP_PULLM(16, 2, 8);
   else if (d <= 48) RP_PULLM(16, 3, 8);

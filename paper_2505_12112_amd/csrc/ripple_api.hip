@@ -110,8 +110,9 @@ struct ripple_ctx {
   int *lists[rp::kMaxL + 1] = {};
   long long *doff[rp::kMaxL + 1] = {};  // out-degree prefix of lists[l] (first arc index per vertex)
   long long *ioff = nullptr;            // in-degree prefix of the current layer's A^l (pull form)
-  unsigned *keep[2] = {nullptr, nullptr};  // bitmap of lists[k] for k = 0, 1 mod 2 (pull membership)
-  int *wprefix[2] = {nullptr, nullptr};    // members of lists[k] before each bitmap word (message rows)
+  // per bitmap word of lists[k], k = 0, 1 mod 2: (member bits, members before the
+  // word); the pull form's membership test and message row in one load
+  uint2 *memb[2] = {nullptr, nullptr};
   int scatter_mode = RIPPLE_SCATTER_AUTO;
   long long last_pushed[rp::kMaxL + 1] = {};
   long long last_in[rp::kMaxL + 1] = {};
@@ -488,8 +489,7 @@ void free_model(ripple_ctx *c) {
   dfree_t(c, c->delta[1]);
   dfree_t(c, c->ioff);
   for (int k = 0; k < 2; ++k) {
-    dfree_t(c, c->keep[k]);
-    dfree_t(c, c->wprefix[k]);
+    dfree_t(c, c->memb[k]);
   }
   free_batch_scratch(c);
   c->inited = false;
@@ -749,8 +749,7 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
     co.doff = c->doff[0];
     co.out_total = &dc->pushed[1];
     const bool members = p.mode[1] != kPushLayer;  // layer 1 pulls: it needs A^0's membership
-    co.keep = members ? c->keep[0] : nullptr;
-    co.wprefix = members ? c->wprefix[0] : nullptr;
+    co.memb = members ? c->memb[0] : nullptr;
     rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
     const rp::Delta0Args z{c->agg, c->dims[0], rp::row_ld(c->dims[0]), c->d_ops, c->d_in, c->fop, c->H[0],
                            c->adj[0].len, c->ddeg, c->delta[0], dc};
@@ -774,8 +773,7 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
     }
     const int mode = p.mode[l];
     const int ld = rp::row_ld(c->sw[l]);  // message row stride
-    const unsigned *member = c->keep[(l - 1) & 1];
-    const int *wprefix = c->wprefix[(l - 1) & 1];
+    const uint2 *memb = c->memb[(l - 1) & 1];
     if (mode == kDenseLayer) {
       // dense: mark the net arcs' heads and D (no arcs), list every vertex with its
       // in-arc prefix, pull over every in-arc and mark the sinks that received a
@@ -798,7 +796,7 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
         add_launches(c, RIPPLE_PHASE_COMPACT, 1);
       }
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
-      rp::launch_pull_msgs(s, c->n, c->sw[l], ld, nullptr, &dc->count_all, c->ioff, in_msg, member, wprefix, msg,
+      rp::launch_pull_msgs(s, c->n, c->sw[l], ld, nullptr, &dc->count_all, c->ioff, in_msg, memb, msg,
                            c->S[l], c->bm_out, dc);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     } else {
@@ -822,14 +820,13 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
       co.out_total = l < c->L ? &dc->pushed[l + 1] : nullptr;
       co.sinks_a = &dc->dest[l];  // distinct sinks of the arcs pushed at layer l
       const bool members = l < c->L && p.mode[l + 1] != kPushLayer;
-      co.keep = members ? c->keep[l & 1] : nullptr;
-      co.wprefix = members ? c->wprefix[l & 1] : nullptr;
+      co.memb = members ? c->memb[l & 1] : nullptr;
       rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
       add_launches(c, RIPPLE_PHASE_COMPACT, 1);
     }
     if (mode == kPullLayer) {
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
-      rp::launch_pull_msgs(s, c->n, c->sw[l], ld, c->lists[l], &dc->count[l], c->ioff, in_msg, member, wprefix, msg,
+      rp::launch_pull_msgs(s, c->n, c->sw[l], ld, c->lists[l], &dc->count[l], c->ioff, in_msg, memb, msg,
                            c->S[l], nullptr, dc);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
@@ -1313,8 +1310,7 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   RP_TRY(dalloc_n(c, &c->delta[1], n * rp::row_ld(c->dmax_delta)));
   RP_TRY(dalloc_n(c, &c->ioff, n + 1));
   for (int k = 0; k < 2; ++k) {
-    RP_TRY(dalloc_n(c, &c->keep[k], (n + 31) / 32));
-    RP_TRY(dalloc_n(c, &c->wprefix[k], (n + 31) / 32));
+    RP_TRY(dalloc_n(c, &c->memb[k], (n + 31) / 32));
   }
   if (msg_width > 0) RP_TRY(dalloc_n(c, &c->msg, n * rp::row_ld(msg_width)));
   if (gin) {
