@@ -684,10 +684,17 @@ BatchPlan make_plan(const ripple_ctx *c) {
   BatchPlan p{};
   unsigned long long key = static_cast<unsigned long long>(c->parity);
   int bit = 1;
+  // expected rows: the previous batch's counts; before any batch, the batch's ops
+  // times the mean degree per hop (no more than n)
+  long long guess[rp::kMaxL + 1];
+  const double deg = static_cast<double>(c->arcs_now) / static_cast<double>(c->n);
+  double g = static_cast<double>(c->h_in->num_ops);
+  for (int l = 0; l <= c->L; ++l, g *= deg)
+    guess[l] = c->has_batch ? c->last_count[l] : static_cast<long long>(std::min(g, static_cast<double>(c->n)));
   for (int l = 1; l <= c->L; ++l) {
     p.mode[l] = layer_mode(c, l);
-    p.tf_rows[l] = c->has_batch ? c->last_count[l - 1] : 0;
-    p.rows[l] = c->has_batch ? c->last_count[l] : 0;
+    p.tf_rows[l] = guess[l - 1];
+    p.rows[l] = guess[l];
     key |= static_cast<unsigned long long>(p.mode[l]) << bit;
     key |= static_cast<unsigned long long>(rp::gemm_variant(p.tf_rows[l])) << (bit + 2);
     key |= static_cast<unsigned long long>(rp::gemm_variant(p.rows[l])) << (bit + 3);
