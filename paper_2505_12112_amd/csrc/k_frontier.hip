@@ -23,6 +23,7 @@ constexpr int kWordsPerBlock = kCompactThreads * kWordsPerThread;
 // resident at once (graphs up to 2M vertices; larger ones, whose compactions take
 // long enough not to notice a round trip, go in ticket order).
 constexpr long long kIndexTiles = 64;
+static_assert(kIndexTiles <= kWave, "one lane per predecessor tile");
 
 __device__ inline int lane_id() { return threadIdx.x & (kWave - 1); }
 
@@ -236,11 +237,12 @@ __device__ inline bool fetch(const u64 *p, u64 epoch, long long (&v)[kVals]) {
 // Single-pass compaction (a decoupled look-back prefix scan). Tiles of
 // kWordsPerBlock bitmap words go to blocks by index when all tiles fit on the GPU at
 // once, else in ticket order; either way a tile's predecessors are running or done
-// when it waits for them. Each tile publishes its sums at once,
-// then wave 0 walks back over the predecessors (64 per step), adding their tile
-// sums until it meets one that has published its inclusive prefix. A tile
-// publishes its own sums before it waits, so every wait is for work that needs no
-// waiting: all waits end. A wait that outlasts kSpinLimit polls (a predecessor
+// when it waits for them. Each tile publishes its sums at once. A tile placed by
+// index then reads all its predecessors' sums in one round (one lane each); in
+// ticket order, wave 0 walks back over the predecessors (64 per step), adding
+// their tile sums until it meets one that has published its inclusive prefix. A
+// tile publishes its own sums before it waits, so every wait is for work that
+// needs no waiting: all waits end. A wait that outlasts kSpinLimit polls (a predecessor
 // that never ran) sets bit 2 of the error word and counts the tile as empty (the
 // batch then fails loudly instead of hanging).
 // Output: the marked vertices of both bitmaps as a sorted list with prefix sums of
@@ -293,8 +295,36 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
   long long ex[kVals], tot[kVals];
   block_scan(st, ex, tot, red);  // its barriers also publish epoch_s
   const u64 epoch = epoch_s;
-  if (threadIdx.x == 0) publish((tile == 0 ? inc : agg) + tile * kVals, epoch, tot);
-  if (threadIdx.x < kWave) {
+  // Tiles by index publish their sums only: every predecessor's are read in one
+  // round (one lane each). Tiles in ticket order also publish inclusive prefixes.
+  if (threadIdx.x == 0) publish((by_ticket && tile == 0 ? inc : agg) + tile * kVals, epoch, tot);
+  if (threadIdx.x < kWave && !by_ticket) {
+    const int lane = lane_id();
+    long long v[kVals] = {};
+    bool timed_out = false;
+    if (lane < tile) {
+      for (int it = 0;; ++it) {
+        if (fetch(agg + lane * kVals, epoch, v)) break;
+        if (it >= kSpinLimit) {
+          timed_out = true;
+#pragma unroll
+          for (int k = 0; k < kVals; ++k) v[k] = 0;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kVals; ++k) {
+#pragma unroll
+      for (int o2 = kWave / 2; o2 > 0; o2 >>= 1) v[k] += __shfl_xor(v[k], o2);
+    }
+    if (timed_out) atomicOr(err, 4ull);
+    if (lane == 0) {
+#pragma unroll
+      for (int k = 0; k < kVals; ++k) base_s[k] = v[k];
+    }
+  } else if (threadIdx.x < kWave) {
     const int lane = lane_id();
     long long acc[kVals] = {};
     bool timed_out = false;
@@ -304,8 +334,13 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
       bool incl = true;  // lanes before tile 0 end the walk with zeros
       if (p >= 0) {
         for (int it = 0;; ++it) {
-          if (fetch(inc + p * kVals, epoch, v)) break;
-          if (fetch(agg + p * kVals, epoch, v)) {
+          long long va[kVals];  // both words are read in the same round
+          const bool got_inc = fetch(inc + p * kVals, epoch, v);
+          const bool got_agg = fetch(agg + p * kVals, epoch, va);
+          if (got_inc) break;
+          if (got_agg) {
+#pragma unroll
+            for (int k = 0; k < kVals; ++k) v[k] = va[k];
             incl = false;
             break;
           }
