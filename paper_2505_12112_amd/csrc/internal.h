@@ -236,10 +236,22 @@ void launch_topo_fill(hipStream_t s, int cap_arcs, Adj out, Adj in, const LongRo
 // the adjacency keeps weights).
 // ins_w / del_w (nullable): the arcs' weights as the corrections use them
 // (weighted-sum model).
+// direct.list != nullptr: the layer-1 dirty set is the feature-written vertices
+// alone (no GCN term; flist holds each once) and at most kDirectListMax of them.
+// Then they are not marked: the kernel lists them itself, in flist's order, with
+// their out-degree prefix (the compaction's list, doff, count and out_total
+// outputs; a larger count sets check bit 2).
+constexpr int kDirectListMax = 1024;
+struct DirectList {
+  int *list;
+  long long *doff;
+  u64 *count;
+  u64 *out_total;
+};
 void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerPtrs lp, Adj out, Adj in,
                       const int *ins_rank, const float *arc_w, const int *ddeg, const int *flist, const int *ins_src,
                       const int *ins_dst, const int *del_src, const int *del_dst, const float *ins_w,
-                      const float *del_w, unsigned *bm, Counters *c);
+                      const float *del_w, unsigned *bm, Counters *c, const DirectList &direct);
 int compact_blocks(long long n);
 // Outputs of one compaction of bitmaps (a | b) into an ascending list. Optional
 // (nullptr = skipped): list, doff[j] = sum of out_deg over list[0..j) (doff[count]

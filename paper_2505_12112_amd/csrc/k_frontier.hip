@@ -50,13 +50,62 @@ inline int blocks_for(long long items, int threads, int cap = 4096) {
 __global__ void k_corr_mark(int agg, LayerPtrs lp, Adj out, Adj in, const int *ins_rank, const float *arc_w,
                             const int *ddeg, const int *flist, const int *ins_src, const int *ins_dst,
                             const int *del_src, const int *del_dst, const float *ins_w, const float *del_w,
-                            unsigned *bm, Counters *c) {
+                            unsigned *bm, Counters *c, DirectList dl) {
   const long long nf = static_cast<long long>(c->n_feat);
   const long long ni = static_cast<long long>(c->n_ins);
   const long long na = ni + static_cast<long long>(c->n_del);
   if (aborted_with(c->abort, nf, na)) return;
   const int lane = lane_id();
   const int *out_len = out.len;
+  if (dl.list != nullptr && blockIdx.x == 0) {
+    // block 0 lists the dirty set (flist[0, nf), distinct vertices) with the
+    // exclusive prefix of their post-batch out-degrees: four entries per thread
+    constexpr int kPer = kDirectListMax / 256;
+    static_assert(kPer * 256 == kDirectListMax, "four entries per thread");
+    __shared__ long long wsum[4];
+    int v[kPer], dg[kPer];
+    long long sum = 0;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const long long i = static_cast<long long>(threadIdx.x) * kPer + q;
+      v[q] = i < nf ? flist[i] : -1;
+    }
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      dg[q] = v[q] >= 0 ? out_len[v[q]] : 0;
+      sum += dg[q];
+    }
+    long long incl = sum;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const long long y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    const int wave = threadIdx.x / kWave;
+    if (lane == kWave - 1) wsum[wave] = incl;
+    __syncthreads();
+    long long pos = incl - sum, total = 0;
+    for (int w = 0; w < 4; ++w) {
+      if (w < wave) pos += wsum[w];
+      total += wsum[w];
+    }
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const long long i = static_cast<long long>(threadIdx.x) * kPer + q;
+      if (i < nf) {
+        dl.list[i] = v[q];
+        dl.doff[i] = pos;
+      }
+      pos += dg[q];
+    }
+    if (threadIdx.x == 0) {
+      const long long listed = nf < kDirectListMax ? nf : kDirectListMax;
+      dl.doff[listed] = total;
+      *dl.count = static_cast<u64>(listed);
+      *dl.out_total = static_cast<u64>(total);
+      if (nf > kDirectListMax) atomicOr(&c->err, 2ull);
+    }
+  }
   {
     // item w = 2 * arc + direction: its row's inserts follow the kept entries, in
     // rank order
@@ -89,7 +138,7 @@ __global__ void k_corr_mark(int agg, LayerPtrs lp, Adj out, Adj in, const int *i
   }
   const long long total = nf + (agg == kGcn ? na : 0);
   const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
-  for (long long i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+  for (long long i = blockIdx.x * blockDim.x + threadIdx.x + (dl.list != nullptr ? nf : 0); i < total; i += stride) {
     if (i < nf) {
       mark_only(bm, flist[i]);
     } else {
@@ -849,12 +898,12 @@ __global__ void k_gather_rows(const float *src, int d, const int *ids, long long
 void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerPtrs lp, Adj out, Adj in,
                       const int *ins_rank, const float *arc_w, const int *ddeg, const int *flist, const int *ins_src,
                       const int *ins_dst, const int *del_src, const int *del_dst, const float *ins_w,
-                      const float *del_w, unsigned *bm, Counters *c) {
+                      const float *del_w, unsigned *bm, Counters *c, const DirectList &direct) {
   const long long waves = 2LL * cap_arcs * lp.L;
   const long long threads = static_cast<long long>(cap_feat) + 2LL * cap_arcs;
   const long long items = waves * kWave > threads ? waves * kWave : threads;
   hipLaunchKernelGGL(k_corr_mark, dim3(blocks_for(items, 256)), dim3(256), 0, s, agg, lp, out, in, ins_rank, arc_w,
-                     ddeg, flist, ins_src, ins_dst, del_src, del_dst, ins_w, del_w, bm, c);
+                     ddeg, flist, ins_src, ins_dst, del_src, del_dst, ins_w, del_w, bm, c, direct);
 }
 
 int compact_blocks(long long n) {

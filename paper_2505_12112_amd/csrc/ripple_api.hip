@@ -677,6 +677,7 @@ struct BatchPlan {
   int mode[rp::kMaxL + 1];             // [l]: message form of layer l
   long long tf_rows[rp::kMaxL + 1];    // [l]: expected rows of layer l's transform-first GEMM
   long long rows[rp::kMaxL + 1];       // [l]: expected rows of layer l's GEMM
+  bool direct0;                        // the corrections kernel lists the layer-1 dirty set
   unsigned long long key;              // the above as GEMM variants, and the counter parity
 };
 
@@ -700,6 +701,11 @@ BatchPlan make_plan(const ripple_ctx *c) {
     key |= static_cast<unsigned long long>(rp::gemm_variant(p.rows[l])) << (bit + 3);
     bit += 4;
   }
+  // the layer-1 dirty set is the feature-written vertices alone unless GCN adds
+  // the sources whose out-degree changed; listed directly when layer 1 pushes (a
+  // pull needs the compaction's membership words) and the ops bound its size
+  p.direct0 = c->agg != rp::kGcn && p.mode[1] == kPushLayer && c->h_in->num_ops <= rp::kDirectListMax;
+  key |= static_cast<unsigned long long>(p.direct0) << 62;
   p.key = key;
   return p;
 }
@@ -746,22 +752,26 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
   {
     PhaseScope ps(c, RIPPLE_PHASE_LAYER0);
     // also writes the inserted arcs into their slots
+    rp::DirectList direct{};
+    if (p.direct0) direct = rp::DirectList{c->lists[0], c->doff[0], &dc->count[0], &dc->pushed[1]};
     rp::launch_corr_mark(s, cap_ops, cap_arcs, c->agg, layer_ptrs(c), out, in, c->ins_rank, c->ins_w, c->ddeg,
                          c->flist, c->ins_src, c->ins_dst, c->del_src, c->del_dst,
-                         c->agg == rp::kGcWsum ? c->ins_w : nullptr, c->del_w, c->bm_x, dc);
-    rp::CompactOut co{};
-    co.list = c->lists[0];
-    co.count = &dc->count[0];
-    co.out_deg = c->adj[0].len;
-    co.doff = c->doff[0];
-    co.out_total = &dc->pushed[1];
-    const bool members = p.mode[1] != kPushLayer;  // layer 1 pulls: it needs A^0's membership
-    co.memb = members ? c->memb[0] : nullptr;
-    rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
+                         c->agg == rp::kGcWsum ? c->ins_w : nullptr, c->del_w, c->bm_x, dc, direct);
+    if (!p.direct0) {
+      rp::CompactOut co{};
+      co.list = c->lists[0];
+      co.count = &dc->count[0];
+      co.out_deg = c->adj[0].len;
+      co.doff = c->doff[0];
+      co.out_total = &dc->pushed[1];
+      const bool members = p.mode[1] != kPushLayer;  // layer 1 pulls: it needs A^0's membership
+      co.memb = members ? c->memb[0] : nullptr;
+      rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
+    }
     const rp::Delta0Args z{c->agg, c->dims[0], rp::row_ld(c->dims[0]), c->d_ops, c->d_in, c->fop, c->H[0],
                            c->adj[0].len, c->ddeg, c->delta[0], dc};
     rp::launch_delta0(s, c->n, z, c->lists[0], &dc->count[0]);
-    add_launches(c, RIPPLE_PHASE_LAYER0, 3);
+    add_launches(c, RIPPLE_PHASE_LAYER0, p.direct0 ? 2 : 3);
   }
   for (int l = 1; l <= c->L; ++l) {
     float *din = c->delta[(l - 1) & 1];
