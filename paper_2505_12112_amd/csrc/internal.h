@@ -241,12 +241,32 @@ void launch_topo_fill(hipStream_t s, int cap_arcs, Adj out, Adj in, const LongRo
 // Then they are not marked: the kernel lists them itself, in flist's order, with
 // their out-degree prefix (the compaction's list, doff, count and out_total
 // outputs; a larger count sets check bit 2).
+// direct.delta != nullptr as well: it also writes their layer-0 deltas (x' - x at
+// list position j, row stride ld) and stages x' at row j of stage (stride ld);
+// X keeps x, which the corrections read, until the layer-1 scatter copies the
+// staged rows in (ScatterCopy).
 constexpr int kDirectListMax = 1024;
 struct DirectList {
   int *list;
   long long *doff;
   u64 *count;
   u64 *out_total;
+  float *delta;
+  float *stage;
+  int ld;
+  int d0;
+  const float *X;
+  const ripple_op *ops;
+  const BatchIn *in;
+  const int *fop;
+};
+// Rows the layer-1 scatter copies after the direct listing: X[list[j]] = stage[j]
+// for every listed j (dst == nullptr: none).
+struct ScatterCopy {
+  float *dst;
+  const float *stage;
+  int d;
+  int ld;
 };
 void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerPtrs lp, Adj out, Adj in,
                       const int *ins_rank, const float *arc_w, const int *ddeg, const int *flist, const int *ins_src,
@@ -315,7 +335,8 @@ void launch_delta0(hipStream_t s, long long n, const Delta0Args &z, const int *l
 // a self term).
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
-                    const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list);
+                    const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list,
+                    const ScatterCopy &copy = ScatterCopy{});
 
 // pull: for every vertex v of the sorted list A (in-arc prefix ioff; list null =
 // the identity), S[v] += sum of msg[rank(u)] over in-arcs (u -> v) whose source u

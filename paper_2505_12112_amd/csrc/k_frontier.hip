@@ -106,6 +106,24 @@ __global__ void k_corr_mark(int agg, LayerPtrs lp, Adj out, Adj in, const int *i
       if (nf > kDirectListMax) atomicOr(&c->err, 2ull);
     }
   }
+  if (dl.delta != nullptr) {
+    // layer-0 deltas of the listed vertices, one wave per row from the grid's last
+    // wave down (the corrections start at wave 0); x' is staged, X keeps x
+    const float *feat = dl.in->feat;
+    const long long nl = nf < kDirectListMax ? nf : kDirectListMax;
+    for (long long j = num_waves() - 1 - global_wave(); j < nl; j += num_waves()) {
+      const int u = flist[j];
+      const float *xu = dl.X + static_cast<long long>(u) * dl.d0;
+      const float *xn = feat + static_cast<long long>(dl.ops[dl.fop[u]].feat_row) * dl.d0;
+      float *dj = dl.delta + j * dl.ld;
+      float *sj = dl.stage + j * dl.ld;
+      for (int k = lane; k < dl.d0; k += kWave) {
+        const float x1 = xn[k];
+        dj[k] = x1 - xu[k];
+        sj[k] = x1;
+      }
+    }
+  }
   {
     // item w = 2 * arc + direction: its row's inserts follow the kept entries, in
     // rank order
@@ -572,7 +590,8 @@ template <int G, int NC, bool PUSH>
 __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list, const u64 *count, const long long *doff,
                                                  const float *delta, Adj out, float *S, unsigned *bm_out,
                                                  unsigned *bm_x, const int *ins_dst, const int *del_dst,
-                                                 const u64 *pushed, const Counters *c, int mark_list) {
+                                                 const u64 *pushed, const Counters *c, int mark_list,
+                                                 ScatterCopy copy) {
   const long long nD = static_cast<long long>(*count);
   const long long E = static_cast<long long>(*pushed);
   const long long ni = static_cast<long long>(c->n_ins);
@@ -585,6 +604,15 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
     for (long long i = t0; i < na; i += stride) mark_only(bm_x, i < ni ? ins_dst[i] : del_dst[i - ni]);
     if (mark_list)
       for (long long j = t0; j < nD; j += stride) mark_only(bm_x, list[j]);
+  }
+  if (copy.dst != nullptr) {
+    // the staged rows of the listed vertices, one wave each from the grid's last
+    // wave down (nothing in this kernel reads them)
+    for (long long j = num_waves() - 1 - global_wave(); j < nD; j += num_waves()) {
+      float *xu = copy.dst + static_cast<long long>(list[j]) * copy.d;
+      const float *sj = copy.stage + j * copy.ld;
+      for (int k = lane; k < copy.d; k += kWave) xu[k] = sj[k];
+    }
   }
   const long long waves = num_waves();
   int C = 1;
@@ -927,11 +955,12 @@ long long compact_scratch_words(long long n) { return 2LL * compact_blocks(n) * 
 
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
-                    const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list) {
+                    const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list,
+                    const ScatterCopy &copy) {
   const int blocks = 2048;
 #define RP_SCATTER(GV, NCV, P)                                                                                     \
   hipLaunchKernelGGL((k_scatter<GV, NCV, P>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, doff, delta, out, S, \
-                     bm_out, bm_x, ins_dst, del_dst, pushed, c, mark_list ? 1 : 0)
+                     bm_out, bm_x, ins_dst, del_dst, pushed, c, mark_list ? 1 : 0, copy)
   if (!push) RP_SCATTER(64, 1, false);
   else if (d <= 16) RP_SCATTER(16, 1, true);
   else if (d <= 32) RP_SCATTER(32, 1, true);

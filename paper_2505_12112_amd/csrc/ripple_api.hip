@@ -752,8 +752,19 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
   {
     PhaseScope ps(c, RIPPLE_PHASE_LAYER0);
     // also writes the inserted arcs into their slots
+    // listed directly, the layer-0 deltas come with the list unless layer 1
+    // transforms first (its GEMM reads the new rows of X before the scatter); x'
+    // is staged in delta[1], which layer 1's GEMM fills only after the scatter
     rp::DirectList direct{};
-    if (p.direct0) direct = rp::DirectList{c->lists[0], c->doff[0], &dc->count[0], &dc->pushed[1]};
+    if (p.direct0)
+      direct = rp::DirectList{c->lists[0], c->doff[0],  &dc->count[0],           &dc->pushed[1],
+                              nullptr,     nullptr,     rp::row_ld(c->dims[0]), c->dims[0],
+                              c->H[0],     c->d_ops,    c->d_in,                c->fop};
+    const bool direct_delta = p.direct0 && !c->tf[1];
+    if (direct_delta) {
+      direct.delta = c->delta[0];
+      direct.stage = c->delta[1];
+    }
     rp::launch_corr_mark(s, cap_ops, cap_arcs, c->agg, layer_ptrs(c), out, in, c->ins_rank, c->ins_w, c->ddeg,
                          c->flist, c->ins_src, c->ins_dst, c->del_src, c->del_dst,
                          c->agg == rp::kGcWsum ? c->ins_w : nullptr, c->del_w, c->bm_x, dc, direct);
@@ -768,10 +779,12 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
       co.memb = members ? c->memb[0] : nullptr;
       rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
     }
-    const rp::Delta0Args z{c->agg, c->dims[0], rp::row_ld(c->dims[0]), c->d_ops, c->d_in, c->fop, c->H[0],
-                           c->adj[0].len, c->ddeg, c->delta[0], dc};
-    rp::launch_delta0(s, c->n, z, c->lists[0], &dc->count[0]);
-    add_launches(c, RIPPLE_PHASE_LAYER0, p.direct0 ? 2 : 3);
+    if (!direct_delta) {
+      const rp::Delta0Args z{c->agg, c->dims[0], rp::row_ld(c->dims[0]), c->d_ops, c->d_in, c->fop, c->H[0],
+                             c->adj[0].len, c->ddeg, c->delta[0], dc};
+      rp::launch_delta0(s, c->n, z, c->lists[0], &dc->count[0]);
+    }
+    add_launches(c, RIPPLE_PHASE_LAYER0, 1 + (p.direct0 ? 0 : 1) + (direct_delta ? 0 : 1));
   }
   for (int l = 1; l <= c->L; ++l) {
     float *din = c->delta[(l - 1) & 1];
@@ -819,9 +832,13 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
     } else {
       // push: marks + atomic adds; pull: marks only (the adds follow the compaction)
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
+      // after a direct listing with its deltas, layer 1's scatter also moves the
+      // staged x' rows into X
+      rp::ScatterCopy copy{};
+      if (l == 1 && p.direct0 && !c->tf[1]) copy = rp::ScatterCopy{c->H[0], c->delta[1], c->dims[0], rp::row_ld(c->dims[0])};
       rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out_msg,
                          c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc,
-                         mode == kPushLayer, rp::has_self_term(c->agg));
+                         mode == kPushLayer, rp::has_self_term(c->agg), copy);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     {

@@ -309,8 +309,8 @@ def test_degenerate_and_extreme_shapes(case):
 def test_phase_stats_count_launches_and_bytes(mode):
     """Phase events: every phase of a profiled batch is timed, the launches are
     counted per phase (two netting, two topology, three layer-0 launches per
-    batch, two when layer 1 pushes: the corrections kernel then lists the
-    feature-written vertices itself; per layer one message launch when pushing,
+    batch, one when layer 1 pushes: the corrections kernel then lists the
+    feature-written vertices and their deltas itself; per layer one message launch when pushing,
     two when pulling; the dense form's full listing counts with the
     compactions), and the no-reuse byte bound
     of the message step is at least its algorithmic bytes."""
@@ -327,7 +327,7 @@ def test_phase_stats_count_launches_and_bytes(mode):
         ph = p.lib.phase_stats()
         L = len(dims) - 1
         assert ph["net"]["launches"] == 2 * nb and ph["topo"]["launches"] == 2 * nb
-        assert ph["layer0"]["launches"] == (2 if mode == "push" else 3) * nb
+        assert ph["layer0"]["launches"] == (1 if mode == "push" else 3) * nb
         assert ph["scatter"]["launches"] == (1 if mode == "push" else 2) * L * nb
         assert ph["compact"]["launches"] == (2 if mode == "dense" else 1) * L * nb
         assert ph["gemm"]["launches"] == L * nb and ph["total"]["launches"] == nb
