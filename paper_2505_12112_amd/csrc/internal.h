@@ -48,7 +48,11 @@ struct Counters {
   u64 zero;               // never written: an arc count of zero for kernels that only mark
   u64 long_rows;          // long rows swept in chunks: count << 40 | chunks handed out
   u64 long_pool;          // pool slots handed out to them
+  u64 app[kMaxL + 1];     // [l]: A^l listed by its scatter: count << 40 | sum of out-degrees
+  u64 app_sinks[kMaxL + 1];  // [l]: and its distinct sinks << 40 | sum of in-degrees
 };
+constexpr int kAppShift = 40;
+constexpr u64 kAppMask = (1ull << kAppShift) - 1;
 
 // Rows at least kLongRow entries long from which a batch deletes entries (and that
 // keep their slots) are swept by many waves, kLongChunk entries each: the sweeps
@@ -333,10 +337,29 @@ void launch_delta0(hipStream_t s, long long n, const Delta0Args &z, const int *l
 // by the compaction that built the list).
 // mark_list: also mark the listed (dirty) vertices themselves in bm_x (models with
 // a self term).
+// A^l listed by the push scatter itself (list != nullptr), for a layer whose list
+// needs no order and no membership words: the first wave to set a vertex's bit in
+// bm_x (every mark also goes there) appends it to list at a position taken with
+// one 64-bit atomic on *app (count << kAppShift | out-degree sum), which also gives
+// its doff entry (doff nullable: not wanted). Sinks are marked in bm_out as well;
+// *sinks receives the distinct sinks (first setters of a bit there) << kAppShift |
+// the members' in-degree sum. The bitmaps stay set; the next transform of the list
+// clears them (GemmArgs::clear_a / clear_b).
+struct ScatterList {
+  int *list;
+  long long *doff;
+  u64 *app;
+  u64 *sinks;
+  const int *out_len;
+  const int *in_len;
+};
+// packed_in: count points at a scatter-built list's packed counter (count and arc
+// total in one word; pushed is then not read).
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
                     const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list,
-                    const ScatterCopy &copy = ScatterCopy{});
+                    const ScatterCopy &copy = ScatterCopy{}, const ScatterList &lo = ScatterList{},
+                    bool packed_in = false);
 
 // pull: for every vertex v of the sorted list A (in-arc prefix ioff; list null =
 // the identity), S[v] += sum of msg[rank(u)] over in-arcs (u -> v) whose source u
@@ -397,6 +420,10 @@ struct GemmArgs {
   int cleanup_blocks;
   CleanupArgs cleanup;
   long long max_rows;  // rows (list entries) the launch may read; set by launch_gemm
+  int count_shift;     // the row count is *count >> count_shift (a scatter's packed list counter)
+  // clear_a / clear_b (nullable): bitmaps whose words holding a listed row are
+  // zeroed (a scatter-built list leaves its marks for the next transform to clear)
+  unsigned *clear_a, *clear_b;
 };
 // Blocks a batch's clean-up takes for cap_ops ops.
 int cleanup_blocks_for(long long cap_ops);

@@ -578,6 +578,74 @@ __global__ void k_delta0(Delta0Args z, const int *list, const u64 *count, long l
   }
 }
 
+// Arc e = e0 + lane (e <= elast) of the scatter's numbering, for a run whose first
+// and last arcs belong to list positions ja and jb: its sink (-1 past elast).
+__device__ inline int run_sink(const long long *doff, const int *list, const Adj &out, long long e0,
+                               long long elast, long long ja, long long jb) {
+  const int lane = lane_id();
+  const long long e = e0 + lane;
+  const bool active = e <= elast;
+  int j = static_cast<int>(ja);
+  if (jb > ja) {
+    if (jb - ja < kWave) {
+      const long long mine = ja + lane <= jb ? doff[ja + lane] : (1LL << 62);
+      int cnt_le = 0;
+      for (int t = 0; t <= static_cast<int>(jb - ja); ++t) cnt_le += __shfl(mine, t) <= e ? 1 : 0;
+      j = static_cast<int>(ja) + cnt_le - 1;
+    } else if (active) {
+      j = static_cast<int>(upper_bound(doff, ja, jb + 1, e) - 1);
+    }
+  }
+  if (!active) return -1;
+  const int u = list[j];
+  return out.col[out.off[u] + (e - doff[j])];
+}
+
+// One mark per lane (v < 0: none) by a scatter that lists A^l itself (see
+// ScatterList): the membership and sink bits are set with returning atomics, the
+// degrees are read beside them, and the lanes that set a membership bit first take
+// consecutive list positions and out-arc offsets with one atomic for the wave.
+__device__ inline void list_mark(int v, bool sink, const ScatterList &lo, unsigned *bm_out, unsigned *bm_x) {
+  const int lane = lane_id();
+  bool fresh = false, fresh_sink = false;
+  long long dv = 0, iv = 0;
+  if (v >= 0) {
+    const unsigned bit = 1u << (v & 31);
+    const unsigned om = atomicOr(&bm_x[v >> 5], bit);
+    const unsigned os = sink ? atomicOr(&bm_out[v >> 5], bit) : bit;
+    dv = lo.doff != nullptr ? lo.out_len[v] : 0;
+    iv = lo.in_len[v];
+    fresh = (om & bit) == 0;
+    fresh_sink = (os & bit) == 0;
+  }
+  const u64 ms = __ballot(fresh_sink);
+  const u64 m = __ballot(fresh);
+  if ((m | ms) == 0) return;
+  if (!fresh) dv = iv = 0;
+  long long dinc = dv, itot = iv;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const long long y = __shfl_up(dinc, o);
+    if (lane >= o) dinc += y;
+    itot += __shfl_xor(itot, o);
+  }
+  const long long dtot = __shfl(dinc, kWave - 1);
+  const int leader = __ffsll(static_cast<long long>(m | ms)) - 1;
+  u64 base = 0;
+  if (lane == leader) {
+    if (m != 0) base = atomicAdd(lo.app, static_cast<u64>(__popcll(m)) << kAppShift | static_cast<u64>(dtot));
+    atomicAdd(lo.sinks, static_cast<u64>(__popcll(ms)) << kAppShift | static_cast<u64>(itot));
+  }
+  base = __shfl(base, leader);
+  if (fresh) {
+    const int below = static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+        static_cast<unsigned>(m >> 32), __builtin_amdgcn_mbcnt_lo(static_cast<unsigned>(m), 0u)));
+    const long long pos = static_cast<long long>(base >> kAppShift) + below;
+    lo.list[pos] = v;
+    if (lo.doff != nullptr) lo.doff[pos] = static_cast<long long>(base & kAppMask) + dinc - dv;
+  }
+}
+
 // Edge-parallel scatter. Pushed arcs are numbered: arc e of listed vertex j has
 // index doff[j] + its position in j's out-row. A wave takes a chunk of C
 // consecutive arcs (C = 1 when there are few arcs, so that many waves run at
@@ -586,14 +654,15 @@ __global__ void k_delta0(Delta0Args z, const int *list, const u64 *count, long l
 // into the sink's row of S with fp32 atomics (coalesced across the G lanes). The
 // delta row stays in registers while consecutive arcs share a source, so a hub's
 // arcs cost one row load per chunk; hubs spread over many waves.
-template <int G, int NC, bool PUSH>
+template <int G, int NC, bool PUSH, bool LIST>
 __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list, const u64 *count, const long long *doff,
                                                  const float *delta, Adj out, float *S, unsigned *bm_out,
                                                  unsigned *bm_x, const int *ins_dst, const int *del_dst,
                                                  const u64 *pushed, const Counters *c, int mark_list,
-                                                 ScatterCopy copy) {
-  const long long nD = static_cast<long long>(*count);
-  const long long E = static_cast<long long>(*pushed);
+                                                 ScatterCopy copy, ScatterList lo, int packed_in) {
+  const u64 cw = *count;
+  const long long nD = static_cast<long long>(packed_in ? cw >> kAppShift : cw);
+  const long long E = static_cast<long long>(packed_in ? cw & kAppMask : *pushed);
   const long long ni = static_cast<long long>(c->n_ins);
   const long long na = ni + static_cast<long long>(c->n_del);
   if (aborted_with(c->abort, nD, E, na)) return;
@@ -601,9 +670,19 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
   {
     const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
     const long long t0 = blockIdx.x * blockDim.x + threadIdx.x;
-    for (long long i = t0; i < na; i += stride) mark_only(bm_x, i < ni ? ins_dst[i] : del_dst[i - ni]);
-    if (mark_list)
-      for (long long j = t0; j < nD; j += stride) mark_only(bm_x, list[j]);
+    if (!LIST) {
+      for (long long i = t0; i < na; i += stride) mark_only(bm_x, i < ni ? ins_dst[i] : del_dst[i - ni]);
+      if (mark_list)
+        for (long long j = t0; j < nD; j += stride) mark_only(bm_x, list[j]);
+    } else {
+      // the net arcs' heads, then D when it joins A^l: whole waves step together
+      const long long marks = na + (mark_list ? nD : 0);
+      for (long long b = t0 - lane; b < marks; b += stride) {
+        const long long i = b + lane;
+        const int v = i >= marks ? -1 : i < ni ? ins_dst[i] : i < na ? del_dst[i - ni] : list[i - na];
+        list_mark(v, false, lo, bm_out, bm_x);
+      }
+    }
   }
   if (copy.dst != nullptr) {
     // the staged rows of the listed vertices, one wave each from the grid's last
@@ -615,6 +694,22 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
     }
   }
   const long long waves = num_waves();
+  if (LIST) {
+    // A^l listed here: the sinks are marked 64 arcs per wave (one list append per
+    // wave), by waves from the grid's last one down (the adds below start at wave 0)
+    const long long groups = (E + kWave - 1) / kWave;
+    for (long long g = waves - 1 - global_wave(); g < groups; g += waves) {
+      const long long e0 = g * kWave;
+      const long long elast = e0 + kWave - 1 < E - 1 ? e0 + kWave - 1 : E - 1;
+      const long long ja = wave_last_le(doff, 0, nD, e0);
+      const long long jb = owner_from(doff, ja, nD, elast);
+      list_mark(run_sink(doff, list, out, e0, elast, ja, jb), true, lo, bm_out, bm_x);
+    }
+  }
+  // the owner searches run over doff[0, n1): a compacted list's doff[nD] holds the
+  // arc total; a scatter-built list has no such entry, and needs none, as every
+  // arc index is below the total
+  const long long n1 = packed_in ? nD : nD + 1;
   int C = 1;
   while (C < kWave && static_cast<long long>(C) * waves < E) C <<= 1;
   constexpr int kEdgesPerStep = kWave / G;
@@ -631,7 +726,7 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
   for (long long ch = c0; ch < c1; ++ch) {
     const long long e0 = ch * C;
     const long long elast = e0 + C - 1 < E - 1 ? e0 + C - 1 : E - 1;
-    ja = ja < 0 ? wave_last_le(doff, 0, nD + 1, e0) : owner_from(doff, ja, nD + 1, e0);
+    ja = ja < 0 ? wave_last_le(doff, 0, n1, e0) : owner_from(doff, ja, n1, e0);
     if (PUSH && ja != cached) {
       // the chunk's first source is known before its arcs are resolved: fetch its
       // delta row now so that the load overlaps the list / offset / column reads
@@ -643,7 +738,7 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
       }
       cached = static_cast<int>(ja);
     }
-    const long long jb = C == 1 ? ja : owner_from(doff, ja, nD + 1, elast);
+    const long long jb = C == 1 ? ja : owner_from(doff, ja, n1, elast);
     const long long e = e0 + lane;
     const bool active = e <= elast;
     int j = static_cast<int>(ja);
@@ -666,7 +761,7 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
       v = out.col[slot];
       if (PUSH && out.wt != nullptr) wv = out.wt[slot];
     }
-    if (v >= 0) mark_only(bm_out, v);
+    if (!LIST && v >= 0) mark_only(bm_out, v);
     const int cnt = PUSH ? static_cast<int>(elast - e0 + 1) : 0;
     for (int i = 0; i < cnt; i += kEdgesPerStep) {
       const int vv = __shfl(v, i + grp);
@@ -956,11 +1051,18 @@ long long compact_scratch_words(long long n) { return 2LL * compact_blocks(n) * 
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
                     const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list,
-                    const ScatterCopy &copy) {
+                    const ScatterCopy &copy, const ScatterList &lo, bool packed_in) {
   const int blocks = 2048;
-#define RP_SCATTER(GV, NCV, P)                                                                                     \
-  hipLaunchKernelGGL((k_scatter<GV, NCV, P>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, doff, delta, out, S, \
-                     bm_out, bm_x, ins_dst, del_dst, pushed, c, mark_list ? 1 : 0, copy)
+#define RP_SCATTER_L(GV, NCV, P, LV)                                                                               \
+  hipLaunchKernelGGL((k_scatter<GV, NCV, P, LV>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, doff, delta, out, \
+                     S, bm_out, bm_x, ins_dst, del_dst, pushed, c, mark_list ? 1 : 0, copy, lo, packed_in ? 1 : 0)
+#define RP_SCATTER(GV, NCV, P)                \
+  do {                                        \
+    if (P && lo.list != nullptr)              \
+      RP_SCATTER_L(GV, NCV, P, P);            \
+    else                                      \
+      RP_SCATTER_L(GV, NCV, P, false);        \
+  } while (0)
   if (!push) RP_SCATTER(64, 1, false);
   else if (d <= 16) RP_SCATTER(16, 1, true);
   else if (d <= 32) RP_SCATTER(32, 1, true);
@@ -970,6 +1072,7 @@ void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, 
   else if (d <= 512) RP_SCATTER(64, 8, true);
   else RP_SCATTER(64, 16, true);
 #undef RP_SCATTER
+#undef RP_SCATTER_L
 }
 
 void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count,

@@ -155,7 +155,7 @@ template <typename... T>
 __device__ inline bool abort_or_rows(const GemmArgs &a, long long &M, T... more) {
   if (a.abort != nullptr && a.count != nullptr) {
     const u64 ab = *a.abort;
-    M = static_cast<long long>(*a.count);
+    M = static_cast<long long>(*a.count >> a.count_shift);
     return aborted_with(ab, M, more...);
   }
   M = a.count_fixed;
@@ -261,6 +261,10 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
           tv = 1.0f;
           if (MODE == kGin1) sv = a.eps1;
         }
+      }
+      if (v >= 0 && n0 == 0 && a.clear_a != nullptr) {  // a scatter-built list's marks
+        a.clear_a[v >> 5] = 0u;
+        a.clear_b[v >> 5] = 0u;
       }
       rv[r] = v;
       rt[r] = tv;
@@ -450,6 +454,10 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
     }
     const long long ar = m0 + lr;
     const long long arow = MODE == kGin2 ? (ar < M ? ar : -1) : va;  // operand row (kGin2: list position)
+    if (va >= 0 && n0 == 0 && wave == 0 && lq == 0 && a.clear_a != nullptr) {  // a scatter-built list's marks
+      a.clear_a[va >> 5] = 0u;
+      a.clear_b[va >> 5] = 0u;
+    }
     // operand-row scales (layer mode): mean t = 1/deg_in; GCN t = (deg_in+1)^-1/2,
     // s = (deg_out+1)^-1/2
     float ta = 1.f, sa = 0.f;

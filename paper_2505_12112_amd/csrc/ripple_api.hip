@@ -118,6 +118,7 @@ struct ripple_ctx {
   long long last_in[rp::kMaxL + 1] = {};
   int last_pull = 0;   // layers that pulled over A^l's in-arcs (bit l)
   int last_dense = 0;  // layers that pulled over every in-arc (bit l)
+  int last_app = 0;    // layers whose A^l its scatter listed, unordered (bit l)
   float *delta[2] = {nullptr, nullptr};
   rp::Counters *d_counters = nullptr;  // two buffers; batch parity picks one
   int parity = 0;
@@ -569,9 +570,14 @@ rp::GemmArgs p_gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 
 // batch's clean-up, run by extra blocks of the last launch. Returns the launches.
 int launch_layer_gemm(const ripple_ctx *c, hipStream_t s, int l, const int *rows, const u64 *count,
                       long long count_fixed, float *delta, const u64 *abort, long long max_rows,
-                      long long expected_rows, const rp::CleanupArgs *cleanup = nullptr) {
+                      long long expected_rows, const rp::CleanupArgs *cleanup = nullptr, bool packed = false) {
   rp::GemmArgs g = gemm_args(c, l, rows, count, count_fixed, delta, abort);
+  if (packed) g.count_shift = rp::kAppShift;
   if (c->agg != rp::kGin) {
+    if (packed) {  // the scatter left the list's marks set
+      g.clear_a = c->bm_out;
+      g.clear_b = c->bm_x;
+    }
     if (cleanup != nullptr) {
       g.cleanup = *cleanup;
       g.cleanup_blocks = rp::cleanup_blocks_for(c->cap_ops);
@@ -584,6 +590,10 @@ int launch_layer_gemm(const ripple_ctx *c, hipStream_t s, int l, const int *rows
   g1.relu = 1;
   g1.H = c->gin_rows;
   g1.delta = nullptr;
+  if (packed) {  // the scatter left the list's marks set
+    g1.clear_a = c->bm_out;
+    g1.clear_b = c->bm_x;
+  }
   rp::launch_gemm(s, g1, max_rows, expected_rows);
   rp::GemmArgs g2 = g;  // y = W2 hidden + b2, then the layer's activation, delta and write-back
   g2.mode = rp::kGin2;
@@ -678,8 +688,14 @@ struct BatchPlan {
   long long tf_rows[rp::kMaxL + 1];    // [l]: expected rows of layer l's transform-first GEMM
   long long rows[rp::kMaxL + 1];       // [l]: expected rows of layer l's GEMM
   bool direct0;                        // the corrections kernel lists the layer-1 dirty set
+  int app;                             // bit l: layer l's scatter lists A^l (see ScatterList)
   unsigned long long key;              // the above as GEMM variants, and the counter parity
 };
+
+// Pushed arcs up to which a layer's scatter lists A^l itself, and that the next
+// layer may push from such a list.
+constexpr double kAppMaxArcs = 65536.0;
+constexpr double kAppMaxNextArcs = 1048576.0;
 
 BatchPlan make_plan(const ripple_ctx *c) {
   BatchPlan p{};
@@ -706,6 +722,20 @@ BatchPlan make_plan(const ripple_ctx *c) {
   // pull needs the compaction's membership words) and the ops bound its size
   p.direct0 = c->agg != rp::kGcn && p.mode[1] == kPushLayer && c->h_in->num_ops <= rp::kDirectListMax;
   key |= static_cast<unsigned long long>(p.direct0) << 62;
+  // a pushing layer lists A^l in its scatter unless the next layer pulls (a pull
+  // reads the sorted list's membership words), it is expected to push many arcs
+  // (the appends then queue on one counter and a compaction is cheaper), or the
+  // next layer pushes many arcs from the list (its row reads keep their locality
+  // in vertex order)
+  p.app = 0;
+  double arcs[rp::kMaxL + 2] = {};
+  for (int l = 1; l <= c->L; ++l)
+    arcs[l] = c->has_batch ? static_cast<double>(c->last_pushed[l]) : static_cast<double>(guess[l - 1]) * deg;
+  for (int l = 1; l <= c->L; ++l) {
+    const bool next_ok = l == c->L || (p.mode[l + 1] == kPushLayer && arcs[l + 1] <= kAppMaxNextArcs);
+    if (p.mode[l] == kPushLayer && arcs[l] <= kAppMaxArcs && next_ok) p.app |= 1 << l;
+  }
+  key |= static_cast<unsigned long long>(p.app) << 40;
   p.key = key;
   return p;
 }
@@ -792,12 +822,17 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
     // (its messages then come from its own P rows)
     float *dout = l < c->L && !c->tf[l + 1] ? c->delta[l & 1] : nullptr;
     const float *msg = din;
+    // A^{l-1} listed by its scatter: its count and arc total are one packed word
+    const bool packed_in = p.app >> (l - 1) & 1;
+    const u64 *count_in = packed_in ? &dc->app[l - 1] : &dc->count[l - 1];
+    const bool app = p.app >> l & 1;
     if (c->tf[l]) {
       // transform-first layer: refresh P = W_neigh h for the dirty rows and form
       // their messages c' P' - c P
       PhaseScope ps(c, RIPPLE_PHASE_GEMM);
-      rp::launch_gemm(s, p_gemm_args(c, l, c->lists[l - 1], &dc->count[l - 1], 0, c->msg, &dc->abort), c->n,
-                      p.tf_rows[l]);
+      rp::GemmArgs pg = p_gemm_args(c, l, c->lists[l - 1], count_in, 0, c->msg, &dc->abort);
+      if (packed_in) pg.count_shift = rp::kAppShift;
+      rp::launch_gemm(s, pg, c->n, p.tf_rows[l]);
       add_launches(c, RIPPLE_PHASE_GEMM, 1);
       msg = c->msg;
     }
@@ -836,12 +871,16 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
       // staged x' rows into X
       rp::ScatterCopy copy{};
       if (l == 1 && p.direct0 && !c->tf[1]) copy = rp::ScatterCopy{c->H[0], c->delta[1], c->dims[0], rp::row_ld(c->dims[0])};
-      rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], msg, out_msg,
-                         c->S[l], c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc,
-                         mode == kPushLayer, rp::has_self_term(c->agg), copy);
+      rp::ScatterList lo{};
+      if (app)
+        lo = rp::ScatterList{c->lists[l],       l < c->L ? c->doff[l] : nullptr, &dc->app[l], &dc->app_sinks[l],
+                             c->adj[0].len, c->adj[1].len};
+      rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], count_in, c->doff[l - 1], msg, out_msg, c->S[l],
+                         c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc, mode == kPushLayer,
+                         rp::has_self_term(c->agg), copy, lo, packed_in);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
-    {
+    if (!app) {
       PhaseScope ps(c, RIPPLE_PHASE_COMPACT);
       rp::CompactOut co{};
       co.list = c->lists[l];
@@ -868,8 +907,8 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
       // the last layer's GEMM also resets the batch's scratch (extra blocks)
       PhaseScope ps(c, RIPPLE_PHASE_GEMM);
       add_launches(c, RIPPLE_PHASE_GEMM,
-                   launch_layer_gemm(c, s, l, c->lists[l], &dc->count[l], 0, dout, &dc->abort, c->n, p.rows[l],
-                                     l == c->L ? &cleanup : nullptr));
+                   launch_layer_gemm(c, s, l, c->lists[l], app ? &dc->app[l] : &dc->count[l], 0, dout, &dc->abort,
+                                     c->n, p.rows[l], l == c->L ? &cleanup : nullptr, app));
     }
   }
   total.close();
@@ -921,6 +960,7 @@ ripple_status launch_batch(ripple_ctx *c) {
     if (p.mode[l] == kPullLayer) c->last_pull |= 1 << l;
     if (p.mode[l] == kDenseLayer) c->last_dense |= 1 << l;
   }
+  c->last_app = p.app;
   c->last_graph = false;
   hipGraphExec_t g = c->use_graphs && !c->graphs_failed && !c->prof ? plan_graph(c, p) : nullptr;
   if (g != nullptr) {
@@ -975,7 +1015,10 @@ void account_phases(ripple_ctx *c) {
       c->ph_bytes[RIPPLE_PHASE_GEMM] += 8.0 * m * N + 4.0 * N * N;
     }
     c->ph_bytes[RIPPLE_PHASE_GEMM] += 4.0 * m * K + 4.0 * N * K + 4.0 * m * N * (l < c->L && !c->tf[l + 1] ? 3.0 : 2.0);
-    c->ph_bytes[RIPPLE_PHASE_COMPACT] += 24.0 * words + 4.0 * m;
+    if (c->last_app >> l & 1)  // listed by the scatter: each member's id, offset and degrees
+      c->ph_bytes[RIPPLE_PHASE_SCATTER] += 20.0 * m;
+    else
+      c->ph_bytes[RIPPLE_PHASE_COMPACT] += 24.0 * words + 4.0 * m;
   }
   c->ev_log.clear();
   c->ev_used = 0;
@@ -1421,7 +1464,15 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
     RP_TRY(repack_adj(c, 1));
     ++repacks;
   }
-  const rp::Counters &k = *c->h_counters;
+  rp::Counters &k = *c->h_counters;
+  // lists built by a scatter keep their count and out-arc total in one word
+  for (int l = 1; l <= c->L; ++l) {
+    if (!(c->last_app >> l & 1)) continue;
+    k.count[l] = k.app[l] >> rp::kAppShift;
+    if (l < c->L) k.pushed[l + 1] = k.app[l] & rp::kAppMask;
+    k.dest[l] = k.app_sinks[l] >> rp::kAppShift;
+    k.indeg[l] = k.app_sinks[l] & rp::kAppMask;
+  }
   if (k.err) {
     c->poisoned = true;
     // bit 0: a net-deleted arc was not found; bit 1: a rewritten row's length did not
@@ -1568,6 +1619,17 @@ ripple_status ripple_get_affected(ripple_ctx *c, int32_t layer, int32_t *ids, in
   const long long cnt = c->last_count[layer];
   *count = cnt;
   const long long w = std::min<long long>(cnt, capacity);
+  if (c->last_app >> layer & 1) {
+    // listed by its scatter in no particular order: sort the whole list
+    std::vector<int> all(cnt);
+    if (cnt > 0) {
+      RP_HIP(c, hipMemcpyAsync(all.data(), c->lists[layer], cnt * sizeof(int), hipMemcpyDeviceToHost, c->stream));
+      RP_HIP(c, hipStreamSynchronize(c->stream));
+    }
+    std::sort(all.begin(), all.end());
+    if (w > 0) std::memcpy(ids, all.data(), w * sizeof(int));
+    return RIPPLE_OK;
+  }
   if (w > 0) {
     RP_HIP(c, hipMemcpyAsync(ids, c->lists[layer], w * sizeof(int), hipMemcpyDeviceToHost, c->stream));
     RP_HIP(c, hipStreamSynchronize(c->stream));

@@ -311,7 +311,8 @@ def test_phase_stats_count_launches_and_bytes(mode):
     counted per phase (two netting, two topology, three layer-0 launches per
     batch, one when layer 1 pushes: the corrections kernel then lists the
     feature-written vertices and their deltas itself; per layer one message launch when pushing,
-    two when pulling; the dense form's full listing counts with the
+    two when pulling; a pushing layer's scatter lists A^l itself, a pulling one
+    compacts it, and the dense form's full listing counts with the
     compactions), and the no-reuse byte bound
     of the message step is at least its algorithmic bytes."""
     rng = np.random.default_rng(51)
@@ -329,9 +330,12 @@ def test_phase_stats_count_launches_and_bytes(mode):
         assert ph["net"]["launches"] == 2 * nb and ph["topo"]["launches"] == 2 * nb
         assert ph["layer0"]["launches"] == (1 if mode == "push" else 3) * nb
         assert ph["scatter"]["launches"] == (1 if mode == "push" else 2) * L * nb
-        assert ph["compact"]["launches"] == (2 if mode == "dense" else 1) * L * nb
+        assert ph["compact"]["launches"] == {"push": 0, "pull": 1, "dense": 2}[mode] * L * nb
         assert ph["gemm"]["launches"] == L * nb and ph["total"]["launches"] == nb
         for name in ("net", "topo", "layer0", "scatter", "compact", "gemm", "total"):
+            if name == "compact" and mode == "push":
+                assert ph[name]["ms"] == 0
+                continue
             assert ph[name]["ms"] > 0, name
         assert ph["scatter"]["bytes"] > 0 and ph["scatter"]["bytes_no_reuse"] >= ph["scatter"]["bytes"]
         assert ph["gemm"]["flops"] > 0
