@@ -435,8 +435,13 @@ ripple_status ensure_batch_scratch(ripple_ctx *c, long long ops, long long frows
   RP_HIP(c, hipStreamSynchronize(c->stream));
   free_batch_scratch(c);
   const long long arcs = 2 * cap;           // net arcs (undirected edges give two)
-  unsigned ht = 64;  // at most an eighth full: probe chains stay short
-  while (ht < 8 * static_cast<unsigned long long>(cap)) ht <<= 1;
+  // at most 1/64 full up to 4M slots (64 MB), else at most an eighth: the topology
+  // pass probes every entry of a row that loses arcs, and a probe that meets an
+  // occupied slot costs another dependent round
+  const unsigned long long sparse = 64 * static_cast<unsigned long long>(cap);
+  const unsigned long long want = sparse <= (1ull << 22) ? sparse : 8 * static_cast<unsigned long long>(cap);
+  unsigned ht = 64;
+  while (ht < want) ht <<= 1;
   RP_TRY(dalloc_n(c, &c->d_ops, cap));
   RP_TRY(dalloc_n(c, &c->ht_key, ht));
   RP_TRY(dalloc_n(c, &c->ht_val, ht));
