@@ -36,7 +36,7 @@ struct Counters {
   u64 n_reloc;            // rows to move to the arena
   u64 arena_need[2];      // arena slots those moves need, per direction
   u64 err;                // device-side check failed: bit 0 deleted arc not found, bit 1 row length
-                          // mismatch, bit 2 compaction wait timed out
+                          // mismatch, bit 2 compaction wait timed out, bit 3 row move past the buffer
   u64 plan_done;          // blocks of the plan kernel that finished (last one checks the arena)
   u64 count[kMaxL + 1];   // [0] = |dirty set of layer 1|, [l] = |A^l|
   u64 pushed[kMaxL + 1];  // [l] = out-arcs pushed at layer l
@@ -50,6 +50,8 @@ struct Counters {
   u64 long_pool;          // pool slots handed out to them
   u64 app[kMaxL + 1];     // [l]: A^l listed by its scatter: count << 40 | sum of out-degrees
   u64 app_sinks[kMaxL + 1];  // [l]: and its distinct sinks << 40 | sum of in-degrees
+  u64 maxlen[2];          // per direction: the largest new row length above RewriteBounds::maxlen, else 0
+  u64 top_end[2];         // per direction: the arena top after this batch's row moves (0: none moved)
 };
 constexpr int kAppShift = 40;
 constexpr u64 kAppMask = (1ull << kAppShift) - 1;
@@ -224,10 +226,19 @@ void launch_net_decide(hipStream_t s, int cap_ops, const BatchIn *in, const ripp
 void launch_topo_plan(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
                       const int *del_src, const int *del_dst, const int *ins_rank, const int *del_rank,
                       int long_ok, LongRow *tab, Counters *c, const Persist *p, long long cap_out, long long cap_in);
+// The host's view of the adjacency for the rewrite: per direction, a bound on every
+// row's length (rows that grow past it report their new length in Counters::maxlen)
+// and the column buffer's size (a row move that would end past it sets check bit 3
+// and writes nothing).
+struct RewriteBounds {
+  long long maxlen[2];
+  long long capacity[2];
+};
 void launch_topo_rewrite(hipStream_t s, int cap_arcs, int undirected, long long n, Adj out, Adj in,
                          const int *ins_src, const int *ins_dst, const int *del_src, const int *del_dst,
                          const int *ins_rank, const int *del_rank, const u64 *ht_key, const int *ht_net,
-                         unsigned mask, Persist *p, int *ddeg, int long_ok, LongRow *tab, int *pool, Counters *c);
+                         unsigned mask, Persist *p, int *ddeg, int long_ok, LongRow *tab, int *pool, Counters *c,
+                         const RewriteBounds &rb);
 void launch_topo_fill(hipStream_t s, int cap_arcs, Adj out, Adj in, const LongRow *tab, const int *pool,
                       Counters *c);
 

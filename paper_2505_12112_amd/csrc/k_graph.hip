@@ -239,7 +239,6 @@ __global__ void k_topo_plan(Adj out, Adj in, const int *ins_src, const int *ins_
     if (!ins_item && nins != 0) continue;
     const int need = len0 - k + nins;
     if (need > cap) {
-      atomicAdd(&c->n_reloc, 1ull);
       atomicAdd(&c->arena_need[dir], static_cast<u64>(grow_cap(need)));
     } else if (long_ok && k > 0 && len0 >= kLongRow) {
       // a long row that keeps its slots: list it for the chunked sweep
@@ -363,7 +362,8 @@ __device__ inline void append_positions(bool flag, int e, int *list, int *count,
 __global__ __launch_bounds__(256) void k_topo_rewrite(int undirected, long long n, Adj out, Adj in, const int *ins_src,
                                const int *ins_dst, const int *del_src, const int *del_dst, const int *ins_rank,
                                const int *del_rank, const u64 *ht_key, const int *ht_net, unsigned mask,
-                               Persist *p, int *ddeg, int long_ok, LongRow *tab, int *pool, Counters *c) {
+                               Persist *p, int *ddeg, int long_ok, LongRow *tab, int *pool, Counters *c,
+                               RewriteBounds rb) {
   const long long ni = 2 * static_cast<long long>(c->n_ins);
   const long long nd = 2 * static_cast<long long>(c->n_del);
   const u64 lr = c->long_rows;
@@ -429,7 +429,12 @@ __global__ __launch_bounds__(256) void k_topo_rewrite(int undirected, long long 
     // row is read (its value is needed only for the writes)
     long long moved_to = 0;
     if (move && lane == 0) moved_to = static_cast<long long>(atomicAdd(&p->top[dir], static_cast<u64>(nc)));
+    if (lane == 0 && need > rb.maxlen[dir]) atomicMax(&c->maxlen[dir], static_cast<u64>(need));
     long long dst_off = src_off;
+    // a move past the arena's end (possible only if the plan did not run and the
+    // host's bound was wrong) writes nothing and fails the batch
+    const long long arena_end = rb.capacity[dir];
+    bool overflow = false;
     if (!swept && (k > 0 || move)) {
       const int *src = a.col + src_off;
       const float *srcw = a.wt != nullptr ? a.wt + src_off : nullptr;  // weights move with their slots
@@ -450,26 +455,38 @@ __global__ __launch_bounds__(256) void k_topo_rewrite(int undirected, long long 
           xw[u] = keep[u] && srcw != nullptr ? srcw[e] : 0.0f;
         }
         if (k > 0) drop_deleted(x, keep, row, dir, undirected, n, ht_key, ht_net, mask);
-        if (base == 0 && move) dst_off = __shfl(moved_to, 0);
+        if (base == 0 && move) {
+          dst_off = __shfl(moved_to, 0);
+          overflow = dst_off + nc > arena_end;
+        }
         int *dst = a.col + dst_off;
         float *dstw = a.wt != nullptr ? a.wt + dst_off : nullptr;
 #pragma unroll
         for (int u = 0; u < kRewriteU; ++u) {
           const u64 m = __ballot(keep[u]);
-          if (keep[u]) {
+          if (keep[u] && !overflow) {
             dst[wpos + lanes_below(m)] = x[u];
             if (dstw != nullptr) dstw[wpos + lanes_below(m)] = xw[u];
           }
           wpos += __popcll(m);
         }
       }
-      if (move && len0 == 0) dst_off = __shfl(moved_to, 0);  // no step ran
+      if (move && len0 == 0) {  // no step ran
+        dst_off = __shfl(moved_to, 0);
+        overflow = dst_off + nc > arena_end;
+      }
       if (lane == 0 && wpos != len0 - k) atomicOr(&c->err, 2ull);
+    }
+    if (overflow) {
+      if (lane == 0) atomicOr(&c->err, 8ull);
+      continue;
     }
     if (lane == 0) {
       if (move) {
         a.off[row] = dst_off;
         a.cap[row] = nc;
+        atomicAdd(&c->n_reloc, 1ull);
+        atomicMax(&c->top_end[dir], static_cast<u64>(dst_off + nc));
       }
       a.len[row] = need;
       if (dir == 0) ddeg[row] = nins - k;
@@ -550,10 +567,11 @@ void launch_topo_plan(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *i
 void launch_topo_rewrite(hipStream_t s, int cap_arcs, int undirected, long long n, Adj out, Adj in,
                          const int *ins_src, const int *ins_dst, const int *del_src, const int *del_dst,
                          const int *ins_rank, const int *del_rank, const u64 *ht_key, const int *ht_net,
-                         unsigned mask, Persist *p, int *ddeg, int long_ok, LongRow *tab, int *pool, Counters *c) {
+                         unsigned mask, Persist *p, int *ddeg, int long_ok, LongRow *tab, int *pool, Counters *c,
+                         const RewriteBounds &rb) {
   hipLaunchKernelGGL(k_topo_rewrite, dim3(blocks_for(4LL * cap_arcs * kWave, 256)), dim3(256), 0, s, undirected,
                      n, out, in, ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank, ht_key, ht_net, mask, p,
-                     ddeg, long_ok, tab, pool, c);
+                     ddeg, long_ok, tab, pool, c, rb);
 }
 
 void launch_topo_fill(hipStream_t s, int cap_arcs, Adj out, Adj in, const LongRow *tab, const int *pool,

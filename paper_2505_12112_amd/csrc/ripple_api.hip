@@ -74,6 +74,8 @@ struct ripple_ctx {
   // adjacency: [0] out (CSR by source), [1] in (CSC by sink)
   rp::Adj adj[2] = {};
   long long col_capacity[2] = {0, 0};
+  long long row_max[2] = {0, 0};     // per direction: no row is longer
+  long long arena_top[2] = {0, 0};   // per direction: first free arena slot (as of the last batch)
   int *col_alt[2] = {nullptr, nullptr};   // spare column buffer per direction (same capacity)
   float *wt_alt[2] = {nullptr, nullptr};  // weighted graphs: the spare buffer of the slots' weights
   bool weighted = false;                  // the arcs carry weights
@@ -325,6 +327,8 @@ ripple_status upload_adj(ripple_ctx *c, int dir, const std::vector<int> &len, co
   RP_HIP(c, hipMemcpyAsync(&c->d_persist->top[dir], &top, sizeof(u64), hipMemcpyHostToDevice, c->stream));
   RP_HIP(c, hipStreamSynchronize(c->stream));
   c->col_capacity[dir] = capacity;
+  c->arena_top[dir] = total;
+  c->row_max[dir] = len.empty() ? 0 : *std::max_element(len.begin(), len.end());
   return RIPPLE_OK;
 }
 
@@ -376,6 +380,7 @@ ripple_status repack_adj_grow(ripple_ctx *c, int dir) {
   RP_HIP(c, hipMemcpyAsync(&c->d_persist->top[dir], &top, sizeof(u64), hipMemcpyHostToDevice, c->stream));
   RP_HIP(c, hipStreamSynchronize(c->stream));
   c->col_capacity[dir] = capacity;
+  c->arena_top[dir] = total;
   return RIPPLE_OK;
 }
 
@@ -398,6 +403,7 @@ ripple_status repack_adj(ripple_ctx *c, int dir) {
   drop_graphs(c);  // the launches name the row table's buffers
   std::swap(a.col, c->col_alt[dir]);
   if (c->weighted) std::swap(a.wt, c->wt_alt[dir]);
+  c->arena_top[dir] = total;  // the new layout's rows end there
   return RIPPLE_OK;
 }
 
@@ -694,6 +700,7 @@ struct BatchPlan {
   long long rows[rp::kMaxL + 1];       // [l]: expected rows of layer l's GEMM
   bool direct0;                        // the corrections kernel lists the layer-1 dirty set
   int app;                             // bit l: layer l's scatter lists A^l (see ScatterList)
+  bool arena_plan;                     // the arena check runs (else every possible row move fits)
   unsigned long long key;              // the above as GEMM variants, and the counter parity
 };
 
@@ -741,6 +748,25 @@ BatchPlan make_plan(const ripple_ctx *c) {
     if (p.mode[l] == kPushLayer && arcs[l] <= kAppMaxArcs && next_ok) p.app |= 1 << l;
   }
   key |= static_cast<unsigned long long>(p.app) << 40;
+  // The plan launch sums the arena slots that growing rows need and aborts the
+  // batch if they do not fit. Only rows that gain arcs move: at most (2 for
+  // undirected graphs) x ops rows per direction, each to grow_cap of at most its
+  // length bound + as many arcs. When that fits in every direction's free arena the
+  // check cannot fail and is left out (the rewrite still refuses a move past the
+  // buffer). Rows swept in chunks are listed by the plan, so it always runs then.
+  p.arena_plan = true;
+  if (!c->long_ok) {
+    const long long grow = (c->undirected ? 2LL : 1LL) * c->h_in->num_ops;
+    bool fits = true;
+    for (int d = 0; d < 2; ++d) {
+      const long long newlen = c->row_max[d] + grow;
+      const long long g = newlen + newlen / 2 + 4;  // the rewrite's grow_cap
+      const long long worst = grow * ((g + 3) / 4 * 4);
+      fits = fits && worst <= c->col_capacity[d] - c->arena_top[d];
+    }
+    p.arena_plan = !fits;
+  }
+  key |= static_cast<unsigned long long>(p.arena_plan) << 61;
   p.key = key;
   return p;
 }
@@ -775,14 +801,16 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
   }
   {
     PhaseScope ps(c, RIPPLE_PHASE_TOPO);
-    rp::launch_topo_plan(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank,
-                         c->del_rank, c->long_ok, c->long_tab, dc, c->d_persist, c->col_capacity[0],
-                         c->col_capacity[1]);
+    if (p.arena_plan)
+      rp::launch_topo_plan(s, cap_arcs, out, in, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank,
+                           c->del_rank, c->long_ok, c->long_tab, dc, c->d_persist, c->col_capacity[0],
+                           c->col_capacity[1]);
+    const rp::RewriteBounds rb{{c->row_max[0], c->row_max[1]}, {c->col_capacity[0], c->col_capacity[1]}};
     rp::launch_topo_rewrite(s, cap_arcs, c->undirected, c->n, out, in, c->ins_src, c->ins_dst, c->del_src,
                             c->del_dst, c->ins_rank, c->del_rank, c->ht_key, c->ht_net, c->ht_mask, c->d_persist,
-                            c->ddeg, c->long_ok, c->long_tab, c->long_pool, dc);
+                            c->ddeg, c->long_ok, c->long_tab, c->long_pool, dc, rb);
     if (c->long_ok) rp::launch_topo_fill(s, cap_arcs, out, in, c->long_tab, c->long_pool, dc);
-    add_launches(c, RIPPLE_PHASE_TOPO, c->long_ok ? 3 : 2);
+    add_launches(c, RIPPLE_PHASE_TOPO, (p.arena_plan ? 1 : 0) + 1 + (c->long_ok ? 1 : 0));
   }
   {
     PhaseScope ps(c, RIPPLE_PHASE_LAYER0);
@@ -1481,10 +1509,15 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
   if (k.err) {
     c->poisoned = true;
     // bit 0: a net-deleted arc was not found; bit 1: a rewritten row's length did not
-    // match; bit 2: the compaction's wait for a predecessor tile timed out
+    // match; bit 2: the compaction's wait for a predecessor tile timed out; bit 3: a
+    // row move would have ended past the column buffer
     return fail(c, RIPPLE_E_DEVICE, "ripple: device-side check failed (err bits " + std::to_string(k.err) + ")");
   }
   c->arcs_now += static_cast<long long>(k.n_ins) - static_cast<long long>(k.n_del);
+  for (int d = 0; d < 2; ++d) {
+    c->row_max[d] = std::max(c->row_max[d], static_cast<long long>(k.maxlen[d]));
+    if (k.top_end[d] != 0) c->arena_top[d] = static_cast<long long>(k.top_end[d]);
+  }
   account_phases(c);
   c->has_batch = true;
   c->last_nfeat = static_cast<long long>(k.n_feat);

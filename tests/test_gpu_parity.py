@@ -308,7 +308,8 @@ def test_degenerate_and_extreme_shapes(case):
 @pytest.mark.parametrize("mode", ["push", "pull", "dense"])
 def test_phase_stats_count_launches_and_bytes(mode):
     """Phase events: every phase of a profiled batch is timed, the launches are
-    counted per phase (two netting, two topology, three layer-0 launches per
+    counted per phase (two netting, one topology (the arena check only when the
+    spare arena might not hold the batch's row moves), three layer-0 launches per
     batch, one when layer 1 pushes: the corrections kernel then lists the
     feature-written vertices and their deltas itself; per layer one message launch when pushing,
     two when pulling; a pushing layer's scatter lists A^l itself, a pulling one
@@ -327,7 +328,9 @@ def test_phase_stats_count_launches_and_bytes(mode):
             p.step(random_valid_batch(rng, p.orc, 30, dims[0]))
         ph = p.lib.phase_stats()
         L = len(dims) - 1
-        assert ph["net"]["launches"] == 2 * nb and ph["topo"]["launches"] == 2 * nb
+        # (the arena check is left out: this graph's spare arena holds any row move
+        # a 30-op batch can cause)
+        assert ph["net"]["launches"] == 2 * nb and ph["topo"]["launches"] == nb
         assert ph["layer0"]["launches"] == (1 if mode == "push" else 3) * nb
         assert ph["scatter"]["launches"] == (1 if mode == "push" else 2) * L * nb
         assert ph["compact"]["launches"] == {"push": 0, "pull": 1, "dense": 2}[mode] * L * nb
