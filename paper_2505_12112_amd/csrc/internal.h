@@ -211,6 +211,15 @@ void launch_net_hash(hipStream_t s, int cap_ops, const BatchIn *host_in, const B
                      ripple_op *ops,
                      int undirected, int weighted, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot,
                      int *fop, Counters *c);
+// Both netting steps in one launch, for a batch of at most kNetDirectMax ops: the
+// same outputs, except that only net-deleted edge keys enter the hash table (tagged
+// -1, their slots in op_slot; every other op's op_slot is -1) and ht_val is unused.
+constexpr int kNetDirectMax = 512;
+void launch_net_direct(hipStream_t s, int cap_ops, const BatchIn *host_in, const BatchIn &now, BatchIn *dev_in,
+                       ripple_op *ops, int undirected, int weighted, long long n, u64 *ht_key, int *ht_net,
+                       unsigned mask, int *op_slot, int *fop, Adj out, Adj in_adj, int *ins_src, int *ins_dst,
+                       int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w, float *del_w,
+                       int *flist, Counters *c);
 void launch_net_decide(hipStream_t s, int cap_ops, const BatchIn *in, const ripple_op *ops, int undirected,
                        const int *ht_val, int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in_adj,
                        int *ins_src, int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank,

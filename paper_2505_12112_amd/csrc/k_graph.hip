@@ -149,6 +149,55 @@ __global__ void k_net_hash(const BatchIn *host_in, BatchIn now, BatchIn *dev_in,
   op_slot[i] = static_cast<int>(s);
 }
 
+// The decision of edge (a, b)'s deciding op (a <= b on undirected graphs; a's
+// out-row and b's in-row have lengths la, lb and offsets oa, ob): is the edge present
+// before the batch (searched in the shorter row), and then either a no-op or the net
+// arcs with their ranks among their rows' inserts or deletes. Returns the edge's net
+// change on every lane: +1 inserted, -1 deleted or reweighted, 0 none.
+__device__ inline int emit_edge(const ripple_op &op, int a, int b, int la, int lb, long long oa, long long ob,
+                                int undirected, Adj out, Adj in, int *ins_src, int *ins_dst, int *del_src,
+                                int *del_dst, int *ins_rank, int *del_rank, float *ins_w, float *del_w, Counters *c) {
+  const int lane = lane_id();
+  const bool use_out = la <= lb;
+  const long long row0 = use_out ? oa : ob;
+  const int pos = wave_find((use_out ? out.col : in.col) + row0, use_out ? la : lb, use_out ? b : a);
+  const bool present = pos >= 0;
+  const bool want = op.kind == RIPPLE_OP_INSERT;
+  const bool weighted = out.wt != nullptr;
+  const float w_old = weighted && present ? (use_out ? out.wt : in.wt)[row0 + pos] : 1.0f;
+  const float w_new = weighted ? op.weight : 1.0f;
+  const bool reweight = want && present && w_old != w_new;
+  const bool noop = want == present && !reweight;
+  if (lane == 0) {
+    atomicAdd(&c->edge_keys, 1ull);
+    if (noop) {
+      atomicAdd(&c->noop_edge, 1ull);
+    } else {
+      // a reweight drops the old entry (as a delete) and puts the arc back with its
+      // new weight (as an insert)
+      const int narcs = undirected ? 2 : 1;
+      if (reweight) atomicAdd(&c->n_rew, static_cast<u64>(narcs));
+      for (int kind = 0; kind < 2; ++kind) {  // 0: delete item, 1: insert item
+        if (kind == 0 ? !present : !want) continue;
+        const bool ins = kind == 1;
+        int *ps = ins ? ins_src : del_src;
+        int *pd = ins ? ins_dst : del_dst;
+        int *rank = ins ? ins_rank : del_rank;
+        const u64 j = atomicAdd(ins ? &c->n_ins : &c->n_del, static_cast<u64>(narcs));
+        for (int t = 0; t < narcs; ++t) {
+          const int su = t == 0 ? a : b, sv = t == 0 ? b : a;
+          ps[j + t] = su;
+          pd[j + t] = sv;
+          (ins ? ins_w : del_w)[j + t] = ins ? w_new : w_old;
+          rank[2 * (j + t)] = atomicAdd(ins ? &out.inscnt[su] : &out.delcnt[su], 1);
+          rank[2 * (j + t) + 1] = atomicAdd(ins ? &in.inscnt[sv] : &in.delcnt[sv], 1);
+        }
+      }
+    }
+  }
+  return noop ? 0 : want && !reweight ? 1 : -1;
+}
+
 __global__ void k_net_decide(const BatchIn *bin, const ripple_op *ops, int undirected, const int *ht_val,
                              int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src,
                              int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w,
@@ -180,44 +229,124 @@ __global__ void k_net_decide(const BatchIn *bin, const ripple_op *ops, int undir
     if (static_cast<int>(s < 0 || winner != i) |
         (la | lb | static_cast<int>(oa >> 32) | static_cast<int>(ob >> 32)) >> 31)
       continue;  // self-loop, or a later op names this edge
-    const bool use_out = la <= lb;
-    const long long row0 = use_out ? oa : ob;
-    const int pos = wave_find((use_out ? out.col : in.col) + row0, use_out ? la : lb, use_out ? b : a);
-    const bool present = pos >= 0;
-    const bool want = op.kind == RIPPLE_OP_INSERT;
-    const bool weighted = out.wt != nullptr;
-    const float w_old = weighted && present ? (use_out ? out.wt : in.wt)[row0 + pos] : 1.0f;
-    const float w_new = weighted ? op.weight : 1.0f;
-    const bool reweight = want && present && w_old != w_new;
+    const int net = emit_edge(op, a, b, la, lb, oa, ob, undirected, out, in, ins_src, ins_dst, del_src, del_dst,
+                              ins_rank, del_rank, ins_w, del_w, c);
+    if (lane == 0) ht_net[s] = net;
+  }
+}
+
+// Netting in one launch for batches of at most kNetDirectMax ops (see
+// launch_net_direct). Wave i takes op i: it checks the op as k_net_hash does, and
+// compares it with every later op of the batch (64 per round, all rounds' loads in
+// flight together). An op that no later op overrides (same edge key; for feature
+// writes, same vertex) decides: a feature write sets fop and lists its vertex, an
+// edge op runs the decision of k_net_decide. Only net-deleted keys enter the hash
+// table (the row rewrite looks up nothing else; an absent key is kept), tagged -1,
+// and op_slot names their slots for the clean-up.
+constexpr int kNetDirectRounds = kNetDirectMax / kWave;
+static_assert(kNetDirectRounds * kWave == kNetDirectMax, "whole rounds");
+
+__global__ void k_net_direct(const BatchIn *host_in, BatchIn now, BatchIn *dev_in, ripple_op *ops, int undirected,
+                             int weighted, long long n, u64 *ht_key, int *ht_net, unsigned mask, int *op_slot,
+                             int *fop, Adj out, Adj in, int *ins_src, int *ins_dst, int *del_src, int *del_dst,
+                             int *ins_rank, int *del_rank, float *ins_w, float *del_w, int *flist, Counters *c) {
+  if (host_in != nullptr) {
+    const auto word = [&](const void *f) {
+      return __hip_atomic_load(static_cast<const u64 *>(f), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    };
+    now.ops = reinterpret_cast<const ripple_op *>(word(&host_in->ops));
+    now.feat = reinterpret_cast<const float *>(word(&host_in->feat));
+    now.num_ops = static_cast<long long>(word(&host_in->num_ops));
+    now.num_feat_rows = static_cast<long long>(word(&host_in->num_feat_rows));
+  }
+  const ripple_op *src_ops = now.ops;
+  const long long B = now.num_ops;
+  const long long i = global_wave();
+  const int lane = lane_id();
+  if (i == 0 && lane == 0) *dev_in = now;
+  if (i >= B) return;
+  ripple_op op = src_ops[i];
+  ripple_op later[kNetDirectRounds];
+#pragma unroll
+  for (int t = 0; t < kNetDirectRounds; ++t) {
+    const long long j = i + 1 + lane + static_cast<long long>(t) * kWave;
+    later[t] = j < B ? src_ops[j] : ripple_op{-1, 0, 0, 0};
+  }
+  bool bad;
+  if (op.kind == RIPPLE_OP_INSERT || op.kind == RIPPLE_OP_DELETE)
+    bad = op.u < 0 || op.u >= n || op.v < 0 || op.v >= n ||
+          (weighted && op.kind == RIPPLE_OP_INSERT && !isfinite(op.weight));
+  else if (op.kind == RIPPLE_OP_FEATURE)
+    bad = op.u < 0 || op.u >= n || op.feat_row < 0 || op.feat_row >= now.num_feat_rows;
+  else
+    bad = true;
+  if (bad) {
+    // the batch aborts before anything is mutated; the later kernels see a harmless self-loop
     if (lane == 0) {
-      atomicAdd(&c->edge_keys, 1ull);
-      if (want == present && !reweight) {
-        atomicAdd(&c->noop_edge, 1ull);
-        ht_net[s] = 0;
-      } else {
-        // a reweight drops the old entry (as a delete) and puts the arc back with its
-        // new weight (as an insert)
-        ht_net[s] = want && !reweight ? 1 : -1;
-        const int narcs = undirected ? 2 : 1;
-        if (reweight) atomicAdd(&c->n_rew, static_cast<u64>(narcs));
-        for (int kind = 0; kind < 2; ++kind) {  // 0: delete item, 1: insert item
-          if (kind == 0 ? !present : !want) continue;
-          const bool ins = kind == 1;
-          int *ps = ins ? ins_src : del_src;
-          int *pd = ins ? ins_dst : del_dst;
-          int *rank = ins ? ins_rank : del_rank;
-          const u64 j = atomicAdd(ins ? &c->n_ins : &c->n_del, static_cast<u64>(narcs));
-          for (int t = 0; t < narcs; ++t) {
-            const int su = t == 0 ? a : b, sv = t == 0 ? b : a;
-            ps[j + t] = su;
-            pd[j + t] = sv;
-            (ins ? ins_w : del_w)[j + t] = ins ? w_new : w_old;
-            rank[2 * (j + t)] = atomicAdd(ins ? &out.inscnt[su] : &out.delcnt[su], 1);
-            rank[2 * (j + t) + 1] = atomicAdd(ins ? &in.inscnt[sv] : &in.delcnt[sv], 1);
-          }
-        }
+      atomicMax(&c->bad_op, static_cast<u64>(B - i));
+      c->abort = 1;
+      ops[i] = ripple_op{RIPPLE_OP_INSERT, 0, 0, -1};
+      op_slot[i] = -1;
+    }
+    return;
+  }
+  if (lane == 0) ops[i] = op;
+  if (op.kind == RIPPLE_OP_FEATURE) {
+    bool over = false;
+#pragma unroll
+    for (int t = 0; t < kNetDirectRounds; ++t) over = over || (later[t].kind == RIPPLE_OP_FEATURE && later[t].u == op.u);
+    const bool decides = __ballot(over) == 0;
+    if (lane == 0) {
+      op_slot[i] = -1;
+      if (decides) {
+        fop[op.u] = static_cast<int>(i);
+        flist[atomicAdd(&c->n_feat, 1ull)] = op.u;
       }
     }
+    return;
+  }
+  if (op.u == op.v) {
+    if (lane == 0) {
+      atomicAdd(&c->noop_edge, 1ull);
+      op_slot[i] = -1;
+    }
+    return;
+  }
+  int a = op.u, b = op.v;
+  if (undirected && a > b) {
+    const int t = a;
+    a = b;
+    b = t;
+  }
+  const u64 key = edge_key(a, b, undirected, n);
+  bool over = false;
+#pragma unroll
+  for (int t = 0; t < kNetDirectRounds; ++t) {
+    const bool edge = later[t].kind == RIPPLE_OP_INSERT || later[t].kind == RIPPLE_OP_DELETE;
+    over = over || (edge && later[t].u != later[t].v && edge_key(later[t].u, later[t].v, undirected, n) == key);
+  }
+  // the rows the decision reads go out with the comparison (ids are checked)
+  const int la = out.len[a], lb = in.len[b];
+  const long long oa = out.off[a], ob = in.off[b];
+  if (__ballot(over) != 0) {
+    if (lane == 0) op_slot[i] = -1;
+    return;
+  }
+  const int net = emit_edge(op, a, b, la, lb, oa, ob, undirected, out, in, ins_src, ins_dst, del_src, del_dst,
+                            ins_rank, del_rank, ins_w, del_w, c);
+  if (lane == 0) {
+    int slot = -1;
+    if (net == -1) {
+      unsigned sl = hash_slot(key, mask);
+      while (true) {
+        const u64 prev = atomicCAS(&ht_key[sl], kEmptyKey, key);
+        if (prev == kEmptyKey || prev == key) break;
+        sl = (sl + 1) & mask;
+      }
+      ht_net[sl] = -1;
+      slot = static_cast<int>(sl);
+    }
+    op_slot[i] = slot;
   }
 }
 
@@ -545,6 +674,17 @@ void launch_net_hash(hipStream_t s, int cap_ops, const BatchIn *host_in, const B
                      int *fop, Counters *c) {
   hipLaunchKernelGGL(k_net_hash, dim3(blocks_for(cap_ops, 256, 1 << 20)), dim3(256), 0, s, host_in, now, dev_in, ops,
                      undirected, weighted, n, ht_key, ht_val, mask, op_slot, fop, c);
+}
+
+void launch_net_direct(hipStream_t s, int cap_ops, const BatchIn *host_in, const BatchIn &now, BatchIn *dev_in,
+                       ripple_op *ops, int undirected, int weighted, long long n, u64 *ht_key, int *ht_net,
+                       unsigned mask, int *op_slot, int *fop, Adj out, Adj in_adj, int *ins_src, int *ins_dst,
+                       int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w, float *del_w,
+                       int *flist, Counters *c) {
+  const int ops_cap = cap_ops < kNetDirectMax ? cap_ops : kNetDirectMax;
+  hipLaunchKernelGGL(k_net_direct, dim3(blocks_for(static_cast<long long>(ops_cap) * kWave, 256)), dim3(256), 0, s,
+                     host_in, now, dev_in, ops, undirected, weighted, n, ht_key, ht_net, mask, op_slot, fop, out,
+                     in_adj, ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank, ins_w, del_w, flist, c);
 }
 
 void launch_net_decide(hipStream_t s, int cap_ops, const BatchIn *in, const ripple_op *ops, int undirected,

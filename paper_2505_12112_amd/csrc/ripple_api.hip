@@ -701,6 +701,7 @@ struct BatchPlan {
   bool direct0;                        // the corrections kernel lists the layer-1 dirty set
   int app;                             // bit l: layer l's scatter lists A^l (see ScatterList)
   bool arena_plan;                     // the arena check runs (else every possible row move fits)
+  bool net_direct;                     // netting in one launch (small batches)
   unsigned long long key;              // the above as GEMM variants, and the counter parity
 };
 
@@ -767,6 +768,8 @@ BatchPlan make_plan(const ripple_ctx *c) {
     p.arena_plan = !fits;
   }
   key |= static_cast<unsigned long long>(p.arena_plan) << 61;
+  p.net_direct = c->h_in->num_ops <= rp::kNetDirectMax;
+  key |= static_cast<unsigned long long>(p.net_direct) << 60;
   p.key = key;
   return p;
 }
@@ -792,12 +795,19 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
   PhaseScope total(c, RIPPLE_PHASE_TOTAL);
   {
     PhaseScope ps(c, RIPPLE_PHASE_NET);
-    rp::launch_net_hash(s, cap_ops, replay ? c->h_in : nullptr, *c->h_in, c->d_in, c->d_ops, c->undirected,
-                        c->weighted ? 1 : 0, c->n, c->ht_key, c->ht_val, c->ht_mask, c->op_slot, c->fop, dc);
-    rp::launch_net_decide(s, cap_ops, c->d_in, c->d_ops, c->undirected, c->ht_val, c->ht_net, c->op_slot, c->fop, out,
-                          in, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank, c->del_rank, c->ins_w,
-                          c->del_w, c->flist, dc);
-    add_launches(c, RIPPLE_PHASE_NET, 2);
+    if (p.net_direct) {
+      rp::launch_net_direct(s, cap_ops, replay ? c->h_in : nullptr, *c->h_in, c->d_in, c->d_ops, c->undirected,
+                            c->weighted ? 1 : 0, c->n, c->ht_key, c->ht_net, c->ht_mask, c->op_slot, c->fop, out, in,
+                            c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank, c->del_rank, c->ins_w,
+                            c->del_w, c->flist, dc);
+    } else {
+      rp::launch_net_hash(s, cap_ops, replay ? c->h_in : nullptr, *c->h_in, c->d_in, c->d_ops, c->undirected,
+                          c->weighted ? 1 : 0, c->n, c->ht_key, c->ht_val, c->ht_mask, c->op_slot, c->fop, dc);
+      rp::launch_net_decide(s, cap_ops, c->d_in, c->d_ops, c->undirected, c->ht_val, c->ht_net, c->op_slot, c->fop,
+                            out, in, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank, c->del_rank,
+                            c->ins_w, c->del_w, c->flist, dc);
+    }
+    add_launches(c, RIPPLE_PHASE_NET, p.net_direct ? 1 : 2);
   }
   {
     PhaseScope ps(c, RIPPLE_PHASE_TOPO);
