@@ -401,6 +401,9 @@ __global__ void k_topo_plan(Adj out, Adj in, const int *ins_src, const int *ins_
 }
 
 constexpr int kRewriteU = 16;  // row entries per lane per step: 1024 per wave
+// Rows up to this long whose only change is one delete are fixed by a search and a
+// swap-remove (at most four rounds of wave_find) instead of a full rewrite.
+constexpr int kSoloDeleteMax = 2048;
 
 // Clears keep[u] for the entries x[u] of `row` (direction dir) that the batch
 // deletes. Each entry's edge-key slot is probed together with the slot's net
@@ -553,6 +556,27 @@ __global__ __launch_bounds__(256) void k_topo_rewrite(int undirected, long long 
     const int need = len0 - k + nins;
     const bool move = nins > 0 && need > cap0;
     const bool swept = long_ok && k > 0 && !move && len0 >= kLongRow;  // listed by the plan
+    if (!ins_item && k == 1 && nins == 0 && len0 > 0 && len0 <= kSoloDeleteMax) {
+      // this delete is the row's only change: find its entry (the row's last entry is
+      // read in the same round) and move the last entry into its slot; rows are
+      // unordered, so the swap-remove keeps the row valid
+      int *rc = a.col + src_off;
+      float *rw = a.wt != nullptr ? a.wt + src_off : nullptr;
+      const int last = rc[len0 - 1];
+      const float last_w = rw != nullptr ? rw[len0 - 1] : 0.0f;
+      const int pos = wave_find(rc, len0, entry);
+      if (lane == 0) {
+        if (pos < 0) {
+          atomicOr(&c->err, 1ull);  // a net-deleted arc that is not in its row
+        } else if (pos != len0 - 1) {
+          rc[pos] = last;
+          if (rw != nullptr) rw[pos] = last_w;
+        }
+        a.len[row] = need;
+        if (dir == 0) ddeg[row] = -1;
+      }
+      continue;
+    }
     const int nc = move ? grow_cap(need) : 0;
     // a moving row's arena slots: the returning atomic stays in flight while the
     // row is read (its value is needed only for the writes)
