@@ -219,11 +219,11 @@ void launch_net_direct(hipStream_t s, int cap_ops, const BatchIn *host_in, const
                        ripple_op *ops, int undirected, int weighted, long long n, u64 *ht_key, int *ht_net,
                        unsigned mask, int *op_slot, int *fop, Adj out, Adj in_adj, int *ins_src, int *ins_dst,
                        int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w, float *del_w,
-                       int *flist, Counters *c);
+                       int *flist, int *frow, Counters *c);
 void launch_net_decide(hipStream_t s, int cap_ops, const BatchIn *in, const ripple_op *ops, int undirected,
                        const int *ht_val, int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in_adj,
                        int *ins_src, int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank,
-                       float *ins_w, float *del_w, int *flist, Counters *c);
+                       float *ins_w, float *del_w, int *flist, int *frow, Counters *c);
 
 // topology (cap_arcs bounds n_ins and n_del): plan row moves and check the arena
 // (aborting before any mutation), then one owner wave per touched row removes its
@@ -280,9 +280,8 @@ struct DirectList {
   int ld;
   int d0;
   const float *X;
-  const ripple_op *ops;
+  const int *frow;  // feature row of each listed vertex (flist order)
   const BatchIn *in;
-  const int *fop;
 };
 // Rows the layer-1 scatter copies after the direct listing: X[list[j]] = stage[j]
 // for every listed j (dst == nullptr: none).

@@ -114,7 +114,7 @@ __global__ void k_corr_mark(int agg, LayerPtrs lp, Adj out, Adj in, const int *i
     for (long long j = num_waves() - 1 - global_wave(); j < nl; j += num_waves()) {
       const int u = flist[j];
       const float *xu = dl.X + static_cast<long long>(u) * dl.d0;
-      const float *xn = feat + static_cast<long long>(dl.ops[dl.fop[u]].feat_row) * dl.d0;
+      const float *xn = feat + static_cast<long long>(dl.frow[j]) * dl.d0;
       float *dj = dl.delta + j * dl.ld;
       float *sj = dl.stage + j * dl.ld;
       for (int k = lane; k < dl.d0; k += kWave) {

@@ -201,7 +201,7 @@ __device__ inline int emit_edge(const ripple_op &op, int a, int b, int la, int l
 __global__ void k_net_decide(const BatchIn *bin, const ripple_op *ops, int undirected, const int *ht_val,
                              int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in, int *ins_src,
                              int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w,
-                             float *del_w, int *flist, Counters *c) {
+                             float *del_w, int *flist, int *frow, Counters *c) {
   const int lane = lane_id();
   const long long B = bin->num_ops;
   for (long long i = global_wave(); i < B; i += num_waves()) {
@@ -211,6 +211,7 @@ __global__ void k_net_decide(const BatchIn *bin, const ripple_op *ops, int undir
       if (lane == 0 && fop[op.u] == i) {
         const u64 j = atomicAdd(&c->n_feat, 1ull);
         flist[j] = op.u;
+        frow[j] = op.feat_row;
       }
       continue;
     }
@@ -249,7 +250,8 @@ static_assert(kNetDirectRounds * kWave == kNetDirectMax, "whole rounds");
 __global__ void k_net_direct(const BatchIn *host_in, BatchIn now, BatchIn *dev_in, ripple_op *ops, int undirected,
                              int weighted, long long n, u64 *ht_key, int *ht_net, unsigned mask, int *op_slot,
                              int *fop, Adj out, Adj in, int *ins_src, int *ins_dst, int *del_src, int *del_dst,
-                             int *ins_rank, int *del_rank, float *ins_w, float *del_w, int *flist, Counters *c) {
+                             int *ins_rank, int *del_rank, float *ins_w, float *del_w, int *flist, int *frow,
+                             Counters *c) {
   if (host_in != nullptr) {
     const auto word = [&](const void *f) {
       return __hip_atomic_load(static_cast<const u64 *>(f), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
@@ -300,7 +302,9 @@ __global__ void k_net_direct(const BatchIn *host_in, BatchIn now, BatchIn *dev_i
       op_slot[i] = -1;
       if (decides) {
         fop[op.u] = static_cast<int>(i);
-        flist[atomicAdd(&c->n_feat, 1ull)] = op.u;
+        const u64 j = atomicAdd(&c->n_feat, 1ull);
+        flist[j] = op.u;
+        frow[j] = op.feat_row;
       }
     }
     return;
@@ -704,20 +708,20 @@ void launch_net_direct(hipStream_t s, int cap_ops, const BatchIn *host_in, const
                        ripple_op *ops, int undirected, int weighted, long long n, u64 *ht_key, int *ht_net,
                        unsigned mask, int *op_slot, int *fop, Adj out, Adj in_adj, int *ins_src, int *ins_dst,
                        int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w, float *del_w,
-                       int *flist, Counters *c) {
+                       int *flist, int *frow, Counters *c) {
   const int ops_cap = cap_ops < kNetDirectMax ? cap_ops : kNetDirectMax;
   hipLaunchKernelGGL(k_net_direct, dim3(blocks_for(static_cast<long long>(ops_cap) * kWave, 256)), dim3(256), 0, s,
                      host_in, now, dev_in, ops, undirected, weighted, n, ht_key, ht_net, mask, op_slot, fop, out,
-                     in_adj, ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank, ins_w, del_w, flist, c);
+                     in_adj, ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank, ins_w, del_w, flist, frow, c);
 }
 
 void launch_net_decide(hipStream_t s, int cap_ops, const BatchIn *in, const ripple_op *ops, int undirected,
                        const int *ht_val, int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in_adj,
                        int *ins_src, int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank,
-                       float *ins_w, float *del_w, int *flist, Counters *c) {
+                       float *ins_w, float *del_w, int *flist, int *frow, Counters *c) {
   hipLaunchKernelGGL(k_net_decide, dim3(blocks_for(static_cast<long long>(cap_ops) * kWave, 256)), dim3(256), 0, s,
                      in, ops, undirected, ht_val, ht_net, op_slot, fop, out, in_adj, ins_src, ins_dst, del_src,
-                     del_dst, ins_rank, del_rank, ins_w, del_w, flist, c);
+                     del_dst, ins_rank, del_rank, ins_w, del_w, flist, frow, c);
 }
 
 void launch_topo_plan(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,

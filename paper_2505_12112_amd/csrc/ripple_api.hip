@@ -152,6 +152,7 @@ struct ripple_ctx {
   int *ins_rank = nullptr, *del_rank = nullptr;
   float *ins_w = nullptr, *del_w = nullptr;  // the net arcs' weights (weighted graphs)
   int *flist = nullptr;
+  int *frow = nullptr;  // feature row of each flist entry
   // rows long enough for the chunked delete sweep exist (or may, once rows grow):
   // the plan lists such rows in long_tab, their sweeps record positions in long_pool
   int long_ok = 0;
@@ -424,6 +425,7 @@ void free_batch_scratch(ripple_ctx *c) {
   dfree_t(c, c->ins_w);
   dfree_t(c, c->del_w);
   dfree_t(c, c->flist);
+  dfree_t(c, c->frow);
   if (c->h_ops) (void)hipHostFree(c->h_ops);
   if (c->h_feat) (void)hipHostFree(c->h_feat);
   c->h_ops = nullptr;
@@ -462,6 +464,7 @@ ripple_status ensure_batch_scratch(ripple_ctx *c, long long ops, long long frows
   RP_TRY(dalloc_n(c, &c->del_w, arcs));
   RP_TRY(dalloc_n(c, &c->del_rank, 2 * arcs));
   RP_TRY(dalloc_n(c, &c->flist, cap));
+  RP_TRY(dalloc_n(c, &c->frow, cap));
   if (c->long_ok) {  // at most one long row per (net arc, direction), and two slots per deleted entry
     RP_TRY(dalloc_n(c, &c->long_tab, 2 * arcs));
     RP_TRY(dalloc_n(c, &c->long_pool, 4 * arcs));
@@ -799,13 +802,13 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
       rp::launch_net_direct(s, cap_ops, replay ? c->h_in : nullptr, *c->h_in, c->d_in, c->d_ops, c->undirected,
                             c->weighted ? 1 : 0, c->n, c->ht_key, c->ht_net, c->ht_mask, c->op_slot, c->fop, out, in,
                             c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank, c->del_rank, c->ins_w,
-                            c->del_w, c->flist, dc);
+                            c->del_w, c->flist, c->frow, dc);
     } else {
       rp::launch_net_hash(s, cap_ops, replay ? c->h_in : nullptr, *c->h_in, c->d_in, c->d_ops, c->undirected,
                           c->weighted ? 1 : 0, c->n, c->ht_key, c->ht_val, c->ht_mask, c->op_slot, c->fop, dc);
       rp::launch_net_decide(s, cap_ops, c->d_in, c->d_ops, c->undirected, c->ht_val, c->ht_net, c->op_slot, c->fop,
                             out, in, c->ins_src, c->ins_dst, c->del_src, c->del_dst, c->ins_rank, c->del_rank,
-                            c->ins_w, c->del_w, c->flist, dc);
+                            c->ins_w, c->del_w, c->flist, c->frow, dc);
     }
     add_launches(c, RIPPLE_PHASE_NET, p.net_direct ? 1 : 2);
   }
@@ -830,9 +833,9 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
     // is staged in delta[1], which layer 1's GEMM fills only after the scatter
     rp::DirectList direct{};
     if (p.direct0)
-      direct = rp::DirectList{c->lists[0], c->doff[0],  &dc->count[0],           &dc->pushed[1],
-                              nullptr,     nullptr,     rp::row_ld(c->dims[0]), c->dims[0],
-                              c->H[0],     c->d_ops,    c->d_in,                c->fop};
+      direct = rp::DirectList{c->lists[0], c->doff[0], &dc->count[0],           &dc->pushed[1],
+                              nullptr,     nullptr,    rp::row_ld(c->dims[0]), c->dims[0],
+                              c->H[0],     c->frow,    c->d_in};
     const bool direct_delta = p.direct0 && !c->tf[1];
     if (direct_delta) {
       direct.delta = c->delta[0];
