@@ -214,7 +214,7 @@ void launch_net_hash(hipStream_t s, int cap_ops, const BatchIn *host_in, const B
 // Both netting steps in one launch, for a batch of at most kNetDirectMax ops: the
 // same outputs, except that only net-deleted edge keys enter the hash table (tagged
 // -1, their slots in op_slot; every other op's op_slot is -1) and ht_val is unused.
-constexpr int kNetDirectMax = 512;
+constexpr int kNetDirectMax = 1024;
 void launch_net_direct(hipStream_t s, int cap_ops, const BatchIn *host_in, const BatchIn &now, BatchIn *dev_in,
                        ripple_op *ops, int undirected, int weighted, long long n, u64 *ht_key, int *ht_net,
                        unsigned mask, int *op_slot, int *fop, Adj out, Adj in_adj, int *ins_src, int *ins_dst,

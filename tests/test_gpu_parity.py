@@ -99,9 +99,10 @@ def test_adversarial_batches(agg, undirected, mode):
 @pytest.mark.parametrize("agg", ["sum", "gcn", "gc_wsum"])
 @pytest.mark.parametrize("undirected", [False, True])
 def test_adversarial_batches_of_either_netting(agg, undirected):
-    """The same colliding ops in batches of 1-512 ops (netted in one launch, each op
-    compared with the later ones) and of 513-1200 ops (hashed, then decided), on one
-    context: the two nettings must agree with the oracle's sequential semantics."""
+    """The same colliding ops in batches of at most 1024 ops (netted in one launch,
+    each op compared with the later ones) and of 1025-1600 ops (hashed, then
+    decided), on one context: the two nettings must agree with the oracle's
+    sequential semantics."""
     _say("adversarial netting", agg, undirected)
     rng = np.random.default_rng(97 + 5 * undirected + len(agg))
     dims = (8, 24, 6)
@@ -109,7 +110,7 @@ def test_adversarial_batches_of_either_netting(agg, undirected):
     p = Pair(300, src, dst, x, w, undirected=undirected, edge_w=_edge_w(rng, agg, src.size))
     try:
         for b in range(12):
-            bs = int(rng.integers(513, 1201)) if b % 2 else int(rng.integers(400, 513))
+            bs = int(rng.integers(1025, 1601)) if b % 2 else int(rng.integers(800, 1025))
             a, bb = p.orc.graph.arcs()
             batch = synth.adversarial_batch(rng, 300, dims[0], bs=bs, hot=10, existing=(a, bb),
                                             weighted=agg == "gc_wsum")
@@ -333,7 +334,7 @@ def test_degenerate_and_extreme_shapes(case):
 @pytest.mark.parametrize("mode", ["push", "pull", "dense"])
 def test_phase_stats_count_launches_and_bytes(mode):
     """Phase events: every phase of a profiled batch is timed, the launches are
-    counted per phase (one netting (two for batches over 512 ops), one topology (the arena check only when the
+    counted per phase (one netting (two for batches over 1024 ops), one topology (the arena check only when the
     spare arena might not hold the batch's row moves), three layer-0 launches per
     batch, one when layer 1 pushes: the corrections kernel then lists the
     feature-written vertices and their deltas itself; per layer one message launch when pushing,
@@ -355,7 +356,7 @@ def test_phase_stats_count_launches_and_bytes(mode):
         L = len(dims) - 1
         # (the arena check is left out: this graph's spare arena holds any row move
         # a 30-op batch can cause)
-        # (one netting launch: batches of up to 512 ops are netted in one pass)
+        # (one netting launch: batches of up to 1024 ops are netted in one pass)
         assert ph["net"]["launches"] == nb and ph["topo"]["launches"] == nb
         assert ph["layer0"]["launches"] == (1 if mode == "push" else 3) * nb
         assert ph["scatter"]["launches"] == (1 if mode == "push" else 2) * L * nb
