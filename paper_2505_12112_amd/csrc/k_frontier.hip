@@ -8,7 +8,10 @@
 // is collected in two bitmaps (one for the out-arc sinks, so that their distinct
 // count is known exactly) and compacted into a sorted list by a popcount prefix
 // sum, which also yields each listed vertex's first out-arc index for the next
-// layer's scatter.
+// layer's scatter. A pushing layer with a small frontier instead lists A^l in its
+// own scatter, in no particular order: the first setter of a member's bit appends
+// it (see ScatterList). The layer-1 dirty set of a batch without GCN terms is
+// listed by the correction kernel itself, with its deltas.
 #include "internal.h"
 
 namespace rp {

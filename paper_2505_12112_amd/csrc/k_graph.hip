@@ -6,15 +6,19 @@
 // pass lets each winning op compare the final state with the pre-batch adjacency,
 // emit the net inserted / deleted arcs, tag the edge's hash slot (+1 insert,
 // -1 delete) and take a rank among its rows' inserts or deletes. The last feature
-// write per vertex is found the same way with a per-vertex atomicMax.
+// write per vertex is found the same way with a per-vertex atomicMax. Batches of
+// up to kNetDirectMax ops are netted in one pass instead: each op is compared with
+// every later op, and only net-deleted keys are hashed (for the row rewrite).
 //
 // Adjacency update: row slots are [off, off+cap), the first len used, in no
 // particular order. A plan pass sums the spare-arena slots that growing rows need
 // and the last block to finish checks them against the arena: a batch that does
 // not fit is aborted before anything is mutated (the host then re-lays the rows
-// out and runs the batch again). Then one owner wave per touched row drops its
-// net-deleted entries (hash lookups), moves the row to the arena if it must grow,
-// and sets the new length; finally every insert is written at its rank.
+// out and runs the batch again). The host leaves the plan out when the free arena
+// holds every move the batch could cause. Then one owner wave per touched row
+// drops its net-deleted entries (hash lookups; a lone delete is found by a search
+// and swap-removed), moves the row to the arena if it must grow, and sets the new
+// length; finally every insert is written at its rank.
 #include "internal.h"
 
 namespace rp {

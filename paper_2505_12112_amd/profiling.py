@@ -38,15 +38,48 @@ TRAFFIC_MD = os.path.join(ROOT, "profiles", "hbm_traffic_counters.md")
 PHASE_KERNELS = {"scatter": ("k_scatter", "k_pull_msgs"), "gemm": ("k_gemm",)}
 
 
+def code_only(text: str) -> str:
+    """C/C++ source without its comments, whitespace runs collapsed to one space
+    (string and character literals kept as written)."""
+    parts = []  # code runs (whitespace collapsed) and literals (kept)
+    code = []
+    i, n = 0, len(text)
+    while i < n:
+        c = text[i]
+        if c == "/" and text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+            continue
+        if c == "/" and text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            code.append(" ")
+            continue
+        if c in "\"'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            parts.append(" ".join("".join(code).split()))
+            parts.append(text[i:j + 1])
+            code = []
+            i = j + 1
+            continue
+        code.append(c)
+        i += 1
+    parts.append(" ".join("".join(code).split()))
+    return " ".join(p for p in parts if p)
+
+
 def source_hash() -> str:
-    """sha256 over the HIP sources and headers the library is built from."""
+    """sha256 over the code of the HIP sources and headers the library is built from
+    (comments and layout do not change it)."""
     h = hashlib.sha256()
     files = sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")) + glob.glob(os.path.join(HERE, "csrc", "*.h"))
                    + [os.path.join(ROOT, "include", "ripple.h")])
     for f in files:
         h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8") as fh:
+            h.update(code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 
