@@ -705,8 +705,26 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
       const long long e0 = g * kWave;
       const long long elast = e0 + kWave - 1 < E - 1 ? e0 + kWave - 1 : E - 1;
       const long long ja = wave_last_le(doff, 0, nD, e0);
-      const long long jb = owner_from(doff, ja, nD, elast);
-      list_mark(run_sink(doff, list, out, e0, elast, ja, jb), true, lo, bm_out, bm_x);
+      // the owners' offsets doff[ja ..], one per lane: when the group's last arc
+      // falls in this window (it spans at most 64 owners), each arc's owner and
+      // offset come from it by shuffles, with no second search
+      const long long mine = ja + lane < nD ? doff[ja + lane] : (1LL << 62);
+      const u64 in_run = __ballot(mine <= elast);
+      const int owners = __popcll(in_run);
+      int v = -1;
+      if (owners < kWave || ja + kWave >= nD) {
+        const long long e = e0 + lane;
+        int cnt_le = 0;
+        for (int t = 0; t < owners; ++t) cnt_le += __shfl(mine, t) <= e ? 1 : 0;
+        const long long start = __shfl(mine, cnt_le > 0 ? cnt_le - 1 : 0);
+        if (e <= elast) {
+          const int u = list[ja + cnt_le - 1];
+          v = out.col[out.off[u] + (e - start)];
+        }
+      } else {
+        v = run_sink(doff, list, out, e0, elast, ja, owner_from(doff, ja, nD, elast));
+      }
+      list_mark(v, true, lo, bm_out, bm_x);
     }
   }
   // the owner searches run over doff[0, n1): a compacted list's doff[nD] holds the
