@@ -536,6 +536,26 @@ __device__ inline long long wave_last_le(const long long *a, long long lo, long 
   return lo + __popcll(__ballot(le)) - 1;
 }
 
+// wave_last_le over [0, n) that also hands back its last round's loads: lane t
+// holds a[w0 + t] (1 << 62 past n), w0 <= the answer.
+__device__ inline long long wave_last_le_win(const long long *a, long long n, long long x, long long &win,
+                                             long long &w0) {
+  const int lane = lane_id();
+  long long lo = 0, hi = n;
+  while (hi - lo > kWave) {
+    const long long step = (hi - lo + kWave - 1) / kWave;
+    const long long idx = lo + lane * step;
+    const bool le = idx < hi && a[idx] <= x;
+    const int last = __popcll(__ballot(le)) - 1;
+    lo = lo + last * step;
+    hi = lo + step < hi ? lo + step : hi;
+  }
+  const long long idx = lo + lane;
+  win = idx < n ? a[idx] : (1LL << 62);
+  w0 = lo;
+  return lo + __popcll(__ballot(idx < hi && win <= x)) - 1;
+}
+
 // Same answer as wave_last_le(a, from, n1, x), for a lower bound `from` whose
 // answer is usually close: one round of 64 probes from `from`, and the full
 // search only when every probe is <= x. Used when a wave walks consecutive arcs.
@@ -704,21 +724,22 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
     for (long long g = waves - 1 - global_wave(); g < groups; g += waves) {
       const long long e0 = g * kWave;
       const long long elast = e0 + kWave - 1 < E - 1 ? e0 + kWave - 1 : E - 1;
-      const long long ja = wave_last_le(doff, 0, nD, e0);
-      // the owners' offsets doff[ja ..], one per lane: when the group's last arc
-      // falls in this window (it spans at most 64 owners), each arc's owner and
-      // offset come from it by shuffles, with no second search
-      const long long mine = ja + lane < nD ? doff[ja + lane] : (1LL << 62);
-      const u64 in_run = __ballot(mine <= elast);
-      const int owners = __popcll(in_run);
+      // the search's last round leaves doff[w0 .. w0 + 63] in the lanes (w0 <= ja):
+      // when the group's last arc falls in that window (no more than 64 - (ja - w0)
+      // owners), each arc's owner and offset come from it by shuffles, with no
+      // further load of the offsets
+      long long mine, w0;
+      const long long ja = wave_last_le_win(doff, nD, e0, mine, w0);
+      const int owners = __popcll(__ballot(mine <= elast));  // window entries starting at or before elast
       int v = -1;
-      if (owners < kWave || ja + kWave >= nD) {
+      if (owners < kWave || w0 + kWave >= nD) {
         const long long e = e0 + lane;
         int cnt_le = 0;
-        for (int t = 0; t < owners; ++t) cnt_le += __shfl(mine, t) <= e ? 1 : 0;
-        const long long start = __shfl(mine, cnt_le > 0 ? cnt_le - 1 : 0);
+        for (int t = static_cast<int>(ja - w0); t < owners; ++t) cnt_le += __shfl(mine, t) <= e ? 1 : 0;
+        const int at = static_cast<int>(ja - w0) + (cnt_le > 0 ? cnt_le - 1 : 0);
+        const long long start = __shfl(mine, at);
         if (e <= elast) {
-          const int u = list[ja + cnt_le - 1];
+          const int u = list[w0 + at];
           v = out.col[out.off[u] + (e - start)];
         }
       } else {
