@@ -446,7 +446,8 @@ struct GemmArgs {
 };
 // Blocks a batch's clean-up takes for cap_ops ops.
 int cleanup_blocks_for(long long cap_ops);
-// expected_rows picks the tile height (large tiles when many rows are expected);
+// expected_rows picks the kernel: 0 = 16-row tiles split over eight waves (short
+// lists), 2 = the same over four waves, 1 = 128-row tiles (many rows);
 // gemm_variant(expected_rows) names the choice (launches with the same variant
 // and arguments are the same launch).
 void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows, long long expected_rows);

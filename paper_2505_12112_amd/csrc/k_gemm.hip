@@ -386,24 +386,30 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
 }
 
 // Small-row-count variant, built for latency: a block owns a 16 x BN output tile
-// and its four waves split K into four contiguous ranges. Every lane loads its
+// and its W waves split K into W contiguous ranges. Every lane loads its
 // operands straight from global memory into registers as float4: lane (r, q)
 // holds A row r and B column r at k = 16 f + 4 q .. 16 f + 4 q + 3 of its range,
 // and at MFMA sub-step i both operands give component i, the same permutation of
-// k on both sides. A range of up to 128 k values thus costs one round of loads and
+// k on both sides. A range of up to 64 (W = 8) or 128 (W = 4) k values thus costs one round of loads and
 // no LDS staging. The epilogue's inputs (old embedding row, cached transform,
 // degrees, bias) are fetched as soon as the row ids are known, together with the
 // operands, so a tile takes three dependent rounds of memory access: row count,
-// row ids, then everything else. The four partial tiles meet in LDS.
+// row ids, then everything else. The W partial tiles meet in LDS.
 constexpr int kRowsBM = 16;
-constexpr int kRowsKC = 128;  // k values per wave per round of loads
+// Lists of up to this many expected rows take eight waves per tile (64 k values
+// per wave per round: the MFMA chain of a wave is half as long); longer ones four
+// (128 k values per round, twice the tiles per compute unit).
+constexpr long long kRowsWideMax = 2048;
 
-template <int BN, int AGG, int MODE>
-__global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
+template <int BN, int AGG, int MODE, int W>
+__global__ __launch_bounds__(W * kWave) void k_gemm_rows(GemmArgs a) {
+  constexpr int kRowsWaves = W;  // waves per tile, each on its own range of k
+  constexpr int kRowsThreads = W * kWave;
+  constexpr int kRowsKC = W == 8 ? 64 : 128;  // k values per wave per round of loads
   constexpr int WN = BN / 16;
-  constexpr int kF = kRowsKC / 16;            // float4 per lane per operand row and round
-  constexpr int kEl = kRowsBM * BN / kThreads;  // output elements per thread
-  static_assert(kRowsBM * BN % kThreads == 0, "whole elements per thread");
+  constexpr int kF = kRowsKC / 16;  // float4 per lane per operand row and round
+  constexpr int kTile = kRowsBM * BN;
+  constexpr int kEl = (kTile + kRowsThreads - 1) / kRowsThreads;  // output elements per thread (at most)
   unsigned gemm_grid;
   if (cleanup_role(a, gemm_grid)) return;
   const int N = a.N, K = a.K, dp = a.dprev;
@@ -422,8 +428,9 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
     va = ar < limit ? (a.rows != nullptr ? a.rows[ar] : static_cast<int>(ar)) : -1;
 #pragma unroll
     for (int i = 0; i < kEl; ++i) {
-      const long long row = m0 + (tid + i * kThreads) / BN;
-      ve[i] = row < limit ? (a.rows != nullptr ? a.rows[row] : static_cast<int>(row)) : -1;
+      const int e = tid + i * kRowsThreads;
+      const long long row = m0 + e / BN;
+      ve[i] = e < kTile && row < limit ? (a.rows != nullptr ? a.rows[row] : static_cast<int>(row)) : -1;
     }
   };
   // The first tile's ids are fetched with the row count: the list holds max_rows
@@ -435,9 +442,9 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
   if (abort_or_rows(a, M, static_cast<unsigned>(va) >> 1, static_cast<unsigned>(ve[0]) >> 1)) return;
   const long long tiles = ((M + kRowsBM - 1) / kRowsBM) * tiles_n;
 
-  __shared__ float red[4][kRowsBM][BN + 1];
+  __shared__ float red[kRowsWaves][kRowsBM][BN + 1];
 
-  const int kw = (K + 63) / 64 * 16;  // k values per wave, a multiple of 16
+  const int kw = (K + kRowsWaves * 16 - 1) / (kRowsWaves * 16) * 16;  // k values per wave, a multiple of 16
   const int kb = wave * kw;
   const int ke = K < kb + kw ? K : kb + kw;
 
@@ -448,7 +455,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
       if (m0 + lr >= M) va = -1;
 #pragma unroll
       for (int i = 0; i < kEl; ++i)
-        if (m0 + (tid + i * kThreads) / BN >= M) ve[i] = -1;
+        if (m0 + (tid + i * kRowsThreads) / BN >= M) ve[i] = -1;
     } else {
       row_ids(t, M);
     }
@@ -475,7 +482,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
     float e_old[kEl], e_t[kEl], e_tv[kEl], e_sv[kEl], e_co[kEl], e_b[kEl];
 #pragma unroll
     for (int i = 0; i < kEl; ++i) {
-      const int col = n0 + (tid + i * kThreads) % BN;
+      const int col = n0 + (tid + i * kRowsThreads) % BN;
       const int v = ve[i];
       e_old[i] = 0.f;
       e_t[i] = 0.f;
@@ -571,12 +578,14 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < kEl; ++i) {
-      const int e = tid + i * kThreads;
+      const int e = tid + i * kRowsThreads;
       const int ml = e / BN, cl = e % BN;
       const int col = n0 + cl;
       const int v = ve[i];
       if (v < 0 || col >= N) continue;
-      float y = red[0][ml][cl] + red[1][ml][cl] + red[2][ml][cl] + red[3][ml][cl];
+      float y = 0.f;
+#pragma unroll
+      for (int w = 0; w < kRowsWaves; ++w) y += red[w][ml][cl];
       if (MODE == kTransformFirst) y = AGG == kGcn ? e_tv[i] * (e_t[i] + e_sv[i] * y) : y + e_tv[i] * e_t[i];
       y += e_b[i];
       if (a.relu) y = fmaxf(y, 0.f);
@@ -592,11 +601,14 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(GemmArgs a) {
 }
 
 template <int BN, int AGG, int MODE>
-void launch_rows(hipStream_t s, const GemmArgs &a, long long max_rows) {
+void launch_rows(hipStream_t s, const GemmArgs &a, long long max_rows, bool wide) {
   const long long tiles = ((max_rows + kRowsBM - 1) / kRowsBM) * ((a.N + BN - 1) / BN);
   long long blocks = tiles < 1 ? 1 : tiles;
   if (blocks > 2048) blocks = 2048;
-  hipLaunchKernelGGL((k_gemm_rows<BN, AGG, MODE>), dim3(blocks + a.cleanup_blocks), dim3(kThreads), 0, s, a);
+  if (wide)
+    hipLaunchKernelGGL((k_gemm_rows<BN, AGG, MODE, 8>), dim3(blocks + a.cleanup_blocks), dim3(8 * kWave), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_gemm_rows<BN, AGG, MODE, 4>), dim3(blocks + a.cleanup_blocks), dim3(4 * kWave), 0, s, a);
 }
 
 template <int BM, int BN, int WM, int WN, int AGG, bool VEC, int MODE>
@@ -608,9 +620,11 @@ void launch_shape(hipStream_t s, const GemmArgs &a, long long max_rows) {
                      a);
 }
 
-// BN follows N. Few expected rows: the 16-row split-K kernel; many: 128-row tiles.
+// BN follows N. Few expected rows: the 16-row split-K kernel; many: 128-row tiles
+// (variant: see gemm_variant).
 template <int AGG, bool VEC, int MODE>
-void launch_agg(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) {
+void launch_agg(hipStream_t s, const GemmArgs &a, long long max_rows, int variant) {
+  const bool big = variant == 1, wide = variant == 0;
   const int N = a.N;
   if (!VEC) {
     if (N <= 16) launch_shape<64, 16, 1, 1, AGG, VEC, MODE>(s, a, max_rows);
@@ -621,10 +635,10 @@ void launch_agg(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) 
     return;
   }
   if (!big) {
-    if (N <= 16) launch_rows<16, AGG, MODE>(s, a, max_rows);
-    else if (N <= 32) launch_rows<32, AGG, MODE>(s, a, max_rows);
-    else if (N <= 48) launch_rows<48, AGG, MODE>(s, a, max_rows);
-    else launch_rows<64, AGG, MODE>(s, a, max_rows);  // N > 64: several 64-wide column tiles
+    if (N <= 16) launch_rows<16, AGG, MODE>(s, a, max_rows, wide);
+    else if (N <= 32) launch_rows<32, AGG, MODE>(s, a, max_rows, wide);
+    else if (N <= 48) launch_rows<48, AGG, MODE>(s, a, max_rows, wide);
+    else launch_rows<64, AGG, MODE>(s, a, max_rows, wide);  // N > 64: several 64-wide column tiles
     return;
   }
   if (N <= 16) launch_shape<64, 16, 1, 1, AGG, VEC, MODE>(s, a, max_rows);
@@ -635,32 +649,32 @@ void launch_agg(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) 
 }
 
 template <int AGG, int MODE>
-void launch_vec(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) {
+void launch_vec(hipStream_t s, const GemmArgs &a, long long max_rows, int variant) {
   const bool vec = (a.dprev % 4 == 0) && (a.K % 4 == 0);
-  if (vec) launch_agg<AGG, true, MODE>(s, a, max_rows, big);
-  else launch_agg<AGG, false, MODE>(s, a, max_rows, big);
+  if (vec) launch_agg<AGG, true, MODE>(s, a, max_rows, variant);
+  else launch_agg<AGG, false, MODE>(s, a, max_rows, variant);
 }
 
 template <int MODE>
-void launch_mode(hipStream_t s, const GemmArgs &a, long long max_rows, bool big) {
+void launch_mode(hipStream_t s, const GemmArgs &a, long long max_rows, int variant) {
   if constexpr (MODE == kGin1 || MODE == kGin2) {
-    launch_vec<kSum, MODE>(s, a, max_rows, big);  // GIN sums with coefficient 1
+    launch_vec<kSum, MODE>(s, a, max_rows, variant);  // GIN sums with coefficient 1
   } else {
     switch (a.agg) {
       case kMean:
-        launch_vec<kMean, MODE>(s, a, max_rows, big);
+        launch_vec<kMean, MODE>(s, a, max_rows, variant);
         break;
       case kGcn:
-        launch_vec<kGcn, MODE>(s, a, max_rows, big);
+        launch_vec<kGcn, MODE>(s, a, max_rows, variant);
         break;
       case kGcSum:
-        if constexpr (MODE == kLayer) launch_vec<kGcSum, MODE>(s, a, max_rows, big);
+        if constexpr (MODE == kLayer) launch_vec<kGcSum, MODE>(s, a, max_rows, variant);
         break;
       case kGcMean:
-        if constexpr (MODE == kLayer) launch_vec<kGcMean, MODE>(s, a, max_rows, big);
+        if constexpr (MODE == kLayer) launch_vec<kGcMean, MODE>(s, a, max_rows, variant);
         break;
       default:
-        launch_vec<kSum, MODE>(s, a, max_rows, big);
+        launch_vec<kSum, MODE>(s, a, max_rows, variant);
         break;
     }
   }
@@ -668,7 +682,9 @@ void launch_mode(hipStream_t s, const GemmArgs &a, long long max_rows, bool big)
 
 }  // namespace
 
-int gemm_variant(long long expected_rows) { return expected_rows >= 32768 ? 1 : 0; }
+int gemm_variant(long long expected_rows) {
+  return expected_rows >= 32768 ? 1 : expected_rows > kRowsWideMax ? 2 : 0;
+}
 
 int cleanup_blocks_for(long long cap_ops) {
   // up to 4 * cap_ops (arc, direction) items and cap_ops ops, grid-strided
@@ -679,12 +695,12 @@ int cleanup_blocks_for(long long cap_ops) {
 void launch_gemm(hipStream_t s, const GemmArgs &args, long long max_rows, long long expected_rows) {
   GemmArgs a = args;
   a.max_rows = max_rows;
-  const bool big = gemm_variant(expected_rows) == 1;
-  if (a.mode == kTransformFirst) launch_mode<kTransformFirst>(s, a, max_rows, big);
-  else if (a.mode == kPlain) launch_mode<kPlain>(s, a, max_rows, big);
-  else if (a.mode == kGin1) launch_mode<kGin1>(s, a, max_rows, big);
-  else if (a.mode == kGin2) launch_mode<kGin2>(s, a, max_rows, big);
-  else launch_mode<kLayer>(s, a, max_rows, big);
+  const int variant = gemm_variant(expected_rows);
+  if (a.mode == kTransformFirst) launch_mode<kTransformFirst>(s, a, max_rows, variant);
+  else if (a.mode == kPlain) launch_mode<kPlain>(s, a, max_rows, variant);
+  else if (a.mode == kGin1) launch_mode<kGin1>(s, a, max_rows, variant);
+  else if (a.mode == kGin2) launch_mode<kGin2>(s, a, max_rows, variant);
+  else launch_mode<kLayer>(s, a, max_rows, variant);
 }
 
 }  // namespace rp

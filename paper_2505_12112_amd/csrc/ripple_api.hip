@@ -730,8 +730,8 @@ BatchPlan make_plan(const ripple_ctx *c) {
     p.rows[l] = guess[l];
     key |= static_cast<unsigned long long>(p.mode[l]) << bit;
     key |= static_cast<unsigned long long>(rp::gemm_variant(p.tf_rows[l])) << (bit + 2);
-    key |= static_cast<unsigned long long>(rp::gemm_variant(p.rows[l])) << (bit + 3);
-    bit += 4;
+    key |= static_cast<unsigned long long>(rp::gemm_variant(p.rows[l])) << (bit + 4);
+    bit += 6;  // up to bit 48 for 8 layers
   }
   // the layer-1 dirty set is the feature-written vertices alone unless GCN adds
   // the sources whose out-degree changed; listed directly when layer 1 pushes (a
@@ -751,7 +751,7 @@ BatchPlan make_plan(const ripple_ctx *c) {
     const bool next_ok = l == c->L || (p.mode[l + 1] == kPushLayer && arcs[l + 1] <= kAppMaxNextArcs);
     if (p.mode[l] == kPushLayer && arcs[l] <= kAppMaxArcs && next_ok) p.app |= 1 << l;
   }
-  key |= static_cast<unsigned long long>(p.app) << 40;
+  key |= static_cast<unsigned long long>(p.app) << 49;  // bits 50-57
   // The plan launch sums the arena slots that growing rows need and aborts the
   // batch if they do not fit. Only rows that gain arcs move: at most (2 for
   // undirected graphs) x ops rows per direction, each to grow_cap of at most its
