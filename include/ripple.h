@@ -51,7 +51,8 @@
  *     context exactly as it was.
  *   - A HIP runtime error, or a failed device-side consistency check (a deleted
  *     arc missing from its row, a row length mismatch, a compaction wait that
- *     timed out), poisons the context: that call returns RIPPLE_E_DEVICE and every
+ *     timed out, a row move that would end past its column buffer), poisons the
+ *     context: that call returns RIPPLE_E_DEVICE and every
  *     later call except ripple_last_error / ripple_destroy returns RIPPLE_E_STATE.
  *   - A context is used by one host thread at a time. Calls are synchronous:
  *     they return after the device work they issued has finished.
@@ -299,8 +300,9 @@ enum {
   RIPPLE_PHASE_NET = 0,      /* op netting (hash + membership) */
   RIPPLE_PHASE_TOPO = 1,     /* pre-batch corrections + adjacency update */
   RIPPLE_PHASE_LAYER0 = 2,   /* feature writes and layer-0 deltas */
-  RIPPLE_PHASE_SCATTER = 3,  /* delta scatter-add + frontier marking, all layers */
-  RIPPLE_PHASE_COMPACT = 4,  /* frontier bitmaps -> sorted lists, all layers */
+  RIPPLE_PHASE_SCATTER = 3,  /* delta scatter-add + frontier marking (and listing, for small push
+                                frontiers), all layers */
+  RIPPLE_PHASE_COMPACT = 4,  /* frontier bitmaps -> sorted lists (pulls, large frontiers), all layers */
   RIPPLE_PHASE_GEMM = 5,     /* gather + transform + epilogue, all layers */
   RIPPLE_PHASE_OTHER = 6,    /* scratch clean-up */
   RIPPLE_PHASE_TOTAL = 7     /* first to last kernel of the batch */
