@@ -158,9 +158,14 @@ __global__ void k_net_hash(const BatchIn *host_in, BatchIn now, BatchIn *dev_in,
 // before the batch (searched in the shorter row), and then either a no-op or the net
 // arcs with their ranks among their rows' inserts or deletes. Returns the edge's net
 // change on every lane: +1 inserted, -1 deleted or reweighted, 0 none.
+// ht_key != nullptr: a net-deleted key is also entered into the hash table, its
+// slot tagged -1 in ht_net and written to *slot (-1 otherwise); the first probe
+// goes out with the emission's atomics.
 __device__ inline int emit_edge(const ripple_op &op, int a, int b, int la, int lb, long long oa, long long ob,
                                 int undirected, Adj out, Adj in, int *ins_src, int *ins_dst, int *del_src,
-                                int *del_dst, int *ins_rank, int *del_rank, float *ins_w, float *del_w, Counters *c) {
+                                int *del_dst, int *ins_rank, int *del_rank, float *ins_w, float *del_w, Counters *c,
+                                u64 *ht_key = nullptr, int *ht_net = nullptr, unsigned mask = 0, u64 key = 0,
+                                int *slot = nullptr) {
   const int lane = lane_id();
   const bool use_out = la <= lb;
   const long long row0 = use_out ? oa : ob;
@@ -172,6 +177,14 @@ __device__ inline int emit_edge(const ripple_op &op, int a, int b, int la, int l
   const float w_new = weighted ? op.weight : 1.0f;
   const bool reweight = want && present && w_old != w_new;
   const bool noop = want == present && !reweight;
+  const int net = noop ? 0 : want && !reweight ? 1 : -1;
+  const bool probe = ht_key != nullptr && net == -1;
+  unsigned sl = 0;
+  u64 prev = kEmptyKey;
+  if (lane == 0 && probe) {
+    sl = hash_slot(key, mask);
+    prev = atomicCAS(&ht_key[sl], kEmptyKey, key);
+  }
   if (lane == 0) {
     atomicAdd(&c->edge_keys, 1ull);
     if (noop) {
@@ -198,8 +211,18 @@ __device__ inline int emit_edge(const ripple_op &op, int a, int b, int la, int l
         }
       }
     }
+    if (ht_key != nullptr) {
+      if (probe) {  // walk on from the first probe to the key's slot
+        while (prev != kEmptyKey && prev != key) {
+          sl = (sl + 1) & mask;
+          prev = atomicCAS(&ht_key[sl], kEmptyKey, key);
+        }
+        ht_net[sl] = -1;
+      }
+      *slot = probe ? static_cast<int>(sl) : -1;
+    }
   }
-  return noop ? 0 : want && !reweight ? 1 : -1;
+  return net;
 }
 
 __global__ void k_net_decide(const BatchIn *bin, const ripple_op *ops, int undirected, const int *ht_val,
@@ -340,22 +363,8 @@ __global__ void k_net_direct(const BatchIn *host_in, BatchIn now, BatchIn *dev_i
     if (lane == 0) op_slot[i] = -1;
     return;
   }
-  const int net = emit_edge(op, a, b, la, lb, oa, ob, undirected, out, in, ins_src, ins_dst, del_src, del_dst,
-                            ins_rank, del_rank, ins_w, del_w, c);
-  if (lane == 0) {
-    int slot = -1;
-    if (net == -1) {
-      unsigned sl = hash_slot(key, mask);
-      while (true) {
-        const u64 prev = atomicCAS(&ht_key[sl], kEmptyKey, key);
-        if (prev == kEmptyKey || prev == key) break;
-        sl = (sl + 1) & mask;
-      }
-      ht_net[sl] = -1;
-      slot = static_cast<int>(sl);
-    }
-    op_slot[i] = slot;
-  }
+  emit_edge(op, a, b, la, lb, oa, ob, undirected, out, in, ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank,
+            ins_w, del_w, c, ht_key, ht_net, mask, key, op_slot + i);
 }
 
 __global__ void k_topo_plan(Adj out, Adj in, const int *ins_src, const int *ins_dst, const int *del_src,
