@@ -51,8 +51,8 @@ __device__ inline u64 edge_key(int a, int b, int undirected, long long n) {
 
 // Position of `target` in row[0, len) or -1; all lanes of the wave get the answer.
 // Reads kFindU entries per lane per round, all in flight together, so a row of up
-// to 512 entries costs one round trip.
-constexpr int kFindU = 8;
+// to 1024 entries costs one round trip.
+constexpr int kFindU = 16;
 
 __device__ inline int wave_find(const int *row, int len, int target) {
   const int lane = lane_id();
@@ -419,7 +419,7 @@ __global__ void k_topo_plan(Adj out, Adj in, const int *ins_src, const int *ins_
 
 constexpr int kRewriteU = 16;  // row entries per lane per step: 1024 per wave
 // Rows up to this long whose only change is one delete are fixed by a search and a
-// swap-remove (at most four rounds of wave_find) instead of a full rewrite.
+// swap-remove (at most two rounds of wave_find) instead of a full rewrite.
 constexpr int kSoloDeleteMax = 2048;
 
 // Clears keep[u] for the entries x[u] of `row` (direction dir) that the batch
