@@ -120,7 +120,8 @@ struct ripple_ctx {
   long long last_in[rp::kMaxL + 1] = {};
   int last_pull = 0;   // layers that pulled over A^l's in-arcs (bit l)
   int last_dense = 0;  // layers that pulled over every in-arc (bit l)
-  int last_app = 0;    // layers whose A^l its scatter listed, unordered (bit l)
+  int last_app = 0;    // layers whose A^l its scatter listed, unordered (bit l), as of the last completed batch
+  int run_app = 0;     // the same for the batch in flight (it becomes last_app once that batch completes)
   float *delta[2] = {nullptr, nullptr};
   rp::Counters *d_counters = nullptr;  // two buffers; batch parity picks one
   int parity = 0;
@@ -1006,7 +1007,7 @@ ripple_status launch_batch(ripple_ctx *c) {
     if (p.mode[l] == kPullLayer) c->last_pull |= 1 << l;
     if (p.mode[l] == kDenseLayer) c->last_dense |= 1 << l;
   }
-  c->last_app = p.app;
+  c->run_app = p.app;
   c->last_graph = false;
   hipGraphExec_t g = c->use_graphs && !c->graphs_failed && !c->prof ? plan_graph(c, p) : nullptr;
   if (g != nullptr) {
@@ -1513,7 +1514,7 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
   rp::Counters &k = *c->h_counters;
   // lists built by a scatter keep their count and out-arc total in one word
   for (int l = 1; l <= c->L; ++l) {
-    if (!(c->last_app >> l & 1)) continue;
+    if (!(c->run_app >> l & 1)) continue;
     k.count[l] = k.app[l] >> rp::kAppShift;
     if (l < c->L) k.pushed[l + 1] = k.app[l] & rp::kAppMask;
     k.dest[l] = k.app_sinks[l] >> rp::kAppShift;
@@ -1526,6 +1527,7 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
     // row move would have ended past the column buffer
     return fail(c, RIPPLE_E_DEVICE, "ripple: device-side check failed (err bits " + std::to_string(k.err) + ")");
   }
+  c->last_app = c->run_app;  // the lists now hold this batch's sets
   c->arcs_now += static_cast<long long>(k.n_ins) - static_cast<long long>(k.n_del);
   for (int d = 0; d < 2; ++d) {
     c->row_max[d] = std::max(c->row_max[d], static_cast<long long>(k.maxlen[d]));

@@ -447,15 +447,16 @@ def test_invalid_batch_changes_nothing():
 
 def test_device_resident_batch_is_checked_on_the_device():
     """A batch in device memory with a bad op is rejected by the kernels before
-    anything changes, naming the first bad op; a host pointer is refused; the next
-    valid batch goes through."""
+    anything changes, naming the first bad op (the affected sets still read as the
+    last good batch's, ascending); a host pointer is refused; the next valid batch
+    goes through."""
     import torch
     rng = np.random.default_rng(18)
     dims = (6, 8, 3)
     src, dst, x, w = _small(rng, 100, 300, dims, "mean")
     p = Pair(100, src, dst, x, w, inputs="device")
     try:
-        p.step(random_valid_batch(rng, p.orc, 20, dims[0]))
+        _, _, sets_before = p.step(random_valid_batch(rng, p.orc, 20, dims[0]))
         before = [p.lib.get_embeddings(l) for l in range(3)]
         good = random_valid_batch(rng, p.orc, 12, dims[0])
         for bad_op in ([1, 0, 100, -1], [3, 1, -1, 1000], [9, 1, 2, -1], [2, -1, 2, -1]):
@@ -470,6 +471,8 @@ def test_device_resident_batch_is_checked_on_the_device():
         assert e.value.status == E_INVALID
         for l in range(3):
             np.testing.assert_array_equal(p.lib.get_embeddings(l), before[l])
+        for l in range(1, 3):
+            np.testing.assert_array_equal(p.lib.get_affected(l), np.sort(sets_before[l]))
         p.check_arcs()
         p.step(good)
         p.check_embeddings()
