@@ -53,7 +53,11 @@
  *     arc missing from its row, a row length mismatch, a compaction wait that
  *     timed out, a row move that would end past its column buffer), poisons the
  *     context: that call returns RIPPLE_E_DEVICE and every
- *     later call except ripple_last_error / ripple_destroy returns RIPPLE_E_STATE.
+ *     later call except ripple_last_error / ripple_device_bytes / ripple_destroy
+ *     returns RIPPLE_E_STATE. For tests of this path, the environment variable
+ *     RIPPLE_DEBUG_FAIL_BATCH=k, read by ripple_load_graph, makes the k-th batch
+ *     that completes on that context report a failed device-side check (after
+ *     all of its kernels have finished normally).
  *   - A context is used by one host thread at a time. Calls are synchronous:
  *     they return after the device work they issued has finished.
  */
@@ -182,6 +186,9 @@ typedef struct {
                                    ripple_set_graphs); 0: its kernels were queued one by one */
   int64_t long_rows;            /* adjacency rows of at least 16384 entries whose deletes were swept by
                                    many waves in chunks (graphs whose snapshot has rows of 8192 or more) */
+  int32_t recompute_layers;     /* bit l set: layer l recomputed the aggregate rows of A^l from the
+                                   current embeddings (re-anchoring; see ripple_set_reanchor) */
+  int32_t reserved;
 } ripple_batch_stats;
 
 /* Part 1 of the problem statement: copies the snapshot to the device as an
@@ -259,10 +266,29 @@ RIPPLE_API ripple_status ripple_get_arc_weights(ripple_ctx *ctx, int32_t directi
  * RIPPLE_SCATTER_PULL, each affected vertex sums the messages of its dirty
  * in-neighbours and adds them once; RIPPLE_SCATTER_DENSE, the pull form over every
  * in-arc of the graph, which also finds the sinks (no per-arc marks; for layers
- * where most arcs carry a message); RIPPLE_SCATTER_AUTO (default), per layer from
- * the previous batch's counts (push on the first batch). */
-enum { RIPPLE_SCATTER_AUTO = 0, RIPPLE_SCATTER_PUSH = 1, RIPPLE_SCATTER_PULL = 2, RIPPLE_SCATTER_DENSE = 3 };
+ * where most arcs carry a message); RIPPLE_SCATTER_RECOMPUTE, no messages: each
+ * affected vertex's aggregate row is summed afresh over all its in-arcs from the
+ * current embeddings (reads only, summed in fp64 and rounded once: the
+ * layer-wise recompute of Sec. IV-B, to which the incremental path degrades when
+ * a hop covers the graph, Sec. VII-C; it also re-anchors the cached rows);
+ * RIPPLE_SCATTER_AUTO (default), per layer from the previous batch's counts, or
+ * for the first batch from an estimate based on the snapshot's degrees. */
+enum {
+  RIPPLE_SCATTER_AUTO = 0,
+  RIPPLE_SCATTER_PUSH = 1,
+  RIPPLE_SCATTER_PULL = 2,
+  RIPPLE_SCATTER_DENSE = 3,
+  RIPPLE_SCATTER_RECOMPUTE = 4
+};
 RIPPLE_API ripple_status ripple_set_scatter_mode(ripple_ctx *ctx, int32_t mode);
+
+/* Drift budget of the cached aggregates. Messages add fp32 rounding to a cached
+ * row every time they reach it; with every = k >= 1, every k-th batch (counted
+ * from ripple_init_embeddings) runs each layer in the RIPPLE_SCATTER_RECOMPUTE
+ * form, whatever form ripple_set_scatter_mode asks for, so every row that batch
+ * affects is recomputed afresh. every = 0: never. Default 64. RIPPLE_E_INVALID
+ * for every < 0. */
+RIPPLE_API ripple_status ripple_set_reanchor(ripple_ctx *ctx, int64_t every);
 
 /* How a batch's kernels reach the GPU. enable = 1: the first batch of each launch
  * plan (message form and GEMM tile per layer) is captured as a HIP graph on the

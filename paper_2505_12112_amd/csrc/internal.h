@@ -133,6 +133,8 @@ struct CleanupArgs {
   int *out_inscnt, *out_delcnt, *in_inscnt, *in_delcnt;
   const int *ins_src, *ins_dst, *del_src, *del_dst;
   int *ddeg;
+  const int *flist;   // the batch's feature-written vertices (A^0), n_feat of them
+  int *flist_done;    // A^0 of the last batch that completed: flist is copied here unless the batch aborted
   const Counters *c;  // this batch's counters, copied to host
   Counters *next;     // the other counter buffer, zeroed for the next batch
   Counters *host;     // pinned
@@ -140,7 +142,9 @@ struct CleanupArgs {
 
 // Resets every per-batch scratch word the batch touched (also after an abort),
 // copies the batch's counters to pinned host memory and clears the other counter
-// buffer. Thread t of `threads` (t = 0 also copies the counters, with the rest of
+// buffer. A batch that did not abort also leaves its A^0 in flist_done, so a
+// rejected batch (whose netting rewrote flist) cannot change the sets that the
+// last completed batch returns. Thread t of `threads` (t = 0 also copies the counters, with the rest of
 // its block: block is the calling block's index among the cleanup blocks). Runs in
 // the batch's last kernel beside work that reads none of this scratch.
 __device__ inline void batch_cleanup(const CleanupArgs &a, int block, long long t0, long long threads) {
@@ -175,6 +179,10 @@ __device__ inline void batch_cleanup(const CleanupArgs &a, int block, long long 
       a.out_delcnt[u] = 0;
       a.ddeg[u] = 0;
     }
+  }
+  if (a.c->abort == 0) {
+    const long long nf = static_cast<long long>(a.c->n_feat);
+    for (long long i = t0; i < nf; i += threads) a.flist_done[i] = a.flist[i];
   }
   for (long long i = t0; i < B; i += threads) {
     const int s = a.op_slot[i];
@@ -314,7 +322,15 @@ struct CompactOut {
   u64 *out_total;      // receives the sum of out_deg over the list (the next scatter's arcs)
   u64 *sinks_a;        // receives the number of bits set in the first bitmap
   uint2 *memb;
+  // zero_rows (nullable, with ioff): rows zero_w floats wide of every listed vertex
+  // whose in-degree exceeds kRecomputeSeg are zeroed (the recompute form adds such
+  // rows up from several segments)
+  float *zero_rows;
+  int zero_w;
 };
+// The recompute form (launch_recompute) sums an in-row of more than kRecomputeSeg
+// arcs in segments of that many, each added to the row with fp32 atomics.
+constexpr int kRecomputeSeg = 256;
 // Tile sums published by the single-pass compaction: compact_scratch_words(n)
 // words, zero when first used, then owned by the compactions of one vertex count
 // (each launch finds its epoch from a ticket counter kept there).
@@ -387,6 +403,17 @@ void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, 
 // set the bit of every sink that received a message (the dense form's frontier).
 void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *ioff,
                       Adj in, const uint2 *memb, const float *msg, float *S, unsigned *mark, const Counters *c);
+
+// recompute (re-anchoring) form of the message step: for every vertex v of the
+// sorted list A (in-arc prefix ioff), S[v] = sum over in-arcs (u -> v) of c'_u
+// src[u] (c' = 1, or 1/sqrt(dout'(u)+1) under GCN, times the arc's weight when
+// in.wt is set), with the post-batch graph and the current source rows: reads
+// only, summed in fp64 and rounded once, a plain store per row. Rows of more than
+// kRecomputeSeg in-arcs are summed in segments added with fp32 atomics (the
+// compaction that listed A zeroed them, see CompactOut::zero_rows). d is the row
+// width of src and S.
+void launch_recompute(hipStream_t s, long long n, int d, int gcn, const int *list, const u64 *count,
+                      const long long *ioff, Adj in, const int *out_len, const float *src, float *S, const Counters *c);
 
 // bootstrap pull: S[v] = sum over in-arcs c_u H[u]
 void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev, Adj in, const int *out_len,

@@ -483,6 +483,10 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
         o.ioff[pos] = ipos;
         ipos += iv[j];
       }
+      if (o.zero_rows != nullptr && iv[j] > kRecomputeSeg) {  // summed in segments by the recompute
+        float *r = o.zero_rows + static_cast<long long>(v[j]) * o.zero_w;
+        for (int k = 0; k < o.zero_w; ++k) r[k] = 0.f;
+      }
       ++pos;
     }
   }
@@ -999,33 +1003,156 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
   }
 }
 
+// Recompute form of the message step (see launch_recompute). The in-arcs of the
+// sorted list A are numbered by ioff. A wave takes ranges of C consecutive arc
+// numbers (a contiguous run of ranges per wave, so that each range's sinks are
+// found from the previous range's) and owns every segment that starts in its
+// range: a segment is up to kRecomputeSeg consecutive in-arcs of one sink, the
+// sink's own arcs from ioff_j + s kRecomputeSeg on. So a range owns segment 0 of
+// the sinks that start in it (with C <= kRecomputeSeg no other segment of those),
+// and at most one later segment of the sink that covers its first arc. The
+// range's segments go round-robin to the wave's G-lane groups; a group walks its
+// segment U arcs at a time (one lane per arc fetches the source id, coefficient
+// and weight, then the G lanes fetch the U source rows), summing in fp64. A sink
+// of one segment is stored once, rounded to fp32; the segments of longer sinks
+// are added with fp32 atomics into rows the compaction zeroed. The last range
+// also owns the sinks past the last arc (rows without in-arcs, stored as zeros).
+template <int G, int NC, int U>
+__global__ __launch_bounds__(256) void k_recompute(int d, int gcn, const int *list, const u64 *count,
+                                                   const long long *ioff, Adj in, const int *out_len,
+                                                   const float *src, float *S, const Counters *c) {
+  static_assert(U <= G, "one lane per arc of a step");
+  const long long nA = static_cast<long long>(*count);
+  if (aborted_with(c->abort, nA)) return;
+  const int lane = lane_id();
+  constexpr int kGroups = kWave / G;
+  const int grp = lane / G, k0 = lane % G;
+  const bool weighted = in.wt != nullptr;
+  const long long E = ioff[nA];
+  const long long waves = num_waves();
+  long long C = 16;
+  while (C < kRecomputeSeg && C * waves < E) C <<= 1;
+  const long long ranges = E > 0 ? (E + C - 1) / C : 1;
+  const long long per = (ranges + waves - 1) / waves;
+  const long long r0 = global_wave() * per;
+  const long long r1 = r0 + per < ranges ? r0 + per : ranges;
+  long long jlast = -1;  // the last sink of the previous range (its successor starts this one's)
+  for (long long r = r0; r < r1; ++r) {
+    const long long R0 = r * C;
+    const bool last_range = r == ranges - 1;
+    const long long R1 = last_range ? (1LL << 62) : R0 + C;
+    // first sink starting at or after R0, then the last one starting before R1
+    const long long jf = r == r0 ? (R0 == 0 ? 0 : wave_last_le(ioff, 0, nA + 1, R0 - 1) + 1) : jlast + 1;
+    long long jl = last_range ? nA - 1 : owner_from(ioff, jf > 0 ? jf - 1 : 0, nA + 1, R1 - 1);
+    if (jl > nA - 1) jl = nA - 1;
+    jlast = jl;
+    // the sink before jf covers arc R0 when it ends past it: it may have a segment
+    // starting in this range
+    long long pstart = -1, pend = 0, pj = jf - 1;
+    if (pj >= 0) {
+      const long long a = ioff[pj], b = ioff[pj + 1];
+      if (b > R0) {
+        const long long s = (R0 - a + kRecomputeSeg - 1) / kRecomputeSeg;
+        const long long st = a + s * kRecomputeSeg;
+        if (st < R1 && st < b) {
+          pstart = st;
+          pend = st + kRecomputeSeg < b ? st + kRecomputeSeg : b;
+        }
+      }
+    }
+    const long long has_pred = pstart >= 0 ? 1 : 0;
+    const long long items = has_pred + (jl >= jf ? jl - jf + 1 : 0);
+    for (long long it = grp; it < items; it += kGroups) {  // the same bounds for a group's lanes
+      long long j, a0, a1;
+      bool whole;
+      if (it < has_pred) {
+        j = pj;
+        a0 = pstart;
+        a1 = pend;
+        whole = false;
+      } else {
+        j = jf + (it - has_pred);
+        const long long a = ioff[j], b = ioff[j + 1];
+        a0 = a;
+        whole = b - a <= kRecomputeSeg;
+        a1 = whole ? b : a + kRecomputeSeg;
+      }
+      const int v = list != nullptr ? list[j] : static_cast<int>(j);
+      const long long row0 = in.off[v] - ioff[j];  // slot of arc number e is row0 + e
+      double acc[NC];
+#pragma unroll
+      for (int q = 0; q < NC; ++q) acc[q] = 0.0;
+      for (long long e0 = a0; e0 < a1; e0 += U) {
+        int ul = -1;
+        double cl = 0.0;
+        if (k0 < U && e0 + k0 < a1) {
+          const long long slot = row0 + e0 + k0;
+          ul = in.col[slot];
+          cl = weighted ? static_cast<double>(in.wt[slot]) : 1.0;
+        }
+        if (gcn && ul >= 0) cl /= sqrt(static_cast<double>(out_len[ul]) + 1.0);
+        int uu[U];
+        double cc[U];
+#pragma unroll
+        for (int t = 0; t < U; ++t) {
+          uu[t] = __shfl(ul, grp * G + t);
+          cc[t] = __shfl(cl, grp * G + t);
+        }
+        float row[U][NC];
+#pragma unroll
+        for (int t = 0; t < U; ++t) {
+          const float *su = src + static_cast<long long>(uu[t] >= 0 ? uu[t] : 0) * d;
+#pragma unroll
+          for (int q = 0; q < NC; ++q) {
+            const int k = k0 + q * G;
+            row[t][q] = uu[t] >= 0 && k < d ? su[k] : 0.f;
+          }
+        }
+#pragma unroll
+        for (int t = 0; t < U; ++t)
+#pragma unroll
+          for (int q = 0; q < NC; ++q) acc[q] += cc[t] * static_cast<double>(row[t][q]);
+      }
+      float *sv = S + static_cast<long long>(v) * d;
+#pragma unroll
+      for (int q = 0; q < NC; ++q) {
+        const int k = k0 + q * G;
+        if (k < d) {
+          if (whole) sv[k] = static_cast<float>(acc[q]);
+          else unsafeAtomicAdd(&sv[k], static_cast<float>(acc[q]));
+        }
+      }
+    }
+  }
+}
+
 // Bootstrap: S[v] = sum over in-arcs (u -> v) of c_u H[u], one wave per vertex,
-// in the in-row's order.
+// in the in-row's order, summed in fp64 and rounded once.
 template <int NC>
 __global__ __launch_bounds__(256) void k_pull(long long n, int d, int agg, const float *Hprev, Adj in,
                                               const int *out_len, float *S) {
   const int lane = lane_id();
   for (long long v = global_wave(); v < n; v += num_waves()) {
-    float acc[NC];
+    double acc[NC];
 #pragma unroll
-    for (int q = 0; q < NC; ++q) acc[q] = 0.0f;
+    for (int q = 0; q < NC; ++q) acc[q] = 0.0;
     const int deg = in.len[v];
     const int *row = in.col + in.off[v];
     for (int e0 = 0; e0 < deg; e0 += kWave) {
       const int e = e0 + lane;
       const int uid = e < deg ? row[e] : 0;
-      float cu = 1.0f;
-      if (agg == kGcn && e < deg) cu = 1.0f / sqrtf(static_cast<float>(out_len[uid]) + 1.0f);
-      if (in.wt != nullptr && e < deg) cu *= in.wt[in.off[v] + e];  // the arc's weight
+      double cu = 1.0;
+      if (agg == kGcn && e < deg) cu = 1.0 / sqrt(static_cast<double>(out_len[uid]) + 1.0);
+      if (in.wt != nullptr && e < deg) cu *= static_cast<double>(in.wt[in.off[v] + e]);  // the arc's weight
       const int cnt = deg - e0 < kWave ? deg - e0 : kWave;
       for (int i = 0; i < cnt; ++i) {
         const int u = __shfl(uid, i);
-        const float cf = __shfl(cu, i);
+        const double cf = __shfl(cu, i);
         const float *hu = Hprev + static_cast<long long>(u) * d;
 #pragma unroll
         for (int q = 0; q < NC; ++q) {
           const int k = lane + q * kWave;
-          if (k < d) acc[q] += cf * hu[k];
+          if (k < d) acc[q] += cf * static_cast<double>(hu[k]);
         }
       }
     }
@@ -1033,7 +1160,7 @@ __global__ __launch_bounds__(256) void k_pull(long long n, int d, int agg, const
 #pragma unroll
     for (int q = 0; q < NC; ++q) {
       const int k = lane + q * kWave;
-      if (k < d) sv[k] = acc[q];
+      if (k < d) sv[k] = static_cast<float>(acc[q]);
     }
   }
 }
@@ -1133,6 +1260,23 @@ void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list
   else if (d <= 512) RP_PULLM(64, 8, 4);
   else RP_PULLM(64, 16, 2);
 #undef RP_PULLM
+}
+
+void launch_recompute(hipStream_t s, long long n, int d, int gcn, const int *list, const u64 *count,
+                      const long long *ioff, Adj in, const int *out_len, const float *src, float *S, const Counters *c) {
+  const int blocks = 2048;
+#define RP_RECOMP(GV, NCV, UV)                                                                                   \
+  hipLaunchKernelGGL((k_recompute<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, gcn, list, count, ioff, in, \
+                     out_len, src, S, c)
+  if (d <= 16) RP_RECOMP(16, 1, 8);
+  else if (d <= 32) RP_RECOMP(16, 2, 8);
+  else if (d <= 48) RP_RECOMP(16, 3, 8);
+  else if (d <= 64) RP_RECOMP(16, 4, 8);
+  else if (d <= 128) RP_RECOMP(64, 2, 8);
+  else if (d <= 256) RP_RECOMP(64, 4, 8);
+  else if (d <= 512) RP_RECOMP(64, 8, 4);
+  else RP_RECOMP(64, 16, 2);
+#undef RP_RECOMP
 }
 
 void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev, Adj in, const int *out_len,

@@ -24,6 +24,7 @@
 #include <chrono>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <numeric>
 #include <string>
@@ -36,6 +37,9 @@
 using rp::u64;
 
 namespace {
+
+// Batches between two re-anchoring batches by default (see ripple_set_reanchor).
+constexpr long long kDefaultReanchor = 64;
 
 struct PhaseEv {
   int phase;
@@ -70,6 +74,11 @@ struct ripple_ctx {
   std::string err;
   bool poisoned = false;
   bool inited = false;
+  // test hook (RIPPLE_DEBUG_FAIL_BATCH=k, read by ripple_load_graph): the k-th batch
+  // that completes on the device reports a failed device-side check (err bit 4),
+  // set in the host copy of its counters after every kernel has exited normally
+  long long debug_fail_batch = 0;
+  long long batches_checked = 0;
 
   // adjacency: [0] out (CSR by source), [1] in (CSC by sink)
   rp::Adj adj[2] = {};
@@ -116,10 +125,19 @@ struct ripple_ctx {
   // word); the pull form's membership test and message row in one load
   uint2 *memb[2] = {nullptr, nullptr};
   int scatter_mode = RIPPLE_SCATTER_AUTO;
+  // drift budget: every reanchor_every-th batch recomputes each layer's aggregate
+  // rows of A^l from the current embeddings (0: never)
+  long long reanchor_every = kDefaultReanchor;
+  long long batches_done = 0;  // batches completed since the model was set up
+  // snapshot degrees, kept to plan the first batch (no earlier batch's counts exist)
+  std::vector<int> snap_out, snap_in;
+  const ripple_op *plan_ops = nullptr;  // host copy of the first batch's ops, for its plan
+  std::vector<ripple_op> plan_buf;
   long long last_pushed[rp::kMaxL + 1] = {};
   long long last_in[rp::kMaxL + 1] = {};
   int last_pull = 0;   // layers that pulled over A^l's in-arcs (bit l)
   int last_dense = 0;  // layers that pulled over every in-arc (bit l)
+  int last_recompute = 0;  // layers whose aggregate rows of A^l were recomputed (bit l)
   int last_app = 0;    // layers whose A^l its scatter listed, unordered (bit l), as of the last completed batch
   int run_app = 0;     // the same for the batch in flight (it becomes last_app once that batch completes)
   float *delta[2] = {nullptr, nullptr};
@@ -154,6 +172,7 @@ struct ripple_ctx {
   float *ins_w = nullptr, *del_w = nullptr;  // the net arcs' weights (weighted graphs)
   int *flist = nullptr;
   int *frow = nullptr;  // feature row of each flist entry
+  int *flist_done = nullptr;  // [n]: A^0 of the last completed batch (written by its clean-up)
   // rows long enough for the chunked delete sweep exist (or may, once rows grow):
   // the plan lists such rows in long_tab, their sweeps record positions in long_pool
   int long_ok = 0;
@@ -504,6 +523,7 @@ void free_model(ripple_ctx *c) {
   dfree_t(c, c->delta[0]);
   dfree_t(c, c->delta[1]);
   dfree_t(c, c->ioff);
+  dfree_t(c, c->flist_done);
   for (int k = 0; k < 2; ++k) {
     dfree_t(c, c->memb[k]);
   }
@@ -665,32 +685,96 @@ void add_launches(ripple_ctx *c, int phase, int k) {
 }
 
 // How layer l adds its messages to S^l. Forced modes aside, the form with the
-// least estimated time for the previous batch's counts at this layer (push on the
-// first batch). The rates are fits to MI355X kernel traces of the three forms on
-// the dense_large and stress workloads:
-//   push   per pushed arc: a fixed 90 ps plus its row of fp32 atomics at 1.3 TB/s;
-//   pull   a bit atomic per pushed arc to mark its sink (38 ps), 35 ps per in-arc
-//          of A^l scanned, every message read once at 10 TB/s (the rows are mostly
-//          cache hits), one row of atomics per affected vertex at 1.3 TB/s;
-//   dense  25 ps per in-arc of the whole graph and 20 ps per vertex (the full
-//          listing) instead of the marks and A^l's in-arcs, reads and flushes as pull.
-enum LayerMode { kPushLayer = 0, kPullLayer = 1, kDenseLayer = 2 };
+// least estimated time for the layer's expected counts (pushed arcs, affected rows,
+// their in-arcs: the previous batch's, or for the first batch an estimate from the
+// snapshot's degrees). The rates are fits to MI355X kernel traces of the forms on
+// the dense_large and stress workloads, and to row micro-benchmarks:
+//   push       per pushed arc: a fixed 90 ps plus its row of fp32 atomics at 1.3 TB/s;
+//   pull       a bit atomic per pushed arc to mark its sink (38 ps), 35 ps per in-arc
+//              of A^l scanned (its source's membership looked up), every message
+//              read once at 10 TB/s (the rows are mostly cache hits), one row of
+//              atomics per affected vertex at 1.3 TB/s;
+//   dense      25 ps per in-arc of the whole graph and 20 ps per vertex (the full
+//              listing) instead of the marks and A^l's in-arcs, reads and flushes as
+//              pull;
+//   recompute  the pull's marks, then every in-arc of A^l carries its source's row
+//              (15 ps per arc plus the row at 6 TB/s, the rate of random row reads
+//              from a table larger than the caches), one plain row store per
+//              affected vertex at 5 TB/s.
+// Every reanchor_every-th batch recomputes every layer (the drift budget), whatever
+// the form.
+enum LayerMode { kPushLayer = 0, kPullLayer = 1, kDenseLayer = 2, kRecomputeLayer = 3 };
 
-int layer_mode(const ripple_ctx *c, int l) {
+int layer_mode(const ripple_ctx *c, int l, double pushed, double count, double in_arcs, bool reanchor) {
+  if (reanchor || c->scatter_mode == RIPPLE_SCATTER_RECOMPUTE) return kRecomputeLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_PUSH) return kPushLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_PULL) return kPullLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_DENSE) return kDenseLayer;
-  if (!c->has_batch) return kPushLayer;
   constexpr double kArc = 90e-12, kAtomicRate = 1.3e12, kMark = 38e-12, kPullScan = 35e-12;
   constexpr double kDenseScan = 25e-12, kDenseVertex = 20e-12, kReadRate = 10e12;
+  constexpr double kRecScan = 15e-12, kGatherRate = 6e12, kStoreRate = 5e12;
   const double w = 4.0 * c->sw[l];  // message row bytes
-  const double pushed = static_cast<double>(c->last_pushed[l]);
   const double push = pushed * (kArc + w / kAtomicRate);
-  const double settle = pushed * w / kReadRate + static_cast<double>(c->last_count[l]) * w / kAtomicRate;
-  const double pull = pushed * kMark + static_cast<double>(c->last_in[l]) * kPullScan + settle;
+  const double settle = pushed * w / kReadRate + count * w / kAtomicRate;
+  const double pull = pushed * kMark + in_arcs * kPullScan + settle;
   const double dense = static_cast<double>(c->arcs_now) * kDenseScan + static_cast<double>(c->n) * kDenseVertex + settle;
-  if (push <= pull && push <= dense) return kPushLayer;
-  return pull <= dense ? kPullLayer : kDenseLayer;
+  const double recompute = pushed * kMark + in_arcs * (kRecScan + w / kGatherRate) + count * w / kStoreRate;
+  int best = kPushLayer;
+  double t = push;
+  if (pull < t) best = kPullLayer, t = pull;
+  if (dense < t) best = kDenseLayer, t = dense;
+  if (recompute < t) best = kRecomputeLayer, t = recompute;
+  return best;
+}
+
+// Expected counts of the first batch (no earlier batch to learn from), from the
+// snapshot's degree sequences: layer 1's dirty set is the batch's feature-written
+// vertices (under GCN also the tails of its edge ops), which push their out-degrees;
+// a pushed arc reaches a sink with probability proportional to the sink's
+// in-degree, so x pushed arcs reach sink v with probability 1 - exp(-x din(v)/m).
+// Summed over (a sample of) the vertices this gives the affected rows, their
+// in-arcs and their out-arcs, which the next layer pushes. The heads of the edge
+// ops are affected at every layer, and under a self term the dirty set too.
+void first_batch_counts(const ripple_ctx *c, const ripple_op *ops, long long B, double (&pushed)[rp::kMaxL + 1],
+                        double (&count)[rp::kMaxL + 1], double (&in_arcs)[rp::kMaxL + 1]) {
+  const long long n = c->n;
+  const double m = std::max<double>(1.0, static_cast<double>(c->arcs_loaded));
+  const double mean = m / static_cast<double>(n);
+  const bool gcn = c->agg == rp::kGcn;
+  std::vector<int> dirty;
+  double heads = 0.0;
+  for (long long i = 0; i < B && ops != nullptr; ++i) {
+    const ripple_op &o = ops[i];
+    if (o.kind == RIPPLE_OP_FEATURE) {
+      dirty.push_back(o.u);
+    } else if (o.u != o.v) {
+      heads += c->undirected ? 2.0 : 1.0;
+      if (gcn) dirty.push_back(o.u);
+      if (gcn && c->undirected) dirty.push_back(o.v);
+    }
+  }
+  std::sort(dirty.begin(), dirty.end());
+  dirty.erase(std::unique(dirty.begin(), dirty.end()), dirty.end());
+  double x = 0.0;
+  for (int u : dirty) x += u >= 0 && u < n ? c->snap_out[u] : 0;
+  double prev = static_cast<double>(dirty.size());
+  const long long stride = std::max<long long>(1, n / 65536);
+  const bool self = rp::has_self_term(c->agg);
+  for (int l = 1; l <= c->L; ++l) {
+    double a = 0.0, ia = 0.0, oa = 0.0;
+    for (long long v = 0; v < n; v += stride) {
+      const double p = 1.0 - std::exp(-x * static_cast<double>(c->snap_in[v]) / m);
+      a += p;
+      ia += p * c->snap_in[v];
+      oa += p * c->snap_out[v];
+    }
+    const double extra = heads + (self ? prev : 0.0);  // rows affected without a pushed arc
+    pushed[l] = x;
+    count[l] = std::min(static_cast<double>(n), a * stride + extra);
+    in_arcs[l] = ia * stride + extra * mean;
+    x = oa * stride + extra * mean;
+    prev = count[l];
+  }
 }
 
 rp::CompactScratch compact_scratch(ripple_ctx *c, rp::Counters *dc) {
@@ -718,15 +802,23 @@ BatchPlan make_plan(const ripple_ctx *c) {
   BatchPlan p{};
   unsigned long long key = static_cast<unsigned long long>(c->parity);
   int bit = 1;
-  // expected rows: the previous batch's counts; before any batch, the batch's ops
-  // times the mean degree per hop (no more than n)
+  // expected counts per layer: the previous batch's, or an estimate for the first
+  double pushed[rp::kMaxL + 1] = {}, count[rp::kMaxL + 1] = {}, in_arcs[rp::kMaxL + 1] = {};
+  if (c->has_batch) {
+    for (int l = 0; l <= c->L; ++l) {
+      pushed[l] = static_cast<double>(c->last_pushed[l]);
+      count[l] = static_cast<double>(c->last_count[l]);
+      in_arcs[l] = static_cast<double>(c->last_in[l]);
+    }
+  } else {
+    first_batch_counts(c, c->plan_ops, c->h_in->num_ops, pushed, count, in_arcs);
+    count[0] = static_cast<double>(std::min<long long>(c->h_in->num_ops, c->n));
+  }
+  const bool reanchor = c->reanchor_every > 0 && (c->batches_done + 1) % c->reanchor_every == 0;
   long long guess[rp::kMaxL + 1];
-  const double deg = static_cast<double>(c->arcs_now) / static_cast<double>(c->n);
-  double g = static_cast<double>(c->h_in->num_ops);
-  for (int l = 0; l <= c->L; ++l, g *= deg)
-    guess[l] = c->has_batch ? c->last_count[l] : static_cast<long long>(std::min(g, static_cast<double>(c->n)));
+  for (int l = 0; l <= c->L; ++l) guess[l] = static_cast<long long>(count[l]);
   for (int l = 1; l <= c->L; ++l) {
-    p.mode[l] = layer_mode(c, l);
+    p.mode[l] = layer_mode(c, l, pushed[l], count[l], in_arcs[l], reanchor);
     p.tf_rows[l] = guess[l - 1];
     p.rows[l] = guess[l];
     key |= static_cast<unsigned long long>(p.mode[l]) << bit;
@@ -746,8 +838,7 @@ BatchPlan make_plan(const ripple_ctx *c) {
   // in vertex order)
   p.app = 0;
   double arcs[rp::kMaxL + 2] = {};
-  for (int l = 1; l <= c->L; ++l)
-    arcs[l] = c->has_batch ? static_cast<double>(c->last_pushed[l]) : static_cast<double>(guess[l - 1]) * deg;
+  for (int l = 1; l <= c->L; ++l) arcs[l] = pushed[l];
   for (int l = 1; l <= c->L; ++l) {
     const bool next_ok = l == c->L || (p.mode[l + 1] == kPushLayer && arcs[l + 1] <= kAppMaxNextArcs);
     if (p.mode[l] == kPushLayer && arcs[l] <= kAppMaxArcs && next_ok) p.app |= 1 << l;
@@ -794,8 +885,8 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
   if (c->agg != rp::kGcWsum) out_msg.wt = in_msg.wt = nullptr;
   rp::CleanupArgs cleanup{c->d_in,      c->d_ops,      c->op_slot,   c->ht_key,    c->ht_val,    c->ht_net,
                           c->fop,       out.inscnt,    out.delcnt,   in.inscnt,    in.delcnt,    c->ins_src,
-                          c->ins_dst,   c->del_src,    c->del_dst,   c->ddeg,      dc,           dnext,
-                          c->h_counters};
+                          c->ins_dst,   c->del_src,    c->del_dst,   c->ddeg,      c->flist,     c->flist_done,
+                          dc,           dnext,         c->h_counters};
   PhaseScope total(c, RIPPLE_PHASE_TOTAL);
   {
     PhaseScope ps(c, RIPPLE_PHASE_NET);
@@ -852,7 +943,8 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
       co.out_deg = c->adj[0].len;
       co.doff = c->doff[0];
       co.out_total = &dc->pushed[1];
-      const bool members = p.mode[1] != kPushLayer;  // layer 1 pulls: it needs A^0's membership
+      // layer 1 pulls messages: it looks up A^0's membership
+      const bool members = p.mode[1] == kPullLayer || p.mode[1] == kDenseLayer;
       co.memb = members ? c->memb[0] : nullptr;
       rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
     }
@@ -935,11 +1027,15 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
       co.out_deg = c->adj[0].len;
       co.doff = l < c->L ? c->doff[l] : nullptr;
       co.in_deg = c->adj[1].len;
-      co.ioff = mode == kPullLayer ? c->ioff : nullptr;
+      co.ioff = mode == kPullLayer || mode == kRecomputeLayer ? c->ioff : nullptr;
+      if (mode == kRecomputeLayer) {  // rows summed in segments start from zero
+        co.zero_rows = c->S[l];
+        co.zero_w = c->sw[l];
+      }
       co.in_total = &dc->indeg[l];
       co.out_total = l < c->L ? &dc->pushed[l + 1] : nullptr;
       co.sinks_a = &dc->dest[l];  // distinct sinks of the arcs pushed at layer l
-      const bool members = l < c->L && p.mode[l + 1] != kPushLayer;
+      const bool members = l < c->L && (p.mode[l + 1] == kPullLayer || p.mode[l + 1] == kDenseLayer);
       co.memb = members ? c->memb[l & 1] : nullptr;
       rp::launch_compact(s, c->n, c->bm_out, c->bm_x, compact_scratch(c, dc), co);
       add_launches(c, RIPPLE_PHASE_COMPACT, 1);
@@ -948,6 +1044,14 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
       rp::launch_pull_msgs(s, c->n, c->sw[l], ld, c->lists[l], &dc->count[l], c->ioff, in_msg, memb, msg,
                            c->S[l], nullptr, dc);
+      add_launches(c, RIPPLE_PHASE_SCATTER, 1);
+    } else if (mode == kRecomputeLayer) {
+      // re-anchoring: every aggregate row of A^l summed afresh from the current
+      // source rows (the messages and the layer-0 corrections of these rows are
+      // superseded)
+      PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
+      rp::launch_recompute(s, c->n, c->sw[l], c->agg == rp::kGcn ? 1 : 0, c->lists[l], &dc->count[l], c->ioff,
+                           in_msg, c->adj[0].len, layer_ptrs(c).src[l], c->S[l], dc);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     {
@@ -1003,9 +1107,11 @@ ripple_status launch_batch(ripple_ctx *c) {
   const BatchPlan p = make_plan(c);
   c->last_pull = 0;
   c->last_dense = 0;
+  c->last_recompute = 0;
   for (int l = 1; l <= c->L; ++l) {
     if (p.mode[l] == kPullLayer) c->last_pull |= 1 << l;
     if (p.mode[l] == kDenseLayer) c->last_dense |= 1 << l;
+    if (p.mode[l] == kRecomputeLayer) c->last_recompute |= 1 << l;
   }
   c->run_app = p.app;
   c->last_graph = false;
@@ -1033,14 +1139,25 @@ void account_phases(ripple_ctx *c) {
   for (int l = 1; l <= c->L; ++l) {
     const double d = c->sw[l];
     const double nd = static_cast<double>(k.count[l - 1]);
-    c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * k.pushed[l] + 8.0 * nd + 4.0 * d * nd + 8.0 * d * k.dest[l];
-    // without on-chip reuse: a message row read per arc that carries it, and under
-    // push a row of atomics per arc rather than per sink
     const double per_arc = static_cast<double>(k.pushed[l]);
     const double sinks = static_cast<double>(k.dest[l]);
-    c->ph_extra[RIPPLE_PHASE_SCATTER] += 4.0 * d * std::max(per_arc - nd, 0.0);
-    if (!((c->last_pull | c->last_dense) >> l & 1))
-      c->ph_extra[RIPPLE_PHASE_SCATTER] += 8.0 * d * std::max(per_arc - sinks, 0.0);
+    if (c->last_recompute >> l & 1) {
+      // recompute: the marks (arc ids and row offsets of D), every in-arc id of A^l and
+      // its in-row offset, each source row read once (at most n of them) and each row
+      // of A^l written once; without reuse, a source row per in-arc
+      const double in_l = static_cast<double>(k.indeg[l]);
+      const double rows = std::min(in_l, static_cast<double>(c->n));
+      c->ph_bytes[RIPPLE_PHASE_SCATTER] +=
+          4.0 * per_arc + 8.0 * nd + 4.0 * in_l + 12.0 * k.count[l] + 4.0 * d * rows + 4.0 * d * k.count[l];
+      c->ph_extra[RIPPLE_PHASE_SCATTER] += 4.0 * d * (in_l - rows);
+    } else {
+      c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * per_arc + 8.0 * nd + 4.0 * d * nd + 8.0 * d * sinks;
+      // without on-chip reuse: a message row read per arc that carries it, and under
+      // push a row of atomics per arc rather than per sink
+      c->ph_extra[RIPPLE_PHASE_SCATTER] += 4.0 * d * std::max(per_arc - nd, 0.0);
+      if (!((c->last_pull | c->last_dense) >> l & 1))
+        c->ph_extra[RIPPLE_PHASE_SCATTER] += 8.0 * d * std::max(per_arc - sinks, 0.0);
+    }
     if (c->last_pull >> l & 1)  // pull: every in-arc id of A^l and its in-row offset
       c->ph_bytes[RIPPLE_PHASE_SCATTER] += 4.0 * k.indeg[l] + 12.0 * k.count[l];
     if (c->last_dense >> l & 1) {
@@ -1188,6 +1305,7 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
     }
   c->slack = g->slack;
   c->min_slack = g->min_slack;
+  if (const char *hook = std::getenv("RIPPLE_DEBUG_FAIL_BATCH")) c->debug_fail_batch = std::atoll(hook);
   c->device = g->device;
   c->max_bytes = g->max_device_bytes;
   c->arena_slots = g->arena_slots;
@@ -1311,6 +1429,8 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   if (e != hipSuccess) return bail(device_fail(c, e, "hipHostMalloc"));
   *c->h_in = rp::BatchIn{};
   std::vector<int> olen(outdeg), ilen(indeg);
+  c->snap_out = outdeg;
+  c->snap_in = indeg;
   // hubs of half the long-row length or more: their rows may need the chunked sweep
   const int max_len = std::max(olen.empty() ? 0 : *std::max_element(olen.begin(), olen.end()),
                                ilen.empty() ? 0 : *std::max_element(ilen.begin(), ilen.end()));
@@ -1433,6 +1553,7 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   RP_TRY(dalloc_n(c, &c->delta[0], n * rp::row_ld(c->dmax_delta)));
   RP_TRY(dalloc_n(c, &c->delta[1], n * rp::row_ld(c->dmax_delta)));
   RP_TRY(dalloc_n(c, &c->ioff, n + 1));
+  RP_TRY(dalloc_n(c, &c->flist_done, n));
   for (int k = 0; k < 2; ++k) {
     RP_TRY(dalloc_n(c, &c->memb[k], (n + 31) / 32));
   }
@@ -1464,6 +1585,7 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   RP_HIP(c, hipStreamSynchronize(c->stream));
   c->inited = true;
   c->has_batch = false;
+  c->batches_done = 0;
   return RIPPLE_OK;
 }
 
@@ -1481,6 +1603,19 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
   c->h_in->feat = src_feat;
   c->h_in->num_ops = B;
   c->h_in->num_feat_rows = num_feat_rows;
+  if (!c->has_batch) {
+    // the first batch's plan estimates its frontiers from its ops (see
+    // first_batch_counts): a batch in device memory is copied to host once
+    if (caller_ops == nullptr) {
+      c->plan_ops = src_ops;
+    } else {
+      c->plan_buf.resize(static_cast<size_t>(B));
+      if (B > 0)
+        RP_HIP(c, hipMemcpy(c->plan_buf.data(), caller_ops, static_cast<size_t>(B) * sizeof(ripple_op),
+                            hipMemcpyDeviceToHost));
+      c->plan_ops = c->plan_buf.data();
+    }
+  }
   for (int attempt = 0;; ++attempt) {
     RP_TRY(launch_batch(c));
     RP_TRY(wait_stream(c));
@@ -1520,11 +1655,12 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
     k.dest[l] = k.app_sinks[l] >> rp::kAppShift;
     k.indeg[l] = k.app_sinks[l] & rp::kAppMask;
   }
+  if (c->debug_fail_batch > 0 && ++c->batches_checked == c->debug_fail_batch) k.err |= 16ull;
   if (k.err) {
     c->poisoned = true;
     // bit 0: a net-deleted arc was not found; bit 1: a rewritten row's length did not
     // match; bit 2: the compaction's wait for a predecessor tile timed out; bit 3: a
-    // row move would have ended past the column buffer
+    // row move would have ended past the column buffer; bit 4: set by the test hook
     return fail(c, RIPPLE_E_DEVICE, "ripple: device-side check failed (err bits " + std::to_string(k.err) + ")");
   }
   c->last_app = c->run_app;  // the lists now hold this batch's sets
@@ -1535,6 +1671,8 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
   }
   account_phases(c);
   c->has_batch = true;
+  ++c->batches_done;
+  c->plan_ops = nullptr;
   c->last_nfeat = static_cast<long long>(k.n_feat);
   for (int l = 0; l <= c->L; ++l) {
     c->last_count[l] = static_cast<long long>(k.count[l]);
@@ -1562,6 +1700,7 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
     for (int l = 1; l <= c->L; ++l) stats->in_arcs[l] = static_cast<int64_t>(k.indeg[l]);
     stats->pull_layers = c->last_pull;
     stats->dense_layers = c->last_dense;
+    stats->recompute_layers = c->last_recompute;
     stats->graph_replay = c->last_graph ? 1 : 0;
     stats->long_rows = static_cast<int64_t>(k.long_rows >> 40);
   }
@@ -1660,7 +1799,7 @@ ripple_status ripple_get_affected(ripple_ctx *c, int32_t layer, int32_t *ids, in
     const long long nf = c->last_nfeat;
     std::vector<int> f(nf);
     if (nf > 0) {
-      RP_HIP(c, hipMemcpyAsync(f.data(), c->flist, nf * sizeof(int), hipMemcpyDeviceToHost, c->stream));
+      RP_HIP(c, hipMemcpyAsync(f.data(), c->flist_done, nf * sizeof(int), hipMemcpyDeviceToHost, c->stream));
       RP_HIP(c, hipStreamSynchronize(c->stream));
     }
     std::sort(f.begin(), f.end());
@@ -1748,8 +1887,15 @@ ripple_status ripple_get_arc_weights(ripple_ctx *c, int32_t direction, float *we
 
 ripple_status ripple_set_scatter_mode(ripple_ctx *c, int32_t mode) {
   RP_TRY(check_ctx(c));
-  if (mode < RIPPLE_SCATTER_AUTO || mode > RIPPLE_SCATTER_DENSE) return fail(c, RIPPLE_E_INVALID, "ripple: bad mode");
+  if (mode < RIPPLE_SCATTER_AUTO || mode > RIPPLE_SCATTER_RECOMPUTE) return fail(c, RIPPLE_E_INVALID, "ripple: bad mode");
   c->scatter_mode = mode;
+  return RIPPLE_OK;
+}
+
+ripple_status ripple_set_reanchor(ripple_ctx *c, int64_t every) {
+  RP_TRY(check_ctx(c));
+  if (every < 0) return fail(c, RIPPLE_E_INVALID, "ripple: every must be >= 0");
+  c->reanchor_every = every;
   return RIPPLE_OK;
 }
 

@@ -30,9 +30,9 @@ EXPORTED = [
     "ripple_get_affected", "ripple_get_aggregates", "ripple_get_arcs", "ripple_device_bytes",
     "ripple_set_profiling", "ripple_get_phase_stats", "ripple_phase_name", "ripple_last_error",
     "ripple_destroy", "ripple_set_scatter_mode", "ripple_apply_updates_device", "ripple_get_arc_weights",
-    "ripple_set_graphs",
+    "ripple_set_graphs", "ripple_set_reanchor",
 ]
-SCATTER = {"auto": 0, "push": 1, "pull": 2, "dense": 3}
+SCATTER = {"auto": 0, "push": 1, "pull": 2, "dense": 3, "recompute": 4}
 
 
 class RippleUnavailable(RuntimeError):
@@ -75,6 +75,7 @@ class BatchStats(C.Structure):
         ("relocated_rows", C.c_int64), ("repacks", C.c_int64),
         ("in_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("pull_layers", C.c_int32), ("dense_layers", C.c_int32),
         ("reweighted_arcs", C.c_int64), ("graph_replay", C.c_int64), ("long_rows", C.c_int64),
+        ("recompute_layers", C.c_int32), ("reserved", C.c_int32),
     ]
 
 
@@ -109,6 +110,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.ripple_set_profiling.argtypes = [vp, C.c_int32]
     lib.ripple_set_scatter_mode.argtypes = [vp, C.c_int32]
     lib.ripple_set_graphs.argtypes = [vp, C.c_int32]
+    lib.ripple_set_reanchor.argtypes = [vp, C.c_int64]
     lib.ripple_get_phase_stats.argtypes = [vp, P(PhaseStats), C.c_int32]
     lib.ripple_phase_name.argtypes = [C.c_int32]
     lib.ripple_phase_name.restype = C.c_char_p
@@ -257,6 +259,7 @@ class Ripple:
             "relocated_rows": st.relocated_rows, "repacks": st.repacks,
             "in_arcs": list(st.in_arcs[:L + 1]), "pull_layers": st.pull_layers, "dense_layers": st.dense_layers,
             "reweighted_arcs": st.reweighted_arcs, "graph_replay": st.graph_replay, "long_rows": st.long_rows,
+            "recompute_layers": st.recompute_layers,
         }
 
     def apply_updates_raw(self, ops: np.ndarray, feat_rows: Optional[np.ndarray], stats: BatchStats) -> None:
@@ -328,8 +331,13 @@ class Ripple:
         return w
 
     def set_scatter_mode(self, mode: str):
-        """"auto" (default), "push", "pull" or "dense": how layers add their messages."""
+        """"auto" (default), "push", "pull", "dense" or "recompute": how layers update
+        their cached aggregates."""
         self._check(self._lib.ripple_set_scatter_mode(self._ctx, SCATTER[mode]))
+
+    def set_reanchor(self, every: int):
+        """Every `every`-th batch recomputes the affected aggregate rows afresh (0: never)."""
+        self._check(self._lib.ripple_set_reanchor(self._ctx, int(every)))
 
     def set_graphs(self, enable: bool):
         """True: batches replay captured HIP graphs; False (default): kernels are queued one by one."""

@@ -53,7 +53,16 @@ def _hip():
         _HIP.hipFree.argtypes = [C.c_void_p]
         _HIP.hipStreamCreateWithFlags.argtypes = [C.POINTER(C.c_void_p), C.c_uint]
         _HIP.hipStreamDestroy.argtypes = [C.c_void_p]
+        _HIP.hipMemGetInfo.argtypes = [C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)]
     return _HIP
+
+
+def device_free_bytes() -> int:
+    """Free device memory on the current device (hipMemGetInfo)."""
+    free, total = C.c_size_t(), C.c_size_t()
+    if _hip().hipMemGetInfo(C.byref(free), C.byref(total)) != 0:
+        raise RuntimeError("hipMemGetInfo failed")
+    return free.value
 
 
 class CallerStream:
@@ -210,3 +219,65 @@ def random_valid_batch(rng, orc: O.OracleState, bs: int, d0: int, mix=(1 / 3, 1 
             nfeat += 1
     feats = rng.standard_normal((nfeat, d0), dtype=np.float32)
     return synth.Batch(ops, feats)
+
+
+def fp32_forward_bound(orc: O.OracleState, ref, l: int) -> np.ndarray:
+    """Per row v of layer l: the forward error bound of evaluating the layer in fp32
+    from exact inputs, 2 (K + 16) 2^-24 max_k B_vk, where B_vk sums the magnitudes
+    of every term of output k's pre-activation (|W_self| |h_v| + |W_neigh| sum_u
+    |c_uv h_u| + |b|) and K is the length of the row's dot products. For GraphSAGE
+    (sum, mean) and GCN models."""
+    m = orc.model
+    habs = np.abs(ref[l - 1])
+    aabs = O.aggregate(orc.graph, habs, m.agg)  # the coefficients are non-negative
+    b = aabs @ np.abs(m.w_neigh[l - 1]).T + np.abs(m.bias[l - 1])
+    k = m.w_neigh[l - 1].shape[1]
+    if m.w_self[l - 1] is not None:
+        b = b + habs @ np.abs(m.w_self[l - 1]).T
+        k *= 2
+    return 2.0 * (k + 16) * 2.0 ** -24 * np.max(b, axis=1)
+
+
+def check_embeddings_conditioned(pair: "Pair", tol=FP32_TOL):
+    """Every row of every layer meets R16 (max row-relative error tol, floor 1e-3
+    RMS), or, where R16 asks for more than fp32 resolves (a row whose pre-activation
+    cancels to far below the magnitude of its terms), lies within the fp32 forward
+    error bound of its layer (fp32_forward_bound). Returns per layer (max R16
+    error, rows that needed the bound)."""
+    ref = pair.orc.embeddings()
+    out = []
+    for l in range(1, pair.L + 1):
+        got = pair.lib.get_embeddings(l).astype(np.float64)
+        diff = np.max(np.abs(got - ref[l]), axis=1)
+        floor = 1e-3 * float(np.sqrt(np.mean(ref[l] * ref[l])))
+        r16 = diff / np.maximum(np.max(np.abs(ref[l]), axis=1), floor)
+        bound = fp32_forward_bound(pair.orc, ref, l)
+        over = np.flatnonzero(r16 > tol)
+        bad = over[diff[over] > bound[over]]
+        assert bad.size == 0, (l, bad[:5], r16[bad[:5]], diff[bad[:5]], bound[bad[:5]])
+        out.append((float(r16.max()), int(over.size)))
+    return out
+
+
+def aggregate_drift_ulps(pair: "Pair", rows) -> list:
+    """How far the cached aggregate rows S^l_v of `rows` are from their definition
+    sum_u c_u h*_u (float64, on the oracle's embeddings), in units of 2^-24 times the
+    magnitude of the sum's terms, max_k sum_u |c_u h*_uk|: a fresh fp32 sum of the
+    row is within about its in-degree of these units, and every message added since
+    the row was last summed afresh can add half a unit. Per layer, the worst row."""
+    ref = pair.orc.embeddings()
+    g = pair.orc.graph
+    c = np.ones(pair.n)
+    if pair.orc.model.agg == "gcn":
+        c = 1.0 / np.sqrt(g.out_degree() + 1.0)
+    u, _ = g.arcs()
+    a = g.in_adjacency(weights=c[u] * (g.w if pair.orc.model.agg == "gc_wsum" else 1.0))
+    rows = np.asarray(rows, np.int64)
+    out = []
+    for l in range(1, pair.L + 1):
+        want = (a @ ref[l - 1])[rows]
+        mag = np.max((abs(a) @ np.abs(ref[l - 1]))[rows], axis=1)
+        got = pair.lib.get_aggregates(l, rows.astype(np.int32)).astype(np.float64)
+        err = np.max(np.abs(got - want), axis=1)
+        out.append(float(np.max(err / (np.maximum(mag, 1e-300) * 2.0 ** -24))))
+    return out

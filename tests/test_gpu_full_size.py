@@ -82,9 +82,11 @@ def test_sparse_mid_mean_thousand_batches():
         p.close()
 
 
-def _sample_vertices(rng, orc, affected, k, max_reach):
+def _sample_vertices(rng, orc, affected, k, max_reach, hubs=16):
     """Up to k affected and k other vertices whose two-hop in-neighbourhood (in arcs)
-    stays below max_reach, so the oracle can evaluate them one by one."""
+    stays below max_reach, so the oracle can evaluate them one by one, plus the
+    `hubs` vertices of highest in-degree whatever their reach (the rows that receive
+    the most messages, and so the most rounding)."""
     src_s, dst_s = orc.graph.in_sorted()
     indeg = np.bincount(dst_s, minlength=orc.graph.n)
     picked = []
@@ -99,7 +101,8 @@ def _sample_vertices(rng, orc, affected, k, max_reach):
                 got += 1
                 if got == k:
                     break
-    return np.unique(np.array(picked, np.int64))
+    top = np.argsort(indeg, kind="stable")[-hubs:] if hubs else np.zeros(0, np.int64)
+    return np.unique(np.concatenate([np.array(picked, np.int64), top.astype(np.int64)])), top
 
 
 def _check_sampled(p, verts, layers, tol=1e-4):
@@ -114,34 +117,42 @@ def _check_sampled(p, verts, layers, tol=1e-4):
     return errs
 
 
-def test_dense_large_full_size():
+@pytest.mark.parametrize("config,bs,nb", [("dense_large", 100, 3), ("dense_large", 1000, 2),
+                                          ("dense_large_2l", 100, 3), ("dense_large_2l", 1000, 2)])
+def test_dense_large_full_size(config, bs, nb):
     """Products-shaped undirected graph at full size (2,449,029 vertices, 61,859,140
-    edges, GraphSAGE-sum 100-256-256-47): three batches of 100 with affected sets
-    compared bit for bit, then embeddings of sampled vertices at every layer."""
+    edges), GraphSAGE-sum 100-256-256-47 or 100-256-47, message forms chosen by the
+    library as bench.py runs it: batches of 100 or 1000 with affected sets compared
+    bit for bit, then embeddings of sampled vertices (the 16 highest in-degrees
+    among them) at every layer."""
     t0 = time.time()
-    wl = synth.build_workload("dense_large")
-    _say(f"dense_large generated in {time.time() - t0:.0f}s")
+    wl = synth.build_workload(config)
+    _say(f"{config} bs={bs} generated in {time.time() - t0:.0f}s")
     p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, undirected=True)
+    L = len(wl.weights.dims) - 1
     try:
         _say(f"  loaded + bootstrapped, oracle built ({time.time() - t0:.0f}s)")
-        rng = np.random.default_rng(5)
-        for b in range(3):
-            st, _, sets = p.step(wl.stream.next_batch(100))
+        rng = np.random.default_rng(5 + bs)
+        for b in range(nb):
+            st, _, sets = p.step(wl.stream.next_batch(bs))
             _say(f"  batch {b}: |A| = {[s.size for s in sets]}, pull layers {st['pull_layers']:b}, "
                  f"dense layers {st['dense_layers']:b} ({time.time() - t0:.0f}s)")
-        assert (st["pull_layers"] | st["dense_layers"]) & 0b1000, "the third layer should switch to a pull form"
-        verts = _sample_vertices(rng, p.orc, sets[3], 24, 400_000)
-        errs = _check_sampled(p, verts, (1, 2, 3))
-        _say(f"  {verts.size} sampled vertices, row-relative errors {errs} ({time.time() - t0:.0f}s)")
+        if config == "dense_large" and bs == 100:
+            assert (st["pull_layers"] | st["dense_layers"]) & 0b1000, "the third layer should switch to a pull form"
+        verts, hubs = _sample_vertices(rng, p.orc, sets[L], 24, 400_000)
+        errs = _check_sampled(p, verts, range(1, L + 1))
+        _say(f"  {verts.size} sampled vertices (hub in-degrees {np.bincount(p.orc.graph.in_sorted()[1], minlength=wl.n)[hubs][-3:]}), "
+             f"row-relative errors {errs} ({time.time() - t0:.0f}s)")
     finally:
         p.close()
 
 
-@pytest.mark.parametrize("mode", ["pull", "dense"])
+@pytest.mark.parametrize("mode", ["auto", "pull", "dense"])
 def test_stress_full_size(mode):
     """RMAT graph at full size (2^23 vertices, 200M arcs, GCN 64-256-64), one
-    hub-biased batch of 10,000 ops: affected sets bit for bit, embeddings of
-    sampled vertices at both layers."""
+    hub-biased batch of 10,000 ops, with the message forms the library chooses
+    (as bench.py runs it) or forced: affected sets bit for bit, embeddings of
+    sampled vertices (the 16 highest in-degrees among them) at both layers."""
     t0 = time.time()
     wl = synth.build_workload("stress")
     _say(f"stress generated in {time.time() - t0:.0f}s ({mode})")
@@ -149,10 +160,12 @@ def test_stress_full_size(mode):
     try:
         _say(f"  loaded + bootstrapped, oracle built ({time.time() - t0:.0f}s)")
         st, _, sets = p.step(wl.stream.next_batch(10_000))
-        assert st["pull_layers" if mode == "pull" else "dense_layers"] == 0b110
-        _say(f"  batch: |A| = {[s.size for s in sets]}, pushed {st['pushed_arcs']} ({time.time() - t0:.0f}s)")
+        if mode != "auto":
+            assert st["pull_layers" if mode == "pull" else "dense_layers"] == 0b110
+        _say(f"  batch: |A| = {[s.size for s in sets]}, pushed {st['pushed_arcs']}, pull {st['pull_layers']:b}, "
+             f"dense {st['dense_layers']:b} ({time.time() - t0:.0f}s)")
         rng = np.random.default_rng(6)
-        verts = _sample_vertices(rng, p.orc, sets[2], 24, 2_000_000)
+        verts, _ = _sample_vertices(rng, p.orc, sets[2], 24, 2_000_000)
         errs = _check_sampled(p, verts, (1, 2))
         _say(f"  {verts.size} sampled vertices, row-relative errors {errs} ({time.time() - t0:.0f}s)")
     finally:
