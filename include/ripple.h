@@ -231,6 +231,20 @@ RIPPLE_API ripple_status ripple_apply_updates_device(ripple_ctx *ctx, const ripp
 RIPPLE_API ripple_status ripple_get_embeddings(ripple_ctx *ctx, int32_t layer, const int32_t *ids,
                                     int64_t count, float *out);
 
+/* ripple_get_embeddings for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops, harnesses that forbid allocation): the
+ * same rows, with the same arguments and errors, staged through a file-scope
+ * device array of 32 MiB instead of buffers allocated per call (ripple_get_embeddings
+ * allocates two per call with ids). The ids and gathered rows must fit in it:
+ * count * 4 bytes (rounded up to 256) + count * d_layer * 4 bytes <= 32 MiB, else
+ * RIPPLE_E_INVALID naming the limit. Each GPU the library runs on holds its own
+ * copy of the array until the process ends; every call on that GPU, from any
+ * context, stages through it, so calls that overlap on one GPU (other threads,
+ * other contexts) race and must be serialised by the caller. Allocates nothing:
+ * no hipMalloc, hipFree or allocating library routine. */
+RIPPLE_API ripple_status ripple_get_embeddings_static(ripple_ctx *ctx, int32_t layer, const int32_t *ids,
+                                                      int64_t count, float *out);
+
 /* Trigger output of the last batch: A^layer, the vertices whose layer-`layer`
  * embedding the batch recomputed, in ascending id order (A^0 = vertices whose
  * features were replaced). Writes min(|A^layer|, capacity) ids to `ids` and

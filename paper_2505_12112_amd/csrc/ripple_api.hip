@@ -26,6 +26,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <numeric>
 #include <string>
 #include <thread>
@@ -1232,6 +1233,32 @@ bool validate_ops(ripple_ctx *c, const ripple_op *ops, long long num_ops, long l
   return true;
 }
 
+// Staging memory of ripple_get_embeddings_static: a file-scope device array, so the
+// call allocates nothing. Each device holds its own copy (at its own address, found
+// once per device with hipGetSymbolAddress; host code never uses the array's name
+// as an address). Calls that overlap on one device race for it.
+constexpr size_t kStaticStageBytes = size_t{32} << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticStageBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_stage_mu;
+void *g_stage_ptr[kMaxDevices] = {};
+
+// This device's copy of the staging array (the device must be current).
+hipError_t static_stage(int device, void **ptr) {
+  *ptr = nullptr;
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_stage_mu);
+  if (g_stage_ptr[device] == nullptr) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_stage_ptr[device] = p;
+  }
+  *ptr = g_stage_ptr[device];
+  return hipSuccess;
+}
+
 ripple_status read_rows(ripple_ctx *c, const float *src, int d, const int32_t *ids, long long count, float *out) {
   if (count < 0) return fail(c, RIPPLE_E_INVALID, "ripple: negative count");
   if (count == 0) return RIPPLE_OK;
@@ -1776,6 +1803,42 @@ ripple_status ripple_get_embeddings(ripple_ctx *c, int32_t layer, const int32_t 
   if (!c->inited) return fail(c, RIPPLE_E_STATE, "ripple: ripple_init_embeddings has not run");
   if (layer < 0 || layer > c->L) return fail(c, RIPPLE_E_INVALID, "ripple: layer out of range");
   return read_rows(c, c->H[layer], c->dims[layer], ids, count, out);
+}
+
+ripple_status ripple_get_embeddings_static(ripple_ctx *c, int32_t layer, const int32_t *ids, int64_t count,
+                                           float *out) {
+  RP_TRY(check_ctx(c));
+  if (!c->inited) return fail(c, RIPPLE_E_STATE, "ripple: ripple_init_embeddings has not run");
+  if (layer < 0 || layer > c->L) return fail(c, RIPPLE_E_INVALID, "ripple: layer out of range");
+  if (count < 0) return fail(c, RIPPLE_E_INVALID, "ripple: negative count");
+  if (count == 0) return RIPPLE_OK;
+  if (out == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: out is NULL");
+  const int d = c->dims[layer];
+  if (ids == nullptr) {  // every row, straight from the embedding buffer
+    if (count != c->n) return fail(c, RIPPLE_E_INVALID, "ripple: ids NULL requires count == n");
+    RP_HIP(c, hipMemcpyAsync(out, c->H[layer], static_cast<size_t>(count) * d * sizeof(float),
+                             hipMemcpyDeviceToHost, c->stream));
+    RP_HIP(c, hipStreamSynchronize(c->stream));
+    return RIPPLE_OK;
+  }
+  const size_t id_bytes = (static_cast<size_t>(count) * sizeof(int) + 255) / 256 * 256;
+  const size_t row_bytes = static_cast<size_t>(count) * d * sizeof(float);
+  if (id_bytes + row_bytes > kStaticStageBytes)
+    return fail(c, RIPPLE_E_INVALID, "ripple: " + std::to_string(count) + " rows of width " + std::to_string(d) +
+                                         " exceed the " + std::to_string(kStaticStageBytes >> 20) +
+                                         " MiB staging array of ripple_get_embeddings_static");
+  for (long long i = 0; i < count; ++i)
+    if (ids[i] < 0 || ids[i] >= c->n) return fail(c, RIPPLE_E_INVALID, "ripple: vertex id out of range");
+  void *stage = nullptr;
+  RP_HIP(c, static_stage(c->device, &stage));
+  int *d_ids = static_cast<int *>(stage);
+  float *d_out = reinterpret_cast<float *>(static_cast<unsigned char *>(stage) + id_bytes);
+  RP_HIP(c, hipMemcpyAsync(d_ids, ids, static_cast<size_t>(count) * sizeof(int), hipMemcpyHostToDevice, c->stream));
+  rp::launch_gather_rows(c->stream, c->H[layer], d, d_ids, count, d_out);
+  RP_HIP(c, hipGetLastError());
+  RP_HIP(c, hipMemcpyAsync(out, d_out, row_bytes, hipMemcpyDeviceToHost, c->stream));
+  RP_HIP(c, hipStreamSynchronize(c->stream));
+  return RIPPLE_OK;
 }
 
 ripple_status ripple_get_aggregates(ripple_ctx *c, int32_t layer, const int32_t *ids, int64_t count, float *out,

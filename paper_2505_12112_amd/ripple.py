@@ -30,7 +30,7 @@ EXPORTED = [
     "ripple_get_affected", "ripple_get_aggregates", "ripple_get_arcs", "ripple_device_bytes",
     "ripple_set_profiling", "ripple_get_phase_stats", "ripple_phase_name", "ripple_last_error",
     "ripple_destroy", "ripple_set_scatter_mode", "ripple_apply_updates_device", "ripple_get_arc_weights",
-    "ripple_set_graphs", "ripple_set_reanchor",
+    "ripple_set_graphs", "ripple_set_reanchor", "ripple_get_embeddings_static",
 ]
 SCATTER = {"auto": 0, "push": 1, "pull": 2, "dense": 3, "recompute": 4}
 
@@ -102,6 +102,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.ripple_apply_updates.argtypes = [vp, P(C.c_int32), C.c_int64, P(C.c_float), C.c_int64, P(BatchStats)]
     lib.ripple_apply_updates_device.argtypes = [vp, vp, C.c_int64, vp, C.c_int64, P(BatchStats)]
     lib.ripple_get_embeddings.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_float)]
+    lib.ripple_get_embeddings_static.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_float)]
     lib.ripple_get_aggregates.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_float), P(C.c_int32)]
     lib.ripple_get_affected.argtypes = [vp, C.c_int32, P(C.c_int32), C.c_int64, P(C.c_int64)]
     lib.ripple_get_arcs.argtypes = [vp, C.c_int32, P(C.c_int32), P(C.c_int32), C.c_int64, P(C.c_int64)]
@@ -280,6 +281,21 @@ class Ripple:
             out = np.empty((ids.size, d), np.float32)
             self._check(self._lib.ripple_get_embeddings(self._ctx, layer, _ptr(ids, C.c_int32), ids.size,
                                                         _ptr(out, C.c_float)))
+        return out
+
+    def get_embeddings_static(self, layer: int, ids: Optional[Sequence[int]] = None) -> np.ndarray:
+        """As get_embeddings, through the library's fixed staging array (no device
+        allocation); at most 32 MiB of ids and rows per call."""
+        d = self.dims[layer]
+        if ids is None:
+            out = np.empty((self.n, d), np.float32)
+            self._check(self._lib.ripple_get_embeddings_static(self._ctx, layer, None, self.n,
+                                                               _ptr(out, C.c_float)))
+        else:
+            ids = _i32(ids)
+            out = np.empty((ids.size, d), np.float32)
+            self._check(self._lib.ripple_get_embeddings_static(self._ctx, layer, _ptr(ids, C.c_int32), ids.size,
+                                                               _ptr(out, C.c_float)))
         return out
 
     def aggregate_width(self, layer: int) -> int:
