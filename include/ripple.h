@@ -300,7 +300,7 @@ RIPPLE_API ripple_status ripple_set_scatter_mode(ripple_ctx *ctx, int32_t mode);
  * row every time they reach it; with every = k >= 1, every k-th batch (counted
  * from ripple_init_embeddings) runs each layer in the RIPPLE_SCATTER_RECOMPUTE
  * form, whatever form ripple_set_scatter_mode asks for, so every row that batch
- * affects is recomputed afresh. every = 0: never. Default 64. RIPPLE_E_INVALID
+ * affects is recomputed afresh. every = 0: never. Default 256. RIPPLE_E_INVALID
  * for every < 0. */
 RIPPLE_API ripple_status ripple_set_reanchor(ripple_ctx *ctx, int64_t every);
 
@@ -320,12 +320,16 @@ RIPPLE_API ripple_status ripple_set_graphs(ripple_ctx *ctx, int32_t enable);
 RIPPLE_API ripple_status ripple_device_bytes(ripple_ctx *ctx, int64_t *bytes);
 
 /* Kernel timing (for measurement). ripple_set_profiling(ctx, mask) makes every
- * later ripple_apply_updates record a HIP event pair on the context's stream
- * around each kernel phase p whose bit (1 << p) is set in mask (bit
- * RIPPLE_PHASE_TOTAL: first to last kernel of the batch); mask 0 stops recording.
- * Per phase the library accumulates event milliseconds, kernel launches, and the
- * phase's algorithmic HBM bytes and flops computed from the batch's own counts
- * (each input row read once, each output row written once):
+ * later ripple_apply_updates time each kernel of each phase p whose bit (1 << p)
+ * is set in mask: the kernel is launched with a start / stop event pair that takes
+ * its own start and end (hipExtLaunchKernelGGL), so the times are kernel
+ * durations as a profiler's kernel trace gives them, without the dispatch gaps
+ * between kernels. Bit RIPPLE_PHASE_TOTAL instead brackets the whole batch with
+ * an event pair on the context's stream (first to last kernel, gaps included).
+ * mask 0 stops recording; batches that record run kernel by kernel, never as
+ * graph replays. Per phase the library accumulates the milliseconds, kernel
+ * launches, and the phase's algorithmic HBM bytes and flops computed from the
+ * batch's own counts (each input row read once, each output row written once):
  *   SCATTER, per layer l with dirty set D, pushed arcs E_D, distinct sinks R,
  *            width d = d_{l-1}:  4 E_D + 8 |D| + 4 d |D| + 8 d R  bytes
  *   GEMM,    per layer l with |A^l| rows, K = 2 d_{l-1} (SAGE) or d_{l-1} (GCN),

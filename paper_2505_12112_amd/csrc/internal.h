@@ -12,12 +12,30 @@
 //   delta[2] ping-pong [n][max d] rows of c'_u h'_u - c_u h_u aligned with lists[l].
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "ripple.h"
 
 namespace rp {
+
+// Kernel timing for measurement (ripple_set_profiling). While a batch records the
+// kernels of a phase, launch_timer hands out a fresh start / stop event pair for
+// each launch (and counts it for that phase), and the launch goes through
+// hipExtLaunchKernelGGL, whose events take the kernel's own start and end, as a
+// profiler's kernel trace does, without the dispatch gap before it. Otherwise it
+// returns false and the launch is a plain one.
+bool launch_timer(hipEvent_t *start, hipEvent_t *stop);
+
+#define RP_LAUNCH(K, G, B, SHM, S, ...)                                        \
+  do {                                                                         \
+    hipEvent_t rp_ev_a_, rp_ev_b_;                                             \
+    if (::rp::launch_timer(&rp_ev_a_, &rp_ev_b_))                              \
+      hipExtLaunchKernelGGL(K, G, B, SHM, S, rp_ev_a_, rp_ev_b_, 0, __VA_ARGS__); \
+    else                                                                       \
+      hipLaunchKernelGGL(K, G, B, SHM, S, __VA_ARGS__);                        \
+  } while (0)
 
 constexpr int kWave = 64;
 constexpr int kMaxL = RIPPLE_MAX_LAYERS;
@@ -330,7 +348,7 @@ struct CompactOut {
 };
 // The recompute form (launch_recompute) sums an in-row of more than kRecomputeSeg
 // arcs in segments of that many, each added to the row with fp32 atomics.
-constexpr int kRecomputeSeg = 256;
+constexpr int kRecomputeSeg = 64;
 // Tile sums published by the single-pass compaction: compact_scratch_words(n)
 // words, zero when first used, then owned by the compactions of one vertex count
 // (each launch finds its epoch from a ticket counter kept there).

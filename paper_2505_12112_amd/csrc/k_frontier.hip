@@ -324,6 +324,10 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
   __shared__ long long red[kCompactWaves][kVals];
   __shared__ long long base_s[kVals];
   __shared__ u64 epoch_s, ticket_s;
+  constexpr int kZeroList = 1024;  // long rows a tile zeroes cooperatively (more: by their own thread)
+  __shared__ int zlist[kZeroList];
+  __shared__ int zcount;
+  if (threadIdx.x == 0) zcount = 0;  // published by the scan's barriers
   const long long tiles = gridDim.x;
   // Up to kIndexTiles tiles all fit on the GPU at once, so block b takes tile b and
   // its ticket (for the epoch) is in flight beside the bitmap loads. Beyond that,
@@ -484,10 +488,24 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
         ipos += iv[j];
       }
       if (o.zero_rows != nullptr && iv[j] > kRecomputeSeg) {  // summed in segments by the recompute
-        float *r = o.zero_rows + static_cast<long long>(v[j]) * o.zero_w;
-        for (int k = 0; k < o.zero_w; ++k) r[k] = 0.f;
+        const int slot = atomicAdd(&zcount, 1);
+        if (slot < kZeroList) {
+          zlist[slot] = v[j];  // zeroed by the whole block below
+        } else {
+          float *r = o.zero_rows + static_cast<long long>(v[j]) * o.zero_w;
+          for (int k = 0; k < o.zero_w; ++k) r[k] = 0.f;
+        }
       }
       ++pos;
+    }
+  }
+  if (o.zero_rows != nullptr) {
+    // the tile's long rows, a wave per row and a lane per element
+    __syncthreads();
+    const int nz = zcount < kZeroList ? zcount : kZeroList;
+    for (int r = threadIdx.x / kWave; r < nz; r += kCompactWaves) {
+      float *row = o.zero_rows + static_cast<long long>(zlist[r]) * o.zero_w;
+      for (int k = lane_id(); k < o.zero_w; k += kWave) row[k] = 0.f;
     }
   }
 #pragma unroll
@@ -957,14 +975,18 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
         jj[t] = pr.y;
         wt[t] = pw;
       }
+      // unconditional loads (an empty slot reads message row 0, a column past the
+      // end the last column) masked to zero afterwards: no branch between the
+      // loads (columns past the end are summed but never flushed)
       float row[U][NC];
 #pragma unroll
       for (int t = 0; t < U; ++t) {
-        const float *mj = msg + static_cast<long long>(jj[t]) * ld;
+        const float *mj = msg + static_cast<long long>(jj[t] >= 0 ? jj[t] : 0) * ld;
+        const unsigned keep = jj[t] >= 0 ? ~0u : 0u;
 #pragma unroll
         for (int q = 0; q < NC; ++q) {
           const int k = k0 + q * G;
-          row[t][q] = jj[t] >= 0 && k < d ? mj[k] : 0.0f;
+          row[t][q] = __uint_as_float(__float_as_uint(mj[k < d ? k : d - 1]) & keep);
         }
       }
 #pragma unroll
@@ -1011,17 +1033,20 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
 // sink's own arcs from ioff_j + s kRecomputeSeg on. So a range owns segment 0 of
 // the sinks that start in it (with C <= kRecomputeSeg no other segment of those),
 // and at most one later segment of the sink that covers its first arc. The
-// range's segments go round-robin to the wave's G-lane groups; a group walks its
-// segment U arcs at a time (one lane per arc fetches the source id, coefficient
-// and weight, then the G lanes fetch the U source rows), summing in fp64. A sink
-// of one segment is stored once, rounded to fp32; the segments of longer sinks
-// are added with fp32 atomics into rows the compaction zeroed. The last range
-// also owns the sinks past the last arc (rows without in-arcs, stored as zeros).
+// range's segments go round-robin to the wave's G-lane groups. A group fetches
+// its segment's source ids, weights and coefficients in one round (each lane
+// kRecomputeSeg / G arcs), then its source rows U at a time, summing in fp64. A
+// sink of one segment is stored once, rounded to fp32; the segments of longer
+// sinks are added with fp32 atomics into rows the compaction zeroed. The last
+// range also owns the sinks past the last arc (rows without in-arcs, stored as
+// zeros).
 template <int G, int NC, int U>
 __global__ __launch_bounds__(256) void k_recompute(int d, int gcn, const int *list, const u64 *count,
                                                    const long long *ioff, Adj in, const int *out_len,
                                                    const float *src, float *S, const Counters *c) {
-  static_assert(U <= G, "one lane per arc of a step");
+  static_assert(G % U == 0 && kRecomputeSeg % G == 0, "steps of U arcs stay within one fetch slot");
+  constexpr int kPer = kRecomputeSeg / G;  // arcs fetched per lane
+  constexpr int kSteps = kRecomputeSeg / U;
   const long long nA = static_cast<long long>(*count);
   if (aborted_with(c->abort, nA)) return;
   const int lane = lane_id();
@@ -1078,48 +1103,64 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int gcn, const int *li
         a1 = whole ? b : a + kRecomputeSeg;
       }
       const int v = list != nullptr ? list[j] : static_cast<int>(j);
-      const long long row0 = in.off[v] - ioff[j];  // slot of arc number e is row0 + e
+      const long long row0 = in.off[v] - ioff[j] + a0;  // slot of the segment's first arc
+      const int na = static_cast<int>(a1 - a0);         // arcs in the segment (<= kRecomputeSeg)
+      // arc i of the segment is fetched by lane i % G of the group, into slot i / G
+      int uq[kPer];
+      double cq[kPer];
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const int i = k0 + q * G;
+        uq[q] = i < na ? in.col[row0 + i] : -1;
+        cq[q] = i < na && weighted ? static_cast<double>(in.wt[row0 + i]) : 1.0;
+      }
+      if (gcn) {
+#pragma unroll
+        for (int q = 0; q < kPer; ++q)
+          if (uq[q] >= 0) cq[q] /= sqrt(static_cast<double>(out_len[uq[q]]) + 1.0);
+      }
       double acc[NC];
 #pragma unroll
       for (int q = 0; q < NC; ++q) acc[q] = 0.0;
-      for (long long e0 = a0; e0 < a1; e0 += U) {
-        int ul = -1;
-        double cl = 0.0;
-        if (k0 < U && e0 + k0 < a1) {
-          const long long slot = row0 + e0 + k0;
-          ul = in.col[slot];
-          cl = weighted ? static_cast<double>(in.wt[slot]) : 1.0;
-        }
-        if (gcn && ul >= 0) cl /= sqrt(static_cast<double>(out_len[ul]) + 1.0);
+#pragma unroll
+      for (int st = 0; st < kSteps; ++st) {
+        if (st * U >= na) break;  // the same for the group's lanes
+        const int q = st * U / G;  // the fetch slot of this step's arcs
         int uu[U];
         double cc[U];
 #pragma unroll
         for (int t = 0; t < U; ++t) {
-          uu[t] = __shfl(ul, grp * G + t);
-          cc[t] = __shfl(cl, grp * G + t);
+          const int from = grp * G + (st * U + t) % G;
+          uu[t] = __shfl(uq[q], from);
+          cc[t] = __shfl(cq[q], from);
         }
+        // every lane loads (an empty slot reads row 0, a column past the end the
+        // last column) and the value is masked to zero afterwards: the loads carry
+        // no branch and are all in flight together (columns past the end are
+        // summed but never stored)
         float row[U][NC];
 #pragma unroll
         for (int t = 0; t < U; ++t) {
           const float *su = src + static_cast<long long>(uu[t] >= 0 ? uu[t] : 0) * d;
+          const unsigned keep = uu[t] >= 0 ? ~0u : 0u;
 #pragma unroll
-          for (int q = 0; q < NC; ++q) {
-            const int k = k0 + q * G;
-            row[t][q] = uu[t] >= 0 && k < d ? su[k] : 0.f;
+          for (int p = 0; p < NC; ++p) {
+            const int k = k0 + p * G;
+            row[t][p] = __uint_as_float(__float_as_uint(su[k < d ? k : d - 1]) & keep);
           }
         }
 #pragma unroll
         for (int t = 0; t < U; ++t)
 #pragma unroll
-          for (int q = 0; q < NC; ++q) acc[q] += cc[t] * static_cast<double>(row[t][q]);
+          for (int p = 0; p < NC; ++p) acc[p] += cc[t] * static_cast<double>(row[t][p]);
       }
       float *sv = S + static_cast<long long>(v) * d;
 #pragma unroll
-      for (int q = 0; q < NC; ++q) {
-        const int k = k0 + q * G;
+      for (int p = 0; p < NC; ++p) {
+        const int k = k0 + p * G;
         if (k < d) {
-          if (whole) sv[k] = static_cast<float>(acc[q]);
-          else unsafeAtomicAdd(&sv[k], static_cast<float>(acc[q]));
+          if (whole) sv[k] = static_cast<float>(acc[p]);
+          else unsafeAtomicAdd(&sv[k], static_cast<float>(acc[p]));
         }
       }
     }
@@ -1194,7 +1235,7 @@ void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerP
   const long long waves = 2LL * cap_arcs * lp.L;
   const long long threads = static_cast<long long>(cap_feat) + 2LL * cap_arcs;
   const long long items = waves * kWave > threads ? waves * kWave : threads;
-  hipLaunchKernelGGL(k_corr_mark, dim3(blocks_for(items, 256)), dim3(256), 0, s, agg, lp, out, in, ins_rank, arc_w,
+  RP_LAUNCH(k_corr_mark, dim3(blocks_for(items, 256)), dim3(256), 0, s, agg, lp, out, in, ins_rank, arc_w,
                      ddeg, flist, ins_src, ins_dst, del_src, del_dst, ins_w, del_w, bm, c, direct);
 }
 
@@ -1207,12 +1248,12 @@ void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, 
                     const CompactOut &o) {
   const long long words = (n + 31) / 32;
   const int tiles = compact_blocks(n);
-  hipLaunchKernelGGL(k_compact, dim3(tiles), dim3(kCompactThreads), 0, s, bm_a, bm_b, words, o, cs.words,
+  RP_LAUNCH(k_compact, dim3(tiles), dim3(kCompactThreads), 0, s, bm_a, bm_b, words, o, cs.words,
                      cs.words + static_cast<long long>(tiles) * kVals, cs.words + 2LL * tiles * kVals, cs.err);
 }
 
 void launch_delta0(hipStream_t s, long long n, const Delta0Args &z, const int *list, const u64 *count) {
-  hipLaunchKernelGGL(k_delta0, dim3(blocks_for(n * kWave, 256, 2048)), dim3(256), 0, s, z, list, count, n);
+  RP_LAUNCH(k_delta0, dim3(blocks_for(n * kWave, 256, 2048)), dim3(256), 0, s, z, list, count, n);
 }
 
 long long compact_scratch_words(long long n) { return 2LL * compact_blocks(n) * kVals + 1; }
@@ -1223,7 +1264,7 @@ void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, 
                     const ScatterCopy &copy, const ScatterList &lo, bool packed_in) {
   const int blocks = 2048;
 #define RP_SCATTER_L(GV, NCV, P, LV)                                                                               \
-  hipLaunchKernelGGL((k_scatter<GV, NCV, P, LV>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, doff, delta, out, \
+  RP_LAUNCH((k_scatter<GV, NCV, P, LV>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, doff, delta, out, \
                      S, bm_out, bm_x, ins_dst, del_dst, pushed, c, mark_list ? 1 : 0, copy, lo, packed_in ? 1 : 0)
 #define RP_SCATTER(GV, NCV, P)                \
   do {                                        \
@@ -1249,7 +1290,7 @@ void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list
                       float *S, unsigned *mark, const Counters *c) {
   const int blocks = 2048;
 #define RP_PULLM(GV, NCV, UV)                                                                                    \
-  hipLaunchKernelGGL((k_pull_msgs<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, ioff, in, \
+  RP_LAUNCH((k_pull_msgs<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, ioff, in, \
                      memb, msg, S, mark, c)
   if (d <= 16) RP_PULLM(16, 1, 8);
   else if (d <= 32) RP_PULLM(16, 2, 8);
@@ -1266,7 +1307,7 @@ void launch_recompute(hipStream_t s, long long n, int d, int gcn, const int *lis
                       const long long *ioff, Adj in, const int *out_len, const float *src, float *S, const Counters *c) {
   const int blocks = 2048;
 #define RP_RECOMP(GV, NCV, UV)                                                                                   \
-  hipLaunchKernelGGL((k_recompute<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, gcn, list, count, ioff, in, \
+  RP_LAUNCH((k_recompute<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, gcn, list, count, ioff, in, \
                      out_len, src, S, c)
   if (d <= 16) RP_RECOMP(16, 1, 8);
   else if (d <= 32) RP_RECOMP(16, 2, 8);
@@ -1283,7 +1324,7 @@ void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev,
                  float *S) {
   const int blocks = blocks_for(n * kWave, 256, 8192);
   const int nc = (d + kWave - 1) / kWave;
-#define RP_PULL(NCV) hipLaunchKernelGGL(k_pull<NCV>, dim3(blocks), dim3(256), 0, s, n, d, agg, Hprev, in, out_len, S)
+#define RP_PULL(NCV) RP_LAUNCH(k_pull<NCV>, dim3(blocks), dim3(256), 0, s, n, d, agg, Hprev, in, out_len, S)
   if (nc <= 1) RP_PULL(1);
   else if (nc == 2) RP_PULL(2);
   else if (nc <= 4) RP_PULL(4);
@@ -1294,17 +1335,17 @@ void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev,
 
 void launch_fill_i32(hipStream_t s, int *p, long long count, int value) {
   if (count <= 0) return;
-  hipLaunchKernelGGL(k_fill_i32, dim3(blocks_for(count, 256)), dim3(256), 0, s, p, count, value);
+  RP_LAUNCH(k_fill_i32, dim3(blocks_for(count, 256)), dim3(256), 0, s, p, count, value);
 }
 
 void launch_fill_u64(hipStream_t s, u64 *p, long long count, u64 value) {
   if (count <= 0) return;
-  hipLaunchKernelGGL(k_fill_u64, dim3(blocks_for(count, 256)), dim3(256), 0, s, p, count, value);
+  RP_LAUNCH(k_fill_u64, dim3(blocks_for(count, 256)), dim3(256), 0, s, p, count, value);
 }
 
 void launch_gather_rows(hipStream_t s, const float *src, int d, const int *ids, long long count, float *out) {
   if (count <= 0) return;
-  hipLaunchKernelGGL(k_gather_rows, dim3(blocks_for(count * d, 256)), dim3(256), 0, s, src, d, ids, count, out);
+  RP_LAUNCH(k_gather_rows, dim3(blocks_for(count * d, 256)), dim3(256), 0, s, src, d, ids, count, out);
 }
 
 }  // namespace rp

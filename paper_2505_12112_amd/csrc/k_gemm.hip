@@ -125,6 +125,59 @@ __device__ inline float4 load_b(const GemmArgs &a, int col, int k) {
   return make_float4(t[0], t[1], t[2], t[3]);
 }
 
+// The raw operand data of one float4 chunk (columns k .. k+3) of A row v (kGin2: a
+// list position), fetched without a branch so that every load of a round is in
+// flight together: a row past the count (v < 0) reads row 0 and a chunk past K the
+// last chunk; finish_a drops them and applies the row's scales. x holds the S part
+// or the plain row, h the previous layer's row of a sum form. (Widths are multiples
+// of 4 here, so no chunk straddles h and S.)
+struct AChunk {
+  float4 x, h;
+};
+
+template <int AGG, int MODE>
+__device__ inline AChunk fetch_a(const GemmArgs &a, long long v, int k) {
+  const long long base = (v < 0 ? 0 : v) * a.dprev;
+  const int kk = k < a.K ? k : a.K - 4;
+  AChunk c;
+  c.h = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (neigh_only<AGG, MODE>()) {
+    c.x = *reinterpret_cast<const float4 *>(a.S + base + kk);
+  } else if (MODE != kLayer && MODE != kGin1) {
+    c.x = *reinterpret_cast<const float4 *>(a.Hprev + base + kk);
+  } else if (sum_form<AGG, MODE>()) {
+    c.x = *reinterpret_cast<const float4 *>(a.S + base + kk);
+    c.h = *reinterpret_cast<const float4 *>(a.Hprev + base + kk);
+  } else {
+    const float *p = kk < a.dprev ? a.Hprev + base + kk : a.S + base + (kk - a.dprev);
+    c.x = *reinterpret_cast<const float4 *>(p);
+  }
+  return c;
+}
+
+template <int AGG, int MODE>
+__device__ inline float4 finish_a(const GemmArgs &a, const AChunk &c, bool valid, float tv, float sv, int k) {
+  if (!valid || k >= a.K) return make_float4(0.f, 0.f, 0.f, 0.f);
+  if (neigh_only<AGG, MODE>() || (MODE == kLayer && !sum_form<AGG, MODE>() && k >= a.dprev))
+    return make_float4(tv * c.x.x, tv * c.x.y, tv * c.x.z, tv * c.x.w);
+  if (sum_form<AGG, MODE>())
+    return make_float4(tv * (c.x.x + sv * c.h.x), tv * (c.x.y + sv * c.h.y), tv * (c.x.z + sv * c.h.z),
+                       tv * (c.x.w + sv * c.h.w));
+  return c.x;
+}
+
+// W row `col`, columns k .. k+3, fetched without a branch (a column past N reads
+// the last row and a chunk past K the last chunk; finish_b drops them).
+__device__ inline float4 fetch_b(const GemmArgs &a, int col, int k) {
+  const int cc = col < a.N ? col : a.N - 1;
+  const int kk = k < a.K ? k : a.K - 4;
+  return *reinterpret_cast<const float4 *>(a.W + static_cast<long long>(cc) * a.K + kk);
+}
+
+__device__ inline float4 finish_b(const GemmArgs &a, float4 b, int col, int k) {
+  return col < a.N && k < a.K ? b : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
 // Bias, cached transformed aggregate (kTransformFirst), activation, delta and write-back for
 // output element (row slot m with vertex v, column col).
 template <int AGG, int MODE>
@@ -272,8 +325,14 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
     }
     __syncthreads();
 
+    // the next K step's operands: VEC kernels issue the raw loads here (no branch,
+    // no arithmetic, so none of them waits) and finish the chunks (scales, dropped
+    // rows and columns) when they are stored to LDS, after the current step's MFMAs
     float4 ra[Sh::kAPer], rb[Sh::kBPer];
+    AChunk rc[Sh::kAPer];
+    int kload = 0;
     auto load_regs = [&](int k0) {
+      kload = k0;
 #pragma unroll
       for (int i = 0; i < Sh::kAPer; ++i) {
         const int c = tid + i * kThreads;
@@ -281,7 +340,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
           const int m = c / (kBK / 4);
           const int q = c % (kBK / 4);
           const long long arow = MODE == kGin2 ? (rv[m] >= 0 ? m0 + m : -1) : rv[m];
-          ra[i] = load_a<AGG, VEC, MODE>(a, arow, rt[m], rs[m], k0 + 4 * q);
+          if (VEC) rc[i] = fetch_a<AGG, MODE>(a, arow, k0 + 4 * q);
+          else ra[i] = load_a<AGG, VEC, MODE>(a, arow, rt[m], rs[m], k0 + 4 * q);
         }
       }
 #pragma unroll
@@ -290,7 +350,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
         if (c < Sh::kBChunks) {
           const int nn = c / (kBK / 4);
           const int q = c % (kBK / 4);
-          rb[i] = load_b<VEC>(a, n0 + nn, k0 + 4 * q);
+          rb[i] = VEC ? fetch_b(a, n0 + nn, k0 + 4 * q) : load_b<VEC>(a, n0 + nn, k0 + 4 * q);
         }
       }
     };
@@ -301,7 +361,12 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
         if (c < Sh::kAChunks) {
           const int m = c / (kBK / 4);
           const int q = c % (kBK / 4);
-          *reinterpret_cast<float4 *>(&As[buf][m][4 * q]) = ra[i];
+          float4 x = ra[i];
+          if (VEC) {
+            const bool valid = MODE == kGin2 ? rv[m] >= 0 : rv[m] >= 0;
+            x = finish_a<AGG, MODE>(a, rc[i], valid, rt[m], rs[m], kload + 4 * q);
+          }
+          *reinterpret_cast<float4 *>(&As[buf][m][4 * q]) = x;
         }
       }
 #pragma unroll
@@ -310,7 +375,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
         if (c < Sh::kBChunks) {
           const int nn = c / (kBK / 4);
           const int q = c % (kBK / 4);
-          *reinterpret_cast<float4 *>(&Bs[buf][nn][4 * q]) = rb[i];
+          *reinterpret_cast<float4 *>(&Bs[buf][nn][4 * q]) =
+              VEC ? finish_b(a, rb[i], n0 + nn, kload + 4 * q) : rb[i];
         }
       }
     };
@@ -606,9 +672,9 @@ void launch_rows(hipStream_t s, const GemmArgs &a, long long max_rows, bool wide
   long long blocks = tiles < 1 ? 1 : tiles;
   if (blocks > 2048) blocks = 2048;
   if (wide)
-    hipLaunchKernelGGL((k_gemm_rows<BN, AGG, MODE, 8>), dim3(blocks + a.cleanup_blocks), dim3(8 * kWave), 0, s, a);
+    RP_LAUNCH((k_gemm_rows<BN, AGG, MODE, 8>), dim3(blocks + a.cleanup_blocks), dim3(8 * kWave), 0, s, a);
   else
-    hipLaunchKernelGGL((k_gemm_rows<BN, AGG, MODE, 4>), dim3(blocks + a.cleanup_blocks), dim3(4 * kWave), 0, s, a);
+    RP_LAUNCH((k_gemm_rows<BN, AGG, MODE, 4>), dim3(blocks + a.cleanup_blocks), dim3(4 * kWave), 0, s, a);
 }
 
 template <int BM, int BN, int WM, int WN, int AGG, bool VEC, int MODE>
@@ -616,7 +682,7 @@ void launch_shape(hipStream_t s, const GemmArgs &a, long long max_rows) {
   const long long tiles = ((max_rows + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   long long blocks = tiles < 1 ? 1 : tiles;
   if (blocks > 2048) blocks = 2048;
-  hipLaunchKernelGGL((k_gemm<BM, BN, WM, WN, AGG, VEC, MODE>), dim3(blocks + a.cleanup_blocks), dim3(kThreads), 0, s,
+  RP_LAUNCH((k_gemm<BM, BN, WM, WN, AGG, VEC, MODE>), dim3(blocks + a.cleanup_blocks), dim3(kThreads), 0, s,
                      a);
 }
 

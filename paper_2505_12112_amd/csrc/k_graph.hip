@@ -713,7 +713,7 @@ void launch_net_hash(hipStream_t s, int cap_ops, const BatchIn *host_in, const B
                      ripple_op *ops,
                      int undirected, int weighted, long long n, u64 *ht_key, int *ht_val, unsigned mask, int *op_slot,
                      int *fop, Counters *c) {
-  hipLaunchKernelGGL(k_net_hash, dim3(blocks_for(cap_ops, 256, 1 << 20)), dim3(256), 0, s, host_in, now, dev_in, ops,
+  RP_LAUNCH(k_net_hash, dim3(blocks_for(cap_ops, 256, 1 << 20)), dim3(256), 0, s, host_in, now, dev_in, ops,
                      undirected, weighted, n, ht_key, ht_val, mask, op_slot, fop, c);
 }
 
@@ -723,7 +723,7 @@ void launch_net_direct(hipStream_t s, int cap_ops, const BatchIn *host_in, const
                        int *del_src, int *del_dst, int *ins_rank, int *del_rank, float *ins_w, float *del_w,
                        int *flist, int *frow, Counters *c) {
   const int ops_cap = cap_ops < kNetDirectMax ? cap_ops : kNetDirectMax;
-  hipLaunchKernelGGL(k_net_direct, dim3(blocks_for(static_cast<long long>(ops_cap) * kWave, 256)), dim3(256), 0, s,
+  RP_LAUNCH(k_net_direct, dim3(blocks_for(static_cast<long long>(ops_cap) * kWave, 256)), dim3(256), 0, s,
                      host_in, now, dev_in, ops, undirected, weighted, n, ht_key, ht_net, mask, op_slot, fop, out,
                      in_adj, ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank, ins_w, del_w, flist, frow, c);
 }
@@ -732,7 +732,7 @@ void launch_net_decide(hipStream_t s, int cap_ops, const BatchIn *in, const ripp
                        const int *ht_val, int *ht_net, const int *op_slot, const int *fop, Adj out, Adj in_adj,
                        int *ins_src, int *ins_dst, int *del_src, int *del_dst, int *ins_rank, int *del_rank,
                        float *ins_w, float *del_w, int *flist, int *frow, Counters *c) {
-  hipLaunchKernelGGL(k_net_decide, dim3(blocks_for(static_cast<long long>(cap_ops) * kWave, 256)), dim3(256), 0, s,
+  RP_LAUNCH(k_net_decide, dim3(blocks_for(static_cast<long long>(cap_ops) * kWave, 256)), dim3(256), 0, s,
                      in, ops, undirected, ht_val, ht_net, op_slot, fop, out, in_adj, ins_src, ins_dst, del_src,
                      del_dst, ins_rank, del_rank, ins_w, del_w, flist, frow, c);
 }
@@ -740,7 +740,7 @@ void launch_net_decide(hipStream_t s, int cap_ops, const BatchIn *in, const ripp
 void launch_topo_plan(hipStream_t s, int cap_arcs, Adj out, Adj in, const int *ins_src, const int *ins_dst,
                       const int *del_src, const int *del_dst, const int *ins_rank, const int *del_rank,
                       int long_ok, LongRow *tab, Counters *c, const Persist *p, long long cap_out, long long cap_in) {
-  hipLaunchKernelGGL(k_topo_plan, dim3(blocks_for((long_ok ? 4LL : 2LL) * cap_arcs, 256, 1024)), dim3(256), 0, s,
+  RP_LAUNCH(k_topo_plan, dim3(blocks_for((long_ok ? 4LL : 2LL) * cap_arcs, 256, 1024)), dim3(256), 0, s,
                      out, in, ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank, long_ok, tab, c, p, cap_out,
                      cap_in);
 }
@@ -750,20 +750,20 @@ void launch_topo_rewrite(hipStream_t s, int cap_arcs, int undirected, long long 
                          const int *ins_rank, const int *del_rank, const u64 *ht_key, const int *ht_net,
                          unsigned mask, Persist *p, int *ddeg, int long_ok, LongRow *tab, int *pool, Counters *c,
                          const RewriteBounds &rb) {
-  hipLaunchKernelGGL(k_topo_rewrite, dim3(blocks_for(4LL * cap_arcs * kWave, 256)), dim3(256), 0, s, undirected,
+  RP_LAUNCH(k_topo_rewrite, dim3(blocks_for(4LL * cap_arcs * kWave, 256)), dim3(256), 0, s, undirected,
                      n, out, in, ins_src, ins_dst, del_src, del_dst, ins_rank, del_rank, ht_key, ht_net, mask, p,
                      ddeg, long_ok, tab, pool, c, rb);
 }
 
 void launch_topo_fill(hipStream_t s, int cap_arcs, Adj out, Adj in, const LongRow *tab, const int *pool,
                       Counters *c) {
-  hipLaunchKernelGGL(k_topo_fill, dim3(blocks_for(2LL * cap_arcs * kWave, 256, 1024)), dim3(256), 0, s, out, in,
+  RP_LAUNCH(k_topo_fill, dim3(blocks_for(2LL * cap_arcs * kWave, 256, 1024)), dim3(256), 0, s, out, in,
                      tab, pool, c);
 }
 
 void launch_repack_copy(hipStream_t s, long long n, const int *old_col, const long long *old_off, const int *len,
                         int *new_col, const long long *new_off, const float *old_wt, float *new_wt) {
-  hipLaunchKernelGGL(k_repack_copy, dim3(blocks_for(n * kWave, 256, 8192)), dim3(256), 0, s, n, old_col, old_off,
+  RP_LAUNCH(k_repack_copy, dim3(blocks_for(n * kWave, 256, 8192)), dim3(256), 0, s, n, old_col, old_off,
                      len, new_col, new_off, old_wt, new_wt);
 }
 
@@ -882,20 +882,20 @@ int relayout_blocks(long long n) { return static_cast<int>((n + kScanPerBlock - 
 void launch_relayout_sums(hipStream_t s, long long n, float slack, int min_slack, const int *len,
                           long long *blocksums) {
   const int nb = relayout_blocks(n);
-  hipLaunchKernelGGL(k_relayout_sums, dim3(nb), dim3(kScanThreads), 0, s, n, len, slack, min_slack, blocksums);
-  hipLaunchKernelGGL(k_relayout_scan_sums, dim3(1), dim3(kScanThreads), 0, s, blocksums, nb);
+  RP_LAUNCH(k_relayout_sums, dim3(nb), dim3(kScanThreads), 0, s, n, len, slack, min_slack, blocksums);
+  RP_LAUNCH(k_relayout_scan_sums, dim3(1), dim3(kScanThreads), 0, s, blocksums, nb);
 }
 
 void launch_relayout_apply(hipStream_t s, long long n, float slack, int min_slack, Adj a, int *new_col,
                            float *new_wt, const long long *blocksums, long long *new_off, int *new_cap, u64 *top) {
   const int nb = relayout_blocks(n);
-  hipLaunchKernelGGL(k_relayout_offsets, dim3(nb), dim3(kScanThreads), 0, s, n, a.len, slack, min_slack, blocksums,
+  RP_LAUNCH(k_relayout_offsets, dim3(nb), dim3(kScanThreads), 0, s, n, a.len, slack, min_slack, blocksums,
                      new_off, new_cap);
-  hipLaunchKernelGGL(k_repack_copy, dim3(blocks_for(n * kWave, 256, 8192)), dim3(256), 0, s, n, a.col, a.off, a.len,
+  RP_LAUNCH(k_repack_copy, dim3(blocks_for(n * kWave, 256, 8192)), dim3(256), 0, s, n, a.col, a.off, a.len,
                      new_col, new_off, a.wt, new_wt);
   long long ib = (n + 255) / 256;
   if (ib > 4096) ib = 4096;
-  hipLaunchKernelGGL(k_relayout_install, dim3(ib), dim3(256), 0, s, n, new_off, new_cap, a.off, a.cap, blocksums, nb,
+  RP_LAUNCH(k_relayout_install, dim3(ib), dim3(256), 0, s, n, new_off, new_cap, a.off, a.cap, blocksums, nb,
                      top);
 }
 

@@ -40,7 +40,7 @@ using rp::u64;
 namespace {
 
 // Batches between two re-anchoring batches by default (see ripple_set_reanchor).
-constexpr long long kDefaultReanchor = 64;
+constexpr long long kDefaultReanchor = 256;
 
 struct PhaseEv {
   int phase;
@@ -658,15 +658,33 @@ hipEvent_t next_event(ripple_ctx *c) {
   return c->ev_pool[c->ev_used++];
 }
 
+// The phase whose launches are being timed on this thread (see rp::launch_timer).
+thread_local ripple_ctx *t_timed_ctx = nullptr;
+thread_local int t_timed_phase = -1;
+
+// Records the kernel times of one phase of a profiled batch: the launches made in
+// its scope take an event pair each (rp::launch_timer). The whole batch
+// (RIPPLE_PHASE_TOTAL) is bracketed by an event pair on the stream instead, from
+// before its first kernel to after its last.
 struct PhaseScope {
   ripple_ctx *c;
   int phase;
   hipEvent_t a = nullptr;
+  ripple_ctx *prev_ctx = nullptr;
+  int prev_phase = -1;
+  bool timing = false;
   PhaseScope(ripple_ctx *cc, int ph) : c(cc), phase(ph) {
-    if (c->prof && (c->prof_mask >> ph & 1u)) {
+    if (!c->prof || !(c->prof_mask >> ph & 1u)) return;
+    if (ph == RIPPLE_PHASE_TOTAL) {
       a = next_event(c);
       if (a) (void)hipEventRecord(a, c->stream);
+      return;
     }
+    prev_ctx = t_timed_ctx;
+    prev_phase = t_timed_phase;
+    t_timed_ctx = c;
+    t_timed_phase = ph;
+    timing = true;
   }
   void close() {
     if (a) {
@@ -676,6 +694,11 @@ struct PhaseScope {
         c->ev_log.push_back(PhaseEv{phase, a, b});
       }
       a = nullptr;
+    }
+    if (timing) {
+      t_timed_ctx = prev_ctx;
+      t_timed_phase = prev_phase;
+      timing = false;
     }
   }
   ~PhaseScope() { close(); }
@@ -1295,6 +1318,20 @@ ripple_status read_rows(ripple_ctx *c, const float *src, int d, const int32_t *i
 }
 
 }  // namespace
+
+namespace rp {
+
+bool launch_timer(hipEvent_t *start, hipEvent_t *stop) {
+  ripple_ctx *c = t_timed_ctx;
+  if (c == nullptr) return false;
+  *start = next_event(c);
+  *stop = next_event(c);
+  if (*start == nullptr || *stop == nullptr) return false;
+  c->ev_log.push_back(PhaseEv{t_timed_phase, *start, *stop});
+  return true;
+}
+
+}  // namespace rp
 
 extern "C" {
 
@@ -1981,7 +2018,7 @@ ripple_status ripple_set_profiling(ripple_ctx *c, int32_t mask) {
   c->prof_mask = static_cast<unsigned>(mask) & ((1u << RIPPLE_NUM_PHASES) - 1u);
   c->prof = c->prof_mask != 0;
   // create the events now so that the first recorded batch does not pay for it
-  const size_t want = 2 * (4 + 6 * static_cast<size_t>(rp::kMaxL));  // every scope of a batch
+  const size_t want = 2 * (8 + 8 * static_cast<size_t>(rp::kMaxL));  // every timed launch of a batch
   while (c->prof && c->ev_pool.size() < want) {
     hipEvent_t e;
     RP_HIP(c, hipEventCreate(&e));

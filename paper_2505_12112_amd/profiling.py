@@ -35,7 +35,7 @@ ROOT = os.path.dirname(HERE)
 TRAFFIC_MD = os.path.join(ROOT, "profiles", "hbm_traffic_counters.md")
 
 # kernels whose launches make up each rooflined phase of bench.py
-PHASE_KERNELS = {"scatter": ("k_scatter", "k_pull_msgs"), "gemm": ("k_gemm",)}
+PHASE_KERNELS = {"scatter": ("k_scatter", "k_pull_msgs", "k_recompute"), "gemm": ("k_gemm",)}
 
 
 def code_only(text: str) -> str:
@@ -108,12 +108,13 @@ def stats_table(trace_dir: str, title: str, command: str, top: int = 24) -> str:
 
 def _counter(dirpath: str, batches_only: bool = False):
     """kernel -> list of (value KiB, duration ns) per dispatch; batches_only keeps
-    the dispatches from the first batch on (the first k_net_hash), leaving out the
+    the dispatches from the first batch on (its netting kernel), leaving out the
     bootstrap."""
     rows = list(csv.DictReader(open(_one(dirpath, "*counter_collection.csv"))))
     t0 = 0
     if batches_only:
-        starts = [int(r["Start_Timestamp"]) for r in rows if kernel_name(r["Kernel_Name"]) == "k_net_hash"]
+        starts = [int(r["Start_Timestamp"]) for r in rows
+                  if kernel_name(r["Kernel_Name"]) in ("k_net_hash", "k_net_direct")]
         t0 = min(starts) if starts else 0
     d = defaultdict(list)
     for r in rows:

@@ -690,8 +690,8 @@ def test_thousand_batches_on_a_hub_heavy_graph_with_narrow_rows(agg, mode):
     fraction of its terms, hubs included), lies within the fp32 forward error
     bound of its layer; and the cached aggregates of the 16 highest in-degrees stay
     within 64 units of 2^-24 times the magnitude of their terms (drift). Every 64th
-    batch re-anchors (the default drift budget, whatever the form); mode
-    "recompute" re-anchors in every batch."""
+    batch re-anchors (the drift budget, whatever the form); mode "recompute"
+    re-anchors in every batch."""
     _say("hub-heavy 1000 batches", agg, mode)
     rng = np.random.default_rng(83 + 5 * ("sum", "gcn").index(agg) + ("auto", "push", "dense", "recompute").index(mode))
     dims = (8, 6, 4)
@@ -702,6 +702,7 @@ def test_thousand_batches_on_a_hub_heavy_graph_with_narrow_rows(agg, mode):
     x = rng.standard_normal((n, dims[0])).astype(np.float32)
     w = synth.model_weights(synth.ModelSpec(agg, dims), rng, bias_std=0.1)
     p = Pair(n, src, dst, x, w, mode=mode)
+    p.lib.set_reanchor(64)
     try:
         hubs = np.argsort(indeg)[-16:]
         reanchored = 0
