@@ -150,7 +150,12 @@ typedef struct {
                                     GIN: the MLP's first layer W1 */
   const float *const *bias;      /* [L] [d_l]; NULL array or NULL entry = zero bias (GIN: b1) */
   const int32_t *relu;           /* [L] 1 = ReLU after layer l, 0 = identity */
-  int32_t gemm_prec;             /* ripple_gemm_prec; RIPPLE_GEMM_FP32 only in this version */
+  int32_t gemm_prec;             /* ripple_gemm_prec. RIPPLE_GEMM_FP32: the transforms' MFMA takes fp32
+                                    operands. RIPPLE_GEMM_BF16: it takes bf16 operands (the gathered rows
+                                    and the weights rounded to nearest even), accumulating in fp32;
+                                    results within about 1e-2 of the fp32 path's. Needs the widths
+                                    d_0 .. d_{L-1} (GIN: d_0 .. d_L) to be multiples of 4, else
+                                    RIPPLE_E_INVALID. */
   int32_t transform_first;       /* per-layer choice of what the aggregate cache holds (see
                                     ripple_get_aggregates): -1 = for layers with d_l < d_{l-1} when the
                                     graph has at least 2^24 arcs (on smaller graphs the message step is

@@ -469,6 +469,8 @@ struct GemmArgs {
   const int *out_len;
   const int *ddeg;
   const float *W;   // [N][K]
+  const unsigned short *Wb;  // bf16 transforms: W rounded to bf16 (RN-even) as raw bits, [N][K]
+  int bf16;         // 1: the MFMA takes bf16 operands (rounded RN-even at the gather), fp32 accumulation
   int K;
   int N;
   const float *bias;

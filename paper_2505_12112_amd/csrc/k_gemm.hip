@@ -32,6 +32,21 @@ namespace rp {
 namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// bf16 transforms use v_mfma_f32_16x16x32_bf16: per lane eight consecutive k
+// values of its A row and of its B column, the same eight on both sides (the
+// product is a sum over k, so which eight a lane holds does not matter as long as
+// A and B agree); the 16 x 16 fp32 result has the layout of the fp32 MFMA's.
+__device__ inline bf16x4 to_bf16(float4 x) {
+  bf16x4 r;
+  r[0] = static_cast<__bf16>(x.x);  // v_cvt_pk_bf16_f32: round to nearest even
+  r[1] = static_cast<__bf16>(x.y);
+  r[2] = static_cast<__bf16>(x.z);
+  r[3] = static_cast<__bf16>(x.w);
+  return r;
+}
 
 constexpr int kBK = 32;
 constexpr int kLdk = kBK + 4;  // LDS row stride (floats)
@@ -178,6 +193,17 @@ __device__ inline float4 finish_b(const GemmArgs &a, float4 b, int col, int k) {
   return col < a.N && k < a.K ? b : make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
+// The same four weights in bf16 (raw bits, 8 bytes).
+__device__ inline uint2 fetch_b_bf(const GemmArgs &a, int col, int k) {
+  const int cc = col < a.N ? col : a.N - 1;
+  const int kk = k < a.K ? k : a.K - 4;
+  return *reinterpret_cast<const uint2 *>(a.Wb + static_cast<long long>(cc) * a.K + kk);
+}
+
+__device__ inline uint2 finish_b_bf(const GemmArgs &a, uint2 b, int col, int k) {
+  return col < a.N && k < a.K ? b : make_uint2(0u, 0u);
+}
+
 // Bias, cached transformed aggregate (kTransformFirst), activation, delta and write-back for
 // output element (row slot m with vertex v, column col).
 template <int AGG, int MODE>
@@ -264,8 +290,9 @@ __device__ inline bool cleanup_role(const GemmArgs &a, unsigned &gemm_grid) {
   return true;
 }
 
-template <int BM, int BN, int WM, int WN, int AGG, bool VEC, int MODE>
+template <int BM, int BN, int WM, int WN, int AGG, bool VEC, int MODE, bool BF = false>
 __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
+  static_assert(!BF || VEC, "bf16 operands are gathered as float4 chunks");
   using Sh = Shape<BM, BN, WM, WN>;
   unsigned gemm_grid;
   if (cleanup_role(a, gemm_grid)) return;
@@ -282,6 +309,11 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) float smem[kSmem];
   float(*As)[BM][kLdk] = reinterpret_cast<float(*)[BM][kLdk]>(smem);
   float(*Bs)[BN][kLdk] = reinterpret_cast<float(*)[BN][kLdk]>(smem + kAsz);
+  // bf16 operand tiles in the same buffer: rows of kBK + 8 bf16 (80 bytes), so each
+  // lane's eight k values are one aligned 16-byte read
+  constexpr int kLdb = kBK + 8;
+  unsigned short(*Ab)[BM][kLdb] = reinterpret_cast<unsigned short(*)[BM][kLdb]>(smem);
+  unsigned short(*Bb)[BN][kLdb] = reinterpret_cast<unsigned short(*)[BN][kLdb]>(smem + kAsz);
   __shared__ int rv[BM];
   __shared__ float rt[BM];
   __shared__ float rs[BM];
@@ -329,6 +361,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
     // no arithmetic, so none of them waits) and finish the chunks (scales, dropped
     // rows and columns) when they are stored to LDS, after the current step's MFMAs
     float4 ra[Sh::kAPer], rb[Sh::kBPer];
+    uint2 rbb[Sh::kBPer];
     AChunk rc[Sh::kAPer];
     int kload = 0;
     auto load_regs = [&](int k0) {
@@ -350,7 +383,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
         if (c < Sh::kBChunks) {
           const int nn = c / (kBK / 4);
           const int q = c % (kBK / 4);
-          rb[i] = VEC ? fetch_b(a, n0 + nn, k0 + 4 * q) : load_b<VEC>(a, n0 + nn, k0 + 4 * q);
+          if (BF) rbb[i] = fetch_b_bf(a, n0 + nn, k0 + 4 * q);
+          else rb[i] = VEC ? fetch_b(a, n0 + nn, k0 + 4 * q) : load_b<VEC>(a, n0 + nn, k0 + 4 * q);
         }
       }
     };
@@ -366,7 +400,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
             const bool valid = MODE == kGin2 ? rv[m] >= 0 : rv[m] >= 0;
             x = finish_a<AGG, MODE>(a, rc[i], valid, rt[m], rs[m], kload + 4 * q);
           }
-          *reinterpret_cast<float4 *>(&As[buf][m][4 * q]) = x;
+          if (BF) *reinterpret_cast<bf16x4 *>(&Ab[buf][m][4 * q]) = to_bf16(x);
+          else *reinterpret_cast<float4 *>(&As[buf][m][4 * q]) = x;
         }
       }
 #pragma unroll
@@ -375,8 +410,11 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
         if (c < Sh::kBChunks) {
           const int nn = c / (kBK / 4);
           const int q = c % (kBK / 4);
-          *reinterpret_cast<float4 *>(&Bs[buf][nn][4 * q]) =
-              VEC ? finish_b(a, rb[i], n0 + nn, kload + 4 * q) : rb[i];
+          if (BF)
+            *reinterpret_cast<uint2 *>(&Bb[buf][nn][4 * q]) = finish_b_bf(a, rbb[i], n0 + nn, kload + 4 * q);
+          else
+            *reinterpret_cast<float4 *>(&Bs[buf][nn][4 * q]) =
+                VEC ? finish_b(a, rb[i], n0 + nn, kload + 4 * q) : rb[i];
         }
       }
     };
@@ -394,18 +432,33 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmArgs a) {
     for (int k0 = 0; k0 < K; k0 += kBK) {
       const bool more = k0 + kBK < K;
       if (more) load_regs(k0 + kBK);
+      if constexpr (BF) {
+        // the step's 32 k values in one MFMA per output tile: lane (r, q) holds k
+        // values 8q .. 8q+7 of its A row and B column
+        bf16x8 av[WM], bv[WN];
 #pragma unroll
-      for (int kk = 0; kk < kBK; kk += 4) {
-        float av[WM], bv[WN];
+        for (int i = 0; i < WM; ++i) av[i] = *reinterpret_cast<const bf16x8 *>(&Ab[buf][wm0 + i * 16 + lr][8 * lk]);
 #pragma unroll
-        for (int i = 0; i < WM; ++i) av[i] = As[buf][wm0 + i * 16 + lr][kk + lk];
-#pragma unroll
-        for (int j = 0; j < WN; ++j) bv[j] = Bs[buf][wn0 + j * 16 + lr][kk + lk];
+        for (int j = 0; j < WN; ++j) bv[j] = *reinterpret_cast<const bf16x8 *>(&Bb[buf][wn0 + j * 16 + lr][8 * lk]);
 #pragma unroll
         for (int i = 0; i < WM; ++i)
 #pragma unroll
           for (int j = 0; j < WN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < kBK; kk += 4) {
+          float av[WM], bv[WN];
+#pragma unroll
+          for (int i = 0; i < WM; ++i) av[i] = As[buf][wm0 + i * 16 + lr][kk + lk];
+#pragma unroll
+          for (int j = 0; j < WN; ++j) bv[j] = Bs[buf][wn0 + j * 16 + lr][kk + lk];
+#pragma unroll
+          for (int i = 0; i < WM; ++i)
+#pragma unroll
+            for (int j = 0; j < WN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+        }
       }
       if (more) store_lds(buf ^ 1);
       __syncthreads();
@@ -467,7 +520,7 @@ constexpr int kRowsBM = 16;
 // (128 k values per round, twice the tiles per compute unit).
 constexpr long long kRowsWideMax = 2048;
 
-template <int BN, int AGG, int MODE, int W>
+template <int BN, int AGG, int MODE, int W, bool BF = false>
 __global__ __launch_bounds__(W * kWave) void k_gemm_rows(GemmArgs a) {
   constexpr int kRowsWaves = W;  // waves per tile, each on its own range of k
   constexpr int kRowsThreads = W * kWave;
@@ -580,6 +633,72 @@ __global__ __launch_bounds__(W * kWave) void k_gemm_rows(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < WN; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
     const long long abase = arow * dp;
+    if constexpr (BF) {
+      // bf16: per round each lane takes eight consecutive k values (two float4 of
+      // its A row, each all h or all S since the widths are multiples of 4) and the
+      // same eight weights of each B column, one MFMA per 32 k values and column tile
+      for (int kc = kb; kc < ke; kc += kRowsKC) {
+        constexpr int kG = kRowsKC / 32;
+        float4 zh[kG][2], zs[kG][2];
+        uint2 wb[WN][kG][2];
+#pragma unroll
+        for (int g = 0; g < kG; ++g)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const int k = kc + 32 * g + 8 * lq + 4 * hh;
+            const bool ok = arow >= 0 && k < ke;
+            float4 x = make_float4(0.f, 0.f, 0.f, 0.f), h = x;
+            if (ok) {
+              if (neigh_only<AGG, MODE>()) {
+                x = *reinterpret_cast<const float4 *>(a.S + abase + k);
+              } else if (sum_form<AGG, MODE>()) {
+                x = *reinterpret_cast<const float4 *>(a.S + abase + k);
+                h = *reinterpret_cast<const float4 *>(a.Hprev + abase + k);
+              } else if (MODE != kLayer) {
+                x = *reinterpret_cast<const float4 *>(a.Hprev + abase + k);
+              } else {
+                x = k < dp ? *reinterpret_cast<const float4 *>(a.Hprev + abase + k)
+                           : *reinterpret_cast<const float4 *>(a.S + abase + (k - dp));
+              }
+            }
+            zs[g][hh] = x;
+            zh[g][hh] = h;
+#pragma unroll
+            for (int j = 0; j < WN; ++j) {
+              const int col = n0 + 16 * j + lr;
+              wb[j][g][hh] = col < N && k < ke
+                                 ? *reinterpret_cast<const uint2 *>(a.Wb + static_cast<long long>(col) * K + k)
+                                 : make_uint2(0u, 0u);
+            }
+          }
+#pragma unroll
+        for (int g = 0; g < kG; ++g) {
+          float4 z[2];
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const int k = kc + 32 * g + 8 * lq + 4 * hh;
+            const float4 x = zs[g][hh], h = zh[g][hh];
+            if (sum_form<AGG, MODE>() && ((MODE == kLayer && AGG != kSum && AGG != kGcSum) || MODE == kGin1))
+              z[hh] = make_float4(ta * (x.x + sa * h.x), ta * (x.y + sa * h.y), ta * (x.z + sa * h.z),
+                                  ta * (x.w + sa * h.w));
+            else if (((MODE == kLayer && AGG != kSum && AGG != kGcSum) || MODE == kGin1) &&
+                     (neigh_only<AGG, MODE>() || k >= dp))
+              z[hh] = make_float4(ta * x.x, ta * x.y, ta * x.z, ta * x.w);
+            else
+              z[hh] = x;
+          }
+          const bf16x4 lo = to_bf16(z[0]), hi = to_bf16(z[1]);
+          const bf16x8 a8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+#pragma unroll
+          for (int j = 0; j < WN; ++j) {
+            const uint4 w4 = make_uint4(wb[j][g][0].x, wb[j][g][0].y, wb[j][g][1].x, wb[j][g][1].y);
+            bf16x8 b8;
+            __builtin_memcpy(&b8, &w4, sizeof(b8));
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8, b8, acc[j], 0, 0, 0);
+          }
+        }
+      }
+    } else
     for (int kc = kb; kc < ke; kc += kRowsKC) {
       float4 av[kF], ah[kF], bv[WN][kF];
 #pragma unroll
@@ -671,10 +790,11 @@ void launch_rows(hipStream_t s, const GemmArgs &a, long long max_rows, bool wide
   const long long tiles = ((max_rows + kRowsBM - 1) / kRowsBM) * ((a.N + BN - 1) / BN);
   long long blocks = tiles < 1 ? 1 : tiles;
   if (blocks > 2048) blocks = 2048;
-  if (wide)
-    RP_LAUNCH((k_gemm_rows<BN, AGG, MODE, 8>), dim3(blocks + a.cleanup_blocks), dim3(8 * kWave), 0, s, a);
-  else
-    RP_LAUNCH((k_gemm_rows<BN, AGG, MODE, 4>), dim3(blocks + a.cleanup_blocks), dim3(4 * kWave), 0, s, a);
+  const dim3 grid(static_cast<unsigned>(blocks + a.cleanup_blocks));
+  if (a.bf16 && wide) RP_LAUNCH((k_gemm_rows<BN, AGG, MODE, 8, true>), grid, dim3(8 * kWave), 0, s, a);
+  else if (a.bf16) RP_LAUNCH((k_gemm_rows<BN, AGG, MODE, 4, true>), grid, dim3(4 * kWave), 0, s, a);
+  else if (wide) RP_LAUNCH((k_gemm_rows<BN, AGG, MODE, 8>), grid, dim3(8 * kWave), 0, s, a);
+  else RP_LAUNCH((k_gemm_rows<BN, AGG, MODE, 4>), grid, dim3(4 * kWave), 0, s, a);
 }
 
 template <int BM, int BN, int WM, int WN, int AGG, bool VEC, int MODE>
@@ -682,8 +802,14 @@ void launch_shape(hipStream_t s, const GemmArgs &a, long long max_rows) {
   const long long tiles = ((max_rows + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   long long blocks = tiles < 1 ? 1 : tiles;
   if (blocks > 2048) blocks = 2048;
-  RP_LAUNCH((k_gemm<BM, BN, WM, WN, AGG, VEC, MODE>), dim3(blocks + a.cleanup_blocks), dim3(kThreads), 0, s,
-                     a);
+  const dim3 grid(static_cast<unsigned>(blocks + a.cleanup_blocks));
+  if constexpr (VEC) {
+    if (a.bf16) {
+      RP_LAUNCH((k_gemm<BM, BN, WM, WN, AGG, VEC, MODE, true>), grid, dim3(kThreads), 0, s, a);
+      return;
+    }
+  }
+  RP_LAUNCH((k_gemm<BM, BN, WM, WN, AGG, VEC, MODE>), grid, dim3(kThreads), 0, s, a);
 }
 
 // BN follows N. Few expected rows: the 16-row split-K kernel; many: 128-row tiles

@@ -102,6 +102,11 @@ struct ripple_ctx {
   float *Wn[rp::kMaxL] = {};    // transform-first layers: W_neigh [d_l][d_{l-1}] (GCN: W)
   float *P[rp::kMaxL + 1] = {};  // [l], transform-first layers: P = W_neigh H^{l-1}, [n][d_l]
   float *bias[rp::kMaxL] = {};
+  // bf16 transforms (gemm_prec RIPPLE_GEMM_BF16): the same matrices rounded to bf16
+  bool gemm_bf16 = false;
+  unsigned short *Wb[rp::kMaxL] = {};
+  unsigned short *Wnb[rp::kMaxL] = {};
+  unsigned short *W2b[rp::kMaxL] = {};
   float *W2[rp::kMaxL] = {};     // GIN: the MLP's second layer [d_l][d_l]
   float *b2[rp::kMaxL] = {};
   float gin_eps1 = 1.0f;         // GIN: 1 + eps
@@ -511,6 +516,9 @@ void free_model(ripple_ctx *c) {
     dfree_t(c, c->bias[l]);
     dfree_t(c, c->W2[l]);
     dfree_t(c, c->b2[l]);
+    dfree_t(c, c->Wb[l]);
+    dfree_t(c, c->Wnb[l]);
+    dfree_t(c, c->W2b[l]);
   }
   dfree_t(c, c->gin_rows);
   dfree_t(c, c->msg);
@@ -558,6 +566,8 @@ rp::GemmArgs gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 *c
   g.out_len = c->adj[0].len;
   g.ddeg = c->ddeg;
   g.W = c->W[l - 1];
+  g.Wb = c->Wb[l - 1];
+  g.bf16 = c->gemm_bf16 ? 1 : 0;
   g.K = c->K[l - 1];
   g.N = c->dims[l];
   g.bias = c->bias[l - 1];
@@ -589,6 +599,8 @@ rp::GemmArgs p_gemm_args(const ripple_ctx *c, int l, const int *rows, const u64 
   g.out_len = c->adj[0].len;
   g.ddeg = c->ddeg;
   g.W = c->Wn[l - 1];
+  g.Wb = c->Wnb[l - 1];
+  g.bf16 = c->gemm_bf16 ? 1 : 0;
   g.K = c->dims[l - 1];
   g.N = c->dims[l];
   g.bias = nullptr;
@@ -637,6 +649,7 @@ int launch_layer_gemm(const ripple_ctx *c, hipStream_t s, int l, const int *rows
   g2.dprev = c->dims[l];
   g2.S = nullptr;
   g2.W = c->W2[l - 1];
+  g2.Wb = c->W2b[l - 1];
   g2.K = c->dims[l];
   g2.bias = c->b2[l - 1];
   if (cleanup != nullptr) {
@@ -1525,6 +1538,28 @@ ripple_status ripple_load_graph(const ripple_graph_desc *g, ripple_ctx **out) {
   return RIPPLE_OK;
 }
 
+namespace {
+
+// x rounded to bf16, round to nearest even (NaN kept a quiet NaN), as raw bits.
+unsigned short bf16_bits(float x) {
+  unsigned u;
+  std::memcpy(&u, &x, sizeof(u));
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu) != 0) return static_cast<unsigned short>((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<unsigned short>(u >> 16);
+}
+
+// A device copy of host matrix w (count floats) rounded to bf16.
+ripple_status upload_bf16(ripple_ctx *c, unsigned short **dst, const float *w, long long count) {
+  std::vector<unsigned short> b(static_cast<size_t>(count));
+  for (long long i = 0; i < count; ++i) b[i] = bf16_bits(w[i]);
+  RP_TRY(dalloc_n(c, dst, count));
+  RP_HIP(c, hipMemcpy(*dst, b.data(), static_cast<size_t>(count) * sizeof(unsigned short), hipMemcpyHostToDevice));
+  return RIPPLE_OK;
+}
+
+}  // namespace
+
 ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple_model_desc *md) {
   RP_TRY(check_ctx(c));
   if (x == nullptr || md == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: x and model must be non-NULL");
@@ -1540,12 +1575,18 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   if (!sage && md->agg != RIPPLE_AGG_GCN && md->transform_first == 1)
     return fail(c, RIPPLE_E_INVALID, "ripple: transform_first = 1 needs a GraphSAGE or GCN model");
   if (gin && md->w_out == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: w_out must be non-NULL for GIN");
-  if (md->gemm_prec != RIPPLE_GEMM_FP32) return fail(c, RIPPLE_E_INVALID, "ripple: only RIPPLE_GEMM_FP32 is built");
+  if (md->gemm_prec != RIPPLE_GEMM_FP32 && md->gemm_prec != RIPPLE_GEMM_BF16)
+    return fail(c, RIPPLE_E_INVALID, "ripple: unknown gemm_prec");
   if (md->dims == nullptr || md->w_neigh == nullptr || md->relu == nullptr)
     return fail(c, RIPPLE_E_INVALID, "ripple: dims, w_neigh and relu must be non-NULL");
   if (sage && md->w_self == nullptr) return fail(c, RIPPLE_E_INVALID, "ripple: w_self must be non-NULL for GraphSAGE");
   for (int l = 0; l <= L; ++l)
     if (md->dims[l] < 1 || md->dims[l] > RIPPLE_MAX_DIM) return fail(c, RIPPLE_E_INVALID, "ripple: dim out of range");
+  if (md->gemm_prec == RIPPLE_GEMM_BF16)  // every transform input is gathered in float4 chunks
+    for (int l = 0; l < L + (md->agg == RIPPLE_AGG_GIN ? 1 : 0); ++l)
+      if (md->dims[l] % 4 != 0)
+        return fail(c, RIPPLE_E_INVALID,
+                    "ripple: RIPPLE_GEMM_BF16 needs the widths of the transforms' inputs to be multiples of 4");
   for (int l = 0; l < L; ++l) {
     if (md->w_neigh[l] == nullptr || (sage && md->w_self[l] == nullptr) || (gin && md->w_out[l] == nullptr))
       return fail(c, RIPPLE_E_INVALID, "ripple: missing weight matrix");
@@ -1555,6 +1596,7 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
   free_model(c);
   c->L = L;
   c->agg = md->agg;
+  c->gemm_bf16 = md->gemm_prec == RIPPLE_GEMM_BF16;
   for (int l = 0; l <= L; ++l) c->dims[l] = md->dims[l];
   c->dmax_delta = 0;
   for (int l = 0; l < L; ++l) c->dmax_delta = std::max(c->dmax_delta, c->dims[l]);
@@ -1592,10 +1634,12 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
     RP_TRY(dalloc_n(c, &c->bias[l - 1], dn));
     RP_HIP(c, hipMemcpyAsync(c->W[l - 1], w.data(), w.size() * sizeof(float), hipMemcpyHostToDevice, c->stream));
     RP_HIP(c, hipMemcpyAsync(c->bias[l - 1], b.data(), dn * sizeof(float), hipMemcpyHostToDevice, c->stream));
+    if (c->gemm_bf16) RP_TRY(upload_bf16(c, &c->Wb[l - 1], w.data(), static_cast<long long>(w.size())));
     if (c->tf[l]) {
       RP_TRY(dalloc_n(c, &c->Wn[l - 1], static_cast<long long>(dn) * dp));
       RP_HIP(c, hipMemcpyAsync(c->Wn[l - 1], md->w_neigh[l - 1], static_cast<size_t>(dn) * dp * sizeof(float),
                                hipMemcpyHostToDevice, c->stream));
+      if (c->gemm_bf16) RP_TRY(upload_bf16(c, &c->Wnb[l - 1], md->w_neigh[l - 1], static_cast<long long>(dn) * dp));
     }
     if (gin) {
       std::vector<float> b2(dn, 0.0f);
@@ -1604,6 +1648,7 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
       RP_TRY(dalloc_n(c, &c->b2[l - 1], dn));
       RP_HIP(c, hipMemcpyAsync(c->W2[l - 1], md->w_out[l - 1], static_cast<size_t>(dn) * dn * sizeof(float),
                                hipMemcpyHostToDevice, c->stream));
+      if (c->gemm_bf16) RP_TRY(upload_bf16(c, &c->W2b[l - 1], md->w_out[l - 1], static_cast<long long>(dn) * dn));
       RP_HIP(c, hipMemcpyAsync(c->b2[l - 1], b2.data(), dn * sizeof(float), hipMemcpyHostToDevice, c->stream));
     }
     RP_HIP(c, hipStreamSynchronize(c->stream));

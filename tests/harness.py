@@ -81,11 +81,15 @@ class CallerStream:
         return False
 
 
+FP32_TOL_BF16 = 2e-2   # max row-relative error with bf16 transform operands
+BF16_UNIT = 2.0 ** -8  # unit roundoff of bf16 (8 significand bits), rounded up
+
+
 class Pair:
     def __init__(self, n, src, dst, x, weights, undirected=False, transform_first=-1, mode="auto", inputs="host",
-                 edge_w=None, graphs=False, **lib_kw):
+                 edge_w=None, graphs=False, gemm="fp32", **lib_kw):
         self.lib = Ripple(n, src, dst, undirected=undirected, weights=edge_w, **lib_kw)
-        self.lib.init_embeddings(x, weights, transform_first=transform_first)
+        self.lib.init_embeddings(x, weights, transform_first=transform_first, gemm=gemm)
         self.lib.set_scatter_mode(mode)
         self.lib.set_graphs(graphs)
         self.graphs = graphs  # batches replay captured HIP graphs, else kernels are queued one by one
@@ -221,29 +225,35 @@ def random_valid_batch(rng, orc: O.OracleState, bs: int, d0: int, mix=(1 / 3, 1 
     return synth.Batch(ops, feats)
 
 
-def fp32_forward_bound(orc: O.OracleState, ref, l: int) -> np.ndarray:
-    """Per row v of layer l: the forward error bound of evaluating the layer in fp32
-    from exact inputs, 2 (K + 16) 2^-24 max_k B_vk, where B_vk sums the magnitudes
-    of every term of output k's pre-activation (|W_self| |h_v| + |W_neigh| sum_u
-    |c_uv h_u| + |b|) and K is the length of the row's dot products. For GraphSAGE
-    (sum, mean) and GCN models."""
+def fp32_forward_bound(orc: O.OracleState, ref, l: int, unit: float = 2.0 ** -24) -> np.ndarray:
+    """Per row v of layer l: the forward error bound of evaluating the layer from
+    exact inputs in arithmetic of unit roundoff `unit` (fp32 by default),
+    2 (K + 16) unit max_k B_vk, where B_vk sums the magnitudes of every term of
+    output k's pre-activation (|W_self| |h_v| + |W_neigh| sum_u |c_uv h_u| + |b|;
+    GIN: through both layers of its MLP) and K is the length of the row's dot
+    products."""
     m = orc.model
     habs = np.abs(ref[l - 1])
     aabs = O.aggregate(orc.graph, habs, m.agg)  # the coefficients are non-negative
-    b = aabs @ np.abs(m.w_neigh[l - 1]).T + np.abs(m.bias[l - 1])
     k = m.w_neigh[l - 1].shape[1]
-    if m.w_self[l - 1] is not None:
-        b = b + habs @ np.abs(m.w_self[l - 1]).T
-        k *= 2
-    return 2.0 * (k + 16) * 2.0 ** -24 * np.max(b, axis=1)
+    if m.agg == "gin":
+        hidden = ((1.0 + m.gin_eps) * habs + aabs) @ np.abs(m.w_neigh[l - 1]).T + np.abs(m.bias[l - 1])
+        b = hidden @ np.abs(m.w_out[l - 1]).T + np.abs(m.b_out[l - 1])
+        k += m.w_out[l - 1].shape[1]
+    else:
+        b = aabs @ np.abs(m.w_neigh[l - 1]).T + np.abs(m.bias[l - 1])
+        if m.w_self[l - 1] is not None:
+            b = b + habs @ np.abs(m.w_self[l - 1]).T
+            k *= 2
+    return 2.0 * (k + 16) * unit * np.max(b, axis=1)
 
 
-def check_embeddings_conditioned(pair: "Pair", tol=FP32_TOL):
+def check_embeddings_conditioned(pair: "Pair", tol=FP32_TOL, unit: float = 2.0 ** -24):
     """Every row of every layer meets R16 (max row-relative error tol, floor 1e-3
-    RMS), or, where R16 asks for more than fp32 resolves (a row whose pre-activation
-    cancels to far below the magnitude of its terms), lies within the fp32 forward
-    error bound of its layer (fp32_forward_bound). Returns per layer (max R16
-    error, rows that needed the bound)."""
+    RMS), or, where R16 asks for more than the arithmetic resolves (a row whose
+    pre-activation cancels to far below the magnitude of its terms), lies within
+    the forward error bound of its layer (fp32_forward_bound with that unit
+    roundoff). Returns per layer (max R16 error, rows that needed the bound)."""
     ref = pair.orc.embeddings()
     out = []
     for l in range(1, pair.L + 1):
@@ -251,7 +261,7 @@ def check_embeddings_conditioned(pair: "Pair", tol=FP32_TOL):
         diff = np.max(np.abs(got - ref[l]), axis=1)
         floor = 1e-3 * float(np.sqrt(np.mean(ref[l] * ref[l])))
         r16 = diff / np.maximum(np.max(np.abs(ref[l]), axis=1), floor)
-        bound = fp32_forward_bound(pair.orc, ref, l)
+        bound = fp32_forward_bound(pair.orc, ref, l, unit)
         over = np.flatnonzero(r16 > tol)
         bad = over[diff[over] > bound[over]]
         assert bad.size == 0, (l, bad[:5], r16[bad[:5]], diff[bad[:5]], bound[bad[:5]])

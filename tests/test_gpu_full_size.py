@@ -8,7 +8,7 @@ import pytest
 
 from oracle import ripple_oracle as O
 from paper_2505_12112_amd import synth
-from tests.harness import Pair
+from tests.harness import BF16_UNIT, FP32_TOL_BF16, Pair, check_embeddings_conditioned
 
 pytestmark = pytest.mark.gpu
 
@@ -32,6 +32,23 @@ def test_sparse_mid_full_size(bs):
         _say(f"sparse_mid bs={bs}: {nb} batches in {time.time() - t0:.1f}s, last |A| = {[s.size for s in sets]}")
         errs = p.check_embeddings()
         _say("  row-relative errors", errs)
+        p.check_arcs()
+    finally:
+        p.close()
+
+
+def test_sparse_mid_bf16_full_size():
+    """The headline workload with bf16 transform operands: 20 batches of 100 with
+    affected sets every batch, then every row against a float64 full recompute at
+    2e-2 (R16, or the bf16 forward error bound where R16 asks for more than bf16
+    resolves)."""
+    wl = synth.build_workload("sparse_mid")
+    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, gemm="bf16")
+    try:
+        for b in range(20):
+            p.step(wl.stream.next_batch(100))
+        res = check_embeddings_conditioned(p, FP32_TOL_BF16, BF16_UNIT)
+        _say(f"sparse_mid bf16: per layer (max R16 error, rows within the bf16 bound) {res}")
         p.check_arcs()
     finally:
         p.close()

@@ -11,8 +11,8 @@ import pytest
 from oracle import ripple_oracle as O
 from paper_2505_12112_amd import synth
 from paper_2505_12112_amd.ripple import PHASES, Ripple, RippleError, E_INVALID, E_STATE, E_OOM
-from tests.harness import (CallerStream, Pair, random_valid_batch, FP32_TOL, aggregate_drift_ulps,
-                           check_embeddings_conditioned)
+from tests.harness import (BF16_UNIT, FP32_TOL, FP32_TOL_BF16, CallerStream, Pair, aggregate_drift_ulps,
+                           check_embeddings_conditioned, random_valid_batch)
 
 pytestmark = pytest.mark.gpu
 
@@ -720,3 +720,70 @@ def test_thousand_batches_on_a_hub_heavy_graph_with_narrow_rows(agg, mode):
         p.check_aggregates()
     finally:
         p.close()
+
+
+@pytest.mark.parametrize("agg", AGGS)
+@pytest.mark.parametrize("tf", [0, 1])
+def test_bf16_transforms(agg, tf):
+    """Transforms with bf16 operands (RIPPLE_GEMM_BF16; rounded to nearest even at the
+    gather, fp32 accumulation), every aggregator, transform-first on every layer or
+    none (GraphConv and GIN take none): the bootstrap and 40 batches (colliding ones
+    among them) in the automatic forms, then every row within 2e-2 row-relative error
+    of the float64 recompute, or within the bf16 forward error bound where R16 asks
+    for more than bf16 resolves; affected sets bit for bit every batch."""
+    if tf and agg not in ("sum", "mean", "gcn"):
+        pytest.skip("transform-first caching is for GraphSAGE and GCN models")
+    _say("bf16", agg, tf)
+    rng = np.random.default_rng(101 + AGGS.index(agg) + 10 * tf)
+    dims = (24, 64, 12) if agg == "gin" else (24, 64, 13)  # an output width that is no multiple of 4
+    src, dst, x, w = _small(rng, 500, 3000, dims, agg)
+    p = Pair(500, src, dst, x, w, gemm="bf16", transform_first=tf, edge_w=_edge_w(rng, agg, src.size))
+    try:
+        check_embeddings_conditioned(p, FP32_TOL_BF16, BF16_UNIT)
+        for b in range(40):
+            a, bb = p.orc.graph.arcs()
+            if b % 4 == 3:
+                batch = synth.adversarial_batch(rng, 500, dims[0], bs=30, hot=10, existing=(a, bb),
+                                                weighted=agg == "gc_wsum")
+            else:
+                batch = random_valid_batch(rng, p.orc, 30, dims[0])
+            p.step(batch)
+        res = check_embeddings_conditioned(p, FP32_TOL_BF16, BF16_UNIT)
+        _say("  per layer (max R16 error, rows within the bf16 bound)", res)
+        p.check_arcs()
+    finally:
+        p.close()
+
+
+@pytest.mark.parametrize("agg", ["sum", "gcn", "gin"])
+def test_bf16_thousand_batches(agg):
+    """1000 consecutive batches with bf16 transform operands: sets every 10th batch,
+    embeddings every 250 against the float64 recompute at 2e-2 (R16, or the bf16
+    forward error bound where R16 asks for more than bf16 resolves)."""
+    _say("bf16 1000 batches", agg)
+    rng = np.random.default_rng(131 + AGGS.index(agg))
+    dims = (16, 32, 8)
+    src, dst, x, w = _small(rng, 400, 2400, dims, agg)
+    p = Pair(400, src, dst, x, w, gemm="bf16")
+    try:
+        for b in range(1000):
+            p.step(random_valid_batch(rng, p.orc, 20, dims[0]), check_sets=b % 10 == 0)
+            if (b + 1) % 250 == 0:
+                res = check_embeddings_conditioned(p, FP32_TOL_BF16, BF16_UNIT)
+                _say(f"  batch {b + 1}: {res}")
+        p.check_arcs()
+    finally:
+        p.close()
+
+
+def test_bf16_needs_input_widths_that_are_multiples_of_four():
+    rng = np.random.default_rng(141)
+    src, dst, x, w = _small(rng, 50, 200, (8, 6, 3), "sum")  # the second layer's input is 6 wide
+    lib = Ripple(50, src, dst)
+    try:
+        with pytest.raises(RippleError) as e:
+            lib.init_embeddings(x, w, gemm="bf16")
+        assert e.value.status == E_INVALID and "multiples of 4" in str(e.value)
+        lib.init_embeddings(x, w)  # the fp32 path takes any width
+    finally:
+        lib.close()
