@@ -19,6 +19,7 @@ makes them stale, and then the field is null).
 
     python -m paper_2505_12112_amd.profiling stats TRACE_DIR TITLE COMMAND > profiles/x.txt
     python -m paper_2505_12112_amd.profiling traffic OUT.md COPY_DIR WORKLOAD=FETCH_DIR,WRITE_DIR,BATCHES,CMD ...
+    python -m paper_2505_12112_amd.profiling mfma OUT.md TITLE NAME=DIR,DTYPE,CMD ...
 """
 from __future__ import annotations
 
@@ -95,6 +96,40 @@ def _one(dirpath: str, pattern: str) -> str:
     return hits[0]
 
 
+NETTING = ("k_net_hash", "k_net_direct", "k_net_decide")
+
+
+def workload_segments(trace_dir: str):
+    """Splits a kernel trace into the workloads one process ran: a segment starts at
+    a bootstrap (k_pull) dispatch that follows update batches. Returns, per segment,
+    the per-batch kernel time (netting kernel to netting kernel, the netting
+    kernels of one batch counted together) and each phase's dispatch durations
+    over the segment's batches."""
+    rows = list(csv.DictReader(open(_one(trace_dir, "*kernel_trace.csv"))))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    segs, cur, seen_batch, prev = [], None, False, ""
+    for r in rows:
+        k = kernel_name(r["Kernel_Name"])
+        ns = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        if k.startswith("k_pull<") and (cur is None or seen_batch):
+            cur = {"batches": [], "phases": defaultdict(list)}
+            segs.append(cur)
+            seen_batch = False
+        last, prev = prev, k
+        if cur is None:
+            continue
+        if k in NETTING and last not in NETTING:  # a batch's netting kernels run back to back
+            cur["batches"].append([0, k])
+            seen_batch = True
+        if not cur["batches"]:
+            continue
+        cur["batches"][-1][0] += ns
+        for ph, prefixes in PHASE_KERNELS.items():
+            if k.startswith(prefixes):
+                cur["phases"][ph].append(ns)
+    return segs
+
+
 def stats_table(trace_dir: str, title: str, command: str, top: int = 24) -> str:
     rows = list(csv.DictReader(open(_one(trace_dir, "*kernel_stats.csv"))))
     out = [f"# {title}", "", f"command: {command}", "",
@@ -103,6 +138,21 @@ def stats_table(trace_dir: str, title: str, command: str, top: int = 24) -> str:
         out.append(f"{int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:10.2f} {int(r['MinNs']) / 1e3:10.2f} "
                    f"{int(r['MaxNs']) / 1e3:10.2f} {float(r['TotalDurationNs']) / 1e6:10.3f} "
                    f"{float(r['Percentage']):6.2f}  {kernel_name(r['Name'])}")
+    segs = workload_segments(trace_dir)
+    if segs:
+        out += ["", "Per workload the process ran (in order), over its update batches (bootstrap left out):",
+                "kernel time per batch (first batch, median of the rest) and the average dispatch of each "
+                "rooflined phase (gemm: k_gemm*; scatter: k_scatter*, k_pull_msgs*, k_recompute*)."]
+        for i, sg in enumerate(segs):
+            b = [ns for ns, _ in sg["batches"]]
+            if not b:
+                continue
+            rest = sorted(b[1:]) or b
+            med = rest[len(rest) // 2]
+            ph = "; ".join(f"{p} {len(v)} dispatches avg {sum(v) / len(v) / 1e3:.2f} us"
+                           for p, v in sg["phases"].items() if v)
+            out.append(f"  workload {i}: {len(b)} batches, first {b[0] / 1e6:.3f} ms, median of the rest "
+                       f"{med / 1e6:.3f} ms; {ph}")
     return "\n".join(out) + "\n"
 
 
@@ -170,6 +220,71 @@ def traffic_md(copy_fetch: str, copy_write: str, copy_mib: int, workloads) -> st
     return "\n".join(out) + "\n"
 
 
+def _counters_multi(dirpath: str, batches_only: bool = True):
+    """kernel -> {counter -> list of per-dispatch values} from a counter-collection
+    CSV holding several counters (one row per dispatch and counter)."""
+    rows = list(csv.DictReader(open(_one(dirpath, "*counter_collection.csv"))))
+    t0 = 0
+    if batches_only:
+        starts = [int(r["Start_Timestamp"]) for r in rows
+                  if kernel_name(r["Kernel_Name"]) in ("k_net_hash", "k_net_direct")]
+        t0 = min(starts) if starts else 0
+    d = defaultdict(lambda: defaultdict(list))
+    seen = set()
+    for r in rows:
+        if int(r["Start_Timestamp"]) < t0:
+            continue
+        k = kernel_name(r["Kernel_Name"])
+        d[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+        key = (r.get("Dispatch_Id"), k)
+        if key not in seen:  # one duration per dispatch, whatever the number of counters
+            seen.add(key)
+            d[k]["_ns"].append(float(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
+    return d
+
+
+MFMA_PEAK_TFLOPS = {"F32": 157.3, "BF16": 2500.0}  # dense MFMA peaks of MI355X
+
+
+def mfma_md(title: str, runs, simds: int = 1024, clock_ghz: float = 2.4) -> str:
+    """MFMA use of the transform kernels from runs of --pmc SQ_INSTS_VALU_MFMA_MOPS_<T>
+    SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE: runs = list of (name, dir, command, dtype).
+    Per kernel: MFMA flops per dispatch (MOPS x 512), their rate over the
+    dispatch's duration (counter-run timestamps) against the dtype's dense peak, and
+    the busy fraction of the MFMA units, busy cycles (summed over SIMDs) over the
+    duration's cycles at the nominal clock times the SIMD count. GRBM_GUI_ACTIVE
+    over the duration's cycles is listed as a check: about 8 (it is summed over the
+    XCDs) for long dispatches, more for short ones, whose counting window outlasts
+    the kernel."""
+    out = [f"# {title}", "",
+           f"MFMA flops = SQ_INSTS_VALU_MFMA_MOPS_<T> x 512; rate = flops / dispatch duration; MfmaUtil = "
+           f"SQ_VALU_MFMA_BUSY_CYCLES / (duration x {clock_ghz} GHz x {simds} SIMDs); GUI/dur = GRBM_GUI_ACTIVE / "
+           f"(duration x {clock_ghz} GHz). Dispatches from the first update batch on; durations are those of the "
+           f"counter run (dispatches serialised by the profiler).", ""]
+    for name, d, cmd, dtype in runs:
+        c = _counters_multi(d)
+        mops = f"SQ_INSTS_VALU_MFMA_MOPS_{dtype}"
+        peak = MFMA_PEAK_TFLOPS[dtype]
+        out += [f"## {name}", "", f"command: {cmd}", "",
+                f"| kernel | dispatches | MFMA MFLOP/disp | avg us | TFLOP/s | % of {peak:g} TFLOP/s | "
+                "MFMA busy cycles/disp | MfmaUtil % | GUI/dur |", "|---|---|---|---|---|---|---|---|---|"]
+        for k in sorted(c, key=lambda k: -sum(c[k].get(mops, [0.0]))):
+            m, b, g, ns = (c[k].get(x, []) for x in (mops, "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", "_ns"))
+            if not k.startswith("k_gemm") or not m or not ns:
+                continue
+            n = len(m)
+            fl = 512.0 * sum(m) / n
+            dur = sum(ns) / len(ns)
+            cyc = dur * clock_ghz
+            busy = sum(b) / len(b) if b else 0.0
+            gui = (sum(g) / len(g)) / cyc if g and cyc else 0.0
+            rate = fl / dur / 1e3
+            out.append(f"| {k} | {n} | {fl / 1e6:.2f} | {dur / 1e3:.2f} | {rate:.2f} | {100 * rate / peak:.2f} | "
+                       f"{busy:.0f} | {100 * busy / (cyc * simds):.2f} | {gui:.2f} |")
+        out.append("")
+    return "\n".join(out) + "\n"
+
+
 def read_traffic(workload: str, phase: str):
     """Calibrated HBM bytes per launch of `phase` on `workload` from the committed
     table, or None when there is none or it predates the current sources."""
@@ -187,6 +302,15 @@ def read_traffic(workload: str, phase: str):
 def main(argv):
     if argv[:1] == ["stats"]:
         sys.stdout.write(stats_table(argv[1], argv[2], argv[3]))
+    elif argv[:1] == ["mfma"]:
+        # mfma OUT TITLE NAME=DIR,DTYPE,CMD ...
+        runs = []
+        for spec in argv[3:]:
+            name, rest = spec.split("=", 1)
+            d, dtype, cmd = rest.split(",", 2)
+            runs.append((name, d, cmd, dtype))
+        with open(argv[1], "w") as fh:
+            fh.write(mfma_md(argv[2], runs))
     elif argv[:1] == ["traffic"]:
         out, copy_mib, cf, cw = argv[1], int(argv[2]), argv[3], argv[4]
         wls = []
