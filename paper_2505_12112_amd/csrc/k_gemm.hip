@@ -673,6 +673,7 @@ __global__ __launch_bounds__(W * kWave) void k_gemm_rows(GemmArgs a) {
           }
 #pragma unroll
         for (int g = 0; g < kG; ++g) {
+          if (kc + 32 * g >= ke) break;  // the wave's k range ends inside the round (uniform)
           float4 z[2];
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh) {
@@ -746,6 +747,7 @@ __global__ __launch_bounds__(W * kWave) void k_gemm_rows(GemmArgs a) {
       }
 #pragma unroll
       for (int f = 0; f < kF; ++f) {
+        if (kc + 16 * f >= ke) break;  // the wave's k range ends inside the round (uniform)
         const float ax[4] = {av[f].x, av[f].y, av[f].z, av[f].w};
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
