@@ -68,7 +68,7 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--graphs", action="store_true",
                     help="replay captured HIP graphs instead of queueing every kernel on its own")
-    ap.add_argument("--scatter-mode", default="auto", choices=["auto", "push", "pull", "dense", "recompute"],
+    ap.add_argument("--scatter-mode", default="auto", choices=["auto", "push", "pull", "dense", "recompute", "bucket"],
                     help="how every layer updates its cached aggregates (default: chosen per layer by the library)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-mebibyte device buffer into another (torch copy kernel), ten times: "
@@ -174,12 +174,13 @@ def profiled(lib, staged, phases):
     lib.set_profiling(phases)
     lib.phase_stats()  # reset the sums
     st = BatchStats()
-    modes = {"pull": 0, "dense": 0, "recompute": 0}
+    modes = {"pull": 0, "dense": 0, "recompute": 0, "bucket": 0}
     for _, _, op, no, fp, nf in staged:
         lib.apply_updates_device(op, no, fp, nf, st)
         modes["pull"] |= st.pull_layers
         modes["dense"] |= st.dense_layers
         modes["recompute"] |= st.recompute_layers
+        modes["bucket"] |= st.bucket_layers
     ph = lib.phase_stats()
     lib.set_profiling(())
     return ph, modes
@@ -204,7 +205,7 @@ def roof(p, name, traffic, peak_tflops, gemm_label):
                 "frac": ach / peak_tflops, "algorithmic_per_launch": per, **common}
     per = p["bytes"] / p["launches"]
     ach = per / avg_s / 1e9
-    return {"kernel": "k_scatter / k_pull_msgs / k_recompute (message step)", "bound": "hbm", "achieved": ach,
+    return {"kernel": "k_scatter / k_pull_msgs / k_recompute / k_bucket_fill (message step)", "bound": "hbm", "achieved": ach,
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "algorithmic_per_launch": per,
             "no_reuse_per_launch": p["bytes_no_reuse"] / p["launches"],
             "bytes_note": "algorithmic: each message row read once, each sink row of S read and written once (each "
@@ -299,11 +300,12 @@ def main():
     aff = np.array([s.affected[:L + 1] for s in stats], np.float64).mean(0)
     pushed = np.array([s.pushed_arcs[:L + 1] for s in stats], np.float64).mean(0)
     in_arcs = np.array([s.in_arcs[:L + 1] for s in stats], np.float64).mean(0)
-    forms = {"pull": 0, "dense": 0, "recompute": 0}
+    forms = {"pull": 0, "dense": 0, "recompute": 0, "bucket": 0}
     for s in stats:
         forms["pull"] |= s.pull_layers
         forms["dense"] |= s.dense_layers
         forms["recompute"] |= s.recompute_layers
+        forms["bucket"] |= s.bucket_layers
     replays = sum(s.graph_replay for s in stats)
     relocated = sum(s.relocated_rows for s in stats)
     repacks = sum(s.repacks for s in stats)

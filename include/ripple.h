@@ -193,7 +193,7 @@ typedef struct {
                                    many waves in chunks (graphs whose snapshot has rows of 8192 or more) */
   int32_t recompute_layers;     /* bit l set: layer l recomputed the aggregate rows of A^l from the
                                    current embeddings (re-anchoring; see ripple_set_reanchor) */
-  int32_t reserved;
+  int32_t bucket_layers;        /* bit l set: layer l summed its messages per sink bucket */
 } ripple_batch_stats;
 
 /* Part 1 of the problem statement: copies the snapshot to the device as an
@@ -290,6 +290,11 @@ RIPPLE_API ripple_status ripple_get_arc_weights(ripple_ctx *ctx, int32_t directi
  * current embeddings (reads only, summed in fp64 and rounded once: the
  * layer-wise recompute of Sec. IV-B, to which the incremental path degrades when
  * a hop covers the graph, Sec. VII-C; it also re-anchors the cached rows);
+ * RIPPLE_SCATTER_BUCKET, the pushed arcs sorted by sink (counted, then placed in
+ * per-sink buckets) and each sink's bucket summed and added to its row once (the
+ * messages of Sec. IV-C.1 combined per sink before they reach the aggregate; the
+ * first batch that uses the form allocates 4 bytes per out-arc slot, 8 under the
+ * weighted-sum model, and n counters);
  * RIPPLE_SCATTER_AUTO (default), per layer from the previous batch's counts, or
  * for the first batch from an estimate based on the snapshot's degrees. */
 enum {
@@ -297,7 +302,8 @@ enum {
   RIPPLE_SCATTER_PUSH = 1,
   RIPPLE_SCATTER_PULL = 2,
   RIPPLE_SCATTER_DENSE = 3,
-  RIPPLE_SCATTER_RECOMPUTE = 4
+  RIPPLE_SCATTER_RECOMPUTE = 4,
+  RIPPLE_SCATTER_BUCKET = 5
 };
 RIPPLE_API ripple_status ripple_set_scatter_mode(ripple_ctx *ctx, int32_t mode);
 

@@ -322,6 +322,9 @@ void launch_corr_mark(hipStream_t s, int cap_feat, int cap_arcs, int agg, LayerP
                       const int *ins_dst, const int *del_src, const int *del_dst, const float *ins_w,
                       const float *del_w, unsigned *bm, Counters *c, const DirectList &direct);
 int compact_blocks(long long n);
+// Entries of the bucket form's counter array for n vertices: every vertex of every
+// compaction tile (the compaction reads whole tiles of counters).
+long long bucket_counter_slots(long long n);
 // Outputs of one compaction of bitmaps (a | b) into an ascending list. Optional
 // (nullptr = skipped): list, doff[j] = sum of out_deg over list[0..j) (doff[count]
 // = total), ioff likewise over in_deg, memb[w] = (the compacted bitmap word w,
@@ -345,6 +348,14 @@ struct CompactOut {
   // rows up from several segments)
   float *zero_rows;
   int zero_w;
+  // bucket form (all three set, or none): a vertex with bkt_cnt[v] > 0 counts as
+  // marked in the first bitmap (the sinks are not marked there); boff receives the
+  // prefix of bkt_cnt over the list (boff[count] = the total), and bkt_start[v] the
+  // start of v's bucket for every listed v with bkt_cnt[v] > 0 (bkt_start may alias
+  // bkt_cnt: each count is read before its start is written over it)
+  const int *bkt_cnt;
+  long long *boff;
+  int *bkt_start;
 };
 // The recompute form (launch_recompute) sums an in-row of more than kRecomputeSeg
 // arcs in segments of that many, each added to the row with fp32 atomics.
@@ -408,11 +419,30 @@ struct ScatterList {
 };
 // packed_in: count points at a scatter-built list's packed counter (count and arc
 // total in one word; pushed is then not read).
+// The bucket form's arrays: per-vertex counters (zero between batches), per pushed
+// arc its rank among its sink's arcs, and per bucket slot the source's list
+// position (its message row) and the arc's weight (weighted-sum model only, else
+// null).
+struct Buckets {
+  int *cnt;
+  int *rank;
+  int *idx;
+  float *wt;
+};
+// bk (nullable, marks-only scatters): the bucket form's counting pass; each pushed
+// arc e = (u -> v) takes rank[e] = cnt[v]++ and its sink is not marked in bm_out
+// (the compaction reads the counts instead).
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
                     const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list,
                     const ScatterCopy &copy = ScatterCopy{}, const ScatterList &lo = ScatterList{},
-                    bool packed_in = false);
+                    bool packed_in = false, const Buckets *bk = nullptr);
+// bucket fill: every arc e pushed from list (numbered as the scatter numbers them)
+// goes to slot b.cnt[v] + b.rank[e] of its sink's bucket (b.cnt[v] holds the
+// bucket's start, written by the compaction), which receives the source's list
+// position and, with b.wt, the arc's weight.
+void launch_bucket_fill(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
+                        const u64 *pushed, const Buckets &b, const Counters *c);
 
 // pull: for every vertex v of the sorted list A (in-arc prefix ioff; list null =
 // the identity), S[v] += sum of msg[rank(u)] over in-arcs (u -> v) whose source u
@@ -432,6 +462,14 @@ void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list
 // width of src and S.
 void launch_recompute(hipStream_t s, long long n, int d, int gcn, const int *list, const u64 *count,
                       const long long *ioff, Adj in, const int *out_len, const float *src, float *S, const Counters *c);
+// The bucket form's sums, with the recompute's work split: for every vertex v of
+// the sorted list A (bucket-slot prefix boff), S[v] += the sum over its bucket's
+// slots e of bk.wt[e] (or 1) times message row bk.idx[e] of msg (row stride ld), in
+// fp32; a bucket of at most kRecomputeSeg slots is added with a plain load and
+// store, longer ones in segments with fp32 atomics. Each sink's counter bk.cnt[v]
+// is reset to zero.
+void launch_bucket_sum(hipStream_t s, int d, int ld, const int *list, const u64 *count, const long long *boff,
+                       const Buckets &bk, const float *msg, float *S, const Counters *c);
 
 // bootstrap pull: S[v] = sum over in-arcs c_u H[u]
 void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev, Adj in, const int *out_len,

@@ -12,6 +12,8 @@
 // own scatter, in no particular order: the first setter of a member's bit appends
 // it (see ScatterList). The layer-1 dirty set of a batch without GCN terms is
 // listed by the correction kernel itself, with its deltas.
+#include <type_traits>
+
 #include "internal.h"
 
 namespace rp {
@@ -212,12 +214,38 @@ __device__ inline void load_words(const unsigned *bm_a, const unsigned *bm_b, lo
   }
 }
 
-// Sums of the out- and in-degrees (either may be null) over the cursor's bits.
-// The degrees of the first kBatch bits are kept in d0 / i0 (most threads have no
-// more), so the pass that writes the offsets need not fetch them again.
-__device__ inline void degree_sums(BitCursor c, const int *odeg, const int *ideg, long long &dsum, long long &isum,
-                                   int (&d0)[kBatch], int (&i0)[kBatch]) {
-  if (odeg == nullptr && ideg == nullptr) return;
+// The bucket form's sinks, from their counts: bit b of word w is set when
+// cnt[32 w + b] > 0; they count as first-bitmap bits. The counter array covers
+// every word of every compaction tile (bucket_counter_slots), so all loads are in
+// bounds and go out together; counters past n stay zero.
+__device__ inline void count_words(const int *cnt, long long w0, unsigned (&wv)[kWordsPerThread], int &pop_a) {
+  int4 x[kWordsPerThread][8];
+#pragma unroll
+  for (int i = 0; i < kWordsPerThread; ++i) {
+    const int4 *q = reinterpret_cast<const int4 *>(cnt + (w0 + i) * 32);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) x[i][k] = q[k];
+  }
+#pragma unroll
+  for (int i = 0; i < kWordsPerThread; ++i) {
+    unsigned bits = 0u;
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      bits |= (x[i][k].x > 0 ? 1u : 0u) << (4 * k) | (x[i][k].y > 0 ? 2u : 0u) << (4 * k) |
+              (x[i][k].z > 0 ? 4u : 0u) << (4 * k) | (x[i][k].w > 0 ? 8u : 0u) << (4 * k);
+    wv[i] |= bits;
+    pop_a += __popc(bits);
+  }
+}
+
+// Sums of the out- and in-degrees and bucket counts (any may be null) over the
+// cursor's bits. The values of the first kBatch bits are kept in d0 / i0 / b0
+// (most threads have no more), so the pass that writes the offsets need not fetch
+// them again.
+__device__ inline void degree_sums(BitCursor c, const int *odeg, const int *ideg, const int *bcnt, long long &dsum,
+                                   long long &isum, long long &bsum, int (&d0)[kBatch], int (&i0)[kBatch],
+                                   int (&b0)[kBatch]) {
+  if (odeg == nullptr && ideg == nullptr && bcnt == nullptr) return;
   bool first = true;
   while (!c.empty()) {
     int v[kBatch];
@@ -227,11 +255,14 @@ __device__ inline void degree_sums(BitCursor c, const int *odeg, const int *ideg
     for (int j = 0; j < kBatch; ++j) {
       const int dv = odeg != nullptr && v[j] >= 0 ? odeg[v[j]] : 0;
       const int iv = ideg != nullptr && v[j] >= 0 ? ideg[v[j]] : 0;
+      const int bv = bcnt != nullptr && v[j] >= 0 ? bcnt[v[j]] : 0;
       dsum += dv;
       isum += iv;
+      bsum += bv;
       if (first) {
         d0[j] = dv;
         i0[j] = iv;
+        b0[j] = bv;
       }
     }
     first = false;
@@ -239,8 +270,8 @@ __device__ inline void degree_sums(BitCursor c, const int *odeg, const int *ideg
 }
 
 // Per-tile sums carried by the compaction: marked vertices, their out-degrees,
-// their in-degrees, marked vertices of the first bitmap.
-constexpr int kVals = 4;
+// their in-degrees, marked vertices of the first bitmap, their bucket counts.
+constexpr int kVals = 5;
 
 // Exclusive block scan of kVals values at once (one LDS round).
 __device__ inline void block_scan(const long long (&v)[kVals], long long (&excl)[kVals], long long (&total)[kVals],
@@ -355,13 +386,14 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
     }
   } else {
     load_words(bm_a, bm_b, w0, words, wv, pop_a);
+    if (o.bkt_cnt != nullptr) count_words(o.bkt_cnt, w0, wv, pop_a);
   }
   if (!by_ticket && threadIdx.x == 0) ticket_no = atomicAdd(ticket, 1ull);  // in flight beside the loads
-  long long st[kVals] = {0, 0, 0, pop_a};
+  long long st[kVals] = {0, 0, 0, pop_a, 0};
 #pragma unroll
   for (int i = 0; i < kWordsPerThread; ++i) st[0] += __popc(wv[i]);
-  int d0[kBatch], i0[kBatch];
-  degree_sums(BitCursor(wv, w0), odeg, ideg, st[1], st[2], d0, i0);
+  int d0[kBatch], i0[kBatch], b0[kBatch];
+  degree_sums(BitCursor(wv, w0), odeg, ideg, o.bkt_cnt, st[1], st[2], st[4], d0, i0, b0);
   // The ticket counter only grows and every launch on this scratch has the same
   // number of blocks, each taking one ticket, so launch k holds tickets k * tiles
   // .. k * tiles + tiles - 1: the ticket's quotient names the launch.
@@ -454,7 +486,7 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
   long long base[kVals];
 #pragma unroll
   for (int k = 0; k < kVals; ++k) base[k] = base_s[k];
-  long long pos = base[0] + ex[0], dpos = base[1] + ex[1], ipos = base[2] + ex[2];
+  long long pos = base[0] + ex[0], dpos = base[1] + ex[1], ipos = base[2] + ex[2], bpos = base[4] + ex[4];
   if (o.memb != nullptr) {
     long long wp = pos;
 #pragma unroll
@@ -465,14 +497,15 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
   }
   BitCursor c(wv, w0);
   bool first = true;  // the cursor repeats the first pass's order: its first batch is cached
-  while ((o.list != nullptr || o.doff != nullptr || o.ioff != nullptr) && !c.empty()) {
-    int v[kBatch], dv[kBatch], iv[kBatch];
+  while ((o.list != nullptr || o.doff != nullptr || o.ioff != nullptr || o.boff != nullptr) && !c.empty()) {
+    int v[kBatch], dv[kBatch], iv[kBatch], bv[kBatch];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) v[j] = c.next();
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       dv[j] = o.doff == nullptr || v[j] < 0 ? 0 : first ? d0[j] : odeg[v[j]];
       iv[j] = o.ioff == nullptr || v[j] < 0 ? 0 : first ? i0[j] : ideg[v[j]];
+      bv[j] = o.boff == nullptr || v[j] < 0 ? 0 : first ? b0[j] : o.bkt_cnt[v[j]];
     }
     first = false;
 #pragma unroll
@@ -486,6 +519,11 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
       if (o.ioff != nullptr) {
         o.ioff[pos] = ipos;
         ipos += iv[j];
+      }
+      if (o.boff != nullptr) {  // the count is read above before its start is written over it
+        o.boff[pos] = bpos;
+        if (bv[j] > 0) o.bkt_start[v[j]] = static_cast<int>(bpos);
+        bpos += bv[j];
       }
       if (o.zero_rows != nullptr && iv[j] > kRecomputeSeg) {  // summed in segments by the recompute
         const int slot = atomicAdd(&zcount, 1);
@@ -523,6 +561,7 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(unsigned *bm_a, uns
     *o.count = static_cast<u64>(total);
     if (o.doff != nullptr) o.doff[total] = base[1] + tot[1];
     if (o.ioff != nullptr) o.ioff[total] = base[2] + tot[2];
+    if (o.boff != nullptr) o.boff[total] = base[4] + tot[4];
     if (o.out_total != nullptr) *o.out_total = static_cast<u64>(base[1] + tot[1]);
     if (o.in_total != nullptr) *o.in_total = static_cast<u64>(base[2] + tot[2]);
     if (o.sinks_a != nullptr) *o.sinks_a = static_cast<u64>(base[3] + tot[3]);
@@ -704,7 +743,7 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
                                                  const float *delta, Adj out, float *S, unsigned *bm_out,
                                                  unsigned *bm_x, const int *ins_dst, const int *del_dst,
                                                  const u64 *pushed, const Counters *c, int mark_list,
-                                                 ScatterCopy copy, ScatterList lo, int packed_in) {
+                                                 ScatterCopy copy, ScatterList lo, int packed_in, Buckets bk) {
   const u64 cw = *count;
   const long long nD = static_cast<long long>(packed_in ? cw >> kAppShift : cw);
   const long long E = static_cast<long long>(packed_in ? cw & kAppMask : *pushed);
@@ -825,7 +864,12 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
       v = out.col[slot];
       if (PUSH && out.wt != nullptr) wv = out.wt[slot];
     }
-    if (!LIST && v >= 0) mark_only(bm_out, v);
+    if (!LIST && v >= 0) {
+      if (!PUSH && bk.cnt != nullptr)
+        bk.rank[e] = atomicAdd(&bk.cnt[v], 1);  // the bucket form's count (its sinks are found from it)
+      else
+        mark_only(bm_out, v);
+    }
     const int cnt = PUSH ? static_cast<int>(elast - e0 + 1) : 0;
     for (int i = 0; i < cnt; i += kEdgesPerStep) {
       const int vv = __shfl(v, i + grp);
@@ -848,6 +892,57 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
           if (k < d) unsafeAtomicAdd(&sv[k], ww * dreg[q]);
         }
       }
+    }
+  }
+}
+
+// Bucket form, second pass: the pushed arcs numbered as in the scatter, in chunks
+// of C consecutive arcs per wave (a contiguous run of chunks per wave), each lane
+// resolving one arc's source position j and sink v; the arc's slot is v's bucket
+// start (which the compaction wrote over v's count) plus the rank the counting
+// pass gave it, and receives j, with the arc's weight when the model weights arcs.
+__global__ __launch_bounds__(256) void k_bucket_fill(const int *list, const u64 *count, const long long *doff,
+                                                      Adj out, const u64 *pushed, Buckets b, const Counters *c) {
+  const long long nD = static_cast<long long>(*count);
+  const long long E = static_cast<long long>(*pushed);
+  if (aborted_with(c->abort, nD, E)) return;
+  const int lane = lane_id();
+  const long long waves = num_waves();
+  const long long n1 = nD + 1;  // a compacted list: doff[nD] holds the arc total
+  int C = 1;
+  while (C < kWave && static_cast<long long>(C) * waves < E) C <<= 1;
+  const long long chunks = (E + C - 1) / C;
+  const long long per = (chunks + waves - 1) / waves;
+  const long long c0 = global_wave() * per;
+  const long long c1 = c0 + per < chunks ? c0 + per : chunks;
+  long long ja = -1;
+  for (long long ch = c0; ch < c1; ++ch) {
+    const long long e0 = ch * C;
+    const long long elast = e0 + C - 1 < E - 1 ? e0 + C - 1 : E - 1;
+    ja = ja < 0 ? wave_last_le(doff, 0, n1, e0) : owner_from(doff, ja, n1, e0);
+    const long long jb = C == 1 ? ja : owner_from(doff, ja, n1, elast);
+    const long long e = e0 + lane;
+    const bool active = e <= elast;
+    int j = static_cast<int>(ja);
+    if (jb > ja) {
+      if (jb - ja < kWave) {
+        // the window's offsets, one per lane; every lane takes part in the shuffles
+        const long long mine = ja + lane <= jb ? doff[ja + lane] : (1LL << 62);
+        int cnt_le = 0;
+        for (int t = 0; t <= static_cast<int>(jb - ja); ++t) cnt_le += __shfl(mine, t) <= e ? 1 : 0;
+        j = static_cast<int>(ja) + cnt_le - 1;
+      } else if (active) {
+        j = static_cast<int>(upper_bound(doff, ja, jb + 1, e) - 1);
+      }
+    }
+    if (active) {
+      const int u = list[j];
+      const long long slot = out.off[u] + (e - doff[j]);
+      const int v = out.col[slot];
+      const float w = b.wt != nullptr ? out.wt[slot] : 1.0f;
+      const int at = b.cnt[v] + b.rank[e];
+      b.idx[at] = j;
+      if (b.wt != nullptr) b.wt[at] = w;
     }
   }
 }
@@ -1040,10 +1135,16 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
 // sinks are added with fp32 atomics into rows the compaction zeroed. The last
 // range also owns the sinks past the last arc (rows without in-arcs, stored as
 // zeros).
-template <int G, int NC, int U>
-__global__ __launch_bounds__(256) void k_recompute(int d, int gcn, const int *list, const u64 *count,
+// BK: the bucket form's sums on the same split. The numbered items are bucket
+// slots (ioff is the bucket prefix), a slot holds its message row (stride sld) and
+// weight, sums are fp32 and are added to the row: with a plain load and store
+// when the bucket is one segment, with atomics otherwise. Sinks with empty buckets
+// are left alone; each sink's first segment resets its counter.
+template <int G, int NC, int U, bool BK>
+__global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, const int *list, const u64 *count,
                                                    const long long *ioff, Adj in, const int *out_len,
-                                                   const float *src, float *S, const Counters *c) {
+                                                   const float *src, float *S, const Counters *c, Buckets bk) {
+  using Acc = typename std::conditional<BK, float, double>::type;
   static_assert(G % U == 0 && kRecomputeSeg % G == 0, "steps of U arcs stay within one fetch slot");
   constexpr int kPer = kRecomputeSeg / G;  // arcs fetched per lane
   constexpr int kSteps = kRecomputeSeg / U;
@@ -1052,7 +1153,7 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int gcn, const int *li
   const int lane = lane_id();
   constexpr int kGroups = kWave / G;
   const int grp = lane / G, k0 = lane % G;
-  const bool weighted = in.wt != nullptr;
+  const bool weighted = BK ? bk.wt != nullptr : in.wt != nullptr;
   const long long E = ioff[nA];
   const long long waves = num_waves();
   long long C = 16;
@@ -1103,31 +1204,50 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int gcn, const int *li
         a1 = whole ? b : a + kRecomputeSeg;
       }
       const int v = list != nullptr ? list[j] : static_cast<int>(j);
-      const long long row0 = in.off[v] - ioff[j] + a0;  // slot of the segment's first arc
-      const int na = static_cast<int>(a1 - a0);         // arcs in the segment (<= kRecomputeSeg)
+      const int na = static_cast<int>(a1 - a0);  // arcs in the segment (<= kRecomputeSeg)
+      if (BK && na == 0) continue;                // no message reached the sink (the same for the group)
+      float *sv = S + static_cast<long long>(v) * d;
+      // BK: the row's current values, fetched with the segment's slots (used when the
+      // bucket is one segment; the load is unconditional so that it goes out at once)
+      float prev[NC];
+      if (BK) {
+#pragma unroll
+        for (int p = 0; p < NC; ++p) {
+          const int k = k0 + p * G;
+          prev[p] = sv[k < d ? k : d - 1];
+        }
+      }
+      // BK: slot a0 + i of the buckets; else in-arc a0 + i of the sink's row
+      const long long row0 = BK ? a0 : in.off[v] - ioff[j] + a0;
+      if (BK && k0 == 0 && a0 == ioff[j]) bk.cnt[v] = 0;  // the bucket's start is no longer needed
       // arc i of the segment is fetched by lane i % G of the group, into slot i / G
       int uq[kPer];
-      double cq[kPer];
+      Acc cq[kPer];
 #pragma unroll
       for (int q = 0; q < kPer; ++q) {
         const int i = k0 + q * G;
-        uq[q] = i < na ? in.col[row0 + i] : -1;
-        cq[q] = i < na && weighted ? static_cast<double>(in.wt[row0 + i]) : 1.0;
+        if (BK) {
+          uq[q] = i < na ? bk.idx[row0 + i] : -1;
+          cq[q] = i < na && weighted ? bk.wt[row0 + i] : 1.0f;
+        } else {
+          uq[q] = i < na ? in.col[row0 + i] : -1;
+          cq[q] = i < na && weighted ? static_cast<double>(in.wt[row0 + i]) : 1.0;
+        }
       }
-      if (gcn) {
+      if (!BK && gcn) {
 #pragma unroll
         for (int q = 0; q < kPer; ++q)
           if (uq[q] >= 0) cq[q] /= sqrt(static_cast<double>(out_len[uq[q]]) + 1.0);
       }
-      double acc[NC];
+      Acc acc[NC];
 #pragma unroll
-      for (int q = 0; q < NC; ++q) acc[q] = 0.0;
+      for (int q = 0; q < NC; ++q) acc[q] = 0;
 #pragma unroll
       for (int st = 0; st < kSteps; ++st) {
         if (st * U >= na) break;  // the same for the group's lanes
         const int q = st * U / G;  // the fetch slot of this step's arcs
         int uu[U];
-        double cc[U];
+        Acc cc[U];
 #pragma unroll
         for (int t = 0; t < U; ++t) {
           const int from = grp * G + (st * U + t) % G;
@@ -1141,7 +1261,7 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int gcn, const int *li
         float row[U][NC];
 #pragma unroll
         for (int t = 0; t < U; ++t) {
-          const float *su = src + static_cast<long long>(uu[t] >= 0 ? uu[t] : 0) * d;
+          const float *su = src + static_cast<long long>(uu[t] >= 0 ? uu[t] : 0) * sld;
           const unsigned keep = uu[t] >= 0 ? ~0u : 0u;
 #pragma unroll
           for (int p = 0; p < NC; ++p) {
@@ -1152,14 +1272,13 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int gcn, const int *li
 #pragma unroll
         for (int t = 0; t < U; ++t)
 #pragma unroll
-          for (int p = 0; p < NC; ++p) acc[p] += cc[t] * static_cast<double>(row[t][p]);
+          for (int p = 0; p < NC; ++p) acc[p] += cc[t] * static_cast<Acc>(row[t][p]);
       }
-      float *sv = S + static_cast<long long>(v) * d;
 #pragma unroll
       for (int p = 0; p < NC; ++p) {
         const int k = k0 + p * G;
         if (k < d) {
-          if (whole) sv[k] = static_cast<float>(acc[p]);
+          if (whole) sv[k] = BK ? prev[p] + static_cast<float>(acc[p]) : static_cast<float>(acc[p]);
           else unsafeAtomicAdd(&sv[k], static_cast<float>(acc[p]));
         }
       }
@@ -1244,6 +1363,8 @@ int compact_blocks(long long n) {
   return static_cast<int>((words + kWordsPerBlock - 1) / kWordsPerBlock);
 }
 
+long long bucket_counter_slots(long long n) { return static_cast<long long>(compact_blocks(n)) * kWordsPerBlock * 32; }
+
 void launch_compact(hipStream_t s, long long n, unsigned *bm_a, unsigned *bm_b, const CompactScratch &cs,
                     const CompactOut &o) {
   const long long words = (n + 31) / 32;
@@ -1261,11 +1382,13 @@ long long compact_scratch_words(long long n) { return 2LL * compact_blocks(n) * 
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
                     const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list,
-                    const ScatterCopy &copy, const ScatterList &lo, bool packed_in) {
+                    const ScatterCopy &copy, const ScatterList &lo, bool packed_in, const Buckets *bk) {
   const int blocks = 2048;
+  const Buckets b = bk != nullptr && !push ? *bk : Buckets{};
 #define RP_SCATTER_L(GV, NCV, P, LV)                                                                               \
   RP_LAUNCH((k_scatter<GV, NCV, P, LV>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, doff, delta, out, \
-                     S, bm_out, bm_x, ins_dst, del_dst, pushed, c, mark_list ? 1 : 0, copy, lo, packed_in ? 1 : 0)
+                     S, bm_out, bm_x, ins_dst, del_dst, pushed, c, mark_list ? 1 : 0, copy, lo, packed_in ? 1 : 0, \
+                     b)
 #define RP_SCATTER(GV, NCV, P)                \
   do {                                        \
     if (P && lo.list != nullptr)              \
@@ -1283,6 +1406,11 @@ void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, 
   else RP_SCATTER(64, 16, true);
 #undef RP_SCATTER
 #undef RP_SCATTER_L
+}
+
+void launch_bucket_fill(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
+                        const u64 *pushed, const Buckets &b, const Counters *c) {
+  RP_LAUNCH(k_bucket_fill, dim3(2048), dim3(256), 0, s, list, count, doff, out, pushed, b, c);
 }
 
 void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count,
@@ -1303,22 +1431,38 @@ void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list
 #undef RP_PULLM
 }
 
+#define RP_RECOMP_ALL(BKV)                                                                                     \
+  do {                                                                                                         \
+    if (d <= 16) RP_RECOMP(16, 1, 8, BKV);                                                                     \
+    else if (d <= 32) RP_RECOMP(16, 2, 8, BKV);                                                                \
+    else if (d <= 48) RP_RECOMP(16, 3, 8, BKV);                                                                \
+    else if (d <= 64) RP_RECOMP(16, 4, 8, BKV);                                                                \
+    else if (d <= 128) RP_RECOMP(64, 2, 8, BKV);                                                               \
+    else if (d <= 256) RP_RECOMP(64, 4, 8, BKV);                                                               \
+    else if (d <= 512) RP_RECOMP(64, 8, 4, BKV);                                                               \
+    else RP_RECOMP(64, 16, 2, BKV);                                                                            \
+  } while (0)
+
 void launch_recompute(hipStream_t s, long long n, int d, int gcn, const int *list, const u64 *count,
                       const long long *ioff, Adj in, const int *out_len, const float *src, float *S, const Counters *c) {
   const int blocks = 2048;
-#define RP_RECOMP(GV, NCV, UV)                                                                                   \
-  RP_LAUNCH((k_recompute<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, gcn, list, count, ioff, in, \
-                     out_len, src, S, c)
-  if (d <= 16) RP_RECOMP(16, 1, 8);
-  else if (d <= 32) RP_RECOMP(16, 2, 8);
-  else if (d <= 48) RP_RECOMP(16, 3, 8);
-  else if (d <= 64) RP_RECOMP(16, 4, 8);
-  else if (d <= 128) RP_RECOMP(64, 2, 8);
-  else if (d <= 256) RP_RECOMP(64, 4, 8);
-  else if (d <= 512) RP_RECOMP(64, 8, 4);
-  else RP_RECOMP(64, 16, 2);
+#define RP_RECOMP(GV, NCV, UV, BKV)                                                                              \
+  RP_LAUNCH((k_recompute<GV, NCV, UV, BKV>), dim3(blocks), dim3(256), 0, s, d, d, gcn, list, count, ioff, in, \
+            out_len, src, S, c, Buckets{})
+  RP_RECOMP_ALL(false);
 #undef RP_RECOMP
 }
+
+void launch_bucket_sum(hipStream_t s, int d, int ld, const int *list, const u64 *count, const long long *boff,
+                       const Buckets &bk, const float *msg, float *S, const Counters *c) {
+  const int blocks = 2048;
+#define RP_RECOMP(GV, NCV, UV, BKV)                                                                              \
+  RP_LAUNCH((k_recompute<GV, NCV, UV, BKV>), dim3(blocks), dim3(256), 0, s, d, ld, 0, list, count, boff, Adj{}, \
+            nullptr, msg, S, c, bk)
+  RP_RECOMP_ALL(true);
+#undef RP_RECOMP
+}
+#undef RP_RECOMP_ALL
 
 void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev, Adj in, const int *out_len,
                  float *S) {

@@ -51,6 +51,7 @@ struct PhaseEv {
 // One captured batch: the executable graph of the plan with this key.
 struct GraphSlot {
   unsigned long long key;
+  unsigned long long key2;
   hipGraphExec_t exec;
   unsigned long long used;  // last use, for eviction
 };
@@ -144,6 +145,7 @@ struct ripple_ctx {
   int last_pull = 0;   // layers that pulled over A^l's in-arcs (bit l)
   int last_dense = 0;  // layers that pulled over every in-arc (bit l)
   int last_recompute = 0;  // layers whose aggregate rows of A^l were recomputed (bit l)
+  int last_bucket = 0;     // layers that summed their messages per sink bucket (bit l)
   int last_app = 0;    // layers whose A^l its scatter listed, unordered (bit l), as of the last completed batch
   int run_app = 0;     // the same for the batch in flight (it becomes last_app once that batch completes)
   float *delta[2] = {nullptr, nullptr};
@@ -179,6 +181,11 @@ struct ripple_ctx {
   int *flist = nullptr;
   int *frow = nullptr;  // feature row of each flist entry
   int *flist_done = nullptr;  // [n]: A^0 of the last completed batch (written by its clean-up)
+  // the bucket form's arrays, allocated when a plan first uses the form: per-vertex
+  // counters (zero between batches) and bucket slots for as many arcs as the
+  // out-direction has slots, which bounds the arcs any layer pushes
+  rp::Buckets bkt{nullptr, nullptr, nullptr, nullptr};
+  long long bkt_cap = 0;
   // rows long enough for the chunked delete sweep exist (or may, once rows grow):
   // the plan lists such rows in long_tab, their sweeps record positions in long_pool
   int long_ok = 0;
@@ -533,6 +540,11 @@ void free_model(ripple_ctx *c) {
   dfree_t(c, c->delta[1]);
   dfree_t(c, c->ioff);
   dfree_t(c, c->flist_done);
+  dfree_t(c, c->bkt.cnt);
+  dfree_t(c, c->bkt.rank);
+  dfree_t(c, c->bkt.idx);
+  dfree_t(c, c->bkt.wt);
+  c->bkt_cap = 0;
   for (int k = 0; k < 2; ++k) {
     dfree_t(c, c->memb[k]);
   }
@@ -737,17 +749,24 @@ void add_launches(ripple_ctx *c, int phase, int k) {
 //   recompute  the pull's marks, then every in-arc of A^l carries its source's row
 //              (15 ps per arc plus the row at 6 TB/s, the rate of random row reads
 //              from a table larger than the caches), one plain row store per
-//              affected vertex at 5 TB/s.
+//              affected vertex at 5 TB/s;
+//   bucket     104 ps per pushed arc (its count and rank, its bucket slot written,
+//              read back and its message row summed), one read-modify-write of
+//              each affected row at 0.87 TB/s, and 10 us for the two extra
+//              launches (fitted to the form's kernels on dense_large's second
+//              layer at batches 100 and 1000).
 // Every reanchor_every-th batch recomputes every layer (the drift budget), whatever
 // the form.
-enum LayerMode { kPushLayer = 0, kPullLayer = 1, kDenseLayer = 2, kRecomputeLayer = 3 };
+enum LayerMode { kPushLayer = 0, kPullLayer = 1, kDenseLayer = 2, kRecomputeLayer = 3, kBucketLayer = 4 };
 
 int layer_mode(const ripple_ctx *c, int l, double pushed, double count, double in_arcs, bool reanchor) {
   if (reanchor || c->scatter_mode == RIPPLE_SCATTER_RECOMPUTE) return kRecomputeLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_PUSH) return kPushLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_PULL) return kPullLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_DENSE) return kDenseLayer;
+  if (c->scatter_mode == RIPPLE_SCATTER_BUCKET) return kBucketLayer;
   constexpr double kArc = 90e-12, kAtomicRate = 1.3e12, kMark = 38e-12, kPullScan = 35e-12;
+  constexpr double kBucketArc = 104e-12, kBucketRowRate = 0.87e12, kBucketFixed = 10e-6;
   constexpr double kDenseScan = 25e-12, kDenseVertex = 20e-12, kReadRate = 10e12;
   constexpr double kRecScan = 15e-12, kGatherRate = 6e12, kStoreRate = 5e12;
   const double w = 4.0 * c->sw[l];  // message row bytes
@@ -756,11 +775,13 @@ int layer_mode(const ripple_ctx *c, int l, double pushed, double count, double i
   const double pull = pushed * kMark + in_arcs * kPullScan + settle;
   const double dense = static_cast<double>(c->arcs_now) * kDenseScan + static_cast<double>(c->n) * kDenseVertex + settle;
   const double recompute = pushed * kMark + in_arcs * (kRecScan + w / kGatherRate) + count * w / kStoreRate;
+  const double bucket = pushed * kBucketArc + count * w / kBucketRowRate + kBucketFixed;
   int best = kPushLayer;
   double t = push;
   if (pull < t) best = kPullLayer, t = pull;
   if (dense < t) best = kDenseLayer, t = dense;
   if (recompute < t) best = kRecomputeLayer, t = recompute;
+  if (bucket < t) best = kBucketLayer, t = bucket;
   return best;
 }
 
@@ -828,6 +849,7 @@ struct BatchPlan {
   bool arena_plan;                     // the arena check runs (else every possible row move fits)
   bool net_direct;                     // netting in one launch (small batches)
   unsigned long long key;              // the above as GEMM variants, and the counter parity
+  unsigned long long key2;             // bit l: layer l takes the bucket form (its mode bits in key read push)
 };
 
 // Pushed arcs up to which a layer's scatter lists A^l itself, and that the next
@@ -858,7 +880,8 @@ BatchPlan make_plan(const ripple_ctx *c) {
     p.mode[l] = layer_mode(c, l, pushed[l], count[l], in_arcs[l], reanchor);
     p.tf_rows[l] = guess[l - 1];
     p.rows[l] = guess[l];
-    key |= static_cast<unsigned long long>(p.mode[l]) << bit;
+    if (p.mode[l] == kBucketLayer) p.key2 |= 1ull << l;
+    key |= static_cast<unsigned long long>(p.mode[l] & 3) << bit;
     key |= static_cast<unsigned long long>(rp::gemm_variant(p.tf_rows[l])) << (bit + 2);
     key |= static_cast<unsigned long long>(rp::gemm_variant(p.rows[l])) << (bit + 4);
     bit += 6;  // up to bit 48 for 8 layers
@@ -1053,7 +1076,7 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
                              c->adj[0].len, c->adj[1].len};
       rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], count_in, c->doff[l - 1], msg, out_msg, c->S[l],
                          c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc, mode == kPushLayer,
-                         rp::has_self_term(c->agg), copy, lo, packed_in);
+                         rp::has_self_term(c->agg), copy, lo, packed_in, mode == kBucketLayer ? &c->bkt : nullptr);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     if (!app) {
@@ -1068,6 +1091,11 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
       if (mode == kRecomputeLayer) {  // rows summed in segments start from zero
         co.zero_rows = c->S[l];
         co.zero_w = c->sw[l];
+      }
+      if (mode == kBucketLayer) {  // the sinks from their counts; the buckets' offsets (in ioff) and starts
+        co.bkt_cnt = c->bkt.cnt;
+        co.boff = c->ioff;
+        co.bkt_start = c->bkt.cnt;
       }
       co.in_total = &dc->indeg[l];
       co.out_total = l < c->L ? &dc->pushed[l + 1] : nullptr;
@@ -1090,6 +1118,16 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
       rp::launch_recompute(s, c->n, c->sw[l], c->agg == rp::kGcn ? 1 : 0, c->lists[l], &dc->count[l], c->ioff,
                            in_msg, c->adj[0].len, layer_ptrs(c).src[l], c->S[l], dc);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
+    } else if (mode == kBucketLayer) {
+      // each pushed arc placed in its sink's bucket, then each sink's bucket summed
+      // into its row (D is a compacted list here: a scatter lists A^{l-1} only when
+      // layer l pushes, and the corrections kernel lists A^0 only when layer 1 does)
+      PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
+      rp::Buckets b = c->bkt;
+      if (out_msg.wt == nullptr) b.wt = nullptr;
+      rp::launch_bucket_fill(s, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], out_msg, &dc->pushed[l], b, dc);
+      rp::launch_bucket_sum(s, c->sw[l], ld, c->lists[l], &dc->count[l], c->ioff, b, msg, c->S[l], dc);
+      add_launches(c, RIPPLE_PHASE_SCATTER, 2);
     }
     {
       // the last layer's GEMM also resets the batch's scratch (extra blocks)
@@ -1107,7 +1145,7 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
 hipGraphExec_t plan_graph(ripple_ctx *c, const BatchPlan &p) {
   constexpr size_t kMaxGraphs = 16;
   for (GraphSlot &g : c->graphs) {
-    if (g.key == p.key) {
+    if (g.key == p.key && g.key2 == p.key2) {
       g.used = ++c->graph_clock;
       return g.exec;
     }
@@ -1134,14 +1172,39 @@ hipGraphExec_t plan_graph(ripple_ctx *c, const BatchPlan &p) {
     (void)hipGraphExecDestroy(old->exec);
     c->graphs.erase(old);
   }
-  c->graphs.push_back(GraphSlot{p.key, exec, ++c->graph_clock});
+  c->graphs.push_back(GraphSlot{p.key, p.key2, exec, ++c->graph_clock});
   return exec;
+}
+
+// The bucket form's arrays, allocated (or grown with the out-direction's slots) when
+// a plan first needs them; the counters start at zero and every batch leaves them
+// so.
+ripple_status ensure_buckets(ripple_ctx *c) {
+  if (c->bkt.cnt == nullptr) {
+    const long long slots = rp::bucket_counter_slots(c->n);
+    RP_TRY(dalloc_n(c, &c->bkt.cnt, slots));
+    RP_HIP(c, hipMemsetAsync(c->bkt.cnt, 0, static_cast<size_t>(slots) * sizeof(int), c->stream));
+  }
+  const long long need = std::max<long long>(1, c->col_capacity[0]);
+  if (c->bkt_cap < need) {
+    dfree_t(c, c->bkt.rank);
+    dfree_t(c, c->bkt.idx);
+    dfree_t(c, c->bkt.wt);
+    c->bkt_cap = 0;
+    RP_TRY(dalloc_n(c, &c->bkt.rank, need));
+    RP_TRY(dalloc_n(c, &c->bkt.idx, need));
+    if (c->agg == rp::kGcWsum) RP_TRY(dalloc_n(c, &c->bkt.wt, need));
+    c->bkt_cap = need;
+  }
+  return RIPPLE_OK;
 }
 
 // Queues one batch whose inputs are in c->h_in: as a graph replay unless graphs
 // are off or this batch records phase events.
 ripple_status launch_batch(ripple_ctx *c) {
   const BatchPlan p = make_plan(c);
+  if (p.key2 != 0) RP_TRY(ensure_buckets(c));
+  c->last_bucket = static_cast<int>(p.key2);
   c->last_pull = 0;
   c->last_dense = 0;
   c->last_recompute = 0;
@@ -1192,7 +1255,7 @@ void account_phases(ripple_ctx *c) {
       // without on-chip reuse: a message row read per arc that carries it, and under
       // push a row of atomics per arc rather than per sink
       c->ph_extra[RIPPLE_PHASE_SCATTER] += 4.0 * d * std::max(per_arc - nd, 0.0);
-      if (!((c->last_pull | c->last_dense) >> l & 1))
+      if (!((c->last_pull | c->last_dense | c->last_bucket) >> l & 1))
         c->ph_extra[RIPPLE_PHASE_SCATTER] += 8.0 * d * std::max(per_arc - sinks, 0.0);
     }
     if (c->last_pull >> l & 1)  // pull: every in-arc id of A^l and its in-row offset
@@ -1810,6 +1873,7 @@ ripple_status run_batch(ripple_ctx *c, int B, long long num_feat_rows, const rip
     stats->pull_layers = c->last_pull;
     stats->dense_layers = c->last_dense;
     stats->recompute_layers = c->last_recompute;
+    stats->bucket_layers = c->last_bucket;
     stats->graph_replay = c->last_graph ? 1 : 0;
     stats->long_rows = static_cast<int64_t>(k.long_rows >> 40);
   }
@@ -2032,7 +2096,7 @@ ripple_status ripple_get_arc_weights(ripple_ctx *c, int32_t direction, float *we
 
 ripple_status ripple_set_scatter_mode(ripple_ctx *c, int32_t mode) {
   RP_TRY(check_ctx(c));
-  if (mode < RIPPLE_SCATTER_AUTO || mode > RIPPLE_SCATTER_RECOMPUTE) return fail(c, RIPPLE_E_INVALID, "ripple: bad mode");
+  if (mode < RIPPLE_SCATTER_AUTO || mode > RIPPLE_SCATTER_BUCKET) return fail(c, RIPPLE_E_INVALID, "ripple: bad mode");
   c->scatter_mode = mode;
   return RIPPLE_OK;
 }

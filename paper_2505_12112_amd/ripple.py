@@ -32,7 +32,7 @@ EXPORTED = [
     "ripple_destroy", "ripple_set_scatter_mode", "ripple_apply_updates_device", "ripple_get_arc_weights",
     "ripple_set_graphs", "ripple_set_reanchor", "ripple_get_embeddings_static",
 ]
-SCATTER = {"auto": 0, "push": 1, "pull": 2, "dense": 3, "recompute": 4}
+SCATTER = {"auto": 0, "push": 1, "pull": 2, "dense": 3, "recompute": 4, "bucket": 5}
 
 
 class RippleUnavailable(RuntimeError):
@@ -75,7 +75,7 @@ class BatchStats(C.Structure):
         ("relocated_rows", C.c_int64), ("repacks", C.c_int64),
         ("in_arcs", C.c_int64 * (MAX_LAYERS + 1)), ("pull_layers", C.c_int32), ("dense_layers", C.c_int32),
         ("reweighted_arcs", C.c_int64), ("graph_replay", C.c_int64), ("long_rows", C.c_int64),
-        ("recompute_layers", C.c_int32), ("reserved", C.c_int32),
+        ("recompute_layers", C.c_int32), ("bucket_layers", C.c_int32),
     ]
 
 
@@ -261,6 +261,7 @@ class Ripple:
             "in_arcs": list(st.in_arcs[:L + 1]), "pull_layers": st.pull_layers, "dense_layers": st.dense_layers,
             "reweighted_arcs": st.reweighted_arcs, "graph_replay": st.graph_replay, "long_rows": st.long_rows,
             "recompute_layers": st.recompute_layers,
+            "bucket_layers": st.bucket_layers,
         }
 
     def apply_updates_raw(self, ops: np.ndarray, feat_rows: Optional[np.ndarray], stats: BatchStats) -> None:

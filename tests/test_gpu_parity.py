@@ -54,7 +54,7 @@ def test_bootstrap_matches_full_recompute(agg, dims):
 
 @pytest.mark.parametrize("launch", ["graph", "direct"])
 @pytest.mark.parametrize("inputs", ["host", "device"])
-@pytest.mark.parametrize("mode", ["push", "pull", "dense", "recompute"])
+@pytest.mark.parametrize("mode", ["push", "pull", "dense", "recompute", "bucket"])
 def test_tiny_config_stream(mode, inputs, launch):
     """The tiny workload as specified: 10 batches of 45 inserts, 45 deletes, 10
     features, handed over from host memory or already resident in device memory,
@@ -75,7 +75,7 @@ def test_tiny_config_stream(mode, inputs, launch):
 
 @pytest.mark.parametrize("agg", AGGS)
 @pytest.mark.parametrize("undirected", [False, True])
-@pytest.mark.parametrize("mode", ["push", "pull", "dense", "recompute"])
+@pytest.mark.parametrize("mode", ["push", "pull", "dense", "recompute", "bucket"])
 def test_adversarial_batches(agg, undirected, mode):
     """Colliding ops: repeated inserts/deletes of one edge, insert-then-delete,
     absent deletes, self-loops, repeated feature writes (sequential semantics)."""
@@ -141,7 +141,9 @@ def _hub_graph(rng, n, hub_in, hub_out, extra, undirected):
 @pytest.mark.parametrize("agg,slack,undirected,mode", [("sum", 0.25, False, "auto"), ("gcn", 0.25, False, "auto"),
                                                        ("sum", 0.0, False, "auto"), ("mean", 0.25, True, "auto"),
                                                        ("gcn", 0.25, False, "recompute"),
-                                                       ("sum", 0.25, True, "recompute")])
+                                                       ("sum", 0.25, True, "recompute"),
+                                                       ("gcn", 0.25, False, "bucket"),
+                                                       ("sum", 0.0, True, "bucket")])
 def test_long_rows_swept_in_chunks(agg, slack, undirected, mode):
     """A hub with ~20,000 in- and out-arcs: batches that delete and insert hub arcs.
     Rows of 16384 entries or more that keep their slots have their deletes swept by
@@ -215,7 +217,7 @@ def test_no_slack_forces_row_moves_and_relayouts(agg, arena):
 
 @pytest.mark.parametrize("agg", ["sum", "mean", "gcn"])
 @pytest.mark.parametrize("tf", [0, 1])
-@pytest.mark.parametrize("mode", ["push", "pull", "dense", "recompute"])
+@pytest.mark.parametrize("mode", ["push", "pull", "dense", "recompute", "bucket"])
 def test_transform_first_choice_gives_the_same_results(agg, tf, mode):
     """Caching W_neigh S instead of S (and pushing W_neigh times the deltas) on
     every layer, or on none, matches the oracle like the default choice."""
@@ -334,16 +336,16 @@ def test_degenerate_and_extreme_shapes(case):
         p.close()
 
 
-@pytest.mark.parametrize("mode", ["push", "pull", "dense", "recompute"])
+@pytest.mark.parametrize("mode", ["push", "pull", "dense", "recompute", "bucket"])
 def test_phase_stats_count_launches_and_bytes(mode):
     """Phase events: every phase of a profiled batch is timed, the launches are
     counted per phase (one netting (two for batches over 1024 ops), one topology (the arena check only when the
     spare arena might not hold the batch's row moves), three layer-0 launches per
     batch, one when layer 1 pushes: the corrections kernel then lists the
     feature-written vertices and their deltas itself; per layer one message launch when pushing,
-    two when pulling; a pushing layer's scatter lists A^l itself, a pulling one
-    compacts it, and the dense form's full listing counts with the
-    compactions), and the no-reuse byte bound
+    two when pulling, three in the bucket form (count, fill, sum); a pushing layer's
+    scatter lists A^l itself, the other forms compact it, and the dense form's full
+    listing counts with the compactions), and the no-reuse byte bound
     of the message step is at least its algorithmic bytes."""
     rng = np.random.default_rng(51)
     dims = (8, 16, 4)
@@ -362,8 +364,8 @@ def test_phase_stats_count_launches_and_bytes(mode):
         # (one netting launch: batches of up to 1024 ops are netted in one pass)
         assert ph["net"]["launches"] == nb and ph["topo"]["launches"] == nb
         assert ph["layer0"]["launches"] == (1 if mode == "push" else 3) * nb
-        assert ph["scatter"]["launches"] == (1 if mode == "push" else 2) * L * nb
-        assert ph["compact"]["launches"] == {"push": 0, "pull": 1, "dense": 2, "recompute": 1}[mode] * L * nb
+        assert ph["scatter"]["launches"] == {"push": 1, "bucket": 3}.get(mode, 2) * L * nb
+        assert ph["compact"]["launches"] == {"push": 0, "pull": 1, "dense": 2, "recompute": 1, "bucket": 1}[mode] * L * nb
         assert ph["gemm"]["launches"] == L * nb and ph["total"]["launches"] == nb
         for name in ("net", "topo", "layer0", "scatter", "compact", "gemm", "total"):
             if name == "compact" and mode == "push":
@@ -511,7 +513,9 @@ def test_call_order_and_device_byte_cap():
                          [(a, m, "direct") for a in ("sum", "mean", "gcn") for m in ("auto", "pull", "dense")]
                          + [(a, m, "direct") for a in ("gc_sum", "gc_mean", "gin", "gc_wsum") for m in ("auto", "dense")]
                          + [(a, "recompute", "direct") for a in AGGS]
-                         + [("sum", "auto", "graph"), ("gcn", "dense", "graph"), ("gin", "auto", "graph")])
+                         + [(a, "bucket", "direct") for a in AGGS]
+                         + [("sum", "auto", "graph"), ("gcn", "dense", "graph"), ("gin", "auto", "graph"),
+                            ("gc_wsum", "bucket", "graph")])
 def test_thousand_batches_on_a_small_graph(agg, mode, launch):
     """1000 consecutive batches: sets every batch, embeddings every 100 and at the
     end; with launch "graph" every batch replays a captured graph."""
@@ -622,7 +626,7 @@ def test_failed_device_check_poisons_the_context(monkeypatch):
 
 @pytest.mark.parametrize("agg", ["sum", "gcn"])
 @pytest.mark.parametrize("dims", [(100, 256, 256, 47), (96, 128, 200, 8)])
-@pytest.mark.parametrize("mode", ["pull", "dense", "recompute"])
+@pytest.mark.parametrize("mode", ["pull", "dense", "recompute", "bucket"])
 def test_pull_and_dense_at_wide_message_rows(agg, dims, mode):
     """Message rows 96 to 256 floats wide (the pull kernel's 64-lane groups, two
     or four floats per lane) in the forced pull and dense forms, on a graph of
@@ -643,7 +647,8 @@ def test_pull_and_dense_at_wide_message_rows(agg, dims, mode):
             else:
                 batch = random_valid_batch(rng, p.orc, 40, dims[0])
             st, _, _ = p.step(batch)
-            want = {"pull": "pull_layers", "dense": "dense_layers", "recompute": "recompute_layers"}[mode]
+            want = {"pull": "pull_layers", "dense": "dense_layers", "recompute": "recompute_layers",
+                    "bucket": "bucket_layers"}[mode]
             assert st[want] == sum(1 << l for l in range(1, len(dims))), st
         p.check_embeddings()
         p.check_aggregates()
@@ -652,7 +657,7 @@ def test_pull_and_dense_at_wide_message_rows(agg, dims, mode):
         p.close()
 
 
-@pytest.mark.parametrize("mode", ["pull", "dense", "recompute"])
+@pytest.mark.parametrize("mode", ["pull", "dense", "recompute", "bucket"])
 def test_pull_and_dense_at_the_widest_rows(mode):
     """Message rows of 512 and 1024 floats (eight and sixteen floats per lane) in
     the forced pull and dense forms."""
@@ -679,7 +684,7 @@ def _hub_heavy_chung_lu(rng, n, m):
 
 
 @pytest.mark.parametrize("agg", ["sum", "gcn"])
-@pytest.mark.parametrize("mode", ["auto", "push", "dense", "recompute"])
+@pytest.mark.parametrize("mode", ["auto", "push", "dense", "recompute", "bucket"])
 def test_thousand_batches_on_a_hub_heavy_graph_with_narrow_rows(agg, mode):
     """1000 consecutive batches on a power-law graph (4,000 vertices, 48,000 arcs,
     largest degrees in the hundreds) with narrow rows (8-6-4): a hub's cached
@@ -693,7 +698,8 @@ def test_thousand_batches_on_a_hub_heavy_graph_with_narrow_rows(agg, mode):
     batch re-anchors (the drift budget, whatever the form); mode "recompute"
     re-anchors in every batch."""
     _say("hub-heavy 1000 batches", agg, mode)
-    rng = np.random.default_rng(83 + 5 * ("sum", "gcn").index(agg) + ("auto", "push", "dense", "recompute").index(mode))
+    rng = np.random.default_rng(83 + 5 * ("sum", "gcn").index(agg)
+                                + ("auto", "push", "dense", "recompute", "bucket").index(mode))
     dims = (8, 6, 4)
     n = 4000
     src, dst = _hub_heavy_chung_lu(rng, n, 48000)
