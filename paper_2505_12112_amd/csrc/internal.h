@@ -429,18 +429,21 @@ struct Buckets {
   int *idx;
   float *wt;
 };
-// bk (nullable, marks-only scatters): the bucket form's counting pass; each pushed
-// arc e = (u -> v) takes rank[e] = cnt[v]++ and its sink is not marked in bm_out
-// (the compaction reads the counts instead).
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
                     const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list,
                     const ScatterCopy &copy = ScatterCopy{}, const ScatterList &lo = ScatterList{},
-                    bool packed_in = false, const Buckets *bk = nullptr);
-// bucket fill: every arc e pushed from list (numbered as the scatter numbers them)
-// goes to slot b.cnt[v] + b.rank[e] of its sink's bucket (b.cnt[v] holds the
-// bucket's start, written by the compaction), which receives the source's list
-// position and, with b.wt, the arc's weight.
+                    bool packed_in = false);
+// bucket count (in place of the marks-only scatter): marks the net arcs' heads and,
+// with mark_list, the list in bm_x; every arc e = (u -> v) pushed from the sorted
+// list (numbered as the scatter numbers them) takes rank[e] = b.cnt[v]++, and its
+// sink is not marked (the compaction finds the sinks from the counts).
+void launch_bucket_count(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
+                         const u64 *pushed, const Buckets &b, unsigned *bm_x, const int *ins_dst, const int *del_dst,
+                         bool mark_list, const Counters *c);
+// bucket fill: every pushed arc e goes to slot b.cnt[v] + b.rank[e] of its sink's
+// bucket (b.cnt[v] holds the bucket's start, written by the compaction), which
+// receives the source's list position and, with b.wt, the arc's weight.
 void launch_bucket_fill(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
                         const u64 *pushed, const Buckets &b, const Counters *c);
 

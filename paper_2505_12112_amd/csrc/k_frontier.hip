@@ -743,7 +743,7 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
                                                  const float *delta, Adj out, float *S, unsigned *bm_out,
                                                  unsigned *bm_x, const int *ins_dst, const int *del_dst,
                                                  const u64 *pushed, const Counters *c, int mark_list,
-                                                 ScatterCopy copy, ScatterList lo, int packed_in, Buckets bk) {
+                                                 ScatterCopy copy, ScatterList lo, int packed_in) {
   const u64 cw = *count;
   const long long nD = static_cast<long long>(packed_in ? cw >> kAppShift : cw);
   const long long E = static_cast<long long>(packed_in ? cw & kAppMask : *pushed);
@@ -864,12 +864,7 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
       v = out.col[slot];
       if (PUSH && out.wt != nullptr) wv = out.wt[slot];
     }
-    if (!LIST && v >= 0) {
-      if (!PUSH && bk.cnt != nullptr)
-        bk.rank[e] = atomicAdd(&bk.cnt[v], 1);  // the bucket form's count (its sinks are found from it)
-      else
-        mark_only(bm_out, v);
-    }
+    if (!LIST && v >= 0) mark_only(bm_out, v);
     const int cnt = PUSH ? static_cast<int>(elast - e0 + 1) : 0;
     for (int i = 0; i < cnt; i += kEdgesPerStep) {
       const int vv = __shfl(v, i + grp);
@@ -896,21 +891,41 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
   }
 }
 
-// Bucket form, second pass: the pushed arcs numbered as in the scatter, in chunks
-// of C consecutive arcs per wave (a contiguous run of chunks per wave), each lane
-// resolving one arc's source position j and sink v; the arc's slot is v's bucket
-// start (which the compaction wrote over v's count) plus the rank the counting
-// pass gave it, and receives j, with the arc's weight when the model weights arcs.
-__global__ __launch_bounds__(256) void k_bucket_fill(const int *list, const u64 *count, const long long *doff,
-                                                      Adj out, const u64 *pushed, Buckets b, const Counters *c) {
+constexpr int kPullArcs = 4;  // arcs per lane per chunk (the pull and the bucket passes)
+constexpr int kPullChunk = kWave * kPullArcs;
+
+// The bucket form's passes over the pushed arcs (numbered as in the scatter), in
+// chunks of up to kPullChunk consecutive arcs per wave (a contiguous run of chunks
+// per wave), each lane up to kPullArcs consecutive arcs with all their loads in
+// flight together. The counting pass (FILL false) first marks the net arcs' heads
+// and, under a self term, D in bm_x, then gives each arc e into sink v its rank
+// among v's arcs, rank[e] = cnt[v]++ (the sinks are found from the counts). The
+// fill pass writes the arc's source position j (its message row), and its weight
+// when the model weights arcs, to slot cnt[v] + rank[e] of v's bucket, cnt[v]
+// then holding the bucket's start.
+template <bool FILL>
+__global__ __launch_bounds__(256) void k_bucket_arcs(const int *list, const u64 *count, const long long *doff,
+                                                      Adj out, const u64 *pushed, Buckets b, unsigned *bm_x,
+                                                      const int *ins_dst, const int *del_dst, int mark_list,
+                                                      const Counters *c) {
   const long long nD = static_cast<long long>(*count);
   const long long E = static_cast<long long>(*pushed);
-  if (aborted_with(c->abort, nD, E)) return;
+  const long long ni = static_cast<long long>(c->n_ins);
+  const long long na = ni + static_cast<long long>(c->n_del);
+  if (aborted_with(c->abort, nD, E, na)) return;
   const int lane = lane_id();
+  if (!FILL) {
+    const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
+    const long long t0 = blockIdx.x * blockDim.x + threadIdx.x;
+    for (long long i = t0; i < na; i += stride) mark_only(bm_x, i < ni ? ins_dst[i] : del_dst[i - ni]);
+    if (mark_list)
+      for (long long j = t0; j < nD; j += stride) mark_only(bm_x, list[j]);
+  }
   const long long waves = num_waves();
   const long long n1 = nD + 1;  // a compacted list: doff[nD] holds the arc total
   int C = 1;
-  while (C < kWave && static_cast<long long>(C) * waves < E) C <<= 1;
+  while (C < kPullChunk && static_cast<long long>(C) * waves < E) C <<= 1;
+  const int per_lane = C > kWave ? C / kWave : 1;
   const long long chunks = (E + C - 1) / C;
   const long long per = (chunks + waves - 1) / waves;
   const long long c0 = global_wave() * per;
@@ -921,28 +936,63 @@ __global__ __launch_bounds__(256) void k_bucket_fill(const int *list, const u64 
     const long long elast = e0 + C - 1 < E - 1 ? e0 + C - 1 : E - 1;
     ja = ja < 0 ? wave_last_le(doff, 0, n1, e0) : owner_from(doff, ja, n1, e0);
     const long long jb = C == 1 ? ja : owner_from(doff, ja, n1, elast);
-    const long long e = e0 + lane;
-    const bool active = e <= elast;
-    int j = static_cast<int>(ja);
+    long long e[kPullArcs];
+    int r[kPullArcs];
+    bool on[kPullArcs];
+#pragma unroll
+    for (int a = 0; a < kPullArcs; ++a) {
+      e[a] = e0 + static_cast<long long>(lane) * per_lane + a;
+      on[a] = a < per_lane && e[a] <= elast;
+      r[a] = static_cast<int>(ja);
+    }
     if (jb > ja) {
       if (jb - ja < kWave) {
         // the window's offsets, one per lane; every lane takes part in the shuffles
         const long long mine = ja + lane <= jb ? doff[ja + lane] : (1LL << 62);
-        int cnt_le = 0;
-        for (int t = 0; t <= static_cast<int>(jb - ja); ++t) cnt_le += __shfl(mine, t) <= e ? 1 : 0;
-        j = static_cast<int>(ja) + cnt_le - 1;
-      } else if (active) {
-        j = static_cast<int>(upper_bound(doff, ja, jb + 1, e) - 1);
+        int cnt[kPullArcs] = {};
+        for (int t = 0; t <= static_cast<int>(jb - ja); ++t) {
+          const long long o = __shfl(mine, t);
+#pragma unroll
+          for (int a = 0; a < kPullArcs; ++a) cnt[a] += o <= e[a] ? 1 : 0;
+        }
+#pragma unroll
+        for (int a = 0; a < kPullArcs; ++a) r[a] = static_cast<int>(ja) + cnt[a] - 1;
+      } else {
+#pragma unroll
+        for (int a = 0; a < kPullArcs; ++a)
+          if (on[a]) r[a] = static_cast<int>(upper_bound(doff, ja, jb + 1, e[a]) - 1);
       }
     }
-    if (active) {
-      const int u = list[j];
-      const long long slot = out.off[u] + (e - doff[j]);
-      const int v = out.col[slot];
-      const float w = b.wt != nullptr ? out.wt[slot] : 1.0f;
-      const int at = b.cnt[v] + b.rank[e];
-      b.idx[at] = j;
-      if (b.wt != nullptr) b.wt[at] = w;
+    long long slot[kPullArcs];
+    int v[kPullArcs];
+#pragma unroll
+    for (int a = 0; a < kPullArcs; ++a) {
+      const int u = on[a] ? list[r[a]] : 0;
+      slot[a] = on[a] ? out.off[u] + (e[a] - doff[r[a]]) : 0;
+    }
+#pragma unroll
+    for (int a = 0; a < kPullArcs; ++a) v[a] = on[a] ? out.col[slot[a]] : -1;
+    if (!FILL) {
+      int rk[kPullArcs];
+#pragma unroll
+      for (int a = 0; a < kPullArcs; ++a) rk[a] = on[a] ? atomicAdd(&b.cnt[v[a]], 1) : 0;
+#pragma unroll
+      for (int a = 0; a < kPullArcs; ++a)
+        if (on[a]) b.rank[e[a]] = rk[a];
+    } else {
+      int at[kPullArcs];
+      float w[kPullArcs];
+#pragma unroll
+      for (int a = 0; a < kPullArcs; ++a) {
+        at[a] = on[a] ? b.cnt[v[a]] + b.rank[e[a]] : 0;
+        w[a] = on[a] && b.wt != nullptr ? out.wt[slot[a]] : 1.0f;
+      }
+#pragma unroll
+      for (int a = 0; a < kPullArcs; ++a) {
+        if (!on[a]) continue;
+        b.idx[at[a]] = r[a];
+        if (b.wt != nullptr) b.wt[at[a]] = w[a];
+      }
     }
   }
 }
@@ -960,8 +1010,6 @@ __global__ __launch_bounds__(256) void k_bucket_fill(const int *list, const u64 
 // the sink stays the same and adding each sum to S[v] with one row of fp32
 // atomics: a sink's messages cost one read each, and one row update per window it
 // spans. G = 16 for rows of at most 64 floats (four rows per wave instruction).
-constexpr int kPullArcs = 4;  // arcs per lane per chunk
-constexpr int kPullChunk = kWave * kPullArcs;
 
 template <int G, int NC, int U>
 __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *list, const u64 *count,
@@ -1382,13 +1430,11 @@ long long compact_scratch_words(long long n) { return 2LL * compact_blocks(n) * 
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
                     const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list,
-                    const ScatterCopy &copy, const ScatterList &lo, bool packed_in, const Buckets *bk) {
+                    const ScatterCopy &copy, const ScatterList &lo, bool packed_in) {
   const int blocks = 2048;
-  const Buckets b = bk != nullptr && !push ? *bk : Buckets{};
 #define RP_SCATTER_L(GV, NCV, P, LV)                                                                               \
   RP_LAUNCH((k_scatter<GV, NCV, P, LV>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, doff, delta, out, \
-                     S, bm_out, bm_x, ins_dst, del_dst, pushed, c, mark_list ? 1 : 0, copy, lo, packed_in ? 1 : 0, \
-                     b)
+                     S, bm_out, bm_x, ins_dst, del_dst, pushed, c, mark_list ? 1 : 0, copy, lo, packed_in ? 1 : 0)
 #define RP_SCATTER(GV, NCV, P)                \
   do {                                        \
     if (P && lo.list != nullptr)              \
@@ -1408,9 +1454,17 @@ void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, 
 #undef RP_SCATTER_L
 }
 
+void launch_bucket_count(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
+                         const u64 *pushed, const Buckets &b, unsigned *bm_x, const int *ins_dst, const int *del_dst,
+                         bool mark_list, const Counters *c) {
+  RP_LAUNCH(k_bucket_arcs<false>, dim3(2048), dim3(256), 0, s, list, count, doff, out, pushed, b, bm_x, ins_dst,
+            del_dst, mark_list ? 1 : 0, c);
+}
+
 void launch_bucket_fill(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
                         const u64 *pushed, const Buckets &b, const Counters *c) {
-  RP_LAUNCH(k_bucket_fill, dim3(2048), dim3(256), 0, s, list, count, doff, out, pushed, b, c);
+  RP_LAUNCH(k_bucket_arcs<true>, dim3(2048), dim3(256), 0, s, list, count, doff, out, pushed, b, nullptr, nullptr,
+            nullptr, 0, c);
 }
 
 void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count,

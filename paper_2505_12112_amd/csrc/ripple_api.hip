@@ -754,7 +754,9 @@ void add_launches(ripple_ctx *c, int phase, int k) {
 //              read back and its message row summed), one read-modify-write of
 //              each affected row at 0.87 TB/s, and 10 us for the two extra
 //              launches (fitted to the form's kernels on dense_large's second
-//              layer at batches 100 and 1000).
+//              layer at batches 100 and 1000); it is taken only when its estimate
+//              is a quarter below every other form's (the fit is looser at a
+//              million arcs and below, where it loses to the push).
 // Every reanchor_every-th batch recomputes every layer (the drift budget), whatever
 // the form.
 enum LayerMode { kPushLayer = 0, kPullLayer = 1, kDenseLayer = 2, kRecomputeLayer = 3, kBucketLayer = 4 };
@@ -781,7 +783,7 @@ int layer_mode(const ripple_ctx *c, int l, double pushed, double count, double i
   if (pull < t) best = kPullLayer, t = pull;
   if (dense < t) best = kDenseLayer, t = dense;
   if (recompute < t) best = kRecomputeLayer, t = recompute;
-  if (bucket < t) best = kBucketLayer, t = bucket;
+  if (1.25 * bucket < t) best = kBucketLayer, t = bucket;
   return best;
 }
 
@@ -1074,9 +1076,13 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
       if (app)
         lo = rp::ScatterList{c->lists[l],       l < c->L ? c->doff[l] : nullptr, &dc->app[l], &dc->app_sinks[l],
                              c->adj[0].len, c->adj[1].len};
-      rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], count_in, c->doff[l - 1], msg, out_msg, c->S[l],
-                         c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc, mode == kPushLayer,
-                         rp::has_self_term(c->agg), copy, lo, packed_in, mode == kBucketLayer ? &c->bkt : nullptr);
+      if (mode == kBucketLayer)  // D is a compacted list here (see the bucket branch below)
+        rp::launch_bucket_count(s, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], out_msg, &dc->pushed[l],
+                                c->bkt, c->bm_x, c->ins_dst, c->del_dst, rp::has_self_term(c->agg), dc);
+      else
+        rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], count_in, c->doff[l - 1], msg, out_msg, c->S[l],
+                           c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc, mode == kPushLayer,
+                           rp::has_self_term(c->agg), copy, lo, packed_in);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     if (!app) {

@@ -17,16 +17,17 @@ def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-@pytest.mark.parametrize("bs", [100, 1000])
+@pytest.mark.parametrize("bs", [1, 10, 100, 1000])
 def test_sparse_mid_full_size(bs):
-    """169,343 vertices / 1,166,243 arcs, GraphSAGE-sum 128-256-40: affected sets
-    every batch, all embeddings against a float64 full recompute at the end."""
+    """169,343 vertices / 1,166,243 arcs, GraphSAGE-sum 128-256-40, at each of the
+    workload's batch sizes: affected sets every batch, all embeddings against a
+    float64 full recompute at the end."""
     wl = synth.build_workload("sparse_mid")
     p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights)
     try:
         p.check_embeddings()
         t0 = time.time()
-        nb = 20 if bs == 100 else 5
+        nb = {1: 50, 10: 30, 100: 20, 1000: 5}[bs]
         for b in range(nb):
             st, _, sets = p.step(wl.stream.next_batch(bs))
         _say(f"sparse_mid bs={bs}: {nb} batches in {time.time() - t0:.1f}s, last |A| = {[s.size for s in sets]}")
@@ -134,12 +135,12 @@ def _check_sampled(p, verts, layers, tol=1e-4):
     return errs
 
 
-@pytest.mark.parametrize("config,bs,nb", [("dense_large", 100, 3), ("dense_large", 1000, 2),
+@pytest.mark.parametrize("config,bs,nb", [("dense_large", 10, 5), ("dense_large", 100, 3), ("dense_large", 1000, 2),
                                           ("dense_large_2l", 100, 3), ("dense_large_2l", 1000, 2)])
 def test_dense_large_full_size(config, bs, nb):
     """Products-shaped undirected graph at full size (2,449,029 vertices, 61,859,140
     edges), GraphSAGE-sum 100-256-256-47 or 100-256-47, message forms chosen by the
-    library as bench.py runs it: batches of 100 or 1000 with affected sets compared
+    library as bench.py runs it: batches of 10, 100 or 1000 with affected sets compared
     bit for bit, then embeddings of sampled vertices (the 16 highest in-degrees
     among them) at every layer."""
     t0 = time.time()
