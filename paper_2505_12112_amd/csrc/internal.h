@@ -357,6 +357,12 @@ struct CompactOut {
   long long *boff;
   int *bkt_start;
 };
+// Floats allocated past the last row of every row table (H, S, P, the delta and
+// message rows). Kernels that gather rows with lane groups read a group's whole
+// span (up to 1024 floats) from each row start, masking the columns past the row's
+// width afterwards, so that every lane's offsets are compile-time immediates;
+// the tail keeps those reads inside the allocation for the table's last row.
+constexpr long long kRowTail = 1024;
 // The recompute form (launch_recompute) sums an in-row of more than kRecomputeSeg
 // arcs in segments of that many, each added to the row with fp32 atomics.
 constexpr int kRecomputeSeg = 64;

@@ -1124,13 +1124,12 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
       float row[U][NC];
 #pragma unroll
       for (int t = 0; t < U; ++t) {
-        const float *mj = msg + static_cast<long long>(jj[t] >= 0 ? jj[t] : 0) * ld;
+        // the group's whole span from the row start, column offsets as immediates
+        // (columns past d read the next row or the table's tail, kRowTail)
+        const float *mj = msg + static_cast<long long>(jj[t] >= 0 ? jj[t] : 0) * ld + k0;
         const unsigned keep = jj[t] >= 0 ? ~0u : 0u;
 #pragma unroll
-        for (int q = 0; q < NC; ++q) {
-          const int k = k0 + q * G;
-          row[t][q] = __uint_as_float(__float_as_uint(mj[k < d ? k : d - 1]) & keep);
-        }
+        for (int q = 0; q < NC; ++q) row[t][q] = __uint_as_float(__float_as_uint(mj[q * G]) & keep);
       }
 #pragma unroll
       for (int t = 0; t < U; ++t) {
@@ -1260,10 +1259,7 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
       float prev[NC];
       if (BK) {
 #pragma unroll
-        for (int p = 0; p < NC; ++p) {
-          const int k = k0 + p * G;
-          prev[p] = sv[k < d ? k : d - 1];
-        }
+        for (int p = 0; p < NC; ++p) prev[p] = sv[k0 + p * G];  // past d: the next row or the tail (never used)
       }
       // BK: slot a0 + i of the buckets; else in-arc a0 + i of the sink's row
       const long long row0 = BK ? a0 : in.off[v] - ioff[j] + a0;
@@ -1309,13 +1305,12 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
         float row[U][NC];
 #pragma unroll
         for (int t = 0; t < U; ++t) {
-          const float *su = src + static_cast<long long>(uu[t] >= 0 ? uu[t] : 0) * sld;
+          // the group's whole span from the row start, column offsets as immediates
+          // (columns past d read the next row or the table's tail, kRowTail)
+          const float *su = src + static_cast<long long>(uu[t] >= 0 ? uu[t] : 0) * sld + k0;
           const unsigned keep = uu[t] >= 0 ? ~0u : 0u;
 #pragma unroll
-          for (int p = 0; p < NC; ++p) {
-            const int k = k0 + p * G;
-            row[t][p] = __uint_as_float(__float_as_uint(su[k < d ? k : d - 1]) & keep);
-          }
+          for (int p = 0; p < NC; ++p) row[t][p] = __uint_as_float(__float_as_uint(su[p * G]) & keep);
         }
 #pragma unroll
         for (int t = 0; t < U; ++t)

@@ -1723,26 +1723,27 @@ ripple_status ripple_init_embeddings(ripple_ctx *c, const float *x, const ripple
     RP_HIP(c, hipStreamSynchronize(c->stream));
   }
   for (int l = 0; l <= L; ++l) {
-    RP_TRY(dalloc_n(c, &c->H[l], n * c->dims[l]));
+    // row tables get rp::kRowTail floats past their last row (see there)
+    RP_TRY(dalloc_n(c, &c->H[l], n * c->dims[l] + rp::kRowTail));
     RP_TRY(dalloc_n(c, &c->lists[l], n));
     RP_TRY(dalloc_n(c, &c->doff[l], n + 1));
-    if (l >= 1) RP_TRY(dalloc_n(c, &c->S[l], n * c->sw[l]));
+    if (l >= 1) RP_TRY(dalloc_n(c, &c->S[l], n * c->sw[l] + rp::kRowTail));
   }
-  RP_TRY(dalloc_n(c, &c->delta[0], n * rp::row_ld(c->dmax_delta)));
-  RP_TRY(dalloc_n(c, &c->delta[1], n * rp::row_ld(c->dmax_delta)));
+  RP_TRY(dalloc_n(c, &c->delta[0], n * rp::row_ld(c->dmax_delta) + rp::kRowTail));
+  RP_TRY(dalloc_n(c, &c->delta[1], n * rp::row_ld(c->dmax_delta) + rp::kRowTail));
   RP_TRY(dalloc_n(c, &c->ioff, n + 1));
   RP_TRY(dalloc_n(c, &c->flist_done, n));
   for (int k = 0; k < 2; ++k) {
     RP_TRY(dalloc_n(c, &c->memb[k], (n + 31) / 32));
   }
-  if (msg_width > 0) RP_TRY(dalloc_n(c, &c->msg, n * rp::row_ld(msg_width)));
+  if (msg_width > 0) RP_TRY(dalloc_n(c, &c->msg, n * rp::row_ld(msg_width) + rp::kRowTail));
   if (gin) {
     int dmax = 0;
     for (int l = 1; l <= L; ++l) dmax = std::max(dmax, c->dims[l]);
     RP_TRY(dalloc_n(c, &c->gin_rows, n * dmax));
   }
   for (int l = 1; l <= L; ++l)
-    if (c->tf[l]) RP_TRY(dalloc_n(c, &c->P[l], n * c->dims[l]));
+    if (c->tf[l]) RP_TRY(dalloc_n(c, &c->P[l], n * c->dims[l] + rp::kRowTail));
   RP_HIP(c, hipMemcpyAsync(c->H[0], x, static_cast<size_t>(n) * c->dims[0] * sizeof(float), hipMemcpyHostToDevice,
                            c->stream));
   rp::Adj pull_adj = c->adj[1];  // arc weights only under the weighted-sum model

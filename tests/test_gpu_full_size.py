@@ -55,20 +55,24 @@ def test_sparse_mid_bf16_full_size():
         p.close()
 
 
-@pytest.mark.parametrize("config", ["sparse_mid_gc_sum", "sparse_mid_gc_mean", "sparse_mid_gin", "sparse_mid_gc_wsum"])
-def test_evaluation_workloads_on_the_arxiv_shaped_graph(config):
+@pytest.mark.parametrize("bs", [100, 1000])
+@pytest.mark.parametrize("config", ["sparse_mid_gc_sum", "sparse_mid_gc_mean", "sparse_mid_gin", "sparse_mid_gc_wsum",
+                                    "sparse_mid_mean"])
+def test_evaluation_workloads_on_the_arxiv_shaped_graph(config, bs):
     """GraphConv-sum, GraphConv-mean, GIN-sum and GraphConv-weighted-sum (2 layers,
-    128-256-40) at full size: 20 batches of 100 with affected sets every batch, then
-    all embeddings against a float64 full recompute."""
+    128-256-40) and the 3-layer GraphSAGE-mean at full size, at the batch sizes
+    bench.py reports for them: 20 batches of 100 or 5 of 1000 with affected sets
+    every batch, then all embeddings against a float64 full recompute."""
     wl = synth.build_workload(config)
     p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, edge_w=wl.edge_w)
+    nb = 20 if bs == 100 else 5
     try:
         p.check_embeddings()
         t0 = time.time()
-        for b in range(20):
-            st, _, sets = p.step(wl.stream.next_batch(100))
+        for b in range(nb):
+            st, _, sets = p.step(wl.stream.next_batch(bs))
         errs = p.check_embeddings()
-        _say(f"{config}: 20 batches in {time.time() - t0:.1f}s, last |A| = {[s.size for s in sets]}, "
+        _say(f"{config} bs={bs}: {nb} batches in {time.time() - t0:.1f}s, last |A| = {[s.size for s in sets]}, "
              f"row-relative errors {errs}")
         p.check_arcs()
     finally:
