@@ -1193,6 +1193,12 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
                                                    const float *src, float *S, const Counters *c, Buckets bk) {
   using Acc = typename std::conditional<BK, float, double>::type;
   static_assert(G % U == 0 && kRecomputeSeg % G == 0, "steps of U arcs stay within one fetch slot");
+  // the first kWave sinks of a range, fetched by the wave in one round when the range
+  // starts: their first arc, their end and their vertex (read back by their groups)
+  __shared__ long long sink_a[256 / kWave][kWave], sink_b[256 / kWave][kWave];
+  __shared__ int sink_v[256 / kWave][kWave];
+  long long *pa = sink_a[threadIdx.x / kWave], *pb = sink_b[threadIdx.x / kWave];
+  int *pv = sink_v[threadIdx.x / kWave];
   constexpr int kPer = kRecomputeSeg / G;  // arcs fetched per lane
   constexpr int kSteps = kRecomputeSeg / U;
   const long long nA = static_cast<long long>(*count);
@@ -1234,23 +1240,47 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
       }
     }
     const long long has_pred = pstart >= 0 ? 1 : 0;
-    const long long items = has_pred + (jl >= jf ? jl - jf + 1 : 0);
+    const long long sinks = jl >= jf ? jl - jf + 1 : 0;
+    const long long items = has_pred + sinks;
+    if (lane < sinks) {
+      const long long j = jf + lane;
+      pa[lane] = ioff[j];
+      pb[lane] = ioff[j + 1];
+      pv[lane] = list != nullptr ? list[j] : static_cast<int>(j);
+    }
+    // the sinks are read back by other lanes of this wave only
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     for (long long it = grp; it < items; it += kGroups) {  // the same bounds for a group's lanes
       long long j, a0, a1;
-      bool whole;
+      bool whole, first;
+      int v;
       if (it < has_pred) {
         j = pj;
         a0 = pstart;
         a1 = pend;
         whole = false;
+        first = false;  // a segment starting in this range is not the sink's first
+        v = list != nullptr ? list[j] : static_cast<int>(j);
       } else {
-        j = jf + (it - has_pred);
-        const long long a = ioff[j], b = ioff[j + 1];
+        const long long q = it - has_pred;
+        j = jf + q;
+        long long a, b;
+        if (q < kWave) {
+          a = pa[q];
+          b = pb[q];
+          v = pv[q];
+        } else {
+          a = ioff[j];
+          b = ioff[j + 1];
+          v = list != nullptr ? list[j] : static_cast<int>(j);
+        }
         a0 = a;
         whole = b - a <= kRecomputeSeg;
         a1 = whole ? b : a + kRecomputeSeg;
+        first = true;
       }
-      const int v = list != nullptr ? list[j] : static_cast<int>(j);
       const int na = static_cast<int>(a1 - a0);  // arcs in the segment (<= kRecomputeSeg)
       if (BK && na == 0) continue;                // no message reached the sink (the same for the group)
       float *sv = S + static_cast<long long>(v) * d;
@@ -1263,7 +1293,7 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
       }
       // BK: slot a0 + i of the buckets; else in-arc a0 + i of the sink's row
       const long long row0 = BK ? a0 : in.off[v] - ioff[j] + a0;
-      if (BK && k0 == 0 && a0 == ioff[j]) bk.cnt[v] = 0;  // the bucket's start is no longer needed
+      if (BK && k0 == 0 && first) bk.cnt[v] = 0;  // the bucket's start is no longer needed
       // arc i of the segment is fetched by lane i % G of the group, into slot i / G
       int uq[kPer];
       Acc cq[kPer];
@@ -1271,8 +1301,13 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
       for (int q = 0; q < kPer; ++q) {
         const int i = k0 + q * G;
         if (BK) {
-          uq[q] = i < na ? bk.idx[row0 + i] : -1;
-          cq[q] = i < na && weighted ? bk.wt[row0 + i] : 1.0f;
+          // unconditional loads from a clamped slot (na >= 1 here), masked afterwards:
+          // no branch between them
+          const long long at = row0 + (i < na ? i : na - 1);
+          const int x = bk.idx[at];
+          const float wx = weighted ? bk.wt[at] : 1.0f;
+          uq[q] = i < na ? x : -1;
+          cq[q] = i < na ? wx : 1.0f;
         } else {
           uq[q] = i < na ? in.col[row0 + i] : -1;
           cq[q] = i < na && weighted ? static_cast<double>(in.wt[row0 + i]) : 1.0;
@@ -1326,6 +1361,10 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
         }
       }
     }
+    // the next range overwrites the sinks only after every group has read them
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 }
 
