@@ -750,9 +750,9 @@ void add_launches(ripple_ctx *c, int phase, int k) {
 //              (15 ps per arc plus the row at 6 TB/s, the rate of random row reads
 //              from a table larger than the caches), one plain row store per
 //              affected vertex at 5 TB/s;
-//   bucket     104 ps per pushed arc (its count and rank, its bucket slot written,
+//   bucket     87 ps per pushed arc (its count and rank, its bucket slot written,
 //              read back and its message row summed), one read-modify-write of
-//              each affected row at 0.87 TB/s, and 10 us for the two extra
+//              each affected row at 0.91 TB/s, and 15 us for the two extra
 //              launches (fitted to the form's kernels on dense_large's second
 //              layer at batches 100 and 1000); it is taken only when its estimate
 //              is a quarter below every other form's (the fit is looser at a
@@ -768,7 +768,7 @@ int layer_mode(const ripple_ctx *c, int l, double pushed, double count, double i
   if (c->scatter_mode == RIPPLE_SCATTER_DENSE) return kDenseLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_BUCKET) return kBucketLayer;
   constexpr double kArc = 90e-12, kAtomicRate = 1.3e12, kMark = 38e-12, kPullScan = 35e-12;
-  constexpr double kBucketArc = 104e-12, kBucketRowRate = 0.87e12, kBucketFixed = 10e-6;
+  constexpr double kBucketArc = 87e-12, kBucketRowRate = 0.91e12, kBucketFixed = 15e-6;
   constexpr double kDenseScan = 25e-12, kDenseVertex = 20e-12, kReadRate = 10e12;
   constexpr double kRecScan = 15e-12, kGatherRate = 6e12, kStoreRate = 5e12;
   const double w = 4.0 * c->sw[l];  // message row bytes
