@@ -150,13 +150,20 @@ class Pair:
                 w = self.lib.get_arc_weights(direction)[order]
                 np.testing.assert_array_equal(w.astype(np.float64), self.orc.graph.w, err_msg=f"weights {direction}")
 
-    def check_aggregates(self, tol=FP32_TOL):
+    def check_aggregates(self, tol=FP32_TOL, drift_units=1024.0):
         """The library's cached aggregates against their definition on oracle values:
         S^l_v = sum over in-neighbours u of c_u h^{l-1}_u (c_u = 1, or 1/sqrt(dout+1) for GCN).
 
         S is a running sum of deltas, so a row whose true value cancels to ~0 keeps
-        rounding residue of the order of the contributions that cancelled; the
-        error of each row is therefore measured against max(|S*_v|_inf, RMS(S*))."""
+        rounding residue of the order of the contributions that cancelled. Two
+        measures: the error of each row against max(|S*_v|_inf, RMS(S*)) within tol,
+        and, row by row without any floor, against the magnitude of the row's terms,
+        max_k sum_u |c_u h_uk| (through |W_neigh| for rows cached transformed), within
+        drift_units units of 2^-24: a row summed afresh is within about its in-degree
+        of these units and each message added to it since can add about two, so this
+        bounds the accumulated rounding of every row, cancelling ones included. (The
+        magnitude is floored at a tenth of its RMS over the rows: a row that lost most
+        of its in-arcs keeps the rounding of terms larger than its present ones.)"""
         ref = self.orc.embeddings()
         g = self.orc.graph
         c = np.ones(self.n)
@@ -177,6 +184,14 @@ class Pair:
             worst = int(np.argmax(r))
             errs.append(float(r[worst]))
             assert r[worst] <= tol, (l, worst, float(num[worst]), float(np.max(np.abs(want[worst]))), rms)
+            mag = abs(a) @ np.abs(ref[l - 1])
+            if got.shape[1] != mag.shape[1]:
+                mag = mag @ np.abs(self.orc.model.w_neigh[l - 1]).T
+            m = np.max(mag, axis=1)
+            scale = np.maximum(m, 0.1 * float(np.sqrt(np.mean(m * m)))) * 2.0 ** -24
+            units = np.where(scale > 0, num / np.where(scale > 0, scale, 1.0), np.where(num > 0, np.inf, 0.0))
+            w = int(np.argmax(units))
+            assert units[w] <= drift_units, (l, w, float(units[w]), float(num[w]), float(scale[w]))
         return errs
 
 
