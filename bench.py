@@ -73,6 +73,9 @@ def parse():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-mebibyte device buffer into another (torch copy kernel), ten times: "
                          "the reference reading for the HBM byte counters")
+    ap.add_argument("--gather-calibration", type=int, default=0, metavar="MIB",
+                    help="only gather every 192-byte row of a MIB-mebibyte table once, in random order (torch "
+                         "index_select), ten times: checks the byte counters' scale on random row reads")
     return ap.parse_args()
 
 
@@ -263,6 +266,16 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": 4 * n, "copies": 10}))
+        return
+    if args.gather_calibration:
+        rows = args.gather_calibration * 2**20 // 192
+        table = torch.ones(rows, 48, dtype=torch.float32, device="cuda")
+        perm = torch.randperm(rows, device="cuda")
+        out = torch.empty_like(table)
+        for _ in range(10):
+            torch.index_select(table, 0, perm, out=out)
+        torch.cuda.synchronize()
+        print(json.dumps({"gather_calibration_rows": rows, "row_bytes": 192, "index_bytes": 8, "gathers": 10}))
         return
     from paper_2505_12112_amd.ripple import BatchStats
     from paper_2505_12112_amd.profiling import read_traffic

@@ -1,25 +1,29 @@
 """Summaries of rocprofv3 output for the committed profiles, and the HBM traffic
 figures bench.py reports beside its roofline.
 
-Two kinds of input, both CSV as rocprofv3 writes them with --output-format csv:
+Inputs, all CSV as rocprofv3 writes them with --output-format csv:
 
-* a kernel-trace statistics file (``*_kernel_stats.csv``): calls and durations
-  per kernel;
-* counter-collection files (``*_counter_collection.csv``) of two separate
-  ``--pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE`` runs, per dispatch, in KiB.
+* a kernel-trace statistics file (``*_kernel_stats.csv``) and trace
+  (``*_kernel_trace.csv``): calls and durations per kernel, per-batch kernel time;
+* counter-collection files (``*_counter_collection.csv``): the L2-to-fabric read
+  requests by size (TCC_EA0_RDREQ_32B / _64B / _128B) in one run and the write
+  requests (TCC_EA0_WRREQ, _64B) in another, each request counted at its size; the
+  MFMA counters; and, for the calibration note, FETCH_SIZE and WRITE_SIZE.
 
-The byte counters are scaled by what they read for a plain device-to-device copy
-of known size (``bench.py --copy-calibration MIB``): on gfx950 FETCH_SIZE reads
-half of the bytes such a copy moves and WRITE_SIZE all of them; the factors are
-measured, not assumed, and written into the summary.
+The derived FETCH_SIZE counts 128-byte read requests as 64 bytes on this chip (its
+formula takes them from TCC_BUBBLE); counting requests at their sizes reads a plain
+copy exactly, which the traffic table checks (``bench.py --copy-calibration MIB``).
 
 The traffic table carries a hash of the HIP sources it was measured on; bench.py
 reports the figures only while the sources still hash the same (a changed kernel
 makes them stale, and then the field is null).
 
     python -m paper_2505_12112_amd.profiling stats TRACE_DIR TITLE COMMAND > profiles/x.txt
-    python -m paper_2505_12112_amd.profiling traffic OUT.md COPY_DIR WORKLOAD=FETCH_DIR,WRITE_DIR,BATCHES,CMD ...
+    python -m paper_2505_12112_amd.profiling traffic-sized OUT.md COPY_MIB COPY_RD COPY_WR WORKLOAD=RD,WR,BATCHES,CMD ...
     python -m paper_2505_12112_amd.profiling mfma OUT.md TITLE NAME=DIR,DTYPE,CMD ...
+    python -m paper_2505_12112_amd.profiling calibration OUT.md COPY_MIB GATHER_MIB KEY=DIR ... COMMANDS
+    python -m paper_2505_12112_amd.profiling traffic OUT.md COPY_MIB COPY_F COPY_W WORKLOAD=F_DIR,W_DIR,BATCHES,CMD ...
+      (the FETCH_SIZE / WRITE_SIZE form, scaled by what they read for a copy)
 """
 from __future__ import annotations
 
@@ -182,6 +186,51 @@ def _copy_factor(copy_dir: str, size_kib: float) -> float:
     return size_kib / (sum(vals) / len(vals))
 
 
+def calibration_md(copy_mib: int, gather_mib: int, dirs: dict, commands: str) -> str:
+    """How the byte counters read on a streaming copy and on random row reads (a
+    gather of every 192-byte row of a table once in random order, index_select): the
+    derived FETCH_SIZE and WRITE_SIZE, and the request counters by size. dirs: copy /
+    gather x fetch / write / rd / wr run directories."""
+    rows = gather_mib * 2**20 // 192
+
+    def top(d, multi=False):
+        c = _counters_multi(d, False) if multi else _counter(d)
+        ks = [k for k in c if "copyBuffer" not in k and "fill" not in k.lower() and not k.startswith("k_state")]
+        if multi:
+            return max(ks, key=lambda k: sum(c[k].get("TCC_EA0_RDREQ_sum", c[k].get("TCC_EA0_WRREQ_sum", [0])))), c
+        return max(ks, key=lambda k: sum(v for v, _ in c[k]) / len(c[k])), c
+
+    copy_bytes = copy_mib * 2**20
+    ff = _copy_factor(dirs["copy_fetch"], copy_bytes / 1024.0)
+    fw = _copy_factor(dirs["copy_write"], copy_bytes / 1024.0)
+    kf, cf = top(dirs["gather_fetch"])
+    kw, cw = top(dirs["gather_write"])
+    gf = sum(v for v, _ in cf[kf]) / len(cf[kf]) * 1024.0
+    gw = sum(v for v, _ in cw[kw]) / len(cw[kw]) * 1024.0
+    crd, cwr = _counters_multi(dirs["copy_rd"], False), _counters_multi(dirs["copy_wr"], False)
+    kc = next(k for k in crd if "copyBuffer" in k)
+    _, cshare, crb, cwb = _sized_bytes(crd[kc], cwr.get(kc, {}))
+    kg, grd = top(dirs["gather_rd"], True)
+    gwr = _counters_multi(dirs["gather_wr"], False)
+    greq, gshare, grb, gwb = _sized_bytes(grd[kg], gwr.get(kg, {}))
+    useful = rows * (192 + 8)
+    return "\n".join([
+        "# How the HBM byte counters read (rocprofv3 --pmc; one run per counter set)", "",
+        f"commands: {commands}", "",
+        f"Streaming copy of {copy_mib} MiB (bench.py --copy-calibration {copy_mib}): FETCH_SIZE reads "
+        f"1/{ff:.3f} of the bytes read and WRITE_SIZE 1/{fw:.3f} of those written. Its reads are "
+        f"{100 * cshare:.1f}% 128-byte requests, and counted at their sizes they come to {crb / 2**20:.1f} MiB read and "
+        f"{cwb / 2**20:.1f} MiB written: exact. FETCH_SIZE's formula counts 128-byte requests from TCC_BUBBLE, which "
+        f"does not count them on this chip, so it takes them as 64 bytes.", "",
+        f"Random-order gather of {rows} rows of 192 bytes, each read once, with 8-byte indices "
+        f"(bench.py --gather-calibration {gather_mib}; kernel {kg}): {useful / 2**20:.0f} MiB of useful reads; "
+        f"FETCH_SIZE reads {gf / 2**20:.0f} MiB; the requests counted at their sizes come to {grb / 2**20:.0f} MiB "
+        f"({100 * gshare:.1f}% of {greq:.0f} requests are 128-byte, the rest 64-byte: each row costs two 128-byte "
+        f"requests and one 64-byte request, 320 bytes for 192), written {gwb / 2**20:.0f} MiB. So the FETCH_SIZE x 2 "
+        f"rule holds only for kernels whose reads are all 128-byte requests; the traffic table counts every "
+        f"request at its own size instead (the library's large kernels issue 99-100% 128-byte reads).", ""]) + "\n"
+
+
 def traffic_md(copy_fetch: str, copy_write: str, copy_mib: int, workloads) -> str:
     """workloads: list of (name, fetch_dir, write_dir, batches, command)."""
     kib = copy_mib * 1024.0
@@ -285,6 +334,64 @@ def mfma_md(title: str, runs, simds: int = 1024, clock_ghz: float = 2.4) -> str:
     return "\n".join(out) + "\n"
 
 
+RD_COUNTERS = ("TCC_EA0_RDREQ_sum", "TCC_EA0_RDREQ_32B_sum", "TCC_EA0_RDREQ_64B_sum", "TCC_EA0_RDREQ_128B_sum")
+WR_COUNTERS = ("TCC_EA0_WRREQ_sum", "TCC_EA0_WRREQ_64B_sum")
+
+
+def _sized_bytes(rd: dict, wr: dict):
+    """Per-dispatch averages: (requests, share of 128-byte reads, read bytes, write bytes)
+    from the L2-to-fabric request counters, each request counted at its own size."""
+    def avg(d, name):
+        v = d.get(name, [])
+        return sum(v) / len(v) if v else 0.0
+    req = avg(rd, "TCC_EA0_RDREQ_sum")
+    c32, c64, c128 = (avg(rd, n) for n in RD_COUNTERS[1:])
+    wt, w64 = avg(wr, "TCC_EA0_WRREQ_sum"), avg(wr, "TCC_EA0_WRREQ_64B_sum")
+    return req, (c128 / req if req else 0.0), 32 * c32 + 64 * c64 + 128 * c128, 32 * (wt - w64) + 64 * w64
+
+
+def traffic_sized_md(copy_rd: str, copy_wr: str, copy_mib: int, workloads) -> str:
+    """HBM traffic per dispatch from two runs per workload: --pmc of the read request
+    counters by size (32, 64, 128 bytes) and of the write request counters, each
+    request counted at its size. workloads: list of (name, rd_dir, wr_dir, batches,
+    command). The copy run checks the method: its reads and writes must come out at
+    the bytes the copy moves."""
+    crd, cwr = _counters_multi(copy_rd, False), _counters_multi(copy_wr, False)
+    k = next(k for k in crd if "copyBuffer" in k)
+    _, _, cr, cw = _sized_bytes(crd[k], cwr.get(k, {}))
+    out = ["# HBM traffic per dispatch (L2-to-fabric requests counted at their sizes; reads and writes in separate runs)",
+           "", f"source-hash: {source_hash()}", "",
+           f"Check: a {copy_mib} MiB device-to-device copy (bench.py --copy-calibration {copy_mib}) comes out at "
+           f"{cr / 2**20:.1f} MiB read and {cw / 2**20:.1f} MiB written. Bytes = 32 x TCC_EA0_RDREQ_32B + 64 x "
+           f"TCC_EA0_RDREQ_64B + 128 x TCC_EA0_RDREQ_128B (reads), 64 x TCC_EA0_WRREQ_64B + 32 x the other write "
+           f"requests (writes); MALL hits count as traffic.", ""]
+    for name, rdd, wrd, batches, cmd in workloads:
+        rd, wr = _counters_multi(rdd), _counters_multi(wrd)
+        out += [f"## {name}", "",
+                f"commands (one run per counter set): {cmd.replace('COUNTERS', ' '.join(RD_COUNTERS)).replace('SET', 'rd')} ; "
+                f"{cmd.replace('COUNTERS', ' '.join(WR_COUNTERS)).replace('SET', 'wr')}", "",
+                f"Dispatches from the first of {batches} update batches on (the bootstrap is left out).", "",
+                "| kernel | dispatches | read requests/disp | 128-byte share | read MB/disp | write MB/disp |",
+                "|---|---|---|---|---|---|"]
+        rows = []
+        for kname in rd:
+            req, share, rb, wb = _sized_bytes(rd[kname], wr.get(kname, {}))
+            rows.append((rb + wb, kname, len(rd[kname].get("_ns", [])), req, share, rb, wb))
+        for _, kname, n, req, share, rb, wb in sorted(rows, reverse=True):
+            out.append(f"| {kname} | {n} | {req:.0f} | {share:.3f} | {rb / 1e6:.3f} | {wb / 1e6:.3f} |")
+        out.append("")
+        for phase, prefixes in PHASE_KERNELS.items():
+            tot = cnt = 0.0
+            for _, kname, n, req, share, rb, wb in rows:
+                if kname.startswith(prefixes):
+                    tot += (rb + wb) * n
+                    cnt += n
+            if cnt:
+                out.append(f"traffic {name} {phase} {tot / cnt:.0f}")
+        out.append("")
+    return "\n".join(out) + "\n"
+
+
 def read_traffic(workload: str, phase: str):
     """Calibrated HBM bytes per launch of `phase` on `workload` from the committed
     table, or None when there is none or it predates the current sources."""
@@ -311,6 +418,21 @@ def main(argv):
             runs.append((name, d, cmd, dtype))
         with open(argv[1], "w") as fh:
             fh.write(mfma_md(argv[2], runs))
+    elif argv[:1] == ["traffic-sized"]:
+        # traffic-sized OUT COPY_MIB COPY_RD COPY_WR WORKLOAD=RD_DIR,WR_DIR,BATCHES,CMD ...
+        wls = []
+        for spec in argv[5:]:
+            name, rest = spec.split("=", 1)
+            rdd, wrd, batches, cmd = rest.split(",", 3)
+            wls.append((name, rdd, wrd, int(batches), cmd))
+        with open(argv[1], "w") as fh:
+            fh.write(traffic_sized_md(argv[3], argv[4], int(argv[2]), wls))
+    elif argv[:1] == ["calibration"]:
+        # calibration OUT COPY_MIB GATHER_MIB KEY=DIR ... COMMANDS (keys copy_fetch copy_write gather_fetch
+        # gather_write copy_rd copy_wr gather_rd gather_wr)
+        dirs = dict(a.split("=", 1) for a in argv[4:-1])
+        with open(argv[1], "w") as fh:
+            fh.write(calibration_md(int(argv[2]), int(argv[3]), dirs, argv[-1]))
     elif argv[:1] == ["traffic"]:
         out, copy_mib, cf, cw = argv[1], int(argv[2]), argv[3], argv[4]
         wls = []
