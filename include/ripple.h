@@ -293,8 +293,8 @@ RIPPLE_API ripple_status ripple_get_arc_weights(ripple_ctx *ctx, int32_t directi
  * RIPPLE_SCATTER_BUCKET, the pushed arcs sorted by sink (counted, then placed in
  * per-sink buckets) and each sink's bucket summed and added to its row once (the
  * messages of Sec. IV-C.1 combined per sink before they reach the aggregate; the
- * first batch that uses the form allocates 4 bytes per out-arc slot, 8 under the
- * weighted-sum model, and n counters);
+ * first batch that uses the form allocates 8 bytes per out-arc slot, 12 under the
+ * weighted-sum model, and a counter per vertex);
  * RIPPLE_SCATTER_AUTO (default), per layer from the previous batch's counts, or
  * for the first batch from an estimate based on the snapshot's degrees. */
 enum {
