@@ -186,6 +186,7 @@ struct ripple_ctx {
   // out-direction has slots, which bounds the arcs any layer pushes
   rp::Buckets bkt{nullptr, nullptr, nullptr, nullptr};
   long long bkt_cap = 0;
+  bool bkt_off = false;  // the arrays could not be allocated: the time model leaves the form out
   // rows long enough for the chunked delete sweep exist (or may, once rows grow):
   // the plan lists such rows in long_tab, their sweeps record positions in long_pool
   int long_ok = 0;
@@ -767,6 +768,7 @@ int layer_mode(const ripple_ctx *c, int l, double pushed, double count, double i
   if (c->scatter_mode == RIPPLE_SCATTER_PULL) return kPullLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_DENSE) return kDenseLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_BUCKET) return kBucketLayer;
+  const bool bucket_ok = !c->bkt_off;
   constexpr double kArc = 90e-12, kAtomicRate = 1.3e12, kMark = 38e-12, kPullScan = 35e-12;
   constexpr double kBucketArc = 87e-12, kBucketRowRate = 0.91e12, kBucketFixed = 15e-6;
   constexpr double kDenseScan = 25e-12, kDenseVertex = 20e-12, kReadRate = 10e12;
@@ -783,7 +785,7 @@ int layer_mode(const ripple_ctx *c, int l, double pushed, double count, double i
   if (pull < t) best = kPullLayer, t = pull;
   if (dense < t) best = kDenseLayer, t = dense;
   if (recompute < t) best = kRecomputeLayer, t = recompute;
-  if (1.25 * bucket < t) best = kBucketLayer, t = bucket;
+  if (bucket_ok && 1.25 * bucket < t) best = kBucketLayer, t = bucket;
   return best;
 }
 
@@ -1208,8 +1210,24 @@ ripple_status ensure_buckets(ripple_ctx *c) {
 // Queues one batch whose inputs are in c->h_in: as a graph replay unless graphs
 // are off or this batch records phase events.
 ripple_status launch_batch(ripple_ctx *c) {
-  const BatchPlan p = make_plan(c);
-  if (p.key2 != 0) RP_TRY(ensure_buckets(c));
+  BatchPlan p = make_plan(c);
+  if (p.key2 != 0) {
+    const ripple_status st = ensure_buckets(c);
+    if (st == RIPPLE_E_OOM && c->scatter_mode != RIPPLE_SCATTER_BUCKET) {
+      // chosen by the time model, not asked for: plan again without the form (and
+      // give back what was allocated of its arrays)
+      c->bkt_off = true;
+      c->err.clear();
+      dfree_t(c, c->bkt.cnt);
+      dfree_t(c, c->bkt.rank);
+      dfree_t(c, c->bkt.idx);
+      dfree_t(c, c->bkt.wt);
+      c->bkt_cap = 0;
+      p = make_plan(c);
+    } else if (st != RIPPLE_OK) {
+      return st;
+    }
+  }
   c->last_bucket = static_cast<int>(p.key2);
   c->last_pull = 0;
   c->last_dense = 0;

@@ -509,6 +509,43 @@ def test_call_order_and_device_byte_cap():
         lib.close()
 
 
+def test_bucket_form_without_room_for_its_arrays():
+    """Under a device byte cap that leaves no room for the bucket form's arrays, a
+    batch in the forced bucket form fails with RIPPLE_E_OOM and changes nothing
+    (arcs, embeddings and aggregates still match the oracle, which has not applied
+    it); the context stays usable, and later batches in the automatic forms match
+    the oracle."""
+    rng = np.random.default_rng(71)
+    dims = (8, 16, 4)
+    src, dst, x, w = _small(rng, 400, 2400, dims, "sum")
+    probe = Pair(400, src, dst, x, w)
+    try:
+        probe.step(random_valid_batch(rng, probe.orc, 30, dims[0]))
+        need = probe.lib.device_bytes()
+    finally:
+        probe.close()
+    # the bucket arrays need 8 bytes per out-arc slot (over 64K slots here): far more than the margin
+    p = Pair(400, src, dst, x, w, max_device_bytes=need + (64 << 10))
+    try:
+        p.step(random_valid_batch(rng, p.orc, 30, dims[0]))  # sizes the batch scratch as the probe's did
+        p.lib.set_scatter_mode("bucket")
+        batch = random_valid_batch(rng, p.orc, 30, dims[0])
+        with pytest.raises(RippleError) as e:
+            p.lib.apply_updates(batch.ops, batch.feat_rows)
+        assert e.value.status == E_OOM
+        p.check_arcs()
+        p.check_embeddings()
+        p.check_aggregates()
+        p.lib.set_scatter_mode("auto")
+        for b in range(10):
+            p.step(random_valid_batch(rng, p.orc, 30, dims[0]))
+        p.check_embeddings()
+        p.check_aggregates()
+        p.check_arcs()
+    finally:
+        p.close()
+
+
 @pytest.mark.parametrize("agg,mode,launch",
                          [(a, m, "direct") for a in ("sum", "mean", "gcn") for m in ("auto", "pull", "dense")]
                          + [(a, m, "direct") for a in ("gc_sum", "gc_mean", "gin", "gc_wsum") for m in ("auto", "dense")]
