@@ -21,6 +21,7 @@
 // it (ripple_set_graphs), which takes the queueing of some fifteen dependent
 // kernels off the host thread.
 #include <algorithm>
+#include <limits>
 #include <chrono>
 #include <cmath>
 #include <cstdio>
@@ -1194,6 +1195,8 @@ ripple_status ensure_buckets(ripple_ctx *c) {
     RP_HIP(c, hipMemsetAsync(c->bkt.cnt, 0, static_cast<size_t>(slots) * sizeof(int), c->stream));
   }
   const long long need = std::max<long long>(1, c->col_capacity[0]);
+  if (need > std::numeric_limits<int32_t>::max())  // bucket slots are int32
+    return fail(c, RIPPLE_E_OOM, "ripple: the bucket form needs fewer than 2^31 out-arc slots");
   if (c->bkt_cap < need) {
     dfree_t(c, c->bkt.rank);
     dfree_t(c, c->bkt.idx);
