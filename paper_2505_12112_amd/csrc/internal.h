@@ -542,10 +542,10 @@ struct GemmArgs {
 int cleanup_blocks_for(long long cap_ops);
 // expected_rows picks the kernel: 0 = 16-row tiles split over eight waves (short
 // lists), 2 = the same over four waves, 1 = 128-row tiles (many rows);
-// gemm_variant(expected_rows) names the choice (launches with the same variant
+// gemm_variant(expected_rows, N) names the choice (launches with the same variant
 // and arguments are the same launch).
 void launch_gemm(hipStream_t s, const GemmArgs &a, long long max_rows, long long expected_rows);
-int gemm_variant(long long expected_rows);
+int gemm_variant(long long expected_rows, int n_cols);
 
 // re-layout of one adjacency direction
 // old_wt / new_wt (nullable): the slots' weights move with them.

@@ -876,8 +876,12 @@ void launch_mode(hipStream_t s, const GemmArgs &a, long long max_rows, int varia
 
 }  // namespace
 
-int gemm_variant(long long expected_rows) {
-  return expected_rows >= 32768 ? 1 : expected_rows > kRowsWideMax ? 2 : 0;
+int gemm_variant(long long expected_rows, int n_cols) {
+  // 128-row tiles from 32768 expected rows, or from 4096 when the output is at least
+  // 128 wide (the 3-layer mean workload's 256-wide middle layer at ~15K rows: 7%
+  // faster at batch 1000; the narrow layers lose by it)
+  const long long big = n_cols >= 128 ? 4096 : 32768;
+  return expected_rows >= big ? 1 : expected_rows > kRowsWideMax ? 2 : 0;
 }
 
 int cleanup_blocks_for(long long cap_ops) {
@@ -889,7 +893,7 @@ int cleanup_blocks_for(long long cap_ops) {
 void launch_gemm(hipStream_t s, const GemmArgs &args, long long max_rows, long long expected_rows) {
   GemmArgs a = args;
   a.max_rows = max_rows;
-  const int variant = gemm_variant(expected_rows);
+  const int variant = gemm_variant(expected_rows, a.N);
   if (a.mode == kTransformFirst) launch_mode<kTransformFirst>(s, a, max_rows, variant);
   else if (a.mode == kPlain) launch_mode<kPlain>(s, a, max_rows, variant);
   else if (a.mode == kGin1) launch_mode<kGin1>(s, a, max_rows, variant);

@@ -887,8 +887,8 @@ BatchPlan make_plan(const ripple_ctx *c) {
     p.rows[l] = guess[l];
     if (p.mode[l] == kBucketLayer) p.key2 |= 1ull << l;
     key |= static_cast<unsigned long long>(p.mode[l] & 3) << bit;
-    key |= static_cast<unsigned long long>(rp::gemm_variant(p.tf_rows[l])) << (bit + 2);
-    key |= static_cast<unsigned long long>(rp::gemm_variant(p.rows[l])) << (bit + 4);
+    key |= static_cast<unsigned long long>(rp::gemm_variant(p.tf_rows[l], c->dims[l])) << (bit + 2);
+    key |= static_cast<unsigned long long>(rp::gemm_variant(p.rows[l], c->dims[l])) << (bit + 4);
     bit += 6;  // up to bit 48 for 8 layers
   }
   // the layer-1 dirty set is the feature-written vertices alone unless GCN adds
