@@ -877,10 +877,11 @@ void launch_mode(hipStream_t s, const GemmArgs &a, long long max_rows, int varia
 }  // namespace
 
 int gemm_variant(long long expected_rows, int n_cols) {
-  // 128-row tiles from 32768 expected rows, or from 4096 when the output is at least
-  // 128 wide (the 3-layer mean workload's 256-wide middle layer at ~15K rows: 7%
-  // faster at batch 1000; the narrow layers lose by it)
-  const long long big = n_cols >= 128 ? 4096 : 32768;
+  // 128-row tiles from 32768 expected rows, or from 8192 when the output is at least
+  // 128 wide (the 3-layer mean workload's 256-wide middle layer at ~15K rows: 5%
+  // faster at batch 1000; narrow layers lose by it, and from 4096 rows the tiles
+  // left too many compute units idle at batch 100)
+  const long long big = n_cols >= 128 ? 8192 : 32768;
   return expected_rows >= big ? 1 : expected_rows > kRowsWideMax ? 2 : 0;
 }
 
