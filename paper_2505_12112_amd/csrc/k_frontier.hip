@@ -1182,16 +1182,10 @@ __global__ __launch_bounds__(256) void k_pull_msgs(int d, int ld, const int *lis
 // sinks are added with fp32 atomics into rows the compaction zeroed. The last
 // range also owns the sinks past the last arc (rows without in-arcs, stored as
 // zeros).
-// BK: the bucket form's sums on the same split. The numbered items are bucket
-// slots (ioff is the bucket prefix), a slot holds its message row (stride sld) and
-// weight, sums are fp32 and are added to the row: with a plain load and store
-// when the bucket is one segment, with atomics otherwise. Sinks with empty buckets
-// are left alone; each sink's first segment resets its counter.
-template <int G, int NC, int U, bool BK>
-__global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, const int *list, const u64 *count,
+template <int G, int NC, int U>
+__global__ __launch_bounds__(256) void k_recompute(int d, int gcn, const int *list, const u64 *count,
                                                    const long long *ioff, Adj in, const int *out_len,
-                                                   const float *src, float *S, const Counters *c, Buckets bk) {
-  using Acc = typename std::conditional<BK, float, double>::type;
+                                                   const float *src, float *S, const Counters *c) {
   static_assert(G % U == 0 && kRecomputeSeg % G == 0, "steps of U arcs stay within one fetch slot");
   // the first kWave sinks of a range, fetched by the wave in one round when the range
   // starts: their first arc, their end and their vertex (read back by their groups)
@@ -1206,7 +1200,7 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
   const int lane = lane_id();
   constexpr int kGroups = kWave / G;
   const int grp = lane / G, k0 = lane % G;
-  const bool weighted = BK ? bk.wt != nullptr : in.wt != nullptr;
+  const bool weighted = in.wt != nullptr;
   const long long E = ioff[nA];
   const long long waves = num_waves();
   long long C = 16;
@@ -1254,14 +1248,13 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     for (long long it = grp; it < items; it += kGroups) {  // the same bounds for a group's lanes
       long long j, a0, a1;
-      bool whole, first;
+      bool whole;
       int v;
       if (it < has_pred) {
         j = pj;
         a0 = pstart;
         a1 = pend;
         whole = false;
-        first = false;  // a segment starting in this range is not the sink's first
         v = list != nullptr ? list[j] : static_cast<int>(j);
       } else {
         const long long q = it - has_pred;
@@ -1279,46 +1272,26 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
         a0 = a;
         whole = b - a <= kRecomputeSeg;
         a1 = whole ? b : a + kRecomputeSeg;
-        first = true;
       }
       const int na = static_cast<int>(a1 - a0);  // arcs in the segment (<= kRecomputeSeg)
-      if (BK && na == 0) continue;                // no message reached the sink (the same for the group)
       float *sv = S + static_cast<long long>(v) * d;
-      // BK: the row's current values, fetched with the segment's slots (used when the
-      // bucket is one segment; the load is unconditional so that it goes out at once)
-      float prev[NC];
-      if (BK) {
-#pragma unroll
-        for (int p = 0; p < NC; ++p) prev[p] = sv[k0 + p * G];  // past d: the next row or the tail (never used)
-      }
-      // BK: slot a0 + i of the buckets; else in-arc a0 + i of the sink's row
-      const long long row0 = BK ? a0 : in.off[v] - ioff[j] + a0;
-      if (BK && k0 == 0 && first) bk.cnt[v] = 0;  // the bucket's start is no longer needed
+      // in-arc a0 + i of the sink's row
+      const long long row0 = in.off[v] - ioff[j] + a0;
       // arc i of the segment is fetched by lane i % G of the group, into slot i / G
       int uq[kPer];
-      Acc cq[kPer];
+      double cq[kPer];
 #pragma unroll
       for (int q = 0; q < kPer; ++q) {
         const int i = k0 + q * G;
-        if (BK) {
-          // unconditional loads from a clamped slot (na >= 1 here), masked afterwards:
-          // no branch between them
-          const long long at = row0 + (i < na ? i : na - 1);
-          const int x = bk.idx[at];
-          const float wx = weighted ? bk.wt[at] : 1.0f;
-          uq[q] = i < na ? x : -1;
-          cq[q] = i < na ? wx : 1.0f;
-        } else {
-          uq[q] = i < na ? in.col[row0 + i] : -1;
-          cq[q] = i < na && weighted ? static_cast<double>(in.wt[row0 + i]) : 1.0;
-        }
+        uq[q] = i < na ? in.col[row0 + i] : -1;
+        cq[q] = i < na && weighted ? static_cast<double>(in.wt[row0 + i]) : 1.0;
       }
-      if (!BK && gcn) {
+      if (gcn) {
 #pragma unroll
         for (int q = 0; q < kPer; ++q)
           if (uq[q] >= 0) cq[q] /= sqrt(static_cast<double>(out_len[uq[q]]) + 1.0);
       }
-      Acc acc[NC];
+      double acc[NC];
 #pragma unroll
       for (int q = 0; q < NC; ++q) acc[q] = 0;
 #pragma unroll
@@ -1326,7 +1299,7 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
         if (st * U >= na) break;  // the same for the group's lanes
         const int q = st * U / G;  // the fetch slot of this step's arcs
         int uu[U];
-        Acc cc[U];
+        double cc[U];
 #pragma unroll
         for (int t = 0; t < U; ++t) {
           const int from = grp * G + (st * U + t) % G;
@@ -1342,7 +1315,7 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
         for (int t = 0; t < U; ++t) {
           // the group's whole span from the row start, column offsets as immediates
           // (columns past d read the next row or the table's tail, kRowTail)
-          const float *su = src + static_cast<long long>(uu[t] >= 0 ? uu[t] : 0) * sld + k0;
+          const float *su = src + static_cast<long long>(uu[t] >= 0 ? uu[t] : 0) * d + k0;
           const unsigned keep = uu[t] >= 0 ? ~0u : 0u;
 #pragma unroll
           for (int p = 0; p < NC; ++p) row[t][p] = __uint_as_float(__float_as_uint(su[p * G]) & keep);
@@ -1350,13 +1323,13 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
 #pragma unroll
         for (int t = 0; t < U; ++t)
 #pragma unroll
-          for (int p = 0; p < NC; ++p) acc[p] += cc[t] * static_cast<Acc>(row[t][p]);
+          for (int p = 0; p < NC; ++p) acc[p] += cc[t] * static_cast<double>(row[t][p]);
       }
 #pragma unroll
       for (int p = 0; p < NC; ++p) {
         const int k = k0 + p * G;
         if (k < d) {
-          if (whole) sv[k] = BK ? prev[p] + static_cast<float>(acc[p]) : static_cast<float>(acc[p]);
+          if (whole) sv[k] = static_cast<float>(acc[p]);
           else unsafeAtomicAdd(&sv[k], static_cast<float>(acc[p]));
         }
       }
@@ -1365,6 +1338,198 @@ __global__ __launch_bounds__(256) void k_recompute(int d, int sld, int gcn, cons
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
+// The bucket form's sums (see launch_bucket_sum), on the recompute's split with
+// bucket slots for in-arcs: ranges of C <= kRecomputeSeg consecutive slots, a
+// contiguous run of them per wave; a range owns the first segment (up to
+// kRecomputeSeg slots) of each sink whose bucket starts in it and at most one
+// later segment of the sink before. Besides the message and aggregate rows, a
+// range reads only three windows, which its wave fetches in one round of loads:
+// the bucket starts and the vertices of the 64 sinks from the one before the
+// range's first (lane t: boff and list at jf - 1 + t), and the 128 slots (message
+// row and weight) from the range start, since a segment that starts in a range of
+// at most 64 slots ends within 128 slots of its start. The windows of the wave's
+// next range are fetched while the groups sum this range's segments, so a segment
+// costs one round trip: its message rows, loaded together with its aggregate row.
+// Sums are fp32; a one-segment bucket is added with a plain load and store, longer
+// ones with atomics. Sinks with empty buckets are left alone; each sink's first
+// segment resets its counter.
+template <int G, int NC, int U>
+__global__ __launch_bounds__(256) void k_bucket_sum(int d, int ld, const int *list, const u64 *count,
+                                                    const long long *boff, Buckets bk, const float *msg, float *S,
+                                                    const Counters *c) {
+  static_assert(kWave % G == 0 && G % U == 0 && kRecomputeSeg % U == 0, "steps of U slots");
+  static_assert(kRecomputeSeg <= kWave, "a segment starting in a range ends within two windows of slots");
+  constexpr int kSlots = 2 * kWave;
+  constexpr int kSteps = kRecomputeSeg / U;
+  constexpr int kGroups = kWave / G;
+  __shared__ long long win_b[256 / kWave][kWave];
+  __shared__ int win_v[256 / kWave][kWave];
+  __shared__ int win_u[256 / kWave][kSlots];
+  __shared__ float win_w[256 / kWave][kSlots];
+  const int w = threadIdx.x / kWave;
+  long long *wb = win_b[w];
+  int *wv = win_v[w], *wu = win_u[w];
+  float *ww = win_w[w];
+  const long long nA = static_cast<long long>(*count);
+  if (aborted_with(c->abort, nA) || nA == 0) return;
+  const long long E = boff[nA];
+  if (E == 0) return;  // no message reached any sink
+  const int lane = lane_id();
+  const int grp = lane / G, k0 = lane % G;
+  const bool weighted = bk.wt != nullptr;
+  // the weight window is loaded unconditionally (from the slot array when there are no weights)
+  const float *wsrc = weighted ? bk.wt : reinterpret_cast<const float *>(bk.idx);
+  const long long waves = num_waves();
+  long long C = 16;
+  while (C < kRecomputeSeg && C * waves < E) C <<= 1;
+  const long long ranges = (E + C - 1) / C;
+  const long long per = (ranges + waves - 1) / waves;
+  const long long r0 = global_wave() * per;
+  const long long r1 = r0 + per < ranges ? r0 + per : ranges;
+  if (r0 >= r1) return;
+  // the window registers of the next range (clamped loads: entries outside the
+  // list or the slots repeat its ends and are never used, except boff past nA,
+  // which reads E and so ends the search for the range's last sink)
+  long long nb;
+  int nv, nu0, nu1;
+  float nw0, nw1;
+  const auto fetch = [&](long long jf, long long R0) {
+    const long long i = jf - 1 + lane;
+    const long long ib = i < 0 ? 0 : i > nA ? nA : i;
+    const long long iv = i < 0 ? 0 : i > nA - 1 ? nA - 1 : i;
+    const long long s0 = R0 + lane < E ? R0 + lane : E - 1;
+    const long long s1 = R0 + kWave + lane < E ? R0 + kWave + lane : E - 1;
+    nb = boff[ib];
+    nv = list[iv];
+    nu0 = bk.idx[s0];
+    nu1 = bk.idx[s1];
+    nw0 = wsrc[s0];
+    nw1 = wsrc[s1];
+  };
+  // first sink starting at or after the first range's start
+  long long jf = r0 == 0 ? 0 : wave_last_le(boff, 0, nA + 1, r0 * C - 1) + 1;
+  fetch(jf, r0 * C);
+  for (long long r = r0; r < r1; ++r) {
+    const long long R0 = r * C;
+    const bool last_range = r == ranges - 1;
+    const long long R1 = last_range ? (1LL << 62) : R0 + C;
+    // the previous range's groups have read the windows: publish this range's
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    wb[lane] = nb;
+    wv[lane] = nv;
+    wu[lane] = nu0;
+    wu[kWave + lane] = nu1;
+    ww[lane] = nw0;
+    ww[kWave + lane] = nw1;
+    // the last sink starting before R1: the window's entries <= R1 - 1 form a prefix
+    // (lane 0 stands for the sink before jf, or for nothing when jf = 0)
+    long long jl = nA - 1;
+    if (!last_range) {
+      const bool le = jf - 1 + lane < 0 || nb <= R1 - 1;
+      const int cnt = __popcll(__ballot(le));
+      jl = jf + cnt - 2;
+      if (cnt == kWave && jf - 1 + kWave <= nA) jl = wave_last_le(boff, jf - 2 + kWave, nA + 1, R1 - 1);
+      if (jl > nA - 1) jl = nA - 1;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (r + 1 < r1) fetch(jl + 1, R0 + C);
+    // the sink before jf covers slot R0 when its bucket ends past it: it may have a
+    // segment starting in this range
+    long long pstart = -1, pend = 0;
+    if (jf >= 1) {
+      const long long a = wb[0], b = wb[1];
+      if (b > R0) {
+        const long long s = (R0 - a + kRecomputeSeg - 1) / kRecomputeSeg;
+        const long long st = a + s * kRecomputeSeg;
+        if (st < R1 && st < b) {
+          pstart = st;
+          pend = st + kRecomputeSeg < b ? st + kRecomputeSeg : b;
+        }
+      }
+    }
+    const long long has_pred = pstart >= 0 ? 1 : 0;
+    const long long sinks = jl >= jf ? jl - jf + 1 : 0;
+    const long long items = has_pred + sinks;
+    for (long long it = grp; it < items; it += kGroups) {  // the same bounds for a group's lanes
+      long long a0, a1;
+      bool whole, first;
+      int v;
+      if (it < has_pred) {
+        a0 = pstart;
+        a1 = pend;
+        whole = false;
+        first = false;  // a segment starting in this range is not the sink's first
+        v = wv[0];
+      } else {
+        const long long q = it - has_pred;  // sink jf + q: window entries q + 1 and q + 2
+        long long a, b;
+        if (q + 2 < kWave) {
+          a = wb[q + 1];
+          b = wb[q + 2];
+          v = wv[q + 1];
+        } else {
+          a = boff[jf + q];
+          b = boff[jf + q + 1];
+          v = list[jf + q];
+        }
+        a0 = a;
+        whole = b - a <= kRecomputeSeg;
+        a1 = whole ? b : a + kRecomputeSeg;
+        first = true;
+      }
+      const int na = static_cast<int>(a1 - a0);  // slots in the segment (<= kRecomputeSeg)
+      if (na == 0) continue;                      // no message reached the sink (the same for the group)
+      float *sv = S + static_cast<long long>(v) * d;
+      // the row's current values, loaded with the message rows (used when the
+      // bucket is one segment)
+      float prev[NC];
+#pragma unroll
+      for (int p = 0; p < NC; ++p) prev[p] = sv[k0 + p * G];  // past d: the next row or the tail (never used)
+      if (k0 == 0 && first) bk.cnt[v] = 0;                   // the bucket's start is no longer needed
+      const int o0 = static_cast<int>(a0 - R0);  // the segment's first slot in the window
+      float acc[NC];
+#pragma unroll
+      for (int p = 0; p < NC; ++p) acc[p] = 0.0f;
+#pragma unroll
+      for (int st = 0; st < kSteps; ++st) {
+        if (st * U >= na) break;  // the same for the group's lanes
+        // every lane loads (a slot past the segment repeats its last one, a column
+        // past the end reads the next row or the tail) and the value is masked to
+        // zero afterwards: the loads carry no branch and go out together
+        float row[U][NC];
+        float cc[U];
+#pragma unroll
+        for (int t = 0; t < U; ++t) {
+          const int i = st * U + t;
+          const int o = o0 + (i < na ? i : na - 1);
+          const float *su = msg + static_cast<long long>(wu[o]) * ld + k0;
+          cc[t] = weighted ? ww[o] : 1.0f;
+          const unsigned keep = i < na ? ~0u : 0u;
+#pragma unroll
+          for (int p = 0; p < NC; ++p) row[t][p] = __uint_as_float(__float_as_uint(su[p * G]) & keep);
+        }
+#pragma unroll
+        for (int t = 0; t < U; ++t)
+#pragma unroll
+          for (int p = 0; p < NC; ++p) acc[p] += cc[t] * row[t][p];
+      }
+#pragma unroll
+      for (int p = 0; p < NC; ++p) {
+        const int k = k0 + p * G;
+        if (k < d) {
+          if (whole) sv[k] = prev[p] + acc[p];
+          else unsafeAtomicAdd(&sv[k], acc[p]);
+        }
+      }
+    }
+    jf = jl + 1;
   }
 }
 
@@ -1521,38 +1686,38 @@ void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list
 #undef RP_PULLM
 }
 
-#define RP_RECOMP_ALL(BKV)                                                                                     \
+// (G, NC, U) by row width: lane groups of 16 up to 64 columns, whole waves above
+#define RP_BY_WIDTH(M)                                                                                         \
   do {                                                                                                         \
-    if (d <= 16) RP_RECOMP(16, 1, 8, BKV);                                                                     \
-    else if (d <= 32) RP_RECOMP(16, 2, 8, BKV);                                                                \
-    else if (d <= 48) RP_RECOMP(16, 3, 8, BKV);                                                                \
-    else if (d <= 64) RP_RECOMP(16, 4, 8, BKV);                                                                \
-    else if (d <= 128) RP_RECOMP(64, 2, 8, BKV);                                                               \
-    else if (d <= 256) RP_RECOMP(64, 4, 8, BKV);                                                               \
-    else if (d <= 512) RP_RECOMP(64, 8, 4, BKV);                                                               \
-    else RP_RECOMP(64, 16, 2, BKV);                                                                            \
+    if (d <= 16) M(16, 1, 8);                                                                                  \
+    else if (d <= 32) M(16, 2, 8);                                                                             \
+    else if (d <= 48) M(16, 3, 8);                                                                             \
+    else if (d <= 64) M(16, 4, 8);                                                                             \
+    else if (d <= 128) M(64, 2, 8);                                                                            \
+    else if (d <= 256) M(64, 4, 8);                                                                            \
+    else if (d <= 512) M(64, 8, 4);                                                                            \
+    else M(64, 16, 2);                                                                                         \
   } while (0)
 
 void launch_recompute(hipStream_t s, long long n, int d, int gcn, const int *list, const u64 *count,
                       const long long *ioff, Adj in, const int *out_len, const float *src, float *S, const Counters *c) {
   const int blocks = 2048;
-#define RP_RECOMP(GV, NCV, UV, BKV)                                                                              \
-  RP_LAUNCH((k_recompute<GV, NCV, UV, BKV>), dim3(blocks), dim3(256), 0, s, d, d, gcn, list, count, ioff, in, \
-            out_len, src, S, c, Buckets{})
-  RP_RECOMP_ALL(false);
+#define RP_RECOMP(GV, NCV, UV)                                                                                   \
+  RP_LAUNCH((k_recompute<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, gcn, list, count, ioff, in, out_len, \
+            src, S, c)
+  RP_BY_WIDTH(RP_RECOMP);
 #undef RP_RECOMP
 }
 
 void launch_bucket_sum(hipStream_t s, int d, int ld, const int *list, const u64 *count, const long long *boff,
                        const Buckets &bk, const float *msg, float *S, const Counters *c) {
   const int blocks = 2048;
-#define RP_RECOMP(GV, NCV, UV, BKV)                                                                              \
-  RP_LAUNCH((k_recompute<GV, NCV, UV, BKV>), dim3(blocks), dim3(256), 0, s, d, ld, 0, list, count, boff, Adj{}, \
-            nullptr, msg, S, c, bk)
-  RP_RECOMP_ALL(true);
-#undef RP_RECOMP
+#define RP_BSUM(GV, NCV, UV)                                                                                     \
+  RP_LAUNCH((k_bucket_sum<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, boff, bk, msg, S, c)
+  RP_BY_WIDTH(RP_BSUM);
+#undef RP_BSUM
 }
-#undef RP_RECOMP_ALL
+#undef RP_BY_WIDTH
 
 void launch_pull(hipStream_t s, long long n, int d, int agg, const float *Hprev, Adj in, const int *out_len,
                  float *S) {
