@@ -177,6 +177,27 @@ def test_dense_large_full_size(config, schedule):
         p.close()
 
 
+def test_dense_large_bf16_full_size():
+    """The 3-layer Products-shaped model with bf16 transform operands, as bench.py
+    runs its bf16 line: two batches of 1000 with affected sets bit for bit, then the
+    sampled vertices (the 16 highest in-degrees among them) at every layer within
+    R16's 2e-2 of the float64 oracle."""
+    t0 = time.time()
+    wl = synth.build_workload("dense_large")
+    p = Pair(wl.n, wl.src, wl.dst, wl.x, wl.weights, undirected=True, gemm="bf16")
+    try:
+        _say(f"dense_large bf16: loaded + bootstrapped, oracle built ({time.time() - t0:.0f}s)")
+        for b in range(2):
+            st, _, sets = p.step(wl.stream.next_batch(1000))
+            _say(f"  batch {b}: |A| = {[s.size for s in sets]}, dense layers {st['dense_layers']:b}, "
+                 f"bucket layers {st['bucket_layers']:b} ({time.time() - t0:.0f}s)")
+        verts, _ = _sample_vertices(np.random.default_rng(7), p.orc, sets[3], 24, 400_000)
+        errs = _check_sampled(p, verts, (1, 2, 3), tol=FP32_TOL_BF16)
+        _say(f"  {verts.size} sampled vertices, row-relative errors {errs} ({time.time() - t0:.0f}s)")
+    finally:
+        p.close()
+
+
 @pytest.mark.parametrize("mode", ["auto", "pull", "dense"])
 def test_stress_full_size(mode):
     """RMAT graph at full size (2^23 vertices, 200M arcs, GCN 64-256-64), one
