@@ -208,7 +208,7 @@ def roof(p, name, traffic, peak_tflops, gemm_label):
                 "frac": ach / peak_tflops, "algorithmic_per_launch": per, **common}
     per = p["bytes"] / p["launches"]
     ach = per / avg_s / 1e9
-    return {"kernel": "k_scatter / k_pull_msgs / k_recompute / k_bucket_arcs / k_bucket_sum (message step)", "bound": "hbm", "achieved": ach,
+    return {"kernel": "k_scatter / k_pull_msgs / k_recompute / k_bin_arcs / k_bin_sort / k_bucket_sum (message step)", "bound": "hbm", "achieved": ach,
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "algorithmic_per_launch": per,
             "no_reuse_per_launch": p["bytes_no_reuse"] / p["launches"],
             "bytes_note": "algorithmic: each message row read once, each sink row of S read and written once (each "

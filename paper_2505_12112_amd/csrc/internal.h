@@ -425,33 +425,55 @@ struct ScatterList {
 };
 // packed_in: count points at a scatter-built list's packed counter (count and arc
 // total in one word; pushed is then not read).
-// The bucket form's arrays: per-vertex counters (zero between batches), per pushed
-// arc its rank among its sink's arcs, and per bucket slot the source's list
-// position (its message row) and the arc's weight (weighted-sum model only, else
-// null).
+// The bucket form's arrays. The pushed arcs are sorted by sink in two levels:
+// into bins of 2^shift consecutive sinks (nbins bins), then by sink within each
+// bin. cnt: a counter per vertex (bucket_counter_slots(n) of them, zero between
+// batches); bin_total, bin_base: per bin its arc count (zero between batches) and
+// its first slot; block_off: per counting block and bin the block's place in the
+// bin; tv, tj, tw: the arcs grouped by bin (sink, source list position, weight);
+// idx, wt: the same grouped by sink, each sink's bucket contiguous and the buckets
+// in vertex order. Slots number the pushed arcs (fewer than 2^31); tw and wt only
+// under the weighted-sum model, else null.
 struct Buckets {
   int *cnt;
-  int *rank;
+  int *bin_total;
+  int *bin_base;
+  int *block_off;
+  int *tv;
+  int *tj;
+  float *tw;
   int *idx;
   float *wt;
+  int shift;
+  int nbins;
 };
+// the counting and scatter passes' grid (blocks of kBinThreads threads; per block
+// and bin one atomic), and the most bins (one counter each per block in LDS)
+constexpr int kBinBlocks = 256, kBinThreads = 1024, kMaxBins = 4096;
+// log2 of the sinks per bin for n vertices (bins of 1024 to 8192 sinks, at most
+// kMaxBins bins); -1 when n needs more (the bucket form then is not available)
+int bin_shift(long long n);
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,
                     const int *del_dst, const u64 *pushed, const Counters *c, bool push, bool mark_list,
                     const ScatterCopy &copy = ScatterCopy{}, const ScatterList &lo = ScatterList{},
                     bool packed_in = false);
-// bucket count (in place of the marks-only scatter): marks the net arcs' heads and,
-// with mark_list, the list in bm_x; every arc e = (u -> v) pushed from the sorted
-// list (numbered as the scatter numbers them) takes rank[e] = b.cnt[v]++, and its
-// sink is not marked (the compaction finds the sinks from the counts).
-void launch_bucket_count(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
-                         const u64 *pushed, const Buckets &b, unsigned *bm_x, const int *ins_dst, const int *del_dst,
-                         bool mark_list, const Counters *c);
-// bucket fill: every pushed arc e goes to slot b.cnt[v] + b.rank[e] of its sink's
-// bucket (b.cnt[v] holds the bucket's start, written by the compaction), which
-// receives the source's list position and, with b.wt, the arc's weight.
-void launch_bucket_fill(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
+// bucket counting pass (in place of the marks-only scatter): marks the net arcs'
+// heads and, with mark_list, the list in bm_x; counts the arcs pushed from the
+// sorted list (numbered as the scatter numbers them) per bin and adds the counts
+// to b.bin_total, recording each block's place in b.block_off. Sinks are not
+// marked (the compaction finds them from the counts k_bin_sort leaves in b.cnt).
+void launch_bin_count(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
+                      const u64 *pushed, const Buckets &b, unsigned *bm_x, const int *ins_dst, const int *del_dst,
+                      bool mark_list, const Counters *c);
+// bucket scatter pass: the same arcs, in the same blocks, into their bins (b.tv,
+// b.tj, b.tw from each bin's first slot, stored in b.bin_base).
+void launch_bin_scatter(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
                         const u64 *pushed, const Buckets &b, const Counters *c);
+// bucket sort within the bins: per sink its count into b.cnt (for the compaction)
+// and its arcs' source positions (and weights) into its bucket in b.idx (b.wt);
+// the bins' totals back to zero. n: vertices.
+void launch_bin_sort(hipStream_t s, long long n, const u64 *pushed, const Buckets &b, const Counters *c);
 
 // pull: for every vertex v of the sorted list A (in-arc prefix ioff; list null =
 // the identity), S[v] += sum of msg[rank(u)] over in-arcs (u -> v) whose source u

@@ -894,32 +894,82 @@ __global__ __launch_bounds__(256) void k_scatter(int d, int ld, const int *list,
 constexpr int kPullArcs = 4;  // arcs per lane per chunk (the pull and the bucket passes)
 constexpr int kPullChunk = kWave * kPullArcs;
 
+// Exclusive prefix sums of a[0, n) in LDS, in place, by a block of kBinThreads
+// threads (each a run of consecutive entries); ends with a barrier.
+__device__ inline void block_exclusive_scan(int *a, int n, int *wave_sums) {
+  const int t = threadIdx.x, lane = lane_id(), wave = t / kWave;
+  const int per = (n + kBinThreads - 1) / kBinThreads;
+  int s = 0;
+  for (int i = 0; i < per; ++i) {
+    const int k = t * per + i;
+    if (k < n) s += a[k];
+  }
+  int incl = s;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(incl, o);
+    if (lane >= o) incl += y;
+  }
+  if (lane == kWave - 1) wave_sums[wave] = incl;
+  __syncthreads();
+  int base = incl - s;
+  for (int w = 0; w < wave; ++w) base += wave_sums[w];
+  for (int i = 0; i < per; ++i) {
+    const int k = t * per + i;
+    if (k < n) {
+      const int x = a[k];
+      a[k] = base;
+      base += x;
+    }
+  }
+  __syncthreads();
+}
+
 // The bucket form's passes over the pushed arcs (numbered as in the scatter), in
 // chunks of up to kPullChunk consecutive arcs per wave (a contiguous run of chunks
-// per wave), each lane up to kPullArcs consecutive arcs with all their loads in
-// flight together. The counting pass (FILL false) first marks the net arcs' heads
-// and, under a self term, D in bm_x, then gives each arc e into sink v its rank
-// among v's arcs, rank[e] = cnt[v]++ (the sinks are found from the counts). The
-// fill pass writes the arc's source position j (its message row), and its weight
-// when the model weights arcs, to slot cnt[v] + rank[e] of v's bucket, cnt[v]
-// then holding the bucket's start.
-template <bool FILL>
-__global__ __launch_bounds__(256) void k_bucket_arcs(const int *list, const u64 *count, const long long *doff,
-                                                      Adj out, const u64 *pushed, Buckets b, unsigned *bm_x,
-                                                      const int *ins_dst, const int *del_dst, int mark_list,
-                                                      const Counters *c) {
+// per wave, so that a block owns the same arcs in both passes), each lane up to
+// kPullArcs consecutive arcs with all their loads in flight together. The arcs are
+// sorted by sink in two levels: into bins of 2^shift consecutive sinks here, then
+// by sink within each bin (k_bin_sort). Counting pass (SCATTER false): marks the
+// net arcs' heads and, under a self term, D in bm_x, counts the block's arcs per
+// bin in LDS, and adds each count to its bin's total with one atomic, which hands
+// back the block's place in the bin. Scatter pass: the bins' first slots are the
+// exclusive prefix of their totals (block 0 also stores them); each arc takes the
+// next place of its block in its bin (an LDS cursor) and leaves its sink, its
+// source's list position (its message row) and, when the model weights arcs, its
+// weight there.
+template <bool SCATTER>
+__global__ __launch_bounds__(kBinThreads) void k_bin_arcs(const int *list, const u64 *count, const long long *doff,
+                                                           Adj out, const u64 *pushed, Buckets b, unsigned *bm_x,
+                                                           const int *ins_dst, const int *del_dst, int mark_list,
+                                                           const Counters *c) {
+  extern __shared__ int bins[];  // per bin: the block's count, or its cursor
+  __shared__ int wave_sums[kBinThreads / kWave];
   const long long nD = static_cast<long long>(*count);
   const long long E = static_cast<long long>(*pushed);
   const long long ni = static_cast<long long>(c->n_ins);
   const long long na = ni + static_cast<long long>(c->n_del);
-  if (aborted_with(c->abort, nD, E, na)) return;
+  if (aborted_with(c->abort, nD, E, na)) return;  // the same for the whole block
   const int lane = lane_id();
-  if (!FILL) {
-    const long long stride = static_cast<long long>(gridDim.x) * blockDim.x;
-    const long long t0 = blockIdx.x * blockDim.x + threadIdx.x;
+  const int nb = b.nbins;
+  if (!SCATTER) {
+    for (int i = threadIdx.x; i < nb; i += kBinThreads) bins[i] = 0;
+    const long long stride = static_cast<long long>(gridDim.x) * kBinThreads;
+    const long long t0 = blockIdx.x * static_cast<long long>(kBinThreads) + threadIdx.x;
     for (long long i = t0; i < na; i += stride) mark_only(bm_x, i < ni ? ins_dst[i] : del_dst[i - ni]);
     if (mark_list)
       for (long long j = t0; j < nD; j += stride) mark_only(bm_x, list[j]);
+    __syncthreads();
+  } else {
+    for (int i = threadIdx.x; i < nb; i += kBinThreads) bins[i] = b.bin_total[i];
+    __syncthreads();
+    block_exclusive_scan(bins, nb, wave_sums);
+    const int *own = b.block_off + static_cast<long long>(blockIdx.x) * nb;
+    for (int i = threadIdx.x; i < nb; i += kBinThreads) {
+      if (blockIdx.x == 0) b.bin_base[i] = bins[i];
+      bins[i] += own[i];
+    }
+    __syncthreads();
   }
   const long long waves = num_waves();
   const long long n1 = nD + 1;  // a compacted list: doff[nD] holds the arc total
@@ -971,28 +1021,88 @@ __global__ __launch_bounds__(256) void k_bucket_arcs(const int *list, const u64 
       slot[a] = on[a] ? out.off[u] + (e[a] - doff[r[a]]) : 0;
     }
 #pragma unroll
-    for (int a = 0; a < kPullArcs; ++a) v[a] = on[a] ? out.col[slot[a]] : -1;
-    if (!FILL) {
-      int rk[kPullArcs];
-#pragma unroll
-      for (int a = 0; a < kPullArcs; ++a) rk[a] = on[a] ? atomicAdd(&b.cnt[v[a]], 1) : 0;
+    for (int a = 0; a < kPullArcs; ++a) v[a] = on[a] ? out.col[slot[a]] : 0;
+    if (!SCATTER) {
 #pragma unroll
       for (int a = 0; a < kPullArcs; ++a)
-        if (on[a]) b.rank[e[a]] = rk[a];
+        if (on[a]) atomicAdd(&bins[v[a] >> b.shift], 1);
     } else {
-      int at[kPullArcs];
       float w[kPullArcs];
 #pragma unroll
-      for (int a = 0; a < kPullArcs; ++a) {
-        at[a] = on[a] ? b.cnt[v[a]] + b.rank[e[a]] : 0;
-        w[a] = on[a] && b.wt != nullptr ? out.wt[slot[a]] : 1.0f;
-      }
+      for (int a = 0; a < kPullArcs; ++a) w[a] = on[a] && b.tw != nullptr ? out.wt[slot[a]] : 1.0f;
 #pragma unroll
       for (int a = 0; a < kPullArcs; ++a) {
         if (!on[a]) continue;
-        b.idx[at[a]] = r[a];
-        if (b.wt != nullptr) b.wt[at[a]] = w[a];
+        const int p = atomicAdd(&bins[v[a] >> b.shift], 1);
+        b.tv[p] = v[a];
+        b.tj[p] = r[a];
+        if (b.tw != nullptr) b.tw[p] = w[a];
       }
+    }
+  }
+  if (!SCATTER) {
+    // the block's counts into the bins' totals; a bin it has no arc in gets place 0
+    __syncthreads();
+    int *own = b.block_off + static_cast<long long>(blockIdx.x) * nb;
+    for (int i = threadIdx.x; i < nb; i += kBinThreads) own[i] = bins[i] > 0 ? atomicAdd(&b.bin_total[i], bins[i]) : 0;
+  }
+}
+
+// Second level of the bucket sort: block i takes bin i (sinks i 2^shift ..
+// (i + 1) 2^shift - 1, its arcs in slots bin_base[i] .. + bin_total[i]). It counts
+// the arcs per sink in LDS, stores the counts in cnt (from which the compaction
+// lists the sinks and forms their buckets' offsets, the same prefix sums in vertex
+// order), then places each arc at its sink's next slot: idx (and wt) hold each
+// sink's bucket contiguously, buckets in vertex order. Resets the bin's total.
+__global__ __launch_bounds__(kBinThreads) void k_bin_sort(long long n, const u64 *pushed, Buckets b,
+                                                           const Counters *c) {
+  extern __shared__ int cur[];  // per sink of the bin: its count, then its next slot
+  __shared__ int wave_sums[kBinThreads / kWave];
+  const long long E = static_cast<long long>(*pushed);
+  if (aborted_with(c->abort, E)) return;
+  const int bin = blockIdx.x;
+  const int total = b.bin_total[bin];
+  if (total == 0) return;  // the same for the whole block; its sinks' counters stay zero
+  const int base = b.bin_base[bin];
+  const int span = 1 << b.shift;
+  const long long v0 = static_cast<long long>(bin) << b.shift;
+  const int nv = static_cast<int>(n - v0 < span ? n - v0 : span);
+  const int t = threadIdx.x;
+  for (int i = t; i < span; i += kBinThreads) cur[i] = 0;
+  __syncthreads();
+  if (t == 0) b.bin_total[bin] = 0;  // every thread has read it
+  constexpr int kU = 4;  // arcs per thread in flight
+  for (int p0 = t; p0 < total; p0 += kU * kBinThreads) {
+    int vv[kU];
+#pragma unroll
+    for (int q = 0; q < kU; ++q) {
+      const int p = p0 + q * kBinThreads;
+      vv[q] = p < total ? b.tv[base + p] : -1;
+    }
+#pragma unroll
+    for (int q = 0; q < kU; ++q)
+      if (vv[q] >= 0) atomicAdd(&cur[vv[q] - v0], 1);
+  }
+  __syncthreads();
+  for (int i = t; i < nv; i += kBinThreads) b.cnt[v0 + i] = cur[i];
+  block_exclusive_scan(cur, span, wave_sums);
+  for (int p0 = t; p0 < total; p0 += kU * kBinThreads) {
+    int vv[kU], jj[kU];
+    float ww[kU];
+#pragma unroll
+    for (int q = 0; q < kU; ++q) {
+      const int p = p0 + q * kBinThreads;
+      const bool on = p < total;
+      vv[q] = on ? b.tv[base + p] : -1;
+      jj[q] = on ? b.tj[base + p] : 0;
+      ww[q] = on && b.tw != nullptr ? b.tw[base + p] : 1.0f;
+    }
+#pragma unroll
+    for (int q = 0; q < kU; ++q) {
+      if (vv[q] < 0) continue;
+      const int at = base + atomicAdd(&cur[vv[q] - v0], 1);
+      b.idx[at] = jj[q];
+      if (b.wt != nullptr) b.wt[at] = ww[q];
     }
   }
 }
@@ -1653,17 +1763,29 @@ void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, 
 #undef RP_SCATTER_L
 }
 
-void launch_bucket_count(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
-                         const u64 *pushed, const Buckets &b, unsigned *bm_x, const int *ins_dst, const int *del_dst,
-                         bool mark_list, const Counters *c) {
-  RP_LAUNCH(k_bucket_arcs<false>, dim3(2048), dim3(256), 0, s, list, count, doff, out, pushed, b, bm_x, ins_dst,
-            del_dst, mark_list ? 1 : 0, c);
+int bin_shift(long long n) {
+  // bins of at least 1024 sinks, at most kMaxBins of them, at most 8192 sinks each
+  int s = 10;
+  while ((n + (1LL << s) - 1) >> s > kMaxBins) ++s;
+  return s <= 13 ? s : -1;
 }
 
-void launch_bucket_fill(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
+void launch_bin_count(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
+                      const u64 *pushed, const Buckets &b, unsigned *bm_x, const int *ins_dst, const int *del_dst,
+                      bool mark_list, const Counters *c) {
+  RP_LAUNCH(k_bin_arcs<false>, dim3(kBinBlocks), dim3(kBinThreads), b.nbins * sizeof(int), s, list, count, doff, out,
+            pushed, b, bm_x, ins_dst, del_dst, mark_list ? 1 : 0, c);
+}
+
+void launch_bin_scatter(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
                         const u64 *pushed, const Buckets &b, const Counters *c) {
-  RP_LAUNCH(k_bucket_arcs<true>, dim3(2048), dim3(256), 0, s, list, count, doff, out, pushed, b, nullptr, nullptr,
-            nullptr, 0, c);
+  RP_LAUNCH(k_bin_arcs<true>, dim3(kBinBlocks), dim3(kBinThreads), b.nbins * sizeof(int), s, list, count, doff, out,
+            pushed, b, nullptr, nullptr, nullptr, 0, c);
+}
+
+void launch_bin_sort(hipStream_t s, long long n, const u64 *pushed, const Buckets &b, const Counters *c) {
+  RP_LAUNCH(k_bin_sort, dim3(static_cast<unsigned>(b.nbins)), dim3(kBinThreads), (sizeof(int) << b.shift), s, n,
+            pushed, b, c);
 }
 
 void launch_pull_msgs(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count,

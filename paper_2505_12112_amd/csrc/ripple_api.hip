@@ -183,9 +183,9 @@ struct ripple_ctx {
   int *frow = nullptr;  // feature row of each flist entry
   int *flist_done = nullptr;  // [n]: A^0 of the last completed batch (written by its clean-up)
   // the bucket form's arrays, allocated when a plan first uses the form: per-vertex
-  // counters (zero between batches) and bucket slots for as many arcs as the
-  // out-direction has slots, which bounds the arcs any layer pushes
-  rp::Buckets bkt{nullptr, nullptr, nullptr, nullptr};
+  // counters and per-bin totals (zero between batches), and slots for as many arcs
+  // as the out-direction has slots, which bounds the arcs any layer pushes
+  rp::Buckets bkt{};
   long long bkt_cap = 0;
   bool bkt_off = false;  // the arrays could not be allocated: the time model leaves the form out
   // rows long enough for the chunked delete sweep exist (or may, once rows grow):
@@ -518,6 +518,20 @@ ripple_status ensure_batch_scratch(ripple_ctx *c, long long ops, long long frows
   return RIPPLE_OK;
 }
 
+// The bucket form's arrays (allocated again when a plan next uses the form).
+void free_buckets(ripple_ctx *c) {
+  dfree_t(c, c->bkt.cnt);
+  dfree_t(c, c->bkt.bin_total);
+  dfree_t(c, c->bkt.bin_base);
+  dfree_t(c, c->bkt.block_off);
+  dfree_t(c, c->bkt.tv);
+  dfree_t(c, c->bkt.tj);
+  dfree_t(c, c->bkt.tw);
+  dfree_t(c, c->bkt.idx);
+  dfree_t(c, c->bkt.wt);
+  c->bkt_cap = 0;
+}
+
 void free_model(ripple_ctx *c) {
   for (int l = 0; l < rp::kMaxL; ++l) {
     dfree_t(c, c->W[l]);
@@ -542,11 +556,7 @@ void free_model(ripple_ctx *c) {
   dfree_t(c, c->delta[1]);
   dfree_t(c, c->ioff);
   dfree_t(c, c->flist_done);
-  dfree_t(c, c->bkt.cnt);
-  dfree_t(c, c->bkt.rank);
-  dfree_t(c, c->bkt.idx);
-  dfree_t(c, c->bkt.wt);
-  c->bkt_cap = 0;
+  free_buckets(c);
   for (int k = 0; k < 2; ++k) {
     dfree_t(c, c->memb[k]);
   }
@@ -752,26 +762,28 @@ void add_launches(ripple_ctx *c, int phase, int k) {
 //              (15 ps per arc plus the row at 6 TB/s, the rate of random row reads
 //              from a table larger than the caches), one plain row store per
 //              affected vertex at 5 TB/s;
-//   bucket     87 ps per pushed arc (its count and rank, its bucket slot written,
-//              read back and its message row summed), one read-modify-write of
-//              each affected row at 0.91 TB/s, and 15 us for the two extra
-//              launches (fitted to the form's kernels on dense_large's second
-//              layer at batches 100 and 1000); it is taken only when its estimate
-//              is a quarter below every other form's (the fit is looser at a
-//              million arcs and below, where it loses to the push).
+//   bucket     35 ps per pushed arc for its trip through the bins (counted,
+//              placed, sorted into its sink's bucket), its message row read by the
+//              sums at 10 TB/s while the dirty rows' table stays within 32 MB (it
+//              is then served by the caches; 4 TB/s beyond), each affected row
+//              read and written once at 2.5 TB/s, and 20 us for the three extra
+//              launches (fitted to the form's kernels on dense_large_2l's second
+//              layer at batch 1000, stress's first and dense_large's second at
+//              batch 100); it is taken only when its estimate is a quarter below
+//              every other form's.
 // Every reanchor_every-th batch recomputes every layer (the drift budget), whatever
 // the form.
 enum LayerMode { kPushLayer = 0, kPullLayer = 1, kDenseLayer = 2, kRecomputeLayer = 3, kBucketLayer = 4 };
 
-int layer_mode(const ripple_ctx *c, int l, double pushed, double count, double in_arcs, bool reanchor) {
+int layer_mode(const ripple_ctx *c, int l, double dirty, double pushed, double count, double in_arcs, bool reanchor) {
   if (reanchor || c->scatter_mode == RIPPLE_SCATTER_RECOMPUTE) return kRecomputeLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_PUSH) return kPushLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_PULL) return kPullLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_DENSE) return kDenseLayer;
   if (c->scatter_mode == RIPPLE_SCATTER_BUCKET) return kBucketLayer;
-  const bool bucket_ok = !c->bkt_off;
+  const bool bucket_ok = !c->bkt_off && rp::bin_shift(c->n) >= 0;
   constexpr double kArc = 90e-12, kAtomicRate = 1.3e12, kMark = 38e-12, kPullScan = 35e-12;
-  constexpr double kBucketArc = 87e-12, kBucketRowRate = 0.91e12, kBucketFixed = 15e-6;
+  constexpr double kBinArc = 35e-12, kBucketRmwRate = 2.5e12, kBucketFixed = 20e-6;
   constexpr double kDenseScan = 25e-12, kDenseVertex = 20e-12, kReadRate = 10e12;
   constexpr double kRecScan = 15e-12, kGatherRate = 6e12, kStoreRate = 5e12;
   const double w = 4.0 * c->sw[l];  // message row bytes
@@ -780,7 +792,8 @@ int layer_mode(const ripple_ctx *c, int l, double pushed, double count, double i
   const double pull = pushed * kMark + in_arcs * kPullScan + settle;
   const double dense = static_cast<double>(c->arcs_now) * kDenseScan + static_cast<double>(c->n) * kDenseVertex + settle;
   const double recompute = pushed * kMark + in_arcs * (kRecScan + w / kGatherRate) + count * w / kStoreRate;
-  const double bucket = pushed * kBucketArc + count * w / kBucketRowRate + kBucketFixed;
+  const double gather = dirty * w <= 32e6 ? 10e12 : 4e12;
+  const double bucket = pushed * (kBinArc + w / gather) + count * 2.0 * w / kBucketRmwRate + kBucketFixed;
   int best = kPushLayer;
   double t = push;
   if (pull < t) best = kPullLayer, t = pull;
@@ -882,7 +895,7 @@ BatchPlan make_plan(const ripple_ctx *c) {
   long long guess[rp::kMaxL + 1];
   for (int l = 0; l <= c->L; ++l) guess[l] = static_cast<long long>(count[l]);
   for (int l = 1; l <= c->L; ++l) {
-    p.mode[l] = layer_mode(c, l, pushed[l], count[l], in_arcs[l], reanchor);
+    p.mode[l] = layer_mode(c, l, count[l - 1], pushed[l], count[l], in_arcs[l], reanchor);
     p.tf_rows[l] = guess[l - 1];
     p.rows[l] = guess[l];
     if (p.mode[l] == kBucketLayer) p.key2 |= 1ull << l;
@@ -1079,13 +1092,22 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
       if (app)
         lo = rp::ScatterList{c->lists[l],       l < c->L ? c->doff[l] : nullptr, &dc->app[l], &dc->app_sinks[l],
                              c->adj[0].len, c->adj[1].len};
-      if (mode == kBucketLayer)  // D is a compacted list here (see the bucket branch below)
-        rp::launch_bucket_count(s, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], out_msg, &dc->pushed[l],
-                                c->bkt, c->bm_x, c->ins_dst, c->del_dst, rp::has_self_term(c->agg), dc);
-      else
+      if (mode == kBucketLayer) {
+        // the pushed arcs sorted by sink (D is a compacted list here: a scatter lists
+        // A^{l-1} only when layer l pushes, and the corrections kernel lists A^0 only
+        // when layer 1 does); the compaction below lists the sinks from their counts
+        rp::Buckets b = c->bkt;
+        if (out_msg.wt == nullptr) b.tw = b.wt = nullptr;
+        rp::launch_bin_count(s, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], out_msg, &dc->pushed[l], b,
+                             c->bm_x, c->ins_dst, c->del_dst, rp::has_self_term(c->agg), dc);
+        rp::launch_bin_scatter(s, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], out_msg, &dc->pushed[l], b, dc);
+        rp::launch_bin_sort(s, c->n, &dc->pushed[l], b, dc);
+        add_launches(c, RIPPLE_PHASE_SCATTER, 2);
+      } else {
         rp::launch_scatter(s, c->n, c->sw[l], ld, c->lists[l - 1], count_in, c->doff[l - 1], msg, out_msg, c->S[l],
                            c->bm_out, c->bm_x, c->ins_dst, c->del_dst, &dc->pushed[l], dc, mode == kPushLayer,
                            rp::has_self_term(c->agg), copy, lo, packed_in);
+      }
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     if (!app) {
@@ -1128,15 +1150,12 @@ void issue_batch(ripple_ctx *c, const BatchPlan &p, bool replay) {
                            in_msg, c->adj[0].len, layer_ptrs(c).src[l], c->S[l], dc);
       add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     } else if (mode == kBucketLayer) {
-      // each pushed arc placed in its sink's bucket, then each sink's bucket summed
-      // into its row (D is a compacted list here: a scatter lists A^{l-1} only when
-      // layer l pushes, and the corrections kernel lists A^0 only when layer 1 does)
+      // each sink's bucket summed into its row
       PhaseScope ps(c, RIPPLE_PHASE_SCATTER);
       rp::Buckets b = c->bkt;
-      if (out_msg.wt == nullptr) b.wt = nullptr;
-      rp::launch_bucket_fill(s, c->lists[l - 1], &dc->count[l - 1], c->doff[l - 1], out_msg, &dc->pushed[l], b, dc);
+      if (out_msg.wt == nullptr) b.tw = b.wt = nullptr;
       rp::launch_bucket_sum(s, c->sw[l], ld, c->lists[l], &dc->count[l], c->ioff, b, msg, c->S[l], dc);
-      add_launches(c, RIPPLE_PHASE_SCATTER, 2);
+      add_launches(c, RIPPLE_PHASE_SCATTER, 1);
     }
     {
       // the last layer's GEMM also resets the batch's scratch (extra blocks)
@@ -1189,22 +1208,38 @@ hipGraphExec_t plan_graph(ripple_ctx *c, const BatchPlan &p) {
 // a plan first needs them; the counters start at zero and every batch leaves them
 // so.
 ripple_status ensure_buckets(ripple_ctx *c) {
+  const int shift = rp::bin_shift(c->n);
+  if (shift < 0)
+    return fail(c, RIPPLE_E_INVALID, "ripple: the bucket form takes graphs of at most 2^25 vertices");
   if (c->bkt.cnt == nullptr) {
     const long long slots = rp::bucket_counter_slots(c->n);
+    const int nbins = static_cast<int>((c->n + (1LL << shift) - 1) >> shift);
+    c->bkt.shift = shift;
+    c->bkt.nbins = nbins;
     RP_TRY(dalloc_n(c, &c->bkt.cnt, slots));
     RP_HIP(c, hipMemsetAsync(c->bkt.cnt, 0, static_cast<size_t>(slots) * sizeof(int), c->stream));
+    RP_TRY(dalloc_n(c, &c->bkt.bin_total, nbins));
+    RP_HIP(c, hipMemsetAsync(c->bkt.bin_total, 0, static_cast<size_t>(nbins) * sizeof(int), c->stream));
+    RP_TRY(dalloc_n(c, &c->bkt.bin_base, nbins));
+    RP_TRY(dalloc_n(c, &c->bkt.block_off, static_cast<long long>(rp::kBinBlocks) * nbins));
   }
   const long long need = std::max<long long>(1, c->col_capacity[0]);
   if (need > std::numeric_limits<int32_t>::max())  // bucket slots are int32
     return fail(c, RIPPLE_E_OOM, "ripple: the bucket form needs fewer than 2^31 out-arc slots");
   if (c->bkt_cap < need) {
-    dfree_t(c, c->bkt.rank);
+    dfree_t(c, c->bkt.tv);
+    dfree_t(c, c->bkt.tj);
+    dfree_t(c, c->bkt.tw);
     dfree_t(c, c->bkt.idx);
     dfree_t(c, c->bkt.wt);
     c->bkt_cap = 0;
-    RP_TRY(dalloc_n(c, &c->bkt.rank, need));
+    RP_TRY(dalloc_n(c, &c->bkt.tv, need));
+    RP_TRY(dalloc_n(c, &c->bkt.tj, need));
     RP_TRY(dalloc_n(c, &c->bkt.idx, need));
-    if (c->agg == rp::kGcWsum) RP_TRY(dalloc_n(c, &c->bkt.wt, need));
+    if (c->agg == rp::kGcWsum) {
+      RP_TRY(dalloc_n(c, &c->bkt.tw, need));
+      RP_TRY(dalloc_n(c, &c->bkt.wt, need));
+    }
     c->bkt_cap = need;
   }
   return RIPPLE_OK;
@@ -1221,11 +1256,7 @@ ripple_status launch_batch(ripple_ctx *c) {
       // give back what was allocated of its arrays)
       c->bkt_off = true;
       c->err.clear();
-      dfree_t(c, c->bkt.cnt);
-      dfree_t(c, c->bkt.rank);
-      dfree_t(c, c->bkt.idx);
-      dfree_t(c, c->bkt.wt);
-      c->bkt_cap = 0;
+      free_buckets(c);
       p = make_plan(c);
     } else if (st != RIPPLE_OK) {
       return st;

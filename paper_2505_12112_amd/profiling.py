@@ -40,7 +40,7 @@ ROOT = os.path.dirname(HERE)
 TRAFFIC_MD = os.path.join(ROOT, "profiles", "hbm_traffic_counters.md")
 
 # kernels whose launches make up each rooflined phase of bench.py
-PHASE_KERNELS = {"scatter": ("k_scatter", "k_pull_msgs", "k_recompute", "k_bucket_arcs", "k_bucket_sum"),
+PHASE_KERNELS = {"scatter": ("k_scatter", "k_pull_msgs", "k_recompute", "k_bin_arcs", "k_bin_sort", "k_bucket_sum"),
                  "gemm": ("k_gemm",)}
 
 
@@ -147,8 +147,8 @@ def stats_table(trace_dir: str, title: str, command: str, top: int = 24) -> str:
     if segs:
         out += ["", "Per workload the process ran (in order), over its update batches (bootstrap left out):",
                 "kernel time per batch (first batch, median of the rest) and the average dispatch of each "
-                "rooflined phase (gemm: k_gemm*; scatter: k_scatter*, k_pull_msgs*, k_recompute*, k_bucket_arcs*, "
-                "k_bucket_sum*)."]
+                "rooflined phase (gemm: k_gemm*; scatter: k_scatter*, k_pull_msgs*, k_recompute*, k_bin_arcs*, "
+                "k_bin_sort, k_bucket_sum*)."]
         for i, sg in enumerate(segs):
             b = [ns for ns, _ in sg["batches"]]
             if not b:

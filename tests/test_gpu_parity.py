@@ -343,7 +343,8 @@ def test_phase_stats_count_launches_and_bytes(mode):
     spare arena might not hold the batch's row moves), three layer-0 launches per
     batch, one when layer 1 pushes: the corrections kernel then lists the
     feature-written vertices and their deltas itself; per layer one message launch when pushing,
-    two when pulling, three in the bucket form (count, fill, sum); a pushing layer's
+    two when pulling, four in the bucket form (bin count, bin scatter, sort within
+    the bins, sums); a pushing layer's
     scatter lists A^l itself, the other forms compact it, and the dense form's full
     listing counts with the compactions), and the no-reuse byte bound
     of the message step is at least its algorithmic bytes."""
@@ -364,7 +365,7 @@ def test_phase_stats_count_launches_and_bytes(mode):
         # (one netting launch: batches of up to 1024 ops are netted in one pass)
         assert ph["net"]["launches"] == nb and ph["topo"]["launches"] == nb
         assert ph["layer0"]["launches"] == (1 if mode == "push" else 3) * nb
-        assert ph["scatter"]["launches"] == {"push": 1, "bucket": 3}.get(mode, 2) * L * nb
+        assert ph["scatter"]["launches"] == {"push": 1, "bucket": 4}.get(mode, 2) * L * nb
         assert ph["compact"]["launches"] == {"push": 0, "pull": 1, "dense": 2, "recompute": 1, "bucket": 1}[mode] * L * nb
         assert ph["gemm"]["launches"] == L * nb and ph["total"]["launches"] == nb
         for name in ("net", "topo", "layer0", "scatter", "compact", "gemm", "total"):
@@ -524,7 +525,7 @@ def test_bucket_form_without_room_for_its_arrays():
         need = probe.lib.device_bytes()
     finally:
         probe.close()
-    # the bucket arrays need 8 bytes per out-arc slot (over 64K slots here): far more than the margin
+    # the bucket arrays need 12 bytes per out-arc slot (over 64K slots here): far more than the margin
     p = Pair(400, src, dst, x, w, max_device_bytes=need + (64 << 10))
     try:
         p.step(random_valid_batch(rng, p.orc, 30, dims[0]))  # sizes the batch scratch as the probe's did
