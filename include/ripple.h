@@ -290,11 +290,13 @@ RIPPLE_API ripple_status ripple_get_arc_weights(ripple_ctx *ctx, int32_t directi
  * current embeddings (reads only, summed in fp64 and rounded once: the
  * layer-wise recompute of Sec. IV-B, to which the incremental path degrades when
  * a hop covers the graph, Sec. VII-C; it also re-anchors the cached rows);
- * RIPPLE_SCATTER_BUCKET, the pushed arcs sorted by sink (counted, then placed in
- * per-sink buckets) and each sink's bucket summed and added to its row once (the
- * messages of Sec. IV-C.1 combined per sink before they reach the aggregate; the
- * first batch that uses the form allocates 8 bytes per out-arc slot, 12 under the
- * weighted-sum model, and a counter per vertex);
+ * RIPPLE_SCATTER_BUCKET, the pushed arcs sorted by sink (into bins of consecutive
+ * sinks, then by sink within each bin) and each sink's bucket summed and added to
+ * its row once (the messages of Sec. IV-C.1 combined per sink before they reach
+ * the aggregate; the first batch that uses the form allocates 12 bytes per
+ * out-arc slot, 20 under the weighted-sum model, a counter per vertex and 258 per
+ * bin of 1024 or more vertices; graphs of at most 2^25 vertices, a batch asking
+ * for the form on a larger one fails with RIPPLE_E_INVALID);
  * RIPPLE_SCATTER_AUTO (default), per layer from the previous batch's counts, or
  * for the first batch from an estimate based on the snapshot's degrees. */
 enum {

@@ -10,7 +10,7 @@ import pytest
 
 from oracle import ripple_oracle as O
 from paper_2505_12112_amd import synth
-from paper_2505_12112_amd.ripple import PHASES, Ripple, RippleError, E_INVALID, E_STATE, E_OOM
+from paper_2505_12112_amd.ripple import OP_INSERT, PHASES, Ripple, RippleError, E_INVALID, E_STATE, E_OOM
 from tests.harness import (BF16_UNIT, FP32_TOL, FP32_TOL_BF16, CallerStream, Pair, aggregate_drift_ulps,
                            check_embeddings_conditioned, random_valid_batch)
 
@@ -506,6 +506,36 @@ def test_call_order_and_device_byte_cap():
         with pytest.raises(RippleError) as e:
             lib.init_embeddings(x, w)
         assert e.value.status == E_OOM
+    finally:
+        lib.close()
+
+
+def test_bucket_form_refused_past_its_vertex_limit():
+    """On a graph of 2^25 + 1 vertices (a few thousand edges, 4-4-2 model) a batch
+    that asks for the bucket form fails with RIPPLE_E_INVALID before anything is
+    launched (the embeddings of the touched rows are unchanged), the automatic
+    forms never pick it, and the same batch then goes through."""
+    n = (1 << 25) + 1
+    rng = np.random.default_rng(73)
+    src = rng.integers(0, n, 4000).astype(np.int32)
+    dst = rng.integers(0, n, 4000).astype(np.int32)
+    x = rng.standard_normal((n, 4)).astype(np.float32)
+    w = synth.model_weights(synth.ModelSpec("sum", (4, 4, 2)), rng)
+    lib = Ripple(n, src, dst)
+    try:
+        lib.init_embeddings(x, w)
+        ops = np.array([[OP_INSERT, int(src[i]), int(dst[(i + 1) % 4000]), -1] for i in range(50)], np.int32)
+        rows = np.unique(np.concatenate([ops[:, 1], ops[:, 2]])).astype(np.int32)
+        before = [lib.get_embeddings(l, rows) for l in (1, 2)]
+        lib.set_scatter_mode("bucket")
+        with pytest.raises(RippleError) as e:
+            lib.apply_updates(ops)
+        assert e.value.status == E_INVALID and "2^25" in str(e.value), str(e.value)
+        for l, b in zip((1, 2), before):
+            assert np.array_equal(lib.get_embeddings(l, rows), b)
+        lib.set_scatter_mode("auto")
+        st = lib.apply_updates(ops)
+        assert st["bucket_layers"] == 0 and st["ins_arcs"] > 0
     finally:
         lib.close()
 
