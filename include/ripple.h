@@ -295,7 +295,7 @@ RIPPLE_API ripple_status ripple_get_arc_weights(ripple_ctx *ctx, int32_t directi
  * its row once (the messages of Sec. IV-C.1 combined per sink before they reach
  * the aggregate; the first batch that uses the form allocates 12 bytes per
  * out-arc slot, 20 under the weighted-sum model, a counter per vertex and 258 per
- * bin of 1024 or more vertices; graphs of at most 2^25 vertices, a batch asking
+ * bin of 8192 vertices; graphs of at most 2^25 vertices, a batch asking
  * for the form on a larger one fails with RIPPLE_E_INVALID);
  * RIPPLE_SCATTER_AUTO (default), per layer from the previous batch's counts, or
  * for the first batch from an estimate based on the snapshot's degrees. */

@@ -450,8 +450,8 @@ struct Buckets {
 // the counting and scatter passes' grid (blocks of kBinThreads threads; per block
 // and bin one atomic), and the most bins (one counter each per block in LDS)
 constexpr int kBinBlocks = 256, kBinThreads = 1024, kMaxBins = 4096;
-// log2 of the sinks per bin for n vertices (bins of 1024 to 8192 sinks, at most
-// kMaxBins bins); -1 when n needs more (the bucket form then is not available)
+// log2 of the sinks per bin for n vertices (bins of 8192 sinks, at most kMaxBins
+// bins); -1 when n needs more (the bucket form then is not available)
 int bin_shift(long long n);
 void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, const u64 *count, const long long *doff,
                     const float *delta, Adj out, float *S, unsigned *bm_out, unsigned *bm_x, const int *ins_dst,

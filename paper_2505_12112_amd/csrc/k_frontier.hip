@@ -1764,10 +1764,10 @@ void launch_scatter(hipStream_t s, long long n, int d, int ld, const int *list, 
 }
 
 int bin_shift(long long n) {
-  // bins of at least 1024 sinks, at most kMaxBins of them, at most 8192 sinks each
-  int s = 10;
-  while ((n + (1LL << s) - 1) >> s > kMaxBins) ++s;
-  return s <= 13 ? s : -1;
+  // bins of 8192 sinks (few enough bins that the scatter's runs into them combine
+  // in L2), at most kMaxBins of them
+  const int s = 13;
+  return (n + (1LL << s) - 1) >> s <= kMaxBins ? s : -1;
 }
 
 void launch_bin_count(hipStream_t s, const int *list, const u64 *count, const long long *doff, Adj out,
