@@ -1831,11 +1831,18 @@ void launch_recompute(hipStream_t s, long long n, int d, int gcn, const int *lis
 #undef RP_RECOMP
 }
 
+// Rows per step of the bucket sums: whole-wave groups (rows over 64 wide) take at
+// most four, since a bucket holds a handful of slots and the masked rows of a step
+// of eight reload a 1 KB row (1% on dense_large's 256-wide second layer); 16-lane
+// groups keep eight (with four, buckets of 5-8 slots cost a second round trip).
+constexpr int bucket_rows_per_step(int g, int u) { return g == kWave && u > 4 ? 4 : u; }
+
 void launch_bucket_sum(hipStream_t s, int d, int ld, const int *list, const u64 *count, const long long *boff,
                        const Buckets &bk, const float *msg, float *S, const Counters *c) {
   const int blocks = 2048;
 #define RP_BSUM(GV, NCV, UV)                                                                                     \
-  RP_LAUNCH((k_bucket_sum<GV, NCV, UV>), dim3(blocks), dim3(256), 0, s, d, ld, list, count, boff, bk, msg, S, c)
+  RP_LAUNCH((k_bucket_sum<GV, NCV, bucket_rows_per_step(GV, UV)>), dim3(blocks), dim3(256), 0, s, d, ld, list,    \
+            count, boff, bk, msg, S, c)
   RP_BY_WIDTH(RP_BSUM);
 #undef RP_BSUM
 }
