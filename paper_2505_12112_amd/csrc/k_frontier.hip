@@ -1071,7 +1071,7 @@ __global__ __launch_bounds__(kBinThreads) void k_bin_sort(long long n, const u64
   for (int i = t; i < span; i += kBinThreads) cur[i] = 0;
   __syncthreads();
   if (t == 0) b.bin_total[bin] = 0;  // every thread has read it
-  constexpr int kU = 4;  // arcs per thread in flight
+  constexpr int kU = 8;  // arcs per thread in flight
   for (int p0 = t; p0 < total; p0 += kU * kBinThreads) {
     int vv[kU];
 #pragma unroll
