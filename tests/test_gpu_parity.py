@@ -103,12 +103,17 @@ def test_adversarial_batches_of_either_netting(agg, undirected):
     """The same colliding ops in batches of at most 1024 ops (netted in one launch,
     each op compared with the later ones) and of 1025-1600 ops (hashed, then
     decided), on one context: the two nettings must agree with the oracle's
-    sequential semantics."""
+    sequential semantics. Each batch rewrites most of the 1200-edge graph, so the
+    cached aggregates take thousands of messages per batch and their fp32 rounding
+    grows by about 5e-6 (layer 2, relative) per batch; the context re-anchors every
+    4th batch (the drift budget), as a context under such churn would, so that the
+    embeddings are held to 1e-4."""
     _say("adversarial netting", agg, undirected)
     rng = np.random.default_rng(97 + 5 * undirected + len(agg))
     dims = (8, 24, 6)
     src, dst, x, w = _small(rng, 300, 1200, dims, agg, undirected)
     p = Pair(300, src, dst, x, w, undirected=undirected, edge_w=_edge_w(rng, agg, src.size))
+    p.lib.set_reanchor(4)
     try:
         for b in range(12):
             bs = int(rng.integers(1025, 1601)) if b % 2 else int(rng.integers(800, 1025))
