@@ -1211,7 +1211,14 @@ ripple_status ensure_buckets(ripple_ctx *c) {
   const int shift = rp::bin_shift(c->n);
   if (shift < 0)
     return fail(c, RIPPLE_E_INVALID, "ripple: the bucket form takes graphs of at most 2^25 vertices");
-  if (c->bkt.cnt == nullptr) {
+  if (c->bkt.cnt == nullptr || c->bkt.bin_total == nullptr || c->bkt.bin_base == nullptr ||
+      c->bkt.block_off == nullptr) {
+    // all four or none: an allocation that failed before leaves no part of them in
+    // use (the kernels take every one)
+    dfree_t(c, c->bkt.cnt);
+    dfree_t(c, c->bkt.bin_total);
+    dfree_t(c, c->bkt.bin_base);
+    dfree_t(c, c->bkt.block_off);
     const long long slots = rp::bucket_counter_slots(c->n);
     const int nbins = static_cast<int>((c->n + (1LL << shift) - 1) >> shift);
     c->bkt.shift = shift;
